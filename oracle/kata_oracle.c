@@ -1,0 +1,334 @@
+/*
+ * kata_oracle.c -- plain CPU oracle for the causal KATA-M1 attention forward
+ * (rank-one PSD feature map phi(x) = vec(x x^T)) and its recurrent decode step.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product library links, loads,
+ * imports or calls this file; only the test suite, the smoke check and the
+ * bench's CPU-baseline leg do.  It shares no code, header, table or helper
+ * with the GPU path.
+ *
+ * Everything is evaluated in IEEE double precision from the exact input values
+ * (bf16 or fp32 inputs are widened exactly by the caller).  Loops are written
+ * for a reader checking them against the paper, not for speed; the only
+ * concession is an OpenMP loop over independent (batch, head, row) triples.
+ *
+ * Layouts (all row-major, contiguous):
+ *   q, k : [B][H][T][d]      v : [B][H][T][dv]      out : [B][H][T][dv]
+ *   packed feature index of the pair (a, b), a <= b, in a d x d symmetric
+ *   matrix, upper triangle in row-major order:
+ *       f(a, b) = a*d - a*(a-1)/2 + (b - a),   n = d*(d+1)/2 features.
+ *   decode state: S : [B][H][n][dv],  z : [B][H][n]  (unscaled sums of
+ *   k_a*k_b*v and k_a*k_b).
+ *
+ * Parity status: every function here is pinned by the CPU test suite
+ * (closed forms, invariants, a hand-computed example, brute force with
+ * unpacked d*d features, chunked-versus-definition agreement, scan-versus-
+ * recurrence agreement).  None is "parity unpinned".
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define EXPORT __attribute__((visibility("default")))
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+EXPORT int kata_oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+EXPORT long kata_oracle_packed_dim(long d) { return d * (d + 1) / 2; }
+
+/* Packed index of the unordered pair (a, b) (row-major upper triangle). */
+EXPORT long kata_oracle_packed_index(long a, long b, long d) {
+  if (a > b) { long t = a; a = b; b = t; }
+  return a * d - a * (a - 1) / 2 + (b - a);
+}
+
+/*
+ * Rank-one PSD lift, packed (section "Rank-one packing into the PSD cone" and
+ * "From rank-one rays to low-rank PSD packing"): the feature of x is the
+ * symmetric matrix x x^T, kept as its n = d(d+1)/2 upper-triangle entries.
+ * weighted = 0: out[f(a,b)] = x_a x_b                (state side)
+ * weighted = 1: out[f(a,b)] = (a==b ? 1 : 2) x_a x_b  (query side)
+ * With these, sum_f phi_w(q)_f phi(k)_f equals the Frobenius inner product
+ * <q q^T, k k^T> = (q . k)^2.
+ */
+EXPORT void kata_oracle_phi(const double* x, long d, int weighted, double* out) {
+  for (long a = 0; a < d; ++a)
+    for (long b = a; b < d; ++b) {
+      double w = (weighted && a != b) ? 2.0 : 1.0;
+      out[kata_oracle_packed_index(a, b, d)] = w * x[a] * x[b];
+    }
+}
+
+/*
+ * One output row of the definition: normalised linear attention (eq. linatt)
+ * with psi = phi, where <phi(q), phi(k)> = (q . k)^2:
+ *     w_i = (q_t . k_i)^2 for i <= t,
+ *     o_t = sum_i w_i v_i / sum_i w_i,   o_t = 0 when the sum is 0.
+ * Rows are 0-indexed; the sum includes i = t (the current token, which is the
+ * c_t term of the output-gate proposition).
+ */
+static void definition_row(const double* q, const double* k, const double* v,
+                           long t, long d, long dv, double* o) {
+  double D = 0.0;
+  for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  const double* qt = q + t * d;
+  for (long i = 0; i <= t; ++i) {
+    const double* ki = k + i * d;
+    double s = 0.0;
+    for (long a = 0; a < d; ++a) s += qt[a] * ki[a];
+    double w = s * s;
+    D += w;
+    const double* vi = v + i * dv;
+    for (long j = 0; j < dv; ++j) o[j] += w * vi[j];
+  }
+  if (D > 0.0) {
+    for (long j = 0; j < dv; ++j) o[j] /= D;
+  } else {
+    for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  }
+}
+
+/* Full causal forward by the definition, O(T^2) per head. */
+EXPORT void kata_oracle_fwd(const double* q, const double* k, const double* v,
+                            double* out, long B, long H, long T, long d, long dv) {
+  long BH = B * H;
+#pragma omp parallel for collapse(2) schedule(dynamic, 16)
+  for (long bh = 0; bh < BH; ++bh)
+    for (long t = 0; t < T; ++t)
+      definition_row(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t, d, dv,
+                     out + (bh * T + t) * dv);
+}
+
+/*
+ * The definition evaluated only at listed rows: entry r is head bh_idx[r]
+ * (flattened b*H + h) and token t_idx[r]; out is [nrows][dv].
+ */
+EXPORT void kata_oracle_fwd_rows(const double* q, const double* k, const double* v,
+                                 long B, long H, long T, long d, long dv,
+                                 const long* bh_idx, const long* t_idx, long nrows,
+                                 double* out) {
+  (void)B; (void)H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long r = 0; r < nrows; ++r) {
+    long bh = bh_idx[r];
+    definition_row(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t_idx[r], d, dv,
+                   out + r * dv);
+  }
+}
+
+/*
+ * Exclusive prefix sum along the leading axis of x : [N][E], in place:
+ * x[c] <- sum_{c' < c} x[c'], x[0] <- 0 (section "Tree-scan inter-chunk
+ * reduction": the inter-chunk prefix is exclusive, the first one is zero).
+ * mode 0: the sequential recurrence.  mode 1: the work-efficient tree scan
+ * (up-sweep building partial sums over power-of-two blocks, then down-sweep
+ * distributing them), over N rounded up to a power of two with zero padding;
+ * ceil(log2 N) rounds in each sweep.
+ */
+EXPORT void kata_oracle_scan_exclusive(double* x, long N, long E, int mode) {
+  if (N <= 0) return;
+  if (mode == 0) {
+    double* run = (double*)calloc((size_t)E, sizeof(double));
+    for (long c = 0; c < N; ++c)
+      for (long e = 0; e < E; ++e) {
+        double cur = x[c * E + e];
+        x[c * E + e] = run[e];
+        run[e] += cur;
+      }
+    free(run);
+    return;
+  }
+  long P = 1;
+  while (P < N) P <<= 1;
+  double* a = (double*)calloc((size_t)(P * E), sizeof(double));
+  memcpy(a, x, (size_t)(N * E) * sizeof(double));
+  /* up-sweep: after round r, a[i] for i = m*2^(r+1) - 1 holds the sum of its block */
+  for (long step = 1; step < P; step <<= 1)
+    for (long i = 2 * step - 1; i < P; i += 2 * step)
+      for (long e = 0; e < E; ++e) a[i * E + e] += a[(i - step) * E + e];
+  /* clear the root, then down-sweep: each node passes its prefix to the left
+     child and prefix + left-sum to the right child */
+  for (long e = 0; e < E; ++e) a[(P - 1) * E + e] = 0.0;
+  for (long step = P >> 1; step >= 1; step >>= 1)
+    for (long i = 2 * step - 1; i < P; i += 2 * step)
+      for (long e = 0; e < E; ++e) {
+        double left = a[(i - step) * E + e];
+        a[(i - step) * E + e] = a[i * E + e];
+        a[i * E + e] += left;
+      }
+  memcpy(x, a, (size_t)(N * E) * sizeof(double));
+  free(a);
+}
+
+/*
+ * Chunkwise forward (eq. chunk-SZ and eq. chunk-out; the chunkwise algorithm
+ * of the appendix), for every head, in packed features:
+ *   N_C = ceil(T / C); the last chunk is padded with zero rows; the output is
+ *   truncated to T rows.
+ *   Local chunk state   S_loc[c] = Psi(K_c)^T V_c,  Z_loc[c] = Psi(K_c)^T 1.
+ *   Prefix              S_[c] = sum_{c' < c} S_loc[c'] (exclusive; S_[0] = 0)
+ *                       via the sequential recurrence (scan_mode 0) or the
+ *                       tree scan (scan_mode 1).
+ *   Chunk output        P = (Psi_w(Q_c) Psi(K_c)^T) .* M, M lower-triangular
+ *                       including the diagonal,
+ *                       N = Psi_w(Q_c) S_[c] + P V_c,  D = Psi_w(Q_c) Z_[c] + P 1,
+ *                       O = diag(D)^-1 N  (rows with D = 0 give 0).
+ * Psi_w is the query-side weighted packed feature, so that
+ * Psi_w(q) . Psi(k) = (q . k)^2.
+ */
+EXPORT void kata_oracle_fwd_chunked(const double* q, const double* k, const double* v,
+                                    double* out, long B, long H, long T, long d,
+                                    long dv, long C, int scan_mode) {
+  long n = d * (d + 1) / 2;
+  long NC = (T + C - 1) / C;
+  long BH = B * H;
+  long SE = n * dv + n; /* one state record: S (n x dv) then Z (n) */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    const double* Q = q + bh * T * d;
+    const double* K = k + bh * T * d;
+    const double* V = v + bh * T * dv;
+    double* O = out + bh * T * dv;
+    /* padded chunk inputs */
+    double* Qc = (double*)calloc((size_t)(C * d), sizeof(double));
+    double* Kc = (double*)calloc((size_t)(C * d), sizeof(double));
+    double* Vc = (double*)calloc((size_t)(C * dv), sizeof(double));
+    double* PhiQ = (double*)malloc((size_t)(C * n) * sizeof(double));
+    double* PhiK = (double*)malloc((size_t)(C * n) * sizeof(double));
+    double* P = (double*)malloc((size_t)(C * C) * sizeof(double));
+    double* Nrow = (double*)malloc((size_t)dv * sizeof(double));
+    double* states = (double*)calloc((size_t)(NC * SE), sizeof(double));
+
+    for (long pass = 0; pass < 2; ++pass) {
+      /* pass 0: local chunk states; then the prefix; pass 1: chunk outputs */
+      for (long c = 0; c < NC; ++c) {
+        long t0 = c * C;
+        memset(Qc, 0, (size_t)(C * d) * sizeof(double));
+        memset(Kc, 0, (size_t)(C * d) * sizeof(double));
+        memset(Vc, 0, (size_t)(C * dv) * sizeof(double));
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          memcpy(Qc + r * d, Q + (t0 + r) * d, (size_t)d * sizeof(double));
+          memcpy(Kc + r * d, K + (t0 + r) * d, (size_t)d * sizeof(double));
+          memcpy(Vc + r * dv, V + (t0 + r) * dv, (size_t)dv * sizeof(double));
+        }
+        for (long r = 0; r < C; ++r) {
+          kata_oracle_phi(Kc + r * d, d, 0, PhiK + r * n);
+          kata_oracle_phi(Qc + r * d, d, 1, PhiQ + r * n);
+        }
+        double* St = states + c * SE; /* S then Z of this chunk */
+        if (pass == 0) {
+          /* S_loc = Psi(K_c)^T V_c ; Z_loc = Psi(K_c)^T 1 */
+          for (long f = 0; f < n; ++f) {
+            for (long j = 0; j < dv; ++j) {
+              double s = 0.0;
+              for (long r = 0; r < C; ++r) s += PhiK[r * n + f] * Vc[r * dv + j];
+              St[f * dv + j] = s;
+            }
+            double zs = 0.0;
+            for (long r = 0; r < C; ++r) zs += PhiK[r * n + f];
+            St[n * dv + f] = zs;
+          }
+          continue;
+        }
+        /* pass 1: St now holds the exclusive prefix (S_[c], Z_[c]) */
+        for (long r = 0; r < C; ++r)
+          for (long s = 0; s < C; ++s) {
+            double a = 0.0;
+            for (long f = 0; f < n; ++f) a += PhiQ[r * n + f] * PhiK[s * n + f];
+            P[r * C + s] = (s <= r) ? a : 0.0;
+          }
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          double D = 0.0;
+          for (long f = 0; f < n; ++f) D += PhiQ[r * n + f] * St[n * dv + f];
+          for (long s = 0; s < C; ++s) D += P[r * C + s];
+          for (long j = 0; j < dv; ++j) {
+            double acc = 0.0;
+            for (long f = 0; f < n; ++f) acc += PhiQ[r * n + f] * St[f * dv + j];
+            for (long s = 0; s < C; ++s) acc += P[r * C + s] * Vc[s * dv + j];
+            Nrow[j] = acc;
+          }
+          for (long j = 0; j < dv; ++j) O[(t0 + r) * dv + j] = (D > 0.0) ? Nrow[j] / D : 0.0;
+        }
+      }
+      if (pass == 0) kata_oracle_scan_exclusive(states, NC, SE, scan_mode);
+    }
+    free(Qc); free(Kc); free(Vc); free(PhiQ); free(PhiK); free(P); free(Nrow);
+    free(states);
+  }
+}
+
+/*
+ * State after T tokens by the additive recurrence of eq. linatt:
+ *   S_t = S_{t-1} + phi(k_t) v_t^T,  Z_t = Z_{t-1} + phi(k_t),  S_0 = 0, Z_0 = 0.
+ * Overwrites S : [B][H][n][dv] and z : [B][H][n].
+ */
+EXPORT void kata_oracle_state(const double* k, const double* v, double* S, double* z,
+                              long B, long H, long T, long d, long dv) {
+  long n = d * (d + 1) / 2;
+  long BH = B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    double* Sh = S + bh * n * dv;
+    double* zh = z + bh * n;
+    double* phi = (double*)malloc((size_t)n * sizeof(double));
+    memset(Sh, 0, (size_t)(n * dv) * sizeof(double));
+    memset(zh, 0, (size_t)n * sizeof(double));
+    for (long t = 0; t < T; ++t) {
+      kata_oracle_phi(k + (bh * T + t) * d, d, 0, phi);
+      const double* vt = v + (bh * T + t) * dv;
+      for (long f = 0; f < n; ++f) {
+        for (long j = 0; j < dv; ++j) Sh[f * dv + j] += phi[f] * vt[j];
+        zh[f] += phi[f];
+      }
+    }
+    free(phi);
+  }
+}
+
+/*
+ * One recurrent decode step for every head (eq. linatt's recurrence, then its
+ * normalised readout with the updated state, so the current token is included
+ * as in the forward):
+ *   S <- S + phi(k) v^T,  z <- z + phi(k),
+ *   o = phi_w(q)^T S / phi_w(q)^T z   (o = 0 when the denominator is 0).
+ * q, k : [B][H][d]; v, out : [B][H][dv]; S, z updated in place.
+ */
+EXPORT void kata_oracle_decode_step(double* S, double* z, const double* q,
+                                    const double* k, const double* v, double* out,
+                                    long B, long H, long d, long dv) {
+  long n = d * (d + 1) / 2;
+  long BH = B * H;
+#pragma omp parallel for schedule(static)
+  for (long bh = 0; bh < BH; ++bh) {
+    double* Sh = S + bh * n * dv;
+    double* zh = z + bh * n;
+    double* pk = (double*)malloc((size_t)n * sizeof(double));
+    double* pq = (double*)malloc((size_t)n * sizeof(double));
+    kata_oracle_phi(k + bh * d, d, 0, pk);
+    kata_oracle_phi(q + bh * d, d, 1, pq);
+    const double* vt = v + bh * dv;
+    for (long f = 0; f < n; ++f) {
+      for (long j = 0; j < dv; ++j) Sh[f * dv + j] += pk[f] * vt[j];
+      zh[f] += pk[f];
+    }
+    double D = 0.0;
+    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];
+    for (long j = 0; j < dv; ++j) {
+      double acc = 0.0;
+      for (long f = 0; f < n; ++f) acc += pq[f] * Sh[f * dv + j];
+      out[bh * dv + j] = (D > 0.0) ? acc / D : 0.0;
+    }
+    free(pk);
+    free(pq);
+  }
+}

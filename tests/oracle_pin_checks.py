@@ -1,0 +1,342 @@
+"""Checks that pin the CPU oracle to facts the paper and the mathematics fix.
+
+Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError
+when the oracle disagrees with the fact it checks.  None of them re-types the
+oracle's formula: they compare against closed forms, invariants, a
+hand-computed example, brute force in a different feature space (unpacked
+d*d features) or library routines.  The same functions run against planted
+mutants of the oracle in test_oracle_mutants.py, to show that a plausible
+mistake anywhere in the oracle fails at least one of them.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _rng(seed=1234):
+    return np.random.default_rng(seed)
+
+
+def _rand_qkv(rng, B, H, T, d, dv, unit=True):
+    q = rng.standard_normal((B, H, T, d))
+    k = rng.standard_normal((B, H, T, d))
+    if unit:
+        q /= np.linalg.norm(q, axis=-1, keepdims=True)
+        k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((B, H, T, dv))
+    return q, k, v
+
+
+def _brute_unpacked(q, k, v):
+    """Forward in the unpacked feature space: phi(x) = vec(x x^T) in R^{d^2},
+    scores = Phi(Q) Phi(K)^T with a lower-triangular mask (diagonal kept),
+    O = (P V) / (P 1).  numpy only; a different route from the oracle's
+    (q.k)^2 loop."""
+    B, H, T, d = q.shape
+    out = np.zeros(v.shape)
+    mask = np.tril(np.ones((T, T)))
+    for b in range(B):
+        for h in range(H):
+            PQ = np.einsum("ta,tb->tab", q[b, h], q[b, h]).reshape(T, d * d)
+            PK = np.einsum("ta,tb->tab", k[b, h], k[b, h]).reshape(T, d * d)
+            P = (PQ @ PK.T) * mask
+            D = P.sum(axis=1, keepdims=True)
+            N = P @ v[b, h]
+            out[b, h] = np.where(D > 0, N / np.where(D > 0, D, 1.0), 0.0)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# PIN: packed feature map, sizes
+# ---------------------------------------------------------------------------
+
+def pin_packed_sizes(orc):
+    # Widths printed in the paper: d=64 gives d^2 = 4096 direct and 2080 packed.
+    assert orc.packed_dim(64) == 2080 and 64 * 64 == 4096
+    # KATA-M1 state of the MQAR table: 2 layers x n x dv = 266,240 at d = dv = 64.
+    assert 2 * orc.packed_dim(64) * 64 == 266240
+    # KATA-M2 (two 32-dim blocks): 2 layers x 2 blocks x 528 x 64 = 135,168.
+    assert 2 * 2 * orc.packed_dim(32) * 64 == 135168
+    for d in (1, 2, 3, 16, 32):
+        assert orc.packed_dim(d) == d * (d + 1) // 2
+
+
+def pin_packed_order(orc):
+    # Row-major upper triangle: numpy's triu_indices enumerates exactly that order.
+    for d in (1, 2, 5, 16):
+        ia, ib = np.triu_indices(d)
+        got = [orc.packed_index(int(a), int(b), d) for a, b in zip(ia, ib)]
+        assert got == list(range(len(ia)))
+        # unordered pair
+        assert all(orc.packed_index(int(b), int(a), d) == orc.packed_index(int(a), int(b), d)
+                   for a, b in zip(ia, ib))
+        # phi lays out x_a x_b in that order
+        x = _rng(d).standard_normal(d)
+        assert np.array_equal(orc.phi(x), np.outer(x, x)[ia, ib])
+
+
+def pin_phi_identity(orc):
+    # <phi_w(q), phi(k)> = <q q^T, k k^T>_F = (q . k)^2
+    rng = _rng(7)
+    for d in (1, 2, 3, 8, 16, 64):
+        for _ in range(5):
+            q = rng.standard_normal(d)
+            k = rng.standard_normal(d)
+            packed = float(orc.phi(q, weighted=True) @ orc.phi(k))
+            unpacked = float(np.outer(q, q).ravel() @ np.outer(k, k).ravel())
+            gram = float(q @ np.outer(k, k) @ q)
+            ref = float(np.dot(q, k)) ** 2
+            scale = max(1.0, abs(ref))
+            assert abs(packed - ref) <= 1e-13 * scale
+            assert abs(unpacked - ref) <= 1e-13 * scale
+            assert abs(gram - ref) <= 1e-13 * scale
+
+
+# ---------------------------------------------------------------------------
+# PIN: hand-computed worked example
+# ---------------------------------------------------------------------------
+
+def pin_worked_example(orc):
+    with open(os.path.join(GOLDEN, "worked_example_d2.json")) as f:
+        g = json.load(f)
+    K = np.array(g["keys"])[None, None]
+    V = np.array(g["values"])[None, None]
+    Q = np.array(g["queries"])[None, None]
+    out = orc.fwd(Q, K, V)[0, 0]
+    assert np.allclose(out, np.array(g["outputs"]), rtol=0, atol=1e-15)
+    S, z = orc.state(K[:, :, :2], V[:, :, :2])
+    assert np.allclose(S[0, 0], np.array(g["state_after_2"]["S"]), atol=1e-15)
+    assert np.allclose(z[0, 0], np.array(g["state_after_2"]["z"]), atol=1e-15)
+    q11 = np.array(g["query_11_at_3"]["q"])
+    Q2 = Q.copy()
+    Q2[0, 0, 2] = q11
+    o = orc.fwd(Q2, K, V)[0, 0, 2, 0]
+    assert abs(o - g["query_11_at_3"]["output"]) <= 1e-15
+    # the same through the decode recurrence: state after 2 tokens, then step 3
+    out3, S3, z3 = orc.decode_step(S, z, q11[None, None], K[:, :, 2], V[:, :, 2])
+    assert abs(out3[0, 0, 0] - g["query_11_at_3"]["output"]) <= 1e-15
+    assert abs(float(orc.phi(q11, weighted=True) @ S3[0, 0][:, 0]) - g["query_11_at_3"]["N"]) <= 1e-14
+    assert abs(float(orc.phi(q11, weighted=True) @ z3[0, 0]) - g["query_11_at_3"]["D"]) <= 1e-14
+
+
+# ---------------------------------------------------------------------------
+# PIN: brute force in unpacked feature space
+# ---------------------------------------------------------------------------
+
+def pin_brute_force_unpacked(orc):
+    rng = _rng(11)
+    for (B, H, T, d, dv, unit) in [(1, 2, 13, 3, 2, True), (2, 1, 9, 8, 5, False),
+                                   (1, 1, 1, 4, 3, True), (1, 1, 24, 2, 1, False)]:
+        q, k, v = _rand_qkv(rng, B, H, T, d, dv, unit)
+        ref = _brute_unpacked(q, k, v)
+        got = orc.fwd(q, k, v)
+        assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# PIN: output-gate proposition (convex weights, t = 1, gate recursion)
+# ---------------------------------------------------------------------------
+
+def pin_convex_hull(orc):
+    rng = _rng(3)
+    q, k, v = _rand_qkv(rng, 1, 3, 40, 6, 4, unit=False)
+    o = orc.fwd(q, k, v)
+    lo = np.minimum.accumulate(v, axis=2)
+    hi = np.maximum.accumulate(v, axis=2)
+    assert (o >= lo - 1e-12).all() and (o <= hi + 1e-12).all()
+    # Weights are nonnegative, causal and sum to one: with one-hot values
+    # (dv = T, v_i = e_i) each output row is the weight vector itself.
+    T = 17
+    q, k, _ = _rand_qkv(rng, 1, 1, T, 5, 1)
+    w = orc.fwd(q, k, np.eye(T)[None, None])[0, 0]
+    assert (w >= 0).all()
+    assert np.allclose(w.sum(axis=1), 1.0, atol=1e-14)
+    assert np.all(np.triu(w, 1) == 0.0)
+    # constant values are reproduced exactly (up to rounding)
+    o1 = orc.fwd(q, k, np.full((1, 1, T, 2), 3.25))
+    assert np.allclose(o1, 3.25, atol=1e-14)
+
+
+def pin_first_token(orc):
+    # D_0 = 0, so the first output is the first value (alpha, beta) = (0, 1).
+    rng = _rng(5)
+    q, k, v = _rand_qkv(rng, 2, 2, 6, 4, 3)
+    o = orc.fwd(q, k, v)
+    assert np.allclose(o[:, :, 0], v[:, :, 0], rtol=0, atol=1e-15)
+
+
+def pin_gate_recursion(orc):
+    # o_t = alpha_t zbar_{t|t-1} + beta_t v_t,  alpha = D_{t-1}/D_t, beta = c_t/D_t,
+    # with zbar = phi(q_t)^T S_{t-1} / D_{t-1} read from the state of tokens < t.
+    rng = _rng(9)
+    q, k, v = _rand_qkv(rng, 1, 1, 12, 5, 3)
+    o = orc.fwd(q, k, v)[0, 0]
+    for t in range(1, 12):
+        S, z = orc.state(k[:, :, :t], v[:, :, :t])
+        pq = orc.phi(q[0, 0, t], weighted=True)
+        Dprev = float(pq @ z[0, 0])
+        c = float(np.dot(q[0, 0, t], k[0, 0, t])) ** 2
+        D = Dprev + c
+        zbar = (pq @ S[0, 0]) / Dprev
+        alpha, beta = Dprev / D, c / D
+        assert alpha >= 0 and beta >= 0 and abs(alpha + beta - 1) < 1e-15
+        assert np.allclose(o[t], alpha * zbar + beta * v[0, 0, t], rtol=1e-12, atol=1e-13)
+
+
+def pin_zero_denominator(orc):
+    # A zero query makes D_t = 0; the output row is defined as 0.
+    rng = _rng(13)
+    q, k, v = _rand_qkv(rng, 1, 1, 8, 4, 3)
+    q[0, 0, 5] = 0.0
+    o = orc.fwd(q, k, v)
+    assert np.all(o[0, 0, 5] == 0.0)
+    assert np.all(np.isfinite(o))
+    oc = orc.fwd_chunked(q, k, v, 3, 1)
+    assert np.all(oc[0, 0, 5] == 0.0)
+    # the decode readout follows the same convention
+    S, z = orc.state(k[:, :, :5], v[:, :, :5])
+    out, _, _ = orc.decode_step(S, z, q[:, :, 5], k[:, :, 5], v[:, :, 5])
+    assert np.all(out == 0.0)
+
+
+# ---------------------------------------------------------------------------
+# PIN: closed forms
+# ---------------------------------------------------------------------------
+
+def pin_identical_keys_running_mean(orc):
+    rng = _rng(17)
+    T, d, dv = 20, 6, 3
+    kk = rng.standard_normal(d)
+    k = np.tile(kk, (1, 1, T, 1))
+    q = rng.standard_normal((1, 1, T, d))
+    v = rng.standard_normal((1, 1, T, dv))
+    o = orc.fwd(q, k, v)[0, 0]
+    mean = np.cumsum(v[0, 0], axis=0) / np.arange(1, T + 1)[:, None]
+    assert np.allclose(o, mean, rtol=1e-13, atol=1e-13)
+
+
+def pin_orthonormal_keys_exact_recall(orc):
+    # k_i = e_i (T <= d) and q_t = e_j with j <= t: only token j has nonzero
+    # weight, so o_t = v_j exactly (orthogonal-value identity).
+    d = 8
+    T = 8
+    k = np.eye(d)[None, None, :T]
+    rng = _rng(19)
+    v = rng.standard_normal((1, 1, T, 4))
+    js = [0, 0, 1, 3, 2, 5, 6, 4]
+    q = np.stack([np.eye(d)[j] for j in js])[None, None]
+    o = orc.fwd(q, k, v)[0, 0]
+    for t, j in enumerate(js):
+        assert np.array_equal(o[t], v[0, 0, j])
+
+
+def pin_weight_sample(orc):
+    # Unit q and k at an angle of 0.1024 rad: the KATA weight is cos^2 = 0.9896
+    # (four places, as printed).  Read back through two tokens: k_0 = q (weight 1),
+    # k_1 at the angle, v_0 = 0, v_1 = 1, so o_1 = w / (1 + w).
+    th = 0.1024
+    q = np.array([1.0, 0.0])
+    k0 = q.copy()
+    k1 = np.array([math.cos(th), math.sin(th)])
+    Q = np.stack([q, q])[None, None]
+    K = np.stack([k0, k1])[None, None]
+    V = np.array([[0.0], [1.0]])[None, None]
+    o = orc.fwd(Q, K, V)[0, 0, 1, 0]
+    w = o / (1.0 - o)
+    assert round(w, 4) == 0.9896
+
+
+# ---------------------------------------------------------------------------
+# PIN: invariances (isometric invariance, phi(-x) = phi(x), value affinity)
+# ---------------------------------------------------------------------------
+
+def pin_invariances(orc):
+    rng = _rng(23)
+    q, k, v = _rand_qkv(rng, 1, 2, 15, 5, 3, unit=False)
+    o = orc.fwd(q, k, v)
+    sign = rng.choice([-1.0, 1.0], size=(1, 2, 15, 1))
+    assert np.allclose(orc.fwd(q, k * sign, v), o, rtol=1e-12, atol=1e-12)
+    alpha = rng.uniform(0.3, 3.0, size=(1, 2, 15, 1)) * sign
+    assert np.allclose(orc.fwd(q * alpha, k, v), o, rtol=1e-12, atol=1e-12)
+    U, _ = np.linalg.qr(rng.standard_normal((5, 5)))
+    assert np.allclose(orc.fwd(q @ U.T, k @ U.T, v), o, rtol=1e-12, atol=1e-12)
+    c = rng.standard_normal(3)
+    assert np.allclose(orc.fwd(q, k, v + c), o + c, rtol=1e-12, atol=1e-12)
+    A = rng.standard_normal((3, 4))
+    assert np.allclose(orc.fwd(q, k, v @ A), o @ A, rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# PIN: chunked form = definition, tree scan = recurrence
+# ---------------------------------------------------------------------------
+
+def pin_chunked_equals_definition(orc):
+    rng = _rng(29)
+    B, H, T, d, dv = 1, 2, 37, 4, 3
+    q, k, v = _rand_qkv(rng, B, H, T, d, dv, unit=False)
+    ref = orc.fwd(q, k, v)
+    for C in (1, 2, 3, 5, 7, 16, 32, T, T + 3):
+        for mode in (0, 1):
+            got = orc.fwd_chunked(q, k, v, C, mode)
+            assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), (C, mode)
+
+
+def pin_scan_equals_recurrence(orc):
+    rng = _rng(31)
+    for N in (1, 2, 3, 5, 8, 13, 64, 2048):
+        xi = rng.integers(-50, 50, size=(N, 7)).astype(np.float64)
+        seq = orc.scan_exclusive(xi, 0)
+        tree = orc.scan_exclusive(xi, 1)
+        lib = np.cumsum(xi, axis=0) - xi        # exclusive prefix via numpy
+        assert np.array_equal(seq, lib) and np.array_equal(tree, lib)
+        assert np.all(seq[0] == 0) and np.all(tree[0] == 0)
+        xr = rng.standard_normal((N, 5))
+        ref = np.cumsum(xr, axis=0) - xr
+        scale = np.maximum(1.0, np.abs(np.cumsum(np.abs(xr), axis=0)))
+        assert np.all(np.abs(orc.scan_exclusive(xr, 1) - ref) <= 1e-13 * scale)
+        assert np.all(np.abs(orc.scan_exclusive(xr, 0) - ref) <= 1e-13 * scale)
+
+
+# ---------------------------------------------------------------------------
+# PIN: decode recurrence = forward on the concatenated sequence
+# ---------------------------------------------------------------------------
+
+def pin_decode_equals_forward(orc):
+    rng = _rng(37)
+    B, H, P, steps, d, dv = 2, 2, 10, 6, 4, 3
+    q, k, v = _rand_qkv(rng, B, H, P + steps, d, dv)
+    ref = orc.fwd(q, k, v)
+    S, z = orc.state(k[:, :, :P], v[:, :, :P])
+    for s in range(steps):
+        t = P + s
+        out, S, z = orc.decode_step(S, z, q[:, :, t], k[:, :, t], v[:, :, t])
+        assert np.allclose(out, ref[:, :, t], rtol=1e-12, atol=1e-13)
+    S_all, z_all = orc.state(k, v)
+    assert np.allclose(S, S_all, rtol=1e-12, atol=1e-12)
+    assert np.allclose(z, z_all, rtol=1e-12, atol=1e-12)
+
+
+def pin_rows_match_full(orc):
+    rng = _rng(41)
+    q, k, v = _rand_qkv(rng, 2, 3, 21, 4, 5)
+    full = orc.fwd(q, k, v).reshape(6, 21, 5)
+    bh = rng.integers(0, 6, size=30)
+    tt = rng.integers(0, 21, size=30)
+    rows = orc.fwd_rows(q, k, v, bh, tt)
+    assert np.array_equal(rows, full[bh, tt])
+
+
+ALL_PINS = [
+    pin_packed_sizes, pin_packed_order, pin_phi_identity, pin_worked_example,
+    pin_brute_force_unpacked, pin_convex_hull, pin_first_token, pin_gate_recursion,
+    pin_zero_denominator, pin_identical_keys_running_mean,
+    pin_orthonormal_keys_exact_recall, pin_weight_sample, pin_invariances,
+    pin_chunked_equals_definition, pin_scan_equals_recurrence,
+    pin_decode_equals_forward, pin_rows_match_full,
+]

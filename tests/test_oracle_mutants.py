@@ -1,0 +1,62 @@
+"""Plant plausible mistakes in a copy of the oracle and check the pins catch each.
+
+The mutants are built on the CPU from a temporary, textually edited copy of
+oracle/kata_oracle.c; the committed oracle is never changed.
+"""
+import os
+import tempfile
+
+import pytest
+
+import oracle
+from oracle_pin_checks import ALL_PINS
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "kata_oracle.c")
+
+# (name, exact text in the oracle, replacement)
+MUTANTS = [
+    ("drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {"),
+    ("abs_not_square", "double w = s * s;", "double w = fabs(s);"),
+    ("weight_on_diagonal", "double w = (weighted && a != b) ? 2.0 : 1.0;",
+     "double w = (weighted && a == b) ? 2.0 : 1.0;"),
+    ("packed_index_off_by_one", "return a * d - a * (a - 1) / 2 + (b - a);",
+     "return a * d - a * (a + 1) / 2 + (b - a);"),
+    ("no_zero_guard", "if (D > 0.0) {", "if (1) {"),
+    ("decode_no_zero_guard", "out[bh * dv + j] = (D > 0.0) ? acc / D : 0.0;",
+     "out[bh * dv + j] = acc / D;"),
+    ("inclusive_scan", "x[c * E + e] = run[e];\n        run[e] += cur;",
+     "run[e] += cur;\n        x[c * E + e] = run[e];"),
+    ("tree_no_root_clear", "for (long e = 0; e < E; ++e) a[(P - 1) * E + e] = 0.0;", ""),
+    ("transposed_mask", "P[r * C + s] = (s <= r) ? a : 0.0;", "P[r * C + s] = (s >= r) ? a : 0.0;"),
+    ("chunk_drops_intra_denominator", "for (long s = 0; s < C; ++s) D += P[r * C + s];", ""),
+    ("state_value_index", "Sh[f * dv + j] += phi[f] * vt[j];", "Sh[f * dv + j] += phi[f] * vt[0];"),
+    ("decode_readout_before_update",
+     "    double D = 0.0;\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];",
+     "    double D = -pq[0] * pk[0];\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];"),
+    ("chunk_key_feature_weighted", "kata_oracle_phi(Kc + r * d, d, 0, PhiK + r * n);",
+     "kata_oracle_phi(Kc + r * d, d, 1, PhiK + r * n);"),
+]
+
+
+def _pins_that_fail(orc):
+    failed = []
+    for pin in ALL_PINS:
+        try:
+            pin(orc)
+        except Exception:
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, old, new, tmp_path):
+    with open(SRC) as f:
+        text = f.read()
+    assert text.count(old) == 1, f"mutation site for {name} not found exactly once"
+    src = tmp_path / "mutant.c"
+    src.write_text(text.replace(old, new))
+    lib_path = str(tmp_path / "libmutant.so")
+    oracle.build(str(src), lib_path)
+    mut = oracle.Oracle(oracle.load(lib_path))
+    failed = _pins_that_fail(mut)
+    assert failed, f"mutant {name} passed every pin"
