@@ -1,0 +1,295 @@
+#!/usr/bin/env python3
+"""Benchmark of libkata's causal KATA-M1 forward on one MI355X.
+
+A step is one pass of the chunked-state forward (span state -> associative scan
+-> fused intra-span attention + prefix readout + normalisation) over one batch
+of the long-context workload: B=1, H=16, T=131072, d=dv=64, chunk C=64, bf16
+q/k/v with fp32 accumulation, inputs resident in HBM.  Prints ONE JSON line.
+
+Per-kernel durations are taken live with HIP events recorded on the launch
+stream between the three kernels (kata_fwd_chunked_timed).  The decode
+workload (B=256, H=16, 1024-token prefix, 128 steps) is measured in the same
+run and reported under "decode".  The CPU oracle is timed on a bounded sample
+of rows of the same workload and reported under "cpu_baseline".
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "KATA causal fwd tokens/s at T=131k,d=64 (1 GPU); % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+
+
+def _hip():
+    L = ctypes.CDLL("libamdhip64.so")
+    vp = ctypes.c_void_p
+    L.hipEventCreate.argtypes = [ctypes.POINTER(vp)]
+    L.hipEventRecord.argtypes = [vp, vp]
+    L.hipEventSynchronize.argtypes = [vp]
+    L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+    L.hipEventDestroy.argtypes = [vp]
+    return L
+
+
+class Events:
+    def __init__(self, hip, n):
+        self.hip = hip
+        self.ev = (ctypes.c_void_p * n)()
+        for i in range(n):
+            h = ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(h)) == 0
+            self.ev[i] = h
+
+    def elapsed(self, i, j):
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), self.ev[i], self.ev[j]) == 0
+        return ms.value
+
+    def block(self, i):
+        """Pointer to 4 consecutive events starting at index i."""
+        return ctypes.c_void_p(ctypes.addressof(self.ev) + i * ctypes.sizeof(ctypes.c_void_p))
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(e)
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for f in ("kata_mfma.hip", "kata_scan.hpp", "kata_common.hpp"):
+        with open(os.path.join(ROOT, "paper_2607_17419_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def upload(payload, dtype, dev):
+    import numpy as np
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(payload).view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(payload)).to(dev)
+
+
+def algorithmic(w, L):
+    """Algorithmic work per kernel (packed n = d(d+1)/2 features).
+
+    per head-token:  state   2*n*dv + n          (S += phi(k) v^T, z += phi(k))
+                     output  2*n*dv + 2*n + (C+1)*(d+dv)
+                             (phi(q)^T S and phi(q)^T z readouts, causal
+                              intra-chunk QK^T and PV at chunk size C)
+    scan: one read of every fp32 span state (n*(dv+1) values) and one bf16
+          write of its prefix, per span and head.
+    """
+    n = w.d * (w.d + 1) // 2
+    ht = w.B * w.H * w.T
+    NS = (w.T + L - 1) // L
+    state = (2 * n * w.dv + n) * ht
+    output = (2 * n * w.dv + 2 * n + (w.C + 1) * (w.d + w.dv)) * ht
+    scan_bytes = NS * w.B * w.H * n * (w.dv + 1) * (4 + 2)
+    return dict(n=n, state_flop=state, output_flop=output, scan_bytes=scan_bytes,
+                total_flop=state + output)
+
+
+def cpu_baseline(w, inp, seconds):
+    import numpy as np
+    import oracle
+    orc = oracle.Oracle()
+    q = np.ascontiguousarray(inp["q"], dtype=np.float64)
+    k = np.ascontiguousarray(inp["k"], dtype=np.float64)
+    v = np.ascontiguousarray(inp["v"], dtype=np.float64)
+    BH = w.B * w.H
+    # calibration: one late row per head
+    bh = np.arange(BH)
+    tt = np.full(BH, w.T - 1)
+    t0 = time.perf_counter()
+    orc.fwd_rows(q, k, v, bh, tt)
+    cal = time.perf_counter() - t0
+    per_unit = cal / float(np.sum(tt + 1))
+    # evenly spaced rows per head, sized to about `seconds` of work
+    R = int(seconds / max(per_unit * BH * (w.T / 2.0), 1e-12))
+    R = max(1, min(R, w.T))
+    rows = ((np.arange(R) + 0.5) * w.T / R).astype(np.int64)
+    bh = np.repeat(np.arange(BH), R)
+    tt = np.tile(rows, BH)
+    t0 = time.perf_counter()
+    orc.fwd_rows(q, k, v, bh, tt)
+    el = time.perf_counter() - t0
+    full_units = BH * w.T * (w.T + 1) / 2.0
+    sample_units = float(np.sum(tt + 1))
+    full_time = el * full_units / sample_units
+    return {
+        "value": (w.B * w.T) / full_time,
+        "unit": "tokens/s",
+        "cores": orc.num_threads(),
+        "kind": "oracle",
+        "sample": (f"{bh.size} rows ({R} evenly spaced per head x {BH} heads) of the fp64 "
+                   f"O(T^2) definition on the same inputs, {el:.1f} s; full-workload time "
+                   f"extrapolated by the summed row lengths ({full_time:.3g} s)"),
+    }
+
+
+def bench_decode(kata, dev, hip):
+    import numpy as np
+    import torch
+    import workloads
+    w = workloads.WORKLOADS["decode_bf16"]
+    inp = workloads.make_inputs(w)
+    S, z = kata.prefill_state(upload(inp["k_dev"], "bf16", dev), upload(inp["v_dev"], "bf16", dev))
+    sq = upload(inp["steps_q_dev"], "bf16", dev).permute(2, 0, 1, 3).contiguous()
+    sk = upload(inp["steps_k_dev"], "bf16", dev).permute(2, 0, 1, 3).contiguous()
+    sv = upload(inp["steps_v_dev"], "bf16", dev).permute(2, 0, 1, 3).contiguous()
+    out = torch.empty((w.B, w.H, w.dv), dtype=torch.float32, device=dev)
+    for s in range(4):  # warm-up on a copy of the state
+        kata.decode_step(S.clone(), z.clone(), sq[s], sk[s], sv[s], out=out)
+    ev = Events(hip, w.steps + 1)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hip.hipEventRecord(ev.ev[0], ctypes.c_void_p(stream))
+    for s in range(w.steps):
+        kata.decode_step(S, z, sq[s], sk[s], sv[s], out=out)
+        hip.hipEventRecord(ev.ev[s + 1], ctypes.c_void_p(stream))
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    per_step = [ev.elapsed(s, s + 1) for s in range(w.steps)]
+    ev.close()
+    n = w.d * (w.d + 1) // 2
+    bytes_step = w.B * w.H * (2 * (n * w.dv + n) * 4 + (2 * w.d + w.dv) * 2 + w.dv * 4)
+    avg = sum(per_step) / len(per_step)
+    gbs = bytes_step / (avg * 1e-3) / 1e9
+    return {
+        "workload": f"decode_bf16: {w.note}",
+        "tokens_per_s": w.B * w.steps / el,
+        "ms_per_step": 1e3 * el / w.steps,
+        "kernel_ms_per_step": avg,
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "algorithmic_bytes_per_launch": bytes_step},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long_bf16")
+    ap.add_argument("--span", type=int, default=0, help="span chunks (0 = library default)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE "
+              f"{world}); the forward has no multi-GPU path in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_17419_amd as kata
+    import workloads
+
+    dev = "cuda:0"
+    w = workloads.WORKLOADS[args.workload]
+    hip = _hip()
+    inp = workloads.make_inputs(w)
+    q = upload(inp["q_dev"], w.dtype, dev)
+    k = upload(inp["k_dev"], w.dtype, dev)
+    v = upload(inp["v_dev"], w.dtype, dev)
+    code = kata.KATA_BF16 if w.dtype == "bf16" else kata.KATA_F32
+    span = args.span or kata.default_span(w.B, w.H, w.T, w.d, w.dv, w.C, code)
+    L = min(span * w.C, -(-w.T // w.C) * w.C)
+    out = torch.empty((w.B, w.H, w.T, w.dv), dtype=torch.float32, device=dev)
+    ws = torch.empty(kata.workspace_bytes(w.B, w.H, w.T, w.d, w.dv, w.C, code, span),
+                     dtype=torch.uint8, device=dev)
+    ev = Events(hip, 4 * max(args.steps, args.warmup))
+    for i in range(args.warmup):
+        kata.fwd_chunked_timed(q, k, v, w.C, ev.block(4 * i), span_chunks=span, out=out,
+                               workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        kata.fwd_chunked_timed(q, k, v, w.C, ev.block(4 * i), span_chunks=span, out=out,
+                               workspace=ws)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stage = {"span_state": 0.0, "scan": 0.0, "span_output": 0.0}
+    for i in range(args.steps):
+        stage["span_state"] += ev.elapsed(4 * i, 4 * i + 1)
+        stage["scan"] += ev.elapsed(4 * i + 1, 4 * i + 2)
+        stage["span_output"] += ev.elapsed(4 * i + 2, 4 * i + 3)
+    ev.close()
+    stage = {kname: t / args.steps for kname, t in stage.items()}
+    ms = 1e3 * elapsed / args.steps
+    tokens = w.B * w.T
+    alg = algorithmic(w, L)
+
+    def mfma_roof(flop, t_ms):
+        tf = flop / (t_ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+
+    roofs = {
+        "span_state": mfma_roof(alg["state_flop"], stage["span_state"]),
+        "span_output": mfma_roof(alg["output_flop"], stage["span_output"]),
+    }
+    gbs = alg["scan_bytes"] / (stage["scan"] * 1e-3) / 1e9
+    roofs["scan"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    dominant = max(stage, key=stage.get)
+    roof = dict(roofs[dominant])
+    roof["kernel"] = dominant
+    roof["traffic"] = None
+    sha = source_sha()
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        ent = tr.get(dominant, {})
+        if tr.get("source_sha") == sha and tr.get("workload") == w.name and ent:
+            roof["traffic"] = ent.get("hbm_bytes_per_launch")
+
+    res = {
+        "metric": METRIC,
+        "value": tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.note}", "B": w.B, "H": w.H, "T": w.T, "d": w.d,
+                   "dv": w.dv, "C": w.C, "span_chunks": span, "span_tokens": L,
+                   "inputs": "seeded Gaussian q,k (unit rows), v ~ N(0,1), bf16 RNE"},
+        "roofline": roof,
+        "stages_ms": {kname: round(t, 4) for kname, t in stage.items()},
+        "stage_roofline": roofs,
+        "mfma_frac_end_to_end": round(alg["total_flop"] / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "algorithmic_gflop_per_step": round(alg["total_flop"] / 1e9, 2),
+        "kernel_source_sha": sha,
+    }
+    if not args.no_decode:
+        res["decode"] = bench_decode(kata, dev, hip)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+/*
+ * kata.h -- C ABI of libkata: causal KATA-M1 attention (rank-one PSD feature
+ * map) on AMD Instinct MI355X (gfx950).
+ *
+ * The operation.  For every head, with query q_t, key k_t in R^d and value v_t
+ * in R^dv, the feature map is the rank-one PSD lift phi(x) = vec(x x^T)
+ * (section "Rank-one packing into the PSD cone"), whose inner product is
+ * <phi(q), phi(k)> = (q . k)^2.  Normalised causal linear attention
+ * (eq. linatt) with this map gives
+ *
+ *     o_t = sum_{i<=t} (q_t . k_i)^2 v_i  /  sum_{i<=t} (q_t . k_i)^2 ,
+ *
+ * a convex combination of the values (output-gate proposition).  A row whose
+ * denominator is 0 (q_t orthogonal to every k_i, i <= t, e.g. q_t = 0) is
+ * defined as all zeros; the paper leaves it undefined.
+ *
+ * Conventions shared by every entry point:
+ *  - Tensors are contiguous, row-major, device-resident (HBM), 16-byte aligned:
+ *      q, k : [B][H][T][d]     v : [B][H][T][dv]     out : [B][H][T][dv] fp32.
+ *    q, k, v are fp32 or bf16 (kata_dtype_t); out, S and z are always fp32.
+ *  - The caller owns every buffer.  `out` must not alias an input.
+ *  - Every call validates its arguments on the host before touching the GPU;
+ *    on an error nothing is launched and nothing is written.
+ *  - Calls only enqueue work on `stream` and return; they never synchronise.
+ *    A device fault surfaces at the caller's next synchronisation.
+ *  - The library keeps no global mutable state; calls from several threads
+ *    are safe.  NaN and Inf in inputs propagate; inputs are not normalised.
+ *  - Packed state layout (decode and prefill): the n = d(d+1)/2 features of
+ *    the pair (a, b), a <= b, in row-major upper-triangle order,
+ *        f(a, b) = a*d - a*(a-1)/2 + (b - a),
+ *    S : [B][H][n][dv] holds sum_i k_a k_b v_i (unscaled), z : [B][H][n]
+ *    holds sum_i k_a k_b.
+ */
+#ifndef KATA_H
+#define KATA_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifndef KATA_API
+#define KATA_API __attribute__((visibility("default")))
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KATA_OK = 0,
+  KATA_ERR_INVALID_ARG = 1, /* null pointer, size < 1, or a size product overflows */
+  KATA_ERR_UNSUPPORTED = 2, /* valid arguments outside what is implemented */
+  KATA_ERR_HIP = 3          /* a HIP launch or allocation failed */
+} kata_status_t;
+
+typedef enum { KATA_F32 = 0, KATA_BF16 = 1 } kata_dtype_t;
+
+/*
+ * Causal KATA-M1 forward in the exact O(T) chunked-state form (eq. chunk-SZ,
+ * eq. chunk-out and the chunkwise algorithm of the appendix; the three-stage
+ * state / associative-scan / output pipeline of the tree-scan section).
+ * The final chunk is zero-padded on chip and the output is truncated to T rows.
+ *   q, k, v, out : see the conventions above.
+ *   B, H, T >= 1.  d in 1..64.  dv >= 1.  C >= 1 is the chunk size.
+ *   Fast path (bf16 MFMA): dtype = KATA_BF16, d in {32, 64}, dv = 64,
+ *   C a multiple of 32 up to 1024.  Every other shape with d <= 64, dv <= 256
+ *   and C <= 128 runs on the fp32 path; anything else is KATA_ERR_UNSUPPORTED.
+ *   Workspace (kata_fwd_workspace_bytes) is allocated stream-ordered with
+ *   hipMallocAsync on `stream` and released with hipFreeAsync.
+ */
+KATA_API kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, float* out,
+                               int B, int H, int T, int d, int dv, int C,
+                               kata_dtype_t dtype, hipStream_t stream);
+
+/*
+ * The same forward with caller-provided workspace and an explicit span.
+ *   span_chunks : number of chunks folded into one stored state (the state
+ *                 written to HBM covers span_chunks*C tokens; the chunks inside
+ *                 a span are combined on chip).  0 selects the default
+ *                 (kata_fwd_default_span).  1 is the per-chunk form.  Results do
+ *                 not depend on it beyond rounding.
+ *   workspace   : device buffer of at least kata_fwd_workspace_bytes(...)
+ *                 bytes, 256-byte aligned, owned by the caller, contents
+ *                 ignored on entry and undefined on exit.  Two calls in flight
+ *                 at once must not share it.
+ */
+KATA_API kata_status_t kata_fwd_chunked_ws(const void* q, const void* k, const void* v, float* out,
+                                  int B, int H, int T, int d, int dv, int C,
+                                  kata_dtype_t dtype, int span_chunks, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * kata_fwd_chunked_ws plus stage timing, for profiling: stage_events[0..3]
+ * (caller-created HIP events, all non-null) are recorded on `stream` before the
+ * state kernel and after each of the three stages (chunk or span state,
+ * associative scan, output).  Nothing synchronises; the caller reads the
+ * elapsed times with hipEventElapsedTime once the stream has reached them.
+ */
+KATA_API kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v,
+                                              float* out, int B, int H, int T, int d, int dv,
+                                              int C, kata_dtype_t dtype, int span_chunks,
+                                              void* workspace, size_t workspace_bytes,
+                                              hipEvent_t* stage_events, hipStream_t stream);
+
+/* Workspace bytes kata_fwd_chunked_ws needs for these arguments (0 when the
+ * arguments are invalid or unsupported). */
+KATA_API size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C,
+                                kata_dtype_t dtype, int span_chunks);
+
+/* The span (in chunks) that span_chunks = 0 selects for these arguments. */
+KATA_API int kata_fwd_default_span(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype);
+
+/*
+ * State after T tokens by the additive recurrence of eq. linatt:
+ *   S = sum_{t<T} phi(k_t) v_t^T,  z = sum_{t<T} phi(k_t)   (packed layout above).
+ * Overwrites S : [B][H][n][dv] and z : [B][H][n] (fp32).  Products k_a k_b and
+ * the sums are formed in fp32.  Bridges a prefill to kata_decode_step.
+ *   k, v : [B][H][T][d], [B][H][T][dv];  d in 1..64, dv in 1..256.
+ */
+KATA_API kata_status_t kata_prefill_state(const void* k, const void* v, float* S, float* z,
+                                 int B, int H, int T, int d, int dv,
+                                 kata_dtype_t dtype, hipStream_t stream);
+
+/*
+ * One recurrent decode step for all B*H heads (eq. linatt's recurrence and its
+ * normalised readout, using the updated state so the current token counts, as
+ * in the forward):
+ *   S <- S + phi(k) v^T,  z <- z + phi(k),  out = phi(q)^T S / phi(q)^T z.
+ *   S : [B][H][n][dv] fp32 and z : [B][H][n] fp32, updated in place (packed
+ *       layout above; caller-owned, so a failed step can be retried from the
+ *       caller's copy).
+ *   q, k : [B][H][d], v : [B][H][dv] in `dtype`;  out : [B][H][dv] fp32.
+ *   d in 1..64, dv in 1..256.  State arithmetic is fp32.
+ */
+KATA_API kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k,
+                               const void* v, float* out, int B, int H, int d, int dv,
+                               kata_dtype_t dtype, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+KATA_API const char* kata_status_string(kata_status_t s);
+
+/* ABI version of this header (major*100 + minor). */
+KATA_API int kata_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KATA_H */

@@ -1,0 +1,226 @@
+"""libkata: causal KATA-M1 attention (rank-one PSD feature map) on MI355X.
+
+Thin Python binding over the C ABI in include/kata.h.  It only marshals torch
+device tensors (pointers, sizes, the current HIP stream) into the library;
+every step of the computation runs in the library's HIP kernels.  There is no
+fallback: if libkata.so is missing or fails to load, every call raises.
+
+    import paper_2607_17419_amd as kata
+    out = kata.fwd_chunked(q, k, v, C=64)           # q, k: [B,H,T,d]; v: [B,H,T,dv]
+    S, z = kata.prefill_state(k, v)                 # packed state after T tokens
+    o = kata.decode_step(S, z, q1, k1, v1)          # one token per head, in place
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "KataError", "lib", "fwd_chunked", "fwd_chunked_timed", "fwd_chunked_alloc", "workspace_bytes",
+    "default_span", "prefill_state", "decode_step", "packed_dim", "LIB_PATH",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkata.so")
+
+KATA_OK, KATA_ERR_INVALID_ARG, KATA_ERR_UNSUPPORTED, KATA_ERR_HIP = 0, 1, 2, 3
+KATA_F32, KATA_BF16 = 0, 1
+
+# every symbol include/kata.h declares
+EXPORTED = (
+    "kata_fwd_chunked", "kata_fwd_chunked_ws", "kata_fwd_chunked_timed", "kata_fwd_workspace_bytes",
+    "kata_fwd_default_span", "kata_prefill_state", "kata_decode_step",
+    "kata_status_string", "kata_abi_version",
+)
+
+
+class KataError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {_status_name(status)} ({status})")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libkata (ctypes.CDLL); raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libkata.so not found at {LIB_PATH}; run "
+                          "`python -m paper_2607_17419_amd.build` first")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    L.kata_fwd_chunked.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+    L.kata_fwd_chunked.restype = i
+    L.kata_fwd_chunked_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp]
+    L.kata_fwd_chunked_ws.restype = i
+    L.kata_fwd_chunked_timed.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp, vp]
+    L.kata_fwd_chunked_timed.restype = i
+    L.kata_fwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
+    L.kata_fwd_workspace_bytes.restype = sz
+    L.kata_fwd_default_span.argtypes = [i, i, i, i, i, i, i]
+    L.kata_fwd_default_span.restype = i
+    L.kata_prefill_state.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
+    L.kata_prefill_state.restype = i
+    L.kata_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp]
+    L.kata_decode_step.restype = i
+    L.kata_status_string.argtypes = [i]
+    L.kata_status_string.restype = ctypes.c_char_p
+    L.kata_abi_version.argtypes = []
+    L.kata_abi_version.restype = i
+    _lib = L
+    return L
+
+
+def _status_name(s: int) -> str:
+    try:
+        return lib().kata_status_string(s).decode()
+    except Exception:  # library not loadable: still report the number
+        return f"status {s}"
+
+
+def _check(status: int, what: str):
+    if status != KATA_OK:
+        raise KataError(status, what)
+
+
+def packed_dim(d: int) -> int:
+    return d * (d + 1) // 2
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return KATA_F32
+    if t.dtype == torch.bfloat16:
+        return KATA_BF16
+    raise TypeError(f"q/k/v must be float32 or bfloat16, got {t.dtype}")
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    import torch
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _qkv_shapes(q, k, v):
+    if q.dim() != 4 or k.shape != q.shape or v.dim() != 4 or v.shape[:3] != q.shape[:3]:
+        raise ValueError(f"expected q,k [B,H,T,d] and v [B,H,T,dv]; got {tuple(q.shape)}, "
+                         f"{tuple(k.shape)}, {tuple(v.shape)}")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k and v must share one dtype")
+    B, H, T, d = q.shape
+    return B, H, T, d, v.shape[3]
+
+
+def workspace_bytes(B, H, T, d, dv, C, dtype_code, span_chunks=0) -> int:
+    return int(lib().kata_fwd_workspace_bytes(B, H, T, d, dv, C, dtype_code, span_chunks))
+
+
+def default_span(B, H, T, d, dv, C, dtype_code) -> int:
+    return int(lib().kata_fwd_default_span(B, H, T, d, dv, C, dtype_code))
+
+
+def fwd_chunked(q, k, v, C: int, span_chunks: int = 0, out=None, workspace=None, stream=None):
+    """Causal KATA-M1 forward via kata_fwd_chunked_ws; returns out [B,H,T,dv] fp32.
+
+    The workspace is a torch uint8 device tensor (allocated here if not given).
+    """
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = workspace_bytes(B, H, T, d, dv, C, code, span_chunks)
+    if nbytes == 0:
+        # let the library report why
+        _check(lib().kata_fwd_chunked_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                         _dev(out, "out"), B, H, T, d, dv, C, code,
+                                         span_chunks, ctypes.c_void_p(0), 0,
+                                         _stream(stream, q.device)), "kata_fwd_chunked_ws")
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    _check(lib().kata_fwd_chunked_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                     B, H, T, d, dv, C, code, span_chunks,
+                                     _dev(workspace, "workspace"), workspace.numel(),
+                                     _stream(stream, q.device)), "kata_fwd_chunked_ws")
+    return out
+
+
+def fwd_chunked_timed(q, k, v, C: int, events, span_chunks: int = 0, out=None, workspace=None,
+                      stream=None):
+    """fwd_chunked that also records 4 caller-created HIP events (a ctypes array
+    of 4 void pointers) around the three stages on the launch stream."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = workspace_bytes(B, H, T, d, dv, C, code, span_chunks)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_fwd_chunked_timed(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                        _dev(out, "out"), B, H, T, d, dv, C, code, span_chunks,
+                                        _dev(workspace, "workspace"), workspace.numel(),
+                                        events, _stream(stream, q.device)),
+           "kata_fwd_chunked_timed")
+    return out
+
+
+def fwd_chunked_alloc(q, k, v, C: int, out=None, stream=None):
+    """Causal forward via kata_fwd_chunked (library allocates its workspace
+    stream-ordered); returns out [B,H,T,dv] fp32."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_fwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                  B, H, T, d, dv, C, code, _stream(stream, q.device)),
+           "kata_fwd_chunked")
+    return out
+
+
+def prefill_state(k, v, S=None, z=None, stream=None):
+    """Packed state after all T tokens: S [B,H,n,dv], z [B,H,n] (fp32)."""
+    import torch
+    if k.dim() != 4 or v.dim() != 4 or v.shape[:3] != k.shape[:3] or k.dtype != v.dtype:
+        raise ValueError("expected k [B,H,T,d] and v [B,H,T,dv] of one dtype")
+    B, H, T, d = k.shape
+    dv = v.shape[3]
+    n = packed_dim(d)
+    if S is None:
+        S = torch.empty((B, H, n, dv), dtype=torch.float32, device=k.device)
+    if z is None:
+        z = torch.empty((B, H, n), dtype=torch.float32, device=k.device)
+    _check(lib().kata_prefill_state(_dev(k, "k"), _dev(v, "v"), _dev(S, "S"), _dev(z, "z"),
+                                    B, H, T, d, dv, _dtype_code(k), _stream(stream, k.device)),
+           "kata_prefill_state")
+    return S, z
+
+
+def decode_step(S, z, q, k, v, out=None, stream=None):
+    """One decode step (S, z updated in place); q, k [B,H,d], v [B,H,dv] -> out [B,H,dv]."""
+    import torch
+    if q.dim() != 3 or k.shape != q.shape or v.dim() != 3 or v.shape[:2] != q.shape[:2]:
+        raise ValueError("expected q, k [B,H,d] and v [B,H,dv]")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k and v must share one dtype")
+    B, H, d = q.shape
+    dv = v.shape[2]
+    if out is None:
+        out = torch.empty((B, H, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_decode_step(_dev(S, "S"), _dev(z, "z"), _dev(q, "q"), _dev(k, "k"),
+                                  _dev(v, "v"), _dev(out, "out"), B, H, d, dv, _dtype_code(q),
+                                  _stream(stream, q.device)), "kata_decode_step")
+    return out

@@ -1,0 +1,201 @@
+// kata_api.hip -- host side of the libkata C ABI (include/kata.h): argument
+// validation, path selection (bf16 MFMA fast path or fp32 path), workspace
+// handling and error mapping.  Nothing here touches the GPU before the
+// arguments have been validated.
+#include <climits>
+#include <cstdint>
+
+#include "kata.h"
+#include "kata_internal.hpp"
+
+namespace {
+
+constexpr long long kMaxElems = 1LL << 40;  // per-tensor element bound
+constexpr int kGridYZ = 65535;
+
+enum class Path { kInvalid, kUnsupported, kMfma, kFp32 };
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool product_ok(long long a, long long b, long long c, long long d) {
+  // a*b*c*d <= kMaxElems with every factor >= 1
+  long long p = a;
+  for (long long f : {b, c, d}) {
+    if (p > kMaxElems / f) return false;
+    p *= f;
+  }
+  return true;
+}
+
+// Default span: about 1024 tokens of state per stored record on the MFMA path.
+int default_span(int C, Path path) {
+  if (path != Path::kMfma) return 1;
+  int g = 1024 / C;
+  return g < 1 ? 1 : g;
+}
+
+Path fwd_path(int B, int H, int T, int d, int dv, int C, int dtype) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1 || C < 1) return Path::kInvalid;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return Path::kInvalid;
+  if (!product_ok(B, H, T, d > dv ? d : dv)) return Path::kInvalid;
+  if (static_cast<long long>(B) * H > kGridYZ) return Path::kUnsupported;
+  if (dtype == KATA_BF16 && kata::mfma_supported(d, dv, C)) return Path::kMfma;
+  if (d > 64 || dv > 256 || C > 128) return Path::kUnsupported;
+  if ((static_cast<long long>(T) + C - 1) / C > kGridYZ) return Path::kUnsupported;
+  return Path::kFp32;
+}
+
+int span_tokens(int T, int C, int span_chunks) {
+  long long L = static_cast<long long>(C) * span_chunks;
+  const long long Tc = (static_cast<long long>(T) + C - 1) / C * C;  // T rounded up to C
+  if (L > Tc) L = Tc;
+  return static_cast<int>(L);
+}
+
+size_t workspace_for(Path path, int B, int H, int T, int d, int dv, int C, int span_chunks) {
+  const int BH = B * H;
+  if (path == Path::kFp32) return kata::fp32_forward_workspace(BH, T, d, dv, C);
+  if (path == Path::kMfma) {
+    const int L = span_tokens(T, C, span_chunks);
+    return kata::mfma_forward_workspace(BH, T, d, dv, L);
+  }
+  return 0;
+}
+
+kata_status_t from_hip(hipError_t e) { return e == hipSuccess ? KATA_OK : KATA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int kata_abi_version(void) { return 100; }
+
+const char* kata_status_string(kata_status_t s) {
+  switch (s) {
+    case KATA_OK: return "KATA_OK";
+    case KATA_ERR_INVALID_ARG: return "KATA_ERR_INVALID_ARG";
+    case KATA_ERR_UNSUPPORTED: return "KATA_ERR_UNSUPPORTED";
+    case KATA_ERR_HIP: return "KATA_ERR_HIP";
+  }
+  return "KATA_UNKNOWN_STATUS";
+}
+
+int kata_fwd_default_span(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype) {
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
+  if (p == Path::kInvalid || p == Path::kUnsupported) return 0;
+  return default_span(C, p);
+}
+
+size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype,
+                                int span_chunks) {
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
+  if (p == Path::kInvalid || p == Path::kUnsupported || span_chunks < 0) return 0;
+  if (span_chunks == 0) span_chunks = default_span(C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  return workspace_for(p, B, H, T, d, dv, C, span_chunks);
+}
+
+}  // extern "C"
+
+static kata_status_t fwd_ws(const void* q, const void* k, const void* v, float* out, int B,
+                            int H, int T, int d, int dv, int C, kata_dtype_t dtype,
+                            int span_chunks, void* workspace, size_t workspace_bytes,
+                            hipEvent_t* ev, hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  if (span_chunks < 0) return KATA_ERR_INVALID_ARG;
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (span_chunks == 0) span_chunks = default_span(C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  const size_t need = workspace_for(p, B, H, T, d, dv, C, span_chunks);
+  if (workspace_bytes < need) return KATA_ERR_INVALID_ARG;
+  const int BH = B * H;
+  if (p == Path::kMfma) {
+    const int L = span_tokens(T, C, span_chunks);
+    if ((static_cast<long long>(T) + L - 1) / L > kGridYZ) return KATA_ERR_UNSUPPORTED;
+    return from_hip(
+        kata::launch_mfma_forward(q, k, v, out, BH, T, d, dv, L, workspace, stream, ev));
+  }
+  if (dtype == KATA_F32)
+    return from_hip(
+        kata::launch_fp32_forward<float>(q, k, v, out, BH, T, d, dv, C, workspace, stream, ev));
+  return from_hip(kata::launch_fp32_forward<kata::bf16_t>(q, k, v, out, BH, T, d, dv, C,
+                                                          workspace, stream, ev));
+}
+
+extern "C" {
+
+kata_status_t kata_fwd_chunked_ws(const void* q, const void* k, const void* v, float* out, int B,
+                                  int H, int T, int d, int dv, int C, kata_dtype_t dtype,
+                                  int span_chunks, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span_chunks, workspace, workspace_bytes,
+                nullptr, stream);
+}
+
+kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v, float* out,
+                                     int B, int H, int T, int d, int dv, int C,
+                                     kata_dtype_t dtype, int span_chunks, void* workspace,
+                                     size_t workspace_bytes, hipEvent_t* stage_events,
+                                     hipStream_t stream) {
+  if (!stage_events) return KATA_ERR_INVALID_ARG;
+  for (int i = 0; i < 4; ++i)
+    if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span_chunks, workspace, workspace_bytes,
+                stage_events, stream);
+}
+
+kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
+                               int H, int T, int d, int dv, int C, kata_dtype_t dtype,
+                               hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  const int span = (p == Path::kFp32) ? 1 : default_span(C, p);
+  const size_t bytes = workspace_for(p, B, H, T, d, dv, C, span);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  const kata_status_t st =
+      fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span, ws, bytes, nullptr, stream);
+  const hipError_t fe = hipFreeAsync(ws, stream);
+  if (st != KATA_OK) return st;
+  return from_hip(fe);
+}
+
+kata_status_t kata_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
+                                 int T, int d, int dv, kata_dtype_t dtype, hipStream_t stream) {
+  if (!k || !v || !S || !z) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(S) || !aligned16(z)) return KATA_ERR_INVALID_ARG;
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
+  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
+  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  const int BH = B * H;
+  if (dtype == KATA_F32) return from_hip(kata::launch_prefill<float>(k, v, S, z, BH, T, d, dv, stream));
+  return from_hip(kata::launch_prefill<kata::bf16_t>(k, v, S, z, BH, T, d, dv, stream));
+}
+
+kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k, const void* v,
+                               float* out, int B, int H, int d, int dv, kata_dtype_t dtype,
+                               hipStream_t stream) {
+  if (!S || !z || !q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(S) || !aligned16(z) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
+      !aligned16(out))
+    return KATA_ERR_INVALID_ARG;
+  if (B < 1 || H < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, d * (d + 1) / 2, dv)) return KATA_ERR_INVALID_ARG;
+  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
+  if (static_cast<long long>(B) * H > INT_MAX) return KATA_ERR_UNSUPPORTED;
+  const int BH = B * H;
+  if (dtype == KATA_F32) return from_hip(kata::launch_decode<float>(S, z, q, k, v, out, BH, d, dv, stream));
+  return from_hip(kata::launch_decode<kata::bf16_t>(S, z, q, k, v, out, BH, d, dv, stream));
+}
+
+}  // extern "C"

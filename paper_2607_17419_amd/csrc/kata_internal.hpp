@@ -1,0 +1,50 @@
+// kata_internal.hpp -- internal launch interface between the libkata host
+// dispatch (kata_api.hip) and the kernel files.
+#pragma once
+
+#include "kata_common.hpp"
+
+namespace kata {
+
+// Per-element weight applied by the prefix scan when it writes its output.
+struct UnitWeight {
+  __device__ __forceinline__ float operator()(long long) const { return 1.f; }
+};
+
+__device__ __forceinline__ void store_weighted(float* p, long long i, float x, float w) {
+  p[i] = x * w;
+}
+__device__ __forceinline__ void store_weighted(bf16_t* p, long long i, float x, float w) {
+  __bf16 h = static_cast<__bf16>(x * w);
+  p[i].bits = __builtin_bit_cast(uint16_t, h);
+}
+
+// ---- fp32 path (kata_fp32.hip) -------------------------------------------
+size_t fp32_forward_workspace(int BH, int T, int d, int dv, int C);
+size_t fp32_forward_smem(int d, int C);
+
+// ev: null, or 4 events recorded on `st` before the state kernel and after
+// each of the three stages (state, scan, output).
+template <typename Tin>
+hipError_t launch_fp32_forward(const void* q, const void* k, const void* v, float* out, int BH,
+                               int T, int d, int dv, int C, void* ws, hipStream_t st,
+                               hipEvent_t* ev);
+template <typename Tin>
+hipError_t launch_prefill(const void* k, const void* v, float* S, float* z, int BH, int T, int d,
+                          int dv, hipStream_t st);
+template <typename Tin>
+hipError_t launch_decode(float* S, float* z, const void* q, const void* k, const void* v,
+                         float* out, int BH, int d, int dv, hipStream_t st);
+
+// ---- bf16 MFMA path (kata_mfma.hip) ---------------------------------------
+bool mfma_supported(int d, int dv, int C);
+size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L);
+hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
+                               int T, int d, int dv, int L, void* ws, hipStream_t st,
+                               hipEvent_t* ev);
+
+inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
+  return ev ? hipEventRecord(ev[i], st) : hipSuccess;
+}
+
+}  // namespace kata

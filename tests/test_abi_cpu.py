@@ -1,0 +1,115 @@
+"""libkata on the CPU: the library loads, exports every symbol include/kata.h
+declares, and rejects bad arguments on the host before any GPU call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_17419_amd as kata
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    with open(os.path.join(ROOT, "include", "kata.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(kata_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_matches_binding():
+    assert _declared_symbols() == sorted(kata.EXPORTED)
+
+
+def test_library_exports_every_symbol():
+    L = kata.lib()
+    for name in _declared_symbols():
+        assert hasattr(L, name), name
+
+
+def test_status_strings_and_version():
+    L = kata.lib()
+    assert L.kata_status_string(0) == b"KATA_OK"
+    assert L.kata_status_string(1) == b"KATA_ERR_INVALID_ARG"
+    assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
+    assert L.kata_status_string(3) == b"KATA_ERR_HIP"
+    assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
+    assert L.kata_abi_version() == 100
+
+
+FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
+NUL = ctypes.c_void_p(0)
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((NUL, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 0), 1),          # null q
+    ((FAKE, FAKE, FAKE, FAKE, 0, 1, 8, 16, 16, 32, 0), 1),         # B < 1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 16, 16, 32, 0), 1),         # T < 1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 0, 0), 1),          # C < 1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 7), 1),         # bad dtype
+    ((FAKE, FAKE, FAKE, ctypes.c_void_p(0x10004), 1, 1, 8, 16, 16, 32, 0), 1),  # misaligned
+    ((FAKE, FAKE, FAKE, FAKE, 1 << 20, 1 << 20, 1 << 20, 16, 16, 32, 0), 1),  # overflow
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 65, 16, 32, 1), 2),         # d > 64
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 300, 32, 0), 2),        # dv > 256 on fp32 path
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 200, 0), 2),        # C > 128 on fp32 path
+])
+def test_fwd_rejects_before_gpu(args, expect):
+    L = kata.lib()
+    st = L.kata_fwd_chunked(*args, NUL)
+    assert st == expect
+
+
+def test_ws_variant_rejects():
+    L = kata.lib()
+    # workspace too small for a valid bf16 MFMA shape
+    need = L.kata_fwd_workspace_bytes(1, 1, 128, 64, 64, 64, 1, 0)
+    assert need > 0
+    st = L.kata_fwd_chunked_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 64, 1, 0,
+                               ctypes.c_void_p(0x100000), need - 1, NUL)
+    assert st == 1
+    # misaligned workspace
+    st = L.kata_fwd_chunked_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 64, 1, 0,
+                               ctypes.c_void_p(0x100010), need, NUL)
+    assert st == 1
+    # negative span
+    st = L.kata_fwd_chunked_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 64, 1, -1,
+                               ctypes.c_void_p(0x100000), need, NUL)
+    assert st == 1
+
+
+def test_workspace_and_span_host_logic():
+    L = kata.lib()
+    # fp32 path: one fp32 record (S n x dv, then z n) per chunk and head
+    n = 16 * 17 // 2
+    assert L.kata_fwd_workspace_bytes(1, 2, 256, 16, 16, 32, 0, 0) == 2 * 8 * (n * 16 + n) * 4
+    assert L.kata_fwd_default_span(1, 2, 256, 16, 16, 32, 0) == 1
+    # MFMA path: default span folds about 1024 tokens
+    assert L.kata_fwd_default_span(1, 16, 131072, 64, 64, 64, 1) == 16
+    assert L.kata_fwd_default_span(4, 8, 16384, 32, 64, 128, 1) == 8
+    # MFMA record: 2112 slots x 64 dv + 64 x 64 Z, fp32 then bf16 copies
+    rec = 2112 * 64 + 64 * 64
+    NS = 131072 // 1024
+    expect = 16 * NS * rec * 4 + 16 * NS * rec * 2
+    assert L.kata_fwd_workspace_bytes(1, 16, 131072, 64, 64, 64, 1, 0) == expect
+    # invalid -> 0
+    assert L.kata_fwd_workspace_bytes(1, 1, 0, 64, 64, 64, 1, 0) == 0
+    assert L.kata_fwd_default_span(1, 1, 8, 65, 64, 64, 1) == 0
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((NUL, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 16, 16, 0), 1),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, 16, 16, 0), 1),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 80, 16, 0), 2),
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 16, 512, 1), 2),
+])
+def test_decode_rejects_before_gpu(args, expect):
+    assert kata.lib().kata_decode_step(*args, NUL) == expect
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((FAKE, NUL, FAKE, FAKE, 1, 1, 8, 16, 16, 0), 1),
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 16, 16, 0), 1),
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 100, 16, 0), 2),
+])
+def test_prefill_rejects_before_gpu(args, expect):
+    assert kata.lib().kata_prefill_state(*args, NUL) == expect
