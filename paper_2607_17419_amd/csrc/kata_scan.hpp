@@ -83,3 +83,95 @@ __global__ __launch_bounds__(256) void scan_exclusive(const float* in, OutT* out
 }
 
 }  // namespace kata
+
+namespace kata {
+
+// ---------------------------------------------------------------------------
+// In-place exclusive prefix over bf16 records (the MFMA path's span states):
+//   rec[bh][c][e] <- bf16( w(e) * sum_{c' < c} rec[bh][c'][e] ),  rec[.][0][.] = 0,
+// with the sums carried in fp32.  A workgroup owns kEB16 consecutive elements
+// of every record (512-byte rows, 16-byte accesses); rows are processed in
+// blocks of kNB16 with a Blelloch tree in LDS and an fp32 carry between blocks.
+// E must be a multiple of 8.  grid (ceil(E / kEB16), BH), block 256.
+// ---------------------------------------------------------------------------
+constexpr int kEB16 = 256;
+constexpr int kNB16 = 32;
+
+template <typename Weight>
+__global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N, long long E,
+                                                           long long bh_stride, Weight weight) {
+  __shared__ float tile[kNB16][kEB16 + 4];
+  __shared__ float total_s[kEB16];
+  const int tid = threadIdx.x;
+  const long long e0 = static_cast<long long>(blockIdx.x) * kEB16;
+  uint16_t* rb = rec + blockIdx.y * bh_stride;
+  const int cc = tid & 31;        // 8-element chunk of the column block
+  const int r8 = tid >> 5;        // row inside a pass of 8 rows
+  const long long ec = e0 + 8 * cc;
+  const bool active = ec < E;
+  float carry[8];
+  float w[8];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    carry[x] = 0.f;
+    w[x] = active ? weight(ec + x) : 0.f;
+  }
+  for (int r0 = 0; r0 < N; r0 += kNB16) {
+    const int nr = min(kNB16, N - r0);
+#pragma unroll
+    for (int p = 0; p < kNB16 / 8; ++p) {
+      const int r = r8 + 8 * p;
+      uint4 q4 = make_uint4(0u, 0u, 0u, 0u);
+      if (active && r < nr)
+        q4 = *reinterpret_cast<const uint4*>(rb + static_cast<long long>(r0 + r) * E + ec);
+      const uint32_t q[4] = {q4.x, q4.y, q4.z, q4.w};
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        tile[r][8 * cc + 2 * x] = bf16lo_f32(q[x]);
+        tile[r][8 * cc + 2 * x + 1] = bf16hi_f32(q[x]);
+      }
+    }
+    __syncthreads();
+    for (int step = 1; step < kNB16; step <<= 1) {
+      const int nodes = kNB16 / (2 * step);
+      for (int i = tid; i < nodes * kEB16; i += 256) {
+        const int node = i / kEB16, col = i % kEB16;
+        const int right = (node + 1) * 2 * step - 1;
+        tile[right][col] += tile[right - step][col];
+      }
+      __syncthreads();
+    }
+    total_s[tid] = tile[kNB16 - 1][tid];
+    tile[kNB16 - 1][tid] = 0.f;
+    __syncthreads();
+    for (int step = kNB16 / 2; step >= 1; step >>= 1) {
+      const int nodes = kNB16 / (2 * step);
+      for (int i = tid; i < nodes * kEB16; i += 256) {
+        const int node = i / kEB16, col = i % kEB16;
+        const int right = (node + 1) * 2 * step - 1;
+        const float left = tile[right - step][col];
+        tile[right - step][col] = tile[right][col];
+        tile[right][col] += left;
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int p = 0; p < kNB16 / 8; ++p) {
+      const int r = r8 + 8 * p;
+      if (active && r < nr) {
+        uint32_t q[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+          q[x] = pack_bf16x2(w[2 * x] * (tile[r][8 * cc + 2 * x] + carry[2 * x]),
+                             w[2 * x + 1] * (tile[r][8 * cc + 2 * x + 1] + carry[2 * x + 1]));
+        *reinterpret_cast<uint4*>(rb + static_cast<long long>(r0 + r) * E + ec) =
+            make_uint4(q[0], q[1], q[2], q[3]);
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < 8; ++x) carry[x] += total_s[8 * cc + x];
+    __syncthreads();
+  }
+}
+
+}  // namespace kata
