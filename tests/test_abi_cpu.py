@@ -86,10 +86,11 @@ def test_workspace_and_span_host_logic():
     # MFMA path: default span folds about 1024 tokens
     assert L.kata_fwd_default_span(1, 16, 131072, 64, 64, 64, 1) == 16
     assert L.kata_fwd_default_span(4, 8, 16384, 32, 64, 128, 1) == 8
-    # MFMA record: 2112 slots x 64 dv + 64 x 64 Z, fp32 then bf16 copies
+    # MFMA path: one bf16 record (2112 slots x 64 dv + 64 x 64 Z) per span and
+    # head, scanned in place, plus a bf16 V^T copy (64 x span) per span and head
     rec = 2112 * 64 + 64 * 64
     NS = 131072 // 1024
-    expect = 16 * NS * rec * 4 + 16 * NS * rec * 2
+    expect = 16 * NS * rec * 2 + 16 * NS * 64 * 1024 * 2
     assert L.kata_fwd_workspace_bytes(1, 16, 131072, 64, 64, 64, 1, 0) == expect
     # invalid -> 0
     assert L.kata_fwd_workspace_bytes(1, 1, 0, 64, 64, 64, 1, 0) == 0
