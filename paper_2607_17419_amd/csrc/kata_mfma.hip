@@ -210,13 +210,14 @@ __device__ __forceinline__ int kswz(int r) {
 __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 chunks
 
 // ---------------------------------------------------------------------------
-// K2: span state.  grid (unit blocks, NS, BH), block 256 (4 waves).
-// Units: slot tiles 0..NST-1 (32 slots x dv) and Z tiles NST..NST+ZM-1
-// (32 dims x d).  Wave w of unit block ub owns units [(4*ub + w)*UW, +UW).
+// K2: span state.  grid (UB + 1, NS, BH), block 256 (4 waves).
+// Blocks 0..UB-1: slot tiles.  Wave w of block ub owns tiles
+// [(4*ub + w)*UW, +UW); every wave runs the same branch-free MFMA loop (tiles
+// past the last one compute on a valid row and skip their store), so the
+// accumulators stay in place.  Block UB: Z = K^T K (one 32x32 tile per wave)
+// and the span's V^T (bf16, [dv][LV], keys of every 16-key group in the order
+// 0-3, 8-11, 4-7, 12-15, the K order of the output kernel's P V product).
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
-// Unit block 0 also writes the span's V^T (bf16, [dv][L], keys of every
-// 16-key group in the order 0-3, 8-11, 4-7, 12-15, the K order of the output
-// kernel's P V product).
 // ---------------------------------------------------------------------------
 constexpr int kTB2 = 64;            // tokens per staged block
 constexpr int kRow2 = kTB2 + 8;     // LDS row length (bf16), 144 B
@@ -228,7 +229,6 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
                                                          uint16_t* __restrict__ vtp, int T,
                                                          int L, int LV) {
   using G = Geo<D, DV>;
-  constexpr int NUNITS = G::NST + G::ZM;
   constexpr int NXR = D / 32;  // distinct x rows per lane (x depends on tile % NXR)
   static_assert(UW % NXR == 0, "unit parity must be static");
   __shared__ __attribute__((aligned(16))) uint16_t kT[2][D][kRow2];
@@ -238,12 +238,12 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 31, g = lane >> 5;
   const int s = blockIdx.y, bh = blockIdx.z;
+  const bool zblock = blockIdx.x == gridDim.x - 1;
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
   const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
   const int unit0 = (blockIdx.x * 4 + wave) * UW;
-  const bool write_vt = blockIdx.x == 0;
 
   int xrow[NXR];
 #pragma unroll
@@ -255,16 +255,9 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
 #pragma unroll
   for (int u = 0; u < UW; ++u) {
     int xx;
-    yrow[u] = 0;
-    if (unit0 + u < G::NST) slot_pair<D>(32 * (unit0 + u) + c, xx, yrow[u]);
+    const int unit = unit0 + u < G::NST ? unit0 + u : G::NST - 1;  // valid row; store skipped
+    slot_pair<D>(32 * unit + c, xx, yrow[u]);
   }
-  f32x16 acc[UW][G::MT];
-#pragma unroll
-  for (int u = 0; u < UW; ++u)
-#pragma unroll
-    for (int m = 0; m < G::MT; ++m)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
 
   // staging: task -> (pair p of tokens, 8-wide column group); K then V
   constexpr int KG = D / 8, VG = DV / 8;
@@ -310,30 +303,72 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       }
     }
   };
-  // V^T block -> global, keys permuted inside 16-key groups (unit block 0 only)
-  uint16_t* vt_rec = vtp + (static_cast<long long>(bh) * gridDim.y + s) * DV * LV;
-  auto write_vtp = [&](int buf, int bi) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < (DV * 8) / 256; ++i) {
-      const int task = tid + 256 * i;
-      const int m = task >> 3, h = task & 7;         // row, output chunk of 8 keys
-      const int grp = h >> 1, hg = h & 1;
-      const uint16_t* row = &vT[buf][m][16 * grp + 4 * hg];
-      const uint2 lo = *reinterpret_cast<const uint2*>(row);
-      const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
-      *reinterpret_cast<uint4*>(vt_rec + static_cast<long long>(m) * LV + kTB2 * bi + 8 * h) =
-          make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
-  };
-
   const int nblk = static_cast<int>((span_end - span0 + kTB2 - 1) / kTB2);
+  uint16_t* rec = spanst + (static_cast<long long>(bh) * gridDim.y + s) * G::E;
+
+  if (zblock) {
+    // ---- Z = K^T K over the span, and the span's V^T for the output kernel ----
+    uint16_t* vt_rec = vtp + (static_cast<long long>(bh) * gridDim.y + s) * DV * LV;
+    const int zm = wave / G::ZM, zn = wave % G::ZM;  // this wave's 32x32 tile of Z
+    const bool zwave = wave < G::ZM * G::ZM;
+    f32x16 zacc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) zacc[r] = 0.f;
+    fetch(span0);
+    commit(0);
+    lds_barrier();
+    for (int bi = 0; bi < nblk; ++bi) {
+      const int buf = bi & 1;
+      if (bi + 1 < nblk) fetch(span0 + static_cast<long long>(bi + 1) * kTB2);
+#pragma unroll
+      for (int i = 0; i < (DV * 8) / 256; ++i) {
+        const int task = tid + 256 * i;
+        const int m = task >> 3, h = task & 7;  // row, output chunk of 8 keys
+        const int grp = h >> 1, hg = h & 1;
+        const uint16_t* row = &vT[buf][m][16 * grp + 4 * hg];
+        const uint2 lo = *reinterpret_cast<const uint2*>(row);
+        const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
+        *reinterpret_cast<uint4*>(vt_rec + static_cast<long long>(m) * LV + kTB2 * bi + 8 * h) =
+            make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+      if (zwave) {
+#pragma unroll
+        for (int ks = 0; ks < kTB2 / 16; ++ks) {
+          const int col = 16 * ks + 8 * g;
+          const bf16x8 Az = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * zm + c][col]);
+          const bf16x8 Bz = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * zn + c][col]);
+          zacc = mfma32(Az, Bz, zacc);
+        }
+      }
+      if (bi + 1 < nblk) commit(buf ^ 1);
+      lds_barrier();
+    }
+    if (zwave) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int a = 32 * zm + 8 * (r >> 2) + 4 * g + (r & 3);
+        const int b = 32 * zn + c;
+        __bf16 h = static_cast<__bf16>(zacc[r]);
+        rec[G::ES + zop_index<D>(a, b)] = __builtin_bit_cast(uint16_t, h);
+      }
+    }
+    return;
+  }
+
+  // ---- S_span^T = V^T Phi(K) for this wave's slot tiles ----------------------
+  f32x16 acc[UW][G::MT];
+#pragma unroll
+  for (int u = 0; u < UW; ++u)
+#pragma unroll
+    for (int m = 0; m < G::MT; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
   fetch(span0);
   commit(0);
-  __syncthreads();
+  lds_barrier();
   for (int bi = 0; bi < nblk; ++bi) {
     const int buf = bi & 1;
     if (bi + 1 < nblk) fetch(span0 + static_cast<long long>(bi + 1) * kTB2);
-    if (write_vt) write_vtp(buf, bi);
 #pragma unroll
     for (int ks = 0; ks < kTB2 / 16; ++ks) {
       const int col = 16 * ks + 8 * g;  // first token of this lane's 8
@@ -355,35 +390,23 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       }
 #pragma unroll
       for (int u = 0; u < UW; ++u) {
-        const int unit = unit0 + u;
-        if (unit < G::NST) {
-          const int p = u % NXR;
-          const uint4 Y4 = *reinterpret_cast<const uint4*>(&kT[buf][yrow[u]][col]);
-          const uint32_t Y[4] = {Y4.x, Y4.y, Y4.z, Y4.w};
-          float pr[8];
-          dot2x8(Y, xl[p], xh[p], pr);
-          const bf16x8 Bf = __builtin_bit_cast(
-              bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                                 pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+        const int p = u % NXR;
+        const uint4 Y4 = *reinterpret_cast<const uint4*>(&kT[buf][yrow[u]][col]);
+        const uint32_t Y[4] = {Y4.x, Y4.y, Y4.z, Y4.w};
+        float pr[8];
+        dot2x8(Y, xl[p], xh[p], pr);
+        const bf16x8 Bf = __builtin_bit_cast(
+            bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                               pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
 #pragma unroll
-          for (int m = 0; m < G::MT; ++m) acc[u][m] = mfma32(va[m], Bf, acc[u][m]);
-        } else if (unit < NUNITS) {
-          const int nz = unit - G::NST;
-          const bf16x8 Bz = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * nz + c][col]);
-#pragma unroll
-          for (int m = 0; m < G::ZM; ++m) {
-            const bf16x8 Az = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * m + c][col]);
-            acc[u][m] = mfma32(Az, Bz, acc[u][m]);
-          }
-        }
+        for (int m = 0; m < G::MT; ++m) acc[u][m] = mfma32(va[m], Bf, acc[u][m]);
       }
     }
     if (bi + 1 < nblk) commit(buf ^ 1);
     lds_barrier();
   }
 
-  // write the span record (bf16)
-  uint16_t* rec = spanst + (static_cast<long long>(bh) * gridDim.y + s) * G::E;
+  // write this wave's tiles of the span record (bf16)
 #pragma unroll
   for (int u = 0; u < UW; ++u) {
     const int unit = unit0 + u;
@@ -396,17 +419,6 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
           __bf16 h = static_cast<__bf16>(acc[u][m][r]);
           rec[static_cast<long long>(dvrow) * G::NSLOT + 32 * unit + c] =
               __builtin_bit_cast(uint16_t, h);
-        }
-    } else if (unit < NUNITS) {
-      const int nz = unit - G::NST;
-#pragma unroll
-      for (int m = 0; m < G::ZM; ++m)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int a = 32 * m + 8 * (r >> 2) + 4 * g + (r & 3);
-          const int b = 32 * nz + c;
-          __bf16 h = static_cast<__bf16>(acc[u][m][r]);
-          rec[G::ES + zop_index<D>(a, b)] = __builtin_bit_cast(uint16_t, h);
         }
     }
   }
@@ -811,11 +823,11 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
   constexpr int UW = 6;
-  constexpr int NUNITS = G::NST + G::ZM;
-  const int ub = (NUNITS + 4 * UW - 1) / (4 * UW);
+  const int ub = (G::NST + 4 * UW - 1) / (4 * UW);  // slot-tile blocks; one more for Z
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  span_state_kernel<D, DV, UW><<<dim3(ub, NS, BH), 256, 0, st>>>(kk, vv, spanst, vtp, T, L, LA);
+  span_state_kernel<D, DV, UW><<<dim3(ub + 1, NS, BH), 256, 0, st>>>(kk, vv, spanst, vtp, T, L,
+                                                                     LA);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   dim3 g3(static_cast<unsigned>((G::E + kEB16 - 1) / kEB16), BH);
   scan_exclusive_bf16<SlotWeight<D, DV>><<<g3, 256, 0, st>>>(
