@@ -174,29 +174,62 @@ __device__ __forceinline__ uint32_t word_of(const bf16x8& f, int j) {
   return j == 0 ? w.x : (j == 1 ? w.y : (j == 2 ? w.z : w.w));
 }
 
-// The eight state features of one lane's B fragment: for token pairs
-// e = 0..3, y[e] holds (k_y(t), k_y(t+1)) and xl/xh the masked pairs
-// (k_x(t), 0) and (0, k_x(t+1)).  v_dot2_f32_bf16 with a zero accumulator and
-// one zero lane returns the exact fp32 product.  The eight dot products are
-// issued back to back and followed by s_nop: the hardware does not interlock a
-// dot-product result read by the next few VALU instructions, and the compiler
-// cannot insert those wait states for instructions it does not see.
-__device__ __forceinline__ void dot2x8(const uint32_t y[4], const uint32_t xl[4],
-                                       const uint32_t xh[4], float p[8]) {
+// The two MFMAs of one slot tile (a0 += va0 * bf, a1 += va1 * bf) with the
+// eight feature products of the next tile computed under them: the y pairs
+// (bf16 (y_t, y_{t+1}) per dword) are widened to fp32 (shift / mask, exact)
+// between the MFMAs and multiplied by the widened x values (xf) after the
+// second.  A wave issues in order and an MFMA holds the matrix pipe for 32
+// cycles, so the eight widening instructions also space the two MFMAs; the
+// plain VALU work runs alongside them.  s_nop 1 first: a VALU write of bf
+// (its conversion) must be 2 wait states old when the MFMA reads it.  The
+// accumulators stay in AGPRs, which no VALU instruction writes; any later
+// read of them waits for the MFMA first (mfma_drain).
+__device__ __forceinline__ void mfma2_mul8(f32x16& a0, f32x16& a1, const bf16x8& va0,
+                                           const bf16x8& va1, const bf16x8& bf,
+                                           const uint32_t y[4], const float xf[8], float p[8]) {
+  float t[8];
   asm volatile(
-      "v_dot2_f32_bf16 %0, %8, %12, 0\n\t"
-      "v_dot2_f32_bf16 %1, %8, %16, 0\n\t"
-      "v_dot2_f32_bf16 %2, %9, %13, 0\n\t"
-      "v_dot2_f32_bf16 %3, %9, %17, 0\n\t"
-      "v_dot2_f32_bf16 %4, %10, %14, 0\n\t"
-      "v_dot2_f32_bf16 %5, %10, %18, 0\n\t"
-      "v_dot2_f32_bf16 %6, %11, %15, 0\n\t"
-      "v_dot2_f32_bf16 %7, %11, %19, 0\n\t"
-      "s_nop 4"
-      : "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]), "=&v"(p[5]),
-        "=&v"(p[6]), "=&v"(p[7])
-      : "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(xl[0]), "v"(xl[1]), "v"(xl[2]),
-        "v"(xl[3]), "v"(xh[0]), "v"(xh[1]), "v"(xh[2]), "v"(xh[3]));
+      "s_nop 1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %18, %20, %0\n\t"
+      "v_lshlrev_b32 %10, 16, %21\n\t"
+      "v_and_b32 %11, 0xffff0000, %21\n\t"
+      "v_lshlrev_b32 %12, 16, %22\n\t"
+      "v_and_b32 %13, 0xffff0000, %22\n\t"
+      "v_lshlrev_b32 %14, 16, %23\n\t"
+      "v_and_b32 %15, 0xffff0000, %23\n\t"
+      "v_lshlrev_b32 %16, 16, %24\n\t"
+      "v_and_b32 %17, 0xffff0000, %24\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %19, %20, %1\n\t"
+      "v_mul_f32 %2, %10, %25\n\t"
+      "v_mul_f32 %3, %11, %26\n\t"
+      "v_mul_f32 %4, %12, %27\n\t"
+      "v_mul_f32 %5, %13, %28\n\t"
+      "v_mul_f32 %6, %14, %29\n\t"
+      "v_mul_f32 %7, %15, %30\n\t"
+      "v_mul_f32 %8, %16, %31\n\t"
+      "v_mul_f32 %9, %17, %32"
+      : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
+        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7]), "=&v"(t[0]), "=&v"(t[1]), "=&v"(t[2]),
+        "=&v"(t[3]), "=&v"(t[4]), "=&v"(t[5]), "=&v"(t[6]), "=&v"(t[7])
+      : "v"(va0), "v"(va1), "v"(bf), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(xf[0]),
+        "v"(xf[1]), "v"(xf[2]), "v"(xf[3]), "v"(xf[4]), "v"(xf[5]), "v"(xf[6]), "v"(xf[7]));
+}
+
+// The two MFMAs of the last slot tile of a staged block (nothing to overlap).
+__device__ __forceinline__ void mfma2(f32x16& a0, f32x16& a1, const bf16x8& va0,
+                                      const bf16x8& va1, const bf16x8& bf) {
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %3, %4, %1"
+      : "+a"(a0), "+a"(a1)
+      : "v"(va0), "v"(va1), "v"(bf));
+}
+
+// Wait states after MFMAs issued from inline assembly, before any other
+// instruction reads their accumulators (covers the 16-pass case).
+__device__ __forceinline__ void mfma_drain() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
 // XOR swizzles of 16-byte chunks inside LDS rows; a row's logical chunk c is
@@ -210,152 +243,222 @@ __device__ __forceinline__ int kswz(int r) {
 __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 chunks
 
 // ---------------------------------------------------------------------------
-// K2: span state.  grid (UB + 1, NS, BH), block 256 (4 waves).
-// Blocks 0..UB-1: slot tiles.  Wave w of block ub owns tiles
-// [(4*ub + w)*UW, +UW); every wave runs the same branch-free MFMA loop (tiles
-// past the last one compute on a valid row and skip their store), so the
-// accumulators stay in place.  Block UB: Z = K^T K (one 32x32 tile per wave)
-// and the span's V^T (bf16, [dv][LV], keys of every 16-key group in the order
-// 0-3, 8-11, 4-7, 12-15, the K order of the output kernel's P V product).
+// K2: span state.  1-D grid of workgroups of 256 threads (4 waves).  A span
+// gets NB blocks: NUW = ceil(NST / kUW) slot waves, then one wave for Z and
+// V^T (any further wave only helps stage).  Block id -> (span, part) keeps
+// the blocks of one span on one XCD (equal id % 8), dispatched back to back,
+// so the later blocks' reads of the span's K and V hit that XCD's L2.
+// Slot wave gw owns slot tiles [gw*kUW, +kUW); tiles past the last one
+// compute on a valid row and skip their store, so every wave runs the same
+// branch-free MFMA loop.  The Z wave computes Z = K^T K and writes the span's
+// V^T (bf16, [dv][LV], keys of every 16-key group in the order 0-3, 8-11,
+// 4-7, 12-15: the K order of the output kernel's P V product).
+// K and V are staged transposed ([dim][token]) through LDS in blocks of kTB2
+// tokens, double buffered; a slot wave loads the LDS fragments of K-step
+// ks+1 before it computes K-step ks.
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
 // ---------------------------------------------------------------------------
-constexpr int kTB2 = 64;            // tokens per staged block
-constexpr int kRow2 = kTB2 + 8;     // LDS row length (bf16), 144 B
+constexpr int kTB2 = 128;           // tokens per staged block
+constexpr int kRow2 = kTB2 + 8;     // LDS row length (bf16): rows 272 B apart
+constexpr int kGap2 = 64;           // bf16 gap before key row d/2 (see krow)
+constexpr int kUW = 6;              // slot tiles per slot wave
+constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
 
-template <int D, int DV, int UW>
+template <int D, int DV>
+struct StateGrid {
+  static constexpr int NUW = (Geo<D, DV>::NST + kUW - 1) / kUW;  // slot waves per span
+  static constexpr int NB = (NUW + 1 + 3) / 4;                   // blocks per span
+};
+
+template <int D, int DV>
 __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ spanst,
                                                          uint16_t* __restrict__ vtp, int T,
-                                                         int L, int LV) {
+                                                         int L, int LV, int NS, int sp0,
+                                                         int nsp) {
   using G = Geo<D, DV>;
+  using SG = StateGrid<D, DV>;
+  constexpr int UW = kUW;
   constexpr int NXR = D / 32;  // distinct x rows per lane (x depends on tile % NXR)
   static_assert(UW % NXR == 0, "unit parity must be static");
-  __shared__ __attribute__((aligned(16))) uint16_t kT[2][D][kRow2];
-  __shared__ __attribute__((aligned(16))) uint16_t vT[2][DV][kRow2];
+  static_assert(G::MT == 2, "the slot loop issues the two dv tiles of a slot tile together");
+  constexpr int KS = kTB2 / 16;                      // K-steps per staged block
+  // Key row r of a K buffer starts at krow(r).  The slot tiles read rows r and
+  // r + d/2 in the same 16-lane phase of a ds_read_b128; with a uniform
+  // stride they would share banks, the gap of kGap2 elements (32 banks)
+  // before row d/2 moves the upper half to the other half of the banks.
+  constexpr int KBUFE = D * kRow2 + kGap2;           // elements of one K buffer
+  constexpr unsigned KBUF = KBUFE * 2;               // bytes of one K buffer
+  constexpr unsigned VBUF = DV * kRow2 * 2;          // bytes of one V buffer
+  auto krow = [](int r) { return r * kRow2 + (r >= D / 2 ? kGap2 : 0); };
+  __shared__ __attribute__((aligned(16))) uint16_t kT[kNBuf2][KBUFE];
+  __shared__ __attribute__((aligned(16))) uint16_t vT[kNBuf2][DV][kRow2];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 31, g = lane >> 5;
-  const int s = blockIdx.y, bh = blockIdx.z;
-  const bool zblock = blockIdx.x == gridDim.x - 1;
+  const int id = blockIdx.x;
+  const int jx = id >> 3;
+  const int part = jx % SG::NB;
+  const int sp = sp0 + 8 * (jx / SG::NB) + (id & 7);
+  if (sp >= nsp) return;  // whole workgroup: padding of the grid
+  const int s = sp % NS, bh = sp / NS;
+  const int gw = part * 4 + wave;  // wave index inside the span
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
   const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
-  const int unit0 = (blockIdx.x * 4 + wave) * UW;
+  uint16_t* rec = spanst + static_cast<long long>(sp) * G::E;
+  const int nblk = static_cast<int>((span_end - span0 + kTB2 - 1) / kTB2);
 
-  int xrow[NXR];
-#pragma unroll
-  for (int p = 0; p < NXR; ++p) {
-    int yy;
-    slot_pair<D>(32 * p + c, xrow[p], yy);
-  }
-  int yrow[UW];
-#pragma unroll
-  for (int u = 0; u < UW; ++u) {
-    int xx;
-    const int unit = unit0 + u < G::NST ? unit0 + u : G::NST - 1;  // valid row; store skipped
-    slot_pair<D>(32 * unit + c, xx, yrow[u]);
-  }
-
-  // staging: task -> (pair p of tokens, 8-wide column group); K then V
+  // staging: task -> (pair p of tokens, 8-wide column group cg); K then V
   constexpr int KG = D / 8, VG = DV / 8;
-  constexpr int NTASK = 32 * (KG + VG);
-  constexpr int TPT = (NTASK + 255) / 256;
+  constexpr int NPAIR = kTB2 / 2;
+  constexpr int NTASK = NPAIR * (KG + VG);
+  static_assert(NTASK % 256 == 0 && NPAIR == 64, "staging: one token pair per lane");
+  constexpr int TPT = NTASK / 256;
   uint4 st_lo[TPT], st_hi[TPT];
-  auto fetch = [&](long long t0) __attribute__((always_inline)) {
+  // Fetch / commit the staging tasks [i0, i1) of this thread for the block
+  // starting at token t0.  The loads are unconditional (token index clamped
+  // into the sequence) so that the number of loads in flight is the same on
+  // every path and waits can count them; tokens at or past the span end are
+  // zeroed by the byte selectors of the commit's permutes.
+  auto fetch = [&](long long t0, auto i0_c, auto i1_c) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-      const int task = tid + 256 * i;
-      const int cg = task >> 5, p = task & 31;
-      const long long ta = t0 + 2 * p, tb = ta + 1;
-      st_lo[i] = make_uint4(0u, 0u, 0u, 0u);
-      st_hi[i] = make_uint4(0u, 0u, 0u, 0u);
-      if (task < NTASK) {
-        if (cg < KG) {
-          if (ta < span_end) st_lo[i] = *reinterpret_cast<const uint4*>(kh + ta * D + 8 * cg);
-          if (tb < span_end) st_hi[i] = *reinterpret_cast<const uint4*>(kh + tb * D + 8 * cg);
-        } else {
-          const int vg = cg - KG;
-          if (ta < span_end) st_lo[i] = *reinterpret_cast<const uint4*>(vh + ta * DV + 8 * vg);
-          if (tb < span_end) st_hi[i] = *reinterpret_cast<const uint4*>(vh + tb * DV + 8 * vg);
-        }
+    for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
+      const int cg = wave + 4 * i, p = lane;  // wave-uniform column group
+      const long long ta = min(t0 + 2 * p, static_cast<long long>(T) - 1);
+      const long long tb = min(t0 + 2 * p + 1, static_cast<long long>(T) - 1);
+      if (cg < KG) {
+        st_lo[i] = *reinterpret_cast<const uint4*>(kh + ta * D + 8 * cg);
+        st_hi[i] = *reinterpret_cast<const uint4*>(kh + tb * D + 8 * cg);
+      } else {
+        const int vg = cg - KG;
+        st_lo[i] = *reinterpret_cast<const uint4*>(vh + ta * DV + 8 * vg);
+        st_hi[i] = *reinterpret_cast<const uint4*>(vh + tb * DV + 8 * vg);
       }
     }
   };
-  auto commit = [&](int buf) __attribute__((always_inline)) {
+  auto commit = [&](int buf, long long t0, auto i0_c, auto i1_c) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-      const int task = tid + 256 * i;
-      if (task >= NTASK) continue;
-      const int cg = task >> 5, p = task & 31;
-      uint16_t* base = (cg < KG) ? &kT[buf][8 * cg][0] : &vT[buf][8 * (cg - KG)][0];
+    for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
+      const int cg = wave + 4 * i, p = lane;
+      const bool va = t0 + 2 * p < span_end, vb = t0 + 2 * p + 1 < span_end;
+      // v_perm byte selectors: 0-3 pick bytes of the first token's word,
+      // 4-7 of the second's, 0x0c gives a zero byte
+      const uint32_t sel_e = (va ? 0x0100u : 0x0c0cu) | (vb ? 0x05040000u : 0x0c0c0000u);
+      const uint32_t sel_o = (va ? 0x0302u : 0x0c0cu) | (vb ? 0x07060000u : 0x0c0c0000u);
+      // rows 8*cg .. 8*cg+7 lie on one side of the gap (d/2 is a multiple of 8)
+      uint16_t* base = (cg < KG) ? &kT[buf][krow(8 * cg)] : &vT[buf][8 * (cg - KG)][0];
       const uint32_t a[4] = {st_lo[i].x, st_lo[i].y, st_lo[i].z, st_lo[i].w};
       const uint32_t b[4] = {st_hi[i].x, st_hi[i].y, st_hi[i].z, st_hi[i].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         // element 2e: (a.lo, b.lo); element 2e+1: (a.hi, b.hi)
         *reinterpret_cast<uint32_t*>(base + (2 * e) * kRow2 + 2 * p) =
-            __builtin_amdgcn_perm(b[e], a[e], 0x05040100u);
+            __builtin_amdgcn_perm(b[e], a[e], sel_e);
         *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2 + 2 * p) =
-            __builtin_amdgcn_perm(b[e], a[e], 0x07060302u);
+            __builtin_amdgcn_perm(b[e], a[e], sel_o);
       }
     }
   };
-  const int nblk = static_cast<int>((span_end - span0 + kTB2 - 1) / kTB2);
-  uint16_t* rec = spanst + (static_cast<long long>(bh) * gridDim.y + s) * G::E;
+  using I0 = std::integral_constant<int, 0>;
+  using IT = std::integral_constant<int, TPT>;
+  static_assert(TPT <= KS, "one staging piece per K-step at most");
+  const char* kbase = reinterpret_cast<const char*>(&kT[0][0]);
+  const char* vbase = reinterpret_cast<const char*>(&vT[0][0][0]);
 
-  if (zblock) {
-    // ---- Z = K^T K over the span, and the span's V^T for the output kernel ----
-    uint16_t* vt_rec = vtp + (static_cast<long long>(bh) * gridDim.y + s) * DV * LV;
-    const int zm = wave / G::ZM, zn = wave % G::ZM;  // this wave's 32x32 tile of Z
-    const bool zwave = wave < G::ZM * G::ZM;
-    f32x16 zacc;
+  // Three-deep ring: block bi is read from buffer bi % 3 while block bi+1 is
+  // published into the next buffer piece by piece (staging task j of each
+  // thread), and each piece's registers are refilled with block bi+2 right
+  // away, so a global load has a whole block of compute to arrive.
+  // Every block issues the same loads whether or not their data is used
+  // (past the span's last block they re-read clamped, valid addresses), so the
+  // count of loads in flight is the same on every path.
+  fetch(span0, I0{}, IT{});
+  commit(0, span0, I0{}, IT{});
+  fetch(span0 + kTB2, I0{}, IT{});
+  lds_barrier();
+
+  if (gw >= SG::NUW) {
+    // ---- Z = K^T K over the span and the span's V^T (wave NUW) --------------
+    const bool zwave = gw == SG::NUW;
+    uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
+    f32x16 zacc[G::ZM][G::ZM];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) zacc[r] = 0.f;
-    fetch(span0);
-    commit(0);
-    lds_barrier();
+    for (int a = 0; a < G::ZM; ++a)
+#pragma unroll
+      for (int b = 0; b < G::ZM; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) zacc[a][b][r] = 0.f;
     for (int bi = 0; bi < nblk; ++bi) {
-      const int buf = bi & 1;
-      if (bi + 1 < nblk) fetch(span0 + static_cast<long long>(bi + 1) * kTB2);
-#pragma unroll
-      for (int i = 0; i < (DV * 8) / 256; ++i) {
-        const int task = tid + 256 * i;
-        const int m = task >> 3, h = task & 7;  // row, output chunk of 8 keys
-        const int grp = h >> 1, hg = h & 1;
-        const uint16_t* row = &vT[buf][m][16 * grp + 4 * hg];
-        const uint2 lo = *reinterpret_cast<const uint2*>(row);
-        const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
-        *reinterpret_cast<uint4*>(vt_rec + static_cast<long long>(m) * LV + kTB2 * bi + 8 * h) =
-            make_uint4(lo.x, lo.y, hi.x, hi.y);
-      }
+      const int buf = bi % kNBuf2;
+      if (bi + 1 < nblk)
+        commit((bi + 1) % kNBuf2, span0 + static_cast<long long>(bi + 1) * kTB2, I0{}, IT{});
+      fetch(span0 + static_cast<long long>(bi + 2) * kTB2, I0{}, IT{});
       if (zwave) {
 #pragma unroll
-        for (int ks = 0; ks < kTB2 / 16; ++ks) {
-          const int col = 16 * ks + 8 * g;
-          const bf16x8 Az = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * zm + c][col]);
-          const bf16x8 Bz = *reinterpret_cast<const bf16x8*>(&kT[buf][32 * zn + c][col]);
-          zacc = mfma32(Az, Bz, zacc);
+        for (int i = 0; i < (DV * kTB2 / 8) / 64; ++i) {
+          const int task = lane + 64 * i;
+          const int m = task / (kTB2 / 8), h = task % (kTB2 / 8);  // row, chunk of 8 keys
+          const int grp = h >> 1, hg = h & 1;
+          const uint16_t* row = &vT[buf][m][16 * grp + 4 * hg];
+          const uint2 lo = *reinterpret_cast<const uint2*>(row);
+          const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
+          *reinterpret_cast<uint4*>(vt_rec + static_cast<long long>(m) * LV + kTB2 * bi + 8 * h) =
+              make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          bf16x8 A[G::ZM];
+#pragma unroll
+          for (int a = 0; a < G::ZM; ++a)
+            A[a] = *reinterpret_cast<const bf16x8*>(&kT[buf][krow(32 * a + c) + 16 * ks + 8 * g]);
+#pragma unroll
+          for (int a = 0; a < G::ZM; ++a)
+#pragma unroll
+            for (int b = 0; b < G::ZM; ++b) zacc[a][b] = mfma32(A[a], A[b], zacc[a][b]);
         }
       }
-      if (bi + 1 < nblk) commit(buf ^ 1);
       lds_barrier();
     }
     if (zwave) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int a = 32 * zm + 8 * (r >> 2) + 4 * g + (r & 3);
-        const int b = 32 * zn + c;
-        __bf16 h = static_cast<__bf16>(zacc[r]);
-        rec[G::ES + zop_index<D>(a, b)] = __builtin_bit_cast(uint16_t, h);
-      }
+      for (int za = 0; za < G::ZM; ++za)
+#pragma unroll
+        for (int zb = 0; zb < G::ZM; ++zb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int a = 32 * za + 8 * (r >> 2) + 4 * g + (r & 3);
+            const int b = 32 * zb + c;
+            __bf16 h = static_cast<__bf16>(zacc[za][zb][r]);
+            rec[G::ES + zop_index<D>(a, b)] = __builtin_bit_cast(uint16_t, h);
+          }
     }
     return;
   }
 
   // ---- S_span^T = V^T Phi(K) for this wave's slot tiles ----------------------
+  const int unit0 = gw * UW;
+  // per-lane byte offsets of the fragments inside buffer 0, column 8*g
+  unsigned xo[NXR], yo[UW], vo[G::MT];
+#pragma unroll
+  for (int p = 0; p < NXR; ++p) {
+    int xr, yy;
+    slot_pair<D>(32 * p + c, xr, yy);
+    xo[p] = static_cast<unsigned>((krow(xr) + 8 * g) * 2);
+  }
+#pragma unroll
+  for (int u = 0; u < UW; ++u) {
+    int xx, yr;
+    const int unit = unit0 + u < G::NST ? unit0 + u : G::NST - 1;  // valid row; store skipped
+    slot_pair<D>(32 * unit + c, xx, yr);
+    yo[u] = static_cast<unsigned>((krow(yr) + 8 * g) * 2);
+  }
+#pragma unroll
+  for (int m = 0; m < G::MT; ++m) vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
+
   f32x16 acc[UW][G::MT];
 #pragma unroll
   for (int u = 0; u < UW; ++u)
@@ -363,48 +466,111 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     for (int m = 0; m < G::MT; ++m)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
-  fetch(span0);
-  commit(0);
-  lds_barrier();
-  for (int bi = 0; bi < nblk; ++bi) {
-    const int buf = bi & 1;
-    if (bi + 1 < nblk) fetch(span0 + static_cast<long long>(bi + 1) * kTB2);
+
+  // LDS fragments: the y rows of the slot tiles (each reloaded for the next
+  // K-step as soon as the features it feeds are computed), the x rows of the
+  // next K-step, and V^T double buffered by K-step parity.
+  uint4 fy[UW], fx[NXR], fv[2][G::MT];
+  float xf[NXR][8];  // x values of the K-step's 8 tokens, widened to fp32
+  auto ldv = [&](int set, const char* vb, unsigned ko) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < kTB2 / 16; ++ks) {
-      const int col = 16 * ks + 8 * g;  // first token of this lane's 8
-      bf16x8 va[G::MT];
+    for (int m = 0; m < G::MT; ++m) fv[set][m] = *reinterpret_cast<const uint4*>(vb + vo[m] + ko);
+  };
+  auto ldx = [&](const char* kb, unsigned ko) __attribute__((always_inline)) {
 #pragma unroll
-      for (int m = 0; m < G::MT; ++m)
-        va[m] = *reinterpret_cast<const bf16x8*>(&vT[buf][32 * m + c][col]);
-      // masked x pairs: (x_t, 0) and (0, x_{t+1}) for each token pair
-      uint32_t xl[NXR][4], xh[NXR][4];
+    for (int p = 0; p < NXR; ++p) fx[p] = *reinterpret_cast<const uint4*>(kb + xo[p] + ko);
+  };
+  auto widen_x = [&]() __attribute__((always_inline)) {
 #pragma unroll
-      for (int p = 0; p < NXR; ++p) {
-        const uint4 X4 = *reinterpret_cast<const uint4*>(&kT[buf][xrow[p]][col]);
-        const uint32_t X[4] = {X4.x, X4.y, X4.z, X4.w};
+    for (int p = 0; p < NXR; ++p) {
+      const uint32_t X[4] = {fx[p].x, fx[p].y, fx[p].z, fx[p].w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          xl[p][e] = X[e] & 0x0000FFFFu;
-          xh[p][e] = X[e] & 0xFFFF0000u;
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < UW; ++u) {
-        const int p = u % NXR;
-        const uint4 Y4 = *reinterpret_cast<const uint4*>(&kT[buf][yrow[u]][col]);
-        const uint32_t Y[4] = {Y4.x, Y4.y, Y4.z, Y4.w};
-        float pr[8];
-        dot2x8(Y, xl[p], xh[p], pr);
-        const bf16x8 Bf = __builtin_bit_cast(
-            bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                               pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
-#pragma unroll
-        for (int m = 0; m < G::MT; ++m) acc[u][m] = mfma32(va[m], Bf, acc[u][m]);
+      for (int e = 0; e < 4; ++e) {
+        xf[p][2 * e] = __uint_as_float(X[e] << 16);
+        xf[p][2 * e + 1] = __uint_as_float(X[e] & 0xFFFF0000u);
       }
     }
-    if (bi + 1 < nblk) commit(buf ^ 1);
+  };
+  // the first tile's features of a staged block (nothing to overlap with)
+  auto features = [&](const uint4& yv, const float x8[8]) __attribute__((always_inline)) {
+    const uint32_t Y[4] = {yv.x, yv.y, yv.z, yv.w};
+    float pr[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pr[2 * e] = __uint_as_float(Y[e] << 16) * x8[2 * e];
+      pr[2 * e + 1] = __uint_as_float(Y[e] & 0xFFFF0000u) * x8[2 * e + 1];
+    }
+    return __builtin_bit_cast(
+        bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                           pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+  };
+  auto pack8 = [](const float pr[8]) __attribute__((always_inline)) {
+    return __builtin_bit_cast(
+        bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                           pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+  };
+  // Per staged block: publish block bi+1 and fetch block bi+2 piece by piece;
+  // the features of tile u+1 are computed under the MFMAs of tile u (the
+  // block's first tile beforehand).
+  for (int bi = 0; bi < nblk; ++bi) {
+    const int buf = bi % kNBuf2;
+    const int nbuf = (bi + 1) % kNBuf2;
+    const char* kb = kbase + buf * KBUF;
+    const char* vb = vbase + buf * VBUF;
+    const bool more1 = bi + 1 < nblk;
+    const long long t1 = span0 + static_cast<long long>(bi + 1) * kTB2;
+    const long long t2 = t1 + kTB2;
+    ldv(0, vb, 0u);
+    ldx(kb, 0u);
+#pragma unroll
+    for (int u = 0; u < UW; ++u) fy[u] = *reinterpret_cast<const uint4*>(kb + yo[u]);
+    widen_x();
+    bf16x8 bf = features(fy[0], xf[0]);
+    static_for<0, KS>([&](auto ks_c) {
+      constexpr int ks = decltype(ks_c)::value;
+      constexpr int cur = ks & 1;
+      constexpr unsigned kn = 32u * (ks + 1);  // byte column of K-step ks+1
+      static_for<0, TPT>([&](auto j_c) {  // staging piece j at K-step j*KS/TPT
+        constexpr int j = decltype(j_c)::value;
+        if constexpr (j * KS / TPT == ks) {
+          using J = std::integral_constant<int, j>;
+          using J1 = std::integral_constant<int, j + 1>;
+          if (more1) commit(nbuf, t1, J{}, J1{});
+          fetch(t2, J{}, J1{});
+        }
+      });
+      if constexpr (ks + 1 < KS) {
+        ldv(cur ^ 1, vb, kn);
+        ldx(kb, kn);
+      }
+      const bf16x8 va0 = __builtin_bit_cast(bf16x8, fv[cur][0]);
+      const bf16x8 va1 = __builtin_bit_cast(bf16x8, fv[cur][1]);
+      static_for<0, UW>([&](auto u_c) {
+        constexpr int u = decltype(u_c)::value;
+        // fy[u] fed the features of (ks, u): reload it for (ks+1, u)
+        if constexpr (ks + 1 < KS && u > 0)
+          fy[u] = *reinterpret_cast<const uint4*>(kb + yo[u] + kn);
+        if constexpr (u + 1 < UW) {
+          const uint32_t Y[4] = {fy[u + 1].x, fy[u + 1].y, fy[u + 1].z, fy[u + 1].w};
+          float pr[8];
+          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bf, Y, xf[(u + 1) % NXR], pr);
+          bf = pack8(pr);
+          if constexpr (ks + 1 < KS && u == 0)
+            fy[0] = *reinterpret_cast<const uint4*>(kb + yo[0] + kn);
+        } else if constexpr (ks + 1 < KS) {
+          widen_x();  // x rows of K-step ks+1
+          const uint32_t Y[4] = {fy[0].x, fy[0].y, fy[0].z, fy[0].w};
+          float pr[8];
+          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bf, Y, xf[0], pr);
+          bf = pack8(pr);
+        } else {
+          mfma2(acc[u][0], acc[u][1], va0, va1, bf);
+        }
+      });
+    });
     lds_barrier();
   }
+  mfma_drain();
 
   // write this wave's tiles of the span record (bf16)
 #pragma unroll
@@ -801,6 +967,9 @@ static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255);
 // Span length rounded up to whole intra stages so that every staged key
 // block lies inside the span's V^T record.
 static int span_alloc(int L) { return (L + kKB - 1) / kKB * kKB; }
+static_assert(kKB % kTB2 == 0, "the state kernel writes V^T in whole staged blocks");
+
+constexpr int kSpansPerLaunch = 1 << 20;
 
 size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L) {
   const size_t NS = (static_cast<size_t>(T) + L - 1) / L;
@@ -822,12 +991,16 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
-  constexpr int UW = 6;
-  const int ub = (G::NST + 4 * UW - 1) / (4 * UW);  // slot-tile blocks; one more for Z
+  const int nsp = BH * NS;
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  span_state_kernel<D, DV, UW><<<dim3(ub + 1, NS, BH), 256, 0, st>>>(kk, vv, spanst, vtp, T, L,
-                                                                     LA);
+  // K2 in launches of at most kSpansPerLaunch spans (1-D grid size limit)
+  for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
+    const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
+    const unsigned nb2 = 8u * StateGrid<D, DV>::NB * static_cast<unsigned>((cnt + 7) / 8);
+    span_state_kernel<D, DV><<<nb2, 256, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
+                                                  sp0 + cnt);
+  }
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   dim3 g3(static_cast<unsigned>((G::E + kEB16 - 1) / kEB16), BH);
   scan_exclusive_bf16<SlotWeight<D, DV>><<<g3, 256, 0, st>>>(
