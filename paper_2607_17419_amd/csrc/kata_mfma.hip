@@ -253,9 +253,9 @@ __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 
 // branch-free MFMA loop.  The Z wave computes Z = K^T K and writes the span's
 // V^T (bf16, [dv][LV], keys of every 16-key group in the order 0-3, 8-11,
 // 4-7, 12-15: the K order of the output kernel's P V product).
-// K and V are staged transposed ([dim][token]) through LDS in blocks of kTB2
-// tokens, double buffered; a slot wave loads the LDS fragments of K-step
-// ks+1 before it computes K-step ks.
+// K and V are staged transposed ([dim][token]) through a three-buffer LDS
+// ring in blocks of kTB2 tokens; a slot wave loads the LDS fragments of
+// K-step ks+1 before it computes K-step ks.
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
 // ---------------------------------------------------------------------------
 constexpr int kTB2 = 128;           // tokens per staged block
@@ -591,18 +591,21 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// K4: span output.  grid (query blocks per span, NS, BH), block 256 (4 waves),
-// one workgroup per CU (96 KB of LDS in three 32 KB stage buffers).
+// K4: span output.  1-D grid of workgroups of 256 threads (4 waves), one per
+// CU (96 KB of LDS in three 32 KB stage buffers).  A span has QB = L/256
+// query blocks; block id -> (span, query block) keeps the query blocks of a
+// span on one XCD (equal id % 8), dispatched back to back, so they share the
+// span's prefix record and keys in that XCD's L2.
 // The workgroup owns 8 query tiles of 32 (span-relative tile index 8*qb + i);
 // wave w takes tiles {w, 7-w}, which balances the causal work.
 // Operands are staged by direct global -> LDS copies, three stages deep, so no
 // registers hold staged data and the copies of stage s+2 overlap the
-// arithmetic of stage s.
+// arithmetic of stage s.  LDS fragment reads use per-lane offsets computed
+// once, so every read is a base register plus an immediate.
 // pre[bh][s][E] bf16: weighted S_pre^T as [dv][NSLOT], then Z_pre (operand order).
 // vtp[bh][s][dv][L] bf16: the span's V^T (permuted keys, see K2).
 // ---------------------------------------------------------------------------
-constexpr int kKB = 128;        // keys per intra stage
-constexpr int kUnrolledStages = 8;  // intra stages handled in straight-line code
+constexpr int kKB = 128;        // keys per intra stage (four 32-key blocks)
 constexpr int kKC = 16;         // readout K-steps per stage
 constexpr int kStageBytes = 32768;
 
@@ -610,11 +613,85 @@ __shared__ __attribute__((aligned(16))) uint16_t g_stage0[kStageBytes / 2];
 __shared__ __attribute__((aligned(16))) uint16_t g_stage1[kStageBytes / 2];
 __shared__ __attribute__((aligned(16))) uint16_t g_stage2[kStageBytes / 2];
 
+__device__ __forceinline__ uint16_t* stage_buf(int j) {
+  return j == 0 ? g_stage0 : (j == 1 ? g_stage1 : g_stage2);
+}
+
+// The two MFMAs of one query tile of the prefix readout (a0 += A0 * bf,
+// a1 += A1 * bf) with the eight products of the next tile's query features
+// (p_j = x_j * y_j, fp32 registers) issued under them.  Same wait-state and
+// accumulator rules as mfma2_mul8.
+__device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8& A0,
+                                            const bf16x8& A1, const bf16x8& bf,
+                                            const float x[8], const float y[8], float p[8]) {
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %10, %12, %0\n\t"
+      "v_mul_f32 %2, %13, %21\n\t"
+      "v_mul_f32 %3, %14, %22\n\t"
+      "v_mul_f32 %4, %15, %23\n\t"
+      "v_mul_f32 %5, %16, %24\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1\n\t"
+      "v_mul_f32 %6, %17, %25\n\t"
+      "v_mul_f32 %7, %18, %26\n\t"
+      "v_mul_f32 %8, %19, %27\n\t"
+      "v_mul_f32 %9, %20, %28"
+      : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
+        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7])
+      : "v"(A0), "v"(A1), "v"(bf), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]),
+        "v"(x[5]), "v"(x[6]), "v"(x[7]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(y[4]),
+        "v"(y[5]), "v"(y[6]), "v"(y[7]));
+}
+
+// Scores of two query tiles against one 32-key block: sc_i = K_blk Q_i^T
+// over the d-contraction, the two accumulation chains interleaved, results in
+// VGPRs for the VALU that squares them.  The first MFMA of a chain takes a
+// zero accumulator.  s_nop 4 at the end: with the chains interleaved the last
+// write of sc0 is an MFMA and a full MFMA old when the block ends, sc1's last
+// write is covered by the first VALU instructions, which read sc0.
+template <int KZ>
+__device__ __forceinline__ void score2(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[KZ],
+                                       const bf16x8 (&q0)[KZ], const bf16x8 (&q1)[KZ]);
+template <>
+__device__ __forceinline__ void score2<4>(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[4],
+                                          const bf16x8 (&q0)[4], const bf16x8 (&q1)[4]) {
+  asm volatile(
+      "v_mfma_f32_32x32x16_bf16 %0, %2, %6, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %2, %10, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %3, %7, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %3, %11, %1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %4, %8, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %4, %12, %1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %5, %9, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %5, %13, %1\n\t"
+      "s_nop 4"
+      : "=&v"(sc0), "=&v"(sc1)
+      : "v"(A[0]), "v"(A[1]), "v"(A[2]), "v"(A[3]), "v"(q0[0]), "v"(q0[1]), "v"(q0[2]),
+        "v"(q0[3]), "v"(q1[0]), "v"(q1[1]), "v"(q1[2]), "v"(q1[3]));
+}
+template <>
+__device__ __forceinline__ void score2<2>(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[2],
+                                          const bf16x8 (&q0)[2], const bf16x8 (&q1)[2]) {
+  asm volatile(
+      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %2, %6, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %3, %5, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %3, %7, %1\n\t"
+      "s_nop 4"
+      : "=&v"(sc0), "=&v"(sc1)
+      : "v"(A[0]), "v"(A[1]), "v"(q0[0]), "v"(q0[1]), "v"(q1[0]), "v"(q1[1]));
+}
+
+template <int D, int DV>
+struct OutGrid {
+  static constexpr int QB_TOKENS = 256;  // queries per workgroup
+};
+
 template <int D, int DV>
 __global__ __launch_bounds__(256) void span_output_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
-    int T, int L, int LV) {
+    int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
   using G = Geo<D, DV>;
   constexpr int R = G::R;
   constexpr int NQ = 2, W = 4, NT = 8;
@@ -623,27 +700,35 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   constexpr int VCH = kKB / 8;                  // chunks per V^T row of one stage (16)
   constexpr int VCHUNKS = DV * VCH;
   constexpr int ICH = KCHUNKS + VCHUNKS;        // chunks per intra stage
-  static_assert(ICH * 16 <= kStageBytes && ICH % 256 == 0, "intra stage size");
-  constexpr int IPW_I = ICH / 256;              // copy instructions per wave, intra
+  static_assert(ICH * 16 <= kStageBytes && KCHUNKS % 256 == 0 && VCHUNKS % 256 == 0,
+                "intra stage size");
+  constexpr int IPW_K = KCHUNKS / 256;          // copy instructions per wave: K rows
+  constexpr int IPW_I = ICH / 256;              // ... K rows then V^T rows
   constexpr int SCH = 2 * kKC;                  // chunks per S_pre row of one stage (32)
   constexpr int SCHUNKS = DV * SCH;
   static_assert(SCHUNKS * 16 <= kStageBytes && SCHUNKS % 256 == 0, "readout stage size");
   constexpr int IPW_R = SCHUNKS / 256;
   constexpr int NSTAGE_R = (G::NKS + kKC - 1) / kKC;
+  static_assert(G::MT == 2, "two dv tiles");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 31, g = lane >> 5;
-  const int qb = blockIdx.x, s = blockIdx.y, bh = blockIdx.z;
+  const int id = blockIdx.x;
+  const int jx = id >> 3;
+  const int qb = jx % QB;
+  const int sp = sp0 + 8 * (jx / QB) + (id & 7);
+  if (sp >= nsp) return;  // whole workgroup: padding of the grid
+  const int s = sp % NS, bh = sp / NS;
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
   const long long wg_q0 = span0 + static_cast<long long>(qb) * NT * 32;
   if (wg_q0 >= span_end) return;  // whole workgroup beyond the sequence
   const uint16_t* qh = q + static_cast<long long>(bh) * T * D;
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
-  const uint16_t* rec = pre + (static_cast<long long>(bh) * gridDim.y + s) * G::E;
-  const uint16_t* vt_rec = vtp + (static_cast<long long>(bh) * gridDim.y + s) * DV * LV;
+  const uint16_t* rec = pre + static_cast<long long>(sp) * G::E;
+  const uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
 
   int tile[NQ];
   long long tq0[NQ];
@@ -661,13 +746,10 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   bf16x8 qf[NQ][G::KZ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
-    const long long t = tq0[i] + c;
+    const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
 #pragma unroll
-    for (int kz = 0; kz < G::KZ; ++kz) {
-      uint4 w = make_uint4(0u, 0u, 0u, 0u);
-      if (t < span_end) w = *reinterpret_cast<const uint4*>(qh + t * D + 8 * kz + R * g);
-      qf[i][kz] = __builtin_bit_cast(bf16x8, w);
-    }
+    for (int kz = 0; kz < G::KZ; ++kz)
+      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + 8 * kz + R * g);
   }
 
   f32x16 acc[G::MT][NQ];
@@ -717,138 +799,154 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 
   // ---- causal squared-score attention inside the span -----------------------
   {
+    // key blocks of each tile: 0 .. nb-1, the last one on the diagonal
+    // Stages cover the key blocks of the workgroup's last live tile; every
+    // wave runs all of them (the stage barriers are workgroup-wide).
     int last_tile = qb * NT + NT - 1;
     const int last_key_tile = static_cast<int>((span_end - 1 - span0) / 32);
     if (last_tile > last_key_tile) last_tile = last_key_tile;
     const int nstage = (last_tile + 1 + 3) / 4;  // 128-key stages
-    // issue the copies of intra stage st into buffer `buf`
+    // copy i of this lane: K row / V^T row and the chunk it fetches
+    long long ksrc[IPW_K];  // element offset of the K chunk inside the head, stage 0
+    int krw[IPW_K];
+    int vsrc[IPW_I - IPW_K];
+#pragma unroll
+    for (int i = 0; i < IPW_I; ++i) {
+      const int P = (i * W + wave) * 64 + lane;  // LDS chunk written by this lane
+      if (i < IPW_K) {
+        const int r = P / KCH, pos = P % KCH;
+        krw[i] = r;
+        ksrc[i] = static_cast<long long>(r) * D + 8 * (pos ^ kswz<D>(r));
+      } else {
+        const int P2 = P - KCHUNKS;
+        const int m = P2 / VCH, pos = P2 % VCH;
+        vsrc[i - IPW_K] = m * LV + 8 * (pos ^ rswz(m));
+      }
+    }
     auto issue = [&](int st, uint16_t* buf) __attribute__((always_inline)) {
       const long long key0 = span0 + static_cast<long long>(st) * kKB;
 #pragma unroll
       for (int i = 0; i < IPW_I; ++i) {
-        const int P = (i * W + wave) * 64 + lane;  // LDS chunk written by this lane
         const void* src;
-        if (P < KCHUNKS) {
-          const int r = P / KCH, pos = P % KCH;
-          const int cl = pos ^ kswz<D>(r);
-          long long key = key0 + r;
-          if (key > T - 1) key = T - 1;  // in bounds; such keys are never used
-          src = kh + key * D + 8 * cl;
+        if (i < IPW_K) {
+          // keys past the sequence: re-read the last row (never used)
+          const long long over = key0 + krw[i] - (T - 1);
+          src = kh + key0 * D + ksrc[i] - (over > 0 ? over * D : 0);
         } else {
-          const int P2 = P - KCHUNKS;
-          const int m = P2 / VCH, pos = P2 % VCH;
-          const int cl = pos ^ rswz(m);
-          src = vt_rec + static_cast<long long>(m) * LV + st * kKB + 8 * cl;
+          src = vt_rec + st * kKB + vsrc[i - IPW_K];
         }
         g2lds16(src, buf + (i * W + wave) * 512);
       }
     };
-    auto compute = [&](int st, const uint16_t* Ks) __attribute__((always_inline)) {
-      const uint16_t* Vs = Ks + KCHUNKS * 8;
+    // fragment byte offsets inside a stage buffer
+    //  K rows 32*sb + c, chunk (kz + (R/8)*g) ^ kswz: depends on sb only through sb & 1
+    unsigned kfo[2][G::KZ];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int kz = 0; kz < G::KZ; ++kz) {
+        const int krow = 32 * h + c;
+        kfo[h][kz] = static_cast<unsigned>((krow * KCH + ((kz + (R / 8) * g) ^ kswz<D>(krow))) * 16);
+      }
+    //  V^T rows 32*m + c, chunk (4*sb + 2*kv + g) ^ (c & 15); the row part of m is immediate
+    unsigned vfo[4][2];
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+      for (int kv = 0; kv < 2; ++kv)
+        vfo[sb][kv] = static_cast<unsigned>(
+            (KCHUNKS + c * VCH + ((4 * sb + 2 * kv + g) ^ rswz(c))) * 16);
+
+    // Tiles that are finished (past their diagonal block) or beyond the
+    // sequence keep running through the same MFMAs with zeroed query
+    // fragments, so they add nothing and no branch surrounds an accumulator.
+    bf16x8 qz[NQ][G::KZ];
+#pragma unroll
+    for (int i = 0; i < NQ; ++i)
+#pragma unroll
+      for (int kz = 0; kz < G::KZ; ++kz)
+        qz[i][kz] = tlive[i] ? qf[i][kz] : __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+    auto ldfrag = [&](const char* Ks, int sb, bf16x8 (&A)[G::KZ], bf16x8 (&va)[G::MT][2])
+                      __attribute__((always_inline)) {
+      const unsigned krow0 = static_cast<unsigned>(sb >> 1) * (64u * KCH * 16u);
+#pragma unroll
+      for (int kz = 0; kz < G::KZ; ++kz)
+        A[kz] = *reinterpret_cast<const bf16x8*>(Ks + krow0 + kfo[sb & 1][kz]);
+#pragma unroll
+      for (int m = 0; m < G::MT; ++m)
+#pragma unroll
+        for (int kv = 0; kv < 2; ++kv)
+          va[m][kv] = *reinterpret_cast<const bf16x8*>(Ks + vfo[sb][kv] + m * (32 * VCH * 16));
+    };
+    // squared scores of one tile: p = sc^2, masked above the diagonal when the
+    // block is the tile's diagonal block; returns the two P fragments
+    auto probs = [&](const f32x16& sc, bool diag, float& dacc, bf16x8 (&Bp)[2])
+                     __attribute__((always_inline)) {
+      float p[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[r] = sc[r] * sc[r];
+      if (diag) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 8 * (r >> 2) + 4 * g + (r & 3);
+          p[r] = (key > c) ? 0.f : p[r];
+        }
+      }
+      float dsum = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dsum += p[r];
+      dacc += dsum;
+      asm volatile("" : "+v"(dacc));  // sum here, not at the end of the stage
+#pragma unroll
+      for (int kv = 0; kv < 2; ++kv)
+        Bp[kv] = __builtin_bit_cast(
+            bf16x8, make_uint4(pack_bf16x2(p[8 * kv + 0], p[8 * kv + 1]),
+                               pack_bf16x2(p[8 * kv + 2], p[8 * kv + 3]),
+                               pack_bf16x2(p[8 * kv + 4], p[8 * kv + 5]),
+                               pack_bf16x2(p[8 * kv + 6], p[8 * kv + 7])));
+    };
+    auto compute = [&](int st, const uint16_t* buf) __attribute__((always_inline)) {
+      const char* Ks = reinterpret_cast<const char*>(buf);
+      bf16x8 A[2][G::KZ], va[2][G::MT][2];
+      ldfrag(Ks, 0, A[0], va[0]);
 #pragma unroll
       for (int sb = 0; sb < kKB / 32; ++sb) {
         const int kb = 4 * st + sb;  // 32-key block inside the span
-        bool need[NQ];
-        bool any = false;
-#pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-          need[i] = tlive[i] && kb <= tile[i];
-          any = any || need[i];
-        }
-        if (!any) continue;
-        // S^T = K_blk Q^T : rows = keys, columns = queries
-        f32x16 sc[NQ];
+        const int cur = sb & 1;
+        if (sb + 1 < kKB / 32) ldfrag(Ks, sb + 1, A[cur ^ 1], va[cur ^ 1]);
+        f32x16 sc0, sc1;
+        score2<G::KZ>(sc0, sc1, A[cur], qz[0], qz[1]);
+        bf16x8 B0[2], B1[2];
+        probs(sc0, kb == tile[0], dpart[0], B0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma2(acc[0][0], acc[1][0], va[cur][0][0], va[cur][1][0], B0[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        probs(sc1, kb == tile[1], dpart[1], B1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma2(acc[0][0], acc[1][0], va[cur][0][1], va[cur][1][1], B0[1]);
+        mfma2(acc[0][1], acc[1][1], va[cur][0][0], va[cur][1][0], B1[0]);
+        mfma2(acc[0][1], acc[1][1], va[cur][0][1], va[cur][1][1], B1[1]);
+        // a tile is finished after its diagonal block
 #pragma unroll
         for (int i = 0; i < NQ; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sc[i][r] = 0.f;
-        const int krow = 32 * sb + c;
-#pragma unroll
-        for (int kz = 0; kz < G::KZ; ++kz) {
-          const int cl = kz + (R / 8) * g;
-          const bf16x8 A = *reinterpret_cast<const bf16x8*>(
-              Ks + (krow * KCH + (cl ^ kswz<D>(krow))) * 8);
-#pragma unroll
-          for (int i = 0; i < NQ; ++i)
-            if (need[i]) sc[i] = mfma32(A, qf[i][kz], sc[i]);
-        }
-        // V^T fragments (keys already in the P V K order)
-        bf16x8 va[G::MT][2];
-#pragma unroll
-        for (int m = 0; m < G::MT; ++m)
-#pragma unroll
-          for (int kv = 0; kv < 2; ++kv) {
-            const int vrow = 32 * m + c;
-            const int cl = 4 * sb + 2 * kv + g;
-            va[m][kv] = *reinterpret_cast<const bf16x8*>(Vs + (vrow * VCH + (cl ^ rswz(vrow))) * 8);
-          }
-#pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-          if (!need[i]) continue;
-          float p[16];
-          float dsum = 0.f;
           if (kb == tile[i]) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int key = 8 * (r >> 2) + 4 * g + (r & 3);
-              const float x = sc[i][r] * sc[i][r];
-              p[r] = (key > c) ? 0.f : x;
-              dsum += p[r];
-            }
-          } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              p[r] = sc[i][r] * sc[i][r];
-              dsum += p[r];
-            }
+            for (int kz = 0; kz < G::KZ; ++kz)
+              qz[i][kz] = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
           }
-          dpart[i] += dsum;
-#pragma unroll
-          for (int kv = 0; kv < 2; ++kv) {
-            uint4 w;
-            w.x = pack_bf16x2(p[8 * kv + 0], p[8 * kv + 1]);
-            w.y = pack_bf16x2(p[8 * kv + 2], p[8 * kv + 3]);
-            w.z = pack_bf16x2(p[8 * kv + 4], p[8 * kv + 5]);
-            w.w = pack_bf16x2(p[8 * kv + 6], p[8 * kv + 7]);
-            const bf16x8 Bp = __builtin_bit_cast(bf16x8, w);
-#pragma unroll
-            for (int m = 0; m < G::MT; ++m) acc[m][i] = mfma32(va[m][kv], Bp, acc[m][i]);
-          }
-        }
       }
     };
-    // three-deep pipeline over the stages; buffers chosen statically
+    // three-deep pipeline over the stages
     wait_vmcnt<0>();  // no compiler-issued loads underneath the copies
     issue(0, g_stage0);
     if (nstage > 1) issue(1, g_stage1);
-    if (nstage <= kUnrolledStages) {
-      // straight-line form (spans up to 1024 keys): the compiler can tell the
-      // three buffers apart and inserts no extra waits on in-flight copies
-      static_for<0, kUnrolledStages>([&](auto st_c) {
-        constexpr int j = decltype(st_c)::value;
-        if (j < nstage) {
-          if (j + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
-          lds_barrier();
-          if (j + 2 < nstage)
-            issue(j + 2, (j + 2) % 3 == 0 ? g_stage0 : ((j + 2) % 3 == 1 ? g_stage1 : g_stage2));
-          compute(j, j % 3 == 0 ? g_stage0 : (j % 3 == 1 ? g_stage1 : g_stage2));
-        }
-      });
-    } else {
-      for (int st = 0; st < nstage; st += 3) {
-#pragma unroll
-        for (int j = 0; j < 3; ++j) {
-          const int cur = st + j;
-          if (cur < nstage) {
-            if (cur + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
-            lds_barrier();
-            if (cur + 2 < nstage)
-              issue(cur + 2, j == 0 ? g_stage2 : (j == 1 ? g_stage0 : g_stage1));
-            compute(cur, j == 0 ? g_stage0 : (j == 1 ? g_stage1 : g_stage2));
-          }
-        }
-      }
+    for (int st = 0; st < nstage; ++st) {
+      if (st + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
+      lds_barrier();
+      if (st + 2 < nstage) issue(st + 2, stage_buf((st + 2) % 3));
+      compute(st, stage_buf(st % 3));
     }
+    mfma_drain();   // the P V accumulators are moved by compiler code next
     lds_barrier();  // every wave is done with the intra buffers
   }
 
@@ -858,12 +956,10 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     float qr[NQ][D];
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
-      const long long t = tq0[i] + c;
+      const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
 #pragma unroll
       for (int ch = 0; ch < D / 8; ++ch) {
-        uint4 w4 = make_uint4(0u, 0u, 0u, 0u);
-        if (t < span_end)
-          w4 = *reinterpret_cast<const uint4*>(qh + t * D + ((8 * ch + R * g) % D));
+        const uint4 w4 = *reinterpret_cast<const uint4*>(qh + t * D + ((8 * ch + R * g) % D));
         const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -872,62 +968,102 @@ __global__ __launch_bounds__(256) void span_output_kernel(
         }
       }
     }
-    // stage stg holds slots [16*kKC*stg, +16*kKC) of every dv row
-    auto issue = [&](int stg, uint16_t* buf) __attribute__((always_inline)) {
-      const int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
+    // copy i of this lane: S_pre row m, chunk cl of the stage's 32
+    int rsrc[IPW_R], rcl[IPW_R];
+#pragma unroll
+    for (int i = 0; i < IPW_R; ++i) {
+      const int P = (i * W + wave) * 64 + lane;
+      const int m = P / SCH, pos = P % SCH;
+      rcl[i] = pos ^ rswz(m);
+      rsrc[i] = m * G::NSLOT + 8 * rcl[i];
+    }
+    auto issue = [&](auto stg_c, uint16_t* buf) __attribute__((always_inline)) {
+      constexpr int stg = decltype(stg_c)::value;
+      constexpr int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
 #pragma unroll
       for (int i = 0; i < IPW_R; ++i) {
-        const int P = (i * W + wave) * 64 + lane;
-        const int m = P / SCH, pos = P % SCH;
-        int cl = pos ^ rswz(m);
-        if (cl >= 2 * kc) cl = 0;  // past the last K-step: any in-record chunk, never read
-        const void* src = rec + static_cast<long long>(m) * G::NSLOT + 16 * kKC * stg + 8 * cl;
-        g2lds16(src, buf + (i * W + wave) * 512);
+        // chunks past the last K-step: re-read the row's first chunk (never used)
+        const int off = (kc < kKC && rcl[i] >= 2 * kc) ? rsrc[i] - 8 * rcl[i] : rsrc[i];
+        g2lds16(rec + 16 * kKC * stg + off, buf + (i * W + wave) * 512);
       }
     };
-    auto compute = [&](auto stg_c, const uint16_t* Sb) __attribute__((always_inline)) {
+    // A fragment offsets: rows 32*m + c, chunk (2*kk + g) ^ (c & 15); the kk & 8
+    // and m parts are immediates
+    unsigned afo[8];
+#pragma unroll
+    for (int k7 = 0; k7 < 8; ++k7)
+      afo[k7] = static_cast<unsigned>((c * SCH + ((2 * k7 + g) ^ rswz(c))) * 16);
+    auto pack8 = [](const float pr[8]) __attribute__((always_inline)) {
+      return __builtin_bit_cast(
+          bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                             pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+    };
+    // query feature products of tile i at global K-step kap: slots 16*kap + 8*g + j
+    // pair registers (r1 + j, r1 + j + delta) of the rotated row
+    auto fx = [&](int i, int kap, float x[8], float y[8]) __attribute__((always_inline)) {
+      const int r1 = (8 * kap) % R, dl = (8 * kap) / R;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        x[j] = qr[i][r1 + j];
+        y[j] = qr[i][(r1 + j + dl) % D];
+      }
+    };
+    wait_vmcnt<0>();  // the query rows are loaded; no compiler loads in flight
+    issue(std::integral_constant<int, 0>{}, g_stage0);
+    if constexpr (NSTAGE_R > 1) issue(std::integral_constant<int, 1>{}, g_stage1);
+    // the first item's features
+    bf16x8 bf;
+    {
+      float x[8], y[8];
+      fx(0, 0, x, y);
+      float pr[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pr[j] = x[j] * y[j];
+      bf = pack8(pr);
+    }
+    static_for<0, NSTAGE_R>([&](auto stg_c) {
       constexpr int stg = decltype(stg_c)::value;
       constexpr int k0 = stg * kKC;
       constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
-      static_for<0, kc>([&](auto kk_c) {
-        constexpr int kk = decltype(kk_c)::value;
-        constexpr int kap = k0 + kk;
-        constexpr int r1 = (8 * kap) % R;
-        constexpr int dl = (8 * kap) / R;
-        bf16x8 A[G::MT];
-#pragma unroll
-        for (int m = 0; m < G::MT; ++m) {
-          const int row = 32 * m + c;
-          const int cl = 2 * kk + g;
-          A[m] = *reinterpret_cast<const bf16x8*>(Sb + (row * SCH + (cl ^ rswz(row))) * 8);
-        }
-#pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-          uint32_t wv[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float p0 = qr[i][r1 + 2 * e] * qr[i][r1 + 2 * e + dl];
-            const float p1 = qr[i][r1 + 2 * e + 1] * qr[i][r1 + 2 * e + 1 + dl];
-            wv[e] = pack_bf16x2(p0, p1);
-          }
-          const bf16x8 B = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
-#pragma unroll
-          for (int m = 0; m < G::MT; ++m) acc[m][i] = mfma32(A[m], B, acc[m][i]);
-        }
-      });
-    };
-    wait_vmcnt<0>();  // the query rows are loaded; no compiler loads in flight
-    issue(0, g_stage0);
-    if constexpr (NSTAGE_R > 1) issue(1, g_stage1);
-    static_for<0, NSTAGE_R>([&](auto stg_c) {
-      constexpr int stg = decltype(stg_c)::value;
       if constexpr (stg + 1 < NSTAGE_R) wait_vmcnt<IPW_R>(); else wait_vmcnt<0>();
       lds_barrier();
       if constexpr (stg + 2 < NSTAGE_R)
-        issue(stg + 2, (stg + 2) % 3 == 0 ? g_stage0 : ((stg + 2) % 3 == 1 ? g_stage1 : g_stage2));
-      compute(stg_c, stg % 3 == 0 ? g_stage0 : (stg % 3 == 1 ? g_stage1 : g_stage2));
+        issue(std::integral_constant<int, stg + 2>{}, stage_buf((stg + 2) % 3));
+      const char* Sb = reinterpret_cast<const char*>(stage_buf(stg % 3));
+      auto lda = [&](int kk, bf16x8 A[2]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+          A[m] = *reinterpret_cast<const bf16x8*>(Sb + afo[kk & 7] + (kk >> 3) * 256 +
+                                                  m * (32 * SCH * 16));
+      };
+      bf16x8 Acur[2], Anxt[2];
+      lda(0, Acur);
+      static_for<0, kc>([&](auto kk_c) {
+        constexpr int kk = decltype(kk_c)::value;
+        constexpr int kap = k0 + kk;
+        if constexpr (kk + 1 < kc) lda(kk + 1, Anxt);
+        // item (kap, 0): MFMAs of tile 0, features of tile 1 at kap
+        {
+          float x[8], y[8], pr[8];
+          fx(1, kap, x, y);
+          mfma2_prod8(acc[0][0], acc[1][0], Acur[0], Acur[1], bf, x, y, pr);
+          bf = pack8(pr);
+        }
+        // item (kap, 1): MFMAs of tile 1, features of tile 0 at kap + 1
+        {
+          float x[8], y[8], pr[8];
+          fx(0, (kap + 1 < G::NKS) ? kap + 1 : kap, x, y);
+          mfma2_prod8(acc[0][1], acc[1][1], Acur[0], Acur[1], bf, x, y, pr);
+          bf = pack8(pr);
+        }
+        if constexpr (kk + 1 < kc) {
+          Acur[0] = Anxt[0];
+          Acur[1] = Anxt[1];
+        }
+      });
     });
   }
+  mfma_drain();
 
   // ---- normalise and store ---------------------------------------------------
 #pragma unroll
@@ -1006,9 +1142,13 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   scan_exclusive_bf16<SlotWeight<D, DV>><<<g3, 256, 0, st>>>(
       spanst, NS, G::E, static_cast<long long>(NS) * G::E, SlotWeight<D, DV>{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
-  const int qblocks = (L + 255) / 256;
-  span_output_kernel<D, DV><<<dim3(qblocks, NS, BH), 256, 0, st>>>(qq, kk, spanst, vtp, out, T,
-                                                                   L, LA);
+  const int qblocks = (L + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
+  for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
+    const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
+    const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
+    span_output_kernel<D, DV><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
+                                                   qblocks, sp0, sp0 + cnt);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
 }
