@@ -226,6 +226,19 @@ __device__ __forceinline__ void mfma2(f32x16& a0, f32x16& a1, const bf16x8& va0,
       : "v"(va0), "v"(va1), "v"(bf));
 }
 
+// Keeps the operand registers of recently issued MFMAs live up to this point,
+// so the compiler does not reuse them for new values: an instruction that
+// writes a register an MFMA in flight still reads waits for that MFMA to
+// finish.  Emits nothing.
+template <typename T>
+__device__ __forceinline__ void hold1(const T& x) {
+  asm volatile("" ::"v"(x));
+}
+template <typename... Ts>
+__device__ __forceinline__ void hold(const Ts&... xs) {
+  (hold1(xs), ...);
+}
+
 // Wait states after MFMAs issued from inline assembly, before any other
 // instruction reads their accumulators (covers the 16-pass case).
 __device__ __forceinline__ void mfma_drain() {
@@ -525,7 +538,19 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
 #pragma unroll
     for (int u = 0; u < UW; ++u) fy[u] = *reinterpret_cast<const uint4*>(kb + yo[u]);
     widen_x();
-    bf16x8 bf = features(fy[0], xf[0]);
+    // B fragments: bq[0] the next tile's, bq[1], bq[2] the two before (kept
+    // live so that a new fragment never reuses the registers of an MFMA that
+    // may still be running, see hold)
+    bf16x8 bq[3];
+    bq[0] = features(fy[0], xf[0]);
+    bq[1] = bq[0];
+    bq[2] = bq[0];
+    auto push = [&](const float pr[8]) __attribute__((always_inline)) {
+      bq[2] = bq[1];
+      bq[1] = bq[0];
+      bq[0] = pack8(pr);
+      hold(bq[1], bq[2]);
+    };
     static_for<0, KS>([&](auto ks_c) {
       constexpr int ks = decltype(ks_c)::value;
       constexpr int cur = ks & 1;
@@ -539,10 +564,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
           fetch(t2, J{}, J1{});
         }
       });
-      if constexpr (ks + 1 < KS) {
-        ldv(cur ^ 1, vb, kn);
-        ldx(kb, kn);
-      }
+      if constexpr (ks + 1 < KS) ldx(kb, kn);
       const bf16x8 va0 = __builtin_bit_cast(bf16x8, fv[cur][0]);
       const bf16x8 va1 = __builtin_bit_cast(bf16x8, fv[cur][1]);
       static_for<0, UW>([&](auto u_c) {
@@ -553,18 +575,21 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
         if constexpr (u + 1 < UW) {
           const uint32_t Y[4] = {fy[u + 1].x, fy[u + 1].y, fy[u + 1].z, fy[u + 1].w};
           float pr[8];
-          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bf, Y, xf[(u + 1) % NXR], pr);
-          bf = pack8(pr);
+          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bq[0], Y, xf[(u + 1) % NXR], pr);
+          push(pr);
           if constexpr (ks + 1 < KS && u == 0)
             fy[0] = *reinterpret_cast<const uint4*>(kb + yo[0] + kn);
+          // V^T of K-step ks+1 into the other buffer, whose last readers (the
+          // previous K-step's final tile) are two tiles old now
+          if constexpr (ks + 1 < KS && u == 1) ldv(cur ^ 1, vb, kn);
         } else if constexpr (ks + 1 < KS) {
           widen_x();  // x rows of K-step ks+1
           const uint32_t Y[4] = {fy[0].x, fy[0].y, fy[0].z, fy[0].w};
           float pr[8];
-          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bf, Y, xf[0], pr);
-          bf = pack8(pr);
+          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bq[0], Y, xf[0], pr);
+          push(pr);
         } else {
-          mfma2(acc[u][0], acc[u][1], va0, va1, bf);
+          mfma2(acc[u][0], acc[u][1], va0, va1, bq[0]);
         }
       });
     });
@@ -612,15 +637,23 @@ constexpr int kStageBytes = 32768;
 __shared__ __attribute__((aligned(16))) uint16_t g_stage0[kStageBytes / 2];
 __shared__ __attribute__((aligned(16))) uint16_t g_stage1[kStageBytes / 2];
 __shared__ __attribute__((aligned(16))) uint16_t g_stage2[kStageBytes / 2];
+__shared__ __attribute__((aligned(16))) uint16_t g_stage3[kStageBytes / 2];
+__shared__ __attribute__((aligned(16))) uint16_t g_stage4[kStageBytes / 2];
 
+// Stage buffers 0-2 serve the intra-span stages; the readout's stage s uses
+// buffer (3 + s) % 5, so its first two stages (buffers 3 and 4) can be copied
+// in at the start of the kernel while the other phases run.
 __device__ __forceinline__ uint16_t* stage_buf(int j) {
-  return j == 0 ? g_stage0 : (j == 1 ? g_stage1 : g_stage2);
+  return j == 0 ? g_stage0
+                : (j == 1 ? g_stage1 : (j == 2 ? g_stage2 : (j == 3 ? g_stage3 : g_stage4)));
 }
 
 // The two MFMAs of one query tile of the prefix readout (a0 += A0 * bf,
 // a1 += A1 * bf) with the eight products of the next tile's query features
-// (p_j = x_j * y_j, fp32 registers) issued under them.  Same wait-state and
-// accumulator rules as mfma2_mul8.
+// (p_j = x_j * y_j, fp32 registers) between them: the products take as long
+// as the first MFMA, so the second issues without waiting, and the
+// conversions that follow run under it.  Same wait-state and accumulator
+// rules as mfma2_mul8.
 __device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8& A0,
                                             const bf16x8& A1, const bf16x8& bf,
                                             const float x[8], const float y[8], float p[8]) {
@@ -631,11 +664,11 @@ __device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8
       "v_mul_f32 %3, %14, %22\n\t"
       "v_mul_f32 %4, %15, %23\n\t"
       "v_mul_f32 %5, %16, %24\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1\n\t"
       "v_mul_f32 %6, %17, %25\n\t"
       "v_mul_f32 %7, %18, %26\n\t"
       "v_mul_f32 %8, %19, %27\n\t"
-      "v_mul_f32 %9, %20, %28"
+      "v_mul_f32 %9, %20, %28\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1"
       : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
         "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7])
       : "v"(A0), "v"(A1), "v"(bf), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]),
@@ -752,6 +785,86 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + 8 * kz + R * g);
   }
 
+  // Z_pre operand fragments (see below)
+  const uint16_t* zop = rec + G::ES;
+  bf16x8 zA[G::ZM][G::KZ];
+#pragma unroll
+  for (int m = 0; m < G::ZM; ++m)
+#pragma unroll
+    for (int kz = 0; kz < G::KZ; ++kz)
+      zA[m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * G::KZ + kz) * 64 + lane) * 8);
+
+  // ---- staging copies of both phases ------------------------------------------
+  // Stages cover the key blocks of the workgroup's last live tile; every
+  // wave runs all of them (the stage barriers are workgroup-wide).
+  int last_tile = qb * NT + NT - 1;
+  const int last_key_tile = static_cast<int>((span_end - 1 - span0) / 32);
+  if (last_tile > last_key_tile) last_tile = last_key_tile;
+  const int nstage = (last_tile + 1 + 3) / 4;  // 128-key intra stages
+  // intra copy i of this lane: K row / V^T row and the chunk it fetches
+  int ksrc[IPW_K];  // element offset of the K chunk from the stage's first key row
+  int vsrc[IPW_I - IPW_K];
+#pragma unroll
+  for (int i = 0; i < IPW_I; ++i) {
+    const int P = (i * W + wave) * 64 + lane;  // LDS chunk written by this lane
+    if (i < IPW_K) {
+      const int r = P / KCH, pos = P % KCH;
+      ksrc[i] = r * D + 8 * (pos ^ kswz<D>(r));
+    } else {
+      const int P2 = P - KCHUNKS;
+      const int m = P2 / VCH, pos = P2 % VCH;
+      vsrc[i - IPW_K] = m * LV + 8 * (pos ^ rswz(m));
+    }
+  }
+  auto issue_i = [&](int st, uint16_t* buf) __attribute__((always_inline)) {
+    const long long key0 = span0 + static_cast<long long>(st) * kKB;
+#pragma unroll
+    for (int i = 0; i < IPW_I; ++i) {
+      const void* src;
+      if (i < IPW_K) {
+        // keys past the sequence: re-read the last row (never used)
+        const long long over = key0 + ksrc[i] / D - (T - 1);
+        src = kh + key0 * D + ksrc[i] - (over > 0 ? over * D : 0);
+      } else {
+        src = vt_rec + st * kKB + vsrc[i - IPW_K];
+      }
+      g2lds16(src, buf + (i * W + wave) * 512);
+    }
+  };
+  // readout copy i of this lane: S_pre row m, chunk cl of the stage's 32
+  int rsrc[IPW_R];
+#pragma unroll
+  for (int i = 0; i < IPW_R; ++i) {
+    const int P = (i * W + wave) * 64 + lane;
+    const int m = P / SCH, pos = P % SCH;
+    rsrc[i] = m * G::NSLOT + 8 * (pos ^ rswz(m));
+  }
+  auto issue_r = [&](auto stg_c) __attribute__((always_inline)) {
+    constexpr int stg = decltype(stg_c)::value;
+    constexpr int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
+    uint16_t* buf = stage_buf((3 + stg) % 5);
+#pragma unroll
+    for (int i = 0; i < IPW_R; ++i) {
+      // chunks past the last K-step: re-read the row's first chunk (never used)
+      int off = rsrc[i];
+      if constexpr (kc < kKC) {
+        const int P = (i * W + wave) * 64 + lane;
+        const int cl = (P % SCH) ^ rswz(P / SCH);
+        if (cl >= 2 * kc) off -= 8 * cl;
+      }
+      g2lds16(rec + 16 * kKC * stg + off, buf + (i * W + wave) * 512);
+    }
+  };
+  // The query and Z fragments are in registers before any copy is issued:
+  // copies are not counted by the compiler's waits, and a wait for a load
+  // issued before them must not wait for them.  From here on the only vector
+  // memory operations are copies (and the final stores).
+  wait_vmcnt<0>();
+  issue_r(std::integral_constant<int, 0>{});
+  if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+  issue_i(0, g_stage0);
+  if (nstage > 1) issue_i(1, g_stage1);
+
   f32x16 acc[G::MT][NQ];
 #pragma unroll
   for (int m = 0; m < G::MT; ++m)
@@ -770,16 +883,12 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       for (int i = 0; i < NQ; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) az[m][i][r] = 0.f;
-    const uint16_t* zop = rec + G::ES;
 #pragma unroll
     for (int m = 0; m < G::ZM; ++m)
 #pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz) {
-        const bf16x8 A =
-            *reinterpret_cast<const bf16x8*>(zop + ((m * G::KZ + kz) * 64 + lane) * 8);
+      for (int kz = 0; kz < G::KZ; ++kz)
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) az[m][i] = mfma32(A, qf[i][kz], az[m][i]);
-      }
+        for (int i = 0; i < NQ; ++i) az[m][i] = mfma32(zA[m][kz], qf[i][kz], az[m][i]);
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
       float dsum = 0.f;
@@ -799,45 +908,6 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 
   // ---- causal squared-score attention inside the span -----------------------
   {
-    // key blocks of each tile: 0 .. nb-1, the last one on the diagonal
-    // Stages cover the key blocks of the workgroup's last live tile; every
-    // wave runs all of them (the stage barriers are workgroup-wide).
-    int last_tile = qb * NT + NT - 1;
-    const int last_key_tile = static_cast<int>((span_end - 1 - span0) / 32);
-    if (last_tile > last_key_tile) last_tile = last_key_tile;
-    const int nstage = (last_tile + 1 + 3) / 4;  // 128-key stages
-    // copy i of this lane: K row / V^T row and the chunk it fetches
-    long long ksrc[IPW_K];  // element offset of the K chunk inside the head, stage 0
-    int krw[IPW_K];
-    int vsrc[IPW_I - IPW_K];
-#pragma unroll
-    for (int i = 0; i < IPW_I; ++i) {
-      const int P = (i * W + wave) * 64 + lane;  // LDS chunk written by this lane
-      if (i < IPW_K) {
-        const int r = P / KCH, pos = P % KCH;
-        krw[i] = r;
-        ksrc[i] = static_cast<long long>(r) * D + 8 * (pos ^ kswz<D>(r));
-      } else {
-        const int P2 = P - KCHUNKS;
-        const int m = P2 / VCH, pos = P2 % VCH;
-        vsrc[i - IPW_K] = m * LV + 8 * (pos ^ rswz(m));
-      }
-    }
-    auto issue = [&](int st, uint16_t* buf) __attribute__((always_inline)) {
-      const long long key0 = span0 + static_cast<long long>(st) * kKB;
-#pragma unroll
-      for (int i = 0; i < IPW_I; ++i) {
-        const void* src;
-        if (i < IPW_K) {
-          // keys past the sequence: re-read the last row (never used)
-          const long long over = key0 + krw[i] - (T - 1);
-          src = kh + key0 * D + ksrc[i] - (over > 0 ? over * D : 0);
-        } else {
-          src = vt_rec + st * kKB + vsrc[i - IPW_K];
-        }
-        g2lds16(src, buf + (i * W + wave) * 512);
-      }
-    };
     // fragment byte offsets inside a stage buffer
     //  K rows 32*sb + c, chunk (kz + (R/8)*g) ^ kswz: depends on sb only through sb & 1
     unsigned kfo[2][G::KZ];
@@ -858,14 +928,8 @@ __global__ __launch_bounds__(256) void span_output_kernel(
             (KCHUNKS + c * VCH + ((4 * sb + 2 * kv + g) ^ rswz(c))) * 16);
 
     // Tiles that are finished (past their diagonal block) or beyond the
-    // sequence keep running through the same MFMAs with zeroed query
-    // fragments, so they add nothing and no branch surrounds an accumulator.
-    bf16x8 qz[NQ][G::KZ];
-#pragma unroll
-    for (int i = 0; i < NQ; ++i)
-#pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz)
-        qz[i][kz] = tlive[i] ? qf[i][kz] : __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+    // sequence keep running through the same MFMAs, with zero P fragments
+    // (their VALU work is skipped), so no branch surrounds an accumulator.
     auto ldfrag = [&](const char* Ks, int sb, bf16x8 (&A)[G::KZ], bf16x8 (&va)[G::MT][2])
                       __attribute__((always_inline)) {
       const unsigned krow0 = static_cast<unsigned>(sb >> 1) * (64u * KCH * 16u);
@@ -878,10 +942,16 @@ __global__ __launch_bounds__(256) void span_output_kernel(
         for (int kv = 0; kv < 2; ++kv)
           va[m][kv] = *reinterpret_cast<const bf16x8*>(Ks + vfo[sb][kv] + m * (32 * VCH * 16));
     };
-    // squared scores of one tile: p = sc^2, masked above the diagonal when the
-    // block is the tile's diagonal block; returns the two P fragments
-    auto probs = [&](const f32x16& sc, bool diag, float& dacc, bf16x8 (&Bp)[2])
+    // squared scores of one tile: p = sc^2, masked above the diagonal on the
+    // tile's diagonal block; zero for a finished or dead tile (its MFMAs run
+    // anyway, no branch surrounds an accumulator); returns the two P fragments
+    auto probs = [&](const f32x16& sc, bool diag, bool done, float& dacc, bf16x8 (&Bp)[2])
                      __attribute__((always_inline)) {
+      if (done) {
+        Bp[0] = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+        Bp[1] = Bp[0];
+        return;
+      }
       float p[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) p[r] = sc[r] * sc[r];
@@ -913,37 +983,29 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       for (int sb = 0; sb < kKB / 32; ++sb) {
         const int kb = 4 * st + sb;  // 32-key block inside the span
         const int cur = sb & 1;
-        if (sb + 1 < kKB / 32) ldfrag(Ks, sb + 1, A[cur ^ 1], va[cur ^ 1]);
         f32x16 sc0, sc1;
-        score2<G::KZ>(sc0, sc1, A[cur], qz[0], qz[1]);
+        score2<G::KZ>(sc0, sc1, A[cur], qf[0], qf[1]);
+        // the next block's fragments: the P V MFMAs of the previous block,
+        // which read va[cur ^ 1], are eight MFMAs old by now
+        if (sb + 1 < kKB / 32) ldfrag(Ks, sb + 1, A[cur ^ 1], va[cur ^ 1]);
         bf16x8 B0[2], B1[2];
-        probs(sc0, kb == tile[0], dpart[0], B0);
+        probs(sc0, kb == tile[0], !tlive[0] || kb > tile[0], dpart[0], B0);
         __builtin_amdgcn_sched_barrier(0);
         mfma2(acc[0][0], acc[1][0], va[cur][0][0], va[cur][1][0], B0[0]);
         __builtin_amdgcn_sched_barrier(0);
-        probs(sc1, kb == tile[1], dpart[1], B1);
+        probs(sc1, kb == tile[1], !tlive[1] || kb > tile[1], dpart[1], B1);
         __builtin_amdgcn_sched_barrier(0);
         mfma2(acc[0][0], acc[1][0], va[cur][0][1], va[cur][1][1], B0[1]);
         mfma2(acc[0][1], acc[1][1], va[cur][0][0], va[cur][1][0], B1[0]);
         mfma2(acc[0][1], acc[1][1], va[cur][0][1], va[cur][1][1], B1[1]);
-        // a tile is finished after its diagonal block
-#pragma unroll
-        for (int i = 0; i < NQ; ++i)
-          if (kb == tile[i]) {
-#pragma unroll
-            for (int kz = 0; kz < G::KZ; ++kz)
-              qz[i][kz] = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
-          }
       }
     };
-    // three-deep pipeline over the stages
-    wait_vmcnt<0>();  // no compiler-issued loads underneath the copies
-    issue(0, g_stage0);
-    if (nstage > 1) issue(1, g_stage1);
+    // three-deep pipeline over the stages (0 and 1 were issued at the start,
+    // after the readout's first two stages)
     for (int st = 0; st < nstage; ++st) {
       if (st + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
       lds_barrier();
-      if (st + 2 < nstage) issue(st + 2, stage_buf((st + 2) % 3));
+      if (st + 2 < nstage) issue_i(st + 2, stage_buf((st + 2) % 3));
       compute(st, stage_buf(st % 3));
     }
     mfma_drain();   // the P V accumulators are moved by compiler code next
@@ -952,41 +1014,24 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 
   // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
   {
-    // rotated fp32 query rows: qr[i][x] = q[t][(x + R*g) % D]
+    // rotated fp32 query rows: qr[i][x] = q[t][(x + R*g) % D]; the lane's
+    // own bf16 fragments hold x < R, the lane 32 away holds the rest
     float qr[NQ][D];
 #pragma unroll
-    for (int i = 0; i < NQ; ++i) {
-      const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
+    for (int i = 0; i < NQ; ++i)
 #pragma unroll
-      for (int ch = 0; ch < D / 8; ++ch) {
-        const uint4 w4 = *reinterpret_cast<const uint4*>(qh + t * D + ((8 * ch + R * g) % D));
+      for (int kz = 0; kz < G::KZ; ++kz) {
+        const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
         const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          qr[i][8 * ch + 2 * e] = bf16lo_f32(w[e]);
-          qr[i][8 * ch + 2 * e + 1] = bf16hi_f32(w[e]);
+          const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
+          qr[i][8 * kz + 2 * e] = bf16lo_f32(w[e]);
+          qr[i][8 * kz + 2 * e + 1] = bf16hi_f32(w[e]);
+          qr[i][R + 8 * kz + 2 * e] = bf16lo_f32(pw);
+          qr[i][R + 8 * kz + 2 * e + 1] = bf16hi_f32(pw);
         }
       }
-    }
-    // copy i of this lane: S_pre row m, chunk cl of the stage's 32
-    int rsrc[IPW_R], rcl[IPW_R];
-#pragma unroll
-    for (int i = 0; i < IPW_R; ++i) {
-      const int P = (i * W + wave) * 64 + lane;
-      const int m = P / SCH, pos = P % SCH;
-      rcl[i] = pos ^ rswz(m);
-      rsrc[i] = m * G::NSLOT + 8 * rcl[i];
-    }
-    auto issue = [&](auto stg_c, uint16_t* buf) __attribute__((always_inline)) {
-      constexpr int stg = decltype(stg_c)::value;
-      constexpr int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
-#pragma unroll
-      for (int i = 0; i < IPW_R; ++i) {
-        // chunks past the last K-step: re-read the row's first chunk (never used)
-        const int off = (kc < kKC && rcl[i] >= 2 * kc) ? rsrc[i] - 8 * rcl[i] : rsrc[i];
-        g2lds16(rec + 16 * kKC * stg + off, buf + (i * W + wave) * 512);
-      }
-    };
     // A fragment offsets: rows 32*m + c, chunk (2*kk + g) ^ (c & 15); the kk & 8
     // and m parts are immediates
     unsigned afo[8];
@@ -1008,57 +1053,78 @@ __global__ __launch_bounds__(256) void span_output_kernel(
         y[j] = qr[i][(r1 + j + dl) % D];
       }
     };
-    wait_vmcnt<0>();  // the query rows are loaded; no compiler loads in flight
-    issue(std::integral_constant<int, 0>{}, g_stage0);
-    if constexpr (NSTAGE_R > 1) issue(std::integral_constant<int, 1>{}, g_stage1);
-    // the first item's features
-    bf16x8 bf;
+    // B fragments: bq[0] the next item's, bq[1], bq[2] the two before (kept
+    // live, see hold); the first item's features
+    bf16x8 bq[3];
     {
       float x[8], y[8];
       fx(0, 0, x, y);
       float pr[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) pr[j] = x[j] * y[j];
-      bf = pack8(pr);
+      bq[0] = pack8(pr);
+      bq[1] = bq[0];
+      bq[2] = bq[0];
     }
     static_for<0, NSTAGE_R>([&](auto stg_c) {
       constexpr int stg = decltype(stg_c)::value;
       constexpr int k0 = stg * kKC;
       constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
-      if constexpr (stg + 1 < NSTAGE_R) wait_vmcnt<IPW_R>(); else wait_vmcnt<0>();
-      lds_barrier();
-      if constexpr (stg + 2 < NSTAGE_R)
-        issue(std::integral_constant<int, stg + 2>{}, stage_buf((stg + 2) % 3));
-      const char* Sb = reinterpret_cast<const char*>(stage_buf(stg % 3));
+      // stages 0 and 1 arrived during the earlier phases (the intra part
+      // ends with vmcnt 0 and a barrier)
+      if constexpr (stg >= 2) {
+        if constexpr (stg + 1 < NSTAGE_R) wait_vmcnt<IPW_R>(); else wait_vmcnt<0>();
+        lds_barrier();
+      }
+      if constexpr (stg + 2 < NSTAGE_R) issue_r(std::integral_constant<int, stg + 2>{});
+      const char* Sb = reinterpret_cast<const char*>(stage_buf((3 + stg) % 5));
+      // per-lane fragment bases of this stage buffer, formed once per stage
+      // (opaque to the compiler, which would otherwise fold the buffer's
+      // address back into every read; LDS immediates are only 16 bits)
+      const char* ap[8];
+#pragma unroll
+      for (int k7 = 0; k7 < 8; ++k7) {
+        uint32_t a32 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+                           (const lds_void_t*)Sb)) + afo[k7];
+        asm volatile("" : "+v"(a32));
+        ap[k7] = (const char*)(const lds_void_t*)static_cast<uintptr_t>(a32);
+      }
       auto lda = [&](int kk, bf16x8 A[2]) __attribute__((always_inline)) {
 #pragma unroll
         for (int m = 0; m < 2; ++m)
-          A[m] = *reinterpret_cast<const bf16x8*>(Sb + afo[kk & 7] + (kk >> 3) * 256 +
+          A[m] = *reinterpret_cast<const bf16x8*>(ap[kk & 7] + (kk >> 3) * 256 +
                                                   m * (32 * SCH * 16));
       };
-      bf16x8 Acur[2], Anxt[2];
-      lda(0, Acur);
+      // A fragments in a ring of three K-steps; the load for K-step kk+2 is
+      // issued after the first tile of K-step kk, when the registers it
+      // reuses (K-step kk-1) have not been read for two tiles
+      bf16x8 Ar[3][2];
+      lda(0, Ar[0]);
+      if constexpr (kc > 1) lda(1, Ar[1]);
       static_for<0, kc>([&](auto kk_c) {
         constexpr int kk = decltype(kk_c)::value;
         constexpr int kap = k0 + kk;
-        if constexpr (kk + 1 < kc) lda(kk + 1, Anxt);
+        constexpr int cur = kk % 3;
         // item (kap, 0): MFMAs of tile 0, features of tile 1 at kap
         {
           float x[8], y[8], pr[8];
           fx(1, kap, x, y);
-          mfma2_prod8(acc[0][0], acc[1][0], Acur[0], Acur[1], bf, x, y, pr);
-          bf = pack8(pr);
+          mfma2_prod8(acc[0][0], acc[1][0], Ar[cur][0], Ar[cur][1], bq[0], x, y, pr);
+          bq[2] = bq[1];
+          bq[1] = bq[0];
+          bq[0] = pack8(pr);
+          hold(bq[1], bq[2]);
         }
+        if constexpr (kk + 2 < kc) lda(kk + 2, Ar[(kk + 2) % 3]);
         // item (kap, 1): MFMAs of tile 1, features of tile 0 at kap + 1
         {
           float x[8], y[8], pr[8];
           fx(0, (kap + 1 < G::NKS) ? kap + 1 : kap, x, y);
-          mfma2_prod8(acc[0][1], acc[1][1], Acur[0], Acur[1], bf, x, y, pr);
-          bf = pack8(pr);
-        }
-        if constexpr (kk + 1 < kc) {
-          Acur[0] = Anxt[0];
-          Acur[1] = Anxt[1];
+          mfma2_prod8(acc[0][1], acc[1][1], Ar[cur][0], Ar[cur][1], bq[0], x, y, pr);
+          bq[2] = bq[1];
+          bq[1] = bq[0];
+          bq[0] = pack8(pr);
+          hold(bq[1], bq[2]);
         }
       });
     });
