@@ -88,15 +88,15 @@ def algorithmic(w, L):
                      output  2*n*dv + 2*n + (C+1)*(d+dv)
                              (phi(q)^T S and phi(q)^T z readouts, causal
                               intra-chunk QK^T and PV at chunk size C)
-    scan: one read of every fp32 span state (n*(dv+1) values) and one bf16
-          write of its prefix, per span and head.
+    scan: one bf16 read of every span state (n*(dv+1) values) and one bf16
+          write of its exclusive prefix, per span and head.
     """
     n = w.d * (w.d + 1) // 2
     ht = w.B * w.H * w.T
     NS = (w.T + L - 1) // L
     state = (2 * n * w.dv + n) * ht
     output = (2 * n * w.dv + 2 * n + (w.C + 1) * (w.d + w.dv)) * ht
-    scan_bytes = NS * w.B * w.H * n * (w.dv + 1) * (4 + 2)
+    scan_bytes = NS * w.B * w.H * n * (w.dv + 1) * (2 + 2)
     return dict(n=n, state_flop=state, output_flop=output, scan_bytes=scan_bytes,
                 total_flop=state + output)
 
@@ -179,6 +179,81 @@ def bench_decode(kata, dev, hip):
     }
 
 
+KERNELS = {"span_state": "span_state_kernel", "scan": "scan_exclusive_bf16",
+           "span_output": "span_output_kernel"}
+COPY_BYTES = 1 << 30
+
+
+def copy_probe():
+    """A plain device copy of COPY_BYTES, three times: the calibration kernel
+    for the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": COPY_BYTES, "launches": 3}), flush=True)
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            rows.extend(csv.DictReader(fh))
+    return rows
+
+
+def _per_dispatch(rows, counter, match):
+    """Average over dispatches of the kernels whose name contains `match` of the
+    counter (summed over its instances within a dispatch), in KiB."""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter or match not in r["Kernel_Name"]:
+            continue
+        per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return (sum(per.values()) / len(per), len(per)) if per else (None, 0)
+
+
+def ingest_traffic(root, workload, span):
+    """profiles/traffic_counters.json and its summary from four rocprofv3 --pmc
+    runs under `root`: fetch/ and write/ (bench.py) and cfetch/, cwrite/
+    (bench.py --copy-probe)."""
+    cal = {}
+    for cnt, sub in (("FETCH_SIZE", "cfetch"), ("WRITE_SIZE", "cwrite")):
+        rows = _counter_rows(os.path.join(root, sub))
+        names = {r["Kernel_Name"] for r in rows if r["Counter_Name"] == cnt}
+        copies = [n for n in names if "copy" in n.lower()]  # the runtime's copy kernel
+        if len(copies) != 1:
+            raise SystemExit(f"expected one copy kernel in {sub}, found {sorted(names)}")
+        name = copies[0]
+        kib, nd = _per_dispatch(rows, cnt, name)
+        cal[cnt] = {"copy_kernel": name[:80], "kib_per_dispatch": kib, "dispatches": nd,
+                    "factor": COPY_BYTES / (kib * 1024.0)}
+    res = {"source_sha": source_sha(), "workload": workload, "span_chunks": span,
+           "calibration": {"copy_bytes": COPY_BYTES, **cal}}
+    fetch_rows = _counter_rows(os.path.join(root, "fetch"))
+    write_rows = _counter_rows(os.path.join(root, "write"))
+    for key, match in KERNELS.items():
+        fk, nf = _per_dispatch(fetch_rows, "FETCH_SIZE", match)
+        wk, nw = _per_dispatch(write_rows, "WRITE_SIZE", match)
+        if fk is None or wk is None:
+            continue
+        fb = fk * 1024.0 * cal["FETCH_SIZE"]["factor"]
+        wb = wk * 1024.0 * cal["WRITE_SIZE"]["factor"]
+        res[key] = {"fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
+                    "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                    "hbm_bytes_per_launch": fb + wb}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(res, fh, indent=1)
+    print(json.dumps(res, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -189,12 +264,23 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
+    ap.add_argument("--ingest-traffic", metavar="DIR",
+                    help="write profiles/traffic_counters.json from the --pmc runs under DIR")
     args = ap.parse_args()
+    if args.ingest_traffic:
+        ingest_traffic(args.ingest_traffic, args.workload, args.span or 16)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE "
               f"{world}); the forward has no multi-GPU path in this build.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe()
+        return
 
     import numpy as np
     import torch
@@ -258,7 +344,8 @@ def main():
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
         ent = tr.get(dominant, {})
-        if tr.get("source_sha") == sha and tr.get("workload") == w.name and ent:
+        if (tr.get("source_sha") == sha and tr.get("workload") == w.name
+                and tr.get("span_chunks") == span and ent):
             roof["traffic"] = ent.get("hbm_bytes_per_launch")
 
     res = {
