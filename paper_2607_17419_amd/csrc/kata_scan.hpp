@@ -89,88 +89,108 @@ namespace kata {
 // ---------------------------------------------------------------------------
 // In-place exclusive prefix over bf16 records (the MFMA path's span states):
 //   rec[bh][c][e] <- bf16( w(e) * sum_{c' < c} rec[bh][c'][e] ),  rec[.][0][.] = 0,
-// with the sums carried in fp32.  A workgroup owns kEB16 consecutive elements
-// of every record (512-byte rows, 16-byte accesses); rows are processed in
-// blocks of kNB16 with a Blelloch tree in LDS and an fp32 carry between blocks.
+// with the sums carried in fp32.  Blocked Blelloch scan along the record
+// axis: a workgroup owns kEB16 consecutive elements of every record; thread
+// (column group cg, row group rg) holds 8 elements x kRPT16 records in
+// registers and runs the up-sweep / down-sweep over its records there; the
+// row-group totals are scanned across the kRG16 groups through LDS; blocks of
+// kRG16 * kRPT16 records are chained by an fp32 carry.  All of a thread's
+// loads of a block are in flight together (16-byte accesses, 512-byte rows).
 // E must be a multiple of 8.  grid (ceil(E / kEB16), BH), block 256.
 // ---------------------------------------------------------------------------
-constexpr int kEB16 = 256;
-constexpr int kNB16 = 32;
+constexpr int kCG16 = 32;                // column groups of 8 elements
+constexpr int kEB16 = 8 * kCG16;         // elements per workgroup (256)
+constexpr int kRG16 = 256 / kCG16;       // row groups (8)
+constexpr int kRPT16 = 16;               // records per thread and block
+constexpr int kNB16 = kRG16 * kRPT16;    // records per block (128)
 
 template <typename Weight>
 __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N, long long E,
                                                            long long bh_stride, Weight weight) {
-  __shared__ float tile[kNB16][kEB16 + 4];
-  __shared__ float total_s[kEB16];
+  __shared__ float tot[kRG16][kEB16];
   const int tid = threadIdx.x;
-  const long long e0 = static_cast<long long>(blockIdx.x) * kEB16;
+  const int cg = tid % kCG16, rg = tid / kCG16;
+  const long long ec = static_cast<long long>(blockIdx.x) * kEB16 + 8 * cg;
   uint16_t* rb = rec + blockIdx.y * bh_stride;
-  const int cc = tid & 31;        // 8-element chunk of the column block
-  const int r8 = tid >> 5;        // row inside a pass of 8 rows
-  const long long ec = e0 + 8 * cc;
   const bool active = ec < E;
-  float carry[8];
-  float w[8];
+  float w[8], carry[8];
 #pragma unroll
   for (int x = 0; x < 8; ++x) {
-    carry[x] = 0.f;
     w[x] = active ? weight(ec + x) : 0.f;
+    carry[x] = 0.f;
   }
   for (int r0 = 0; r0 < N; r0 += kNB16) {
-    const int nr = min(kNB16, N - r0);
+    const int rbase = r0 + rg * kRPT16;  // this thread's first record
+    float v[kRPT16][8];
 #pragma unroll
-    for (int p = 0; p < kNB16 / 8; ++p) {
-      const int r = r8 + 8 * p;
+    for (int j = 0; j < kRPT16; ++j) {
       uint4 q4 = make_uint4(0u, 0u, 0u, 0u);
-      if (active && r < nr)
-        q4 = *reinterpret_cast<const uint4*>(rb + static_cast<long long>(r0 + r) * E + ec);
+      if (active && rbase + j < N)
+        q4 = *reinterpret_cast<const uint4*>(rb + static_cast<long long>(rbase + j) * E + ec);
       const uint32_t q[4] = {q4.x, q4.y, q4.z, q4.w};
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
-        tile[r][8 * cc + 2 * x] = bf16lo_f32(q[x]);
-        tile[r][8 * cc + 2 * x + 1] = bf16hi_f32(q[x]);
+        v[j][2 * x] = bf16lo_f32(q[x]);
+        v[j][2 * x + 1] = bf16hi_f32(q[x]);
       }
     }
-    __syncthreads();
-    for (int step = 1; step < kNB16; step <<= 1) {
-      const int nodes = kNB16 / (2 * step);
-      for (int i = tid; i < nodes * kEB16; i += 256) {
-        const int node = i / kEB16, col = i % kEB16;
-        const int right = (node + 1) * 2 * step - 1;
-        tile[right][col] += tile[right - step][col];
-      }
-      __syncthreads();
+    // up-sweep: v[j] for j = 2^(l+1)-1 (mod 2^(l+1)) accumulates its left subtree
+#pragma unroll
+    for (int d = 1; d < kRPT16; d <<= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kRPT16; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v[j][x] += v[j - d][x];
+    float gsum[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      gsum[x] = v[kRPT16 - 1][x];
+      v[kRPT16 - 1][x] = 0.f;
     }
-    total_s[tid] = tile[kNB16 - 1][tid];
-    tile[kNB16 - 1][tid] = 0.f;
+    // down-sweep: exclusive prefixes within the thread's records
+#pragma unroll
+    for (int d = kRPT16 / 2; d >= 1; d >>= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kRPT16; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          const float left = v[j - d][x];
+          v[j - d][x] = v[j][x];
+          v[j][x] += left;
+        }
+    // exclusive scan of the row-group totals, plus the block total for the carry
+#pragma unroll
+    for (int x = 0; x < 8; ++x) tot[rg][8 * cg + x] = gsum[x];
     __syncthreads();
-    for (int step = kNB16 / 2; step >= 1; step >>= 1) {
-      const int nodes = kNB16 / (2 * step);
-      for (int i = tid; i < nodes * kEB16; i += 256) {
-        const int node = i / kEB16, col = i % kEB16;
-        const int right = (node + 1) * 2 * step - 1;
-        const float left = tile[right - step][col];
-        tile[right - step][col] = tile[right][col];
-        tile[right][col] += left;
-      }
-      __syncthreads();
+    float pre[8], blk[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      pre[x] = carry[x];
+      blk[x] = 0.f;
     }
 #pragma unroll
-    for (int p = 0; p < kNB16 / 8; ++p) {
-      const int r = r8 + 8 * p;
-      if (active && r < nr) {
+    for (int g2 = 0; g2 < kRG16; ++g2)
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        const float t = tot[g2][8 * cg + x];
+        if (g2 < rg) pre[x] += t;
+        blk[x] += t;
+      }
+    __syncthreads();  // tot is rewritten by the next block
+#pragma unroll
+    for (int j = 0; j < kRPT16; ++j) {
+      if (active && rbase + j < N) {
         uint32_t q[4];
 #pragma unroll
         for (int x = 0; x < 4; ++x)
-          q[x] = pack_bf16x2(w[2 * x] * (tile[r][8 * cc + 2 * x] + carry[2 * x]),
-                             w[2 * x + 1] * (tile[r][8 * cc + 2 * x + 1] + carry[2 * x + 1]));
-        *reinterpret_cast<uint4*>(rb + static_cast<long long>(r0 + r) * E + ec) =
+          q[x] = pack_bf16x2(w[2 * x] * (pre[2 * x] + v[j][2 * x]),
+                             w[2 * x + 1] * (pre[2 * x + 1] + v[j][2 * x + 1]));
+        *reinterpret_cast<uint4*>(rb + static_cast<long long>(rbase + j) * E + ec) =
             make_uint4(q[0], q[1], q[2], q[3]);
       }
     }
 #pragma unroll
-    for (int x = 0; x < 8; ++x) carry[x] += total_s[8 * cc + x];
-    __syncthreads();
+    for (int x = 0; x < 8; ++x) carry[x] += blk[x];
   }
 }
 
