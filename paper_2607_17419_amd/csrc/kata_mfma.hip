@@ -174,45 +174,35 @@ __device__ __forceinline__ uint32_t word_of(const bf16x8& f, int j) {
   return j == 0 ? w.x : (j == 1 ? w.y : (j == 2 ? w.z : w.w));
 }
 
-// The two MFMAs of one slot tile (a0 += va0 * bf, a1 += va1 * bf) with the
-// eight feature products of the next tile computed under them: the y pairs
-// (bf16 (y_t, y_{t+1}) per dword) are widened to fp32 (shift / mask, exact)
-// between the MFMAs and multiplied by the widened x values (xf) after the
-// second.  A wave issues in order and an MFMA holds the matrix pipe for 32
-// cycles, so the eight widening instructions also space the two MFMAs; the
-// plain VALU work runs alongside them.  s_nop 1 first: a VALU write of bf
+// The two MFMAs of one tile (a0 += A0 * bf, a1 += A1 * bf: the two 32-wide
+// halves of dv) with the eight feature products of the next tile
+// (p_j = x_j * y_j, fp32) issued between them.  A wave issues in order and an
+// MFMA holds the matrix pipe for 32 cycles: the products take about as long
+// as the first MFMA, so the second issues without waiting, and the
+// conversions that follow run under it.  s_nop 1 first: a VALU write of bf
 // (its conversion) must be 2 wait states old when the MFMA reads it.  The
 // accumulators stay in AGPRs, which no VALU instruction writes; any later
 // read of them waits for the MFMA first (mfma_drain).
-__device__ __forceinline__ void mfma2_mul8(f32x16& a0, f32x16& a1, const bf16x8& va0,
-                                           const bf16x8& va1, const bf16x8& bf,
-                                           const uint32_t y[4], const float xf[8], float p[8]) {
-  float t[8];
+__device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8& A0,
+                                            const bf16x8& A1, const bf16x8& bf,
+                                            const float x[8], const float y[8], float p[8]) {
   asm volatile(
       "s_nop 1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %18, %20, %0\n\t"
-      "v_lshlrev_b32 %10, 16, %21\n\t"
-      "v_and_b32 %11, 0xffff0000, %21\n\t"
-      "v_lshlrev_b32 %12, 16, %22\n\t"
-      "v_and_b32 %13, 0xffff0000, %22\n\t"
-      "v_lshlrev_b32 %14, 16, %23\n\t"
-      "v_and_b32 %15, 0xffff0000, %23\n\t"
-      "v_lshlrev_b32 %16, 16, %24\n\t"
-      "v_and_b32 %17, 0xffff0000, %24\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %19, %20, %1\n\t"
-      "v_mul_f32 %2, %10, %25\n\t"
-      "v_mul_f32 %3, %11, %26\n\t"
-      "v_mul_f32 %4, %12, %27\n\t"
-      "v_mul_f32 %5, %13, %28\n\t"
-      "v_mul_f32 %6, %14, %29\n\t"
-      "v_mul_f32 %7, %15, %30\n\t"
-      "v_mul_f32 %8, %16, %31\n\t"
-      "v_mul_f32 %9, %17, %32"
+      "v_mfma_f32_32x32x16_bf16 %0, %10, %12, %0\n\t"
+      "v_mul_f32 %2, %13, %21\n\t"
+      "v_mul_f32 %3, %14, %22\n\t"
+      "v_mul_f32 %4, %15, %23\n\t"
+      "v_mul_f32 %5, %16, %24\n\t"
+      "v_mul_f32 %6, %17, %25\n\t"
+      "v_mul_f32 %7, %18, %26\n\t"
+      "v_mul_f32 %8, %19, %27\n\t"
+      "v_mul_f32 %9, %20, %28\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1"
       : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
-        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7]), "=&v"(t[0]), "=&v"(t[1]), "=&v"(t[2]),
-        "=&v"(t[3]), "=&v"(t[4]), "=&v"(t[5]), "=&v"(t[6]), "=&v"(t[7])
-      : "v"(va0), "v"(va1), "v"(bf), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(xf[0]),
-        "v"(xf[1]), "v"(xf[2]), "v"(xf[3]), "v"(xf[4]), "v"(xf[5]), "v"(xf[6]), "v"(xf[7]));
+        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7])
+      : "v"(A0), "v"(A1), "v"(bf), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]),
+        "v"(x[5]), "v"(x[6]), "v"(x[7]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(y[4]),
+        "v"(y[5]), "v"(y[6]), "v"(y[7]));
 }
 
 // The two MFMAs of the last slot tile of a staged block (nothing to overlap).
@@ -272,8 +262,9 @@ __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
 // ---------------------------------------------------------------------------
 constexpr int kTB2 = 128;           // tokens per staged block
-constexpr int kRow2 = kTB2 + 8;     // LDS row length (bf16): rows 272 B apart
-constexpr int kGap2 = 64;           // bf16 gap before key row d/2 (see krow)
+constexpr int kRow2 = kTB2 + 8;     // V^T row length in LDS (bf16): rows 272 B apart
+constexpr int kRowK2 = kTB2 + 4;    // K row length in LDS (fp32): rows 528 B apart
+constexpr int kGapK2 = 32;          // fp32 gap before key row d/2 (see krow)
 constexpr int kUW = 6;              // slot tiles per slot wave
 constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
 
@@ -297,15 +288,17 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   static_assert(UW % NXR == 0, "unit parity must be static");
   static_assert(G::MT == 2, "the slot loop issues the two dv tiles of a slot tile together");
   constexpr int KS = kTB2 / 16;                      // K-steps per staged block
-  // Key row r of a K buffer starts at krow(r).  The slot tiles read rows r and
-  // r + d/2 in the same 16-lane phase of a ds_read_b128; with a uniform
-  // stride they would share banks, the gap of kGap2 elements (32 banks)
-  // before row d/2 moves the upper half to the other half of the banks.
-  constexpr int KBUFE = D * kRow2 + kGap2;           // elements of one K buffer
-  constexpr unsigned KBUF = KBUFE * 2;               // bytes of one K buffer
+  // K is kept in LDS widened to fp32 (exact), so that the feature products
+  // are plain multiplies of LDS values.  Key row r of a K buffer starts at
+  // krow(r).  The slot tiles read rows r and r + d/2 in the same 16-lane phase
+  // of a ds_read_b128; with a uniform stride they would share banks, the gap
+  // of kGapK2 floats (32 banks) before row d/2 moves the upper half to the
+  // other half of the banks.
+  constexpr int KBUFE = D * kRowK2 + kGapK2;         // floats of one K buffer
+  constexpr unsigned KBUF = KBUFE * 4;               // bytes of one K buffer
   constexpr unsigned VBUF = DV * kRow2 * 2;          // bytes of one V buffer
-  auto krow = [](int r) { return r * kRow2 + (r >= D / 2 ? kGap2 : 0); };
-  __shared__ __attribute__((aligned(16))) uint16_t kT[kNBuf2][KBUFE];
+  auto krow = [](int r) { return r * kRowK2 + (r >= D / 2 ? kGapK2 : 0); };
+  __shared__ __attribute__((aligned(16))) float kT[kNBuf2][KBUFE];
   __shared__ __attribute__((aligned(16))) uint16_t vT[kNBuf2][DV][kRow2];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -358,28 +351,44 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
       const int cg = wave + 4 * i, p = lane;
       const bool va = t0 + 2 * p < span_end, vb = t0 + 2 * p + 1 < span_end;
-      // v_perm byte selectors: 0-3 pick bytes of the first token's word,
-      // 4-7 of the second's, 0x0c gives a zero byte
-      const uint32_t sel_e = (va ? 0x0100u : 0x0c0cu) | (vb ? 0x05040000u : 0x0c0c0000u);
-      const uint32_t sel_o = (va ? 0x0302u : 0x0c0cu) | (vb ? 0x07060000u : 0x0c0c0000u);
-      // rows 8*cg .. 8*cg+7 lie on one side of the gap (d/2 is a multiple of 8)
-      uint16_t* base = (cg < KG) ? &kT[buf][krow(8 * cg)] : &vT[buf][8 * (cg - KG)][0];
       const uint32_t a[4] = {st_lo[i].x, st_lo[i].y, st_lo[i].z, st_lo[i].w};
       const uint32_t b[4] = {st_hi[i].x, st_hi[i].y, st_hi[i].z, st_hi[i].w};
+      // v_perm byte selectors: 0-3 pick bytes of the second operand, 4-7 of
+      // the first, 0x0c gives a zero byte; tokens at or past the span end
+      // become zeros
+      if (cg < KG) {
+        // K: dim 8cg+2e of tokens (2p, 2p+1) is (a.lo, b.lo) widened to fp32,
+        // dim 8cg+2e+1 is (a.hi, b.hi); rows 8cg .. 8cg+7 lie on one side of the
+        // gap (d/2 is a multiple of 8)
+        const uint32_t lo_a = va ? 0x01000c0cu : 0x0c0c0c0cu, hi_a = va ? 0x03020c0cu : 0x0c0c0c0cu;
+        const uint32_t lo_b = vb ? 0x01000c0cu : 0x0c0c0c0cu, hi_b = vb ? 0x03020c0cu : 0x0c0c0c0cu;
+        float* base = &kT[buf][krow(8 * cg) + 2 * p];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        // element 2e: (a.lo, b.lo); element 2e+1: (a.hi, b.hi)
-        *reinterpret_cast<uint32_t*>(base + (2 * e) * kRow2 + 2 * p) =
-            __builtin_amdgcn_perm(b[e], a[e], sel_e);
-        *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2 + 2 * p) =
-            __builtin_amdgcn_perm(b[e], a[e], sel_o);
+        for (int e = 0; e < 4; ++e) {
+          *reinterpret_cast<uint2*>(base + (2 * e) * kRowK2) =
+              make_uint2(__builtin_amdgcn_perm(0u, a[e], lo_a), __builtin_amdgcn_perm(0u, b[e], lo_b));
+          *reinterpret_cast<uint2*>(base + (2 * e + 1) * kRowK2) =
+              make_uint2(__builtin_amdgcn_perm(0u, a[e], hi_a), __builtin_amdgcn_perm(0u, b[e], hi_b));
+        }
+      } else {
+        // V^T (bf16): element 2e is (a.lo, b.lo), 2e+1 (a.hi, b.hi)
+        const uint32_t sel_e = (va ? 0x0100u : 0x0c0cu) | (vb ? 0x05040000u : 0x0c0c0000u);
+        const uint32_t sel_o = (va ? 0x0302u : 0x0c0cu) | (vb ? 0x07060000u : 0x0c0c0000u);
+        uint16_t* base = &vT[buf][8 * (cg - KG)][0];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          *reinterpret_cast<uint32_t*>(base + (2 * e) * kRow2 + 2 * p) =
+              __builtin_amdgcn_perm(b[e], a[e], sel_e);
+          *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2 + 2 * p) =
+              __builtin_amdgcn_perm(b[e], a[e], sel_o);
+        }
       }
     }
   };
   using I0 = std::integral_constant<int, 0>;
   using IT = std::integral_constant<int, TPT>;
   static_assert(TPT <= KS, "one staging piece per K-step at most");
-  const char* kbase = reinterpret_cast<const char*>(&kT[0][0]);
+  const char* kbase = reinterpret_cast<const char*>(&kT[0][0]);  // fp32 K buffers
   const char* vbase = reinterpret_cast<const char*>(&vT[0][0][0]);
 
   // Three-deep ring: block bi is read from buffer bi % 3 while block bi+1 is
@@ -426,8 +435,17 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
         for (int ks = 0; ks < KS; ++ks) {
           bf16x8 A[G::ZM];
 #pragma unroll
-          for (int a = 0; a < G::ZM; ++a)
-            A[a] = *reinterpret_cast<const bf16x8*>(&kT[buf][krow(32 * a + c) + 16 * ks + 8 * g]);
+          for (int a = 0; a < G::ZM; ++a) {
+            // the fp32 values are bf16 values: keep their upper halves
+            const float* kr = &kT[buf][krow(32 * a + c) + 16 * ks + 8 * g];
+            const uint4 f0 = *reinterpret_cast<const uint4*>(kr);
+            const uint4 f1 = *reinterpret_cast<const uint4*>(kr + 4);
+            A[a] = __builtin_bit_cast(
+                bf16x8, make_uint4(__builtin_amdgcn_perm(f0.y, f0.x, 0x07060302u),
+                                   __builtin_amdgcn_perm(f0.w, f0.z, 0x07060302u),
+                                   __builtin_amdgcn_perm(f1.y, f1.x, 0x07060302u),
+                                   __builtin_amdgcn_perm(f1.w, f1.z, 0x07060302u)));
+          }
 #pragma unroll
           for (int a = 0; a < G::ZM; ++a)
 #pragma unroll
@@ -460,14 +478,14 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   for (int p = 0; p < NXR; ++p) {
     int xr, yy;
     slot_pair<D>(32 * p + c, xr, yy);
-    xo[p] = static_cast<unsigned>((krow(xr) + 8 * g) * 2);
+    xo[p] = static_cast<unsigned>((krow(xr) + 8 * g) * 4);
   }
 #pragma unroll
   for (int u = 0; u < UW; ++u) {
     int xx, yr;
     const int unit = unit0 + u < G::NST ? unit0 + u : G::NST - 1;  // valid row; store skipped
     slot_pair<D>(32 * unit + c, xx, yr);
-    yo[u] = static_cast<unsigned>((krow(yr) + 8 * g) * 2);
+    yo[u] = static_cast<unsigned>((krow(yr) + 8 * g) * 4);
   }
 #pragma unroll
   for (int m = 0; m < G::MT; ++m) vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
@@ -480,47 +498,46 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
 
-  // LDS fragments: the y rows of the slot tiles (each reloaded for the next
-  // K-step as soon as the features it feeds are computed), the x rows of the
-  // next K-step, and V^T double buffered by K-step parity.
-  uint4 fy[UW], fx[NXR], fv[2][G::MT];
-  float xf[NXR][8];  // x values of the K-step's 8 tokens, widened to fp32
+  // LDS fragments: the y rows of the slot tiles (8 fp32 tokens each, reloaded
+  // for the next K-step as soon as the features they feed are computed), the
+  // x rows (reloaded for the next K-step after their last use in this one)
+  // and V^T double buffered by K-step parity.
+  struct F8 {
+    float v[8];
+  };
+  F8 fy[UW], fx[NXR];
+  uint4 fv[2][G::MT];
+  auto ld8 = [](const char* p) __attribute__((always_inline)) {
+    const uint4 a = *reinterpret_cast<const uint4*>(p);
+    const uint4 b = *reinterpret_cast<const uint4*>(p + 16);
+    F8 r;
+    r.v[0] = __uint_as_float(a.x);
+    r.v[1] = __uint_as_float(a.y);
+    r.v[2] = __uint_as_float(a.z);
+    r.v[3] = __uint_as_float(a.w);
+    r.v[4] = __uint_as_float(b.x);
+    r.v[5] = __uint_as_float(b.y);
+    r.v[6] = __uint_as_float(b.z);
+    r.v[7] = __uint_as_float(b.w);
+    return r;
+  };
   auto ldv = [&](int set, const char* vb, unsigned ko) __attribute__((always_inline)) {
 #pragma unroll
     for (int m = 0; m < G::MT; ++m) fv[set][m] = *reinterpret_cast<const uint4*>(vb + vo[m] + ko);
-  };
-  auto ldx = [&](const char* kb, unsigned ko) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < NXR; ++p) fx[p] = *reinterpret_cast<const uint4*>(kb + xo[p] + ko);
-  };
-  auto widen_x = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < NXR; ++p) {
-      const uint32_t X[4] = {fx[p].x, fx[p].y, fx[p].z, fx[p].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        xf[p][2 * e] = __uint_as_float(X[e] << 16);
-        xf[p][2 * e + 1] = __uint_as_float(X[e] & 0xFFFF0000u);
-      }
-    }
-  };
-  // the first tile's features of a staged block (nothing to overlap with)
-  auto features = [&](const uint4& yv, const float x8[8]) __attribute__((always_inline)) {
-    const uint32_t Y[4] = {yv.x, yv.y, yv.z, yv.w};
-    float pr[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      pr[2 * e] = __uint_as_float(Y[e] << 16) * x8[2 * e];
-      pr[2 * e + 1] = __uint_as_float(Y[e] & 0xFFFF0000u) * x8[2 * e + 1];
-    }
-    return __builtin_bit_cast(
-        bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                           pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
   };
   auto pack8 = [](const float pr[8]) __attribute__((always_inline)) {
     return __builtin_bit_cast(
         bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
                            pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+  };
+  // tile u of a K-step computes the features of tile u+1, whose x row has
+  // parity (u+1) % NXR; the x row of parity p is reloaded for the next K-step
+  // after xlast(p), the last tile of this K-step that uses it
+  auto xlast = [](int p) {
+    int last = -1;
+    for (int u = 0; u + 1 < UW; ++u)
+      if ((u + 1) % NXR == p) last = u;
+    return last;
   };
   // Per staged block: publish block bi+1 and fetch block bi+2 piece by piece;
   // the features of tile u+1 are computed under the MFMAs of tile u (the
@@ -534,15 +551,20 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     const long long t1 = span0 + static_cast<long long>(bi + 1) * kTB2;
     const long long t2 = t1 + kTB2;
     ldv(0, vb, 0u);
-    ldx(kb, 0u);
 #pragma unroll
-    for (int u = 0; u < UW; ++u) fy[u] = *reinterpret_cast<const uint4*>(kb + yo[u]);
-    widen_x();
+    for (int p = 0; p < NXR; ++p) fx[p] = ld8(kb + xo[p]);
+#pragma unroll
+    for (int u = 0; u < UW; ++u) fy[u] = ld8(kb + yo[u]);
     // B fragments: bq[0] the next tile's, bq[1], bq[2] the two before (kept
     // live so that a new fragment never reuses the registers of an MFMA that
     // may still be running, see hold)
     bf16x8 bq[3];
-    bq[0] = features(fy[0], xf[0]);
+    {
+      float pr[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pr[j] = fx[0].v[j] * fy[0].v[j];
+      bq[0] = pack8(pr);
+    }
     bq[1] = bq[0];
     bq[2] = bq[0];
     auto push = [&](const float pr[8]) __attribute__((always_inline)) {
@@ -554,7 +576,8 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     static_for<0, KS>([&](auto ks_c) {
       constexpr int ks = decltype(ks_c)::value;
       constexpr int cur = ks & 1;
-      constexpr unsigned kn = 32u * (ks + 1);  // byte column of K-step ks+1
+      constexpr unsigned kn = 64u * (ks + 1);  // byte column of K-step ks+1 (16 fp32)
+      constexpr unsigned vn = 32u * (ks + 1);  // ... in the bf16 V^T rows
       static_for<0, TPT>([&](auto j_c) {  // staging piece j at K-step j*KS/TPT
         constexpr int j = decltype(j_c)::value;
         if constexpr (j * KS / TPT == ks) {
@@ -564,29 +587,29 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
           fetch(t2, J{}, J1{});
         }
       });
-      if constexpr (ks + 1 < KS) ldx(kb, kn);
       const bf16x8 va0 = __builtin_bit_cast(bf16x8, fv[cur][0]);
       const bf16x8 va1 = __builtin_bit_cast(bf16x8, fv[cur][1]);
       static_for<0, UW>([&](auto u_c) {
         constexpr int u = decltype(u_c)::value;
         // fy[u] fed the features of (ks, u): reload it for (ks+1, u)
-        if constexpr (ks + 1 < KS && u > 0)
-          fy[u] = *reinterpret_cast<const uint4*>(kb + yo[u] + kn);
+        if constexpr (ks + 1 < KS && u > 0) fy[u] = ld8(kb + yo[u] + kn);
         if constexpr (u + 1 < UW) {
-          const uint32_t Y[4] = {fy[u + 1].x, fy[u + 1].y, fy[u + 1].z, fy[u + 1].w};
           float pr[8];
-          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bq[0], Y, xf[(u + 1) % NXR], pr);
+          mfma2_prod8(acc[u][0], acc[u][1], va0, va1, bq[0], fx[(u + 1) % NXR].v,
+                      fy[u + 1].v, pr);
           push(pr);
-          if constexpr (ks + 1 < KS && u == 0)
-            fy[0] = *reinterpret_cast<const uint4*>(kb + yo[0] + kn);
+          if constexpr (ks + 1 < KS && u == 0) fy[0] = ld8(kb + yo[0] + kn);
           // V^T of K-step ks+1 into the other buffer, whose last readers (the
           // previous K-step's final tile) are two tiles old now
-          if constexpr (ks + 1 < KS && u == 1) ldv(cur ^ 1, vb, kn);
+          if constexpr (ks + 1 < KS && u == 1) ldv(cur ^ 1, vb, vn);
+          if constexpr (ks + 1 < KS) {
+#pragma unroll
+            for (int p = 0; p < NXR; ++p)
+              if (u == xlast(p)) fx[p] = ld8(kb + xo[p] + kn);
+          }
         } else if constexpr (ks + 1 < KS) {
-          widen_x();  // x rows of K-step ks+1
-          const uint32_t Y[4] = {fy[0].x, fy[0].y, fy[0].z, fy[0].w};
           float pr[8];
-          mfma2_mul8(acc[u][0], acc[u][1], va0, va1, bq[0], Y, xf[0], pr);
+          mfma2_prod8(acc[u][0], acc[u][1], va0, va1, bq[0], fx[0].v, fy[0].v, pr);
           push(pr);
         } else {
           mfma2(acc[u][0], acc[u][1], va0, va1, bq[0]);
@@ -648,33 +671,6 @@ __device__ __forceinline__ uint16_t* stage_buf(int j) {
                 : (j == 1 ? g_stage1 : (j == 2 ? g_stage2 : (j == 3 ? g_stage3 : g_stage4)));
 }
 
-// The two MFMAs of one query tile of the prefix readout (a0 += A0 * bf,
-// a1 += A1 * bf) with the eight products of the next tile's query features
-// (p_j = x_j * y_j, fp32 registers) between them: the products take as long
-// as the first MFMA, so the second issues without waiting, and the
-// conversions that follow run under it.  Same wait-state and accumulator
-// rules as mfma2_mul8.
-__device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8& A0,
-                                            const bf16x8& A1, const bf16x8& bf,
-                                            const float x[8], const float y[8], float p[8]) {
-  asm volatile(
-      "s_nop 1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %10, %12, %0\n\t"
-      "v_mul_f32 %2, %13, %21\n\t"
-      "v_mul_f32 %3, %14, %22\n\t"
-      "v_mul_f32 %4, %15, %23\n\t"
-      "v_mul_f32 %5, %16, %24\n\t"
-      "v_mul_f32 %6, %17, %25\n\t"
-      "v_mul_f32 %7, %18, %26\n\t"
-      "v_mul_f32 %8, %19, %27\n\t"
-      "v_mul_f32 %9, %20, %28\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1"
-      : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
-        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7])
-      : "v"(A0), "v"(A1), "v"(bf), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]),
-        "v"(x[5]), "v"(x[6]), "v"(x[7]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(y[4]),
-        "v"(y[5]), "v"(y[6]), "v"(y[7]));
-}
 
 // Scores of two query tiles against one 32-key block: sc_i = K_blk Q_i^T
 // over the d-contraction, the two accumulation chains interleaved, results in
