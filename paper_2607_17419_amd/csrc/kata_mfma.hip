@@ -640,7 +640,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
 
 // ---------------------------------------------------------------------------
 // K4: span output.  1-D grid of workgroups of 256 threads (4 waves), one per
-// CU (96 KB of LDS in three 32 KB stage buffers).  A span has QB = L/256
+// CU (160 KB of LDS in five 32 KB stage buffers).  A span has QB = L/256
 // query blocks; block id -> (span, query block) keeps the query blocks of a
 // span on one XCD (equal id % 8), dispatched back to back, so they share the
 // span's prefix record and keys in that XCD's L2.
