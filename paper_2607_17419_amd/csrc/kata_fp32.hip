@@ -167,6 +167,8 @@ __global__ __launch_bounds__(256) void chunk_out_f32(
 // state).  One workgroup per head; S is streamed once (read-modify-write).
 // grid BH, block 256; d <= 64, dv <= 256.
 // ---------------------------------------------------------------------------
+constexpr int kDecodeUnroll = 8;  // S rows per thread whose loads are in flight together
+
 template <typename Tin>
 __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
                                                        float* __restrict__ z,
@@ -199,22 +201,34 @@ __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
     const int g = dv / 4;
     const int rows_per_pass = 256 / g;
     jbase = 4 * (tid % g);
-    for (int f = tid / g; f < n; f += rows_per_pass) {
-      int a = pairs[f] & 0xFF, b = pairs[f] >> 8;
-      float pk = ks[a] * ks[b];
-      float pq = ((a == b) ? 1.f : 2.f) * qs[a] * qs[b];
-      float4* p = reinterpret_cast<float4*>(Sh + static_cast<long long>(f) * dv + jbase);
-      float4 s = *p;
-      s.x += pk * vs[jbase + 0];
-      s.y += pk * vs[jbase + 1];
-      s.z += pk * vs[jbase + 2];
-      s.w += pk * vs[jbase + 3];
-      *p = s;
+    const float v0 = vs[jbase + 0], v1 = vs[jbase + 1], v2 = vs[jbase + 2], v3 = vs[jbase + 3];
+    auto row = [&](int f, float4 s) {
+      const int a = pairs[f] & 0xFF, b = pairs[f] >> 8;
+      const float pk = ks[a] * ks[b];
+      const float pq = ((a == b) ? 1.f : 2.f) * qs[a] * qs[b];
+      s.x += pk * v0;
+      s.y += pk * v1;
+      s.z += pk * v2;
+      s.w += pk * v3;
+      *reinterpret_cast<float4*>(Sh + static_cast<long long>(f) * dv + jbase) = s;
       num[0] += pq * s.x;
       num[1] += pq * s.y;
       num[2] += pq * s.z;
       num[3] += pq * s.w;
+    };
+    // kDecodeUnroll rows per thread in flight: their loads are issued together
+    int f = tid / g;
+    for (; f + (kDecodeUnroll - 1) * rows_per_pass < n; f += kDecodeUnroll * rows_per_pass) {
+      float4 s[kDecodeUnroll];
+#pragma unroll
+      for (int u = 0; u < kDecodeUnroll; ++u)
+        s[u] = *reinterpret_cast<const float4*>(
+            Sh + static_cast<long long>(f + u * rows_per_pass) * dv + jbase);
+#pragma unroll
+      for (int u = 0; u < kDecodeUnroll; ++u) row(f + u * rows_per_pass, s[u]);
     }
+    for (; f < n; f += rows_per_pass)
+      row(f, *reinterpret_cast<const float4*>(Sh + static_cast<long long>(f) * dv + jbase));
   } else {
     const int rows_per_pass = 256 / dv;  // dv <= 256
     jbase = tid % dv;
