@@ -196,6 +196,34 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": COPY_BYTES, "launches": 3}), flush=True)
 
 
+def hbm_ceiling(dev, nbytes=COPY_BYTES, reps=10):
+    """Practical HBM read+write rate on this GPU: a plain device copy of
+    `nbytes` into a second buffer, and an in-place elementwise scale of the same
+    buffer (one read and one write per element, the access pattern of the scan
+    and of the decode step).  Bytes counted: read + written."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    rates = {}
+    for name, op in (("copy", lambda: b.copy_(a)), ("inplace_scale", lambda: a.mul_(1.0))):
+        for _ in range(3):
+            op()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            op()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        rates[name + "_GBps"] = round(2 * nbytes / (ms * 1e-3) / 1e9, 1)
+    del a, b
+    rates["bytes"] = nbytes
+    rates["nominal_GBps"] = PEAK_HBM_GBS
+    return rates
+
+
 def _counter_rows(d):
     import csv
     import glob
@@ -373,6 +401,7 @@ def main():
     }
     if not args.no_decode:
         res["decode"] = bench_decode(kata, dev, hip)
+        res["practical_hbm"] = hbm_ceiling(dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)
