@@ -216,6 +216,20 @@ __device__ __forceinline__ void mfma2(f32x16& a0, f32x16& a1, const bf16x8& va0,
       : "v"(va0), "v"(va1), "v"(bf));
 }
 
+// Single MFMAs from inline assembly, for sequences whose order the caller
+// fixes with scheduling barriers: mfma_a accumulates into AGPRs, mfma_vz and
+// mfma_v start and continue a chain in VGPRs (read by VALU afterwards, which
+// the caller keeps at least two MFMA issues away from the chain's last MFMA).
+__device__ __forceinline__ void mfma_a(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_vz(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_v(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
 // Keeps the operand registers of recently issued MFMAs live up to this point,
 // so the compiler does not reuse them for new values: an instruction that
 // writes a register an MFMA in flight still reads waits for that MFMA to
@@ -861,13 +875,20 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   issue_i(0, g_stage0);
   if (nstage > 1) issue_i(1, g_stage1);
 
+  // The P V / readout accumulators live in AGPRs from here to the stores.
+  // The empty asm makes the zeros exist here: otherwise the compiler writes
+  // them just before the first MFMA that reads them, and as that MFMA is
+  // inline assembly it would not insert the wait states an MFMA needs after a
+  // VALU write of its accumulator.
   f32x16 acc[G::MT][NQ];
 #pragma unroll
   for (int m = 0; m < G::MT; ++m)
 #pragma unroll
-    for (int i = 0; i < NQ; ++i)
+    for (int i = 0; i < NQ; ++i) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][i][r] = 0.f;
+      asm volatile("" : "+a"(acc[m][i]));
+    }
   float dpart[NQ];
 
   // ---- denominator from the prefix: q^T Z_pre q ------------------------------
@@ -903,6 +924,20 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   }
 
   // ---- causal squared-score attention inside the span -----------------------
+  // Per 32-key block kb and query tile i: S_i = K_kb Q_i^T (a chain of KZ
+  // MFMAs into VGPRs), P_i = S_i^2 masked above the diagonal on the tile's
+  // diagonal block (VALU, with the row sums for the denominator), and
+  // O_i += V_kb^T P_i (four MFMAs: two dv halves x two 16-key halves).  The
+  // wave's two tiles run half a block apart, so every VALU step has MFMAs of
+  // the other tile to issue between:
+  //   group A of block kb: S_0(kb) and P V of tile 0 at kb-1; P_1(kb-1)
+  //   group B of block kb: S_1(kb) and P V of tile 1 at kb-1; P_0(kb)
+  // A wave issues in order and an MFMA holds the matrix pipe for 32 cycles;
+  // each group alternates its two MFMA chains (never two dependent MFMAs in a
+  // row) and places a quarter of the P work after each MFMA (scheduling
+  // barriers keep that order).  A tile whose diagonal block is past, or that
+  // lies beyond the sequence, gets zero P fragments: its MFMAs still run, so
+  // no branch surrounds an accumulator.
   {
     // fragment byte offsets inside a stage buffer
     //  K rows 32*sb + c, chunk (kz + (R/8)*g) ^ kswz: depends on sb only through sb & 1
@@ -923,86 +958,209 @@ __global__ __launch_bounds__(256) void span_output_kernel(
         vfo[sb][kv] = static_cast<unsigned>(
             (KCHUNKS + c * VCH + ((4 * sb + 2 * kv + g) ^ rswz(c))) * 16);
 
-    // Tiles that are finished (past their diagonal block) or beyond the
-    // sequence keep running through the same MFMAs, with zero P fragments
-    // (their VALU work is skipped), so no branch surrounds an accumulator.
-    auto ldfrag = [&](const char* Ks, int sb, bf16x8 (&A)[G::KZ], bf16x8 (&va)[G::MT][2])
-                      __attribute__((always_inline)) {
-      const unsigned krow0 = static_cast<unsigned>(sb >> 1) * (64u * KCH * 16u);
+    // a tile's diagonal block, -1 for a tile beyond the sequence (wave-uniform)
+    int tdiag[NQ];
 #pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz)
-        A[kz] = *reinterpret_cast<const bf16x8*>(Ks + krow0 + kfo[sb & 1][kz]);
+    for (int i = 0; i < NQ; ++i) tdiag[i] = __builtin_amdgcn_readfirstlane(tlive[i] ? tile[i] : -1);
+    // Fragment loads of block kb at stage position sb (known at compile time)
+    // from its stage buffer; one 16-byte read per call, so that the callers
+    // can spread them over the MFMA slots of a group.
+    auto ldA1 = [&](const char* buf, auto sb_c, int kz, bf16x8& dst) __attribute__((always_inline)) {
+      constexpr int sb = decltype(sb_c)::value;
+      dst = *reinterpret_cast<const bf16x8*>(buf + (sb >> 1) * (64 * KCH * 16) + kfo[sb & 1][kz]);
+    };
+    auto ldV1 = [&](const char* buf, auto sb_c, int m, int kv, bf16x8& dst)
+                    __attribute__((always_inline)) {
+      constexpr int sb = decltype(sb_c)::value;
+      dst = *reinterpret_cast<const bf16x8*>(buf + vfo[sb][kv] + m * (32 * VCH * 16));
+    };
+    auto ldA = [&](const char* buf, auto sb_c, bf16x8 (&A)[G::KZ]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int kz = 0; kz < G::KZ; ++kz) ldA1(buf, sb_c, kz, A[kz]);
+    };
+    auto ldV = [&](const char* buf, auto sb_c, bf16x8 (&va)[G::MT][2]) __attribute__((always_inline)) {
 #pragma unroll
       for (int m = 0; m < G::MT; ++m)
 #pragma unroll
-        for (int kv = 0; kv < 2; ++kv)
-          va[m][kv] = *reinterpret_cast<const bf16x8*>(Ks + vfo[sb][kv] + m * (32 * VCH * 16));
+        for (int kv = 0; kv < 2; ++kv) ldV1(buf, sb_c, m, kv, va[m][kv]);
     };
-    // squared scores of one tile: p = sc^2, masked above the diagonal on the
-    // tile's diagonal block; zero for a finished or dead tile (its MFMAs run
-    // anyway, no branch surrounds an accumulator); returns the two P fragments
-    auto probs = [&](const f32x16& sc, bool diag, bool done, float& dacc, bf16x8 (&Bp)[2])
+    // P elements 2j and 2j+1 of a tile on a block before its diagonal, packed.
+    // The empty asm statement consumes the results before the next asm (an
+    // MFMA), so the compiler can neither sink the part below it nor merge it
+    // into the fix-up that follows the group.
+    auto ppart = [&](int j, const f32x16& sc, float& dacc, uint32_t (&bw)[8])
                      __attribute__((always_inline)) {
-      if (done) {
-        Bp[0] = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
-        Bp[1] = Bp[0];
-        return;
+      const float p0 = sc[2 * j] * sc[2 * j];
+      const float p1 = sc[2 * j + 1] * sc[2 * j + 1];
+      dacc += p0 + p1;
+      bw[j] = pack_bf16x2(p0, p1);
+      asm volatile("" : "+v"(dacc), "+v"(bw[j]));
+    };
+    // on tile i's diagonal block (keys above the query masked) and past it
+    // (zero; also a tile beyond the sequence) the tile's P of block kb is
+    // redone after its group, VALU only; dsave is the row sum before the group
+    auto fixup = [&](int kb, int i, const f32x16& sc, float dsave, float& dacc, uint32_t (&bw)[8])
+                     __attribute__((always_inline)) {
+      if (__builtin_expect(kb < tdiag[i], 1)) return;  // nothing to redo (the common case)
+      if (kb == tdiag[i]) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int r0 = 2 * j, r1 = 2 * j + 1;
+          const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : sc[r0] * sc[r0];
+          const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : sc[r1] * sc[r1];
+          dsave += p0 + p1;
+          bw[j] = pack_bf16x2(p0, p1);
+        }
+        dacc = dsave;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) bw[j] = 0u;
+        dacc = dsave;
       }
-      float p[16];
+    };
+    auto bfrag = [](const uint32_t (&bw)[8], int kv) __attribute__((always_inline)) {
+      return __builtin_bit_cast(bf16x8, make_uint4(bw[4 * kv], bw[4 * kv + 1], bw[4 * kv + 2],
+                                                   bw[4 * kv + 3]));
+    };
+    // one group: score chain into scs (if S), P V into (a0, a1) from fragments
+    // vb and P words bv (if V), and the P words bw of the other tile from scp
+    // (full mode; the caller fixes them up for the other modes); extra(i)
+    // adds the caller's work (fragment loads) to slot i
+    auto group = [&](auto s_c, auto v_c, f32x16& scs, const bf16x8 (&Ab)[G::KZ],
+                     const bf16x8 (&qs)[G::KZ], f32x16& a0, f32x16& a1,
+                     const bf16x8 (&vb)[G::MT][2], const uint32_t (&bv)[8], f32x16& scp,
+                     float& dacc, uint32_t (&bw)[8], auto&& extra) __attribute__((always_inline)) {
+      constexpr bool HS = decltype(s_c)::value, HV = decltype(v_c)::value;
+      bf16x8 Bv[2];
+      if constexpr (HV) {
+        Bv[0] = bfrag(bv, 0);
+        Bv[1] = bfrag(bv, 1);
+      }
+      static_for<0, 4>([&](auto i_c) {
+        constexpr int i = decltype(i_c)::value;
+        if constexpr (HS && i < G::KZ) {
+          if constexpr (i == 0) mfma_vz(scs, Ab[0], qs[0]);
+          else mfma_v(scs, Ab[i], qs[i]);
+        }
+        // without a score chain the P V MFMA goes first, so that the VALU
+        // reads scp two MFMA issues after the chain that wrote it
+        if constexpr (!HS && HV) mfma_a((i & 1) ? a1 : a0, vb[i & 1][i >> 1], Bv[i >> 1]);
+        // the scores become available to the VALU only after the first MFMA
+        if constexpr (i == 0) asm volatile("" : "+v"(scp));
+        __builtin_amdgcn_sched_barrier(0);
+        ppart(2 * i, scp, dacc, bw);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (HS && HV) mfma_a((i & 1) ? a1 : a0, vb[i & 1][i >> 1], Bv[i >> 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        ppart(2 * i + 1, scp, dacc, bw);
+        extra(i_c);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+    auto none = [](auto) {};
+    using Yes = std::true_type;
+    using No = std::false_type;
+    using std::integral_constant;
+
+    const int NB = 4 * nstage;  // 32-key blocks, all waves alike (stage barriers)
+    bf16x8 A[2][G::KZ], va[2][G::MT][2];
+    f32x16 sc[NQ];
+    uint32_t bw[NQ][8];
+    // stage buffers of stages st, st+1, st+2 (rotated once per stage)
+    const char* b0 = reinterpret_cast<const char*>(g_stage0);
+    const char* b1 = reinterpret_cast<const char*>(g_stage1);
+    const char* b2 = reinterpret_cast<const char*>(g_stage2);
+    // stage 0 (copies issued at the start, after the readout's first two)
+    if (nstage > 1) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
+    lds_barrier();
+    if (nstage > 2) issue_i(2, g_stage2);
+    ldA(b0, integral_constant<int, 0>{}, A[0]);
+    ldA(b0, integral_constant<int, 1>{}, A[1]);
+    ldV(b0, integral_constant<int, 0>{}, va[0]);
+    // block 0: both score chains interleaved (no earlier block to finish),
+    // then P_0(0); score2 leaves sc[0] readable by VALU
+    score2<G::KZ>(sc[0], sc[1], A[0], qf[0], qf[1]);
+    {
+      const float dsave = dpart[0];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) p[r] = sc[r] * sc[r];
-      if (diag) {
+      for (int j = 0; j < 8; ++j) ppart(j, sc[0], dpart[0], bw[0]);
+      fixup(0, 0, sc[0], dsave, dpart[0], bw[0]);
+    }
+    // block kb >= 1 at stage position sb: A[sb & 1] holds A(kb) and V(kb) is
+    // loaded into va[sb & 1]; P V of block kb-1 uses va[(sb & 1) ^ 1].  Inside
+    // a stage the loads of V(kb) and A(kb+1) ride in group A's MFMA slots; the
+    // last block of a stage loads up front, around the stage change.
+    auto step = [&](auto sb_c, int kb) __attribute__((always_inline)) {
+      constexpr int sb = decltype(sb_c)::value;
+      constexpr int cur = sb & 1;
+      auto loads = [&](auto i_c) __attribute__((always_inline)) {
+        constexpr int i = decltype(i_c)::value;
+        if constexpr (sb != 3) {
+          if constexpr (i < 2) {
+            ldV1(b0, sb_c, i, 0, va[cur][i][0]);
+            ldV1(b0, sb_c, i, 1, va[cur][i][1]);
+          } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 8 * (r >> 2) + 4 * g + (r & 3);
-          p[r] = (key > c) ? 0.f : p[r];
+            for (int kz = 2 * (i - 2); kz < 2 * (i - 2) + 2; ++kz)
+              if (kz < G::KZ) ldA1(b0, integral_constant<int, sb + 1>{}, kz, A[cur ^ 1][kz]);
+          }
+        }
+      };
+      if constexpr (sb == 3) {
+        ldV(b0, sb_c, va[cur]);
+        if (kb + 1 < NB) {  // block kb+1 opens stage st
+          const int st = (kb + 1) >> 2;
+          if (st + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
+          lds_barrier();  // also: every wave has read stage st-1 (V(kb) above)
+          if (st + 2 < nstage) issue_i(st + 2, const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(b0)));
+          ldA(b1, integral_constant<int, 0>{}, A[cur ^ 1]);
         }
       }
-      float dsum = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) dsum += p[r];
-      dacc += dsum;
-      asm volatile("" : "+v"(dacc));  // sum here, not at the end of the stage
-#pragma unroll
-      for (int kv = 0; kv < 2; ++kv)
-        Bp[kv] = __builtin_bit_cast(
-            bf16x8, make_uint4(pack_bf16x2(p[8 * kv + 0], p[8 * kv + 1]),
-                               pack_bf16x2(p[8 * kv + 2], p[8 * kv + 3]),
-                               pack_bf16x2(p[8 * kv + 4], p[8 * kv + 5]),
-                               pack_bf16x2(p[8 * kv + 6], p[8 * kv + 7])));
-    };
-    auto compute = [&](int st, const uint16_t* buf) __attribute__((always_inline)) {
-      const char* Ks = reinterpret_cast<const char*>(buf);
-      bf16x8 A[2][G::KZ], va[2][G::MT][2];
-      ldfrag(Ks, 0, A[0], va[0]);
-#pragma unroll
-      for (int sb = 0; sb < kKB / 32; ++sb) {
-        const int kb = 4 * st + sb;  // 32-key block inside the span
-        const int cur = sb & 1;
-        f32x16 sc0, sc1;
-        score2<G::KZ>(sc0, sc1, A[cur], qf[0], qf[1]);
-        // the next block's fragments: the P V MFMAs of the previous block,
-        // which read va[cur ^ 1], are eight MFMAs old by now
-        if (sb + 1 < kKB / 32) ldfrag(Ks, sb + 1, A[cur ^ 1], va[cur ^ 1]);
-        bf16x8 B0[2], B1[2];
-        probs(sc0, kb == tile[0], !tlive[0] || kb > tile[0], dpart[0], B0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma2(acc[0][0], acc[1][0], va[cur][0][0], va[cur][1][0], B0[0]);
-        __builtin_amdgcn_sched_barrier(0);
-        probs(sc1, kb == tile[1], !tlive[1] || kb > tile[1], dpart[1], B1);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma2(acc[0][0], acc[1][0], va[cur][0][1], va[cur][1][1], B0[1]);
-        mfma2(acc[0][1], acc[1][1], va[cur][0][0], va[cur][1][0], B1[0]);
-        mfma2(acc[0][1], acc[1][1], va[cur][0][1], va[cur][1][1], B1[1]);
+      {
+        const float dsave = dpart[1];
+        group(Yes{}, Yes{}, sc[0], A[cur], qf[0], acc[0][0], acc[1][0], va[cur ^ 1], bw[0], sc[1],
+              dpart[1], bw[1], loads);
+        fixup(kb - 1, 1, sc[1], dsave, dpart[1], bw[1]);
+      }
+      {
+        const float dsave = dpart[0];
+        group(Yes{}, Yes{}, sc[1], A[cur], qf[1], acc[0][1], acc[1][1], va[cur ^ 1], bw[1], sc[0],
+              dpart[0], bw[0], none);
+        fixup(kb, 0, sc[0], dsave, dpart[0], bw[0]);
       }
     };
-    // three-deep pipeline over the stages (0 and 1 were issued at the start,
-    // after the readout's first two stages)
-    for (int st = 0; st < nstage; ++st) {
-      if (st + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
-      lds_barrier();
-      if (st + 2 < nstage) issue_i(st + 2, stage_buf((st + 2) % 3));
-      compute(st, stage_buf(st % 3));
+    auto rotate = [&]() __attribute__((always_inline)) {
+      const char* t = b0;
+      b0 = b1;
+      b1 = b2;
+      b2 = t;
+    };
+    step(integral_constant<int, 1>{}, 1);
+    step(integral_constant<int, 2>{}, 2);
+    step(integral_constant<int, 3>{}, 3);
+    rotate();
+    for (int st = 1; st < nstage; ++st) {
+      step(integral_constant<int, 0>{}, 4 * st);
+      step(integral_constant<int, 1>{}, 4 * st + 1);
+      step(integral_constant<int, 2>{}, 4 * st + 2);
+      step(integral_constant<int, 3>{}, 4 * st + 3);
+      rotate();
+    }
+    // finish the last block (kb = NB - 1, odd): P V of both tiles
+    {
+      const float dsave = dpart[1];
+      group(No{}, Yes{}, sc[0], A[0], qf[0], acc[0][0], acc[1][0], va[1], bw[0], sc[1], dpart[1],
+            bw[1], none);
+      fixup(NB - 1, 1, sc[1], dsave, dpart[1], bw[1]);
+    }
+    {
+      // no P left to compute: the VALU parts of this group redo P_0 of the
+      // last block into a scratch copy, which is discarded
+      float dd = 0.f;
+      uint32_t bx[8];
+      group(No{}, Yes{}, sc[1], A[0], qf[1], acc[0][1], acc[1][1], va[1], bw[1], sc[0], dd, bx,
+            none);
+      hold(bx[0]);
     }
     mfma_drain();   // the P V accumulators are moved by compiler code next
     lds_barrier();  // every wave is done with the intra buffers
