@@ -179,6 +179,51 @@ def bench_decode(kata, dev, hip):
     }
 
 
+def bench_quadratic(kata, dev, Ts=(4096, 16384, 32768), reps=5):
+    """Quadratic (flash-style) form against the chunked form at B=1, H=16,
+    d=dv=64 (bf16, seeded Gaussian inputs of the long-context recipe), kernel
+    time with torch events on the current stream.  MFMA work of the quadratic
+    form: the causal half of QK^T and P V, 2*(d+dv) flop per (query, key) pair
+    with key <= query."""
+    import torch
+    import workloads
+    rows = []
+    for T in Ts:
+        inp = workloads.make_inputs("long_bf16", B=1, H=16, T=T)
+        q = upload(inp["q_dev"], "bf16", dev)
+        k = upload(inp["k_dev"], "bf16", dev)
+        v = upload(inp["v_dev"], "bf16", dev)
+        out = torch.empty((1, 16, T, 64), dtype=torch.float32, device=dev)
+        wq = torch.empty(kata.quadratic_workspace_bytes(1, 16, T, 64, 64, kata.KATA_BF16),
+                         dtype=torch.uint8, device=dev)
+        wc = torch.empty(kata.workspace_bytes(1, 16, T, 64, 64, 64, kata.KATA_BF16, 0),
+                         dtype=torch.uint8, device=dev)
+        ms = {}
+        for name, fn in (("quadratic", lambda: kata.fwd_quadratic(q, k, v, out=out, workspace=wq)),
+                         ("chunked", lambda: kata.fwd_chunked(q, k, v, 64, out=out, workspace=wc))):
+            for _ in range(2):
+                fn()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms[name] = e0.elapsed_time(e1) / reps
+        flop = 16 * (T * (T + 1) / 2) * 2 * (64 + 64)
+        tf = flop / (ms["quadratic"] * 1e-3) / 1e12
+        rows.append({"T": T, "quadratic_ms": round(ms["quadratic"], 4),
+                     "chunked_ms": round(ms["chunked"], 4),
+                     "quadratic_tokens_per_s": T / (ms["quadratic"] * 1e-3),
+                     "chunked_tokens_per_s": T / (ms["chunked"] * 1e-3),
+                     "quadratic_mfma": {"achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
+                                        "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}})
+        del q, k, v, out, wq, wc
+    return {"config": "B1 H16 d64 dv64 bf16, C64 for the chunked form", "rows": rows}
+
+
 KERNELS = {"span_state": "span_state_kernel", "scan": "scan_exclusive_bf16",
            "span_output": "span_output_kernel"}
 COPY_BYTES = 1 << 30
@@ -244,6 +289,8 @@ def _per_dispatch(rows, counter, match):
     for r in rows:
         if r["Counter_Name"] != counter or match not in r["Kernel_Name"]:
             continue
+        if ", true>" in r["Kernel_Name"]:  # the quadratic form's output kernel
+            continue
         per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     return (sum(per.values()) / len(per), len(per)) if per else (None, 0)
 
@@ -292,6 +339,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-quadratic", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
     ap.add_argument("--ingest-traffic", metavar="DIR",
@@ -402,6 +450,8 @@ def main():
     if not args.no_decode:
         res["decode"] = bench_decode(kata, dev, hip)
         res["practical_hbm"] = hbm_ceiling(dev)
+    if not args.no_quadratic:
+        res["quadratic_vs_chunked"] = bench_quadratic(kata, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -110,6 +110,34 @@ KATA_API size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int
 KATA_API int kata_fwd_default_span(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype);
 
 /*
+ * The same causal KATA-M1 forward in the quadratic (flash-style) form: the
+ * O(T^2) definition above evaluated in 32x32 query-key blocks on chip
+ * (squared scores, causal mask, P V and the row sums), never forming a
+ * feature state (section "Synthetic induction and hardware microbenchmarks",
+ * paragraph "Kernel latency and throughput ratios": the quadratic operating
+ * point, preferable to the O(T) form at short T).  Same outputs as
+ * kata_fwd_chunked up to rounding.
+ *   Supported: dtype = KATA_BF16, d in {32, 64}, dv = 64 (bf16 MFMA);
+ *   other valid arguments give KATA_ERR_UNSUPPORTED.  B*H <= 65535.
+ *   workspace : device buffer of at least kata_fwd_quadratic_workspace_bytes(...)
+ *               bytes, 256-byte aligned, caller-owned (it receives a permuted
+ *               bf16 copy of V^T), contents undefined on exit.
+ * kata_fwd_quadratic allocates that workspace stream-ordered (hipMallocAsync /
+ * hipFreeAsync on `stream`).
+ */
+KATA_API kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, float* out,
+                                          int B, int H, int T, int d, int dv,
+                                          kata_dtype_t dtype, hipStream_t stream);
+KATA_API kata_status_t kata_fwd_quadratic_ws(const void* q, const void* k, const void* v,
+                                             float* out, int B, int H, int T, int d, int dv,
+                                             kata_dtype_t dtype, void* workspace,
+                                             size_t workspace_bytes, hipStream_t stream);
+/* Workspace bytes kata_fwd_quadratic_ws needs (0 when the arguments are
+ * invalid or unsupported). */
+KATA_API size_t kata_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv,
+                                                   kata_dtype_t dtype);
+
+/*
  * State after T tokens by the additive recurrence of eq. linatt:
  *   S = sum_{t<T} phi(k_t) v_t^T,  z = sum_{t<T} phi(k_t)   (packed layout above).
  * Overwrites S : [B][H][n][dv] and z : [B][H][n] (fp32).  Products k_a k_b and

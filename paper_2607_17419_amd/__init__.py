@@ -28,7 +28,8 @@ KATA_F32, KATA_BF16 = 0, 1
 # every symbol include/kata.h declares
 EXPORTED = (
     "kata_fwd_chunked", "kata_fwd_chunked_ws", "kata_fwd_chunked_timed", "kata_fwd_workspace_bytes",
-    "kata_fwd_default_span", "kata_prefill_state", "kata_decode_step",
+    "kata_fwd_default_span", "kata_fwd_quadratic", "kata_fwd_quadratic_ws",
+    "kata_fwd_quadratic_workspace_bytes", "kata_prefill_state", "kata_decode_step",
     "kata_status_string", "kata_abi_version",
 )
 
@@ -66,6 +67,12 @@ def lib():
     L.kata_prefill_state.restype = i
     L.kata_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, vp]
     L.kata_decode_step.restype = i
+    L.kata_fwd_quadratic.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp]
+    L.kata_fwd_quadratic.restype = i
+    L.kata_fwd_quadratic_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, vp, sz, vp]
+    L.kata_fwd_quadratic_ws.restype = i
+    L.kata_fwd_quadratic_workspace_bytes.argtypes = [i, i, i, i, i, i]
+    L.kata_fwd_quadratic_workspace_bytes.restype = sz
     L.kata_status_string.argtypes = [i]
     L.kata_status_string.restype = ctypes.c_char_p
     L.kata_abi_version.argtypes = []
@@ -188,6 +195,43 @@ def fwd_chunked_alloc(q, k, v, C: int, out=None, stream=None):
     _check(lib().kata_fwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                   B, H, T, d, dv, C, code, _stream(stream, q.device)),
            "kata_fwd_chunked")
+    return out
+
+
+def quadratic_workspace_bytes(B, H, T, d, dv, dtype_code) -> int:
+    return int(lib().kata_fwd_quadratic_workspace_bytes(B, H, T, d, dv, dtype_code))
+
+
+def fwd_quadratic(q, k, v, out=None, workspace=None, stream=None):
+    """Causal KATA-M1 forward in the quadratic form via kata_fwd_quadratic_ws;
+    returns out [B,H,T,dv] fp32.  The workspace (a torch uint8 device tensor)
+    is allocated here if not given."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = quadratic_workspace_bytes(B, H, T, d, dv, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_fwd_quadratic_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                       _dev(out, "out"), B, H, T, d, dv, code,
+                                       _dev(workspace, "workspace"), workspace.numel(),
+                                       _stream(stream, q.device)), "kata_fwd_quadratic_ws")
+    return out
+
+
+def fwd_quadratic_alloc(q, k, v, out=None, stream=None):
+    """Quadratic forward via kata_fwd_quadratic (library allocates its
+    workspace stream-ordered); returns out [B,H,T,dv] fp32."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_fwd_quadratic(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                    B, H, T, d, dv, code, _stream(stream, q.device)),
+           "kata_fwd_quadratic")
     return out
 
 

@@ -167,6 +167,50 @@ kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, floa
   return from_hip(fe);
 }
 
+// Quadratic form: bf16 MFMA path only.
+static kata_status_t quad_check(int B, int H, int T, int d, int dv, int dtype) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
+  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  if (dtype != KATA_BF16 || !kata::mfma_supported(d, dv, 64)) return KATA_ERR_UNSUPPORTED;
+  return KATA_OK;
+}
+
+size_t kata_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, kata_dtype_t dtype) {
+  if (quad_check(B, H, T, d, dv, dtype) != KATA_OK) return 0;
+  return kata::mfma_quadratic_workspace(B * H, T, dv);
+}
+
+kata_status_t kata_fwd_quadratic_ws(const void* q, const void* k, const void* v, float* out, int B,
+                                    int H, int T, int d, int dv, kata_dtype_t dtype,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const kata_status_t c = quad_check(B, H, T, d, dv, dtype);
+  if (c != KATA_OK) return c;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (workspace_bytes < kata::mfma_quadratic_workspace(B * H, T, dv)) return KATA_ERR_INVALID_ARG;
+  return from_hip(kata::launch_mfma_quadratic(q, k, v, out, B * H, T, d, dv, workspace, stream));
+}
+
+kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, float* out, int B,
+                                 int H, int T, int d, int dv, kata_dtype_t dtype,
+                                 hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const kata_status_t c = quad_check(B, H, T, d, dv, dtype);
+  if (c != KATA_OK) return c;
+  const size_t bytes = kata::mfma_quadratic_workspace(B * H, T, dv);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  const kata_status_t st =
+      kata_fwd_quadratic_ws(q, k, v, out, B, H, T, d, dv, dtype, ws, bytes, stream);
+  const hipError_t fe = hipFreeAsync(ws, stream);
+  if (st != KATA_OK) return st;
+  return from_hip(fe);
+}
+
 kata_status_t kata_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
                                  int T, int d, int dv, kata_dtype_t dtype, hipStream_t stream) {
   if (!k || !v || !S || !z) return KATA_ERR_INVALID_ARG;

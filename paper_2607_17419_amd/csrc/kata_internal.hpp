@@ -42,6 +42,9 @@ size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L);
 hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
                                int T, int d, int dv, int L, void* ws, hipStream_t st,
                                hipEvent_t* ev);
+size_t mfma_quadratic_workspace(int BH, int T, int dv);
+hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
+                                 int T, int d, int dv, void* ws, hipStream_t st);
 
 inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
   return ev ? hipEventRecord(ev[i], st) : hipSuccess;

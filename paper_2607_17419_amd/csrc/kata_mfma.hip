@@ -730,7 +730,7 @@ struct OutGrid {
   static constexpr int QB_TOKENS = 256;  // queries per workgroup
 };
 
-template <int D, int DV>
+template <int D, int DV, bool QUAD>
 __global__ __launch_bounds__(256) void span_output_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
@@ -760,7 +760,9 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   const int c = lane & 31, g = lane >> 5;
   const int id = blockIdx.x;
   const int jx = id >> 3;
-  const int qb = jx % QB;
+  // the quadratic form's query blocks differ in work by up to a factor QB:
+  // the longest go first
+  const int qb = QUAD ? QB - 1 - jx % QB : jx % QB;
   const int sp = sp0 + 8 * (jx / QB) + (id & 7);
   if (sp >= nsp) return;  // whole workgroup: padding of the grid
   const int s = sp % NS, bh = sp / NS;
@@ -770,7 +772,7 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   if (wg_q0 >= span_end) return;  // whole workgroup beyond the sequence
   const uint16_t* qh = q + static_cast<long long>(bh) * T * D;
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
-  const uint16_t* rec = pre + static_cast<long long>(sp) * G::E;
+  const uint16_t* rec = QUAD ? nullptr : pre + static_cast<long long>(sp) * G::E;
   const uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
 
   int tile[NQ];
@@ -796,13 +798,15 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   }
 
   // Z_pre operand fragments (see below)
-  const uint16_t* zop = rec + G::ES;
   bf16x8 zA[G::ZM][G::KZ];
+  if constexpr (!QUAD) {
+    const uint16_t* zop = rec + G::ES;
 #pragma unroll
-  for (int m = 0; m < G::ZM; ++m)
+    for (int m = 0; m < G::ZM; ++m)
 #pragma unroll
-    for (int kz = 0; kz < G::KZ; ++kz)
-      zA[m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * G::KZ + kz) * 64 + lane) * 8);
+      for (int kz = 0; kz < G::KZ; ++kz)
+        zA[m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * G::KZ + kz) * 64 + lane) * 8);
+  }
 
   // ---- staging copies of both phases ------------------------------------------
   // Stages cover the key blocks of the workgroup's last live tile; every
@@ -870,8 +874,10 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   // issued before them must not wait for them.  From here on the only vector
   // memory operations are copies (and the final stores).
   wait_vmcnt<0>();
-  issue_r(std::integral_constant<int, 0>{});
-  if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+  if constexpr (!QUAD) {
+    issue_r(std::integral_constant<int, 0>{});
+    if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+  }
   issue_i(0, g_stage0);
   if (nstage > 1) issue_i(1, g_stage1);
 
@@ -892,7 +898,10 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   float dpart[NQ];
 
   // ---- denominator from the prefix: q^T Z_pre q ------------------------------
-  {
+  if constexpr (QUAD) {
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) dpart[i] = 0.f;
+  } else {
     f32x16 az[G::ZM][NQ];
 #pragma unroll
     for (int m = 0; m < G::ZM; ++m)
@@ -1167,7 +1176,7 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   }
 
   // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
-  {
+  if constexpr (!QUAD) {
     // rotated fp32 query rows: qr[i][x] = q[t][(x + R*g) % D]; the lane's
     // own bf16 fragments hold x < R, the lane 32 away holds the rest
     float qr[NQ][D];
@@ -1308,6 +1317,49 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// V^T of a whole head for the quadratic form: vtp[bh][dv][LV] bf16, keys of
+// every 16-key group in the order 0-3, 8-11, 4-7, 12-15 (the key order of the
+// output kernel's P V product, as the state kernel writes it per span), keys
+// at or past T zero.  A workgroup transposes 64 keys through LDS.
+// grid (LV / 64, BH), block 256.
+// ---------------------------------------------------------------------------
+template <int DV>
+__global__ __launch_bounds__(256) void vt_permute_kernel(const uint16_t* __restrict__ v,
+                                                         uint16_t* __restrict__ vtp, int T,
+                                                         int LV) {
+  constexpr int KEYS = 64, CH = DV / 8;  // keys per workgroup, 16-byte chunks per V row
+  __shared__ uint32_t tile[KEYS][DV / 2 + 1];  // [key][dv pair], one word of padding
+  const int bh = blockIdx.y;
+  const long long key0 = static_cast<long long>(blockIdx.x) * KEYS;
+  const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
+  for (int i = threadIdx.x; i < KEYS * CH; i += 256) {
+    const int key = i / CH, ch = i % CH;
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (key0 + key < T) x = *reinterpret_cast<const uint4*>(vh + (key0 + key) * DV + 8 * ch);
+    tile[key][4 * ch + 0] = x.x;
+    tile[key][4 * ch + 1] = x.y;
+    tile[key][4 * ch + 2] = x.z;
+    tile[key][4 * ch + 3] = x.w;
+  }
+  __syncthreads();
+  uint16_t* out = vtp + static_cast<long long>(bh) * DV * LV;
+  for (int i = threadIdx.x; i < DV * (KEYS / 8); i += 256) {
+    const int m = i / (KEYS / 8), h = i % (KEYS / 8);  // dv row, output chunk of 8 keys
+    const int base = 16 * (h >> 1) + 4 * (h & 1);        // keys base+0..3, base+8..11
+    uint16_t e[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w0 = tile[base + j][m >> 1], w1 = tile[base + 8 + j][m >> 1];
+      e[j] = static_cast<uint16_t>((m & 1) ? (w0 >> 16) : w0);
+      e[4 + j] = static_cast<uint16_t>((m & 1) ? (w1 >> 16) : w1);
+    }
+    *reinterpret_cast<uint4*>(out + static_cast<long long>(m) * LV + key0 + 8 * h) =
+        make_uint4(e[0] | (static_cast<uint32_t>(e[1]) << 16), e[2] | (static_cast<uint32_t>(e[3]) << 16),
+                   e[4] | (static_cast<uint32_t>(e[5]) << 16), e[6] | (static_cast<uint32_t>(e[7]) << 16));
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
 bool mfma_supported(int d, int dv, int C) {
@@ -1366,11 +1418,46 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output_kernel<D, DV><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
-                                                   qblocks, sp0, sp0 + cnt);
+    span_output_kernel<D, DV, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA,
+                                                          NS, qblocks, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
+}
+
+// Quadratic form: one span per head covering the whole sequence, no state,
+// no scan, no prefix readout; the workspace holds the permuted V^T.
+size_t mfma_quadratic_workspace(int BH, int T, int dv) {
+  return align256(static_cast<size_t>(BH) * dv * span_alloc(T) * sizeof(uint16_t));
+}
+
+template <int D, int DV>
+static hipError_t run_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
+                                int T, void* ws, hipStream_t st) {
+  const int LA = span_alloc(T);
+  static_assert(kKB % 64 == 0, "the transpose writes whole 64-key groups");
+  uint16_t* vtp = static_cast<uint16_t*>(ws);
+  vt_permute_kernel<DV><<<dim3(static_cast<unsigned>(LA / 64), static_cast<unsigned>(BH)), 256, 0,
+                          st>>>(static_cast<const uint16_t*>(v), vtp, T, LA);
+  const int qblocks = (T + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
+  // 8 * qblocks * ceil(cnt / 8) workgroups per launch, below 2^31
+  int per = static_cast<int>((0x7fffffffLL / (8LL * qblocks)) * 8);
+  if (per > kSpansPerLaunch) per = kSpansPerLaunch;
+  for (int sp0 = 0; sp0 < BH; sp0 += per) {
+    const int cnt = BH - sp0 < per ? BH - sp0 : per;
+    const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
+    span_output_kernel<D, DV, true><<<nb4, 256, 0, st>>>(
+        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), nullptr, vtp, out, T, T,
+        LA, 1, qblocks, sp0, sp0 + cnt);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
+                                 int T, int d, int dv, void* ws, hipStream_t st) {
+  if (d == 64 && dv == 64) return run_quadratic<64, 64>(q, k, v, out, BH, T, ws, st);
+  if (d == 32 && dv == 64) return run_quadratic<32, 64>(q, k, v, out, BH, T, ws, st);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,

@@ -114,3 +114,31 @@ def test_decode_rejects_before_gpu(args, expect):
 ])
 def test_prefill_rejects_before_gpu(args, expect):
     assert kata.lib().kata_prefill_state(*args, NUL) == expect
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((NUL, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 1), 1),           # null q
+    ((FAKE, FAKE, FAKE, FAKE, 1, 0, 8, 64, 64, 1), 1),          # H < 1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 5), 1),          # bad dtype
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 0), 2),          # fp32: no quadratic path
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 64, 1), 2),          # d = 16
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 32, 1), 2),          # dv = 32
+    ((FAKE, FAKE, FAKE, FAKE, 256, 256, 8, 64, 64, 1), 2),      # B*H above the grid limit
+])
+def test_quadratic_rejects_before_gpu(args, expect):
+    assert kata.lib().kata_fwd_quadratic(*args, NUL) == expect
+
+
+def test_quadratic_workspace_host_logic():
+    L = kata.lib()
+    # one permuted bf16 V^T per head: dv rows of T rounded up to 128 keys
+    assert L.kata_fwd_quadratic_workspace_bytes(2, 3, 1000, 64, 64, 1) == 6 * 64 * 1024 * 2
+    assert L.kata_fwd_quadratic_workspace_bytes(1, 1, 1, 32, 64, 1) == 64 * 128 * 2
+    assert L.kata_fwd_quadratic_workspace_bytes(1, 1, 8, 64, 64, 0) == 0
+    need = L.kata_fwd_quadratic_workspace_bytes(1, 1, 128, 64, 64, 1)
+    st = L.kata_fwd_quadratic_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 1,
+                                 ctypes.c_void_p(0x100000), need - 1, NUL)
+    assert st == 1
+    st = L.kata_fwd_quadratic_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 1,
+                                 ctypes.c_void_p(0x100040), need, NUL)
+    assert st == 1
