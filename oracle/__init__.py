@@ -1,4 +1,5 @@
-"""CPU oracle for the causal KATA-M1 forward and decode step (test infrastructure).
+"""CPU oracle for the causal KATA-M1 forward and decode step, and for the
+block-diagonal KATA-Mg variant (test infrastructure).
 
 Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product library never does: it
@@ -61,6 +62,17 @@ def load(path: str | None = None):
     lib.kata_oracle_state.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L]
     lib.kata_oracle_decode_step.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp,
                                             _L, _L, _L, _L]
+    lib.kata_oracle_packed_dim_mg.restype = _L
+    lib.kata_oracle_packed_dim_mg.argtypes = [_L, _L]
+    lib.kata_oracle_phi_mg.argtypes = [_dp, _L, _L, ctypes.c_int, _dp]
+    lib.kata_oracle_fwd_mg.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L, _L]
+    lib.kata_oracle_fwd_mg_rows.argtypes = [_dp, _dp, _dp, _L, _L, _L, _L, _L, _L,
+                                            _lp, _lp, _L, _dp]
+    lib.kata_oracle_fwd_chunked_mg.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L,
+                                               _L, _L, _L, ctypes.c_int]
+    lib.kata_oracle_state_mg.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L, _L]
+    lib.kata_oracle_decode_step_mg.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp,
+                                               _L, _L, _L, _L, _L]
     if path is None:
         _lib = lib
     return lib
@@ -159,4 +171,72 @@ class Oracle:
         out = np.empty((B, H, dv))
         self.lib.kata_oracle_decode_step(self._p(S), self._p(z), self._p(q), self._p(k),
                                          self._p(v), self._p(out), B, H, d, dv)
+        return out, S, z
+
+    # ---- KATA-Mg (g blocks of d/g coordinates; g = 1 is KATA-M1) ----------
+
+    def packed_dim_mg(self, d: int, g: int) -> int:
+        return int(self.lib.kata_oracle_packed_dim_mg(d, g))
+
+    def phi_mg(self, x, g: int, weighted: bool = False):
+        x = self._f64(x)
+        d = x.shape[-1]
+        out = np.empty(self.packed_dim_mg(d, g))
+        self.lib.kata_oracle_phi_mg(self._p(x), d, g, int(weighted), self._p(out))
+        return out
+
+    def fwd_mg(self, q, k, v, g: int):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        assert d % g == 0
+        out = np.empty((B, H, T, dv))
+        self.lib.kata_oracle_fwd_mg(self._p(q), self._p(k), self._p(v), self._p(out),
+                                    B, H, T, d, dv, g)
+        return out
+
+    def fwd_mg_rows(self, q, k, v, g: int, bh_idx, t_idx):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        assert d % g == 0
+        bh = np.ascontiguousarray(np.asarray(bh_idx, dtype=np.int64))
+        tt = np.ascontiguousarray(np.asarray(t_idx, dtype=np.int64))
+        assert bh.shape == tt.shape and bh.ndim == 1
+        assert (bh >= 0).all() and (bh < B * H).all() and (tt >= 0).all() and (tt < T).all()
+        out = np.empty((bh.size, dv))
+        self.lib.kata_oracle_fwd_mg_rows(self._p(q), self._p(k), self._p(v), B, H, T, d, dv,
+                                         g, bh.ctypes.data_as(_lp), tt.ctypes.data_as(_lp),
+                                         bh.size, self._p(out))
+        return out
+
+    def fwd_chunked_mg(self, q, k, v, C: int, g: int, scan_mode: int = 1):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        assert d % g == 0
+        out = np.empty((B, H, T, dv))
+        self.lib.kata_oracle_fwd_chunked_mg(self._p(q), self._p(k), self._p(v), self._p(out),
+                                            B, H, T, d, dv, C, g, scan_mode)
+        return out
+
+    def state_mg(self, k, v, g: int):
+        k, v = self._f64(k), self._f64(v)
+        B, H, T, d = k.shape
+        dv = v.shape[-1]
+        n = self.packed_dim_mg(d, g)
+        S = np.empty((B, H, n, dv))
+        z = np.empty((B, H, n))
+        self.lib.kata_oracle_state_mg(self._p(k), self._p(v), self._p(S), self._p(z),
+                                      B, H, T, d, dv, g)
+        return S, z
+
+    def decode_step_mg(self, S, z, q, k, v, g: int):
+        S, z = self._f64(S).copy(), self._f64(z).copy()
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, d = q.shape
+        dv = v.shape[-1]
+        out = np.empty((B, H, dv))
+        self.lib.kata_oracle_decode_step_mg(self._p(S), self._p(z), self._p(q), self._p(k),
+                                            self._p(v), self._p(out), B, H, d, dv, g)
         return out, S, z

@@ -1,6 +1,8 @@
 /*
  * kata_oracle.c -- plain CPU oracle for the causal KATA-M1 attention forward
- * (rank-one PSD feature map phi(x) = vec(x x^T)) and its recurrent decode step.
+ * (rank-one PSD feature map phi(x) = vec(x x^T)) and its recurrent decode step,
+ * and for the block-diagonal KATA-Mg variant (one rank-one factor per block of
+ * d/g coordinates; g = 1 is M1).
  *
  * TEST INFRASTRUCTURE ONLY. Nothing in the product library links, loads,
  * imports or calls this file; only the test suite, the smoke check and the
@@ -316,6 +318,215 @@ EXPORT void kata_oracle_decode_step(double* S, double* z, const double* q,
     double* pq = (double*)malloc((size_t)n * sizeof(double));
     kata_oracle_phi(k + bh * d, d, 0, pk);
     kata_oracle_phi(q + bh * d, d, 1, pq);
+    const double* vt = v + bh * dv;
+    for (long f = 0; f < n; ++f) {
+      for (long j = 0; j < dv; ++j) Sh[f * dv + j] += pk[f] * vt[j];
+      zh[f] += pk[f];
+    }
+    double D = 0.0;
+    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];
+    for (long j = 0; j < dv; ++j) {
+      double acc = 0.0;
+      for (long f = 0; f < n; ++f) acc += pq[f] * Sh[f * dv + j];
+      out[bh * dv + j] = (D > 0.0) ? acc / D : 0.0;
+    }
+    free(pk);
+    free(pq);
+  }
+}
+
+/* ======================================================================
+ * KATA-Mg (section "From rank-one rays to low-rank PSD packing"): each
+ * projected query or key u in R^d is split into g blocks of m = d/g
+ * consecutive coordinates, u = (u_1, ..., u_g), and the feature keeps one
+ * rank-one PSD factor per block, psi_Mg(u) = (u_1 u_1^T, ..., u_g u_g^T), so
+ *     <psi_Mg(q), psi_Mg(k)> = sum_a (q_a . k_a)^2 .
+ * g = 1 is KATA-M1 above.  Packed layout: block a's m(m+1)/2 upper-triangle
+ * entries (row-major, as for M1 with d -> m) at offset a*m(m+1)/2; the
+ * feature width is n_g = g*m(m+1)/2 = d(d/g + 1)/2.
+ * ====================================================================== */
+
+EXPORT long kata_oracle_packed_dim_mg(long d, long g) {
+  long m = d / g;
+  return g * (m * (m + 1) / 2);
+}
+
+/* Blockwise packed lift: kata_oracle_phi applied to each block in turn
+ * (weighted = 1: weight 2 off each block's diagonal, the query side). */
+EXPORT void kata_oracle_phi_mg(const double* x, long d, long g, int weighted, double* out) {
+  long m = d / g, nm = m * (m + 1) / 2;
+  for (long a = 0; a < g; ++a) kata_oracle_phi(x + a * m, m, weighted, out + a * nm);
+}
+
+/* One output row of the definition with the KATA-Mg weight
+ *     w_i = sum_a (q_{t,a} . k_{i,a})^2,  i <= t,
+ *     o_t = sum_i w_i v_i / sum_i w_i  (0 when the sum is 0). */
+static void definition_row_mg(const double* q, const double* k, const double* v, long t,
+                              long d, long dv, long g, double* o) {
+  long m = d / g;
+  double D = 0.0;
+  for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  const double* qt = q + t * d;
+  for (long i = 0; i <= t; ++i) {
+    const double* ki = k + i * d;
+    double w = 0.0;
+    for (long a = 0; a < g; ++a) {
+      double s = 0.0;
+      for (long c = a * m; c < (a + 1) * m; ++c) s += qt[c] * ki[c];
+      w += s * s;
+    }
+    D += w;
+    const double* vi = v + i * dv;
+    for (long j = 0; j < dv; ++j) o[j] += w * vi[j];
+  }
+  if (D > 0.0) {
+    for (long j = 0; j < dv; ++j) o[j] /= D;
+  } else {
+    for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  }
+}
+
+EXPORT void kata_oracle_fwd_mg(const double* q, const double* k, const double* v, double* out,
+                               long B, long H, long T, long d, long dv, long g) {
+  long BH = B * H;
+#pragma omp parallel for collapse(2) schedule(dynamic, 16)
+  for (long bh = 0; bh < BH; ++bh)
+    for (long t = 0; t < T; ++t)
+      definition_row_mg(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t, d, dv, g,
+                        out + (bh * T + t) * dv);
+}
+
+EXPORT void kata_oracle_fwd_mg_rows(const double* q, const double* k, const double* v,
+                                    long B, long H, long T, long d, long dv, long g,
+                                    const long* bh_idx, const long* t_idx, long nrows,
+                                    double* out) {
+  (void)B; (void)H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long r = 0; r < nrows; ++r) {
+    long bh = bh_idx[r];
+    definition_row_mg(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t_idx[r], d, dv, g,
+                      out + r * dv);
+  }
+}
+
+/* Chunkwise KATA-Mg forward: kata_oracle_fwd_chunked with Psi = psi_Mg
+ * (same chunk states, exclusive prefix and chunk output; n = n_g). */
+EXPORT void kata_oracle_fwd_chunked_mg(const double* q, const double* k, const double* v,
+                                       double* out, long B, long H, long T, long d, long dv,
+                                       long C, long g, int scan_mode) {
+  long n = kata_oracle_packed_dim_mg(d, g);
+  long NC = (T + C - 1) / C;
+  long BH = B * H;
+  long SE = n * dv + n; /* one state record: S (n x dv) then Z (n) */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    const double* Q = q + bh * T * d;
+    const double* K = k + bh * T * d;
+    const double* V = v + bh * T * dv;
+    double* O = out + bh * T * dv;
+    double* Qc = (double*)calloc((size_t)(C * d), sizeof(double));
+    double* Kc = (double*)calloc((size_t)(C * d), sizeof(double));
+    double* Vc = (double*)calloc((size_t)(C * dv), sizeof(double));
+    double* PhiQ = (double*)malloc((size_t)(C * n) * sizeof(double));
+    double* PhiK = (double*)malloc((size_t)(C * n) * sizeof(double));
+    double* P = (double*)malloc((size_t)(C * C) * sizeof(double));
+    double* Nrow = (double*)malloc((size_t)dv * sizeof(double));
+    double* states = (double*)calloc((size_t)(NC * SE), sizeof(double));
+    for (long pass = 0; pass < 2; ++pass) {
+      for (long c = 0; c < NC; ++c) {
+        long t0 = c * C;
+        memset(Qc, 0, (size_t)(C * d) * sizeof(double));
+        memset(Kc, 0, (size_t)(C * d) * sizeof(double));
+        memset(Vc, 0, (size_t)(C * dv) * sizeof(double));
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          memcpy(Qc + r * d, Q + (t0 + r) * d, (size_t)d * sizeof(double));
+          memcpy(Kc + r * d, K + (t0 + r) * d, (size_t)d * sizeof(double));
+          memcpy(Vc + r * dv, V + (t0 + r) * dv, (size_t)dv * sizeof(double));
+        }
+        for (long r = 0; r < C; ++r) {
+          kata_oracle_phi_mg(Kc + r * d, d, g, 0, PhiK + r * n);
+          kata_oracle_phi_mg(Qc + r * d, d, g, 1, PhiQ + r * n);
+        }
+        double* St = states + c * SE;
+        if (pass == 0) {
+          for (long f = 0; f < n; ++f) {
+            for (long j = 0; j < dv; ++j) {
+              double s = 0.0;
+              for (long r = 0; r < C; ++r) s += PhiK[r * n + f] * Vc[r * dv + j];
+              St[f * dv + j] = s;
+            }
+            double zs = 0.0;
+            for (long r = 0; r < C; ++r) zs += PhiK[r * n + f];
+            St[n * dv + f] = zs;
+          }
+          continue;
+        }
+        for (long r = 0; r < C; ++r)
+          for (long s = 0; s < C; ++s) {
+            double a = 0.0;
+            for (long f = 0; f < n; ++f) a += PhiQ[r * n + f] * PhiK[s * n + f];
+            P[r * C + s] = (s <= r) ? a : 0.0;
+          }
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          double D = 0.0;
+          for (long f = 0; f < n; ++f) D += PhiQ[r * n + f] * St[n * dv + f];
+          for (long s = 0; s < C; ++s) D += P[r * C + s];
+          for (long j = 0; j < dv; ++j) {
+            double acc = 0.0;
+            for (long f = 0; f < n; ++f) acc += PhiQ[r * n + f] * St[f * dv + j];
+            for (long s = 0; s < C; ++s) acc += P[r * C + s] * Vc[s * dv + j];
+            Nrow[j] = acc;
+          }
+          for (long j = 0; j < dv; ++j) O[(t0 + r) * dv + j] = (D > 0.0) ? Nrow[j] / D : 0.0;
+        }
+      }
+      if (pass == 0) kata_oracle_scan_exclusive(states, NC, SE, scan_mode);
+    }
+    free(Qc); free(Kc); free(Vc); free(PhiQ); free(PhiK); free(P); free(Nrow);
+    free(states);
+  }
+}
+
+/* KATA-Mg state after T tokens (the additive recurrence of eq. linatt with
+ * psi_Mg): S : [B][H][n_g][dv], z : [B][H][n_g]. */
+EXPORT void kata_oracle_state_mg(const double* k, const double* v, double* S, double* z,
+                                 long B, long H, long T, long d, long dv, long g) {
+  long n = kata_oracle_packed_dim_mg(d, g);
+  long BH = B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    double* Sh = S + bh * n * dv;
+    double* zh = z + bh * n;
+    double* phi = (double*)malloc((size_t)n * sizeof(double));
+    memset(Sh, 0, (size_t)(n * dv) * sizeof(double));
+    memset(zh, 0, (size_t)n * sizeof(double));
+    for (long t = 0; t < T; ++t) {
+      kata_oracle_phi_mg(k + (bh * T + t) * d, d, g, 0, phi);
+      const double* vt = v + (bh * T + t) * dv;
+      for (long f = 0; f < n; ++f) {
+        for (long j = 0; j < dv; ++j) Sh[f * dv + j] += phi[f] * vt[j];
+        zh[f] += phi[f];
+      }
+    }
+    free(phi);
+  }
+}
+
+/* One KATA-Mg decode step (kata_oracle_decode_step with psi_Mg): update the
+ * state with the current token, then read out with the updated state. */
+EXPORT void kata_oracle_decode_step_mg(double* S, double* z, const double* q,
+                                       const double* k, const double* v, double* out,
+                                       long B, long H, long d, long dv, long g) {
+  long n = kata_oracle_packed_dim_mg(d, g);
+  long BH = B * H;
+#pragma omp parallel for schedule(static)
+  for (long bh = 0; bh < BH; ++bh) {
+    double* Sh = S + bh * n * dv;
+    double* zh = z + bh * n;
+    double* pk = (double*)malloc((size_t)n * sizeof(double));
+    double* pq = (double*)malloc((size_t)n * sizeof(double));
+    kata_oracle_phi_mg(k + bh * d, d, g, 0, pk);
+    kata_oracle_phi_mg(q + bh * d, d, g, 1, pq);
     const double* vt = v + bh * dv;
     for (long f = 0; f < n; ++f) {
       for (long j = 0; j < dv; ++j) Sh[f * dv + j] += pk[f] * vt[j];

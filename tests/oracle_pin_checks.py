@@ -332,6 +332,152 @@ def pin_rows_match_full(orc):
     assert np.array_equal(rows, full[bh, tt])
 
 
+# ---------------------------------------------------------------------------
+# PIN: KATA-Mg, the block-diagonal PSD feature (section "From rank-one rays to
+# low-rank PSD packing"): g blocks of m = d/g coordinates, weight
+# sum_a (q_a . k_a)^2; g = 1 is KATA-M1
+# ---------------------------------------------------------------------------
+
+def _brute_unpacked_mg(q, k, v, g):
+    """Forward with unpacked blockwise features, the concatenation over blocks
+    of vec(u_a u_a^T) in R^(g m^2); numpy only, a different route from the
+    oracle's per-block dot-product loop."""
+    B, H, T, d = q.shape
+    m = d // g
+    out = np.zeros(v.shape)
+    mask = np.tril(np.ones((T, T)))
+
+    def feats(x):
+        return np.concatenate([np.einsum("ta,tb->tab", x[:, a * m:(a + 1) * m],
+                                         x[:, a * m:(a + 1) * m]).reshape(T, m * m)
+                               for a in range(g)], axis=1)
+    for b in range(B):
+        for h in range(H):
+            P = (feats(q[b, h]) @ feats(k[b, h]).T) * mask
+            D = P.sum(axis=1, keepdims=True)
+            N = P @ v[b, h]
+            out[b, h] = np.where(D > 0, N / np.where(D > 0, D, 1.0), 0.0)
+    return out
+
+
+def pin_mg_widths(orc):
+    # State sizes printed in the MQAR table (tab:mqar) at d_h = 64: KATA-M1
+    # 266,240, KATA-M2 135,168, KATA-M4 69,632, each 2 x n_g x d_v (d_v = 64).
+    for g, dims in ((1, 266240), (2, 135168), (4, 69632)):
+        assert 2 * orc.packed_dim_mg(64, g) * 64 == dims
+    # the paper's closed form of the state size: g m(m+1)/2 = d(d/g + 1)/2
+    for d in (2, 4, 6, 8, 16, 32, 64):
+        for g in range(1, d + 1):
+            if d % g == 0:
+                assert orc.packed_dim_mg(d, g) == d * (d // g + 1) // 2
+    assert orc.packed_dim_mg(64, 1) == orc.packed_dim(64)
+
+
+def pin_mg_phi(orc):
+    rng = _rng(43)
+    # layout: block a's packed M1 lift at offset a m(m+1)/2
+    x = rng.standard_normal(12)
+    for g in (1, 2, 3, 4, 6, 12):
+        m = 12 // g
+        ref = np.concatenate([orc.phi(x[a * m:(a + 1) * m]) for a in range(g)])
+        assert np.array_equal(orc.phi_mg(x, g), ref)
+    # <psi_w(q), psi(k)> = sum_a (q_a . k_a)^2, against unpacked block outer products
+    for d, g in ((4, 2), (6, 3), (8, 2), (8, 4), (16, 2), (64, 2), (64, 4)):
+        m = d // g
+        for _ in range(4):
+            q = rng.standard_normal(d)
+            k = rng.standard_normal(d)
+            packed = float(orc.phi_mg(q, g, weighted=True) @ orc.phi_mg(k, g))
+            unpacked = sum(float(np.outer(q[a * m:(a + 1) * m], q[a * m:(a + 1) * m]).ravel()
+                                 @ np.outer(k[a * m:(a + 1) * m], k[a * m:(a + 1) * m]).ravel())
+                           for a in range(g))
+            ref = sum(float(q[a * m:(a + 1) * m] @ k[a * m:(a + 1) * m]) ** 2 for a in range(g))
+            scale = max(1.0, abs(ref))
+            assert abs(packed - ref) <= 1e-13 * scale
+            assert abs(unpacked - ref) <= 1e-13 * scale
+
+
+def pin_mg_brute_force(orc):
+    rng = _rng(47)
+    q, k, v = _rand_qkv(rng, 2, 2, 19, 8, 3, unit=False)
+    for g in (1, 2, 4, 8):
+        assert np.allclose(orc.fwd_mg(q, k, v, g), _brute_unpacked_mg(q, k, v, g),
+                           rtol=1e-11, atol=1e-12), g
+    assert np.array_equal(orc.fwd_mg(q, k, v, 1), orc.fwd(q, k, v))
+
+
+def pin_mg_special_cases(orc):
+    rng = _rng(53)
+    q, k, v = _rand_qkv(rng, 1, 2, 23, 8, 4, unit=False)
+    # only the first block of the queries non-zero: the weight is (q_1 . k_1)^2,
+    # i.e. KATA-M1 on the first block
+    q1 = q.copy()
+    q1[..., 4:] = 0.0
+    assert np.allclose(orc.fwd_mg(q1, k, v, 2), orc.fwd(q[..., :4], k[..., :4], v),
+                       rtol=1e-12, atol=1e-12)
+    # g = d (m = 1): w = sum_i q_i^2 k_i^2, linear attention with the feature x -> x*x
+    w = np.einsum("bhtd,bhsd->bhts", q * q, k * k) * np.tril(np.ones((23, 23)))
+    ref = np.einsum("bhts,bhsj->bhtj", w, v) / w.sum(axis=-1, keepdims=True)
+    assert np.allclose(orc.fwd_mg(q, k, v, 8), ref, rtol=1e-12, atol=1e-12)
+    # permuting the blocks of q and k together, and rotating inside each block
+    # (an isometry per block), leaves the output unchanged
+    o = orc.fwd_mg(q, k, v, 2)
+    perm = np.r_[4:8, 0:4]
+    assert np.allclose(orc.fwd_mg(q[..., perm], k[..., perm], v, 2), o, rtol=1e-12, atol=1e-12)
+    U1, _ = np.linalg.qr(rng.standard_normal((4, 4)))
+    U2, _ = np.linalg.qr(rng.standard_normal((4, 4)))
+    U = np.zeros((8, 8))
+    U[:4, :4], U[4:, 4:] = U1, U2
+    assert np.allclose(orc.fwd_mg(q @ U.T, k @ U.T, v, 2), o, rtol=1e-12, atol=1e-12)
+    # a rotation that mixes the blocks does change it (the feature is not M1's)
+    R, _ = np.linalg.qr(rng.standard_normal((8, 8)))
+    assert not np.allclose(orc.fwd_mg(q @ R.T, k @ R.T, v, 2), o, rtol=1e-6, atol=1e-6)
+    # convex combination of the values
+    lo = np.minimum.accumulate(v, axis=2)
+    hi = np.maximum.accumulate(v, axis=2)
+    assert np.all(o >= lo - 1e-12) and np.all(o <= hi + 1e-12)
+
+
+def pin_mg_chunked_equals_definition(orc):
+    rng = _rng(59)
+    q, k, v = _rand_qkv(rng, 1, 2, 33, 8, 3, unit=False)
+    for g in (1, 2, 4):
+        ref = orc.fwd_mg(q, k, v, g)
+        for C in (1, 3, 8, 16, 33, 40):
+            for mode in (0, 1):
+                got = orc.fwd_chunked_mg(q, k, v, C, g, mode)
+                assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), (g, C, mode)
+
+
+def pin_mg_decode_equals_forward(orc):
+    rng = _rng(61)
+    B, H, P, steps, d, dv = 2, 2, 9, 5, 8, 3
+    q, k, v = _rand_qkv(rng, B, H, P + steps, d, dv)
+    for g in (2, 4):
+        ref = orc.fwd_mg(q, k, v, g)
+        S, z = orc.state_mg(k[:, :, :P], v[:, :, :P], g)
+        for s in range(steps):
+            t = P + s
+            out, S, z = orc.decode_step_mg(S, z, q[:, :, t], k[:, :, t], v[:, :, t], g)
+            assert np.allclose(out, ref[:, :, t], rtol=1e-12, atol=1e-13)
+        S_all, z_all = orc.state_mg(k, v, g)
+        assert np.allclose(S, S_all, rtol=1e-12, atol=1e-12)
+        assert np.allclose(z, z_all, rtol=1e-12, atol=1e-12)
+    # g = 1 state is M1's
+    S1, z1 = orc.state_mg(k, v, 1)
+    S0, z0 = orc.state(k, v)
+    assert np.array_equal(S1, S0) and np.array_equal(z1, z0)
+
+
+def pin_mg_rows_match_full(orc):
+    rng = _rng(67)
+    q, k, v = _rand_qkv(rng, 2, 2, 17, 8, 5)
+    full = orc.fwd_mg(q, k, v, 2).reshape(4, 17, 5)
+    bh = rng.integers(0, 4, size=25)
+    tt = rng.integers(0, 17, size=25)
+    assert np.array_equal(orc.fwd_mg_rows(q, k, v, 2, bh, tt), full[bh, tt])
+
+
 ALL_PINS = [
     pin_packed_sizes, pin_packed_order, pin_phi_identity, pin_worked_example,
     pin_brute_force_unpacked, pin_convex_hull, pin_first_token, pin_gate_recursion,
@@ -339,4 +485,6 @@ ALL_PINS = [
     pin_orthonormal_keys_exact_recall, pin_weight_sample, pin_invariances,
     pin_chunked_equals_definition, pin_scan_equals_recurrence,
     pin_decode_equals_forward, pin_rows_match_full,
+    pin_mg_widths, pin_mg_phi, pin_mg_brute_force, pin_mg_special_cases,
+    pin_mg_chunked_equals_definition, pin_mg_decode_equals_forward, pin_mg_rows_match_full,
 ]

@@ -13,7 +13,8 @@ from oracle_pin_checks import ALL_PINS
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "kata_oracle.c")
 
-# (name, exact text in the oracle, replacement)
+# (name, exact text in the oracle, replacement[, which occurrence: 0 = the
+# first, in the KATA-M1 code; 1 = the second, in the KATA-Mg code after it])
 MUTANTS = [
     ("drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {"),
     ("abs_not_square", "double w = s * s;", "double w = fabs(s);"),
@@ -35,6 +36,24 @@ MUTANTS = [
      "    double D = -pq[0] * pk[0];\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];"),
     ("chunk_key_feature_weighted", "kata_oracle_phi(Kc + r * d, d, 0, PhiK + r * n);",
      "kata_oracle_phi(Kc + r * d, d, 1, PhiK + r * n);"),
+    # KATA-Mg
+    ("mg_full_dot", "for (long c = a * m; c < (a + 1) * m; ++c) s += qt[c] * ki[c];",
+     "for (long c = 0; c < d; ++c) s += qt[c] * ki[c];"),
+    ("mg_block_offset", "kata_oracle_phi(x + a * m, m, weighted, out + a * nm);",
+     "kata_oracle_phi(x, m, weighted, out + a * nm);"),
+    ("mg_width", "return g * (m * (m + 1) / 2);", "return g * (m * (m + 1) / 2) + 1;"),
+    ("mg_sum_not_squared", "w += s * s;", "w += s * fabs(s);"),
+    ("mg_drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {", 1),
+    ("mg_transposed_mask", "P[r * C + s] = (s <= r) ? a : 0.0;",
+     "P[r * C + s] = (s >= r) ? a : 0.0;", 1),
+    ("mg_chunk_query_unweighted", "kata_oracle_phi_mg(Qc + r * d, d, g, 1, PhiQ + r * n);",
+     "kata_oracle_phi_mg(Qc + r * d, d, g, 0, PhiQ + r * n);"),
+    ("mg_chunk_drops_intra_denominator", "for (long s = 0; s < C; ++s) D += P[r * C + s];", "", 1),
+    ("mg_state_value_index", "Sh[f * dv + j] += phi[f] * vt[j];",
+     "Sh[f * dv + j] += phi[f] * vt[0];", 1),
+    ("mg_decode_readout_before_update",
+     "    double D = 0.0;\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];",
+     "    double D = -pq[0] * pk[0];\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];", 1),
 ]
 
 
@@ -48,13 +67,24 @@ def _pins_that_fail(orc):
     return failed
 
 
-@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_mutant_is_caught(name, old, new, tmp_path):
+def _replace_nth(text, old, new, nth):
+    at = -1
+    for _ in range(nth + 1):
+        at = text.index(old, at + 1)
+    return text[:at] + new + text[at + len(old):]
+
+
+@pytest.mark.parametrize("mutant", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(mutant, tmp_path):
+    name, old, new = mutant[:3]
+    nth = mutant[3] if len(mutant) > 3 else 0
     with open(SRC) as f:
         text = f.read()
-    assert text.count(old) == 1, f"mutation site for {name} not found exactly once"
+    # the site must exist, and (for the first occurrence) be the KATA-M1 one
+    assert text.count(old) == nth + 1 or (nth == 0 and text.count(old) >= 1), \
+        f"mutation site {nth} for {name} not found"
     src = tmp_path / "mutant.c"
-    src.write_text(text.replace(old, new))
+    src.write_text(_replace_nth(text, old, new, nth))
     lib_path = str(tmp_path / "libmutant.so")
     oracle.build(str(src), lib_path)
     mut = oracle.Oracle(oracle.load(lib_path))
