@@ -1,6 +1,6 @@
 /*
  * kata.h -- C ABI of libkata: causal KATA-M1 attention (rank-one PSD feature
- * map) on AMD Instinct MI355X (gfx950).
+ * map), and its block-diagonal KATA-Mg variant, on AMD Instinct MI355X (gfx950).
  *
  * The operation.  For every head, with query q_t, key k_t in R^d and value v_t
  * in R^dv, the feature map is the rank-one PSD lift phi(x) = vec(x x^T)
@@ -162,6 +162,53 @@ KATA_API kata_status_t kata_prefill_state(const void* k, const void* v, float* S
 KATA_API kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k,
                                const void* v, float* out, int B, int H, int d, int dv,
                                kata_dtype_t dtype, hipStream_t stream);
+
+/*
+ * KATA-Mg, the block-diagonal PSD feature (section "From rank-one rays to
+ * low-rank PSD packing").  Each query and key is split into g blocks of
+ * m = d/g consecutive coordinates, u = (u_1, ..., u_g), and the feature keeps
+ * one rank-one factor per block, psi(u) = (u_1 u_1^T, ..., u_g u_g^T), so
+ *
+ *     o_t = sum_{i<=t} w_ti v_i / sum_{i<=t} w_ti,   w_ti = sum_a (q_{t,a} . k_{i,a})^2 .
+ *
+ * g = 1 is KATA-M1 (the calls above).  g >= 1 must divide d, else
+ * KATA_ERR_INVALID_ARG.  Packed state layout (prefill, decode): n = g*m(m+1)/2
+ * features; block a's pair (i, j), i <= j < m, at a*m(m+1)/2 + f_m(i, j)
+ * (the M1 order over m coordinates); S : [B][H][n][dv], z : [B][H][n].
+ * Forward fast path (bf16 MFMA): dtype = KATA_BF16, dv = 64, C a multiple of
+ * 32 up to 1024 and (d, g) in {(64, 1), (64, 2), (32, 1)}; other shapes with
+ * d <= 64, dv <= 256 and C <= 128 run on the fp32 path.  The quadratic form
+ * exists on the fast path only.  Arguments, workspace ownership, errors and
+ * asynchrony otherwise as for the M1 call of the same name.
+ */
+KATA_API kata_status_t kata_mg_fwd_chunked(const void* q, const void* k, const void* v,
+                                           float* out, int B, int H, int T, int d, int dv, int C,
+                                           int g, kata_dtype_t dtype, hipStream_t stream);
+KATA_API kata_status_t kata_mg_fwd_chunked_ws(const void* q, const void* k, const void* v,
+                                              float* out, int B, int H, int T, int d, int dv,
+                                              int C, int g, kata_dtype_t dtype, int span_chunks,
+                                              void* workspace, size_t workspace_bytes,
+                                              hipStream_t stream);
+KATA_API kata_status_t kata_mg_fwd_chunked_timed(const void* q, const void* k, const void* v,
+                                                 float* out, int B, int H, int T, int d, int dv,
+                                                 int C, int g, kata_dtype_t dtype,
+                                                 int span_chunks, void* workspace,
+                                                 size_t workspace_bytes,
+                                                 hipEvent_t* stage_events, hipStream_t stream);
+KATA_API size_t kata_mg_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
+                                            kata_dtype_t dtype, int span_chunks);
+KATA_API kata_status_t kata_mg_fwd_quadratic_ws(const void* q, const void* k, const void* v,
+                                                float* out, int B, int H, int T, int d, int dv,
+                                                int g, kata_dtype_t dtype, void* workspace,
+                                                size_t workspace_bytes, hipStream_t stream);
+KATA_API size_t kata_mg_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, int g,
+                                                      kata_dtype_t dtype);
+KATA_API kata_status_t kata_mg_prefill_state(const void* k, const void* v, float* S, float* z,
+                                             int B, int H, int T, int d, int dv, int g,
+                                             kata_dtype_t dtype, hipStream_t stream);
+KATA_API kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, const void* k,
+                                           const void* v, float* out, int B, int H, int d, int dv,
+                                           int g, kata_dtype_t dtype, hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 KATA_API const char* kata_status_string(kata_status_t s);

@@ -30,6 +30,9 @@ EXPORTED = (
     "kata_fwd_chunked", "kata_fwd_chunked_ws", "kata_fwd_chunked_timed", "kata_fwd_workspace_bytes",
     "kata_fwd_default_span", "kata_fwd_quadratic", "kata_fwd_quadratic_ws",
     "kata_fwd_quadratic_workspace_bytes", "kata_prefill_state", "kata_decode_step",
+    "kata_mg_fwd_chunked", "kata_mg_fwd_chunked_ws", "kata_mg_fwd_chunked_timed",
+    "kata_mg_fwd_workspace_bytes", "kata_mg_fwd_quadratic_ws",
+    "kata_mg_fwd_quadratic_workspace_bytes", "kata_mg_prefill_state", "kata_mg_decode_step",
     "kata_status_string", "kata_abi_version",
 )
 
@@ -73,6 +76,23 @@ def lib():
     L.kata_fwd_quadratic_ws.restype = i
     L.kata_fwd_quadratic_workspace_bytes.argtypes = [i, i, i, i, i, i]
     L.kata_fwd_quadratic_workspace_bytes.restype = sz
+    L.kata_mg_fwd_chunked.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    L.kata_mg_fwd_chunked.restype = i
+    L.kata_mg_fwd_chunked_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp, sz, vp]
+    L.kata_mg_fwd_chunked_ws.restype = i
+    L.kata_mg_fwd_chunked_timed.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, i, vp, sz,
+                                            vp, vp]
+    L.kata_mg_fwd_chunked_timed.restype = i
+    L.kata_mg_fwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i, i]
+    L.kata_mg_fwd_workspace_bytes.restype = sz
+    L.kata_mg_fwd_quadratic_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, vp, sz, vp]
+    L.kata_mg_fwd_quadratic_ws.restype = i
+    L.kata_mg_fwd_quadratic_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
+    L.kata_mg_fwd_quadratic_workspace_bytes.restype = sz
+    L.kata_mg_prefill_state.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+    L.kata_mg_prefill_state.restype = i
+    L.kata_mg_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp]
+    L.kata_mg_decode_step.restype = i
     L.kata_status_string.argtypes = [i]
     L.kata_status_string.restype = ctypes.c_char_p
     L.kata_abi_version.argtypes = []
@@ -267,4 +287,119 @@ def decode_step(S, z, q, k, v, out=None, stream=None):
     _check(lib().kata_decode_step(_dev(S, "S"), _dev(z, "z"), _dev(q, "q"), _dev(k, "k"),
                                   _dev(v, "v"), _dev(out, "out"), B, H, d, dv, _dtype_code(q),
                                   _stream(stream, q.device)), "kata_decode_step")
+    return out
+
+
+# ---- KATA-Mg (g feature blocks of d/g coordinates; g = 1 is KATA-M1) ------------
+
+def packed_dim_mg(d: int, g: int) -> int:
+    m = d // g
+    return g * (m * (m + 1) // 2)
+
+
+def mg_workspace_bytes(B, H, T, d, dv, C, g, dtype_code, span_chunks=0) -> int:
+    return int(lib().kata_mg_fwd_workspace_bytes(B, H, T, d, dv, C, g, dtype_code, span_chunks))
+
+
+def mg_fwd_chunked(q, k, v, C: int, g: int, span_chunks: int = 0, out=None, workspace=None,
+                   stream=None):
+    """Causal KATA-Mg forward via kata_mg_fwd_chunked_ws; returns out [B,H,T,dv] fp32."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = mg_workspace_bytes(B, H, T, d, dv, C, g, code, span_chunks)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_mg_fwd_chunked_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                        _dev(out, "out"), B, H, T, d, dv, C, g, code, span_chunks,
+                                        _dev(workspace, "workspace"), workspace.numel(),
+                                        _stream(stream, q.device)), "kata_mg_fwd_chunked_ws")
+    return out
+
+
+def mg_fwd_chunked_timed(q, k, v, C: int, g: int, events, span_chunks: int = 0, out=None,
+                         workspace=None, stream=None):
+    """mg_fwd_chunked that also records 4 caller-created HIP events around the
+    three stages on the launch stream."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = mg_workspace_bytes(B, H, T, d, dv, C, g, code, span_chunks)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_mg_fwd_chunked_timed(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                           _dev(out, "out"), B, H, T, d, dv, C, g, code,
+                                           span_chunks, _dev(workspace, "workspace"),
+                                           workspace.numel(), events, _stream(stream, q.device)),
+           "kata_mg_fwd_chunked_timed")
+    return out
+
+
+def mg_fwd_chunked_alloc(q, k, v, C: int, g: int, out=None, stream=None):
+    """KATA-Mg forward via kata_mg_fwd_chunked (stream-ordered library workspace)."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_mg_fwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                     B, H, T, d, dv, C, g, code, _stream(stream, q.device)),
+           "kata_mg_fwd_chunked")
+    return out
+
+
+def mg_fwd_quadratic(q, k, v, g: int, out=None, workspace=None, stream=None):
+    """KATA-Mg forward in the quadratic form via kata_mg_fwd_quadratic_ws."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = int(lib().kata_mg_fwd_quadratic_workspace_bytes(B, H, T, d, dv, g, code))
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_mg_fwd_quadratic_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                          _dev(out, "out"), B, H, T, d, dv, g, code,
+                                          _dev(workspace, "workspace"), workspace.numel(),
+                                          _stream(stream, q.device)), "kata_mg_fwd_quadratic_ws")
+    return out
+
+
+def mg_prefill_state(k, v, g: int, S=None, z=None, stream=None):
+    """KATA-Mg packed state after all T tokens: S [B,H,n_g,dv], z [B,H,n_g] (fp32)."""
+    import torch
+    if k.dim() != 4 or v.dim() != 4 or v.shape[:3] != k.shape[:3] or k.dtype != v.dtype:
+        raise ValueError("expected k [B,H,T,d] and v [B,H,T,dv] of one dtype")
+    B, H, T, d = k.shape
+    dv = v.shape[3]
+    n = packed_dim_mg(d, g)
+    if S is None:
+        S = torch.empty((B, H, n, dv), dtype=torch.float32, device=k.device)
+    if z is None:
+        z = torch.empty((B, H, n), dtype=torch.float32, device=k.device)
+    _check(lib().kata_mg_prefill_state(_dev(k, "k"), _dev(v, "v"), _dev(S, "S"), _dev(z, "z"),
+                                       B, H, T, d, dv, g, _dtype_code(k),
+                                       _stream(stream, k.device)), "kata_mg_prefill_state")
+    return S, z
+
+
+def mg_decode_step(S, z, q, k, v, g: int, out=None, stream=None):
+    """One KATA-Mg decode step (S, z updated in place) -> out [B,H,dv]."""
+    import torch
+    if q.dim() != 3 or k.shape != q.shape or v.dim() != 3 or v.shape[:2] != q.shape[:2]:
+        raise ValueError("expected q, k [B,H,d] and v [B,H,dv]")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k and v must share one dtype")
+    B, H, d = q.shape
+    dv = v.shape[2]
+    if out is None:
+        out = torch.empty((B, H, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_mg_decode_step(_dev(S, "S"), _dev(z, "z"), _dev(q, "q"), _dev(k, "k"),
+                                     _dev(v, "v"), _dev(out, "out"), B, H, d, dv, g,
+                                     _dtype_code(q), _stream(stream, q.device)),
+           "kata_mg_decode_step")
     return out

@@ -1,7 +1,8 @@
 // kata_api.hip -- host side of the libkata C ABI (include/kata.h): argument
 // validation, path selection (bf16 MFMA fast path or fp32 path), workspace
 // handling and error mapping.  Nothing here touches the GPU before the
-// arguments have been validated.
+// arguments have been validated.  Every entry point exists for KATA-M1 and,
+// with a feature-block count g (kata_mg_*), for KATA-Mg; g = 1 is M1.
 #include <climits>
 #include <cstdint>
 
@@ -27,19 +28,22 @@ bool product_ok(long long a, long long b, long long c, long long d) {
   return true;
 }
 
+bool blocks_ok(int d, int g) { return g >= 1 && d >= g && d % g == 0; }
+
 // Default span: about 1024 tokens of state per stored record on the MFMA path.
 int default_span(int C, Path path) {
   if (path != Path::kMfma) return 1;
-  int g = 1024 / C;
-  return g < 1 ? 1 : g;
+  int s = 1024 / C;
+  return s < 1 ? 1 : s;
 }
 
-Path fwd_path(int B, int H, int T, int d, int dv, int C, int dtype) {
+Path fwd_path(int B, int H, int T, int d, int dv, int C, int dtype, int g) {
   if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1 || C < 1) return Path::kInvalid;
   if (dtype != KATA_F32 && dtype != KATA_BF16) return Path::kInvalid;
+  if (!blocks_ok(d, g)) return Path::kInvalid;
   if (!product_ok(B, H, T, d > dv ? d : dv)) return Path::kInvalid;
   if (static_cast<long long>(B) * H > kGridYZ) return Path::kUnsupported;
-  if (dtype == KATA_BF16 && kata::mfma_supported(d, dv, C)) return Path::kMfma;
+  if (dtype == KATA_BF16 && kata::mfma_supported(d, dv, C, g)) return Path::kMfma;
   if (d > 64 || dv > 256 || C > 128) return Path::kUnsupported;
   if ((static_cast<long long>(T) + C - 1) / C > kGridYZ) return Path::kUnsupported;
   return Path::kFp32;
@@ -52,23 +56,161 @@ int span_tokens(int T, int C, int span_chunks) {
   return static_cast<int>(L);
 }
 
-size_t workspace_for(Path path, int B, int H, int T, int d, int dv, int C, int span_chunks) {
+size_t workspace_for(Path path, int B, int H, int T, int d, int dv, int C, int g,
+                     int span_chunks) {
   const int BH = B * H;
-  if (path == Path::kFp32) return kata::fp32_forward_workspace(BH, T, d, dv, C);
+  if (path == Path::kFp32) return kata::fp32_forward_workspace(BH, T, d, dv, C, g);
   if (path == Path::kMfma) {
     const int L = span_tokens(T, C, span_chunks);
-    return kata::mfma_forward_workspace(BH, T, d, dv, L);
+    return kata::mfma_forward_workspace(BH, T, d, dv, L, g);
   }
   return 0;
 }
 
 kata_status_t from_hip(hipError_t e) { return e == hipSuccess ? KATA_OK : KATA_ERR_HIP; }
 
+int default_span_of(int B, int H, int T, int d, int dv, int C, int dtype, int g) {
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
+  if (p == Path::kInvalid || p == Path::kUnsupported) return 0;
+  return default_span(C, p);
+}
+
+size_t fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int dtype, int g,
+                           int span_chunks) {
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
+  if (p == Path::kInvalid || p == Path::kUnsupported || span_chunks < 0) return 0;
+  if (span_chunks == 0) span_chunks = default_span(C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  return workspace_for(p, B, H, T, d, dv, C, g, span_chunks);
+}
+
+kata_status_t fwd_ws(const void* q, const void* k, const void* v, float* out, int B, int H,
+                     int T, int d, int dv, int C, int g, kata_dtype_t dtype, int span_chunks,
+                     void* workspace, size_t workspace_bytes, hipEvent_t* ev,
+                     hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  if (span_chunks < 0) return KATA_ERR_INVALID_ARG;
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (span_chunks == 0) span_chunks = default_span(C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  const size_t need = workspace_for(p, B, H, T, d, dv, C, g, span_chunks);
+  if (workspace_bytes < need) return KATA_ERR_INVALID_ARG;
+  const int BH = B * H;
+  if (p == Path::kMfma) {
+    const int L = span_tokens(T, C, span_chunks);
+    if ((static_cast<long long>(T) + L - 1) / L > kGridYZ) return KATA_ERR_UNSUPPORTED;
+    return from_hip(
+        kata::launch_mfma_forward(q, k, v, out, BH, T, d, dv, g, L, workspace, stream, ev));
+  }
+  if (dtype == KATA_F32)
+    return from_hip(kata::launch_fp32_forward<float>(q, k, v, out, BH, T, d, dv, C, g, workspace,
+                                                     stream, ev));
+  return from_hip(kata::launch_fp32_forward<kata::bf16_t>(q, k, v, out, BH, T, d, dv, C, g,
+                                                          workspace, stream, ev));
+}
+
+kata_status_t fwd_timed(const void* q, const void* k, const void* v, float* out, int B, int H,
+                        int T, int d, int dv, int C, int g, kata_dtype_t dtype, int span_chunks,
+                        void* workspace, size_t workspace_bytes, hipEvent_t* stage_events,
+                        hipStream_t stream) {
+  if (!stage_events) return KATA_ERR_INVALID_ARG;
+  for (int i = 0; i < 4; ++i)
+    if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span_chunks, workspace,
+                workspace_bytes, stage_events, stream);
+}
+
+kata_status_t fwd_alloc(const void* q, const void* k, const void* v, float* out, int B, int H,
+                        int T, int d, int dv, int C, int g, kata_dtype_t dtype,
+                        hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  const int span = (p == Path::kFp32) ? 1 : default_span(C, p);
+  const size_t bytes = workspace_for(p, B, H, T, d, dv, C, g, span);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  const kata_status_t st =
+      fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span, ws, bytes, nullptr, stream);
+  const hipError_t fe = hipFreeAsync(ws, stream);
+  if (st != KATA_OK) return st;
+  return from_hip(fe);
+}
+
+// Quadratic form: bf16 MFMA path only.
+kata_status_t quad_check(int B, int H, int T, int d, int dv, int dtype, int g) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!blocks_ok(d, g)) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
+  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  if (dtype != KATA_BF16 || !kata::mfma_supported(d, dv, 64, g)) return KATA_ERR_UNSUPPORTED;
+  return KATA_OK;
+}
+
+size_t quad_workspace_bytes(int B, int H, int T, int d, int dv, int dtype, int g) {
+  if (quad_check(B, H, T, d, dv, dtype, g) != KATA_OK) return 0;
+  return kata::mfma_quadratic_workspace(B * H, T, dv);
+}
+
+kata_status_t quad_ws(const void* q, const void* k, const void* v, float* out, int B, int H,
+                      int T, int d, int dv, int g, kata_dtype_t dtype, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const kata_status_t c = quad_check(B, H, T, d, dv, dtype, g);
+  if (c != KATA_OK) return c;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (workspace_bytes < kata::mfma_quadratic_workspace(B * H, T, dv)) return KATA_ERR_INVALID_ARG;
+  return from_hip(
+      kata::launch_mfma_quadratic(q, k, v, out, B * H, T, d, dv, g, workspace, stream));
+}
+
+kata_status_t prefill(const void* k, const void* v, float* S, float* z, int B, int H, int T,
+                      int d, int dv, int g, kata_dtype_t dtype, hipStream_t stream) {
+  if (!k || !v || !S || !z) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(S) || !aligned16(z)) return KATA_ERR_INVALID_ARG;
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!blocks_ok(d, g)) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
+  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
+  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  const int BH = B * H;
+  if (dtype == KATA_F32)
+    return from_hip(kata::launch_prefill<float>(k, v, S, z, BH, T, d, dv, g, stream));
+  return from_hip(kata::launch_prefill<kata::bf16_t>(k, v, S, z, BH, T, d, dv, g, stream));
+}
+
+kata_status_t decode(float* S, float* z, const void* q, const void* k, const void* v, float* out,
+                     int B, int H, int d, int dv, int g, kata_dtype_t dtype, hipStream_t stream) {
+  if (!S || !z || !q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(S) || !aligned16(z) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
+      !aligned16(out))
+    return KATA_ERR_INVALID_ARG;
+  if (B < 1 || H < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!blocks_ok(d, g)) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, d * (d + 1) / 2, dv)) return KATA_ERR_INVALID_ARG;
+  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
+  if (static_cast<long long>(B) * H > INT_MAX) return KATA_ERR_UNSUPPORTED;
+  const int BH = B * H;
+  if (dtype == KATA_F32)
+    return from_hip(kata::launch_decode<float>(S, z, q, k, v, out, BH, d, dv, g, stream));
+  return from_hip(kata::launch_decode<kata::bf16_t>(S, z, q, k, v, out, BH, d, dv, g, stream));
+}
+
 }  // namespace
 
 extern "C" {
 
-int kata_abi_version(void) { return 100; }
+int kata_abi_version(void) { return 101; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (s) {
@@ -80,60 +222,23 @@ const char* kata_status_string(kata_status_t s) {
   return "KATA_UNKNOWN_STATUS";
 }
 
+// ---- KATA-M1 ----------------------------------------------------------------
+
 int kata_fwd_default_span(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype) {
-  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
-  if (p == Path::kInvalid || p == Path::kUnsupported) return 0;
-  return default_span(C, p);
+  return default_span_of(B, H, T, d, dv, C, dtype, 1);
 }
 
 size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                 int span_chunks) {
-  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
-  if (p == Path::kInvalid || p == Path::kUnsupported || span_chunks < 0) return 0;
-  if (span_chunks == 0) span_chunks = default_span(C, p);
-  if (p == Path::kFp32) span_chunks = 1;
-  return workspace_for(p, B, H, T, d, dv, C, span_chunks);
+  return fwd_workspace_bytes(B, H, T, d, dv, C, dtype, 1, span_chunks);
 }
-
-}  // extern "C"
-
-static kata_status_t fwd_ws(const void* q, const void* k, const void* v, float* out, int B,
-                            int H, int T, int d, int dv, int C, kata_dtype_t dtype,
-                            int span_chunks, void* workspace, size_t workspace_bytes,
-                            hipEvent_t* ev, hipStream_t stream) {
-  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
-  if (span_chunks < 0) return KATA_ERR_INVALID_ARG;
-  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
-  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
-  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
-  if (span_chunks == 0) span_chunks = default_span(C, p);
-  if (p == Path::kFp32) span_chunks = 1;
-  const size_t need = workspace_for(p, B, H, T, d, dv, C, span_chunks);
-  if (workspace_bytes < need) return KATA_ERR_INVALID_ARG;
-  const int BH = B * H;
-  if (p == Path::kMfma) {
-    const int L = span_tokens(T, C, span_chunks);
-    if ((static_cast<long long>(T) + L - 1) / L > kGridYZ) return KATA_ERR_UNSUPPORTED;
-    return from_hip(
-        kata::launch_mfma_forward(q, k, v, out, BH, T, d, dv, L, workspace, stream, ev));
-  }
-  if (dtype == KATA_F32)
-    return from_hip(
-        kata::launch_fp32_forward<float>(q, k, v, out, BH, T, d, dv, C, workspace, stream, ev));
-  return from_hip(kata::launch_fp32_forward<kata::bf16_t>(q, k, v, out, BH, T, d, dv, C,
-                                                          workspace, stream, ev));
-}
-
-extern "C" {
 
 kata_status_t kata_fwd_chunked_ws(const void* q, const void* k, const void* v, float* out, int B,
                                   int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                   int span_chunks, void* workspace, size_t workspace_bytes,
                                   hipStream_t stream) {
-  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span_chunks, workspace, workspace_bytes,
-                nullptr, stream);
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
+                workspace_bytes, nullptr, stream);
 }
 
 kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v, float* out,
@@ -141,57 +246,24 @@ kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v
                                      kata_dtype_t dtype, int span_chunks, void* workspace,
                                      size_t workspace_bytes, hipEvent_t* stage_events,
                                      hipStream_t stream) {
-  if (!stage_events) return KATA_ERR_INVALID_ARG;
-  for (int i = 0; i < 4; ++i)
-    if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
-  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span_chunks, workspace, workspace_bytes,
-                stage_events, stream);
+  return fwd_timed(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
+                   workspace_bytes, stage_events, stream);
 }
 
 kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
                                int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                hipStream_t stream) {
-  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
-  const Path p = fwd_path(B, H, T, d, dv, C, dtype);
-  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
-  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
-  const int span = (p == Path::kFp32) ? 1 : default_span(C, p);
-  const size_t bytes = workspace_for(p, B, H, T, d, dv, C, span);
-  void* ws = nullptr;
-  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
-  const kata_status_t st =
-      fwd_ws(q, k, v, out, B, H, T, d, dv, C, dtype, span, ws, bytes, nullptr, stream);
-  const hipError_t fe = hipFreeAsync(ws, stream);
-  if (st != KATA_OK) return st;
-  return from_hip(fe);
-}
-
-// Quadratic form: bf16 MFMA path only.
-static kata_status_t quad_check(int B, int H, int T, int d, int dv, int dtype) {
-  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
-  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
-  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
-  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
-  if (dtype != KATA_BF16 || !kata::mfma_supported(d, dv, 64)) return KATA_ERR_UNSUPPORTED;
-  return KATA_OK;
+  return fwd_alloc(q, k, v, out, B, H, T, d, dv, C, 1, dtype, stream);
 }
 
 size_t kata_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, kata_dtype_t dtype) {
-  if (quad_check(B, H, T, d, dv, dtype) != KATA_OK) return 0;
-  return kata::mfma_quadratic_workspace(B * H, T, dv);
+  return quad_workspace_bytes(B, H, T, d, dv, dtype, 1);
 }
 
 kata_status_t kata_fwd_quadratic_ws(const void* q, const void* k, const void* v, float* out, int B,
                                     int H, int T, int d, int dv, kata_dtype_t dtype,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
-  const kata_status_t c = quad_check(B, H, T, d, dv, dtype);
-  if (c != KATA_OK) return c;
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
-  if (workspace_bytes < kata::mfma_quadratic_workspace(B * H, T, dv)) return KATA_ERR_INVALID_ARG;
-  return from_hip(kata::launch_mfma_quadratic(q, k, v, out, B * H, T, d, dv, workspace, stream));
+  return quad_ws(q, k, v, out, B, H, T, d, dv, 1, dtype, workspace, workspace_bytes, stream);
 }
 
 kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, float* out, int B,
@@ -199,13 +271,12 @@ kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, fl
                                  hipStream_t stream) {
   if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
-  const kata_status_t c = quad_check(B, H, T, d, dv, dtype);
+  const kata_status_t c = quad_check(B, H, T, d, dv, dtype, 1);
   if (c != KATA_OK) return c;
   const size_t bytes = kata::mfma_quadratic_workspace(B * H, T, dv);
   void* ws = nullptr;
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
-  const kata_status_t st =
-      kata_fwd_quadratic_ws(q, k, v, out, B, H, T, d, dv, dtype, ws, bytes, stream);
+  const kata_status_t st = quad_ws(q, k, v, out, B, H, T, d, dv, 1, dtype, ws, bytes, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);
   if (st != KATA_OK) return st;
   return from_hip(fe);
@@ -213,33 +284,67 @@ kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, fl
 
 kata_status_t kata_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
                                  int T, int d, int dv, kata_dtype_t dtype, hipStream_t stream) {
-  if (!k || !v || !S || !z) return KATA_ERR_INVALID_ARG;
-  if (!aligned16(k) || !aligned16(v) || !aligned16(S) || !aligned16(z)) return KATA_ERR_INVALID_ARG;
-  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
-  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
-  if (!product_ok(B, H, T, d > dv ? d : dv)) return KATA_ERR_INVALID_ARG;
-  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
-  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
-  const int BH = B * H;
-  if (dtype == KATA_F32) return from_hip(kata::launch_prefill<float>(k, v, S, z, BH, T, d, dv, stream));
-  return from_hip(kata::launch_prefill<kata::bf16_t>(k, v, S, z, BH, T, d, dv, stream));
+  return prefill(k, v, S, z, B, H, T, d, dv, 1, dtype, stream);
 }
 
 kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k, const void* v,
                                float* out, int B, int H, int d, int dv, kata_dtype_t dtype,
                                hipStream_t stream) {
-  if (!S || !z || !q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
-  if (!aligned16(S) || !aligned16(z) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
-      !aligned16(out))
-    return KATA_ERR_INVALID_ARG;
-  if (B < 1 || H < 1 || d < 1 || dv < 1) return KATA_ERR_INVALID_ARG;
-  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
-  if (!product_ok(B, H, d * (d + 1) / 2, dv)) return KATA_ERR_INVALID_ARG;
-  if (d > 64 || dv > 256) return KATA_ERR_UNSUPPORTED;
-  if (static_cast<long long>(B) * H > INT_MAX) return KATA_ERR_UNSUPPORTED;
-  const int BH = B * H;
-  if (dtype == KATA_F32) return from_hip(kata::launch_decode<float>(S, z, q, k, v, out, BH, d, dv, stream));
-  return from_hip(kata::launch_decode<kata::bf16_t>(S, z, q, k, v, out, BH, d, dv, stream));
+  return decode(S, z, q, k, v, out, B, H, d, dv, 1, dtype, stream);
+}
+
+// ---- KATA-Mg -----------------------------------------------------------------
+
+size_t kata_mg_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
+                                   kata_dtype_t dtype, int span_chunks) {
+  return fwd_workspace_bytes(B, H, T, d, dv, C, dtype, g, span_chunks);
+}
+
+kata_status_t kata_mg_fwd_chunked_ws(const void* q, const void* k, const void* v, float* out,
+                                     int B, int H, int T, int d, int dv, int C, int g,
+                                     kata_dtype_t dtype, int span_chunks, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span_chunks, workspace,
+                workspace_bytes, nullptr, stream);
+}
+
+kata_status_t kata_mg_fwd_chunked_timed(const void* q, const void* k, const void* v, float* out,
+                                        int B, int H, int T, int d, int dv, int C, int g,
+                                        kata_dtype_t dtype, int span_chunks, void* workspace,
+                                        size_t workspace_bytes, hipEvent_t* stage_events,
+                                        hipStream_t stream) {
+  return fwd_timed(q, k, v, out, B, H, T, d, dv, C, g, dtype, span_chunks, workspace,
+                   workspace_bytes, stage_events, stream);
+}
+
+kata_status_t kata_mg_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
+                                  int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
+                                  hipStream_t stream) {
+  return fwd_alloc(q, k, v, out, B, H, T, d, dv, C, g, dtype, stream);
+}
+
+size_t kata_mg_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, int g,
+                                             kata_dtype_t dtype) {
+  return quad_workspace_bytes(B, H, T, d, dv, dtype, g);
+}
+
+kata_status_t kata_mg_fwd_quadratic_ws(const void* q, const void* k, const void* v, float* out,
+                                       int B, int H, int T, int d, int dv, int g,
+                                       kata_dtype_t dtype, void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
+  return quad_ws(q, k, v, out, B, H, T, d, dv, g, dtype, workspace, workspace_bytes, stream);
+}
+
+kata_status_t kata_mg_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
+                                    int T, int d, int dv, int g, kata_dtype_t dtype,
+                                    hipStream_t stream) {
+  return prefill(k, v, S, z, B, H, T, d, dv, g, dtype, stream);
+}
+
+kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, const void* k, const void* v,
+                                  float* out, int B, int H, int d, int dv, int g,
+                                  kata_dtype_t dtype, hipStream_t stream) {
+  return decode(S, z, q, k, v, out, B, H, d, dv, g, dtype, stream);
 }
 
 }  // extern "C"

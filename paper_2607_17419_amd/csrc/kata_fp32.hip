@@ -4,6 +4,11 @@
 // chunk states that both forward paths use.
 //
 // Feature layout: packed row-major upper triangle, f(a, b) = a*d - a(a-1)/2 + b - a.
+// With g > 1 feature blocks (KATA-Mg, section "From rank-one rays to low-rank
+// PSD packing": one rank-one factor per block of m = d/g coordinates) the
+// features of block i are the pairs of coordinates inside it, packed the same
+// way over m, at offset i*m(m+1)/2; n = g*m(m+1)/2, and the score of a
+// (query, key) pair is sum_i (q_i . k_i)^2.  g = 1 is KATA-M1.
 // A chunk-state record is S[f][j] (n x dv) followed by z[f] (n), fp32.
 #include "kata_common.hpp"
 #include "kata_internal.hpp"
@@ -12,9 +17,24 @@
 namespace kata {
 
 // Pair table for packed features: entry f holds (a, b) in the low/high byte.
-__device__ __forceinline__ void build_pair_table(uint16_t* tab, int d) {
-  for (int a = threadIdx.x; a < d; a += blockDim.x)
-    for (int b = a; b < d; ++b) tab[packed_index(a, b, d)] = static_cast<uint16_t>(a | (b << 8));
+__device__ __forceinline__ void build_pair_table(uint16_t* tab, int d, int g) {
+  const int m = d / g, nm = m * (m + 1) / 2;
+  for (int x = threadIdx.x; x < d; x += blockDim.x) {
+    const int blk = x / m, a = x % m;
+    for (int b = a; b < m; ++b)
+      tab[blk * nm + packed_index(a, b, m)] =
+          static_cast<uint16_t>((blk * m + a) | ((blk * m + b) << 8));
+  }
+}
+
+// The pair (a, b) of feature f (one thread's lookup, no table).
+__device__ __forceinline__ uint16_t pair_of(int f, int d, int g) {
+  const int m = d / g, nm = m * (m + 1) / 2;
+  const int blk = f / nm, fl = f % nm;
+  int a = 0;
+  while (a + 1 < m && packed_index(a + 1, a + 1, m) <= fl) ++a;
+  const int b = a + (fl - packed_index(a, a, m));
+  return static_cast<uint16_t>((blk * m + a) | ((blk * m + b) << 8));
 }
 
 // ---------------------------------------------------------------------------
@@ -29,21 +49,17 @@ constexpr int kTB = 32;   // tokens staged per pass
 template <typename Tin>
 __global__ __launch_bounds__(256) void chunk_state_f32(
     const Tin* __restrict__ k, const Tin* __restrict__ v, float* __restrict__ S_out,
-    float* __restrict__ z_out, int T, int d, int dv, int C, long long S_bh_stride,
+    float* __restrict__ z_out, int T, int d, int dv, int C, int g, long long S_bh_stride,
     long long S_chunk_stride, long long z_bh_stride, long long z_chunk_stride) {
   __shared__ float ks[kTB][65];
   __shared__ float vs[kTB][257];
   __shared__ uint16_t pairs[kFB];
-  const int n = d * (d + 1) / 2;
+  const int n = g * ((d / g) * (d / g + 1) / 2);
   const int f0 = blockIdx.x * kFB;
   const int c = blockIdx.y;
   const int bh = blockIdx.z;
   const int tid = threadIdx.x;
-  if (tid < kFB && f0 + tid < n) {
-    int f = f0 + tid, a = 0;
-    while (packed_index(a + 1, a + 1, d) <= f && a + 1 < d) ++a;
-    pairs[tid] = static_cast<uint16_t>(a | ((a + (f - packed_index(a, a, d))) << 8));
-  }
+  if (tid < kFB && f0 + tid < n) pairs[tid] = pair_of(f0 + tid, d, g);
   const int nf = min(kFB, n - f0);
   const int nout = nf * dv;
   constexpr int R = (kFB * 256) / 256;  // at most 16 outputs per thread
@@ -95,7 +111,8 @@ __global__ __launch_bounds__(256) void chunk_state_f32(
 
 // ---------------------------------------------------------------------------
 // Chunk output (eq. chunk-out): for chunk c of head bh,
-//   P[r][s] = (q_r . k_s)^2 for s <= r (lower-triangular mask incl. diagonal),
+//   P[r][s] = sum_i (q_{r,i} . k_{s,i})^2 over the g blocks, for s <= r
+//   (lower-triangular mask incl. diagonal),
 //   N = Phi_w(Q_c) S_pre + P V_c,  D = Phi_w(Q_c) z_pre + P 1,  O = N / D (0 if D = 0),
 // Phi_w the query-side packed feature (weight 2 off the diagonal).
 // grid (NC, BH), block 256; C <= 128, d <= 64.
@@ -103,10 +120,11 @@ __global__ __launch_bounds__(256) void chunk_state_f32(
 template <typename Tin>
 __global__ __launch_bounds__(256) void chunk_out_f32(
     const Tin* __restrict__ q, const Tin* __restrict__ k, const Tin* __restrict__ v,
-    const float* __restrict__ pre, float* __restrict__ out, int T, int d, int dv, int C,
+    const float* __restrict__ pre, float* __restrict__ out, int T, int d, int dv, int C, int g,
     long long bh_stride, long long chunk_stride) {
   extern __shared__ float smem[];
-  const int n = d * (d + 1) / 2;
+  const int m = d / g;
+  const int n = g * (m * (m + 1) / 2);
   float* qs = smem;                 // [C][d]
   float* ks = qs + C * d;           // [C][d]
   float* P = ks + C * d;            // [C][C]
@@ -120,7 +138,7 @@ __global__ __launch_bounds__(256) void chunk_out_f32(
   const Tin* qh = q + static_cast<long long>(bh) * T * d;
   const Tin* kh = k + static_cast<long long>(bh) * T * d;
   const Tin* vh = v + static_cast<long long>(bh) * T * dv;
-  build_pair_table(pairs, d);
+  build_pair_table(pairs, d, g);
   for (int i = tid; i < C * d; i += 256) {
     int r = i / d, a = i % d;
     qs[i] = (r < nt) ? load_f32(qh, (t0 + r) * d + a) : 0.f;
@@ -129,10 +147,14 @@ __global__ __launch_bounds__(256) void chunk_out_f32(
   __syncthreads();
   for (int i = tid; i < C * C; i += 256) {
     int r = i / C, s = i % C;
-    float a = 0.f;
+    float p = 0.f;
     if (s <= r)
-      for (int x = 0; x < d; ++x) a += qs[r * d + x] * ks[s * d + x];
-    P[i] = (s <= r) ? a * a : 0.f;
+      for (int blk = 0; blk < g; ++blk) {
+        float a = 0.f;
+        for (int x = blk * m; x < blk * m + m; ++x) a += qs[r * d + x] * ks[s * d + x];
+        p += a * a;
+      }
+    P[i] = p;
   }
   __syncthreads();
   const float* Sp = pre + bh * bh_stride + c * chunk_stride;
@@ -175,14 +197,15 @@ __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
                                                        const Tin* __restrict__ q,
                                                        const Tin* __restrict__ k,
                                                        const Tin* __restrict__ v,
-                                                       float* __restrict__ out, int d, int dv) {
+                                                       float* __restrict__ out, int d, int dv,
+                                                       int g) {
   __shared__ float qs[64], ks[64], vs[256];
   __shared__ uint16_t pairs[2080];
   __shared__ float red[256][5];
-  const int n = d * (d + 1) / 2;
+  const int n = g * ((d / g) * (d / g + 1) / 2);
   const int bh = blockIdx.x;
   const int tid = threadIdx.x;
-  build_pair_table(pairs, d);
+  build_pair_table(pairs, d, g);
   if (tid < d) {
     qs[tid] = load_f32(q, static_cast<long long>(bh) * d + tid);
     ks[tid] = load_f32(k, static_cast<long long>(bh) * d + tid);
@@ -283,23 +306,23 @@ __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
 // ---------------------------------------------------------------------------
 // Host launchers
 // ---------------------------------------------------------------------------
-size_t fp32_forward_workspace(int BH, int T, int d, int dv, int C) {
-  const size_t n = static_cast<size_t>(d) * (d + 1) / 2;
+size_t fp32_forward_workspace(int BH, int T, int d, int dv, int C, int g) {
+  const size_t n = static_cast<size_t>(g) * (d / g) * (d / g + 1) / 2;
   const size_t NC = (static_cast<size_t>(T) + C - 1) / C;
   return static_cast<size_t>(BH) * NC * (n * dv + n) * sizeof(float);
 }
 
-size_t fp32_forward_smem(int d, int C) {
-  const size_t n = static_cast<size_t>(d) * (d + 1) / 2;
+size_t fp32_forward_smem(int d, int C, int g) {
+  const size_t n = static_cast<size_t>(g) * (d / g) * (d / g + 1) / 2;
   return (static_cast<size_t>(C) * d * 2 + static_cast<size_t>(C) * C + C) * sizeof(float) +
          n * sizeof(uint16_t);
 }
 
 template <typename Tin>
 hipError_t launch_fp32_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int C, void* ws, hipStream_t st,
+                               int T, int d, int dv, int C, int g, void* ws, hipStream_t st,
                                hipEvent_t* ev) {
-  const int n = d * (d + 1) / 2;
+  const int n = g * ((d / g) * (d / g + 1) / 2);
   const int NC = (T + C - 1) / C;
   const long long rec = static_cast<long long>(n) * dv + n;
   float* states = static_cast<float*>(ws);
@@ -309,13 +332,13 @@ hipError_t launch_fp32_forward(const void* q, const void* k, const void* v, floa
   if (e != hipSuccess) return e;
   chunk_state_f32<Tin><<<g1, 256, 0, st>>>(static_cast<const Tin*>(k), static_cast<const Tin*>(v),
                                            states, states + static_cast<long long>(n) * dv, T, d,
-                                           dv, C, bh_stride, rec, bh_stride, rec);
+                                           dv, C, g, bh_stride, rec, bh_stride, rec);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   dim3 g2(static_cast<unsigned>((rec + kEB - 1) / kEB), BH);
   scan_exclusive<float, UnitWeight><<<g2, 256, 0, st>>>(states, states, NC, rec, bh_stride,
                                                         UnitWeight{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
-  const size_t shm = fp32_forward_smem(d, C);
+  const size_t shm = fp32_forward_smem(d, C, g);
   if (shm > 65536) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chunk_out_f32<Tin>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -324,45 +347,45 @@ hipError_t launch_fp32_forward(const void* q, const void* k, const void* v, floa
   }
   chunk_out_f32<Tin><<<dim3(NC, BH), 256, shm, st>>>(
       static_cast<const Tin*>(q), static_cast<const Tin*>(k), static_cast<const Tin*>(v), states,
-      out, T, d, dv, C, bh_stride, rec);
+      out, T, d, dv, C, g, bh_stride, rec);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
 }
 
 template <typename Tin>
 hipError_t launch_prefill(const void* k, const void* v, float* S, float* z, int BH, int T, int d,
-                          int dv, hipStream_t st) {
-  const int n = d * (d + 1) / 2;
-  dim3 g((n + kFB - 1) / kFB, 1, BH);
+                          int dv, int g, hipStream_t st) {
+  const int n = g * ((d / g) * (d / g + 1) / 2);
+  dim3 grid((n + kFB - 1) / kFB, 1, BH);
   // one chunk covering all T tokens; S and z are separate arrays
-  chunk_state_f32<Tin><<<g, 256, 0, st>>>(static_cast<const Tin*>(k), static_cast<const Tin*>(v),
-                                           S, z, T, d, dv, T, static_cast<long long>(n) * dv, 0,
+  chunk_state_f32<Tin><<<grid, 256, 0, st>>>(static_cast<const Tin*>(k), static_cast<const Tin*>(v),
+                                           S, z, T, d, dv, T, g, static_cast<long long>(n) * dv, 0,
                                            static_cast<long long>(n), 0);
   return hipGetLastError();
 }
 
 template <typename Tin>
 hipError_t launch_decode(float* S, float* z, const void* q, const void* k, const void* v,
-                         float* out, int BH, int d, int dv, hipStream_t st) {
+                         float* out, int BH, int d, int dv, int g, hipStream_t st) {
   decode_step_f32<Tin><<<BH, 256, 0, st>>>(S, z, static_cast<const Tin*>(q),
                                            static_cast<const Tin*>(k), static_cast<const Tin*>(v),
-                                           out, d, dv);
+                                           out, d, dv, g);
   return hipGetLastError();
 }
 
 template hipError_t launch_fp32_forward<float>(const void*, const void*, const void*, float*, int,
-                                               int, int, int, int, void*, hipStream_t,
+                                               int, int, int, int, int, void*, hipStream_t,
                                                hipEvent_t*);
 template hipError_t launch_fp32_forward<bf16_t>(const void*, const void*, const void*, float*, int,
-                                                int, int, int, int, void*, hipStream_t,
+                                                int, int, int, int, int, void*, hipStream_t,
                                                 hipEvent_t*);
 template hipError_t launch_prefill<float>(const void*, const void*, float*, float*, int, int,
-                                          int, int, hipStream_t);
+                                          int, int, int, hipStream_t);
 template hipError_t launch_prefill<bf16_t>(const void*, const void*, float*, float*, int, int,
-                                           int, int, hipStream_t);
+                                           int, int, int, hipStream_t);
 template hipError_t launch_decode<float>(float*, float*, const void*, const void*, const void*,
-                                         float*, int, int, int, hipStream_t);
+                                         float*, int, int, int, int, hipStream_t);
 template hipError_t launch_decode<bf16_t>(float*, float*, const void*, const void*, const void*,
-                                          float*, int, int, int, hipStream_t);
+                                          float*, int, int, int, int, hipStream_t);
 
 }  // namespace kata

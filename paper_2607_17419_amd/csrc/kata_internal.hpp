@@ -20,31 +20,33 @@ __device__ __forceinline__ void store_weighted(bf16_t* p, long long i, float x, 
 }
 
 // ---- fp32 path (kata_fp32.hip) -------------------------------------------
-size_t fp32_forward_workspace(int BH, int T, int d, int dv, int C);
-size_t fp32_forward_smem(int d, int C);
+// g: feature blocks of KATA-Mg (d % g == 0; 1 is KATA-M1)
+size_t fp32_forward_workspace(int BH, int T, int d, int dv, int C, int g);
+size_t fp32_forward_smem(int d, int C, int g);
 
 // ev: null, or 4 events recorded on `st` before the state kernel and after
 // each of the three stages (state, scan, output).
 template <typename Tin>
 hipError_t launch_fp32_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int C, void* ws, hipStream_t st,
+                               int T, int d, int dv, int C, int g, void* ws, hipStream_t st,
                                hipEvent_t* ev);
 template <typename Tin>
 hipError_t launch_prefill(const void* k, const void* v, float* S, float* z, int BH, int T, int d,
-                          int dv, hipStream_t st);
+                          int dv, int g, hipStream_t st);
 template <typename Tin>
 hipError_t launch_decode(float* S, float* z, const void* q, const void* k, const void* v,
-                         float* out, int BH, int d, int dv, hipStream_t st);
+                         float* out, int BH, int d, int dv, int g, hipStream_t st);
 
 // ---- bf16 MFMA path (kata_mfma.hip) ---------------------------------------
-bool mfma_supported(int d, int dv, int C);
-size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L);
+// g: feature blocks of KATA-Mg (1 or, at d = 64, 2)
+bool mfma_supported(int d, int dv, int C, int g);
+size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L, int g);
 hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int L, void* ws, hipStream_t st,
+                               int T, int d, int dv, int g, int L, void* ws, hipStream_t st,
                                hipEvent_t* ev);
 size_t mfma_quadratic_workspace(int BH, int T, int dv);
 hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
-                                 int T, int d, int dv, void* ws, hipStream_t st);
+                                 int T, int d, int dv, int g, void* ws, hipStream_t st);
 
 inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
   return ev ? hipEventRecord(ev[i], st) : hipSuccess;

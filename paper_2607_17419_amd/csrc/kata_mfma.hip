@@ -77,6 +77,32 @@ struct Geo {
   static_assert(D % 32 == 0 && DV % 32 == 0, "tile shapes");
 };
 
+// Block-diagonal feature of KATA-Mg (section "From rank-one rays to low-rank
+// PSD packing"): NG blocks of DM = D/NG consecutive coordinates, each with the
+// slot layout of Geo<DM> (its own rotation R = DM/2), blocks side by side in a
+// span record: S^T as [dv][NG * NSLOT_block], then NG Z blocks of DM x DM in
+// operand order.  NG = 1 is KATA-M1 (GeoG<D, DV, 1> matches Geo<D, DV>).
+template <int D, int DV, int NG>
+struct GeoG {
+  using Blk = Geo<D / NG, DV>;
+  static constexpr int DM = D / NG;          // coordinates per block
+  static constexpr int RM = Blk::R;          // rotation of a block's slots
+  static constexpr int KZM = Blk::KZ;        // 16-wide K-steps over one block
+  static constexpr int KZ = NG * KZM;        // score MFMAs per query tile and key block
+  static constexpr int NKSM = Blk::NKS;      // readout K-steps of one block
+  static constexpr int NKS = NG * NKSM;
+  static constexpr int NSLOTM = Blk::NSLOT;
+  static constexpr int NSLOT = NG * NSLOTM;
+  static constexpr int NSTM = Blk::NST;      // 32-slot tiles of one block
+  static constexpr int NST = NG * NSTM;
+  static constexpr int MT = Blk::MT;
+  static constexpr int ZMB = Blk::ZM;        // 32-wide Z tiles per block dim
+  static constexpr long long ES = static_cast<long long>(DV) * NSLOT;
+  static constexpr long long EZ = static_cast<long long>(NG) * DM * DM;
+  static constexpr long long E = ES + EZ;
+  static_assert(D % NG == 0 && DM % 32 == 0, "blocks of a multiple of 32 coordinates");
+};
+
 // Slot -> (x, y) dims of its pair (see the header comment).
 template <int D>
 __host__ __device__ __forceinline__ void slot_pair(int s, int& x, int& y) {
@@ -112,13 +138,13 @@ __host__ __device__ __forceinline__ int zop_index(int a, int b) {
   return ((mu * KZ + kap) * 64 + lane) * 8 + jb;
 }
 
-// Scan output weights: S region by slot, Z region 1.
-template <int D, int DV>
+// Scan output weights: S region by slot (inside its block), Z region 1.
+template <int D, int DV, int NG>
 struct SlotWeight {
   __device__ __forceinline__ float operator()(long long e) const {
-    using G = Geo<D, DV>;
+    using G = GeoG<D, DV, NG>;
     if (e >= G::ES) return 1.f;
-    return slot_weight<D>(static_cast<int>(e % G::NSLOT));
+    return slot_weight<G::DM>(static_cast<int>(e % G::NSLOT % G::NSLOTM));
   }
 };
 
@@ -282,36 +308,39 @@ constexpr int kGapK2 = 32;          // fp32 gap before key row d/2 (see krow)
 constexpr int kUW = 6;              // slot tiles per slot wave
 constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
 
-template <int D, int DV>
+template <int D, int DV, int NG>
 struct StateGrid {
-  static constexpr int NUW = (Geo<D, DV>::NST + kUW - 1) / kUW;  // slot waves per span
-  static constexpr int NB = (NUW + 1 + 3) / 4;                   // blocks per span
+  // slot waves per feature block (a wave's tiles never straddle two blocks)
+  static constexpr int NUWB = (GeoG<D, DV, NG>::NSTM + kUW - 1) / kUW;
+  static constexpr int NUW = NG * NUWB;        // slot waves per span
+  static constexpr int NB = (NUW + 1 + 3) / 4;  // workgroups per span
 };
 
-template <int D, int DV>
+template <int D, int DV, int NG>
 __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ spanst,
                                                          uint16_t* __restrict__ vtp, int T,
                                                          int L, int LV, int NS, int sp0,
                                                          int nsp) {
-  using G = Geo<D, DV>;
-  using SG = StateGrid<D, DV>;
+  using G = GeoG<D, DV, NG>;
+  using SG = StateGrid<D, DV, NG>;
   constexpr int UW = kUW;
-  constexpr int NXR = D / 32;  // distinct x rows per lane (x depends on tile % NXR)
+  constexpr int DM = G::DM;
+  constexpr int NXR = DM / 32;  // distinct x rows per lane (x depends on tile % NXR)
   static_assert(UW % NXR == 0, "unit parity must be static");
   static_assert(G::MT == 2, "the slot loop issues the two dv tiles of a slot tile together");
   constexpr int KS = kTB2 / 16;                      // K-steps per staged block
   // K is kept in LDS widened to fp32 (exact), so that the feature products
   // are plain multiplies of LDS values.  Key row r of a K buffer starts at
-  // krow(r).  The slot tiles read rows r and r + d/2 in the same 16-lane phase
-  // of a ds_read_b128; with a uniform stride they would share banks, the gap
-  // of kGapK2 floats (32 banks) before row d/2 moves the upper half to the
-  // other half of the banks.
-  constexpr int KBUFE = D * kRowK2 + kGapK2;         // floats of one K buffer
+  // krow(r).  The slot tiles read rows r and r + DM/2 of a feature block in
+  // the same 16-lane phase of a ds_read_b128; with a uniform stride they
+  // would share banks, a gap of kGapK2 floats (32 banks) after every DM/2 rows
+  // moves alternate half-blocks to the other half of the banks.
+  constexpr int KBUFE = D * kRowK2 + (2 * NG - 1) * kGapK2;  // floats of one K buffer
   constexpr unsigned KBUF = KBUFE * 4;               // bytes of one K buffer
   constexpr unsigned VBUF = DV * kRow2 * 2;          // bytes of one V buffer
-  auto krow = [](int r) { return r * kRowK2 + (r >= D / 2 ? kGapK2 : 0); };
+  auto krow = [](int r) { return r * kRowK2 + (r / (DM / 2)) * kGapK2; };
   __shared__ __attribute__((aligned(16))) float kT[kNBuf2][KBUFE];
   __shared__ __attribute__((aligned(16))) uint16_t vT[kNBuf2][DV][kRow2];
   const int tid = threadIdx.x;
@@ -372,8 +401,8 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       // become zeros
       if (cg < KG) {
         // K: dim 8cg+2e of tokens (2p, 2p+1) is (a.lo, b.lo) widened to fp32,
-        // dim 8cg+2e+1 is (a.hi, b.hi); rows 8cg .. 8cg+7 lie on one side of the
-        // gap (d/2 is a multiple of 8)
+        // dim 8cg+2e+1 is (a.hi, b.hi); rows 8cg .. 8cg+7 lie between two
+        // gaps (DM/2 is a multiple of 8)
         const uint32_t lo_a = va ? 0x01000c0cu : 0x0c0c0c0cu, hi_a = va ? 0x03020c0cu : 0x0c0c0c0cu;
         const uint32_t lo_b = vb ? 0x01000c0cu : 0x0c0c0c0cu, hi_b = vb ? 0x03020c0cu : 0x0c0c0c0cu;
         float* base = &kT[buf][krow(8 * cg) + 2 * p];
@@ -421,13 +450,18 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     // ---- Z = K^T K over the span and the span's V^T (wave NUW) --------------
     const bool zwave = gw == SG::NUW;
     uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
-    f32x16 zacc[G::ZM][G::ZM];
+    // Z_blk = K_blk^T K_blk for each feature block: the diagonal ZMB x ZMB
+    // tile blocks of K^T K
+    constexpr int ZT = D / 32;  // 32-row tiles of K
+    f32x16 zacc[NG][G::ZMB][G::ZMB];
 #pragma unroll
-    for (int a = 0; a < G::ZM; ++a)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-      for (int b = 0; b < G::ZM; ++b)
+      for (int a = 0; a < G::ZMB; ++a)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) zacc[a][b][r] = 0.f;
+        for (int b = 0; b < G::ZMB; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) zacc[bb][a][b][r] = 0.f;
     for (int bi = 0; bi < nblk; ++bi) {
       const int buf = bi % kNBuf2;
       if (bi + 1 < nblk)
@@ -447,9 +481,9 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          bf16x8 A[G::ZM];
+          bf16x8 A[ZT];
 #pragma unroll
-          for (int a = 0; a < G::ZM; ++a) {
+          for (int a = 0; a < ZT; ++a) {
             // the fp32 values are bf16 values: keep their upper halves
             const float* kr = &kT[buf][krow(32 * a + c) + 16 * ks + 8 * g];
             const uint4 f0 = *reinterpret_cast<const uint4*>(kr);
@@ -461,45 +495,54 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
                                    __builtin_amdgcn_perm(f1.w, f1.z, 0x07060302u)));
           }
 #pragma unroll
-          for (int a = 0; a < G::ZM; ++a)
+          for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-            for (int b = 0; b < G::ZM; ++b) zacc[a][b] = mfma32(A[a], A[b], zacc[a][b]);
+            for (int a = 0; a < G::ZMB; ++a)
+#pragma unroll
+              for (int b = 0; b < G::ZMB; ++b)
+                zacc[bb][a][b] = mfma32(A[bb * G::ZMB + a], A[bb * G::ZMB + b], zacc[bb][a][b]);
         }
       }
       lds_barrier();
     }
     if (zwave) {
 #pragma unroll
-      for (int za = 0; za < G::ZM; ++za)
+      for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-        for (int zb = 0; zb < G::ZM; ++zb)
+        for (int za = 0; za < G::ZMB; ++za)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int a = 32 * za + 8 * (r >> 2) + 4 * g + (r & 3);
-            const int b = 32 * zb + c;
-            __bf16 h = static_cast<__bf16>(zacc[za][zb][r]);
-            rec[G::ES + zop_index<D>(a, b)] = __builtin_bit_cast(uint16_t, h);
-          }
+          for (int zb = 0; zb < G::ZMB; ++zb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int a = 32 * za + 8 * (r >> 2) + 4 * g + (r & 3);  // inside the block
+              const int b = 32 * zb + c;
+              __bf16 h = static_cast<__bf16>(zacc[bb][za][zb][r]);
+              rec[G::ES + static_cast<long long>(bb) * DM * DM + zop_index<DM>(a, b)] =
+                  __builtin_bit_cast(uint16_t, h);
+            }
     }
     return;
   }
 
   // ---- S_span^T = V^T Phi(K) for this wave's slot tiles ----------------------
-  const int unit0 = gw * UW;
+  // slot wave gw covers tiles [unit0, unit0 + UW) of feature block blk (tiles
+  // past the block's last one are computed on a valid row and not stored)
+  const int blk = gw / SG::NUWB;
+  const int unit0 = (gw % SG::NUWB) * UW;
   // per-lane byte offsets of the fragments inside buffer 0, column 8*g
   unsigned xo[NXR], yo[UW], vo[G::MT];
 #pragma unroll
   for (int p = 0; p < NXR; ++p) {
     int xr, yy;
-    slot_pair<D>(32 * p + c, xr, yy);
-    xo[p] = static_cast<unsigned>((krow(xr) + 8 * g) * 4);
+    slot_pair<DM>(32 * p + c, xr, yy);
+    xo[p] = static_cast<unsigned>((krow(DM * blk + xr) + 8 * g) * 4);
   }
 #pragma unroll
   for (int u = 0; u < UW; ++u) {
     int xx, yr;
-    const int unit = unit0 + u < G::NST ? unit0 + u : G::NST - 1;  // valid row; store skipped
-    slot_pair<D>(32 * unit + c, xx, yr);
-    yo[u] = static_cast<unsigned>((krow(yr) + 8 * g) * 4);
+    const int unit = unit0 + u < G::NSTM ? unit0 + u : G::NSTM - 1;  // valid row; store skipped
+    slot_pair<DM>(32 * unit + c, xx, yr);
+    yo[u] = static_cast<unsigned>((krow(DM * blk + yr) + 8 * g) * 4);
   }
 #pragma unroll
   for (int m = 0; m < G::MT; ++m) vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
@@ -637,8 +680,8 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   // write this wave's tiles of the span record (bf16)
 #pragma unroll
   for (int u = 0; u < UW; ++u) {
-    const int unit = unit0 + u;
-    if (unit < G::NST) {
+    const int unit = blk * G::NSTM + unit0 + u;  // tile of the whole record
+    if (unit0 + u < G::NSTM) {
 #pragma unroll
       for (int m = 0; m < G::MT; ++m)
 #pragma unroll
@@ -725,18 +768,40 @@ __device__ __forceinline__ void score2<2>(f32x16& sc0, f32x16& sc1, const bf16x8
       : "v"(A[0]), "v"(A[1]), "v"(q0[0]), "v"(q0[1]), "v"(q1[0]), "v"(q1[1]));
 }
 
+// Scores of two query tiles against one 32-key block with two feature blocks
+// of 32 coordinates (K-steps 0, 1 of block 0 and 2, 3 of block 1): four
+// chains, tile 0's chains written by the 5th and 7th MFMA, so as for score2
+// tile 0's scores are a full MFMA old when the block ends.
+__device__ __forceinline__ void score2b2(f32x16& s00, f32x16& s01, f32x16& s10, f32x16& s11,
+                                         const bf16x8 (&A)[4], const bf16x8 (&q0)[4],
+                                         const bf16x8 (&q1)[4]) {
+  asm volatile(
+      "v_mfma_f32_32x32x16_bf16 %0, %4, %8, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %2, %4, %12, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %6, %10, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %3, %6, %14, 0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %0, %5, %9, %0\n\t"
+      "v_mfma_f32_32x32x16_bf16 %2, %5, %13, %2\n\t"
+      "v_mfma_f32_32x32x16_bf16 %1, %7, %11, %1\n\t"
+      "v_mfma_f32_32x32x16_bf16 %3, %7, %15, %3\n\t"
+      "s_nop 4"
+      : "=&v"(s00), "=&v"(s01), "=&v"(s10), "=&v"(s11)
+      : "v"(A[0]), "v"(A[1]), "v"(A[2]), "v"(A[3]), "v"(q0[0]), "v"(q0[1]), "v"(q0[2]),
+        "v"(q0[3]), "v"(q1[0]), "v"(q1[1]), "v"(q1[2]), "v"(q1[3]));
+}
+
 template <int D, int DV>
 struct OutGrid {
   static constexpr int QB_TOKENS = 256;  // queries per workgroup
 };
 
-template <int D, int DV, bool QUAD>
+template <int D, int DV, int NG, bool QUAD>
 __global__ __launch_bounds__(256) void span_output_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
     int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
-  using G = Geo<D, DV>;
-  constexpr int R = G::R;
+  using G = GeoG<D, DV, NG>;
+  constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM;
   constexpr int NQ = 2, W = 4, NT = 8;
   constexpr int KCH = D / 8;                    // 16-byte chunks per key row
   constexpr int KCHUNKS = kKB * KCH;            // K rows of one intra stage
@@ -786,26 +851,31 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     tlive[i] = tq0[i] < span_end;
   }
 
-  // bf16 query fragments for the d-contractions: qf[i][kz] holds
-  // q[t][8*kz + R*g .. +7] of this lane's query t = tq0 + c.
+  // bf16 query fragments for the d-contractions, per feature block:
+  // qf[i][KZM*bb + kz] holds q[t][DM*bb + 8*kz + RM*g .. +7] of this lane's
+  // query t = tq0 + c (with one block: q[t][8*kz + R*g ..]).
   bf16x8 qf[NQ][G::KZ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
 #pragma unroll
     for (int kz = 0; kz < G::KZ; ++kz)
-      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + 8 * kz + R * g);
+      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + DM * (kz / KZM) +
+                                                   8 * (kz % KZM) + RM * g);
   }
 
-  // Z_pre operand fragments (see below)
-  bf16x8 zA[G::ZM][G::KZ];
+  // Z_pre operand fragments of each feature block (see below)
+  bf16x8 zA[NG][G::ZMB][KZM];
   if constexpr (!QUAD) {
-    const uint16_t* zop = rec + G::ES;
 #pragma unroll
-    for (int m = 0; m < G::ZM; ++m)
+    for (int bb = 0; bb < NG; ++bb) {
+      const uint16_t* zop = rec + G::ES + static_cast<long long>(bb) * DM * DM;
 #pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz)
-        zA[m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * G::KZ + kz) * 64 + lane) * 8);
+      for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+        for (int kz = 0; kz < KZM; ++kz)
+          zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * KZM + kz) * 64 + lane) * 8);
+    }
   }
 
   // ---- staging copies of both phases ------------------------------------------
@@ -902,32 +972,41 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 #pragma unroll
     for (int i = 0; i < NQ; ++i) dpart[i] = 0.f;
   } else {
-    f32x16 az[G::ZM][NQ];
+    // sum over the feature blocks of q_bb^T Z_bb q_bb
+    f32x16 az[NG][G::ZMB][NQ];
 #pragma unroll
-    for (int m = 0; m < G::ZM; ++m)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-      for (int i = 0; i < NQ; ++i)
+      for (int m = 0; m < G::ZMB; ++m)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) az[m][i][r] = 0.f;
+        for (int i = 0; i < NQ; ++i)
 #pragma unroll
-    for (int m = 0; m < G::ZM; ++m)
+          for (int r = 0; r < 16; ++r) az[bb][m][i][r] = 0.f;
 #pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) az[m][i] = mfma32(zA[m][kz], qf[i][kz], az[m][i]);
+      for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+        for (int kz = 0; kz < KZM; ++kz)
+#pragma unroll
+          for (int i = 0; i < NQ; ++i)
+            az[bb][m][i] = mfma32(zA[bb][m][kz], qf[i][KZM * bb + kz], az[bb][m][i]);
 #pragma unroll
     for (int i = 0; i < NQ; ++i) {
       float dsum = 0.f;
 #pragma unroll
-      for (int m = 0; m < G::ZM; ++m)
+      for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          // row sigma = 16m + r + R*g: element (16m + r) % 8 of fragment (16m + r) / 8
-          const int x = 16 * m + r;
-          const uint32_t w = word_of(qf[i][x >> 3], (x & 7) >> 1);
-          const float qa = (x & 1) ? bf16hi_f32(w) : bf16lo_f32(w);
-          dsum += qa * az[m][i][r];
-        }
+        for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            // row sigma = 16m + r + RM*g of block bb: element (16m + r) % 8 of
+            // the block's fragment (16m + r) / 8
+            const int x = 16 * m + r;
+            const uint32_t w = word_of(qf[i][KZM * bb + (x >> 3)], (x & 7) >> 1);
+            const float qa = (x & 1) ? bf16hi_f32(w) : bf16lo_f32(w);
+            dsum += qa * az[bb][m][i][r];
+          }
       dpart[i] = dsum;
     }
   }
@@ -949,14 +1028,16 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   // no branch surrounds an accumulator.
   {
     // fragment byte offsets inside a stage buffer
-    //  K rows 32*sb + c, chunk (kz + (R/8)*g) ^ kswz: depends on sb only through sb & 1
+    //  K rows 32*sb + c, chunk (DM/8)*bb + kz' + (RM/8)*g of fragment KZM*bb + kz'
+    //  (the layout of qf), ^ kswz: depends on sb only through sb & 1
     unsigned kfo[2][G::KZ];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int kz = 0; kz < G::KZ; ++kz) {
         const int krow = 32 * h + c;
-        kfo[h][kz] = static_cast<unsigned>((krow * KCH + ((kz + (R / 8) * g) ^ kswz<D>(krow))) * 16);
+        const int chunk = (DM / 8) * (kz / KZM) + (kz % KZM) + (RM / 8) * g;
+        kfo[h][kz] = static_cast<unsigned>((krow * KCH + (chunk ^ kswz<D>(krow))) * 16);
       }
     //  V^T rows 32*m + c, chunk (4*sb + 2*kv + g) ^ (c & 15); the row part of m is immediate
     unsigned vfo[4][2];
@@ -993,14 +1074,25 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 #pragma unroll
         for (int kv = 0; kv < 2; ++kv) ldV1(buf, sb_c, m, kv, va[m][kv]);
     };
+    // Score accumulators of one query tile: one per feature block; the weight
+    // of a (query, key) pair is the sum over blocks of the squared scores.
+    struct Sc {
+      f32x16 b[NG];
+    };
+    auto p_of = [](const Sc& sc, int r) __attribute__((always_inline)) {
+      float p = sc.b[0][r] * sc.b[0][r];
+#pragma unroll
+      for (int bb = 1; bb < NG; ++bb) p += sc.b[bb][r] * sc.b[bb][r];
+      return p;
+    };
     // P elements 2j and 2j+1 of a tile on a block before its diagonal, packed.
     // The empty asm statement consumes the results before the next asm (an
     // MFMA), so the compiler can neither sink the part below it nor merge it
     // into the fix-up that follows the group.
-    auto ppart = [&](int j, const f32x16& sc, float& dacc, uint32_t (&bw)[8])
+    auto ppart = [&](int j, const Sc& sc, float& dacc, uint32_t (&bw)[8])
                      __attribute__((always_inline)) {
-      const float p0 = sc[2 * j] * sc[2 * j];
-      const float p1 = sc[2 * j + 1] * sc[2 * j + 1];
+      const float p0 = p_of(sc, 2 * j);
+      const float p1 = p_of(sc, 2 * j + 1);
       dacc += p0 + p1;
       bw[j] = pack_bf16x2(p0, p1);
       asm volatile("" : "+v"(dacc), "+v"(bw[j]));
@@ -1008,15 +1100,15 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     // on tile i's diagonal block (keys above the query masked) and past it
     // (zero; also a tile beyond the sequence) the tile's P of block kb is
     // redone after its group, VALU only; dsave is the row sum before the group
-    auto fixup = [&](int kb, int i, const f32x16& sc, float dsave, float& dacc, uint32_t (&bw)[8])
+    auto fixup = [&](int kb, int i, const Sc& sc, float dsave, float& dacc, uint32_t (&bw)[8])
                      __attribute__((always_inline)) {
       if (__builtin_expect(kb < tdiag[i], 1)) return;  // nothing to redo (the common case)
       if (kb == tdiag[i]) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int r0 = 2 * j, r1 = 2 * j + 1;
-          const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : sc[r0] * sc[r0];
-          const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : sc[r1] * sc[r1];
+          const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : p_of(sc, r0);
+          const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : p_of(sc, r1);
           dsave += p0 + p1;
           bw[j] = pack_bf16x2(p0, p1);
         }
@@ -1031,13 +1123,15 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       return __builtin_bit_cast(bf16x8, make_uint4(bw[4 * kv], bw[4 * kv + 1], bw[4 * kv + 2],
                                                    bw[4 * kv + 3]));
     };
-    // one group: score chain into scs (if S), P V into (a0, a1) from fragments
+    // one group: score chains into scs (if S), P V into (a0, a1) from fragments
     // vb and P words bv (if V), and the P words bw of the other tile from scp
     // (full mode; the caller fixes them up for the other modes); extra(i)
-    // adds the caller's work (fragment loads) to slot i
-    auto group = [&](auto s_c, auto v_c, f32x16& scs, const bf16x8 (&Ab)[G::KZ],
+    // adds the caller's work (fragment loads) to slot i.  Score MFMA i is
+    // K-step i / NG of block i % NG, so consecutive MFMAs of one chain are NG
+    // slots apart.
+    auto group = [&](auto s_c, auto v_c, Sc& scs, const bf16x8 (&Ab)[G::KZ],
                      const bf16x8 (&qs)[G::KZ], f32x16& a0, f32x16& a1,
-                     const bf16x8 (&vb)[G::MT][2], const uint32_t (&bv)[8], f32x16& scp,
+                     const bf16x8 (&vb)[G::MT][2], const uint32_t (&bv)[8], Sc& scp,
                      float& dacc, uint32_t (&bw)[8], auto&& extra) __attribute__((always_inline)) {
       constexpr bool HS = decltype(s_c)::value, HV = decltype(v_c)::value;
       bf16x8 Bv[2];
@@ -1048,14 +1142,18 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       static_for<0, 4>([&](auto i_c) {
         constexpr int i = decltype(i_c)::value;
         if constexpr (HS && i < G::KZ) {
-          if constexpr (i == 0) mfma_vz(scs, Ab[0], qs[0]);
-          else mfma_v(scs, Ab[i], qs[i]);
+          constexpr int bb = i % NG, kz = KZM * bb + i / NG;
+          if constexpr (i / NG == 0) mfma_vz(scs.b[bb], Ab[kz], qs[kz]);
+          else mfma_v(scs.b[bb], Ab[kz], qs[kz]);
         }
         // without a score chain the P V MFMA goes first, so that the VALU
         // reads scp two MFMA issues after the chain that wrote it
         if constexpr (!HS && HV) mfma_a((i & 1) ? a1 : a0, vb[i & 1][i >> 1], Bv[i >> 1]);
         // the scores become available to the VALU only after the first MFMA
-        if constexpr (i == 0) asm volatile("" : "+v"(scp));
+        if constexpr (i == 0) {
+#pragma unroll
+          for (int bb = 0; bb < NG; ++bb) asm volatile("" : "+v"(scp.b[bb]));
+        }
         __builtin_amdgcn_sched_barrier(0);
         ppart(2 * i, scp, dacc, bw);
         __builtin_amdgcn_sched_barrier(0);
@@ -1073,7 +1171,7 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 
     const int NB = 4 * nstage;  // 32-key blocks, all waves alike (stage barriers)
     bf16x8 A[2][G::KZ], va[2][G::MT][2];
-    f32x16 sc[NQ];
+    Sc sc[NQ];
     uint32_t bw[NQ][8];
     // stage buffers of stages st, st+1, st+2 (rotated once per stage)
     const char* b0 = reinterpret_cast<const char*>(g_stage0);
@@ -1088,7 +1186,8 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     ldV(b0, integral_constant<int, 0>{}, va[0]);
     // block 0: both score chains interleaved (no earlier block to finish),
     // then P_0(0); score2 leaves sc[0] readable by VALU
-    score2<G::KZ>(sc[0], sc[1], A[0], qf[0], qf[1]);
+    if constexpr (NG == 1) score2<G::KZ>(sc[0].b[0], sc[1].b[0], A[0], qf[0], qf[1]);
+    else score2b2(sc[0].b[0], sc[0].b[1], sc[1].b[0], sc[1].b[1], A[0], qf[0], qf[1]);
     {
       const float dsave = dpart[0];
 #pragma unroll
@@ -1177,22 +1276,24 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 
   // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
   if constexpr (!QUAD) {
-    // rotated fp32 query rows: qr[i][x] = q[t][(x + R*g) % D]; the lane's
-    // own bf16 fragments hold x < R, the lane 32 away holds the rest
+    // rotated fp32 query rows, per feature block:
+    // qr[i][DM*bb + x] = q[t][DM*bb + (x + RM*g) % DM]; the lane's own bf16
+    // fragments of block bb hold x < RM, the lane 32 away holds the rest
     float qr[NQ][D];
 #pragma unroll
     for (int i = 0; i < NQ; ++i)
 #pragma unroll
       for (int kz = 0; kz < G::KZ; ++kz) {
+        const int base = DM * (kz / KZM) + 8 * (kz % KZM);
         const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
         const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
-          qr[i][8 * kz + 2 * e] = bf16lo_f32(w[e]);
-          qr[i][8 * kz + 2 * e + 1] = bf16hi_f32(w[e]);
-          qr[i][R + 8 * kz + 2 * e] = bf16lo_f32(pw);
-          qr[i][R + 8 * kz + 2 * e + 1] = bf16hi_f32(pw);
+          qr[i][base + 2 * e] = bf16lo_f32(w[e]);
+          qr[i][base + 2 * e + 1] = bf16hi_f32(w[e]);
+          qr[i][base + RM + 2 * e] = bf16lo_f32(pw);
+          qr[i][base + RM + 2 * e + 1] = bf16hi_f32(pw);
         }
       }
     // A fragment offsets: rows 32*m + c, chunk (2*kk + g) ^ (c & 15); the kk & 8
@@ -1206,14 +1307,16 @@ __global__ __launch_bounds__(256) void span_output_kernel(
           bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
                              pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
     };
-    // query feature products of tile i at global K-step kap: slots 16*kap + 8*g + j
-    // pair registers (r1 + j, r1 + j + delta) of the rotated row
+    // query feature products of tile i at global K-step kap (K-step kl of
+    // feature block bb): slots 16*kl + 8*g + j of the block pair registers
+    // (r1 + j, r1 + j + delta) of the block's rotated row
     auto fx = [&](int i, int kap, float x[8], float y[8]) __attribute__((always_inline)) {
-      const int r1 = (8 * kap) % R, dl = (8 * kap) / R;
+      const int bb = kap / G::NKSM, kl = kap % G::NKSM;
+      const int r1 = (8 * kl) % RM, dl = (8 * kl) / RM;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        x[j] = qr[i][r1 + j];
-        y[j] = qr[i][(r1 + j + dl) % D];
+        x[j] = qr[i][DM * bb + r1 + j];
+        y[j] = qr[i][DM * bb + (r1 + j + dl) % DM];
       }
     };
     // B fragments: bq[0] the next item's, bq[1], bq[2] the two before (kept
@@ -1362,12 +1465,14 @@ __global__ __launch_bounds__(256) void vt_permute_kernel(const uint16_t* __restr
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-bool mfma_supported(int d, int dv, int C) {
-  return (d == 64 || d == 32) && dv == 64 && C > 0 && C % 32 == 0 && C <= 1024;
+bool mfma_supported(int d, int dv, int C, int g) {
+  const bool shape = (d == 64 && (g == 1 || g == 2)) || (d == 32 && g == 1);
+  return shape && dv == 64 && C > 0 && C % 32 == 0 && C <= 1024;
 }
 
-static long long mfma_record(int d) {
-  return d == 64 ? Geo<64, 64>::E : Geo<32, 64>::E;
+static long long mfma_record(int d, int g) {
+  if (d == 64) return g == 2 ? GeoG<64, 64, 2>::E : GeoG<64, 64, 1>::E;
+  return GeoG<32, 64, 1>::E;
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -1379,17 +1484,17 @@ static_assert(kKB % kTB2 == 0, "the state kernel writes V^T in whole staged bloc
 
 constexpr int kSpansPerLaunch = 1 << 20;
 
-size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L) {
+size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L, int g) {
   const size_t NS = (static_cast<size_t>(T) + L - 1) / L;
-  const size_t recs = static_cast<size_t>(BH) * NS * static_cast<size_t>(mfma_record(d));
+  const size_t recs = static_cast<size_t>(BH) * NS * static_cast<size_t>(mfma_record(d, g));
   const size_t vt = static_cast<size_t>(BH) * NS * dv * span_alloc(L);
   return align256(recs * sizeof(uint16_t)) + align256(vt * sizeof(uint16_t));
 }
 
-template <int D, int DV>
+template <int D, int DV, int NG>
 static hipError_t run_mfma(const void* q, const void* k, const void* v, float* out, int BH, int T,
                            int L, void* ws, hipStream_t st, hipEvent_t* ev) {
-  using G = Geo<D, DV>;
+  using G = GeoG<D, DV, NG>;
   const int NS = (T + L - 1) / L;
   const int LA = span_alloc(L);
   const size_t recs = static_cast<size_t>(BH) * NS * G::E;
@@ -1405,21 +1510,21 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   // K2 in launches of at most kSpansPerLaunch spans (1-D grid size limit)
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
-    const unsigned nb2 = 8u * StateGrid<D, DV>::NB * static_cast<unsigned>((cnt + 7) / 8);
-    span_state_kernel<D, DV><<<nb2, 256, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
-                                                  sp0 + cnt);
+    const unsigned nb2 = 8u * StateGrid<D, DV, NG>::NB * static_cast<unsigned>((cnt + 7) / 8);
+    span_state_kernel<D, DV, NG><<<nb2, 256, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
+                                                      sp0 + cnt);
   }
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   dim3 g3(static_cast<unsigned>((G::E + kEB16 - 1) / kEB16), BH);
-  scan_exclusive_bf16<SlotWeight<D, DV>><<<g3, 256, 0, st>>>(
-      spanst, NS, G::E, static_cast<long long>(NS) * G::E, SlotWeight<D, DV>{});
+  scan_exclusive_bf16<SlotWeight<D, DV, NG>><<<g3, 256, 0, st>>>(
+      spanst, NS, G::E, static_cast<long long>(NS) * G::E, SlotWeight<D, DV, NG>{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   const int qblocks = (L + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output_kernel<D, DV, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA,
-                                                          NS, qblocks, sp0, sp0 + cnt);
+    span_output_kernel<D, DV, NG, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA,
+                                                              NS, qblocks, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
@@ -1431,7 +1536,7 @@ size_t mfma_quadratic_workspace(int BH, int T, int dv) {
   return align256(static_cast<size_t>(BH) * dv * span_alloc(T) * sizeof(uint16_t));
 }
 
-template <int D, int DV>
+template <int D, int DV, int NG>
 static hipError_t run_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
                                 int T, void* ws, hipStream_t st) {
   const int LA = span_alloc(T);
@@ -1446,7 +1551,7 @@ static hipError_t run_quadratic(const void* q, const void* k, const void* v, flo
   for (int sp0 = 0; sp0 < BH; sp0 += per) {
     const int cnt = BH - sp0 < per ? BH - sp0 : per;
     const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output_kernel<D, DV, true><<<nb4, 256, 0, st>>>(
+    span_output_kernel<D, DV, NG, true><<<nb4, 256, 0, st>>>(
         static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), nullptr, vtp, out, T, T,
         LA, 1, qblocks, sp0, sp0 + cnt);
   }
@@ -1454,17 +1559,19 @@ static hipError_t run_quadratic(const void* q, const void* k, const void* v, flo
 }
 
 hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
-                                 int T, int d, int dv, void* ws, hipStream_t st) {
-  if (d == 64 && dv == 64) return run_quadratic<64, 64>(q, k, v, out, BH, T, ws, st);
-  if (d == 32 && dv == 64) return run_quadratic<32, 64>(q, k, v, out, BH, T, ws, st);
+                                 int T, int d, int dv, int g, void* ws, hipStream_t st) {
+  if (d == 64 && dv == 64 && g == 1) return run_quadratic<64, 64, 1>(q, k, v, out, BH, T, ws, st);
+  if (d == 64 && dv == 64 && g == 2) return run_quadratic<64, 64, 2>(q, k, v, out, BH, T, ws, st);
+  if (d == 32 && dv == 64 && g == 1) return run_quadratic<32, 64, 1>(q, k, v, out, BH, T, ws, st);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int L, void* ws, hipStream_t st,
+                               int T, int d, int dv, int g, int L, void* ws, hipStream_t st,
                                hipEvent_t* ev) {
-  if (d == 64 && dv == 64) return run_mfma<64, 64>(q, k, v, out, BH, T, L, ws, st, ev);
-  if (d == 32 && dv == 64) return run_mfma<32, 64>(q, k, v, out, BH, T, L, ws, st, ev);
+  if (d == 64 && dv == 64 && g == 1) return run_mfma<64, 64, 1>(q, k, v, out, BH, T, L, ws, st, ev);
+  if (d == 64 && dv == 64 && g == 2) return run_mfma<64, 64, 2>(q, k, v, out, BH, T, L, ws, st, ev);
+  if (d == 32 && dv == 64 && g == 1) return run_mfma<32, 64, 1>(q, k, v, out, BH, T, L, ws, st, ev);
   return hipErrorInvalidValue;
 }
 

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 100
+    assert L.kata_abi_version() == 101
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
@@ -142,3 +142,35 @@ def test_quadratic_workspace_host_logic():
     st = L.kata_fwd_quadratic_ws(FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 64, 64, 1,
                                  ctypes.c_void_p(0x100040), need, NUL)
     assert st == 1
+
+
+@pytest.mark.parametrize("g,expect", [(0, 1), (3, 1), (65, 1), (-1, 1)])
+def test_mg_rejects_bad_block_count(g, expect):
+    L = kata.lib()
+    st = L.kata_mg_fwd_chunked(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 64, g, 1, NUL)
+    assert st == expect
+    assert L.kata_mg_fwd_workspace_bytes(1, 1, 8, 64, 64, 64, g, 1, 0) == 0
+    assert L.kata_mg_decode_step(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 64, 64, g, 1, NUL) == 1
+
+
+def test_mg_workspace_host_logic():
+    L = kata.lib()
+    # M2 on the MFMA path: one bf16 record per span and head, S^T over
+    # 2 x 544 slots (the rotated layout of each 32-dim block) x 64 dv, then
+    # two 32 x 32 Z blocks; plus the V^T copy
+    rec = 2 * 544 * 64 + 2 * 32 * 32
+    NS = 131072 // 1024
+    expect = 16 * NS * rec * 2 + 16 * NS * 64 * 1024 * 2
+    assert L.kata_mg_fwd_workspace_bytes(1, 16, 131072, 64, 64, 64, 2, 1, 0) == expect
+    # g = 1 is M1
+    assert (L.kata_mg_fwd_workspace_bytes(1, 16, 131072, 64, 64, 64, 1, 1, 0)
+            == L.kata_fwd_workspace_bytes(1, 16, 131072, 64, 64, 64, 1, 0))
+    # fp32 path with g blocks: n = g m(m+1)/2 per chunk record
+    n = 2 * (8 * 9 // 2)
+    assert L.kata_mg_fwd_workspace_bytes(1, 2, 256, 16, 16, 32, 2, 0, 0) == 2 * 8 * (n * 16 + n) * 4
+    # M4 at d = 64 runs on the fp32 path (no MFMA shape for it)
+    n4 = 4 * (16 * 17 // 2)
+    assert L.kata_mg_fwd_workspace_bytes(1, 1, 128, 64, 64, 64, 4, 1, 0) == 2 * (n4 * 64 + n4) * 4
+    # quadratic M2 exists, M4 does not
+    assert L.kata_mg_fwd_quadratic_workspace_bytes(1, 1, 100, 64, 64, 2, 1) == 64 * 128 * 2
+    assert L.kata_mg_fwd_quadratic_workspace_bytes(1, 1, 100, 64, 64, 4, 1) == 0
