@@ -81,8 +81,9 @@ def upload(payload, dtype, dev):
     return torch.from_numpy(np.ascontiguousarray(payload)).to(dev)
 
 
-def algorithmic(w, L):
-    """Algorithmic work per kernel (packed n = d(d+1)/2 features).
+def algorithmic(w, L, g=1):
+    """Algorithmic work per kernel (packed n = d(d+1)/2 features; with g
+    feature blocks of KATA-Mg, n = g*m(m+1)/2 with m = d/g).
 
     per head-token:  state   2*n*dv + n          (S += phi(k) v^T, z += phi(k))
                      output  2*n*dv + 2*n + (C+1)*(d+dv)
@@ -91,7 +92,8 @@ def algorithmic(w, L):
     scan: one bf16 read of every span state (n*(dv+1) values) and one bf16
           write of its exclusive prefix, per span and head.
     """
-    n = w.d * (w.d + 1) // 2
+    m = w.d // g
+    n = g * (m * (m + 1) // 2)
     ht = w.B * w.H * w.T
     NS = (w.T + L - 1) // L
     state = (2 * n * w.dv + n) * ht
@@ -224,8 +226,53 @@ def bench_quadratic(kata, dev, Ts=(4096, 16384, 32768), reps=5):
     return {"config": "B1 H16 d64 dv64 bf16, C64 for the chunked form", "rows": rows}
 
 
-KERNELS = {"span_state": "span_state_kernel", "scan": "scan_exclusive_bf16",
-           "span_output": "span_output_kernel"}
+def bench_m2(kata, dev, hip, w, q, k, v, steps=10, warmup=3):
+    """KATA-M2 (two 32-dim feature blocks) on the same inputs as the headline
+    line: stage times from HIP events recorded by the library on the launch
+    stream, MFMA rates against the algorithmic work of the M2 feature."""
+    import torch
+    span = 0
+    ws = torch.empty(kata.mg_workspace_bytes(w.B, w.H, w.T, w.d, w.dv, w.C, 2, kata.KATA_BF16,
+                                             span), dtype=torch.uint8, device=dev)
+    out = torch.empty((w.B, w.H, w.T, w.dv), dtype=torch.float32, device=dev)
+    ev = Events(hip, 4 * max(steps, warmup))
+    for i in range(warmup):
+        kata.mg_fwd_chunked_timed(q, k, v, w.C, 2, ev.block(4 * i), out=out, workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        kata.mg_fwd_chunked_timed(q, k, v, w.C, 2, ev.block(4 * i), out=out, workspace=ws)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    names = ("span_state", "scan", "span_output")
+    stage = {nm: sum(ev.elapsed(4 * i + j, 4 * i + j + 1) for i in range(steps)) / steps
+             for j, nm in enumerate(names)}
+    ev.close()
+    L = 1024 if w.T >= 1024 else w.T
+    alg = algorithmic(w, L, g=2)
+    ms = 1e3 * elapsed / steps
+
+    def roof(flop, t_ms):
+        tf = flop / (t_ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+    gbs = alg["scan_bytes"] / (stage["scan"] * 1e-3) / 1e9
+    return {"feature": "KATA-M2: two blocks of 32 coordinates, n = 2 x 528 packed",
+            "tokens_per_s": w.B * w.T / (ms * 1e-3), "ms_per_step": ms,
+            "stages_ms": {nm: round(t, 4) for nm, t in stage.items()},
+            "stage_roofline": {"span_state": roof(alg["state_flop"], stage["span_state"]),
+                               "span_output": roof(alg["output_flop"], stage["span_output"]),
+                               "scan": {"bound": "hbm", "achieved": round(gbs, 1),
+                                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                        "frac": round(gbs / PEAK_HBM_GBS, 4)}},
+            "algorithmic_gflop_per_step": round(alg["total_flop"] / 1e9, 2)}
+
+
+# the KATA-M1 kernels of the d = 64 long-context workload (the M2 and
+# quadratic-form instantiations share the names, not the template arguments)
+KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
+           "scan": "scan_exclusive_bf16<kata::SlotWeight<64, 64, 1> >",
+           "span_output": "span_output_kernel<64, 64, 1, false>"}
 COPY_BYTES = 1 << 30
 
 
@@ -289,8 +336,6 @@ def _per_dispatch(rows, counter, match):
     for r in rows:
         if r["Counter_Name"] != counter or match not in r["Kernel_Name"]:
             continue
-        if ", true>" in r["Kernel_Name"]:  # the quadratic form's output kernel
-            continue
         per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     return (sum(per.values()) / len(per), len(per)) if per else (None, 0)
 
@@ -340,6 +385,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-quadratic", action="store_true")
+    ap.add_argument("--no-m2", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
     ap.add_argument("--ingest-traffic", metavar="DIR",
@@ -450,6 +496,8 @@ def main():
     if not args.no_decode:
         res["decode"] = bench_decode(kata, dev, hip)
         res["practical_hbm"] = hbm_ceiling(dev)
+    if not args.no_m2 and w.d == 64:
+        res["m2"] = bench_m2(kata, dev, hip, w, q, k, v)
     if not args.no_quadratic:
         res["quadratic_vs_chunked"] = bench_quadratic(kata, dev)
     if not args.no_cpu_baseline:
