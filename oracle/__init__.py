@@ -1,5 +1,6 @@
-"""CPU oracle for the causal KATA-M1 forward and decode step, and for the
-block-diagonal KATA-Mg variant (test infrastructure).
+"""CPU oracle for the causal KATA-M1 forward and decode step, for the
+block-diagonal KATA-Mg variant, and for normalised linear attention with the
+linear (n_psi ~ d) feature maps (test infrastructure).
 
 Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product library never does: it
@@ -73,6 +74,17 @@ def load(path: str | None = None):
     lib.kata_oracle_state_mg.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L, _L]
     lib.kata_oracle_decode_step_mg.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp,
                                                _L, _L, _L, _L, _L]
+    lib.kata_oracle_lin_dim.restype = _L
+    lib.kata_oracle_lin_dim.argtypes = [_L, ctypes.c_int]
+    lib.kata_oracle_lin_feature.argtypes = [_dp, _L, ctypes.c_int, ctypes.c_double, _dp]
+    lib.kata_oracle_lin_fwd.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L,
+                                        ctypes.c_int, ctypes.c_double, ctypes.c_int]
+    lib.kata_oracle_lin_fwd_rows.argtypes = [_dp, _dp, _dp, _L, _L, _L, _L, _L,
+                                             ctypes.c_int, ctypes.c_double, ctypes.c_int,
+                                             _lp, _lp, _L, _dp]
+    lib.kata_oracle_lin_fwd_chunked.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L,
+                                                _L, ctypes.c_int, ctypes.c_double,
+                                                ctypes.c_int, ctypes.c_int]
     if path is None:
         _lib = lib
     return lib
@@ -240,3 +252,52 @@ class Oracle:
         self.lib.kata_oracle_decode_step_mg(self._p(S), self._p(z), self._p(q), self._p(k),
                                             self._p(v), self._p(out), B, H, d, dv, g)
         return out, S, z
+
+    # ---- linear features (identity, ReLU+eps, ELU+1, Lorentz lift) --------
+
+    LIN_FEATURES = {"identity": 0, "relu": 1, "elu": 2, "lorentz": 3, "lorentz_s": 4}
+
+    def lin_dim(self, d: int, feature: int) -> int:
+        return int(self.lib.kata_oracle_lin_dim(d, feature))
+
+    def lin_feature(self, x, feature: int, eps: float = 0.0):
+        x = self._f64(x)
+        d = x.shape[-1]
+        out = np.empty(self.lin_dim(d, feature))
+        self.lib.kata_oracle_lin_feature(self._p(x), d, feature, eps, self._p(out))
+        return out
+
+    def lin_fwd(self, q, k, v, feature: int, eps: float = 0.0, normalize: bool = True):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        out = np.empty((B, H, T, dv))
+        self.lib.kata_oracle_lin_fwd(self._p(q), self._p(k), self._p(v), self._p(out),
+                                     B, H, T, d, dv, feature, eps, int(normalize))
+        return out
+
+    def lin_fwd_rows(self, q, k, v, feature: int, eps: float, normalize: bool, bh_idx, t_idx):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        bh = np.ascontiguousarray(np.asarray(bh_idx, dtype=np.int64))
+        tt = np.ascontiguousarray(np.asarray(t_idx, dtype=np.int64))
+        assert bh.shape == tt.shape and bh.ndim == 1
+        assert (bh >= 0).all() and (bh < B * H).all() and (tt >= 0).all() and (tt < T).all()
+        out = np.empty((bh.size, dv))
+        self.lib.kata_oracle_lin_fwd_rows(self._p(q), self._p(k), self._p(v), B, H, T, d, dv,
+                                          feature, eps, int(normalize),
+                                          bh.ctypes.data_as(_lp), tt.ctypes.data_as(_lp),
+                                          bh.size, self._p(out))
+        return out
+
+    def lin_fwd_chunked(self, q, k, v, C: int, feature: int, eps: float = 0.0,
+                        normalize: bool = True, scan_mode: int = 1):
+        q, k, v = self._f64(q), self._f64(k), self._f64(v)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        out = np.empty((B, H, T, dv))
+        self.lib.kata_oracle_lin_fwd_chunked(self._p(q), self._p(k), self._p(v), self._p(out),
+                                             B, H, T, d, dv, C, feature, eps, int(normalize),
+                                             scan_mode)
+        return out

@@ -543,3 +543,189 @@ EXPORT void kata_oracle_decode_step_mg(double* S, double* z, const double* q,
     free(pq);
   }
 }
+
+/* ======================================================================
+ * Linear (n_psi ~ d) features of normalised linear attention (eq. linatt):
+ * the feature maps of section "Classical feature maps", used by the paper's
+ * tree-scan measurements.
+ *   feature 0  identity     psi(x) = x                       n_psi = d
+ *   feature 1  orthant      psi(x) = ReLU(x) + eps           n_psi = d
+ *   feature 2  orthant      psi(x) = ELU(x) + 1              n_psi = d
+ *   feature 3  Lorentz      psi(y) = (y, ||y||_2)            n_psi = d + 1
+ *   feature 4  Lorentz, the appendix variant of the KATA-Lorentz model: with
+ *              y = x_1..x_{d-1} and s = x_d, psi(x) = (y, ||y||_2 (1 + s^2))
+ *                                                            n_psi = d
+ * Output: o_t = N_t / D_t with N_t = sum_{i<=t} w_ti v_i, D_t = sum_{i<=t} w_ti,
+ * w_ti = <psi(q_t), psi(k_i)>, and o_t = 0 unless D_t > 0 (normalize = 1; the
+ * readout is defined for a positive denominator, eq. linatt); or
+ * o_t = N_t (normalize = 0, the unnormalised readout used with psi(x) = x,
+ * whose weights have no sign).
+ * ====================================================================== */
+
+EXPORT long kata_oracle_lin_dim(long d, int feature) { return feature == 3 ? d + 1 : d; }
+
+EXPORT void kata_oracle_lin_feature(const double* x, long d, int feature, double eps,
+                                    double* out) {
+  if (feature == 3) {
+    double s = 0.0;
+    for (long a = 0; a < d; ++a) {
+      out[a] = x[a];
+      s += x[a] * x[a];
+    }
+    out[d] = sqrt(s);
+    return;
+  }
+  if (feature == 4) {
+    double s = 0.0;
+    for (long a = 0; a + 1 < d; ++a) {
+      out[a] = x[a];
+      s += x[a] * x[a];
+    }
+    out[d - 1] = sqrt(s) * (1.0 + x[d - 1] * x[d - 1]);
+    return;
+  }
+  for (long a = 0; a < d; ++a) {
+    double y = x[a];
+    if (feature == 1) y = (y > 0.0 ? y : 0.0) + eps;
+    else if (feature == 2) y = (y > 0.0 ? y : exp(y) - 1.0) + 1.0;
+    out[a] = y;
+  }
+}
+
+static void lin_definition_row(const double* q, const double* k, const double* v, long t,
+                               long d, long dv, int feature, double eps, int normalize,
+                               double* fq, double* fk, double* o) {
+  long n = kata_oracle_lin_dim(d, feature);
+  double D = 0.0;
+  for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  kata_oracle_lin_feature(q + t * d, d, feature, eps, fq);
+  for (long i = 0; i <= t; ++i) {
+    kata_oracle_lin_feature(k + i * d, d, feature, eps, fk);
+    double w = 0.0;
+    for (long f = 0; f < n; ++f) w += fq[f] * fk[f];
+    D += w;
+    const double* vi = v + i * dv;
+    for (long j = 0; j < dv; ++j) o[j] += w * vi[j];
+  }
+  if (!normalize) return;
+  if (D > 0.0) {
+    for (long j = 0; j < dv; ++j) o[j] /= D;
+  } else {
+    for (long j = 0; j < dv; ++j) o[j] = 0.0;
+  }
+}
+
+/* Definition forward, O(T^2) per head. */
+EXPORT void kata_oracle_lin_fwd(const double* q, const double* k, const double* v, double* out,
+                                long B, long H, long T, long d, long dv, int feature, double eps,
+                                int normalize) {
+  long BH = B * H;
+  long n = kata_oracle_lin_dim(d, feature);
+#pragma omp parallel
+  {
+    double* fq = (double*)malloc((size_t)n * sizeof(double));
+    double* fk = (double*)malloc((size_t)n * sizeof(double));
+#pragma omp for collapse(2) schedule(dynamic, 16)
+    for (long bh = 0; bh < BH; ++bh)
+      for (long t = 0; t < T; ++t)
+        lin_definition_row(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t, d, dv, feature,
+                           eps, normalize, fq, fk, out + (bh * T + t) * dv);
+    free(fq);
+    free(fk);
+  }
+}
+
+EXPORT void kata_oracle_lin_fwd_rows(const double* q, const double* k, const double* v, long B,
+                                     long H, long T, long d, long dv, int feature, double eps,
+                                     int normalize, const long* bh_idx, const long* t_idx,
+                                     long nrows, double* out) {
+  (void)B; (void)H;
+  long n = kata_oracle_lin_dim(d, feature);
+#pragma omp parallel
+  {
+    double* fq = (double*)malloc((size_t)n * sizeof(double));
+    double* fk = (double*)malloc((size_t)n * sizeof(double));
+#pragma omp for schedule(dynamic, 1)
+    for (long r = 0; r < nrows; ++r) {
+      long bh = bh_idx[r];
+      lin_definition_row(q + bh * T * d, k + bh * T * d, v + bh * T * dv, t_idx[r], d, dv,
+                         feature, eps, normalize, fq, fk, out + r * dv);
+    }
+    free(fq);
+    free(fk);
+  }
+}
+
+/* Chunkwise form (eq. chunk-SZ, eq. chunk-out) with a linear feature: local
+ * chunk states S_loc = psi(K_c)^T V_c, z_loc = psi(K_c)^T 1, their exclusive
+ * prefix (scan_mode 0 sequential, 1 tree), and per chunk
+ *   N = psi(Q_c) S_[c] + (psi(Q_c) psi(K_c)^T .* M) V_c,
+ *   D = psi(Q_c) z_[c] + (psi(Q_c) psi(K_c)^T .* M) 1, O = N / D (or N). */
+EXPORT void kata_oracle_lin_fwd_chunked(const double* q, const double* k, const double* v,
+                                        double* out, long B, long H, long T, long d, long dv,
+                                        long C, int feature, double eps, int normalize,
+                                        int scan_mode) {
+  long n = kata_oracle_lin_dim(d, feature);
+  long NC = (T + C - 1) / C;
+  long BH = B * H;
+  long SE = n * dv + n;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    const double* Q = q + bh * T * d;
+    const double* K = k + bh * T * d;
+    const double* V = v + bh * T * dv;
+    double* O = out + bh * T * dv;
+    double* FQ = (double*)calloc((size_t)(C * n), sizeof(double));
+    double* FK = (double*)calloc((size_t)(C * n), sizeof(double));
+    double* Vc = (double*)calloc((size_t)(C * dv), sizeof(double));
+    double* states = (double*)calloc((size_t)(NC * SE), sizeof(double));
+    for (long pass = 0; pass < 2; ++pass) {
+      for (long c = 0; c < NC; ++c) {
+        long t0 = c * C;
+        memset(FQ, 0, (size_t)(C * n) * sizeof(double));
+        memset(FK, 0, (size_t)(C * n) * sizeof(double));
+        memset(Vc, 0, (size_t)(C * dv) * sizeof(double));
+        /* rows past T stay zero: a padded key has no feature (weight 0) */
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          kata_oracle_lin_feature(Q + (t0 + r) * d, d, feature, eps, FQ + r * n);
+          kata_oracle_lin_feature(K + (t0 + r) * d, d, feature, eps, FK + r * n);
+          memcpy(Vc + r * dv, V + (t0 + r) * dv, (size_t)dv * sizeof(double));
+        }
+        double* St = states + c * SE;
+        if (pass == 0) {
+          for (long f = 0; f < n; ++f) {
+            for (long j = 0; j < dv; ++j) {
+              double s = 0.0;
+              for (long r = 0; r < C; ++r) s += FK[r * n + f] * Vc[r * dv + j];
+              St[f * dv + j] = s;
+            }
+            double zs = 0.0;
+            for (long r = 0; r < C; ++r) zs += FK[r * n + f];
+            St[n * dv + f] = zs;
+          }
+          continue;
+        }
+        for (long r = 0; r < C && t0 + r < T; ++r) {
+          double D = 0.0;
+          for (long f = 0; f < n; ++f) D += FQ[r * n + f] * St[n * dv + f];
+          for (long j = 0; j < dv; ++j) {
+            double acc = 0.0;
+            for (long f = 0; f < n; ++f) acc += FQ[r * n + f] * St[f * dv + j];
+            O[(t0 + r) * dv + j] = acc;
+          }
+          for (long s = 0; s <= r; ++s) {
+            double w = 0.0;
+            for (long f = 0; f < n; ++f) w += FQ[r * n + f] * FK[s * n + f];
+            D += w;
+            for (long j = 0; j < dv; ++j) O[(t0 + r) * dv + j] += w * Vc[s * dv + j];
+          }
+          if (normalize)
+            for (long j = 0; j < dv; ++j)
+              O[(t0 + r) * dv + j] = (D > 0.0) ? O[(t0 + r) * dv + j] / D : 0.0;
+        }
+      }
+      if (pass == 0) kata_oracle_scan_exclusive(states, NC, SE, scan_mode);
+    }
+    free(FQ); free(FK); free(Vc); free(states);
+  }
+}

@@ -478,6 +478,175 @@ def pin_mg_rows_match_full(orc):
     assert np.array_equal(orc.fwd_mg_rows(q, k, v, 2, bh, tt), full[bh, tt])
 
 
+# ---------------------------------------------------------------------------
+# PIN: linear (n_psi ~ d) features of normalised linear attention
+# ---------------------------------------------------------------------------
+
+LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S = 0, 1, 2, 3, 4
+
+
+def _lib_features(x, feature, eps):
+    """Feature rows from library routines (torch's relu/elu, numpy's norm),
+    independent of the oracle's scalar feature code; x: [T, d]."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if feature == LIN_IDENTITY:
+        return x.copy()
+    if feature == LIN_RELU:
+        return (torch.relu(t) + eps).numpy()
+    if feature == LIN_ELU:
+        return (torch.nn.functional.elu(t) + 1.0).numpy()
+    if feature == LIN_LORENTZ:
+        return np.concatenate([x, np.linalg.norm(x, axis=-1, keepdims=True)], axis=-1)
+    y, s = x[:, :-1], x[:, -1:]
+    return np.concatenate([y, np.linalg.norm(y, axis=-1, keepdims=True) * (1.0 + s * s)],
+                          axis=-1)
+
+
+def _brute_lin(q, k, v, feature, eps, normalize):
+    """Matrix form: P = (Psi(Q) Psi(K)^T) .* tril, N = P V, D = P 1."""
+    B, H, T, d = q.shape
+    out = np.zeros(v.shape)
+    mask = np.tril(np.ones((T, T)))
+    for b in range(B):
+        for h in range(H):
+            P = (_lib_features(q[b, h], feature, eps) @ _lib_features(k[b, h], feature, eps).T) * mask
+            N = P @ v[b, h]
+            if not normalize:
+                out[b, h] = N
+                continue
+            D = P.sum(axis=1, keepdims=True)
+            out[b, h] = np.where(D > 0, N / np.where(D > 0, D, 1.0), 0.0)
+    return out
+
+
+def pin_lin_widths(orc):
+    # n_psi printed for the orthant and Lorentz rows of the associative-scan
+    # throughput table at d = 64 (the appendix Lorentz variant keeps d), and
+    # d + 1 for the lift (y, ||y||) of section "Classical feature maps".
+    for f in (LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ_S):
+        assert orc.lin_dim(64, f) == 64
+    assert orc.lin_dim(64, LIN_LORENTZ) == 65
+    for d in (1, 2, 7, 32):
+        assert orc.lin_dim(d, LIN_LORENTZ) == d + 1 and orc.lin_dim(d, LIN_RELU) == d
+
+
+def pin_lin_features(orc):
+    rng = _rng(71)
+    for d in (1, 3, 8, 64):
+        for _ in range(3):
+            x = rng.standard_normal(d) * 2.0
+            for f in (LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S):
+                if f == LIN_LORENTZ_S and d < 2:
+                    continue
+                got = orc.lin_feature(x, f, 1e-3)
+                ref = _lib_features(x[None, :], f, 1e-3)[0]
+                assert np.allclose(got, ref, rtol=1e-15, atol=1e-15), (d, f)
+            # orthant maps land in the open positive orthant
+            assert (orc.lin_feature(x, LIN_RELU, 1e-3) >= 1e-3).all()
+            assert (orc.lin_feature(x, LIN_ELU) > 0).all()
+    # the Lorentz lift: <psi(x), psi(y)> = <x, y> + ||x|| ||y|| >= 0, and for unit
+    # vectors the halved kernel is 1/2 + z/2 (z = <x, y>), ||psi(x)||^2 = 2
+    for _ in range(20):
+        x = rng.standard_normal(9)
+        y = rng.standard_normal(9)
+        px, py = orc.lin_feature(x, LIN_LORENTZ), orc.lin_feature(y, LIN_LORENTZ)
+        ref = x @ y + np.linalg.norm(x) * np.linalg.norm(y)
+        assert abs(px @ py - ref) <= 1e-13 * max(1.0, abs(ref)) and px @ py >= -1e-13
+        xu, yu = x / np.linalg.norm(x), y / np.linalg.norm(y)
+        pxu, pyu = orc.lin_feature(xu, LIN_LORENTZ), orc.lin_feature(yu, LIN_LORENTZ)
+        assert abs(0.5 * (pxu @ pyu) - (0.5 + 0.5 * (xu @ yu))) <= 1e-14
+        assert abs(pxu @ pxu - 2.0) <= 1e-14
+        # appendix variant: inside the closed cone t >= ||y||; s = 0 gives the lift of y
+        ps = orc.lin_feature(x, LIN_LORENTZ_S)
+        assert ps[-1] >= np.linalg.norm(x[:-1]) and ps @ orc.lin_feature(y, LIN_LORENTZ_S) >= 0
+        x0 = x.copy()
+        x0[-1] = 0.0
+        assert np.array_equal(orc.lin_feature(x0, LIN_LORENTZ_S),
+                              orc.lin_feature(x[:-1], LIN_LORENTZ))
+
+
+def pin_lin_brute_force(orc):
+    rng = _rng(73)
+    q, k, v = _rand_qkv(rng, 2, 2, 21, 8, 5, unit=False)
+    for f in (LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S):
+        for norm in ((False,) if f == LIN_IDENTITY else (True, False)):
+            got = orc.lin_fwd(q, k, v, f, 0.05, norm)
+            ref = _brute_lin(q, k, v, f, 0.05, norm)
+            assert np.allclose(got, ref, rtol=1e-11, atol=1e-12), (f, norm)
+
+
+def pin_lin_special_cases(orc):
+    rng = _rng(79)
+    T = 19
+    q, k, v = _rand_qkv(rng, 1, 2, T, 6, 4, unit=True)
+    tril = np.tril(np.ones((T, T)))
+    # unnormalised identity feature: o = tril(Q K^T) V, bilinear in (q, v)
+    ref = np.einsum("bhts,bhsj->bhtj", np.einsum("bhtd,bhsd->bhts", q, k) * tril, v)
+    o = orc.lin_fwd(q, k, v, LIN_IDENTITY, 0.0, False)
+    assert np.allclose(o, ref, rtol=1e-12, atol=1e-13)
+    assert np.allclose(orc.lin_fwd(-2.5 * q, k, v, LIN_IDENTITY, 0.0, False), -2.5 * o,
+                       rtol=1e-12, atol=1e-13)
+    # Lorentz lift on unit vectors: the weight is 1 + <q, k> (section on the dense
+    # associative memory hierarchy gives the halved kernel 1/2 + z/2)
+    w = (1.0 + np.einsum("bhtd,bhsd->bhts", q, k)) * tril
+    ref = np.einsum("bhts,bhsj->bhtj", w, v) / w.sum(axis=-1, keepdims=True)
+    assert np.allclose(orc.lin_fwd(q, k, v, LIN_LORENTZ, 0.0, True), ref, rtol=1e-12, atol=1e-12)
+    # positive features: the first output is v_0, every output lies in the
+    # running hull of the values, identical keys give the running mean
+    for f in (LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S):
+        on = orc.lin_fwd(q, k, v, f, 1e-2, True)
+        assert np.allclose(on[:, :, 0], v[:, :, 0], rtol=1e-13, atol=1e-14)
+        lo = np.minimum.accumulate(v, axis=2)
+        hi = np.maximum.accumulate(v, axis=2)
+        assert np.all(on >= lo - 1e-12) and np.all(on <= hi + 1e-12)
+        ks = np.broadcast_to(k[:, :, :1], k.shape)
+        mean = np.cumsum(v, axis=2) / np.arange(1, T + 1)[None, None, :, None]
+        assert np.allclose(orc.lin_fwd(q, ks, v, f, 1e-2, True), mean, rtol=1e-12, atol=1e-13)
+    # positively homogeneous features (ReLU with eps = 0, the Lorentz lift): a
+    # positive scale of q or k leaves the normalised output unchanged; a rotation
+    # of both leaves the Lorentz output unchanged
+    for f in (LIN_RELU, LIN_LORENTZ):
+        base = orc.lin_fwd(q, k, v, f, 0.0, True)
+        assert np.allclose(orc.lin_fwd(3.0 * q, 0.25 * k, v, f, 0.0, True), base,
+                           rtol=1e-12, atol=1e-12)
+    U, _ = np.linalg.qr(rng.standard_normal((6, 6)))
+    base = orc.lin_fwd(q, k, v, LIN_LORENTZ, 0.0, True)
+    assert np.allclose(orc.lin_fwd(q @ U.T, k @ U.T, v, LIN_LORENTZ, 0.0, True), base,
+                       rtol=1e-12, atol=1e-12)
+    # a query with no positive coordinate has a zero ReLU feature at eps = 0:
+    # the denominator is 0 and the readout is 0
+    qn = -np.abs(q)
+    assert np.array_equal(orc.lin_fwd(qn, k, v, LIN_RELU, 0.0, True), np.zeros(v.shape))
+    # ... while eps > 0 keeps it defined (a uniform-weight mean of the values only
+    # when the keys have no positive coordinate either)
+    kn = -np.abs(k)
+    mean = np.cumsum(v, axis=2) / np.arange(1, T + 1)[None, None, :, None]
+    assert np.allclose(orc.lin_fwd(qn, kn, v, LIN_RELU, 1e-3, True), mean, rtol=1e-12, atol=1e-13)
+
+
+def pin_lin_chunked_equals_definition(orc):
+    rng = _rng(83)
+    q, k, v = _rand_qkv(rng, 1, 2, 29, 6, 3, unit=False)
+    for f in (LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S):
+        norm = f != LIN_IDENTITY
+        ref = orc.lin_fwd(q, k, v, f, 0.01, norm)
+        for C in (1, 3, 8, 29, 40):
+            for mode in (0, 1):
+                got = orc.lin_fwd_chunked(q, k, v, C, f, 0.01, norm, mode)
+                assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), (f, C, mode)
+
+
+def pin_lin_rows_match_full(orc):
+    rng = _rng(89)
+    q, k, v = _rand_qkv(rng, 2, 2, 15, 8, 5, unit=False)
+    bh = rng.integers(0, 4, size=25)
+    tt = rng.integers(0, 15, size=25)
+    for f, norm in ((LIN_IDENTITY, False), (LIN_ELU, True), (LIN_LORENTZ, True)):
+        full = orc.lin_fwd(q, k, v, f, 0.0, norm).reshape(4, 15, 5)
+        assert np.array_equal(orc.lin_fwd_rows(q, k, v, f, 0.0, norm, bh, tt), full[bh, tt])
+
+
 ALL_PINS = [
     pin_packed_sizes, pin_packed_order, pin_phi_identity, pin_worked_example,
     pin_brute_force_unpacked, pin_convex_hull, pin_first_token, pin_gate_recursion,
@@ -487,4 +656,6 @@ ALL_PINS = [
     pin_decode_equals_forward, pin_rows_match_full,
     pin_mg_widths, pin_mg_phi, pin_mg_brute_force, pin_mg_special_cases,
     pin_mg_chunked_equals_definition, pin_mg_decode_equals_forward, pin_mg_rows_match_full,
+    pin_lin_widths, pin_lin_features, pin_lin_brute_force, pin_lin_special_cases,
+    pin_lin_chunked_equals_definition, pin_lin_rows_match_full,
 ]

@@ -14,7 +14,8 @@ from oracle_pin_checks import ALL_PINS
 SRC = os.path.join(os.path.dirname(oracle.__file__), "kata_oracle.c")
 
 # (name, exact text in the oracle, replacement[, which occurrence: 0 = the
-# first, in the KATA-M1 code; 1 = the second, in the KATA-Mg code after it])
+# first, in the KATA-M1 code; 1 = the second, in the KATA-Mg code after it;
+# 2 = the third, in the linear-feature code])
 MUTANTS = [
     ("drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {"),
     ("abs_not_square", "double w = s * s;", "double w = fabs(s);"),
@@ -54,6 +55,29 @@ MUTANTS = [
     ("mg_decode_readout_before_update",
      "    double D = 0.0;\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];",
      "    double D = -pq[0] * pk[0];\n    for (long f = 0; f < n; ++f) D += pq[f] * zh[f];", 1),
+    # linear features
+    ("lin_relu_no_eps", "y = (y > 0.0 ? y : 0.0) + eps;", "y = (y > 0.0 ? y : 0.0);"),
+    ("lin_elu_no_shift", "exp(y) - 1.0", "exp(y)"),
+    ("lin_lorentz_squared_norm", "out[d] = sqrt(s);", "out[d] = s;"),
+    ("lin_lorentz_s_factor", "(1.0 + x[d - 1] * x[d - 1])", "(1.0 + x[d - 1])"),
+    ("lin_lorentz_width", "return feature == 3 ? d + 1 : d;", "return d;"),
+    ("lin_drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {", 2),
+    ("lin_abs_weight", "for (long f = 0; f < n; ++f) w += fq[f] * fk[f];",
+     "for (long f = 0; f < n; ++f) w += fabs(fq[f] * fk[f]);"),
+    ("lin_normalize_flag_inverted", "if (!normalize) return;", "if (normalize) return;"),
+    ("lin_chunk_strict_mask", "for (long s = 0; s <= r; ++s) {", "for (long s = 0; s < r; ++s) {"),
+    ("lin_chunk_drops_prefix_denominator",
+     "for (long f = 0; f < n; ++f) D += FQ[r * n + f] * St[n * dv + f];", ""),
+    ("lin_chunk_z_from_values", "for (long r = 0; r < C; ++r) zs += FK[r * n + f];",
+     "for (long r = 0; r < C; ++r) zs += Vc[r * dv];"),
+    ("lin_state_transposed", "for (long r = 0; r < C; ++r) s += FK[r * n + f] * Vc[r * dv + j];",
+     "for (long r = 0; r < C; ++r) s += FK[r * n + j % n] * Vc[r * dv + f % dv];"),
+    ("lin_readout_query_index",
+     "for (long f = 0; f < n; ++f) acc += FQ[r * n + f] * St[f * dv + j];",
+     "for (long f = 0; f < n; ++f) acc += FQ[f] * St[f * dv + j];"),
+    ("lin_chunk_key_feature_from_query",
+     "kata_oracle_lin_feature(K + (t0 + r) * d, d, feature, eps, FK + r * n);",
+     "kata_oracle_lin_feature(Q + (t0 + r) * d, d, feature, eps, FK + r * n);"),
 ]
 
 
