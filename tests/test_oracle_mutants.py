@@ -104,9 +104,8 @@ def test_mutant_is_caught(mutant, tmp_path):
     nth = mutant[3] if len(mutant) > 3 else 0
     with open(SRC) as f:
         text = f.read()
-    # the site must exist, and (for the first occurrence) be the KATA-M1 one
-    assert text.count(old) == nth + 1 or (nth == 0 and text.count(old) >= 1), \
-        f"mutation site {nth} for {name} not found"
+    # the site must exist (occurrences follow the file: KATA-M1, KATA-Mg, linear)
+    assert text.count(old) >= nth + 1, f"mutation site {nth} for {name} not found"
     src = tmp_path / "mutant.c"
     src.write_text(_replace_nth(text, old, new, nth))
     lib_path = str(tmp_path / "libmutant.so")
