@@ -210,6 +210,67 @@ KATA_API kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, co
                                            const void* v, float* out, int B, int H, int d, int dv,
                                            int g, kata_dtype_t dtype, hipStream_t stream);
 
+/*
+ * Causal linear attention with a linear (n_psi ~ d) feature map: the orthant
+ * maps and the Lorentz lift of section "Classical feature maps", the n_psi = d
+ * Lorentz variant of the appendix KATA-Lorentz model, and the plain feature
+ * psi(x) = x of the associative-scan measurements (appendix "Associative-scan
+ * kernel", table of small-batch associative-scan throughput).  With
+ * w_ti = <psi(q_t), psi(k_i)>:
+ *     normalize = 1:  o_t = sum_{i<=t} w_ti v_i / sum_{i<=t} w_ti   (eq. linatt),
+ *                     and o_t = 0 when the denominator is not positive;
+ *     normalize = 0:  o_t = sum_{i<=t} w_ti v_i  (unnormalised; the usual
+ *                     choice for KATA_LIN_IDENTITY, whose weights carry a sign).
+ * Computed in the three-stage chunk-state / associative-scan / chunk-output
+ * form (paragraph "Three-kernel pipeline" of that appendix).
+ *   feature : a kata_lin_feature_t; eps (>= 0, finite) is used by
+ *             KATA_LIN_RELU only.  n_psi = kata_lin_dim(d, feature).
+ *   Fast path (bf16 MFMA): dtype = KATA_BF16, d = dv = 64, n_psi = d (every
+ *   feature but KATA_LIN_LORENTZ), C a multiple of 64 up to 1024.  Every
+ *   other shape with d <= 64, dv <= 256 and C <= 128 runs on the fp32 path;
+ *   anything else is KATA_ERR_UNSUPPORTED.
+ *   span_chunks, workspace, stage_events: as for kata_fwd_chunked_ws and
+ *   kata_fwd_chunked_timed (records of span_chunks * C tokens on the fast
+ *   path; one per chunk on the fp32 path).  Tensors, ownership, errors and
+ *   asynchrony as in the conventions at the top of this file.
+ */
+typedef enum {
+  KATA_LIN_IDENTITY = 0,  /* psi(x) = x                                  n_psi = d     */
+  KATA_LIN_RELU = 1,      /* psi(x) = ReLU(x) + eps                      n_psi = d     */
+  KATA_LIN_ELU = 2,       /* psi(x) = ELU(x) + 1                         n_psi = d     */
+  KATA_LIN_LORENTZ = 3,   /* psi(x) = (x, ||x||_2)                       n_psi = d + 1 */
+  KATA_LIN_LORENTZ_S = 4  /* psi(x) = (y, ||y||_2 (1 + s^2)), y = x_1..x_{d-1},
+                             s = x_d                                     n_psi = d     */
+} kata_lin_feature_t;
+
+/* n_psi of a feature at width d (0 when d < 1 or the feature is unknown). */
+KATA_API int kata_lin_dim(int d, kata_lin_feature_t feature);
+KATA_API kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v,
+                                            float* out, int B, int H, int T, int d, int dv,
+                                            int C, kata_lin_feature_t feature, float eps,
+                                            int normalize, kata_dtype_t dtype,
+                                            hipStream_t stream);
+KATA_API kata_status_t kata_lin_fwd_chunked_ws(const void* q, const void* k, const void* v,
+                                               float* out, int B, int H, int T, int d, int dv,
+                                               int C, kata_lin_feature_t feature, float eps,
+                                               int normalize, kata_dtype_t dtype,
+                                               int span_chunks, void* workspace,
+                                               size_t workspace_bytes, hipStream_t stream);
+KATA_API kata_status_t kata_lin_fwd_chunked_timed(const void* q, const void* k, const void* v,
+                                                  float* out, int B, int H, int T, int d, int dv,
+                                                  int C, kata_lin_feature_t feature, float eps,
+                                                  int normalize, kata_dtype_t dtype,
+                                                  int span_chunks, void* workspace,
+                                                  size_t workspace_bytes,
+                                                  hipEvent_t* stage_events, hipStream_t stream);
+/* Workspace bytes for these arguments (0 when invalid or unsupported). */
+KATA_API size_t kata_lin_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C,
+                                             kata_lin_feature_t feature, kata_dtype_t dtype,
+                                             int span_chunks);
+/* The span (in chunks) that span_chunks = 0 selects (0 when invalid or unsupported). */
+KATA_API int kata_lin_default_span(int B, int H, int T, int d, int dv, int C,
+                                   kata_lin_feature_t feature, kata_dtype_t dtype);
+
 /* Static, human-readable name of a status code. */
 KATA_API const char* kata_status_string(kata_status_t s);
 

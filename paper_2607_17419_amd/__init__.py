@@ -33,8 +33,13 @@ EXPORTED = (
     "kata_mg_fwd_chunked", "kata_mg_fwd_chunked_ws", "kata_mg_fwd_chunked_timed",
     "kata_mg_fwd_workspace_bytes", "kata_mg_fwd_quadratic_ws",
     "kata_mg_fwd_quadratic_workspace_bytes", "kata_mg_prefill_state", "kata_mg_decode_step",
+    "kata_lin_dim", "kata_lin_fwd_chunked", "kata_lin_fwd_chunked_ws",
+    "kata_lin_fwd_chunked_timed", "kata_lin_fwd_workspace_bytes", "kata_lin_default_span",
     "kata_status_string", "kata_abi_version",
 )
+
+# kata_lin_feature_t
+LIN_IDENTITY, LIN_RELU, LIN_ELU, LIN_LORENTZ, LIN_LORENTZ_S = 0, 1, 2, 3, 4
 
 
 class KataError(RuntimeError):
@@ -93,6 +98,21 @@ def lib():
     L.kata_mg_prefill_state.restype = i
     L.kata_mg_decode_step.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp]
     L.kata_mg_decode_step.restype = i
+    f = ctypes.c_float
+    L.kata_lin_dim.argtypes = [i, i]
+    L.kata_lin_dim.restype = i
+    L.kata_lin_fwd_chunked.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, vp]
+    L.kata_lin_fwd_chunked.restype = i
+    L.kata_lin_fwd_chunked_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, i, vp,
+                                          sz, vp]
+    L.kata_lin_fwd_chunked_ws.restype = i
+    L.kata_lin_fwd_chunked_timed.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, i, i, vp,
+                                             sz, vp, vp]
+    L.kata_lin_fwd_chunked_timed.restype = i
+    L.kata_lin_fwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i, i]
+    L.kata_lin_fwd_workspace_bytes.restype = sz
+    L.kata_lin_default_span.argtypes = [i, i, i, i, i, i, i, i]
+    L.kata_lin_default_span.restype = i
     L.kata_status_string.argtypes = [i]
     L.kata_status_string.restype = ctypes.c_char_p
     L.kata_abi_version.argtypes = []
@@ -402,4 +422,58 @@ def mg_decode_step(S, z, q, k, v, g: int, out=None, stream=None):
                                      _dev(v, "v"), _dev(out, "out"), B, H, d, dv, g,
                                      _dtype_code(q), _stream(stream, q.device)),
            "kata_mg_decode_step")
+    return out
+
+
+# ---- linear features --------------------------------------------------------
+
+def lin_dim(d: int, feature: int) -> int:
+    return int(lib().kata_lin_dim(d, feature))
+
+
+def lin_workspace_bytes(B, H, T, d, dv, C, feature, dtype_code, span_chunks=0) -> int:
+    return int(lib().kata_lin_fwd_workspace_bytes(B, H, T, d, dv, C, feature, dtype_code,
+                                                  span_chunks))
+
+
+def lin_default_span(B, H, T, d, dv, C, feature, dtype_code) -> int:
+    return int(lib().kata_lin_default_span(B, H, T, d, dv, C, feature, dtype_code))
+
+
+def lin_fwd_chunked(q, k, v, C: int, feature: int, eps: float = 0.0, normalize: bool = True,
+                    span_chunks: int = 0, out=None, workspace=None, stream=None, events=None):
+    """Causal linear attention with a linear feature map via kata_lin_fwd_chunked_ws
+    (or kata_lin_fwd_chunked_timed when `events`, a ctypes array of 4 HIP events,
+    is given); returns out [B,H,T,dv] fp32."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    nbytes = lin_workspace_bytes(B, H, T, d, dv, C, feature, code, span_chunks)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    args = (_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), B, H, T, d, dv, C,
+            feature, float(eps), int(normalize), code, span_chunks, _dev(workspace, "workspace"),
+            workspace.numel())
+    if events is None:
+        _check(lib().kata_lin_fwd_chunked_ws(*args, _stream(stream, q.device)),
+               "kata_lin_fwd_chunked_ws")
+    else:
+        _check(lib().kata_lin_fwd_chunked_timed(*args, events, _stream(stream, q.device)),
+               "kata_lin_fwd_chunked_timed")
+    return out
+
+
+def lin_fwd_chunked_alloc(q, k, v, C: int, feature: int, eps: float = 0.0,
+                          normalize: bool = True, out=None, stream=None):
+    """The same forward via kata_lin_fwd_chunked (stream-ordered library workspace)."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_lin_fwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                      B, H, T, d, dv, C, feature, float(eps), int(normalize),
+                                      code, _stream(stream, q.device)), "kata_lin_fwd_chunked")
     return out

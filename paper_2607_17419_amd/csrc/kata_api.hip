@@ -4,6 +4,7 @@
 // arguments have been validated.  Every entry point exists for KATA-M1 and,
 // with a feature-block count g (kata_mg_*), for KATA-Mg; g = 1 is M1.
 #include <climits>
+#include <cmath>
 #include <cstdint>
 
 #include "kata.h"
@@ -206,11 +207,75 @@ kata_status_t decode(float* S, float* z, const void* q, const void* k, const voi
   return from_hip(kata::launch_decode<kata::bf16_t>(S, z, q, k, v, out, BH, d, dv, g, stream));
 }
 
+// ---- linear features ----------------------------------------------------------
+
+Path lin_path(int B, int H, int T, int d, int dv, int C, int feature, float eps, int normalize,
+              int dtype) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1 || C < 1) return Path::kInvalid;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return Path::kInvalid;
+  if (feature < kata::kLinIdentity || feature > kata::kLinLorentzS) return Path::kInvalid;
+  if (!std::isfinite(eps) || eps < 0.f) return Path::kInvalid;
+  if (normalize != 0 && normalize != 1) return Path::kInvalid;
+  if (!product_ok(B, H, T, d + 1 > dv ? d + 1 : dv)) return Path::kInvalid;
+  if (static_cast<long long>(B) * H > kGridYZ) return Path::kUnsupported;
+  if (dtype == KATA_BF16 && kata::lin_mfma_supported(d, dv, C, feature)) return Path::kMfma;
+  if (d > 64 || dv > 256 || C > 128) return Path::kUnsupported;
+  if ((static_cast<long long>(T) + C - 1) / C * ((C + 31) / 32) > INT_MAX) return Path::kUnsupported;
+  return Path::kFp32;
+}
+
+// Default span on the MFMA path: about 1024 workgroups per launch (four per
+// compute unit) while a span stays within 1024 tokens.
+int lin_default_span(int B, int H, int T, int C, Path path) {
+  if (path != Path::kMfma) return 1;
+  const long long per_wg = static_cast<long long>(T) * B * H / 1024;
+  long long s = per_wg / C;
+  if (s > 1024 / C) s = 1024 / C;
+  return s < 1 ? 1 : static_cast<int>(s);
+}
+
+size_t lin_workspace_for(Path p, int B, int H, int T, int d, int dv, int C, int feature,
+                         int span_chunks) {
+  if (p == Path::kFp32) return kata::lin_fp32_workspace(B * H, T, d, dv, C, feature);
+  if (p == Path::kMfma) return kata::lin_mfma_workspace(B * H, T, span_tokens(T, C, span_chunks));
+  return 0;
+}
+
+kata_status_t lin_ws(const void* q, const void* k, const void* v, float* out, int B, int H, int T,
+                     int d, int dv, int C, int feature, float eps, int normalize,
+                     kata_dtype_t dtype, int span_chunks, void* workspace, size_t workspace_bytes,
+                     hipEvent_t* ev, hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  if (span_chunks < 0) return KATA_ERR_INVALID_ARG;
+  const Path p = lin_path(B, H, T, d, dv, C, feature, eps, normalize, dtype);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (span_chunks == 0) span_chunks = lin_default_span(B, H, T, C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  if (workspace_bytes < lin_workspace_for(p, B, H, T, d, dv, C, feature, span_chunks))
+    return KATA_ERR_INVALID_ARG;
+  const int BH = B * H;
+  if (p == Path::kMfma) {
+    const int L = span_tokens(T, C, span_chunks);
+    if (static_cast<long long>(BH) * ((static_cast<long long>(T) + L - 1) / L) > INT_MAX)
+      return KATA_ERR_UNSUPPORTED;
+    return from_hip(kata::launch_lin_mfma(q, k, v, out, BH, T, feature, eps, normalize, L,
+                                          workspace, stream, ev));
+  }
+  if (dtype == KATA_F32)
+    return from_hip(kata::launch_lin_fp32<float>(q, k, v, out, BH, T, d, dv, C, feature, eps,
+                                                 normalize, workspace, stream, ev));
+  return from_hip(kata::launch_lin_fp32<kata::bf16_t>(q, k, v, out, BH, T, d, dv, C, feature, eps,
+                                                      normalize, workspace, stream, ev));
+}
+
 }  // namespace
 
 extern "C" {
 
-int kata_abi_version(void) { return 101; }
+int kata_abi_version(void) { return 102; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (s) {
@@ -345,6 +410,72 @@ kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, const void*
                                   float* out, int B, int H, int d, int dv, int g,
                                   kata_dtype_t dtype, hipStream_t stream) {
   return decode(S, z, q, k, v, out, B, H, d, dv, g, dtype, stream);
+}
+
+// ---- linear features -----------------------------------------------------------
+
+int kata_lin_dim(int d, kata_lin_feature_t feature) {
+  if (d < 1 || feature < KATA_LIN_IDENTITY || feature > KATA_LIN_LORENTZ_S) return 0;
+  return kata::lin_dim(d, feature);
+}
+
+int kata_lin_default_span(int B, int H, int T, int d, int dv, int C, kata_lin_feature_t feature,
+                          kata_dtype_t dtype) {
+  const Path p = lin_path(B, H, T, d, dv, C, feature, 0.f, 1, dtype);
+  if (p == Path::kInvalid || p == Path::kUnsupported) return 0;
+  return lin_default_span(B, H, T, C, p);
+}
+
+size_t kata_lin_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C,
+                                    kata_lin_feature_t feature, kata_dtype_t dtype,
+                                    int span_chunks) {
+  const Path p = lin_path(B, H, T, d, dv, C, feature, 0.f, 1, dtype);
+  if (p == Path::kInvalid || p == Path::kUnsupported || span_chunks < 0) return 0;
+  if (span_chunks == 0) span_chunks = lin_default_span(B, H, T, C, p);
+  if (p == Path::kFp32) span_chunks = 1;
+  return lin_workspace_for(p, B, H, T, d, dv, C, feature, span_chunks);
+}
+
+kata_status_t kata_lin_fwd_chunked_ws(const void* q, const void* k, const void* v, float* out,
+                                      int B, int H, int T, int d, int dv, int C,
+                                      kata_lin_feature_t feature, float eps, int normalize,
+                                      kata_dtype_t dtype, int span_chunks, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream) {
+  return lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype, span_chunks,
+                workspace, workspace_bytes, nullptr, stream);
+}
+
+kata_status_t kata_lin_fwd_chunked_timed(const void* q, const void* k, const void* v, float* out,
+                                         int B, int H, int T, int d, int dv, int C,
+                                         kata_lin_feature_t feature, float eps, int normalize,
+                                         kata_dtype_t dtype, int span_chunks, void* workspace,
+                                         size_t workspace_bytes, hipEvent_t* stage_events,
+                                         hipStream_t stream) {
+  if (!stage_events) return KATA_ERR_INVALID_ARG;
+  for (int i = 0; i < 4; ++i)
+    if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
+  return lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype, span_chunks,
+                workspace, workspace_bytes, stage_events, stream);
+}
+
+kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
+                                   int H, int T, int d, int dv, int C, kata_lin_feature_t feature,
+                                   float eps, int normalize, kata_dtype_t dtype,
+                                   hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const Path p = lin_path(B, H, T, d, dv, C, feature, eps, normalize, dtype);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  const int span = lin_default_span(B, H, T, C, p);
+  const size_t bytes = lin_workspace_for(p, B, H, T, d, dv, C, feature, span);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  const kata_status_t st = lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype,
+                                  span, ws, bytes, nullptr, stream);
+  const hipError_t fe = hipFreeAsync(ws, stream);
+  if (st != KATA_OK) return st;
+  return from_hip(fe);
 }
 
 }  // extern "C"

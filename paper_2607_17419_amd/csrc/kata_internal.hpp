@@ -48,6 +48,23 @@ size_t mfma_quadratic_workspace(int BH, int T, int dv);
 hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
                                  int T, int d, int dv, int g, void* ws, hipStream_t st);
 
+// ---- linear features (kata_linear.hip) ------------------------------------
+// feature codes of kata_lin_feature_t
+constexpr int kLinIdentity = 0, kLinRelu = 1, kLinElu = 2, kLinLorentz = 3, kLinLorentzS = 4;
+__host__ __device__ inline int lin_dim(int d, int feature) {
+  return feature == kLinLorentz ? d + 1 : d;
+}
+size_t lin_fp32_workspace(int BH, int T, int d, int dv, int C, int feature);
+template <typename Tin>
+hipError_t launch_lin_fp32(const void* q, const void* k, const void* v, float* out, int BH, int T,
+                           int d, int dv, int C, int feature, float eps, int normalize, void* ws,
+                           hipStream_t st, hipEvent_t* ev);
+bool lin_mfma_supported(int d, int dv, int C, int feature);
+size_t lin_mfma_workspace(int BH, int T, int L);
+hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* out, int BH, int T,
+                           int feature, float eps, int normalize, int L, void* ws, hipStream_t st,
+                           hipEvent_t* ev);
+
 inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
   return ev ? hipEventRecord(ev[i], st) : hipSuccess;
 }

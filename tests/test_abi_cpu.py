@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 101
+    assert L.kata_abi_version() == 102
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
@@ -174,3 +174,57 @@ def test_mg_workspace_host_logic():
     # quadratic M2 exists, M4 does not
     assert L.kata_mg_fwd_quadratic_workspace_bytes(1, 1, 100, 64, 64, 2, 1) == 64 * 128 * 2
     assert L.kata_mg_fwd_quadratic_workspace_bytes(1, 1, 100, 64, 64, 4, 1) == 0
+
+
+# ---- linear features ----------------------------------------------------------
+
+F_ = ctypes.c_float
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((NUL, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, F_(0.0), 1, 0), 1),     # null q
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 16, 16, 32, 1, F_(0.0), 1, 0), 1),    # T < 1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 5, F_(0.0), 1, 0), 1),    # unknown feature
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, -1, F_(0.0), 1, 0), 1),   # unknown feature
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, F_(-1e-3), 1, 0), 1),  # eps < 0
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, F_(float("nan")), 1, 0), 1),  # eps NaN
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, F_(0.0), 2, 0), 1),    # normalize not 0/1
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, F_(0.0), 1, 3), 1),    # bad dtype
+    ((FAKE, FAKE, FAKE, ctypes.c_void_p(0x10008), 1, 1, 8, 16, 16, 32, 1, F_(0.0), 1, 0), 1),
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 65, 16, 32, 1, F_(0.0), 1, 0), 2),    # d > 64
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 300, 32, 1, F_(0.0), 1, 0), 2),   # dv > 256
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 200, 1, F_(0.0), 1, 0), 2),   # C > 128, fp32
+    ((FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 2048, 0, F_(0.0), 0, 1), 2),  # C > 1024, bf16
+])
+def test_lin_rejects_before_gpu(args, expect):
+    assert kata.lib().kata_lin_fwd_chunked(*args, NUL) == expect
+
+
+def test_lin_workspace_and_span_host_logic():
+    L = kata.lib()
+    assert [L.kata_lin_dim(64, f) for f in range(5)] == [64, 64, 64, 65, 64]
+    assert L.kata_lin_dim(0, 1) == 0 and L.kata_lin_dim(8, 7) == 0
+    # MFMA path (bf16, d = dv = 64, n_psi = d): one fp32 record (S 64 x 64, z 64)
+    # per span and head; the default span folds 1024 tokens at T = 131072
+    # (128 spans x 16 heads = 2048 workgroups) and shrinks for short sequences
+    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 128, 0, 1) == 8
+    assert L.kata_lin_fwd_workspace_bytes(1, 16, 131072, 64, 64, 128, 0, 1, 0) == \
+        16 * 128 * (64 * 64 + 64) * 4
+    assert L.kata_lin_default_span(1, 16, 2048, 64, 64, 128, 0, 1) == 1
+    assert L.kata_lin_default_span(1, 16, 16384, 64, 64, 64, 2, 1) == 4
+    # the Lorentz lift (n_psi = d + 1) runs on the fp32 path: one record per chunk
+    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 128, 3, 1) == 1
+    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 256, 3, 1) == 0  # C > 128 there
+    assert L.kata_lin_fwd_workspace_bytes(1, 2, 1000, 64, 64, 100, 3, 1, 0) == \
+        2 * 10 * (65 * 64 + 65) * 4
+    # fp32 inputs take the fp32 path, whatever the shape
+    assert L.kata_lin_default_span(1, 16, 4096, 64, 64, 64, 0, 0) == 1
+    assert L.kata_lin_fwd_workspace_bytes(1, 16, 4096, 64, 64, 64, 0, 0, 0) == \
+        16 * 64 * (64 * 64 + 64) * 4
+    # workspace too small / misaligned / negative span
+    need = L.kata_lin_fwd_workspace_bytes(1, 1, 256, 64, 64, 64, 1, 1, 0)
+    base = (FAKE, FAKE, FAKE, FAKE, 1, 1, 256, 64, 64, 64, 1, F_(0.01), 1, 1)
+    assert L.kata_lin_fwd_chunked_ws(*base, 0, ctypes.c_void_p(0x100000), need - 1, NUL) == 1
+    assert L.kata_lin_fwd_chunked_ws(*base, 0, ctypes.c_void_p(0x100080), need, NUL) == 1
+    assert L.kata_lin_fwd_chunked_ws(*base, -1, ctypes.c_void_p(0x100000), need, NUL) == 1
+    assert L.kata_lin_fwd_chunked_timed(*base, 0, ctypes.c_void_p(0x100000), need, NUL, NUL) == 1

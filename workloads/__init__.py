@@ -55,6 +55,10 @@ WORKLOADS = {
     "decode_bf16": Workload("decode_bf16", 256, 16, 1024, 64, 64, 64, "bf16", 4,
                             kind="decode", steps=128,
                             note="B256 H16 d64 dv64, 1024-token prefix then 128 steps"),
+    # linear (n_psi = d) features: the shape of the paper's small-batch
+    # associative-scan table (B = 1, H = 16, d_head = 64, C = 128, bf16)
+    "scan_long_bf16": Workload("scan_long_bf16", 1, 16, 131072, 64, 64, 128, "bf16", 5,
+                               note="B1 H16 T131072 d64 dv64 C128, bf16, linear features"),
 }
 
 
