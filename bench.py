@@ -9,8 +9,11 @@ q/k/v with fp32 accumulation, inputs resident in HBM.  Prints ONE JSON line.
 Per-kernel durations are taken live with HIP events recorded on the launch
 stream between the three kernels (kata_fwd_chunked_timed).  The decode
 workload (B=256, H=16, 1024-token prefix, 128 steps) is measured in the same
-run and reported under "decode".  The CPU oracle is timed on a bounded sample
-of rows of the same workload and reported under "cpu_baseline".
+run and reported under "decode"; KATA-M2 under "m2"; the quadratic form
+against the chunked one under "quadratic_vs_chunked"; causal linear attention
+with the linear feature maps (the paper's associative-scan shape, B=1, H=16,
+d=64, C=128) under "linear_features".  The CPU oracle is timed on a bounded
+sample of rows of the same workload and reported under "cpu_baseline".
 """
 from __future__ import annotations
 
@@ -65,9 +68,13 @@ class Events:
             self.hip.hipEventDestroy(e)
 
 
-def source_sha():
+M1_SOURCES = ("kata_mfma.hip", "kata_scan.hpp", "kata_common.hpp")
+LIN_SOURCES = ("kata_linear.hip", "kata_scan.hpp", "kata_common.hpp")
+
+
+def source_sha(files=M1_SOURCES):
     h = hashlib.sha256()
-    for f in ("kata_mfma.hip", "kata_scan.hpp", "kata_common.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2607_17419_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -268,12 +275,118 @@ def bench_m2(kata, dev, hip, w, q, k, v, steps=10, warmup=3):
             "algorithmic_gflop_per_step": round(alg["total_flop"] / 1e9, 2)}
 
 
+# Paper's tree-scan throughput at B = 1, H = 16, d = 64, C = 128, psi(x) = x on
+# an H100 (table of small-batch associative-scan throughput), Mtok/s: context.
+PAPER_TREE_SCAN_H100 = {2048: 19.4, 4096: 39.9, 8192: 44.5, 16384: 47.6, 32768: 49.4,
+                        65536: 67.5, 131072: 69.4}
+LIN_FEATURES = {0: "identity (plain readout)", 1: "relu+eps", 2: "elu+1",
+                4: "lorentz (n_psi = d variant)"}
+
+
+def lin_bytes(B, H, T, d, dv, L):
+    """Algorithmic HBM bytes of the three linear-feature kernels (bf16 q, k, v;
+    fp32 records of S (d x dv) and z (d) per span of L tokens; fp32 output)."""
+    NS = -(-T // L)
+    rec = B * H * NS * (d * dv + d) * 4
+    qk = B * H * T * d * 2
+    vv = B * H * T * dv * 2
+    return {"span_state": qk + vv + rec, "scan": 2 * rec,
+            "span_output": 2 * qk + vv + rec + B * H * T * dv * 4}
+
+
+def linear_traffic():
+    """Calibrated HBM bytes per launch of the psi(x) = x kernels, when the
+    counters were taken on the current linear-kernel sources (else {})."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return {}
+    with open(TRAFFIC_FILE) as f:
+        lin = json.load(f).get("linear", {})
+    if lin.get("source_sha") != source_sha(LIN_SOURCES):
+        return {}
+    return {k: lin[k]["hbm_bytes_per_launch"] for k in LIN_KERNELS if k in lin}
+
+
+def bench_linear(kata, dev, hip, steps=10, warmup=3, probe=False):
+    """Linear-feature causal linear attention (psi(x) = x and the orthant /
+    Lorentz maps) in the state / associative-scan / output pipeline: the
+    paper's small-batch associative-scan shape (B1 H16 d64 C128, bf16), per
+    feature at T = 131072 with per-stage HBM rooflines, and the T sweep of
+    that table for psi(x) = x."""
+    import torch
+    import workloads
+    w = workloads.WORKLOADS["scan_long_bf16"]
+
+    def run(B, H, T, C, feature, q=None, k=None, v=None):
+        if q is None:
+            inp = workloads.make_inputs(w, B=B, H=H, T=T)
+            q, k, v = (upload(inp[n], "bf16", dev) for n in ("q_dev", "k_dev", "v_dev"))
+        norm = feature != 0
+        span = kata.lin_default_span(B, H, T, w.d, w.dv, C, feature, kata.KATA_BF16)
+        ws = torch.empty(max(256, kata.lin_workspace_bytes(B, H, T, w.d, w.dv, C, feature,
+                                                           kata.KATA_BF16, span)),
+                         dtype=torch.uint8, device=dev)
+        out = torch.empty((B, H, T, w.dv), dtype=torch.float32, device=dev)
+        ev = Events(hip, 4 * max(steps, warmup))
+        for i in range(warmup):
+            kata.lin_fwd_chunked(q, k, v, C, feature, 1e-3, norm, span_chunks=span, out=out,
+                                 workspace=ws, events=ev.block(4 * i))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            kata.lin_fwd_chunked(q, k, v, C, feature, 1e-3, norm, span_chunks=span, out=out,
+                                 workspace=ws, events=ev.block(4 * i))
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / steps
+        names = ("span_state", "scan", "span_output")
+        stage = {nm: sum(ev.elapsed(4 * i + j, 4 * i + j + 1) for i in range(steps)) / steps
+                 for j, nm in enumerate(names)}
+        ev.close()
+        return ms, stage, span * C
+
+    inp = workloads.make_inputs(w)
+    q, k, v = (upload(inp[n], "bf16", dev) for n in ("q_dev", "k_dev", "v_dev"))
+    if probe:  # psi(x) = x only, for the counter runs
+        ms, stage, L = run(w.B, w.H, w.T, w.C, 0, q, k, v)
+        return {"probe": "linear identity", "ms_per_step": ms, "span_tokens": L}
+    traffic = linear_traffic()
+    per_feature = {}
+    for f, name in LIN_FEATURES.items():
+        ms, stage, L = run(w.B, w.H, w.T, w.C, f, q, k, v)
+        by = lin_bytes(w.B, w.H, w.T, w.d, w.dv, L)
+        roofs = {}
+        for nm, t in stage.items():
+            gbs = by[nm] / (t * 1e-3) / 1e9
+            roofs[nm] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes": by[nm],
+                         "traffic": traffic.get(nm) if f == 0 else None}
+        per_feature[name] = {"tokens_per_s": w.B * w.T / (ms * 1e-3), "ms_per_step": ms,
+                             "span_tokens": L,
+                             "stages_ms": {nm: round(t, 4) for nm, t in stage.items()},
+                             "stage_roofline": roofs}
+    del q, k, v
+    sweep = []
+    for T in sorted(PAPER_TREE_SCAN_H100):
+        ms, stage, L = run(1, 16, T, w.C, 0)
+        sweep.append({"T": T, "ms": round(ms, 4), "tokens_per_s": T / (ms * 1e-3),
+                      "span_tokens": L, "kernel_ms": round(sum(stage.values()), 4),
+                      "paper_tree_scan_h100_mtok_s": PAPER_TREE_SCAN_H100[T]})
+    return {"workload": f"{w.name}: {w.note}",
+            "inputs": "seeded Gaussian q,k (unit rows), v ~ N(0,1), bf16 RNE; eps = 1e-3",
+            "kernel_source_sha": source_sha(LIN_SOURCES),
+            "features": per_feature, "t_sweep_identity_B1_H16": sweep}
+
+
 # the KATA-M1 kernels of the d = 64 long-context workload (the M2 and
 # quadratic-form instantiations share the names, not the template arguments)
 KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
            "scan": "scan_exclusive_bf16<kata::SlotWeight<64, 64, 1> >",
            "span_output": "span_output_kernel<64, 64, 1, false>"}
 COPY_BYTES = 1 << 30
+# the linear-feature kernels of psi(x) = x (plain readout) at d = dv = 64
+LIN_KERNELS = {"span_state": "lin_span_state<0>",
+               "scan": "scan_exclusive_f32x4<kata::LinUnitWeight>",
+               "span_output": "lin_span_output<0, false>"}
 
 
 def copy_probe():
@@ -369,6 +482,22 @@ def ingest_traffic(root, workload, span):
         res[key] = {"fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
                     "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
                     "hbm_bytes_per_launch": fb + wb}
+    if os.path.isdir(os.path.join(root, "lfetch")) and os.path.isdir(os.path.join(root, "lwrite")):
+        lres = {"source_sha": source_sha(LIN_SOURCES), "workload": "scan_long_bf16",
+                "feature": "identity"}
+        fetch_rows = _counter_rows(os.path.join(root, "lfetch"))
+        write_rows = _counter_rows(os.path.join(root, "lwrite"))
+        for key, match in LIN_KERNELS.items():
+            fk, nf = _per_dispatch(fetch_rows, "FETCH_SIZE", match)
+            wk, nw = _per_dispatch(write_rows, "WRITE_SIZE", match)
+            if fk is None or wk is None:
+                continue
+            fb = fk * 1024.0 * cal["FETCH_SIZE"]["factor"]
+            wb = wk * 1024.0 * cal["WRITE_SIZE"]["factor"]
+            lres[key] = {"fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
+                         "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                         "hbm_bytes_per_launch": fb + wb}
+        res["linear"] = lres
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(res, fh, indent=1)
     print(json.dumps(res, indent=1))
@@ -386,6 +515,9 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-quadratic", action="store_true")
     ap.add_argument("--no-m2", action="store_true")
+    ap.add_argument("--no-linear", action="store_true")
+    ap.add_argument("--linear-probe", action="store_true",
+                    help="only run the psi(x) = x linear-feature forward (for rocprofv3 --pmc)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
     ap.add_argument("--ingest-traffic", metavar="DIR",
@@ -402,6 +534,11 @@ def main():
 
     if args.copy_probe:
         copy_probe()
+        return
+    if args.linear_probe:
+        import paper_2607_17419_amd as kata
+        res = bench_linear(kata, "cuda:0", _hip(), steps=3, warmup=1, probe=True)
+        print(json.dumps(res), flush=True)
         return
 
     import numpy as np
@@ -500,6 +637,8 @@ def main():
         res["m2"] = bench_m2(kata, dev, hip, w, q, k, v)
     if not args.no_quadratic:
         res["quadratic_vs_chunked"] = bench_quadratic(kata, dev)
+    if not args.no_linear:
+        res["linear_features"] = bench_linear(kata, dev, hip)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -218,7 +218,7 @@ Path lin_path(int B, int H, int T, int d, int dv, int C, int feature, float eps,
   if (normalize != 0 && normalize != 1) return Path::kInvalid;
   if (!product_ok(B, H, T, d + 1 > dv ? d + 1 : dv)) return Path::kInvalid;
   if (static_cast<long long>(B) * H > kGridYZ) return Path::kUnsupported;
-  if (dtype == KATA_BF16 && kata::lin_mfma_supported(d, dv, C, feature)) return Path::kMfma;
+  if (dtype == KATA_BF16 && kata::lin_mfma_supported(T, d, dv, C, feature)) return Path::kMfma;
   if (d > 64 || dv > 256 || C > 128) return Path::kUnsupported;
   if ((static_cast<long long>(T) + C - 1) / C * ((C + 31) / 32) > INT_MAX) return Path::kUnsupported;
   return Path::kFp32;

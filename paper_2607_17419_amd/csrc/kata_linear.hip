@@ -225,6 +225,13 @@ constexpr int kLD = 64;   // feature / value width of the MFMA path
 constexpr int kLCH = 64;  // tokens per chunk inside a span
 constexpr int kLS = 72;   // LDS row stride (bf16 elements)
 constexpr long long kLE = static_cast<long long>(kLD) * kLD + kLD;  // record: S then z
+// Raw-buffer descriptor word 3 (32-bit data format, no swizzle) of gfx9-class
+// buffer resources; out-of-range accesses are dropped.
+constexpr int kBufWord3 = 0x00020000;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// Byte offsets into one head's output rows (up to T + 63 rows of 256 bytes)
+// must fit 31 bits.
+constexpr long long kLinMaxT = (1LL << 31) / (kLD * 4) - kLCH;
 
 template <int F>
 __device__ __forceinline__ float lin_psi(float x, float eps) {
@@ -273,19 +280,28 @@ struct LinStage {
   bool live[2];
 };
 
+// Loads are unconditional (a padded token re-reads the last real row; its
+// values are zeroed when used), so that no branch joins a pending load and
+// the loads of the next chunks stay in flight across the current one.
 __device__ __forceinline__ void lin_stage_load(LinStage& s, const uint16_t* kb, const uint16_t* vb,
                                                long long tc, long long tend, int fg, int tp) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const long long t = tc + 2 * tp + i;
     s.live[i] = t < tend;
-    if (s.live[i]) {
-      s.k[i] = *reinterpret_cast<const uint4*>(kb + t * kLD + 8 * fg);
-      s.v[i] = *reinterpret_cast<const uint4*>(vb + t * kLD + 8 * fg);
-    } else {
-      s.k[i] = make_uint4(0u, 0u, 0u, 0u);
-      s.v[i] = make_uint4(0u, 0u, 0u, 0u);
-    }
+    const long long tr = s.live[i] ? t : tend - 1;
+    s.k[i] = *reinterpret_cast<const uint4*>(kb + tr * kLD + 8 * fg);
+    s.v[i] = *reinterpret_cast<const uint4*>(vb + tr * kLD + 8 * fg);
+  }
+}
+
+// Staged value rows as fp32, zero rows for padded tokens.
+__device__ __forceinline__ void lin_stage_values(const LinStage& s, float (*y)[8]) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    unpack8(s.v[i], y[i]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[i][e] = s.live[i] ? y[i][e] : 0.f;
   }
 }
 
@@ -309,10 +325,8 @@ __device__ __forceinline__ void lin_stage_features(const LinStage& s, float (*x)
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[i][e] = lin_psi<F>(x[i][e], eps);
     }
-    if (!s.live[i]) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[i][e] = 0.f;
-    }
+    for (int e = 0; e < 8; ++e) x[i][e] = s.live[i] ? x[i][e] : 0.f;
   }
 }
 
@@ -349,18 +363,23 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   float zp = 0.f;
-  LinStage sg;
-  lin_stage_load(sg, kb, vb, tbeg, tend, fg, tp);
-  for (int ch = 0; ch < nch; ++ch) {
+  // two chunks in flight: chunk ch + 2 is loaded into the registers chunk ch
+  // has just left, right after the barrier that publishes chunk ch
+  LinStage s0, s1;
+  lin_stage_load(s0, kb, vb, tbeg, tend, fg, tp);
+  if (nch > 1) lin_stage_load(s1, kb, vb, tbeg + kLCH, tend, fg, tp);
+  auto step = [&](LinStage& sg, int ch) {
     const int buf = ch & 1;
     float x[2][8], y[2][8];
     lin_stage_features<F>(sg, x, eps, fg);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) unpack8(sg.v[i], y[i]);
+    lin_stage_values(sg, y);
     lin_write_t(kt[buf], x, fg, tp);
     lin_write_t(vt[buf], y, fg, tp);
     __syncthreads();
-    if (ch + 1 < nch) lin_stage_load(sg, kb, vb, tbeg + (ch + 1) * kLCH, tend, fg, tp);
+    // unconditional (the last chunk is re-read near the end), so that no
+    // branch joins the pending loads
+    const int nx = ch + 2 < nch ? ch + 2 : nch - 1;
+    lin_stage_load(sg, kb, vb, tbeg + static_cast<long long>(nx) * kLCH, tend, fg, tp);
 #pragma unroll
     for (int ks = 0; ks < kLCH / 16; ++ks) {
       const bf16x8 a = lds8(&kt[buf][(32 * fb + l32) * kLS + 16 * ks + 8 * h]);
@@ -368,6 +387,10 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
       acc = lin_mfma(a, b, acc);
       if (vb2 == 0) zp += sum8(a);
     }
+  };
+  for (int ch = 0; ch < nch; ch += 2) {
+    step(s0, ch);
+    if (ch + 1 < nch) step(s1, ch + 1);
   }
   float* r = rec + (static_cast<long long>(bh) * NS + sp) * kLE;
 #pragma unroll
@@ -405,12 +428,14 @@ __device__ __forceinline__ void lin_query_features(const uint4* raw, bf16x8* qa,
   for (int kk = 0; kk < 4; ++kk) qa[kk] = pack8(x[kk]);
 }
 
+// A query row past the span end re-reads the last real row (its output is
+// never stored); unconditional, like the staging loads.
 __device__ __forceinline__ void lin_query_load(uint4* raw, const uint16_t* qb, long long t,
                                                long long tend, int h) {
+  const long long tr = t < tend ? t : tend - 1;
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk)
-    raw[kk] = (t < tend) ? *reinterpret_cast<const uint4*>(qb + t * kLD + 16 * kk + 8 * h)
-                         : make_uint4(0u, 0u, 0u, 0u);
+    raw[kk] = *reinterpret_cast<const uint4*>(qb + tr * kLD + 16 * kk + 8 * h);
 }
 
 // ---------------------------------------------------------------------------
@@ -443,6 +468,9 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
   const int fg = tid & 7, tp = tid >> 3;
   const int qb = w >> 1, vb2 = w & 1, fb = w >> 1;
   const long long hoff = static_cast<long long>(bh) * T * kLD;
+  // this head's output rows as a raw buffer of T * 256 bytes
+  const __amdgpu_buffer_rsrc_t orsrc =
+      __builtin_amdgcn_make_buffer_rsrc(out + hoff, 0, T * (kLD * 4), kBufWord3);
   const uint16_t* qh = q + hoff;
   const uint16_t* kh = k + hoff;
   const uint16_t* vh = v + hoff;
@@ -469,31 +497,38 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
   };
   write_state();
 
+  // Chunk ch + 1 is staged into LDS at the end of iteration ch (after the
+  // barrier that retires chunk ch's operands) from registers loaded one
+  // iteration earlier; the loads for chunk ch + 2 follow at once.  Loads are
+  // unconditional (the last chunk is re-read near the end) and stores go
+  // through the buffer unit without a branch, so no control-flow join forces
+  // an early wait on the pending loads.
   LinStage sg;
-  lin_stage_load(sg, kh, vh, tbeg, tend, fg, tp);
   uint4 qraw[4];
-  lin_query_load(qraw, qh, tbeg + 32 * qb + l32, tend, h);
+  bf16x8 qa[4];
+  auto stage_in = [&]() {
+    float x[2][8], y[2][8];
+    lin_stage_features<F>(sg, x, eps, fg);
+    lin_stage_values(sg, y);
+    lin_write_t(kt, x, fg, tp);
+    lin_write_t(vt, y, fg, tp);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      *reinterpret_cast<bf16x8*>(&kr[(2 * tp + i) * kLS + 8 * fg]) = pack8(x[i]);
+    lin_query_features<F>(qraw, qa, eps, h);
+  };
+  auto load_chunk = [&](int c) {
+    const long long tn = tbeg + static_cast<long long>(c < nch ? c : nch - 1) * kLCH;
+    lin_stage_load(sg, kh, vh, tn, tend, fg, tp);
+    lin_query_load(qraw, qh, tn + 32 * qb + l32, tend, h);
+  };
+  load_chunk(0);
+  stage_in();
+  load_chunk(1);
 
   for (int ch = 0; ch < nch; ++ch) {
     const long long tc = tbeg + static_cast<long long>(ch) * kLCH;
-    {
-      float x[2][8], y[2][8];
-      lin_stage_features<F>(sg, x, eps, fg);
-#pragma unroll
-      for (int i = 0; i < 2; ++i) unpack8(sg.v[i], y[i]);
-      lin_write_t(kt, x, fg, tp);
-      lin_write_t(vt, y, fg, tp);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        *reinterpret_cast<bf16x8*>(&kr[(2 * tp + i) * kLS + 8 * fg]) = pack8(x[i]);
-    }
-    bf16x8 qa[4];
-    lin_query_features<F>(qraw, qa, eps, h);
     __syncthreads();
-    if (ch + 1 < nch) {
-      lin_stage_load(sg, kh, vh, tc + kLCH, tend, fg, tp);
-      lin_query_load(qraw, qh, tc + kLCH + 32 * qb + l32, tend, h);
-    }
 
     f32x16 oacc;
 #pragma unroll
@@ -548,13 +583,19 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
 #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[i] *= inv;
     }
-    const long long t = tc + 32 * qb + l32;
-    if (t < tend) {
-      float* o = out + (static_cast<long long>(bh) * T + t) * kLD + 32 * vb2 + 4 * h;
+    {
+      // rows past T fall outside the head's buffer range and are dropped by
+      // the buffer unit (no branch, so the stores never join a pending load)
+      const int ob = static_cast<int>((tc + 32 * qb + l32) * (kLD * 4)) + (32 * vb2 + 4 * h) * 4;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<float4*>(o + 8 * j) =
-            make_float4(oacc[4 * j], oacc[4 * j + 1], oacc[4 * j + 2], oacc[4 * j + 3]);
+      for (int j = 0; j < 4; ++j) {
+        u32x4 d;
+        d[0] = __float_as_uint(oacc[4 * j]);
+        d[1] = __float_as_uint(oacc[4 * j + 1]);
+        d[2] = __float_as_uint(oacc[4 * j + 2]);
+        d[3] = __float_as_uint(oacc[4 * j + 3]);
+        __builtin_amdgcn_raw_buffer_store_b128(d, orsrc, ob + 32 * j, 0, 0);
+      }
     }
 
     // running state += this chunk (read before the barrier, written after)
@@ -572,12 +613,15 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
         if (vb2 == 0 && h == 0) zs[32 * fb + l32] += zp;
         zp = 0.f;
       }
+      stage_in();
+      load_chunk(ch + 2);
     }
   }
 }
 
-bool lin_mfma_supported(int d, int dv, int C, int feature) {
-  return d == kLD && dv == kLD && feature != kLinLorentz && C % kLCH == 0 && C <= 1024;
+bool lin_mfma_supported(int T, int d, int dv, int C, int feature) {
+  return d == kLD && dv == kLD && feature != kLinLorentz && C % kLCH == 0 && C <= 1024 &&
+         T < kLinMaxT;
 }
 
 size_t lin_mfma_workspace(int BH, int T, int L) {
@@ -597,9 +641,9 @@ static hipError_t run_lin_mfma(const void* q, const void* k, const void* v, floa
   lin_span_state<F><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(k),
                                          static_cast<const uint16_t*>(v), rec, T, L, NS, eps);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
-  scan_exclusive<float, LinUnitWeight><<<dim3(static_cast<unsigned>((kLE + kEB - 1) / kEB), BH),
-                                         256, 0, st>>>(rec, rec, NS, kLE, kLE * NS,
-                                                       LinUnitWeight{});
+  scan_exclusive_f32x4<LinUnitWeight>
+      <<<dim3(static_cast<unsigned>((kLE + kEB4 - 1) / kEB4), BH), 256, 0, st>>>(
+          rec, NS, kLE, kLE * NS, LinUnitWeight{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   lin_span_output<F, NORM><<<grid, 256, 0, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),

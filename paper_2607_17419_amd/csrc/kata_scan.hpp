@@ -195,3 +195,104 @@ __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N,
 }
 
 }  // namespace kata
+
+namespace kata {
+
+// ---------------------------------------------------------------------------
+// In-place exclusive prefix over fp32 records, register-blocked like the bf16
+// scan above:  rec[bh][c][e] <- w(e) * sum_{c' < c} rec[bh][c'][e].
+// Thread (column group cg, row group rg) holds 4 elements (one 16-byte
+// access per record) x kRPT4 records; the up-sweep / down-sweep runs over its
+// records in registers, the row-group totals are scanned through LDS, and
+// blocks of kNB4 records are chained by a carry.  All of a thread's loads of
+// a block are issued together.  E must be a multiple of 4.
+// grid (ceil(E / kEB4), BH), block 256.
+// ---------------------------------------------------------------------------
+constexpr int kCG4 = 32;               // column groups of 4 elements
+constexpr int kEB4 = 4 * kCG4;         // elements per workgroup (128)
+constexpr int kRG4 = 256 / kCG4;       // row groups (8)
+constexpr int kRPT4 = 8;               // records per thread and block
+constexpr int kNB4 = kRG4 * kRPT4;     // records per block (64)
+
+template <typename Weight>
+__global__ __launch_bounds__(256) void scan_exclusive_f32x4(float* rec, int N, long long E,
+                                                            long long bh_stride, Weight weight) {
+  __shared__ float4 tot[kRG4][kCG4];
+  const int tid = threadIdx.x;
+  const int cg = tid % kCG4, rg = tid / kCG4;
+  const long long ec = static_cast<long long>(blockIdx.x) * kEB4 + 4 * cg;
+  float* rb = rec + blockIdx.y * bh_stride;
+  const bool active = ec < E;
+  float w[4], carry[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    w[x] = active ? weight(ec + x) : 0.f;
+    carry[x] = 0.f;
+  }
+  for (int r0 = 0; r0 < N; r0 += kNB4) {
+    const int rbase = r0 + rg * kRPT4;
+    float v[kRPT4][4];
+#pragma unroll
+    for (int j = 0; j < kRPT4; ++j) {
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (active && rbase + j < N)
+        a = *reinterpret_cast<const float4*>(rb + static_cast<long long>(rbase + j) * E + ec);
+      v[j][0] = a.x;
+      v[j][1] = a.y;
+      v[j][2] = a.z;
+      v[j][3] = a.w;
+    }
+#pragma unroll
+    for (int d = 1; d < kRPT4; d <<= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kRPT4; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) v[j][x] += v[j - d][x];
+    float gsum[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      gsum[x] = v[kRPT4 - 1][x];
+      v[kRPT4 - 1][x] = 0.f;
+    }
+#pragma unroll
+    for (int d = kRPT4 / 2; d >= 1; d >>= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kRPT4; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const float left = v[j - d][x];
+          v[j - d][x] = v[j][x];
+          v[j][x] += left;
+        }
+    tot[rg][cg] = make_float4(gsum[0], gsum[1], gsum[2], gsum[3]);
+    __syncthreads();
+    float pre[4], blk[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      pre[x] = carry[x];
+      blk[x] = 0.f;
+    }
+#pragma unroll
+    for (int g2 = 0; g2 < kRG4; ++g2) {
+      const float4 t = tot[g2][cg];
+      const float tv[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        if (g2 < rg) pre[x] += tv[x];
+        blk[x] += tv[x];
+      }
+    }
+    __syncthreads();  // tot is rewritten by the next block
+#pragma unroll
+    for (int j = 0; j < kRPT4; ++j) {
+      if (active && rbase + j < N)
+        *reinterpret_cast<float4*>(rb + static_cast<long long>(rbase + j) * E + ec) =
+            make_float4(w[0] * (pre[0] + v[j][0]), w[1] * (pre[1] + v[j][1]),
+                        w[2] * (pre[2] + v[j][2]), w[3] * (pre[3] + v[j][3]));
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x) carry[x] += blk[x];
+  }
+}
+
+}  // namespace kata
