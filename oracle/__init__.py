@@ -1,4 +1,4 @@
-"""CPU oracle for the causal KATA-M1 forward and decode step, for the
+"""CPU oracle for the causal KATA-M1 forward, backward and decode step, for the
 block-diagonal KATA-Mg variant, and for normalised linear attention with the
 linear (n_psi ~ d) feature maps (test infrastructure).
 
@@ -74,6 +74,10 @@ def load(path: str | None = None):
     lib.kata_oracle_state_mg.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L, _L]
     lib.kata_oracle_decode_step_mg.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp,
                                                _L, _L, _L, _L, _L]
+    lib.kata_oracle_bwd_mg.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp, _dp, _L, _L, _L, _L, _L,
+                                       _L]
+    lib.kata_oracle_bwd_chunked_mg.argtypes = [_dp, _dp, _dp, _dp, _dp, _dp, _dp, _L, _L, _L,
+                                               _L, _L, _L, _L, ctypes.c_int]
     lib.kata_oracle_lin_dim.restype = _L
     lib.kata_oracle_lin_dim.argtypes = [_L, ctypes.c_int]
     lib.kata_oracle_lin_feature.argtypes = [_dp, _L, ctypes.c_int, ctypes.c_double, _dp]
@@ -252,6 +256,31 @@ class Oracle:
         self.lib.kata_oracle_decode_step_mg(self._p(S), self._p(z), self._p(q), self._p(k),
                                             self._p(v), self._p(out), B, H, d, dv, g)
         return out, S, z
+
+    # ---- backward of KATA-Mg (g = 1: KATA-M1) ----------------------------
+
+    def bwd_mg(self, q, k, v, dout, g: int = 1):
+        """Gradients (dq, dk, dv) of sum_t <dout_t, o_t> by the definition."""
+        q, k, v, dout = self._f64(q), self._f64(k), self._f64(v), self._f64(dout)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        assert d % g == 0 and dout.shape == v.shape
+        gq, gk, gv = np.empty(q.shape), np.empty(k.shape), np.empty(v.shape)
+        self.lib.kata_oracle_bwd_mg(self._p(q), self._p(k), self._p(v), self._p(dout),
+                                    self._p(gq), self._p(gk), self._p(gv), B, H, T, d, dv, g)
+        return gq, gk, gv
+
+    def bwd_chunked_mg(self, q, k, v, dout, C: int, g: int = 1, scan_mode: int = 1):
+        """The same gradients by the chunked reverse-scan form."""
+        q, k, v, dout = self._f64(q), self._f64(k), self._f64(v), self._f64(dout)
+        B, H, T, d = q.shape
+        dv = v.shape[-1]
+        assert d % g == 0 and dout.shape == v.shape
+        gq, gk, gv = np.empty(q.shape), np.empty(k.shape), np.empty(v.shape)
+        self.lib.kata_oracle_bwd_chunked_mg(self._p(q), self._p(k), self._p(v), self._p(dout),
+                                            self._p(gq), self._p(gk), self._p(gv), B, H, T, d,
+                                            dv, C, g, scan_mode)
+        return gq, gk, gv
 
     # ---- linear features (identity, ReLU+eps, ELU+1, Lorentz lift) --------
 

@@ -729,3 +729,258 @@ EXPORT void kata_oracle_lin_fwd_chunked(const double* q, const double* k, const 
     free(FQ); free(FK); free(Vc); free(states);
   }
 }
+
+/* ======================================================================
+ * Backward of the causal KATA-Mg forward (g = 1 is KATA-M1) for a loss with
+ * output cotangents dout_t = dL/do_t.  With N_t = sum_{i<=t} w_ti v_i,
+ * D_t = sum_{i<=t} w_ti and o_t = N_t / D_t:
+ *     dL/dN_t = a_t = dout_t / D_t,   dL/dD_t = b_t = -<dout_t, o_t> / D_t,
+ *     dL/dw_ti = <a_t, v_i> + b_t                  (i <= t),
+ *     dv_i = sum_{t >= i} w_ti a_t,
+ * and with s_ti,blk = q_t,blk . k_i,blk (w_ti = sum_blk s^2):
+ *     dq_t,blk = sum_{i <= t} 2 (dL/dw_ti) s_ti,blk k_i,blk,
+ *     dk_i,blk = sum_{t >= i} 2 (dL/dw_ti) s_ti,blk q_t,blk.
+ * A row with D_t = 0 has the constant readout 0 (the reading of the forward),
+ * so it contributes nothing: a_t = 0, b_t = 0.
+ * ====================================================================== */
+
+static void head_readout_mg(const double* Q, const double* K, const double* V, long T, long d,
+                            long dv, long g, const double* G, double* A, double* bvec) {
+  /* per token: o_t, D_t from the definition, then a_t (A, T x dv) and b_t */
+  double* o = (double*)malloc((size_t)dv * sizeof(double));
+  long m = d / g;
+  for (long t = 0; t < T; ++t) {
+    double D = 0.0;
+    for (long j = 0; j < dv; ++j) o[j] = 0.0;
+    for (long i = 0; i <= t; ++i) {
+      double w = 0.0;
+      for (long a = 0; a < g; ++a) {
+        double s = 0.0;
+        for (long c = a * m; c < (a + 1) * m; ++c) s += Q[t * d + c] * K[i * d + c];
+        w += s * s;
+      }
+      D += w;
+      for (long j = 0; j < dv; ++j) o[j] += w * V[i * dv + j];
+    }
+    double bt = 0.0;
+    if (D > 0.0) {
+      double go = 0.0;
+      for (long j = 0; j < dv; ++j) {
+        o[j] /= D;
+        go += G[t * dv + j] * o[j];
+        A[t * dv + j] = G[t * dv + j] / D;
+      }
+      bt = -go / D;
+    } else {
+      for (long j = 0; j < dv; ++j) A[t * dv + j] = 0.0;
+    }
+    bvec[t] = bt;
+  }
+  free(o);
+}
+
+EXPORT void kata_oracle_bwd_mg(const double* q, const double* k, const double* v,
+                               const double* dout, double* dq, double* dk, double* dvo, long B,
+                               long H, long T, long d, long dv, long g) {
+  long BH = B * H, m = d / g;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    const double* Q = q + bh * T * d;
+    const double* K = k + bh * T * d;
+    const double* V = v + bh * T * dv;
+    const double* G = dout + bh * T * dv;
+    double* dQ = dq + bh * T * d;
+    double* dK = dk + bh * T * d;
+    double* dV = dvo + bh * T * dv;
+    double* A = (double*)malloc((size_t)(T * dv) * sizeof(double));
+    double* bv = (double*)malloc((size_t)T * sizeof(double));
+    double* s = (double*)malloc((size_t)g * sizeof(double));
+    head_readout_mg(Q, K, V, T, d, dv, g, G, A, bv);
+    memset(dQ, 0, (size_t)(T * d) * sizeof(double));
+    memset(dK, 0, (size_t)(T * d) * sizeof(double));
+    memset(dV, 0, (size_t)(T * dv) * sizeof(double));
+    for (long t = 0; t < T; ++t) {
+      for (long i = 0; i <= t; ++i) {
+        double w = 0.0;
+        for (long a = 0; a < g; ++a) {
+          s[a] = 0.0;
+          for (long c = a * m; c < (a + 1) * m; ++c) s[a] += Q[t * d + c] * K[i * d + c];
+          w += s[a] * s[a];
+        }
+        double cw = bv[t];
+        for (long j = 0; j < dv; ++j) {
+          cw += A[t * dv + j] * V[i * dv + j];
+          dV[i * dv + j] += w * A[t * dv + j];
+        }
+        for (long a = 0; a < g; ++a)
+          for (long c = a * m; c < (a + 1) * m; ++c) {
+            dQ[t * d + c] += 2.0 * cw * s[a] * K[i * d + c];
+            dK[i * d + c] += 2.0 * cw * s[a] * Q[t * d + c];
+          }
+      }
+    }
+    free(A); free(bv); free(s);
+  }
+}
+
+/* Feature-map VJP of the packed block lift: a cotangent Y over the n packed
+ * features (pair (x, y) of a block, x <= y, unscaled) gives
+ *     dx += 2 X x,  X the symmetric d x d block-diagonal matrix with
+ *     X_xy = X_yx = Y_(x,y),
+ * i.e. dx = (dPsi + dPsi^T) x for each block (the chunked backward's closing
+ * step for queries and keys). */
+static void phi_mg_vjp(const double* Y, const double* x, long d, long g, double* dx) {
+  long m = d / g, nm = m * (m + 1) / 2;
+  for (long blk = 0; blk < g; ++blk)
+    for (long a = 0; a < m; ++a)
+      for (long b = a; b < m; ++b) {
+        double y = Y[blk * nm + kata_oracle_packed_index(a, b, m)];
+        long xa = blk * m + a, xb = blk * m + b;
+        if (a == b) {
+          dx[xa] += 2.0 * y * x[xa];
+        } else {
+          dx[xa] += 2.0 * y * x[xb];
+          dx[xb] += 2.0 * y * x[xa];
+        }
+      }
+}
+
+/* Chunkwise backward (the chunked backward of the appendix's chunkwise
+ * algorithm: a reverse scan over chunks carrying the state cotangent, forward
+ * quantities recomputed from the chunk-boundary states, and the feature-map VJP
+ * closing the chain), for the KATA-Mg forward:
+ *   forward:  S_loc, z_loc per chunk, exclusive prefix S_pre, z_pre; per token
+ *             D_t, o_t from the chunk output, then a_t, b_t;
+ *   backward: dS_loc = sum_{t in c} psi(q_t) a_t^T, dz_loc = sum_t b_t psi(q_t);
+ *             exclusive suffix dS_suf[c] = sum_{c' > c} dS_loc[c'] (the scan of
+ *             the reversed sequence of chunks, scan_mode 0 sequential, 1 tree);
+ *   per chunk: dq_t = VJP(S_pre a_t + b_t z_pre) at q_t + in-chunk terms,
+ *              dk_i = VJP(dS_suf v_i + dz_suf) at k_i + in-chunk terms,
+ *              dv_i = dS_suf^T psi_w(k_i) + sum_{t in c, t >= i} w_ti a_t. */
+EXPORT void kata_oracle_bwd_chunked_mg(const double* q, const double* k, const double* v,
+                                       const double* dout, double* dq, double* dk, double* dvo,
+                                       long B, long H, long T, long d, long dv, long C, long g,
+                                       int scan_mode) {
+  long n = kata_oracle_packed_dim_mg(d, g);
+  long NC = (T + C - 1) / C;
+  long BH = B * H, m = d / g;
+  long SE = n * dv + n;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < BH; ++bh) {
+    const double* Q = q + bh * T * d;
+    const double* K = k + bh * T * d;
+    const double* V = v + bh * T * dv;
+    const double* G = dout + bh * T * dv;
+    double* dQ = dq + bh * T * d;
+    double* dK = dk + bh * T * d;
+    double* dV = dvo + bh * T * dv;
+    double* fst = (double*)calloc((size_t)(NC * SE), sizeof(double));
+    double* bst = (double*)calloc((size_t)(NC * SE), sizeof(double));
+    double* A = (double*)calloc((size_t)(T * dv), sizeof(double));
+    double* bv = (double*)calloc((size_t)T, sizeof(double));
+    double* ph = (double*)malloc((size_t)n * sizeof(double));
+    double* pw = (double*)malloc((size_t)n * sizeof(double));
+    double* Y = (double*)malloc((size_t)n * sizeof(double));
+    double* s = (double*)malloc((size_t)g * sizeof(double));
+    /* forward chunk states and their exclusive prefix */
+    for (long t = 0; t < T; ++t) {
+      double* St = fst + (t / C) * SE;
+      kata_oracle_phi_mg(K + t * d, d, g, 0, ph);
+      for (long f = 0; f < n; ++f) {
+        for (long j = 0; j < dv; ++j) St[f * dv + j] += ph[f] * V[t * dv + j];
+        St[n * dv + f] += ph[f];
+      }
+    }
+    kata_oracle_scan_exclusive(fst, NC, SE, scan_mode);
+    /* forward readout per token: D_t, o_t, then a_t, b_t */
+    for (long t = 0; t < T; ++t) {
+      long c = t / C, t0 = c * C;
+      const double* St = fst + c * SE;
+      kata_oracle_phi_mg(Q + t * d, d, g, 1, pw);
+      double D = 0.0, go = 0.0;
+      /* the A row holds N_t first, then a_t */
+      for (long f = 0; f < n; ++f) D += pw[f] * St[n * dv + f];
+      for (long j = 0; j < dv; ++j) {
+        double acc = 0.0;
+        for (long f = 0; f < n; ++f) acc += pw[f] * St[f * dv + j];
+        A[t * dv + j] = acc; /* N_t, inter part */
+      }
+      for (long i = t0; i <= t; ++i) {
+        double w = 0.0;
+        for (long a = 0; a < g; ++a) {
+          double sa = 0.0;
+          for (long x = a * m; x < (a + 1) * m; ++x) sa += Q[t * d + x] * K[i * d + x];
+          w += sa * sa;
+        }
+        D += w;
+        for (long j = 0; j < dv; ++j) A[t * dv + j] += w * V[i * dv + j];
+      }
+      if (D > 0.0) {
+        for (long j = 0; j < dv; ++j) go += G[t * dv + j] * (A[t * dv + j] / D);
+        for (long j = 0; j < dv; ++j) A[t * dv + j] = G[t * dv + j] / D;
+        bv[t] = -go / D;
+      } else {
+        for (long j = 0; j < dv; ++j) A[t * dv + j] = 0.0;
+        bv[t] = 0.0;
+      }
+    }
+    /* backward chunk states, reversed in chunk order, and their exclusive
+     * prefix = the exclusive suffix in the original order */
+    for (long t = 0; t < T; ++t) {
+      double* Bt = bst + (NC - 1 - t / C) * SE;
+      kata_oracle_phi_mg(Q + t * d, d, g, 0, ph);
+      for (long f = 0; f < n; ++f) {
+        for (long j = 0; j < dv; ++j) Bt[f * dv + j] += ph[f] * A[t * dv + j];
+        Bt[n * dv + f] += bv[t] * ph[f];
+      }
+    }
+    kata_oracle_scan_exclusive(bst, NC, SE, scan_mode);
+    memset(dQ, 0, (size_t)(T * d) * sizeof(double));
+    memset(dK, 0, (size_t)(T * d) * sizeof(double));
+    memset(dV, 0, (size_t)(T * dv) * sizeof(double));
+    for (long t = 0; t < T; ++t) {
+      long c = t / C, t0 = c * C;
+      const double* St = fst + c * SE;                 /* S_pre, z_pre */
+      const double* Bs = bst + (NC - 1 - c) * SE;      /* dS_suf, dz_suf */
+      /* inter-chunk terms of token t as a query, then as a key */
+      for (long f = 0; f < n; ++f) {
+        double y = bv[t] * St[n * dv + f];
+        for (long j = 0; j < dv; ++j) y += St[f * dv + j] * A[t * dv + j];
+        Y[f] = y;
+      }
+      phi_mg_vjp(Y, Q + t * d, d, g, dQ + t * d);
+      for (long f = 0; f < n; ++f) {
+        double y = Bs[n * dv + f];
+        for (long j = 0; j < dv; ++j) y += Bs[f * dv + j] * V[t * dv + j];
+        Y[f] = y;
+      }
+      phi_mg_vjp(Y, K + t * d, d, g, dK + t * d);
+      kata_oracle_phi_mg(K + t * d, d, g, 1, pw);
+      for (long j = 0; j < dv; ++j) {
+        double acc = 0.0;
+        for (long f = 0; f < n; ++f) acc += pw[f] * Bs[f * dv + j];
+        dV[t * dv + j] += acc;
+      }
+      /* in-chunk pairs (t as the query, i <= t in the same chunk) */
+      for (long i = t0; i <= t; ++i) {
+        double w = 0.0;
+        for (long a = 0; a < g; ++a) {
+          s[a] = 0.0;
+          for (long x = a * m; x < (a + 1) * m; ++x) s[a] += Q[t * d + x] * K[i * d + x];
+          w += s[a] * s[a];
+        }
+        double cw = bv[t];
+        for (long j = 0; j < dv; ++j) {
+          cw += A[t * dv + j] * V[i * dv + j];
+          dV[i * dv + j] += w * A[t * dv + j];
+        }
+        for (long a = 0; a < g; ++a)
+          for (long x = a * m; x < (a + 1) * m; ++x) {
+            dQ[t * d + x] += 2.0 * cw * s[a] * K[i * d + x];
+            dK[i * d + x] += 2.0 * cw * s[a] * Q[t * d + x];
+          }
+      }
+    }
+    free(fst); free(bst); free(A); free(bv); free(ph); free(pw); free(Y); free(s);
+  }
+}

@@ -647,6 +647,116 @@ def pin_lin_rows_match_full(orc):
         assert np.array_equal(orc.lin_fwd_rows(q, k, v, f, 0.0, norm, bh, tt), full[bh, tt])
 
 
+# ---------------------------------------------------------------------------
+# PIN: backward (gradients of sum_t <dout_t, o_t>)
+# ---------------------------------------------------------------------------
+
+def _torch_grads(q, k, v, dout, g):
+    """Gradients by torch autograd of a float64 matrix-form forward (scores
+    (Q K^T)^2 summed over blocks, lower-triangular mask, row normalisation):
+    a different route from the oracle's loops."""
+    import torch
+    B, H, T, d = q.shape
+    m = d // g
+    tq = torch.tensor(q, dtype=torch.float64, requires_grad=True)
+    tk = torch.tensor(k, dtype=torch.float64, requires_grad=True)
+    tv = torch.tensor(v, dtype=torch.float64, requires_grad=True)
+    P = 0
+    for a in range(g):
+        sl = slice(a * m, (a + 1) * m)
+        P = P + torch.matmul(tq[..., sl], tk[..., sl].transpose(-1, -2)) ** 2
+    P = P * torch.tril(torch.ones(T, T, dtype=torch.float64))
+    o = torch.matmul(P, tv) / P.sum(-1, keepdim=True)
+    (o * torch.tensor(dout)).sum().backward()
+    return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
+
+
+def pin_bwd_finite_differences(orc):
+    rng = _rng(97)
+    q, k, v = _rand_qkv(rng, 1, 1, 6, 4, 3, unit=False)
+    dout = rng.standard_normal(v.shape)
+    h = 1e-5
+    for g in (1, 2):
+        grads = orc.bwd_mg(q, k, v, dout, g)
+        for idx, X in enumerate((q, k, v)):
+            num = np.zeros_like(X)
+            for ii in np.ndindex(X.shape):
+                args = [q, k, v]
+                Xp, Xm = X.copy(), X.copy()
+                Xp[ii] += h
+                Xm[ii] -= h
+                args[idx] = Xp
+                lp = float((orc.fwd_mg(*args, g) * dout).sum())
+                args[idx] = Xm
+                lm = float((orc.fwd_mg(*args, g) * dout).sum())
+                num[ii] = (lp - lm) / (2 * h)
+            assert np.allclose(grads[idx], num, rtol=1e-6, atol=1e-8), (g, idx)
+
+
+def pin_bwd_torch_autograd(orc):
+    rng = _rng(101)
+    q, k, v = _rand_qkv(rng, 2, 2, 19, 8, 5, unit=False)
+    dout = rng.standard_normal(v.shape)
+    for g in (1, 2, 4):
+        got = orc.bwd_mg(q, k, v, dout, g)
+        ref = _torch_grads(q, k, v, dout, g)
+        for a, b in zip(got, ref):
+            assert np.allclose(a, b, rtol=1e-10, atol=1e-12), g
+    # g = 1 through the M1 forward as well
+    assert np.array_equal(orc.fwd_mg(q, k, v, 1), orc.fwd(q, k, v))
+
+
+def pin_bwd_invariants(orc):
+    rng = _rng(103)
+    T = 17
+    q, k, v = _rand_qkv(rng, 1, 2, T, 6, 4, unit=False)
+    dout = rng.standard_normal(v.shape)
+    for g in (1, 2, 3):
+        dq, dk, dv = orc.bwd_mg(q, k, v, dout, g)
+        # o(v + c) = o(v) + c: the value gradients sum to the output cotangents
+        assert np.allclose(dv.sum(axis=2), dout.sum(axis=2), rtol=1e-12, atol=1e-12)
+        # o_t is invariant to scaling q_t, and to scaling every key together
+        assert np.allclose(np.einsum("bhtd,bhtd->bht", q, dq), 0.0, atol=1e-12)
+        assert np.allclose(np.einsum("bhtd,bhtd->bh", k, dk), 0.0, atol=1e-11)
+        # k -> -k leaves the forward unchanged: dk flips, dq and dv stay
+        dq2, dk2, dv2 = orc.bwd_mg(q, -k, v, dout, g)
+        assert np.allclose(dq2, dq, rtol=1e-12, atol=1e-13)
+        assert np.allclose(dk2, -dk, rtol=1e-12, atol=1e-13)
+        assert np.allclose(dv2, dv, rtol=1e-12, atol=1e-13)
+    # one token: o_0 = v_0, so dv_0 = dout_0 and dq_0 = dk_0 = 0
+    dq, dk, dv = orc.bwd_mg(q[:, :, :1], k[:, :, :1], v[:, :, :1], dout[:, :, :1], 1)
+    assert np.allclose(dv, dout[:, :, :1], rtol=1e-14, atol=1e-15)
+    assert np.allclose(dq, 0.0, atol=1e-14) and np.allclose(dk, 0.0, atol=1e-14)
+
+
+def pin_bwd_zero_denominator(orc):
+    # a zero query row has D_t = 0 and the constant readout 0: it passes no
+    # gradient (its own dq is 0, and its dout changes nothing)
+    rng = _rng(107)
+    q, k, v = _rand_qkv(rng, 1, 1, 9, 4, 3, unit=False)
+    q[:, :, 4] = 0.0
+    dout = rng.standard_normal(v.shape)
+    dq, dk, dv = orc.bwd_mg(q, k, v, dout, 1)
+    assert np.array_equal(dq[:, :, 4], np.zeros_like(dq[:, :, 4]))
+    dout2 = dout.copy()
+    dout2[:, :, 4] += 10.0
+    for a, b in zip(orc.bwd_mg(q, k, v, dout2, 1), (dq, dk, dv)):
+        assert np.array_equal(a, b)
+
+
+def pin_bwd_chunked_equals_definition(orc):
+    rng = _rng(109)
+    q, k, v = _rand_qkv(rng, 1, 2, 27, 8, 3, unit=False)
+    dout = rng.standard_normal(v.shape)
+    for g in (1, 2, 4):
+        ref = orc.bwd_mg(q, k, v, dout, g)
+        for C in (1, 3, 8, 27, 32):
+            for mode in (0, 1):
+                got = orc.bwd_chunked_mg(q, k, v, dout, C, g, mode)
+                for a, b in zip(got, ref):
+                    assert np.allclose(a, b, rtol=1e-11, atol=1e-12), (g, C, mode)
+
+
 ALL_PINS = [
     pin_packed_sizes, pin_packed_order, pin_phi_identity, pin_worked_example,
     pin_brute_force_unpacked, pin_convex_hull, pin_first_token, pin_gate_recursion,
@@ -658,4 +768,6 @@ ALL_PINS = [
     pin_mg_chunked_equals_definition, pin_mg_decode_equals_forward, pin_mg_rows_match_full,
     pin_lin_widths, pin_lin_features, pin_lin_brute_force, pin_lin_special_cases,
     pin_lin_chunked_equals_definition, pin_lin_rows_match_full,
+    pin_bwd_finite_differences, pin_bwd_torch_autograd, pin_bwd_invariants,
+    pin_bwd_zero_denominator, pin_bwd_chunked_equals_definition,
 ]

@@ -78,6 +78,23 @@ MUTANTS = [
     ("lin_chunk_key_feature_from_query",
      "kata_oracle_lin_feature(K + (t0 + r) * d, d, feature, eps, FK + r * n);",
      "kata_oracle_lin_feature(Q + (t0 + r) * d, d, feature, eps, FK + r * n);"),
+    # backward
+    ("bwd_b_sign", "    bt = -go / D;", "    bt = go / D;"),
+    ("bwd_a_not_divided", "        A[t * dv + j] = G[t * dv + j] / D;", "        A[t * dv + j] = G[t * dv + j];"),
+    ("bwd_no_factor_two_q", "            dQ[t * d + c] += 2.0 * cw * s[a] * K[i * d + c];",
+     "            dQ[t * d + c] += cw * s[a] * K[i * d + c];"),
+    ("bwd_dv_unweighted", "          dV[i * dv + j] += w * A[t * dv + j];",
+     "          dV[i * dv + j] += A[t * dv + j];"),
+    ("bwd_dk_from_k", "            dK[i * d + c] += 2.0 * cw * s[a] * Q[t * d + c];",
+     "            dK[i * d + c] += 2.0 * cw * s[a] * K[i * d + c];"),
+    ("bwd_chunk_b_sign", "        bv[t] = -go / D;", "        bv[t] = go / D;"),
+    ("vjp_one_sided", "          dx[xb] += 2.0 * y * x[xa];", ""),
+    ("bwd_chunk_no_reversal", "      double* Bt = bst + (NC - 1 - t / C) * SE;",
+     "      double* Bt = bst + (t / C) * SE;"),
+    ("bwd_chunk_dz_unweighted", "        Bt[n * dv + f] += bv[t] * ph[f];", "        Bt[n * dv + f] += ph[f];"),
+    ("bwd_chunk_dv_query_side_weight", "      kata_oracle_phi_mg(K + t * d, d, g, 1, pw);",
+     "      kata_oracle_phi_mg(K + t * d, d, g, 0, pw);"),
+    ("bwd_chunk_inter_dq_missing_b", "        double y = bv[t] * St[n * dv + f];", "        double y = 0.0;"),
 ]
 
 
