@@ -271,6 +271,49 @@ KATA_API size_t kata_lin_fwd_workspace_bytes(int B, int H, int T, int d, int dv,
 KATA_API int kata_lin_default_span(int B, int H, int T, int d, int dv, int C,
                                    kata_lin_feature_t feature, kata_dtype_t dtype);
 
+/*
+ * Backward of the causal KATA-Mg forward (g = 1: KATA-M1) in the O(T)
+ * chunked form: the chunked backward of the appendix's chunkwise algorithm (a
+ * reverse scan over chunks carrying the state cotangent, forward quantities
+ * recomputed from chunk-boundary states, the feature-map VJP
+ * dx = (dPsi + dPsi^T) x closing the chain).  For output cotangents
+ * dout = dL/do it returns
+ *     dq = dL/dq, dk = dL/dk, dv_out = dL/dv,
+ * with a_t = dout_t / D_t, b_t = -<dout_t, o_t> / D_t, dL/dw_ti = <a_t, v_i> + b_t
+ * (i <= t), w_ti = sum_blk (q_t,blk . k_i,blk)^2.  A row with D_t = 0 (whose
+ * readout is the constant 0) passes no gradient.
+ *   q, k, v : the forward's inputs (dtype), out : its fp32 output
+ *             [B][H][T][dv] (kata_fwd_chunked or kata_mg_fwd_chunked), dout :
+ *             fp32 [B][H][T][dv]; dq, dk : fp32 [B][H][T][d], dv_out : fp32
+ *             [B][H][T][dv], overwritten, none aliasing an input.
+ *   Supported: d <= 64, dv <= 256, C <= 64, g | d, fp32 or bf16 inputs; fp32
+ *   arithmetic.  Else KATA_ERR_UNSUPPORTED (shape) or KATA_ERR_INVALID_ARG.
+ *   workspace : >= kata_bwd_workspace_bytes(...) bytes, 256-byte aligned,
+ *   caller-owned, contents undefined on exit; kata_bwd_chunked allocates it
+ *   stream-ordered.  stage_events : 7 caller-created events, recorded before
+ *   the first launch and after each of the six (forward states, prefix scan,
+ *   per-token coefficients, backward states, suffix scan, gradients).
+ */
+KATA_API kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v,
+                                        const float* out, const float* dout, float* dq,
+                                        float* dk, float* dv_out, int B, int H, int T, int d,
+                                        int dv, int C, int g, kata_dtype_t dtype,
+                                        hipStream_t stream);
+KATA_API kata_status_t kata_bwd_chunked_ws(const void* q, const void* k, const void* v,
+                                           const float* out, const float* dout, float* dq,
+                                           float* dk, float* dv_out, int B, int H, int T, int d,
+                                           int dv, int C, int g, kata_dtype_t dtype,
+                                           void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream);
+KATA_API kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, const void* v,
+                                              const float* out, const float* dout, float* dq,
+                                              float* dk, float* dv_out, int B, int H, int T,
+                                              int d, int dv, int C, int g, kata_dtype_t dtype,
+                                              void* workspace, size_t workspace_bytes,
+                                              hipEvent_t* stage_events, hipStream_t stream);
+KATA_API size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
+                                         kata_dtype_t dtype);
+
 /* Static, human-readable name of a status code. */
 KATA_API const char* kata_status_string(kata_status_t s);
 

@@ -35,6 +35,8 @@ EXPORTED = (
     "kata_mg_fwd_quadratic_workspace_bytes", "kata_mg_prefill_state", "kata_mg_decode_step",
     "kata_lin_dim", "kata_lin_fwd_chunked", "kata_lin_fwd_chunked_ws",
     "kata_lin_fwd_chunked_timed", "kata_lin_fwd_workspace_bytes", "kata_lin_default_span",
+    "kata_bwd_chunked", "kata_bwd_chunked_ws", "kata_bwd_chunked_timed",
+    "kata_bwd_workspace_bytes",
     "kata_status_string", "kata_abi_version",
 )
 
@@ -113,6 +115,16 @@ def lib():
     L.kata_lin_fwd_workspace_bytes.restype = sz
     L.kata_lin_default_span.argtypes = [i, i, i, i, i, i, i, i]
     L.kata_lin_default_span.restype = i
+    L.kata_bwd_chunked.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp]
+    L.kata_bwd_chunked.restype = i
+    L.kata_bwd_chunked_ws.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i,
+                                      vp, sz, vp]
+    L.kata_bwd_chunked_ws.restype = i
+    L.kata_bwd_chunked_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i,
+                                         vp, sz, vp, vp]
+    L.kata_bwd_chunked_timed.restype = i
+    L.kata_bwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
+    L.kata_bwd_workspace_bytes.restype = sz
     L.kata_status_string.argtypes = [i]
     L.kata_status_string.restype = ctypes.c_char_p
     L.kata_abi_version.argtypes = []
@@ -477,3 +489,54 @@ def lin_fwd_chunked_alloc(q, k, v, C: int, feature: int, eps: float = 0.0,
                                       B, H, T, d, dv, C, feature, float(eps), int(normalize),
                                       code, _stream(stream, q.device)), "kata_lin_fwd_chunked")
     return out
+
+
+# ---- backward -----------------------------------------------------------------
+
+def bwd_workspace_bytes(B, H, T, d, dv, C, g, dtype_code) -> int:
+    return int(lib().kata_bwd_workspace_bytes(B, H, T, d, dv, C, g, dtype_code))
+
+
+def bwd_chunked(q, k, v, out, dout, C: int, g: int = 1, workspace=None, stream=None,
+                events=None, grads=None):
+    """Gradients (dq, dk, dv) of the causal KATA-Mg forward (g = 1: M1) via
+    kata_bwd_chunked_ws (or kata_bwd_chunked_timed when `events`, a ctypes
+    array of 7 HIP events, is given); fp32 tensors shaped like q, k, v."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    for name, t in (("out", out), ("dout", dout)):
+        if t.dtype != torch.float32 or tuple(t.shape) != (B, H, T, dv):
+            raise ValueError(f"{name} must be fp32 [B,H,T,dv]")
+    if grads is None:
+        grads = (torch.empty((B, H, T, d), dtype=torch.float32, device=q.device),
+                 torch.empty((B, H, T, d), dtype=torch.float32, device=q.device),
+                 torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device))
+    dq, dk, dvv = grads
+    nbytes = bwd_workspace_bytes(B, H, T, d, dv, C, g, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    args = (_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), _dev(dout, "dout"),
+            _dev(dq, "dq"), _dev(dk, "dk"), _dev(dvv, "dv"), B, H, T, d, dv, C, g, code,
+            _dev(workspace, "workspace"), workspace.numel())
+    if events is None:
+        _check(lib().kata_bwd_chunked_ws(*args, _stream(stream, q.device)), "kata_bwd_chunked_ws")
+    else:
+        _check(lib().kata_bwd_chunked_timed(*args, events, _stream(stream, q.device)),
+               "kata_bwd_chunked_timed")
+    return dq, dk, dvv
+
+
+def bwd_chunked_alloc(q, k, v, out, dout, C: int, g: int = 1, stream=None):
+    """The same gradients via kata_bwd_chunked (stream-ordered library workspace)."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    dq = torch.empty((B, H, T, d), dtype=torch.float32, device=q.device)
+    dk = torch.empty((B, H, T, d), dtype=torch.float32, device=q.device)
+    dvv = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_bwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+                                  _dev(dout, "dout"), _dev(dq, "dq"), _dev(dk, "dk"),
+                                  _dev(dvv, "dv"), B, H, T, d, dv, C, g, code,
+                                  _stream(stream, q.device)), "kata_bwd_chunked")
+    return dq, dk, dvv

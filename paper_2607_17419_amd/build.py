@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libkata.so")
-SOURCES = ["kata_api.hip", "kata_fp32.hip", "kata_mfma.hip", "kata_linear.hip"]
+SOURCES = ["kata_api.hip", "kata_fp32.hip", "kata_mfma.hip", "kata_linear.hip", "kata_bwd.hip"]
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 ARCH = "gfx950"

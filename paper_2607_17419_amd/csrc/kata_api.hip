@@ -271,11 +271,45 @@ kata_status_t lin_ws(const void* q, const void* k, const void* v, float* out, in
                                                       normalize, workspace, stream, ev));
 }
 
+// ---- backward ---------------------------------------------------------------------
+
+kata_status_t bwd_check(int B, int H, int T, int d, int dv, int C, int g, int dtype) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || dv < 1 || C < 1) return KATA_ERR_INVALID_ARG;
+  if (dtype != KATA_F32 && dtype != KATA_BF16) return KATA_ERR_INVALID_ARG;
+  if (!blocks_ok(d, g)) return KATA_ERR_INVALID_ARG;
+  if (!product_ok(B, H, T, d > dv ? d + 1 : dv + 1)) return KATA_ERR_INVALID_ARG;
+  if (!kata::bwd_supported(d, dv, C, g)) return KATA_ERR_UNSUPPORTED;
+  if (static_cast<long long>(B) * H > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  if ((static_cast<long long>(T) + C - 1) / C > kGridYZ) return KATA_ERR_UNSUPPORTED;
+  return KATA_OK;
+}
+
+kata_status_t bwd_ws(const void* q, const void* k, const void* v, const float* out,
+                     const float* dout, float* dq, float* dk, float* dvv, int B, int H, int T,
+                     int d, int dv, int C, int g, kata_dtype_t dtype, void* workspace,
+                     size_t workspace_bytes, hipEvent_t* ev, hipStream_t stream) {
+  if (!q || !k || !v || !out || !dout || !dq || !dk || !dvv) return KATA_ERR_INVALID_ARG;
+  for (const void* p : {q, k, v, static_cast<const void*>(out), static_cast<const void*>(dout),
+                        static_cast<const void*>(dq), static_cast<const void*>(dk),
+                        static_cast<const void*>(dvv)})
+    if (!aligned16(p)) return KATA_ERR_INVALID_ARG;
+  const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
+  if (c != KATA_OK) return c;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
+  if (workspace_bytes < kata::bwd_workspace(B * H, T, d, dv, C, g)) return KATA_ERR_INVALID_ARG;
+  const int BH = B * H;
+  if (dtype == KATA_F32)
+    return from_hip(kata::launch_bwd<float>(q, k, v, out, dout, dq, dk, dvv, BH, T, d, dv, C, g,
+                                            workspace, stream, ev));
+  return from_hip(kata::launch_bwd<kata::bf16_t>(q, k, v, out, dout, dq, dk, dvv, BH, T, d, dv, C,
+                                                 g, workspace, stream, ev));
+}
+
 }  // namespace
 
 extern "C" {
 
-int kata_abi_version(void) { return 102; }
+int kata_abi_version(void) { return 103; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (s) {
@@ -473,6 +507,52 @@ kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v, 
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
   const kata_status_t st = lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype,
                                   span, ws, bytes, nullptr, stream);
+  const hipError_t fe = hipFreeAsync(ws, stream);
+  if (st != KATA_OK) return st;
+  return from_hip(fe);
+}
+
+// ---- backward -------------------------------------------------------------------
+
+size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
+                                kata_dtype_t dtype) {
+  if (bwd_check(B, H, T, d, dv, C, g, dtype) != KATA_OK) return 0;
+  return kata::bwd_workspace(B * H, T, d, dv, C, g);
+}
+
+kata_status_t kata_bwd_chunked_ws(const void* q, const void* k, const void* v, const float* out,
+                                  const float* dout, float* dq, float* dk, float* dv_out, int B,
+                                  int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype, workspace,
+                workspace_bytes, nullptr, stream);
+}
+
+kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, const void* v,
+                                     const float* out, const float* dout, float* dq, float* dk,
+                                     float* dv_out, int B, int H, int T, int d, int dv, int C,
+                                     int g, kata_dtype_t dtype, void* workspace,
+                                     size_t workspace_bytes, hipEvent_t* stage_events,
+                                     hipStream_t stream) {
+  if (!stage_events) return KATA_ERR_INVALID_ARG;
+  for (int i = 0; i < 7; ++i)
+    if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
+  return bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype, workspace,
+                workspace_bytes, stage_events, stream);
+}
+
+kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v, const float* out,
+                               const float* dout, float* dq, float* dk, float* dv_out, int B,
+                               int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
+                               hipStream_t stream) {
+  if (!q || !k || !v || !out || !dout || !dq || !dk || !dv_out) return KATA_ERR_INVALID_ARG;
+  const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
+  if (c != KATA_OK) return c;
+  const size_t bytes = kata::bwd_workspace(B * H, T, d, dv, C, g);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  const kata_status_t st = bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype,
+                                  ws, bytes, nullptr, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);
   if (st != KATA_OK) return st;
   return from_hip(fe);

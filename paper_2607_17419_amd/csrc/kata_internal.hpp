@@ -65,6 +65,17 @@ hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* o
                            int feature, float eps, int normalize, int L, void* ws, hipStream_t st,
                            hipEvent_t* ev);
 
+// ---- backward, fp32 path (kata_bwd.hip) -------------------------------------
+bool bwd_supported(int d, int dv, int C, int g);
+size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g);
+// ev: null, or 7 events recorded before the first kernel and after each of the
+// six launches (forward states, prefix scan, coefficients, backward states,
+// suffix scan, gradients).
+template <typename Tin>
+hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* out,
+                      const float* dout, float* dq, float* dk, float* dv_out, int BH, int T,
+                      int d, int dv, int C, int g, void* ws, hipStream_t st, hipEvent_t* ev);
+
 inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
   return ev ? hipEventRecord(ev[i], st) : hipSuccess;
 }

@@ -11,6 +11,8 @@ namespace kata {
 // Exclusive prefix along the record axis (section "Tree-scan inter-chunk
 // reduction"; the three-stage pipeline's middle stage):
 //   out[bh][c][e] = w(e) * sum_{c' < c} in[bh][c'][e],  out[.][0][.] = 0.
+// kReverse runs the same scan over the records in reverse order (record c
+// receives the sum over c' > c: the exclusive suffix of the backward pass).
 // Each workgroup owns kEB consecutive elements of the record for every chunk;
 // rows are processed in blocks of kNB with a work-efficient (Blelloch) tree in
 // LDS: an up-sweep of log2(kNB) levels, then a down-sweep, plus a carry from
@@ -21,7 +23,7 @@ namespace kata {
 constexpr int kEB = 64;
 constexpr int kNB = 128;
 
-template <typename OutT, typename Weight>
+template <typename OutT, typename Weight, bool kReverse = false>
 __global__ __launch_bounds__(256) void scan_exclusive(const float* in, OutT* out, int N,
                                                       long long E, long long bh_stride,
                                                       Weight weight) {
@@ -41,7 +43,9 @@ __global__ __launch_bounds__(256) void scan_exclusive(const float* in, OutT* out
     const int nr = min(kNB, N - r0);
     // load (zero beyond the last row)
     for (int r = rgrp; r < kNB; r += 4)
-      tile[r][col] = (active && r < nr) ? ib[static_cast<long long>(r0 + r) * E + e] : 0.f;
+      tile[r][col] = (active && r < nr)
+                         ? ib[static_cast<long long>(kReverse ? N - 1 - (r0 + r) : r0 + r) * E + e]
+                         : 0.f;
     __syncthreads();
     // up-sweep: node i (right child index) accumulates its left sibling
     for (int step = 1; step < kNB; step <<= 1) {
@@ -76,7 +80,9 @@ __global__ __launch_bounds__(256) void scan_exclusive(const float* in, OutT* out
     __syncthreads();
     const float cin = carry_s[col];
     for (int r = rgrp; r < nr; r += 4)
-      if (active) store_weighted(ob, static_cast<long long>(r0 + r) * E + e, tile[r][col] + cin, weight(e));
+      if (active)
+        store_weighted(ob, static_cast<long long>(kReverse ? N - 1 - (r0 + r) : r0 + r) * E + e,
+                       tile[r][col] + cin, weight(e));
     if (rgrp == 0) carry += total;
     __syncthreads();
   }

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 102
+    assert L.kata_abi_version() == 103
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
@@ -228,3 +228,38 @@ def test_lin_workspace_and_span_host_logic():
     assert L.kata_lin_fwd_chunked_ws(*base, 0, ctypes.c_void_p(0x100080), need, NUL) == 1
     assert L.kata_lin_fwd_chunked_ws(*base, -1, ctypes.c_void_p(0x100000), need, NUL) == 1
     assert L.kata_lin_fwd_chunked_timed(*base, 0, ctypes.c_void_p(0x100000), need, NUL, NUL) == 1
+
+
+# ---- backward ------------------------------------------------------------------
+
+@pytest.mark.parametrize("args,expect", [
+    ((NUL, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, 0), 1),  # null q
+    ((FAKE, FAKE, FAKE, FAKE, NUL, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, 0), 1),  # null dout
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NUL, 1, 1, 8, 16, 16, 32, 1, 0), 1),  # null dv
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 16, 16, 32, 1, 0), 1),  # T < 1
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 3, 0), 1),  # g !| d
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 1, 4), 1),  # dtype
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 65, 1, 0), 2),  # C > 64
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 80, 16, 32, 1, 0), 2),  # d > 64
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 300, 32, 1, 0), 2),  # dv > 256
+])
+def test_bwd_rejects_before_gpu(args, expect):
+    assert kata.lib().kata_bwd_chunked(*args, NUL) == expect
+
+
+def test_bwd_workspace_host_logic():
+    L = kata.lib()
+    # forward and backward records (n dv + n fp32 per chunk) plus (a_t, b_t)
+    n = 64 * 65 // 2
+    NC = 4096 // 64
+    expect = 128 * (2 * NC * (n * 64 + n) + 4096 * 65) * 4
+    assert L.kata_bwd_workspace_bytes(8, 16, 4096, 64, 64, 64, 1, 1) == expect
+    n2 = 2 * (32 * 33 // 2)
+    assert L.kata_bwd_workspace_bytes(1, 1, 100, 64, 64, 50, 2, 0) == \
+        (2 * 2 * (n2 * 64 + n2) + 100 * 65) * 4
+    assert L.kata_bwd_workspace_bytes(1, 1, 100, 64, 64, 65, 1, 0) == 0
+    need = L.kata_bwd_workspace_bytes(1, 1, 128, 16, 16, 32, 1, 0)
+    base = (FAKE,) * 8 + (1, 1, 128, 16, 16, 32, 1, 0)
+    assert L.kata_bwd_chunked_ws(*base, ctypes.c_void_p(0x100000), need - 1, NUL) == 1
+    assert L.kata_bwd_chunked_ws(*base, ctypes.c_void_p(0x100010), need, NUL) == 1
+    assert L.kata_bwd_chunked_timed(*base, ctypes.c_void_p(0x100000), need, NUL, NUL) == 1

@@ -1,0 +1,205 @@
+"""GPU parity of the O(T) chunked backward (kata_bwd_chunked*) against the CPU
+oracle's backward by the definition.  Gradients are of sum_t <dout_t, o_t>.
+Every case prints its name and shape before it launches.
+
+Tolerances: fp32 inputs, max-abs error <= 1e-5 relative to the gradient's
+scale (max |ref|, at least 1); bf16 inputs, the relative l2 error of each
+gradient tensor per head <= 2e-2.  Rows with a small denominator D_t have
+large gradients (a_t = dout_t / D_t), hence the scale-relative forms."""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import workloads
+from gpu_helpers import log, to_device
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-5
+BF16_REL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def kata():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_17419_amd as k
+    k.lib()  # raises if libkata.so is missing: no fallback
+    return k
+
+
+def _dout(shape, seed):
+    return np.random.default_rng(seed).standard_normal(shape).astype(np.float32)
+
+
+def _gpu_bwd(kata, inp, dtype, dout, C, g, out=None, fwd_C=None):
+    """o from the library forward (unless given), then the library backward."""
+    import torch
+    q, k, v = (to_device(inp[n], dtype) for n in ("q_dev", "k_dev", "v_dev"))
+    if out is None:
+        out = kata.mg_fwd_chunked(q, k, v, fwd_C or C, g)
+    else:
+        out = torch.from_numpy(np.ascontiguousarray(out, dtype=np.float32)).to(q.device)
+    d_out = torch.from_numpy(dout).to(q.device)
+    dq, dk, dv = kata.bwd_chunked(q, k, v, out, d_out, C, g)
+    torch.cuda.synchronize()
+    return dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
+
+
+def _check_f32(got, ref, what):
+    for name, a, b in zip(("dq", "dk", "dv"), got, ref):
+        err = float(np.max(np.abs(a.astype(np.float64) - b)))
+        tol = F32_TOL * max(1.0, float(np.max(np.abs(b))))
+        log(f"  {what} {name}: max abs err {err:.3e} (tol {tol:.2e})")
+        assert np.all(np.isfinite(a)) and err <= tol, (what, name)
+
+
+def _check_rel(got, ref, what, tol=BF16_REL):
+    for name, a, b in zip(("dq", "dk", "dv"), got, ref):
+        a = a.astype(np.float64).reshape(-1, b.shape[2] * b.shape[3])
+        b = b.reshape(-1, b.shape[2] * b.shape[3])
+        rel = np.linalg.norm(a - b, axis=1) / np.maximum(np.linalg.norm(b, axis=1), 1e-30)
+        log(f"  {what} {name}: max per-head rel l2 err {float(rel.max()):.3e} (tol {tol:.0e})")
+        assert np.all(np.isfinite(a)) and float(rel.max()) <= tol, (what, name)
+
+
+@pytest.mark.parametrize("g", [1, 2, 4])
+def test_bwd_fp32_inputs(kata, orc, g):
+    log(f"case bwd fp32 tiny B1 H2 T256 d16 dv16 C32 g={g}")
+    inp = workloads.make_inputs("tiny_f32")
+    dout = _dout(inp["v"].shape, 7 + g)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, g)
+    # the backward alone (o from the oracle), then forward + backward on the GPU
+    o_ref = orc.fwd_mg(inp["q"], inp["k"], inp["v"], g)
+    _check_f32(_gpu_bwd(kata, inp, "f32", dout, 32, g, out=o_ref), ref, f"g{g} bwd")
+    _check_f32(_gpu_bwd(kata, inp, "f32", dout, 32, g), ref, f"g{g} fwd+bwd")
+
+
+def test_bwd_one_token(kata, orc):
+    # T = 1: o_0 = v_0, so dv_0 = dout_0 and dq_0 = dk_0 = 0 exactly; the GPU
+    # values are rounding residues of <dout, v_0 - o_0> / D_0 with D_0 = (q.k)^2
+    log("case bwd one token B1 H2 T1 d64 C64 bf16")
+    inp = workloads.make_inputs("mid_bf16", B=1, H=2, T=1)
+    dout = _dout(inp["v"].shape, 41)
+    o_ref = orc.fwd(inp["q"], inp["k"], inp["v"])
+    dq, dk, dv = _gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=o_ref)
+    assert np.allclose(dv, dout, rtol=1e-5, atol=1e-6)
+    D = np.einsum("bhtd,bhtd->bht", inp["q"], inp["k"]) ** 2
+    scale = 1e-5 * np.abs(dout).sum(-1) * np.abs(inp["v"]).sum(-1) / D  # |<a, v>| bound x 1e-5
+    for g_ in (dq, dk):
+        assert np.all(np.linalg.norm(g_, axis=-1) <= scale * 2 * np.sqrt(D) + 1e-6)
+
+
+@pytest.mark.parametrize("T", [2, 63, 64, 65, 300, 1025])
+def test_bwd_ragged_m1(kata, orc, T):
+    log(f"case bwd M1 bf16 inputs B1 H2 T{T} d64 dv64 C64")
+    inp = workloads.make_inputs("mid_bf16", B=1, H=2, T=T)
+    dout = _dout(inp["v"].shape, 11)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
+    o_ref = orc.fwd(inp["q"], inp["k"], inp["v"])
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=o_ref), ref, f"T{T} bwd", tol=1e-4)
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1), ref, f"T{T} fwd+bwd")
+
+
+@pytest.mark.parametrize("C,g", [(16, 1), (32, 1), (48, 2), (64, 2), (64, 4)])
+def test_bwd_chunks_and_blocks(kata, orc, C, g):
+    T = 700
+    log(f"case bwd bf16 inputs B2 H1 T{T} d64 dv64 C{C} g={g}")
+    inp = workloads.make_inputs("mid_bf16", B=2, H=1, T=T)
+    dout = _dout(inp["v"].shape, 13 + C + g)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, g)
+    o_ref = orc.fwd_mg(inp["q"], inp["k"], inp["v"], g)
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, C, g, out=o_ref), ref, f"C{C} g{g} bwd",
+               tol=1e-4)
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, C, g, fwd_C=64), ref, f"C{C} g{g} fwd+bwd")
+
+
+def test_bwd_value_width_and_recall(kata, orc):
+    # dv != d on the fp32 path, and the recall-shaped inputs (d = 32, C = 64)
+    log("case bwd fp32 inputs d24 dv40 C24 B1 H2 T333")
+    rng = np.random.default_rng(17)
+    q = rng.standard_normal((1, 2, 333, 24)).astype(np.float32)
+    k = rng.standard_normal((1, 2, 333, 24)).astype(np.float32)
+    v = rng.standard_normal((1, 2, 333, 40)).astype(np.float32)
+    dout = _dout(v.shape, 19)
+    inp = dict(q_dev=q, k_dev=k, v_dev=v)
+    ref = orc.bwd_mg(q, k, v, dout, 3)
+    _check_f32(_gpu_bwd(kata, inp, "f32", dout, 24, 3, out=orc.fwd_mg(q, k, v, 3)), ref,
+               "d24 dv40 g3 bwd")
+    log("case bwd recall-shaped bf16 B1 H2 T1500 d32 dv64 C64")
+    inp = workloads.make_inputs("recall_bf16", B=1, H=2, T=1500)
+    dout = _dout(inp["v"].shape, 23)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, fwd_C=128), ref, "recall fwd+bwd")
+
+
+def test_bwd_zero_denominator(kata, orc):
+    import torch
+    log("case bwd zero query rows B1 H1 T200 d16 dv16 C32 fp32")
+    inp = dict(workloads.make_inputs("tiny_f32", B=1, H=1, T=200))
+    q = inp["q_dev"].copy()
+    q[:, :, [0, 77, 199]] = 0.0
+    inp["q_dev"] = q
+    dout = _dout(inp["v"].shape, 29)
+    got = _gpu_bwd(kata, inp, "f32", dout, 32, 1)
+    for t in (0, 77, 199):
+        assert np.array_equal(got[0][:, :, t], np.zeros_like(got[0][:, :, t]))
+    ref = orc.bwd_mg(q, inp["k"], inp["v"], dout, 1)
+    _check_f32(got, ref, "zero rows")
+    torch.cuda.synchronize()
+
+
+def test_bwd_entry_points_match(kata):
+    import torch
+    log("case bwd ws vs timed vs alloc, bf16 B1 H3 T900 d64 C64")
+    inp = workloads.make_inputs("mid_bf16", B=1, H=3, T=900)
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out = kata.fwd_chunked(q, k, v, 64)
+    dout = torch.from_numpy(_dout(inp["v"].shape, 31)).to(q.device)
+    a = kata.bwd_chunked(q, k, v, out, dout, 64)
+    hip = ctypes.CDLL("libamdhip64.so")
+    vp = ctypes.c_void_p
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(vp)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+    hip.hipEventDestroy.argtypes = [vp]
+    evs = (vp * 7)()
+    for i in range(7):
+        h = vp()
+        assert hip.hipEventCreate(ctypes.byref(h)) == 0
+        evs[i] = h
+    b = kata.bwd_chunked(q, k, v, out, dout, 64, events=evs)
+    c = kata.bwd_chunked_alloc(q, k, v, out, dout, 64)
+    torch.cuda.synchronize()
+    for x, y, z in zip(a, b, c):
+        assert torch.equal(x, y) and torch.equal(x, z)
+    for i in range(6):
+        ms = ctypes.c_float()
+        assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[i], evs[i + 1]) == 0
+        assert ms.value >= 0.0
+    for i in range(7):
+        hip.hipEventDestroy(evs[i])
+
+
+def test_bwd_full_length_two_heads(kata, orc):
+    # the mid workload's full sequence (T = 4096, d = 64, C = 64) on two of its
+    # heads, forward on the MFMA path and backward, against the oracle
+    log("case bwd mid workload shape T4096 d64 C64, heads 0..1 (B1 H2)")
+    inp = workloads.make_inputs("mid_bf16", B=1, H=2)
+    dout = _dout(inp["v"].shape, 37)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
+    got = _gpu_bwd(kata, inp, "bf16", dout, 64, 1)
+    _check_rel(got, ref, "T4096 fwd+bwd")
+    # invariants, on the backward fed the exact forward output (q_t . dq_t equals
+    # 2 <dout_t, o_t - o_given>, so it vanishes only for the exact o): the value
+    # gradients sum to the output cotangents; q_t . dq_t = 0
+    o_ref = orc.fwd(inp["q"], inp["k"], inp["v"])
+    ex = _gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=o_ref)
+    _check_rel(ex, ref, "T4096 bwd", tol=1e-4)
+    assert np.allclose(ex[2].sum(axis=2), dout.sum(axis=2), rtol=1e-4, atol=1e-3)
+    qd = np.einsum("bhtd,bhtd->bht", inp["q"].astype(np.float64), ex[0])
+    scale = np.linalg.norm(ex[0], axis=-1) * np.linalg.norm(inp["q"], axis=-1)
+    assert np.all(np.abs(qd) <= 1e-4 * scale + 1e-5)
