@@ -161,19 +161,25 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   }
   __syncthreads();
   const float* zp = frec + bh * bh_stride + c * E + static_cast<long long>(n) * dv;
-  for (int r = tid; r < nt; r += 256) {
+  // four threads per token (consecutive lanes), partial sums joined by shuffles
+  for (int r0 = 0; r0 < C; r0 += 64) {
+    const int r = r0 + (tid >> 2), part = tid & 3;
     float D = 0.f;
-    for (int f = 0; f < n; ++f) {
-      const int a = pairs[f] & 0xFF, b = pairs[f] >> 8;
-      D += ((a == b) ? 1.f : 2.f) * qs[r * d + a] * qs[r * d + b] * zp[f];
-    }
-    for (int s = 0; s <= r; ++s)
-      for (int blk = 0; blk < g; ++blk) {
-        float sc = 0.f;
-        for (int x = blk * m; x < blk * m + m; ++x) sc += qs[r * d + x] * ks[s * d + x];
-        D += sc * sc;
+    if (r < nt) {
+      for (int f = part; f < n; f += 4) {
+        const int a = pairs[f] & 0xFF, b = pairs[f] >> 8;
+        D += ((a == b) ? 1.f : 2.f) * qs[r * d + a] * qs[r * d + b] * zp[f];
       }
-    Dn[r] = D;
+      for (int s = part; s <= r; s += 4)
+        for (int blk = 0; blk < g; ++blk) {
+          float sc = 0.f;
+          for (int x = blk * m; x < blk * m + m; ++x) sc += qs[r * d + x] * ks[s * d + x];
+          D += sc * sc;
+        }
+    }
+    D += __shfl_xor(D, 1);
+    D += __shfl_xor(D, 2);
+    if (r < nt && part == 0) Dn[r] = D;
   }
   __syncthreads();
   for (int r = tid; r < nt; r += 256) {
@@ -323,6 +329,285 @@ __global__ __launch_bounds__(256) void bwd_grad(const Tin* __restrict__ q,
   }
 }
 
+// ===========================================================================
+// fp32 matrix-core variants (v_mfma_f32_32x32x2_f32: lane l holds A[l % 32][l / 32]
+// and B[l / 32][l % 32]; result column l % 32, rows 8 (i / 4) + 4 (l / 32) + i % 4),
+// for C <= 64, d <= 64, dv <= 64.  Same arithmetic (fp32 products, fp32
+// accumulation) as the VALU kernels above, in another summation order.
+// ===========================================================================
+
+typedef float mf32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ mf32x16 mfma_f32(float a, float b, mf32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+constexpr int kMS = 65;  // LDS row stride (floats) of the 64-row staging tiles
+
+// Chunk states on the matrix cores: one workgroup per chunk stages the chunk's
+// x and y rows once; its waves take the (feature tile fp, value tile vj)
+// 32 x 32 tiles of S in turn, two tokens per MFMA; the tiles with vj = 0 also
+// sum z.  grid (NC, BH), block 256.
+template <typename Tx, typename Ty, bool kWeightedZ>
+__global__ __launch_bounds__(256) void bwd_state_mf(const Tx* __restrict__ x,
+                                                    const Ty* __restrict__ y, int y_stride,
+                                                    float* __restrict__ rec, int T, int d, int dv,
+                                                    int C, int g, long long bh_stride,
+                                                    long long E) {
+  __shared__ float xs[64 * kMS];
+  __shared__ float ys[64 * (kMS + 1)];
+  __shared__ uint16_t pairs[2080];
+  const int n = bwd_n(d, g);
+  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  bwd_pair_table(pairs, d, g);
+  const long long tb = static_cast<long long>(c) * C;
+  const int nt = static_cast<int>(min(static_cast<long long>(C), T - tb));
+  const Tx* xh = x + (static_cast<long long>(bh) * T + tb) * d;
+  const Ty* yh = y + (static_cast<long long>(bh) * T + tb) * y_stride;
+  const int yw = kWeightedZ ? dv + 1 : dv;
+  for (int i = tid; i < 64 * d; i += 256) {
+    const int t = i / d, a = i % d;
+    xs[t * kMS + a] = (t < nt) ? load_f32(xh, static_cast<long long>(t) * d + a) : 0.f;
+  }
+  for (int i = tid; i < 64 * (kMS + 1); i += 256) {
+    const int t = i / (kMS + 1), j = i % (kMS + 1);
+    ys[i] = (t < nt && j < yw) ? load_f32(yh, static_cast<long long>(t) * y_stride + j) : 0.f;
+  }
+  __syncthreads();
+  float* r0 = rec + bh * bh_stride + c * E;
+  const int nft = (n + 31) / 32, nvt = (dv + 31) / 32;
+  for (int tile = w; tile < nft * nvt; tile += 4) {
+    const int fp = tile / nvt, vj = tile % nvt;
+    const int p = 32 * fp + l32;
+    // lanes of a partial last feature tile feed zeros and store nothing
+    const uint16_t pr = pairs[p < n ? p : n - 1];
+    const int pa = pr & 0xFF, pb = pr >> 8;
+    const float pon = p < n ? 1.f : 0.f;
+    const int jc = 32 * vj + l32;
+    mf32x16 acc = {};
+    float zp = 0.f;
+    for (int s2 = 0; s2 < 32; ++s2) {
+      const int t = 2 * s2 + h;
+      const float a = pon * xs[t * kMS + pa] * xs[t * kMS + pb];
+      acc = mfma_f32(a, ys[t * (kMS + 1) + jc], acc);  // staged zeros past dv
+      if (vj == 0) zp += a * (kWeightedZ ? ys[t * (kMS + 1) + dv] : 1.f);
+    }
+    zp += __shfl_xor(zp, 32);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int f = 32 * fp + 8 * (i >> 2) + 4 * h + (i & 3);
+      if (f < n && jc < dv) r0[static_cast<long long>(f) * dv + jc] = acc[i];
+    }
+    if (vj == 0 && h == 0 && p < n) r0[static_cast<long long>(n) * dv + p] = zp;
+  }
+}
+
+// Gradients of chunk c with the inter-chunk products on the matrix cores.
+// grid (NC, BH), block 256, dynamic LDS bwd_grad_mf_smem(...).
+template <typename Tin>
+__global__ __launch_bounds__(256) void bwd_grad_mf(const Tin* __restrict__ q,
+                                                   const Tin* __restrict__ k,
+                                                   const Tin* __restrict__ v,
+                                                   const float* __restrict__ ab,
+                                                   const float* __restrict__ frec,
+                                                   const float* __restrict__ brec,
+                                                   float* __restrict__ dq, float* __restrict__ dk,
+                                                   float* __restrict__ dvo, int T, int d, int dv,
+                                                   int C, int g, long long bh_stride,
+                                                   long long E) {
+  extern __shared__ float bsm[];
+  const int n = bwd_n(d, g), m = d / g;
+  float* qs = bsm;              // [64][kMS] queries
+  float* ks = qs + 64 * kMS;    // keys
+  float* vs = ks + 64 * kMS;    // values
+  float* as = vs + 64 * kMS;    // [64][kMS + 1]: a_t (dv), b_t at column dv
+  float* dqs = as + 64 * (kMS + 1);
+  float* dks = dqs + 64 * kMS;
+  float* cs = dks + 64 * kMS;   // [64][kMS] dL/dw_ti, later the in-chunk dv
+  float* sb = cs + 64 * kMS;    // [64][kMS] block scores; later the two slabs
+  float* W = sb + 64 * kMS;     // [64][kMS] in-chunk weights
+  uint16_t* pairs = reinterpret_cast<uint16_t*>(W + 64 * kMS);
+  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  const long long t0 = static_cast<long long>(c) * C;
+  const int nt = static_cast<int>(min(static_cast<long long>(C), T - t0));
+  const long long hb = static_cast<long long>(bh) * T;
+  const Tin* qh = q + (hb + t0) * d;
+  const Tin* kh = k + (hb + t0) * d;
+  const Tin* vh = v + (hb + t0) * dv;
+  const float* abh = ab + (hb + t0) * (dv + 1);
+  bwd_pair_table(pairs, d, g);
+  for (int i = tid; i < 64 * kMS; i += 256) {
+    const int t = i / kMS, a = i % kMS;
+    const bool in = t < nt;
+    qs[i] = (in && a < d) ? load_f32(qh, static_cast<long long>(t) * d + a) : 0.f;
+    ks[i] = (in && a < d) ? load_f32(kh, static_cast<long long>(t) * d + a) : 0.f;
+    vs[i] = (in && a < dv) ? load_f32(vh, static_cast<long long>(t) * dv + a) : 0.f;
+    dqs[i] = 0.f;
+    dks[i] = 0.f;
+    W[i] = 0.f;
+  }
+  for (int i = tid; i < 64 * (kMS + 1); i += 256) {
+    const int t = i / (kMS + 1), j = i % (kMS + 1);
+    as[i] = (t < nt && j <= dv) ? abh[static_cast<long long>(t) * (dv + 1) + j] : 0.f;
+  }
+  __syncthreads();
+  // dL/dw_ti = <a_t, v_i> + b_t for i <= t
+  for (int i = tid; i < 64 * 64; i += 256) {
+    const int t = i >> 6, s = i & 63;
+    float cw = 0.f;
+    if (s <= t && t < nt) {
+      cw = as[t * (kMS + 1) + dv];
+      for (int j = 0; j < dv; ++j) cw += as[t * (kMS + 1) + j] * vs[s * kMS + j];
+    }
+    cs[t * kMS + s] = cw;
+  }
+  __syncthreads();
+  // in-chunk pairs, one feature block at a time
+  for (int blk = 0; blk < g; ++blk) {
+    for (int i = tid; i < 64 * 64; i += 256) {
+      const int t = i >> 6, s = i & 63;
+      float sc = 0.f;
+      if (s <= t)
+        for (int x2 = blk * m; x2 < blk * m + m; ++x2) sc += qs[t * kMS + x2] * ks[s * kMS + x2];
+      sb[t * kMS + s] = sc;
+      W[t * kMS + s] += sc * sc;
+    }
+    __syncthreads();
+    for (int i = tid; i < 64 * m; i += 256) {
+      const int t = i / m, x2 = blk * m + i % m;
+      float aq = 0.f, ak = 0.f;
+      for (int s = 0; s <= t; ++s) aq += cs[t * kMS + s] * sb[t * kMS + s] * ks[s * kMS + x2];
+      for (int u = t; u < 64; ++u) ak += cs[u * kMS + t] * sb[u * kMS + t] * qs[u * kMS + x2];
+      dqs[t * kMS + x2] += 2.f * aq;
+      dks[t * kMS + x2] += 2.f * ak;
+    }
+    __syncthreads();
+  }
+  // in-chunk dv into cs (free now): sum_{t >= i} w_ti a_t
+  for (int i = tid; i < 64 * 64; i += 256) {
+    const int r = i >> 6, j = i & 63;
+    float acc = 0.f;
+    if (j < dv)
+      for (int t = r; t < nt; ++t) acc += W[t * kMS + r] * as[t * (kMS + 1) + j];
+    cs[r * kMS + j] = acc;
+  }
+  __syncthreads();
+  // inter-chunk terms, 32 features per pass: the prefix slab (S_pre rows, then
+  // z_pre) and the suffix slab (dS_suf rows, then dz_suf) staged over sb; the
+  // next pass's slab is loaded into registers while this one is consumed
+  float* Sl = sb;               // [32][kMS]
+  float* Bl = sb + 32 * kMS;    // [32][kMS]
+  float* zl = W;                // [32] z_pre, [32] dz_suf
+  const float* Sp = frec + bh * bh_stride + c * E;
+  const float* Bs = brec + bh * bh_stride + c * E;
+  const int mi = w >> 1, nj = w & 1;  // this wave's token tile and value tile
+  const int sr = tid >> 3, sc = 8 * (tid & 7);  // staging: slab row, first column
+  // loads are unconditional (clamped addresses; out-of-range entries are
+  // zeroed when written to LDS), so no branch joins them while in flight
+  float pS[8], pB[8], pz = 0.f;
+  bool rowin = false, zin = false;
+  auto fetch = [&](int f0) {
+    const int f = f0 + sr;
+    rowin = f < n;
+    const long long fr = rowin ? f : n - 1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int j = sc + e < dv ? sc + e : dv - 1;
+      pS[e] = Sp[fr * dv + j];
+      pB[e] = Bs[fr * dv + j];
+    }
+    const int fz = f0 + (tid & 31);
+    zin = fz < n;
+    pz = (tid < 32 ? Sp : Bs)[static_cast<long long>(n) * dv + (zin ? fz : n - 1)];
+  };
+  mf32x16 dvacc = {};
+  fetch(0);
+  for (int f0 = 0; f0 < n; f0 += 32) {
+    __syncthreads();  // the previous pass's readers are done with the slabs
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const bool in = rowin && sc + e < dv;
+      Sl[sr * kMS + sc + e] = in ? pS[e] : 0.f;
+      Bl[sr * kMS + sc + e] = in ? pB[e] : 0.f;
+    }
+    if (tid < 64) zl[tid] = zin ? pz : 0.f;
+    __syncthreads();
+    fetch(f0 + 32 < n ? f0 + 32 : f0);
+    // feature cotangents, transposed: Y^T (32 features x 32 tokens) with one
+    // token per lane, so the VJP's LDS adds of a lane go to its own token row.
+    // Waves 0-1: query side, Y = S_pre a_t + b_t z_pre; waves 2-3: key side,
+    // Y = dS_suf v_i + dz_suf.
+    {
+      const bool qside = w < 2;
+      const int tt = 32 * (w & 1) + l32;        // B column: token
+      const float* Bt = qside ? as + tt * (kMS + 1) : vs + tt * kMS;
+      const float* Am = qside ? Sl : Bl;
+      mf32x16 y = {};
+      for (int s2 = 0; s2 < 32; ++s2) {
+        const int j = 2 * s2 + h;
+        y = mfma_f32(Am[l32 * kMS + j], Bt[j], y);
+      }
+      // branch-free: a padded token or feature adds zeros; a diagonal pair
+      // (x, x) adds yy x once (its second add is multiplied by 0)
+      const float* X = qside ? qs : ks;
+      float* dX = qside ? dqs : dks;
+      const float bt = (tt < nt) ? (qside ? as[tt * (kMS + 1) + dv] : 1.f) : 0.f;
+      const float tlive = tt < nt ? 2.f : 0.f;
+      int pa[16], pb[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int f = f0 + 8 * (i >> 2) + 4 * h + (i & 3);
+        const uint16_t pr = pairs[f < n ? f : n - 1];
+        pa[i] = pr & 0xFF;
+        pb[i] = pr >> 8;
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int fl = 8 * (i >> 2) + 4 * h + (i & 3);
+        const float fin = (f0 + fl < n) ? tlive : 0.f;
+        const float yy = fin * (y[i] + bt * zl[(qside ? 0 : 32) + fl]);
+        const float xa = X[tt * kMS + pa[i]], xb = X[tt * kMS + pb[i]];
+        atomicAdd(&dX[tt * kMS + pa[i]], yy * xb);
+        atomicAdd(&dX[tt * kMS + pb[i]], (pa[i] != pb[i] ? yy : 0.f) * xa);
+      }
+    }
+    // dv += psi_w(K) dS_suf over these 32 features: wave (token tile mi, value tile nj)
+    {
+      const int ti = 32 * mi + l32;
+      for (int s2 = 0; s2 < 16; ++s2) {
+        const int fl = 2 * s2 + h, f = f0 + fl;
+        const uint16_t pr = pairs[f < n ? f : n - 1];
+        const int pa = pr & 0xFF, pb = pr >> 8;
+        const float wgt = (f < n) ? ((pa == pb) ? 1.f : 2.f) : 0.f;
+        const float a = wgt * ks[ti * kMS + pa] * ks[ti * kMS + pb];
+        dvacc = mfma_f32(a, Bl[fl * kMS + 32 * nj + l32], dvacc);
+      }
+    }
+  }
+  __syncthreads();
+  const int jc = 32 * nj + l32;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = 32 * mi + 8 * (i >> 2) + 4 * h + (i & 3);
+    if (r < nt && jc < dv) dvo[(hb + t0 + r) * dv + jc] = dvacc[i] + cs[r * kMS + jc];
+  }
+  for (int i = tid; i < nt * d; i += 256) {
+    const int r = i / d, x2 = i % d;
+    dq[(hb + t0) * d + i] = dqs[r * kMS + x2];
+    dk[(hb + t0) * d + i] = dks[r * kMS + x2];
+  }
+}
+
+size_t bwd_grad_mf_smem(int d, int g) {
+  const size_t n = static_cast<size_t>(bwd_n(d, g));
+  return (static_cast<size_t>(8) * 64 * kMS + 64 * (kMS + 1)) * sizeof(float) +
+         n * sizeof(uint16_t);
+}
+
+bool bwd_mf_ok(int d, int dv, int C) { return d <= 64 && dv <= 64 && C <= 64; }
+
 size_t bwd_grad_smem(int d, int C, int g) {
   const size_t n = static_cast<size_t>(bwd_n(d, g));
   return (4 * static_cast<size_t>(C) * d + 3 * static_cast<size_t>(C) * C +
@@ -346,7 +631,8 @@ size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g) {
 
 bool bwd_supported(int d, int dv, int C, int g) {
   return d >= 1 && d <= 64 && dv >= 1 && dv <= 256 && C >= 1 && C <= 64 && g >= 1 &&
-         d % g == 0 && bwd_grad_smem(d, C, g) <= 160 * 1024;
+         d % g == 0 && bwd_grad_smem(d, C, g) <= 160 * 1024 &&
+         (!bwd_mf_ok(d, dv, C) || bwd_grad_mf_smem(d, g) <= 160 * 1024);
 }
 
 template <typename Tin>
@@ -365,32 +651,61 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   const Tin* vi = static_cast<const Tin*>(v);
   const dim3 gs((n + kBFB - 1) / kBFB, NC, BH);
   const dim3 gscan(static_cast<unsigned>((E + kEB - 1) / kEB), BH);
+  const bool mf = bwd_mf_ok(d, dv, C);
+  const dim3 gsm(NC, BH);
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  bwd_chunk_state<Tin, Tin, false><<<gs, 256, 0, st>>>(ki, vi, dv, frec, T, d, dv, C, g,
+  if (mf)
+    bwd_state_mf<Tin, Tin, false><<<gsm, 256, 0, st>>>(ki, vi, dv, frec, T, d, dv, C, g,
                                                       bh_stride, E);
+  else
+    bwd_chunk_state<Tin, Tin, false><<<gs, 256, 0, st>>>(ki, vi, dv, frec, T, d, dv, C, g,
+                                                        bh_stride, E);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
-  scan_exclusive<float, BwdUnitWeight, false><<<gscan, 256, 0, st>>>(frec, frec, NC, E, bh_stride,
-                                                                    BwdUnitWeight{});
+  const bool v4 = E % 4 == 0;
+  const dim3 gscan4(static_cast<unsigned>((E + kEB4 - 1) / kEB4), BH);
+  if (v4)
+    scan_exclusive_f32x4<BwdUnitWeight, false><<<gscan4, 256, 0, st>>>(frec, NC, E, bh_stride,
+                                                                      BwdUnitWeight{});
+  else
+    scan_exclusive<float, BwdUnitWeight, false><<<gscan, 256, 0, st>>>(frec, frec, NC, E,
+                                                                      bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   const size_t cshm = bwd_coef_smem(d, C, g);
   bwd_coef<Tin><<<dim3(NC, BH), 256, cshm, st>>>(qi, ki, out, dout, frec, ab, T, d, dv, C, g,
                                                  bh_stride, E);
   if ((e = record(ev, 3, st)) != hipSuccess) return e;
-  bwd_chunk_state<Tin, float, true><<<gs, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
+  if (mf)
+    bwd_state_mf<Tin, float, true><<<gsm, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
                                                        bh_stride, E);
+  else
+    bwd_chunk_state<Tin, float, true><<<gs, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
+                                                         bh_stride, E);
   if ((e = record(ev, 4, st)) != hipSuccess) return e;
-  scan_exclusive<float, BwdUnitWeight, true><<<gscan, 256, 0, st>>>(brec, brec, NC, E, bh_stride,
-                                                                   BwdUnitWeight{});
+  if (v4)
+    scan_exclusive_f32x4<BwdUnitWeight, true><<<gscan4, 256, 0, st>>>(brec, NC, E, bh_stride,
+                                                                     BwdUnitWeight{});
+  else
+    scan_exclusive<float, BwdUnitWeight, true><<<gscan, 256, 0, st>>>(brec, brec, NC, E,
+                                                                     bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 5, st)) != hipSuccess) return e;
-  const size_t gshm = bwd_grad_smem(d, C, g);
-  if (gshm > 65536) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad<Tin>),
+  if (mf) {
+    const size_t gshm = bwd_grad_mf_smem(d, g);
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad_mf<Tin>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(gshm));
     if (e != hipSuccess) return e;
+    bwd_grad_mf<Tin><<<dim3(NC, BH), 256, gshm, st>>>(qi, ki, vi, ab, frec, brec, dq, dk, dv_out,
+                                                      T, d, dv, C, g, bh_stride, E);
+  } else {
+    const size_t gshm = bwd_grad_smem(d, C, g);
+    if (gshm > 65536) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad<Tin>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(gshm));
+      if (e != hipSuccess) return e;
+    }
+    bwd_grad<Tin><<<dim3(NC, BH), 256, gshm, st>>>(qi, ki, vi, ab, frec, brec, dq, dk, dv_out, T,
+                                                   d, dv, C, g, bh_stride, E);
   }
-  bwd_grad<Tin><<<dim3(NC, BH), 256, gshm, st>>>(qi, ki, vi, ab, frec, brec, dq, dk, dv_out, T, d,
-                                                 dv, C, g, bh_stride, E);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 6, st);
 }

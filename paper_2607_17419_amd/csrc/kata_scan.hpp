@@ -211,7 +211,8 @@ namespace kata {
 // access per record) x kRPT4 records; the up-sweep / down-sweep runs over its
 // records in registers, the row-group totals are scanned through LDS, and
 // blocks of kNB4 records are chained by a carry.  All of a thread's loads of
-// a block are issued together.  E must be a multiple of 4.
+// a block are issued together.  E must be a multiple of 4.  kReverse scans the
+// records in reverse order (record c receives the sum over c' > c).
 // grid (ceil(E / kEB4), BH), block 256.
 // ---------------------------------------------------------------------------
 constexpr int kCG4 = 32;               // column groups of 4 elements
@@ -220,7 +221,7 @@ constexpr int kRG4 = 256 / kCG4;       // row groups (8)
 constexpr int kRPT4 = 8;               // records per thread and block
 constexpr int kNB4 = kRG4 * kRPT4;     // records per block (64)
 
-template <typename Weight>
+template <typename Weight, bool kReverse = false>
 __global__ __launch_bounds__(256) void scan_exclusive_f32x4(float* rec, int N, long long E,
                                                             long long bh_stride, Weight weight) {
   __shared__ float4 tot[kRG4][kCG4];
@@ -242,7 +243,8 @@ __global__ __launch_bounds__(256) void scan_exclusive_f32x4(float* rec, int N, l
     for (int j = 0; j < kRPT4; ++j) {
       float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
       if (active && rbase + j < N)
-        a = *reinterpret_cast<const float4*>(rb + static_cast<long long>(rbase + j) * E + ec);
+        a = *reinterpret_cast<const float4*>(
+            rb + static_cast<long long>(kReverse ? N - 1 - (rbase + j) : rbase + j) * E + ec);
       v[j][0] = a.x;
       v[j][1] = a.y;
       v[j][2] = a.z;
@@ -292,7 +294,8 @@ __global__ __launch_bounds__(256) void scan_exclusive_f32x4(float* rec, int N, l
 #pragma unroll
     for (int j = 0; j < kRPT4; ++j) {
       if (active && rbase + j < N)
-        *reinterpret_cast<float4*>(rb + static_cast<long long>(rbase + j) * E + ec) =
+        *reinterpret_cast<float4*>(
+            rb + static_cast<long long>(kReverse ? N - 1 - (rbase + j) : rbase + j) * E + ec) =
             make_float4(w[0] * (pre[0] + v[j][0]), w[1] * (pre[1] + v[j][1]),
                         w[2] * (pre[2] + v[j][2]), w[3] * (pre[3] + v[j][3]));
     }

@@ -130,6 +130,16 @@ def test_bwd_value_width_and_recall(kata, orc):
     ref = orc.bwd_mg(q, k, v, dout, 3)
     _check_f32(_gpu_bwd(kata, inp, "f32", dout, 24, 3, out=orc.fwd_mg(q, k, v, 3)), ref,
                "d24 dv40 g3 bwd")
+    # dv > 64 takes the VALU kernels (the matrix-core variants stage 64 columns)
+    log("case bwd fp32 inputs d16 dv96 C40 B1 H2 T301 (VALU kernels)")
+    q = rng.standard_normal((1, 2, 301, 16)).astype(np.float32)
+    k = rng.standard_normal((1, 2, 301, 16)).astype(np.float32)
+    v = rng.standard_normal((1, 2, 301, 96)).astype(np.float32)
+    dout = _dout(v.shape, 21)
+    inp = dict(q_dev=q, k_dev=k, v_dev=v)
+    ref = orc.bwd_mg(q, k, v, dout, 2)
+    _check_f32(_gpu_bwd(kata, inp, "f32", dout, 40, 2, out=orc.fwd_mg(q, k, v, 2)), ref,
+               "d16 dv96 g2 bwd")
     log("case bwd recall-shaped bf16 B1 H2 T1500 d32 dv64 C64")
     inp = workloads.make_inputs("recall_bf16", B=1, H=2, T=1500)
     dout = _dout(inp["v"].shape, 23)
