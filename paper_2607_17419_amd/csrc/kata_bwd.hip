@@ -403,10 +403,33 @@ __global__ __launch_bounds__(256) void bwd_state_mf(const Tx* __restrict__ x,
   }
 }
 
+// LDS element type of the staged q, k, v rows: bf16 inputs stay bf16 (exact),
+// which halves those tiles; fp32 inputs stay fp32.
+template <typename Tin> struct GradLds { using T = float; static constexpr int S = kMS; };
+template <> struct GradLds<bf16_t> { using T = uint16_t; static constexpr int S = kMS + 1; };
+__device__ __forceinline__ float lds_f32(float x) { return x; }
+__device__ __forceinline__ float lds_f32(uint16_t x) {
+  return __uint_as_float(static_cast<uint32_t>(x) << 16);
+}
+__device__ __forceinline__ void lds_put(float* p, float x) { *p = x; }
+__device__ __forceinline__ void lds_put(uint16_t* p, float x) {
+  *p = static_cast<uint16_t>(__float_as_uint(x) >> 16);  // exact: x is a bf16 value
+}
+__device__ __forceinline__ float in_f32(const float* p, long long i) { return p[i]; }
+__device__ __forceinline__ float in_f32(const bf16_t* p, long long i) { return to_f32(p[i]); }
+
 // Gradients of chunk c with the inter-chunk products on the matrix cores.
-// grid (NC, BH), block 256, dynamic LDS bwd_grad_mf_smem(...).
+// In-chunk terms in VALU with each thread's 16 (token, coordinate) and
+// (token, value) entries kept in registers; inter-chunk terms as dense
+// products over the symmetric states, one coordinate y at a time:
+//   dq_t[x] += 2 sum_y q_t[y] (sum_j S[x,y][j] a_tj + b_t z[x,y])
+//   dk_i[x] += 2 sum_y k_i[y] (sum_j dS[x,y][j] v_ij + dz[x,y])
+//   dv_i[j] += sum_{x >= y} w_xy k_ix k_iy dS[x,y][j]      (w = 1 on x = y, else 2)
+// with S[x,y] = S[y,x] the packed prefix row of the pair (0 across blocks)
+// and dS the suffix row.  grid (NC, BH), block 256, dynamic LDS
+// bwd_grad_mf_smem(...); two workgroups fit a CU for bf16 inputs.
 template <typename Tin>
-__global__ __launch_bounds__(256) void bwd_grad_mf(const Tin* __restrict__ q,
+__global__ __launch_bounds__(256, 2) void bwd_grad_mf(const Tin* __restrict__ q,
                                                    const Tin* __restrict__ k,
                                                    const Tin* __restrict__ v,
                                                    const float* __restrict__ ab,
@@ -416,18 +439,17 @@ __global__ __launch_bounds__(256) void bwd_grad_mf(const Tin* __restrict__ q,
                                                    float* __restrict__ dvo, int T, int d, int dv,
                                                    int C, int g, long long bh_stride,
                                                    long long E) {
+  using LT = typename GradLds<Tin>::T;
+  constexpr int LS = GradLds<Tin>::S;
   extern __shared__ float bsm[];
   const int n = bwd_n(d, g), m = d / g;
-  float* qs = bsm;              // [64][kMS] queries
-  float* ks = qs + 64 * kMS;    // keys
-  float* vs = ks + 64 * kMS;    // values
-  float* as = vs + 64 * kMS;    // [64][kMS + 1]: a_t (dv), b_t at column dv
-  float* dqs = as + 64 * (kMS + 1);
-  float* dks = dqs + 64 * kMS;
-  float* cs = dks + 64 * kMS;   // [64][kMS] dL/dw_ti, later the in-chunk dv
-  float* sb = cs + 64 * kMS;    // [64][kMS] block scores; later the two slabs
-  float* W = sb + 64 * kMS;     // [64][kMS] in-chunk weights
-  uint16_t* pairs = reinterpret_cast<uint16_t*>(W + 64 * kMS);
+  float* as = bsm;                  // [64][kMS + 1]: a_t (dv), b_t at column dv
+  float* cs = as + 64 * (kMS + 1);  // [64][kMS] dL/dw_ti; later the suffix slab SB
+  float* sb = cs + 64 * kMS;        // [64][kMS] block scores; later the prefix slab SA
+  LT* qs = reinterpret_cast<LT*>(sb + 64 * kMS);  // [64][LS]
+  LT* ks = qs + 64 * LS;
+  LT* vs = ks + 64 * LS;            // column dv holds 1 (the coefficient of dz)
+  uint16_t* pairs = reinterpret_cast<uint16_t*>(vs + 64 * LS);
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const long long t0 = static_cast<long long>(c) * C;
@@ -438,15 +460,13 @@ __global__ __launch_bounds__(256) void bwd_grad_mf(const Tin* __restrict__ q,
   const Tin* vh = v + (hb + t0) * dv;
   const float* abh = ab + (hb + t0) * (dv + 1);
   bwd_pair_table(pairs, d, g);
-  for (int i = tid; i < 64 * kMS; i += 256) {
-    const int t = i / kMS, a = i % kMS;
+  for (int i = tid; i < 64 * LS; i += 256) {
+    const int t = i / LS, a = i % LS;
     const bool in = t < nt;
-    qs[i] = (in && a < d) ? load_f32(qh, static_cast<long long>(t) * d + a) : 0.f;
-    ks[i] = (in && a < d) ? load_f32(kh, static_cast<long long>(t) * d + a) : 0.f;
-    vs[i] = (in && a < dv) ? load_f32(vh, static_cast<long long>(t) * dv + a) : 0.f;
-    dqs[i] = 0.f;
-    dks[i] = 0.f;
-    W[i] = 0.f;
+    lds_put(&qs[i], (in && a < d) ? in_f32(qh, static_cast<long long>(t) * d + a) : 0.f);
+    lds_put(&ks[i], (in && a < d) ? in_f32(kh, static_cast<long long>(t) * d + a) : 0.f);
+    lds_put(&vs[i], (in && a < dv) ? in_f32(vh, static_cast<long long>(t) * dv + a)
+                                   : (a == dv ? 1.f : 0.f));
   }
   for (int i = tid; i < 64 * (kMS + 1); i += 256) {
     const int t = i / (kMS + 1), j = i % (kMS + 1);
@@ -455,155 +475,196 @@ __global__ __launch_bounds__(256) void bwd_grad_mf(const Tin* __restrict__ q,
   __syncthreads();
   // dL/dw_ti = <a_t, v_i> + b_t for i <= t
   for (int i = tid; i < 64 * 64; i += 256) {
-    const int t = i >> 6, s = i & 63;
+    const int t = i >> 6, s2 = i & 63;
     float cw = 0.f;
-    if (s <= t && t < nt) {
+    if (s2 <= t && t < nt) {
       cw = as[t * (kMS + 1) + dv];
-      for (int j = 0; j < dv; ++j) cw += as[t * (kMS + 1) + j] * vs[s * kMS + j];
+      for (int j = 0; j < dv; ++j) cw += as[t * (kMS + 1) + j] * lds_f32(vs[s2 * LS + j]);
     }
-    cs[t * kMS + s] = cw;
+    cs[t * kMS + s2] = cw;
   }
+  // this thread's register entries: (token e >> 6, coordinate / value e & 63)
+  // for e = tid + 256 r, r = 0..15
+  float dqi[16], dki[16], dvi[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dqi[r] = dki[r] = dvi[r] = 0.f;
   __syncthreads();
-  // in-chunk pairs, one feature block at a time
   for (int blk = 0; blk < g; ++blk) {
     for (int i = tid; i < 64 * 64; i += 256) {
-      const int t = i >> 6, s = i & 63;
+      const int t = i >> 6, s2 = i & 63;
       float sc = 0.f;
-      if (s <= t)
-        for (int x2 = blk * m; x2 < blk * m + m; ++x2) sc += qs[t * kMS + x2] * ks[s * kMS + x2];
-      sb[t * kMS + s] = sc;
-      W[t * kMS + s] += sc * sc;
+      if (s2 <= t)
+        for (int x2 = blk * m; x2 < blk * m + m; ++x2)
+          sc += lds_f32(qs[t * LS + x2]) * lds_f32(ks[s2 * LS + x2]);
+      sb[t * kMS + s2] = sc;
     }
     __syncthreads();
-    for (int i = tid; i < 64 * m; i += 256) {
-      const int t = i / m, x2 = blk * m + i % m;
-      float aq = 0.f, ak = 0.f;
-      for (int s = 0; s <= t; ++s) aq += cs[t * kMS + s] * sb[t * kMS + s] * ks[s * kMS + x2];
-      for (int u = t; u < 64; ++u) ak += cs[u * kMS + t] * sb[u * kMS + t] * qs[u * kMS + x2];
-      dqs[t * kMS + x2] += 2.f * aq;
-      dks[t * kMS + x2] += 2.f * ak;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int e = tid + 256 * r, t = e >> 6, x2 = e & 63;
+      if (x2 >= blk * m && x2 < blk * m + m && x2 < d) {
+        float aq = 0.f, ak = 0.f;
+        for (int s2 = 0; s2 <= t; ++s2)
+          aq += cs[t * kMS + s2] * sb[t * kMS + s2] * lds_f32(ks[s2 * LS + x2]);
+        for (int u = t; u < 64; ++u)
+          ak += cs[u * kMS + t] * sb[u * kMS + t] * lds_f32(qs[u * LS + x2]);
+        dqi[r] += 2.f * aq;  // row t as the query
+        dki[r] += 2.f * ak;  // row t as the key
+      }
+      if (x2 < dv) {  // in-chunk dv of row t: sum_{u >= t} w_ut a_u over this block
+        float av = 0.f;
+        for (int u = t; u < nt; ++u) av += sb[u * kMS + t] * sb[u * kMS + t] * as[u * (kMS + 1) + x2];
+        dvi[r] += av;
+      }
     }
     __syncthreads();
   }
-  // in-chunk dv into cs (free now): sum_{t >= i} w_ti a_t
-  for (int i = tid; i < 64 * 64; i += 256) {
-    const int r = i >> 6, j = i & 63;
-    float acc = 0.f;
-    if (j < dv)
-      for (int t = r; t < nt; ++t) acc += W[t * kMS + r] * as[t * (kMS + 1) + j];
-    cs[r * kMS + j] = acc;
-  }
-  __syncthreads();
-  // inter-chunk terms, 32 features per pass: the prefix slab (S_pre rows, then
-  // z_pre) and the suffix slab (dS_suf rows, then dz_suf) staged over sb; the
-  // next pass's slab is loaded into registers while this one is consumed
-  float* Sl = sb;               // [32][kMS]
-  float* Bl = sb + 32 * kMS;    // [32][kMS]
-  float* zl = W;                // [32] z_pre, [32] dz_suf
+  // inter-chunk products: the y-slabs SA (prefix rows, z at column dv) and SB
+  // (suffix rows, dz at column dv) over sb and cs; the next y's rows are
+  // gathered into registers while this y is consumed
+  float* SA = sb;
+  float* SB = cs;
   const float* Sp = frec + bh * bh_stride + c * E;
   const float* Bs = brec + bh * bh_stride + c * E;
-  const int mi = w >> 1, nj = w & 1;  // this wave's token tile and value tile
-  const int sr = tid >> 3, sc = 8 * (tid & 7);  // staging: slab row, first column
-  // loads are unconditional (clamped addresses; out-of-range entries are
-  // zeroed when written to LDS), so no branch joins them while in flight
-  float pS[8], pB[8], pz = 0.f;
-  bool rowin = false, zin = false;
-  auto fetch = [&](int f0) {
-    const int f = f0 + sr;
-    rowin = f < n;
-    const long long fr = rowin ? f : n - 1;
+  const int nm = m * (m + 1) / 2;
+  const int mi = w >> 1, nj = w & 1;  // this wave's token tile and value tile (dv)
+  const int sx = tid >> 2, sq = tid & 3;  // staging: slab row x, column quarter
+  float pA[16], pB[16], pzA = 0.f, pzB = 0.f;
+  bool rin = false;
+  // rows start 16-byte aligned when the record length and dv are multiples of
+  // 4: then each thread fetches its 16 columns as four 16-byte loads
+  const bool v4 = (E % 4 == 0) && (dv % 16 == 0);
+  auto fetch = [&](int y) {
+    rin = sx < d && sx / m == y / m;
+    const int a = min(sx, y) % m, b = max(sx, y) % m;
+    const long long f = rin ? static_cast<long long>(y / m) * nm + packed_index(a, b, m) : 0;
+    if (v4) {
+      const int c0 = min(16 * sq, dv - 16);  // clamped address; masked when written
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = sc + e < dv ? sc + e : dv - 1;
-      pS[e] = Sp[fr * dv + j];
-      pB[e] = Bs[fr * dv + j];
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const float4 ua = *reinterpret_cast<const float4*>(Sp + f * dv + c0 + 4 * e4);
+        const float4 ub = *reinterpret_cast<const float4*>(Bs + f * dv + c0 + 4 * e4);
+        pA[4 * e4] = ua.x; pA[4 * e4 + 1] = ua.y; pA[4 * e4 + 2] = ua.z; pA[4 * e4 + 3] = ua.w;
+        pB[4 * e4] = ub.x; pB[4 * e4 + 1] = ub.y; pB[4 * e4 + 2] = ub.z; pB[4 * e4 + 3] = ub.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int j = min(16 * sq + e, dv - 1);  // clamped address; masked when written
+        pA[e] = Sp[f * dv + j];
+        pB[e] = Bs[f * dv + j];
+      }
     }
-    const int fz = f0 + (tid & 31);
-    zin = fz < n;
-    pz = (tid < 32 ? Sp : Bs)[static_cast<long long>(n) * dv + (zin ? fz : n - 1)];
+    pzA = Sp[static_cast<long long>(n) * dv + f];
+    pzB = Bs[static_cast<long long>(n) * dv + f];
   };
+  mf32x16 accx[2] = {{}, {}};  // waves 0-1: dq tiles, waves 2-3: dk tiles (x tile 0, 1)
   mf32x16 dvacc = {};
+  const bool qside = w < 2;
+  const int tt = 32 * (w & 1) + l32;  // A row of the dq / dk product: token
+  const LT* Xr = (qside ? qs : ks) + tt * LS;
+  const int nks = (dv + 2) / 2;       // K-steps over j = 0..dv (column dv: z)
   fetch(0);
-  for (int f0 = 0; f0 < n; f0 += 32) {
-    __syncthreads();  // the previous pass's readers are done with the slabs
+  for (int y = 0; y < d; ++y) {
+    __syncthreads();  // the previous y's readers are done with the slabs
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const bool in = rowin && sc + e < dv;
-      Sl[sr * kMS + sc + e] = in ? pS[e] : 0.f;
-      Bl[sr * kMS + sc + e] = in ? pB[e] : 0.f;
+    for (int e = 0; e < 16; ++e) {
+      const int j = 16 * sq + e;
+      const float za = (j == dv) ? pzA : 0.f, zb = (j == dv) ? pzB : 0.f;
+      SA[sx * kMS + j] = rin ? (j < dv ? pA[e] : za) : 0.f;
+      SB[sx * kMS + j] = rin ? (j < dv ? pB[e] : zb) : 0.f;
     }
-    if (tid < 64) zl[tid] = zin ? pz : 0.f;
+    if (sq == 3) {
+      SA[sx * kMS + 64] = (rin && dv == 64) ? pzA : 0.f;
+      SB[sx * kMS + 64] = (rin && dv == 64) ? pzB : 0.f;
+    }
     __syncthreads();
-    fetch(f0 + 32 < n ? f0 + 32 : f0);
-    // feature cotangents, transposed: Y^T (32 features x 32 tokens) with one
-    // token per lane, so the VJP's LDS adds of a lane go to its own token row.
-    // Waves 0-1: query side, Y = S_pre a_t + b_t z_pre; waves 2-3: key side,
-    // Y = dS_suf v_i + dz_suf.
+    fetch(y + 1 < d ? y + 1 : y);
     {
-      const bool qside = w < 2;
-      const int tt = 32 * (w & 1) + l32;        // B column: token
-      const float* Bt = qside ? as + tt * (kMS + 1) : vs + tt * kMS;
-      const float* Am = qside ? Sl : Bl;
-      mf32x16 y = {};
-      for (int s2 = 0; s2 < 32; ++s2) {
+      // A: x_t[y] times a_tj (j < dv), b_t (j = dv) on the query side, v_ij
+      // (j < dv), 1 (j = dv) on the key side; zero past dv.  Operands of step
+      // s + 1 are loaded before the MFMAs of step s.
+      const float xy = lds_f32(Xr[y]);
+      const float* Bm = qside ? SA : SB;
+      auto ldA = [&](int s2) {
+        const int j = 2 * s2 + h, jj = j <= dv ? j : dv;
+        const float av = qside ? as[tt * (kMS + 1) + jj] : lds_f32(vs[tt * LS + jj]);
+        return (j <= dv ? xy : 0.f) * av;
+      };
+      auto ldB = [&](int s2, int xt) {
         const int j = 2 * s2 + h;
-        y = mfma_f32(Am[l32 * kMS + j], Bt[j], y);
-      }
-      // branch-free: a padded token or feature adds zeros; a diagonal pair
-      // (x, x) adds yy x once (its second add is multiplied by 0)
-      const float* X = qside ? qs : ks;
-      float* dX = qside ? dqs : dks;
-      const float bt = (tt < nt) ? (qside ? as[tt * (kMS + 1) + dv] : 1.f) : 0.f;
-      const float tlive = tt < nt ? 2.f : 0.f;
-      int pa[16], pb[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int f = f0 + 8 * (i >> 2) + 4 * h + (i & 3);
-        const uint16_t pr = pairs[f < n ? f : n - 1];
-        pa[i] = pr & 0xFF;
-        pb[i] = pr >> 8;
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int fl = 8 * (i >> 2) + 4 * h + (i & 3);
-        const float fin = (f0 + fl < n) ? tlive : 0.f;
-        const float yy = fin * (y[i] + bt * zl[(qside ? 0 : 32) + fl]);
-        const float xa = X[tt * kMS + pa[i]], xb = X[tt * kMS + pb[i]];
-        atomicAdd(&dX[tt * kMS + pa[i]], yy * xb);
-        atomicAdd(&dX[tt * kMS + pb[i]], (pa[i] != pb[i] ? yy : 0.f) * xa);
+        return Bm[(32 * xt + l32) * kMS + (j <= dv ? j : dv)];
+      };
+      float a = ldA(0), b0 = ldB(0, 0), b1 = ldB(0, 1);
+      for (int s2 = 0; s2 < nks; ++s2) {
+        const int sn = s2 + 1 < nks ? s2 + 1 : s2;
+        const float an = ldA(sn), b0n = ldB(sn, 0), b1n = ldB(sn, 1);
+        accx[0] = mfma_f32(a, b0, accx[0]);
+        accx[1] = mfma_f32(a, b1, accx[1]);
+        a = an;
+        b0 = b0n;
+        b1 = b1n;
       }
     }
-    // dv += psi_w(K) dS_suf over these 32 features: wave (token tile mi, value tile nj)
     {
       const int ti = 32 * mi + l32;
-      for (int s2 = 0; s2 < 16; ++s2) {
-        const int fl = 2 * s2 + h, f = f0 + fl;
-        const uint16_t pr = pairs[f < n ? f : n - 1];
-        const int pa = pr & 0xFF, pb = pr >> 8;
-        const float wgt = (f < n) ? ((pa == pb) ? 1.f : 2.f) : 0.f;
-        const float a = wgt * ks[ti * kMS + pa] * ks[ti * kMS + pb];
-        dvacc = mfma_f32(a, Bl[fl * kMS + 32 * nj + l32], dvacc);
+      const float ky = lds_f32(ks[ti * LS + y]);
+      const int nx = (64 - y + 1) / 2;
+      auto ldK = [&](int s2) {
+        const int x2 = y + 2 * s2 + h;
+        const int xc = x2 < 64 ? x2 : 63;
+        const float wgt = x2 < 64 ? (x2 == y ? 1.f : 2.f) : 0.f;
+        return wgt * ky * lds_f32(ks[ti * LS + xc]);
+      };
+      auto ldS = [&](int s2) {
+        const int x2 = y + 2 * s2 + h;
+        return SB[(x2 < 64 ? x2 : 63) * kMS + 32 * nj + l32];
+      };
+      float a = ldK(0), b = ldS(0);
+      for (int s2 = 0; s2 < nx; ++s2) {
+        const int sn = s2 + 1 < nx ? s2 + 1 : s2;
+        const float an = ldK(sn), bn = ldS(sn);
+        dvacc = mfma_f32(a, b, dvacc);
+        a = an;
+        b = bn;
       }
     }
   }
   __syncthreads();
-  const int jc = 32 * nj + l32;
+  // the waves' products into LDS (dq over SA, dk over SB, dv over as), then
+  // each thread adds its in-chunk register entries and writes them out
+  {
+    float* dP = qside ? SA : SB;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int r = 32 * mi + 8 * (i >> 2) + 4 * h + (i & 3);
-    if (r < nt && jc < dv) dvo[(hb + t0 + r) * dv + jc] = dvacc[i] + cs[r * kMS + jc];
+    for (int xt = 0; xt < 2; ++xt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int t = 32 * (w & 1) + 8 * (i >> 2) + 4 * h + (i & 3);
+        dP[t * kMS + 32 * xt + l32] = 2.f * accx[xt][i];
+      }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 32 * mi + 8 * (i >> 2) + 4 * h + (i & 3);
+      as[r * (kMS + 1) + 32 * nj + l32] = dvacc[i];
+    }
   }
-  for (int i = tid; i < nt * d; i += 256) {
-    const int r = i / d, x2 = i % d;
-    dq[(hb + t0) * d + i] = dqs[r * kMS + x2];
-    dk[(hb + t0) * d + i] = dks[r * kMS + x2];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int e = tid + 256 * r, t = e >> 6, x2 = e & 63;
+    if (t < nt && x2 < d) {
+      dq[(hb + t0 + t) * d + x2] = dqi[r] + SA[t * kMS + x2];
+      dk[(hb + t0 + t) * d + x2] = dki[r] + SB[t * kMS + x2];
+    }
+    if (t < nt && x2 < dv) dvo[(hb + t0 + t) * dv + x2] = dvi[r] + as[t * (kMS + 1) + x2];
   }
 }
 
-size_t bwd_grad_mf_smem(int d, int g) {
+size_t bwd_grad_mf_smem(int d, int g, bool bf16_lds) {
   const size_t n = static_cast<size_t>(bwd_n(d, g));
-  return (static_cast<size_t>(8) * 64 * kMS + 64 * (kMS + 1)) * sizeof(float) +
-         n * sizeof(uint16_t);
+  const size_t f32 = (static_cast<size_t>(64) * (kMS + 1) + 2 * 64 * kMS) * sizeof(float);
+  const size_t xyz = bf16_lds ? 3 * 64 * (kMS + 1) * sizeof(uint16_t) : 3 * 64 * kMS * sizeof(float);
+  return f32 + xyz + n * sizeof(uint16_t);
 }
 
 bool bwd_mf_ok(int d, int dv, int C) { return d <= 64 && dv <= 64 && C <= 64; }
@@ -632,7 +693,7 @@ size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g) {
 bool bwd_supported(int d, int dv, int C, int g) {
   return d >= 1 && d <= 64 && dv >= 1 && dv <= 256 && C >= 1 && C <= 64 && g >= 1 &&
          d % g == 0 && bwd_grad_smem(d, C, g) <= 160 * 1024 &&
-         (!bwd_mf_ok(d, dv, C) || bwd_grad_mf_smem(d, g) <= 160 * 1024);
+         (!bwd_mf_ok(d, dv, C) || bwd_grad_mf_smem(d, g, false) <= 160 * 1024);
 }
 
 template <typename Tin>
@@ -690,7 +751,7 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
                                                                      bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 5, st)) != hipSuccess) return e;
   if (mf) {
-    const size_t gshm = bwd_grad_mf_smem(d, g);
+    const size_t gshm = bwd_grad_mf_smem(d, g, sizeof(Tin) == 2);
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad_mf<Tin>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(gshm));
     if (e != hipSuccess) return e;
