@@ -12,7 +12,8 @@ workload (B=256, H=16, 1024-token prefix, 128 steps) is measured in the same
 run and reported under "decode"; KATA-M2 under "m2"; the quadratic form
 against the chunked one under "quadratic_vs_chunked"; causal linear attention
 with the linear feature maps (the paper's associative-scan shape, B=1, H=16,
-d=64, C=128) under "linear_features".  The CPU oracle is timed on a bounded
+d=64, C=128) under "linear_features"; the training step (forward + chunked
+backward) at B=8, H=16, d=64 under "backward".  The CPU oracle is timed on a bounded
 sample of rows of the same workload and reported under "cpu_baseline".
 """
 from __future__ import annotations
@@ -377,6 +378,101 @@ def bench_linear(kata, dev, hip, steps=10, warmup=3, probe=False):
             "features": per_feature, "t_sweep_identity_B1_H16": sweep}
 
 
+# Paper's linear-state training step (forward + backward) at B = 8, H = 16,
+# d = 64, bf16 on an H100 (training-step latency table), ms: context.
+PAPER_TRAIN_STEP_H100 = {1024: 10.14, 2048: 20.07, 4096: 39.93, 8192: 79.58}
+PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
+
+
+def bwd_flop(BH, T, d, dv, C):
+    """Algorithmic flops of the chunked backward per stage, counted on the
+    packed features (n = d(d+1)/2): chunk states 2 C n dv per chunk (forward
+    and backward); gradients 4 C n (dv+1) (query- and key-side feature
+    cotangents) + 2 C n dv (dv readout) + C^2 (2 dv + 3 d) (in-chunk terms)."""
+    n = d * (d + 1) // 2
+    NC = -(-T // C)
+    chunks = BH * NC
+    return {"state": chunks * 2 * C * n * dv,
+            "grad": chunks * (4 * C * n * (dv + 1) + 2 * C * n * dv + C * C * (2 * dv + 3 * d))}
+
+
+def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=2):
+    """Training step of KATA-M1 (forward on the bf16 MFMA path, then the O(T)
+    chunked backward) at the paper's training-table shape B = 8, H = 16,
+    d = dv = 64, C = 64, bf16 inputs, fp32 gradients; per-stage HIP-event
+    times of the backward and the fp32 matrix rates of its state and gradient
+    kernels."""
+    import torch
+    import workloads
+    B, H, d, dv, C = 8, 16, 64, 64, 64
+    rows = []
+    for T in Ts:
+        if T == workloads.WORKLOADS["mid_bf16"].T:
+            inp = workloads.make_inputs("mid_bf16")
+            q, k, v = (upload(inp[nm], "bf16", dev) for nm in ("q_dev", "k_dev", "v_dev"))
+            src = "mid_bf16 inputs"
+        else:  # same recipe, drawn on the device
+            g_ = torch.Generator(device=dev)
+            g_.manual_seed(1000 + T)
+            q = torch.randn(B, H, T, d, device=dev, generator=g_)
+            k = torch.randn(B, H, T, d, device=dev, generator=g_)
+            q = (q / q.norm(dim=-1, keepdim=True)).bfloat16().contiguous()
+            k = (k / k.norm(dim=-1, keepdim=True)).bfloat16().contiguous()
+            v = torch.randn(B, H, T, dv, device=dev, generator=g_).bfloat16().contiguous()
+            src = "seeded on device (same recipe)"
+        g2 = torch.Generator(device=dev)
+        g2.manual_seed(7)
+        dout = torch.randn(B, H, T, dv, device=dev, generator=g2)
+        span = kata.default_span(B, H, T, d, dv, C, kata.KATA_BF16)
+        fws = torch.empty(kata.workspace_bytes(B, H, T, d, dv, C, kata.KATA_BF16, span),
+                          dtype=torch.uint8, device=dev)
+        bws = torch.empty(kata.bwd_workspace_bytes(B, H, T, d, dv, C, 1, kata.KATA_BF16),
+                          dtype=torch.uint8, device=dev)
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+        grads = tuple(torch.empty((B, H, T, x), dtype=torch.float32, device=dev)
+                      for x in (d, d, dv))
+        fev = Events(hip, 4 * max(steps, warmup))
+        bev = Events(hip, 7 * max(steps, warmup))
+        for i in range(warmup):
+            kata.fwd_chunked_timed(q, k, v, C, fev.block(4 * i), span_chunks=span, out=out,
+                                   workspace=fws)
+            kata.bwd_chunked(q, k, v, out, dout, C, 1, workspace=bws, events=bev.block(7 * i),
+                             grads=grads)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            kata.fwd_chunked_timed(q, k, v, C, fev.block(4 * i), span_chunks=span, out=out,
+                                   workspace=fws)
+            kata.bwd_chunked(q, k, v, out, dout, C, 1, workspace=bws, events=bev.block(7 * i),
+                             grads=grads)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / steps
+        names = ("fwd_states", "prefix_scan", "coefficients", "bwd_states", "suffix_scan",
+                 "gradients")
+        st = {nm: sum(bev.elapsed(7 * i + j, 7 * i + j + 1) for i in range(steps)) / steps
+              for j, nm in enumerate(names)}
+        fwd_ms = sum(fev.elapsed(4 * i, 4 * i + 3) for i in range(steps)) / steps
+        fev.close()
+        bev.close()
+        fl = bwd_flop(B * H, T, d, dv, C)
+
+        def rate(flop, t_ms):
+            tf = flop / (t_ms * 1e-3) / 1e12
+            return {"bound": "mfma_fp32", "achieved": round(tf, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)}
+        rows.append({"T": T, "inputs": src, "train_step_ms": round(ms, 3),
+                     "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
+                     "tokens_per_s": B * T / (ms * 1e-3),
+                     "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
+                     "gradients_roofline": rate(fl["grad"], st["gradients"]),
+                     "bwd_states_roofline": rate(fl["state"], st["bwd_states"]),
+                     "paper_linear_state_m1_train_step_h100_ms": PAPER_TRAIN_STEP_H100.get(T)})
+        del fws, bws, out, grads, q, k, v, dout
+        torch.cuda.empty_cache()
+    return {"config": "KATA-M1 B8 H16 d64 dv64 C64, bf16 inputs, fp32 gradients of "
+                      "sum <dout, o> (dout ~ N(0,1))", "rows": rows}
+
+
 # the KATA-M1 kernels of the d = 64 long-context workload (the M2 and
 # quadratic-form instantiations share the names, not the template arguments)
 KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
@@ -516,6 +612,7 @@ def main():
     ap.add_argument("--no-quadratic", action="store_true")
     ap.add_argument("--no-m2", action="store_true")
     ap.add_argument("--no-linear", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--linear-probe", action="store_true",
                     help="only run the psi(x) = x linear-feature forward (for rocprofv3 --pmc)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -639,6 +736,8 @@ def main():
         res["quadratic_vs_chunked"] = bench_quadratic(kata, dev)
     if not args.no_linear:
         res["linear_features"] = bench_linear(kata, dev, hip)
+    if not args.no_backward:
+        res["backward"] = bench_backward(kata, dev, hip)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)
