@@ -481,7 +481,7 @@ KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
 COPY_BYTES = 1 << 30
 # the linear-feature kernels of psi(x) = x (plain readout) at d = dv = 64
 LIN_KERNELS = {"span_state": "lin_span_state<0>",
-               "scan": "scan_exclusive_f32x4<kata::LinUnitWeight>",
+               "scan": "scan_exclusive_f32x4<kata::LinUnitWeight",
                "span_output": "lin_span_output<0, false>"}
 
 
