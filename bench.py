@@ -396,12 +396,22 @@ def bwd_flop(BH, T, d, dv, C):
             "grad": chunks * (4 * C * n * (dv + 1) + 2 * C * n * dv + C * C * (2 * dv + 3 * d))}
 
 
+def bwd_grad_bytes(BH, T, d, dv, C):
+    """Algorithmic HBM bytes of the gradients launch: per chunk the prefix and
+    suffix records (n dv + n fp32 each), the bf16 q, k, v rows, the fp32
+    a_t | b_t rows, and the fp32 dq, dk, dv rows written."""
+    n = d * (d + 1) // 2
+    NC = -(-T // C)
+    per_chunk = 2 * (n * dv + n) * 4 + C * (2 * d + dv) * 2 + C * (dv + 1) * 4 + C * (2 * d + dv) * 4
+    return BH * NC * per_chunk
+
+
 def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=2):
     """Training step of KATA-M1 (forward on the bf16 MFMA path, then the O(T)
     chunked backward) at the paper's training-table shape B = 8, H = 16,
     d = dv = 64, C = 64, bf16 inputs, fp32 gradients; per-stage HIP-event
-    times of the backward and the fp32 matrix rates of its state and gradient
-    kernels."""
+    times of the backward, the fp32 matrix rate of its state kernels and the
+    HBM rate (with the bf16 matrix rate beside it) of the gradients kernel."""
     import torch
     import workloads
     B, H, d, dv, C = 8, 16, 64, 64, 64
@@ -460,11 +470,21 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
             tf = flop / (t_ms * 1e-3) / 1e12
             return {"bound": "mfma_fp32", "achieved": round(tf, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)}
+
+        def grad_rate(t_ms):
+            # bf16 inputs at d = dv = C = 64 take the bf16 matrix-core gradients
+            # kernel, whose bound is the two records it streams per chunk
+            gbs = bwd_grad_bytes(B * H, T, d, dv, C) / (t_ms * 1e-3) / 1e9
+            tf = fl["grad"] / (t_ms * 1e-3) / 1e12
+            return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(gbs / PEAK_HBM_GBS, 4),
+                    "mfma_bf16": {"achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
+                                  "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}}
         rows.append({"T": T, "inputs": src, "train_step_ms": round(ms, 3),
                      "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
                      "tokens_per_s": B * T / (ms * 1e-3),
                      "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
-                     "gradients_roofline": rate(fl["grad"], st["gradients"]),
+                     "gradients_roofline": grad_rate(st["gradients"]),
                      "bwd_states_roofline": rate(fl["state"], st["bwd_states"]),
                      "paper_linear_state_m1_train_step_h100_ms": PAPER_TRAIN_STEP_H100.get(T)})
         del fws, bws, out, grads, q, k, v, dout

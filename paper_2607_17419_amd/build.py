@@ -18,7 +18,11 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libkata.so")
-SOURCES = ["kata_api.hip", "kata_fp32.hip", "kata_mfma.hip", "kata_linear.hip", "kata_bwd.hip"]
+SOURCES = ["kata_api.hip", "kata_fp32.hip", "kata_mfma.hip", "kata_linear.hip", "kata_bwd.hip",
+           "kata_bwd_bf.hip"]
+# per-source flags: the bf16 gradients kernel updates MFMA results with VALU code,
+# so its MFMAs write VGPRs (no AGPR copies)
+EXTRA = {"kata_bwd_bf.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 ARCH = "gfx950"
@@ -32,7 +36,7 @@ CFLAGS = [
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                     if "is not a recognized feature for this target" not in l)

@@ -21,6 +21,8 @@
 // Feature layout and records as on the fp32 forward path: packed pairs (x, y),
 // x <= y, of each block of m = d/g coordinates; a record is S[f][j] (n x dv)
 // then z[f] (n), fp32.
+#include <type_traits>
+
 #include "kata_common.hpp"
 #include "kata_internal.hpp"
 #include "kata_scan.hpp"
@@ -130,10 +132,16 @@ __global__ __launch_bounds__(256) void bwd_chunk_state(const Tx* __restrict__ x,
 }
 
 // ---------------------------------------------------------------------------
-// Per-token coefficients: D_t = psi_w(q_t) . z_pre + sum_{s <= t in chunk} w_ts,
-// ab[t] = (dout_t / D_t, -<dout_t, o_t> / D_t), zeros when D_t = 0.
-// grid (NC, BH), block 256, dynamic LDS (2 C d + C) floats + n uint16.
+// Per-token coefficients: D_t = q_t^T Z_pre q_t + sum_{s <= t in chunk} w_ts,
+// with Z_pre the prefix z unpacked into a symmetric d x d matrix (zero across
+// feature blocks), then ab[t] = (dout_t / D_t, -<dout_t, o_t> / D_t), zeros
+// when D_t = 0.  Four lanes per token: lane part p takes the coordinates
+// 16 p .. 16 p + 15 of Z_pre q_t, the keys s = p, p + 4, ... and the values
+// j = p, p + 4, ...; shuffles join the parts.  The token's q row is held in
+// registers.  grid (NC, BH), block 256 (C <= 64), dynamic LDS bwd_coef_smem.
 // ---------------------------------------------------------------------------
+constexpr int kCS = 65;  // fp32 row stride of the coefficient kernel's tiles
+
 template <typename Tin>
 __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
                                                 const Tin* __restrict__ k,
@@ -143,54 +151,72 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
                                                 float* __restrict__ ab, int T, int d, int dv, int C,
                                                 int g, long long bh_stride, long long E) {
   extern __shared__ float bsm[];
-  const int n = bwd_n(d, g), m = d / g;
-  float* qs = bsm;            // [C][d]
-  float* ks = qs + C * d;     // [C][d]
-  float* Dn = ks + C * d;     // [C]
-  uint16_t* pairs = reinterpret_cast<uint16_t*>(Dn + C);
+  const int n = bwd_n(d, g), m = d / g, nm = m * (m + 1) / 2;
+  float* Z = bsm;             // [64][kCS] unpacked z_pre
+  float* qs = Z + 64 * kCS;   // [64][kCS]
+  float* ks = qs + 64 * kCS;  // [64][kCS]
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const long long t0 = static_cast<long long>(c) * C;
   const int nt = static_cast<int>(min(static_cast<long long>(C), T - t0));
-  const Tin* qh = q + static_cast<long long>(bh) * T * d;
-  const Tin* kh = k + static_cast<long long>(bh) * T * d;
-  bwd_pair_table(pairs, d, g);
-  for (int i = tid; i < C * d; i += 256) {
-    const int r = i / d, a = i % d;
-    qs[i] = (r < nt) ? load_f32(qh, (t0 + r) * d + a) : 0.f;
-    ks[i] = (r < nt) ? load_f32(kh, (t0 + r) * d + a) : 0.f;
-  }
-  __syncthreads();
+  const Tin* qh = q + (static_cast<long long>(bh) * T + t0) * d;
+  const Tin* kh = k + (static_cast<long long>(bh) * T + t0) * d;
   const float* zp = frec + bh * bh_stride + c * E + static_cast<long long>(n) * dv;
-  // four threads per token (consecutive lanes), partial sums joined by shuffles
-  for (int r0 = 0; r0 < C; r0 += 64) {
-    const int r = r0 + (tid >> 2), part = tid & 3;
-    float D = 0.f;
-    if (r < nt) {
-      for (int f = part; f < n; f += 4) {
-        const int a = pairs[f] & 0xFF, b = pairs[f] >> 8;
-        D += ((a == b) ? 1.f : 2.f) * qs[r * d + a] * qs[r * d + b] * zp[f];
-      }
-      for (int s = part; s <= r; s += 4)
-        for (int blk = 0; blk < g; ++blk) {
-          float sc = 0.f;
-          for (int x = blk * m; x < blk * m + m; ++x) sc += qs[r * d + x] * ks[s * d + x];
-          D += sc * sc;
-        }
-    }
-    D += __shfl_xor(D, 1);
-    D += __shfl_xor(D, 2);
-    if (r < nt && part == 0) Dn[r] = D;
+  for (int i = tid; i < 64 * 64; i += 256) {
+    const int x = i >> 6, y = i & 63;
+    float zv = 0.f;
+    if (x < d && y < d && x / m == y / m)
+      zv = zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
+    Z[x * kCS + y] = zv;
+    const bool in = x < nt && y < d;
+    qs[x * kCS + y] = in ? load_f32(qh, static_cast<long long>(x) * d + y) : 0.f;
+    ks[x * kCS + y] = in ? load_f32(kh, static_cast<long long>(x) * d + y) : 0.f;
   }
   __syncthreads();
-  for (int r = tid; r < nt; r += 256) {
+  const int r = tid >> 2, p = tid & 3;
+  float qr[64];
+#pragma unroll
+  for (int y = 0; y < 64; ++y) qr[y] = qs[r * kCS + y];
+  float D = 0.f;
+  // prefix: sum over this part's coordinates x of q_x (Z q)_x
+  for (int xi = 0; xi < 16; ++xi) {
+    const int x = 16 * p + xi;
+    const float* zr = Z + x * kCS;
+    float zq = 0.f;
+#pragma unroll
+    for (int y = 0; y < 64; ++y) zq += zr[y] * qr[y];
+    D += qs[r * kCS + x] * zq;
+  }
+  // in-chunk squared scores of the keys s <= r of this part
+  if (g == 1) {
+    for (int s = p; s <= r; s += 4) {
+      const float* kr = ks + s * kCS;
+      float sc = 0.f;
+#pragma unroll
+      for (int x = 0; x < 64; ++x) sc += qr[x] * kr[x];
+      D += sc * sc;
+    }
+  } else {
+    for (int s = p; s <= r; s += 4)
+      for (int blk = 0; blk < g; ++blk) {
+        float sc = 0.f;
+        for (int x = blk * m; x < blk * m + m; ++x) sc += qs[r * kCS + x] * ks[s * kCS + x];
+        D += sc * sc;
+      }
+  }
+  D += __shfl_xor(D, 1);
+  D += __shfl_xor(D, 2);
+  if (r < nt) {
     const long long row = static_cast<long long>(bh) * T + t0 + r;
-    const float D = Dn[r];
+    const float* dr = dout + row * dv;
+    const float* orow = o + row * dv;
     float go = 0.f;
-    for (int j = 0; j < dv; ++j) go += dout[row * dv + j] * o[row * dv + j];
+    for (int j = p; j < dv; j += 4) go += dr[j] * orow[j];
+    go += __shfl_xor(go, 1);
+    go += __shfl_xor(go, 2);
     float* abr = ab + row * (dv + 1);
     const float inv = D > 0.f ? 1.f / D : 0.f;
-    for (int j = 0; j < dv; ++j) abr[j] = dout[row * dv + j] * inv;
-    abr[dv] = -go * inv;
+    for (int j = p; j < dv; j += 4) abr[j] = dr[j] * inv;
+    if (p == 0) abr[dv] = -go * inv;
   }
 }
 
@@ -669,16 +695,15 @@ size_t bwd_grad_mf_smem(int d, int g, bool bf16_lds) {
 
 bool bwd_mf_ok(int d, int dv, int C) { return d <= 64 && dv <= 64 && C <= 64; }
 
+bool aligned(const void* p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+
 size_t bwd_grad_smem(int d, int C, int g) {
   const size_t n = static_cast<size_t>(bwd_n(d, g));
   return (4 * static_cast<size_t>(C) * d + 3 * static_cast<size_t>(C) * C +
           2 * static_cast<size_t>(C) * kYB) * sizeof(float) + n * sizeof(uint16_t);
 }
 
-size_t bwd_coef_smem(int d, int C, int g) {
-  const size_t n = static_cast<size_t>(bwd_n(d, g));
-  return (2 * static_cast<size_t>(C) * d + C) * sizeof(float) + n * sizeof(uint16_t);
-}
+size_t bwd_coef_smem(int, int, int) { return 3 * 64 * kCS * sizeof(float); }
 
 }  // namespace
 
@@ -750,7 +775,14 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
     scan_exclusive<float, BwdUnitWeight, true><<<gscan, 256, 0, st>>>(brec, brec, NC, E,
                                                                      bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 5, st)) != hipSuccess) return e;
-  if (mf) {
+  bool bf = false;
+  if constexpr (std::is_same<Tin, bf16_t>::value)
+    bf = bwd_bf_ok(d, dv, C, g) && aligned(q, 4) && aligned(k, 4) && aligned(v, 4) &&
+         aligned(ws, 16) && aligned(dq, 16) && aligned(dk, 16) && aligned(dv_out, 16);
+  if (bf) {
+    e = launch_bwd_grad_bf(q, k, v, ab, frec, brec, dq, dk, dv_out, BH, T, bh_stride, E, st);
+    if (e != hipSuccess) return e;
+  } else if (mf) {
     const size_t gshm = bwd_grad_mf_smem(d, g, sizeof(Tin) == 2);
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad_mf<Tin>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(gshm));

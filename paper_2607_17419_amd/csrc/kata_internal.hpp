@@ -65,8 +65,16 @@ hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* o
                            int feature, float eps, int normalize, int L, void* ws, hipStream_t st,
                            hipEvent_t* ev);
 
-// ---- backward, fp32 path (kata_bwd.hip) -------------------------------------
+// ---- backward (kata_bwd.hip; gradients of bf16 inputs in kata_bwd_bf.hip) ----
 bool bwd_supported(int d, int dv, int C, int g);
+// Shapes of the bf16 matrix-core gradients kernel: d = dv = C = 64, g = 1.
+bool bwd_bf_ok(int d, int dv, int C, int g);
+// Gradients of every chunk from the records, a_t | b_t rows (ab, row stride
+// 65) and bf16 q, k, v; q, k, v 4-byte and dq, dk, dv 16-byte aligned.
+hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const float* ab,
+                              const float* frec, const float* brec, float* dq, float* dk,
+                              float* dv_out, int BH, int T, long long bh_stride, long long E,
+                              hipStream_t st);
 size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g);
 // ev: null, or 7 events recorded before the first kernel and after each of the
 // six launches (forward states, prefix scan, coefficients, backward states,
