@@ -381,7 +381,6 @@ def bench_linear(kata, dev, hip, steps=10, warmup=3, probe=False):
 # Paper's linear-state training step (forward + backward) at B = 8, H = 16,
 # d = 64, bf16 on an H100 (training-step latency table), ms: context.
 PAPER_TRAIN_STEP_H100 = {1024: 10.14, 2048: 20.07, 4096: 39.93, 8192: 79.58}
-PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 
 
 def bwd_flop(BH, T, d, dv, C):
@@ -396,22 +395,36 @@ def bwd_flop(BH, T, d, dv, C):
             "grad": chunks * (4 * C * n * (dv + 1) + 2 * C * n * dv + C * C * (2 * dv + 3 * d))}
 
 
-def bwd_grad_bytes(BH, T, d, dv, C):
-    """Algorithmic HBM bytes of the gradients launch: per chunk the prefix and
-    suffix records (n dv + n fp32 each), the bf16 q, k, v rows, the fp32
-    a_t | b_t rows, and the fp32 dq, dk, dv rows written."""
+def bwd_record_bytes(d, dv):
+    """Bytes of one chunk record on the bf16 path (bf16 inputs, d = dv = C =
+    64): the state S as bf16 (n dv x 2), then z as fp32 (n x 4)."""
     n = d * (d + 1) // 2
+    return n * dv * 2 + n * 4
+
+
+def bwd_bytes(BH, T, d, dv, C):
+    """Algorithmic HBM bytes per launch of the bf16-path backward kernels:
+    chunk states write one record per chunk and read the chunk's x (bf16) and
+    y rows (v bf16, or a | b fp32); each scan reads and writes every record;
+    the gradients read two records, the bf16 q, k, v rows and the fp32 a | b
+    rows, and write the fp32 dq, dk, dv rows."""
     NC = -(-T // C)
-    per_chunk = 2 * (n * dv + n) * 4 + C * (2 * d + dv) * 2 + C * (dv + 1) * 4 + C * (2 * d + dv) * 4
-    return BH * NC * per_chunk
+    R = bwd_record_bytes(d, dv)
+    rows_qkv = C * (2 * d + dv) * 2
+    rows_ab = C * (dv + 1) * 4
+    return {"fwd_states": BH * NC * (R + C * d * 2 + C * dv * 2),
+            "bwd_states": BH * NC * (R + C * d * 2 + rows_ab),
+            "scan": BH * NC * 2 * R,
+            "gradients": BH * NC * (2 * R + rows_qkv + rows_ab + C * (2 * d + dv) * 4)}
 
 
 def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=2):
     """Training step of KATA-M1 (forward on the bf16 MFMA path, then the O(T)
     chunked backward) at the paper's training-table shape B = 8, H = 16,
     d = dv = 64, C = 64, bf16 inputs, fp32 gradients; per-stage HIP-event
-    times of the backward, the fp32 matrix rate of its state kernels and the
-    HBM rate (with the bf16 matrix rate beside it) of the gradients kernel."""
+    times of the backward, and the HBM rates of its state, scan and gradients
+    kernels against their algorithmic bytes (with the bf16 matrix rates of
+    the state and gradients kernels beside them)."""
     import torch
     import workloads
     B, H, d, dv, C = 8, 16, 64, 64, 64
@@ -466,26 +479,29 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
         bev.close()
         fl = bwd_flop(B * H, T, d, dv, C)
 
-        def rate(flop, t_ms):
-            tf = flop / (t_ms * 1e-3) / 1e12
-            return {"bound": "mfma_fp32", "achieved": round(tf, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)}
+        by = bwd_bytes(B * H, T, d, dv, C)
 
-        def grad_rate(t_ms):
-            # bf16 inputs at d = dv = C = 64 take the bf16 matrix-core gradients
-            # kernel, whose bound is the two records it streams per chunk
-            gbs = bwd_grad_bytes(B * H, T, d, dv, C) / (t_ms * 1e-3) / 1e9
-            tf = fl["grad"] / (t_ms * 1e-3) / 1e12
-            return {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(gbs / PEAK_HBM_GBS, 4),
-                    "mfma_bf16": {"achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
-                                  "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}}
+        def hbm_rate(nbytes, t_ms, flop=None):
+            # bf16 inputs at d = dv = C = 64 take the bf16 matrix-core states and
+            # gradients; their bound is the records they stream
+            gbs = nbytes / (t_ms * 1e-3) / 1e9
+            r = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                 "frac": round(gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": nbytes}
+            if flop is not None:
+                tf = flop / (t_ms * 1e-3) / 1e12
+                r["mfma_bf16"] = {"achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
+                                  "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+            return r
         rows.append({"T": T, "inputs": src, "train_step_ms": round(ms, 3),
                      "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
                      "tokens_per_s": B * T / (ms * 1e-3),
                      "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
-                     "gradients_roofline": grad_rate(st["gradients"]),
-                     "bwd_states_roofline": rate(fl["state"], st["bwd_states"]),
+                     "gradients_roofline": hbm_rate(by["gradients"], st["gradients"], fl["grad"]),
+                     "bwd_states_roofline": hbm_rate(by["bwd_states"], st["bwd_states"],
+                                                     fl["state"]),
+                     "fwd_states_roofline": hbm_rate(by["fwd_states"], st["fwd_states"],
+                                                     fl["state"]),
+                     "suffix_scan_roofline": hbm_rate(by["scan"], st["suffix_scan"]),
                      "paper_linear_state_m1_train_step_h100_ms": PAPER_TRAIN_STEP_H100.get(T)})
         del fws, bws, out, grads, q, k, v, dout
         torch.cuda.empty_cache()

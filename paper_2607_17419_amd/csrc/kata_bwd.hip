@@ -133,7 +133,8 @@ __global__ __launch_bounds__(256) void bwd_chunk_state(const Tx* __restrict__ x,
 
 // ---------------------------------------------------------------------------
 // Per-token coefficients: D_t = q_t^T Z_pre q_t + sum_{s <= t in chunk} w_ts,
-// with Z_pre the prefix z unpacked into a symmetric d x d matrix (zero across
+// with Z_pre the prefix z (fp32, chunk c at zsrc + bh z_bh + c z_c, diagonal
+// features scaled by zdiag) unpacked into a symmetric d x d matrix (zero across
 // feature blocks), then ab[t] = (dout_t / D_t, -<dout_t, o_t> / D_t), zeros
 // when D_t = 0.  Four lanes per token: lane part p takes the coordinates
 // 16 p .. 16 p + 15 of Z_pre q_t, the keys s = p, p + 4, ... and the values
@@ -147,11 +148,12 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
                                                 const Tin* __restrict__ k,
                                                 const float* __restrict__ o,
                                                 const float* __restrict__ dout,
-                                                const float* __restrict__ frec,
+                                                const float* __restrict__ zsrc,
                                                 float* __restrict__ ab, int T, int d, int dv, int C,
-                                                int g, long long bh_stride, long long E) {
+                                                int g, long long z_bh, long long z_c,
+                                                float zdiag) {
   extern __shared__ float bsm[];
-  const int n = bwd_n(d, g), m = d / g, nm = m * (m + 1) / 2;
+  const int m = d / g, nm = m * (m + 1) / 2;
   float* Z = bsm;             // [64][kCS] unpacked z_pre
   float* qs = Z + 64 * kCS;   // [64][kCS]
   float* ks = qs + 64 * kCS;  // [64][kCS]
@@ -160,12 +162,12 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   const int nt = static_cast<int>(min(static_cast<long long>(C), T - t0));
   const Tin* qh = q + (static_cast<long long>(bh) * T + t0) * d;
   const Tin* kh = k + (static_cast<long long>(bh) * T + t0) * d;
-  const float* zp = frec + bh * bh_stride + c * E + static_cast<long long>(n) * dv;
+  const float* zp = zsrc + bh * z_bh + c * z_c;
   for (int i = tid; i < 64 * 64; i += 256) {
     const int x = i >> 6, y = i & 63;
     float zv = 0.f;
     if (x < d && y < d && x / m == y / m)
-      zv = zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
+      zv = (x == y ? zdiag : 1.f) * zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
     Z[x * kCS + y] = zv;
     const bool in = x < nt && y < d;
     qs[x * kCS + y] = in ? load_f32(qh, static_cast<long long>(x) * d + y) : 0.f;
@@ -739,9 +741,17 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   const dim3 gscan(static_cast<unsigned>((E + kEB - 1) / kEB), BH);
   const bool mf = bwd_mf_ok(d, dv, C);
   const dim3 gsm(NC, BH);
+  // bf16 inputs at d = dv = C = 64, g = 1: chunk states and gradients on the
+  // bf16 matrix cores
+  bool bf = false;
+  if constexpr (std::is_same<Tin, bf16_t>::value)
+    bf = bwd_bf_ok(d, dv, C, g) && aligned(q, 4) && aligned(k, 4) && aligned(v, 4) &&
+         aligned(ws, 16) && aligned(dq, 16) && aligned(dk, 16) && aligned(dv_out, 16);
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  if (mf)
+  if (bf) {
+    if ((e = launch_bwd_state_bf(false, k, v, frec, BH, T, st)) != hipSuccess) return e;
+  } else if (mf)
     bwd_state_mf<Tin, Tin, false><<<gsm, 256, 0, st>>>(ki, vi, dv, frec, T, d, dv, C, g,
                                                       bh_stride, E);
   else
@@ -750,7 +760,9 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   const bool v4 = E % 4 == 0;
   const dim3 gscan4(static_cast<unsigned>((E + kEB4 - 1) / kEB4), BH);
-  if (v4)
+  if (bf) {
+    if ((e = launch_bwd_scan_bf(false, frec, BH, T, st)) != hipSuccess) return e;
+  } else if (v4)
     scan_exclusive_f32x4<BwdUnitWeight, false><<<gscan4, 256, 0, st>>>(frec, NC, E, bh_stride,
                                                                       BwdUnitWeight{});
   else
@@ -758,29 +770,36 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
                                                                       bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   const size_t cshm = bwd_coef_smem(d, C, g);
-  bwd_coef<Tin><<<dim3(NC, BH), 256, cshm, st>>>(qi, ki, out, dout, frec, ab, T, d, dv, C, g,
-                                                 bh_stride, E);
+  // z_pre: fp32 after S in both record layouts; the bf16-state records carry
+  // the diagonal features halved
+  const long long rq = static_cast<long long>(bwd_bf_record_bytes() / sizeof(float));
+  const float* zsrc = bf ? reinterpret_cast<const float*>(reinterpret_cast<const char*>(frec) +
+                                                          bwd_bf_record_bytes() - 4 * n)
+                         : frec + static_cast<long long>(n) * dv;
+  bwd_coef<Tin><<<dim3(NC, BH), 256, cshm, st>>>(qi, ki, out, dout, zsrc, ab, T, d, dv, C, g,
+                                                 bf ? NC * rq : bh_stride, bf ? rq : E,
+                                                 bf ? 2.f : 1.f);
   if ((e = record(ev, 3, st)) != hipSuccess) return e;
-  if (mf)
+  if (bf) {
+    if ((e = launch_bwd_state_bf(true, q, ab, brec, BH, T, st)) != hipSuccess) return e;
+  } else if (mf)
     bwd_state_mf<Tin, float, true><<<gsm, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
                                                        bh_stride, E);
   else
     bwd_chunk_state<Tin, float, true><<<gs, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
                                                          bh_stride, E);
   if ((e = record(ev, 4, st)) != hipSuccess) return e;
-  if (v4)
+  if (bf) {
+    if ((e = launch_bwd_scan_bf(true, brec, BH, T, st)) != hipSuccess) return e;
+  } else if (v4)
     scan_exclusive_f32x4<BwdUnitWeight, true><<<gscan4, 256, 0, st>>>(brec, NC, E, bh_stride,
                                                                      BwdUnitWeight{});
   else
     scan_exclusive<float, BwdUnitWeight, true><<<gscan, 256, 0, st>>>(brec, brec, NC, E,
                                                                      bh_stride, BwdUnitWeight{});
   if ((e = record(ev, 5, st)) != hipSuccess) return e;
-  bool bf = false;
-  if constexpr (std::is_same<Tin, bf16_t>::value)
-    bf = bwd_bf_ok(d, dv, C, g) && aligned(q, 4) && aligned(k, 4) && aligned(v, 4) &&
-         aligned(ws, 16) && aligned(dq, 16) && aligned(dk, 16) && aligned(dv_out, 16);
   if (bf) {
-    e = launch_bwd_grad_bf(q, k, v, ab, frec, brec, dq, dk, dv_out, BH, T, bh_stride, E, st);
+    e = launch_bwd_grad_bf(q, k, v, ab, frec, brec, dq, dk, dv_out, BH, T, st);
     if (e != hipSuccess) return e;
   } else if (mf) {
     const size_t gshm = bwd_grad_mf_smem(d, g, sizeof(Tin) == 2);

@@ -16,8 +16,8 @@ namespace {
 // ---------------------------------------------------------------------------
 // Gradients of chunk c on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16,
 // fp32 accumulation): bf16 inputs, d = dv = C = 64, one feature block.  The
-// operands that are not bf16 already (the prefix and suffix records, the
-// in-chunk score products) are rounded to bf16 once, when staged in LDS.  The
+// prefix and suffix records come from the scans with S in bf16 (z in fp32)
+// and the in-chunk score products are rounded to bf16 once in LDS.  The
 // coefficients a_t, b_t enter as a bf16 pair hi + lo (lo = the rounding residue
 // of hi) wherever they multiply a state or a value: <a_t, v_s> + b_t and
 // S a_t + b_t z cancel to small values when the attention of row t is peaked
@@ -30,8 +30,8 @@ namespace {
 //   dq^T += K^T Pm^T,  dk^T += Q^T Pm,  dv^T += A^T W.
 // Inter-chunk terms slab by slab: slab y holds the packed record rows
 // {y, x}, x >= y, which are the consecutive rows packed(y, y) .. packed(y, 63)
-// (the row-major upper triangle), with z (dz) as a 65th column and the
-// diagonal row halved.  For the query side, with G_t[{y,x}] =
+// (the row-major upper triangle), with z (dz) as a 65th column; the diagonal
+// row arrives halved from the scan.  For the query side, with G_t[{y,x}] =
 // S[{y,x}] . a_t + b_t z[{y,x}],
 //   P^T[x][t] = sum_j S_slab[x][j] a_t[j] + z_slab[x] b_t          (MFMA, K = 80)
 //   dq^T[x][t] += 2 q_t[y] P^T[x][t]                 (pair {x,y}, coordinate x)
@@ -39,9 +39,9 @@ namespace {
 // which together count every off-diagonal pair from both sides and the
 // diagonal pair once (the halving).  The key side is the same with the suffix
 // record, v_i and a unit coefficient for dz.  The value gradient takes the
-// slab transposed, DT[j][x] = 2 dS_slab[x][j] (weights 1 on the diagonal, 2
-// off it, 0 below):
-//   dv^T[j][i] += k_i[y] sum_x DT[j][x] k_i[x].
+// slab transposed, DT[j][x] = dS_slab[x][j] (1/2 on the diagonal, 1 off it, 0
+// below), so that with the pair weights (1 on the diagonal, 2 off it)
+//   dv^T[j][i] += 2 k_i[y] sum_x DT[j][x] k_i[x].
 // Waves: 0-1 own dq of token tile w, 2-3 dk of key tile w - 2, and every wave
 // one 32 x 32 tile (value tile w >> 1, key tile w & 1) of dv.  The record rows
 // of the next slab are fetched into registers (buffer loads) while the current
@@ -64,6 +64,13 @@ constexpr int kBfOffR = kBfOffSlab + 2 * kBfSlab;
 constexpr int kBfLds = kBfOffR + 2 * 64 * kBR * 4;
 constexpr int kBfN = 2080;      // packed features of d = 64
 constexpr int kBfWord3 = 0x00020000;  // buffer resource word 3 (raw dword access)
+// Chunk records of this path: S as bf16 rows of 64 (128 bytes), then z as fp32;
+// the scans write the diagonal features f = (a, a) halved (weight 1/2).
+constexpr int kRecSB = kBfN * 64 * 2;    // bytes of the S part
+constexpr int kRecB = kRecSB + kBfN * 4;  // bytes of a record
+constexpr int kRecS16 = kRecSB / 16;      // 16-byte chunks of the S part
+constexpr int kRec16 = kRecB / 16;        // 16-byte chunks of a record
+static_assert(kRecB % 16 == 0, "records are 16-byte aligned");
 static_assert(6 * kBT * 2 <= 2 * kBfSlab, "in-chunk tiles fit the slab buffers");
 
 __device__ __forceinline__ f32x16 mfma_bf(const bf16x8& a, const bf16x8& b, const f32x16& c) {
@@ -87,9 +94,10 @@ __device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {
 }
 
 // One slab's record values in registers: rows 8 rg .. 8 rg + 7 of the slab
-// tile, columns 2 cp, 2 cp + 1 of S and dS, and the z / dz of row tid % 64.
+// tile, columns 2 cp, 2 cp + 1 of S and dS (bf16 pairs), and the z / dz of
+// row tid % 64.
 struct BfSlabRegs {
-  float2 a[8], b[8];
+  uint32_t a[8], b[8];
   float za, zb;
 };
 
@@ -97,12 +105,12 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
                                                       const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v,
                                                       const float* __restrict__ ab,
-                                                      const float* __restrict__ frec,
-                                                      const float* __restrict__ brec,
+                                                      const unsigned char* __restrict__ frec,
+                                                      const unsigned char* __restrict__ brec,
                                                       float* __restrict__ dq,
                                                       float* __restrict__ dk,
                                                       float* __restrict__ dvo, int T,
-                                                      long long bh_stride, long long E) {
+                                                      long long rec_bh) {
   extern __shared__ __align__(16) unsigned char gsm[];
   uint16_t* Qs = reinterpret_cast<uint16_t*>(gsm);
   uint16_t* Ks = reinterpret_cast<uint16_t*>(gsm + kBfOffK);
@@ -126,60 +134,52 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
   const long long t0 = static_cast<long long>(c) * 64;
   const int nt = static_cast<int>(min(64LL, static_cast<long long>(T) - t0));
   const long long hb = static_cast<long long>(bh) * T;
-  const float* Sp = frec + bh * bh_stride + c * E;
-  const float* Bs = brec + bh * bh_stride + c * E;
+  const unsigned char* Sp = frec + bh * rec_bh + static_cast<long long>(c) * kRecB;
+  const unsigned char* Bs = brec + bh * rec_bh + static_cast<long long>(c) * kRecB;
   const int rg = tid >> 5, cp = tid & 31;  // staging: rows 8 rg + r, columns 2 cp, 2 cp + 1
 
   // record rows through buffer loads: the chunk's record as the resource, the
   // slab's first row as the scalar offset, row and column as the vector offset
   const __amdgpu_buffer_rsrc_t rS =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(Sp), 0, static_cast<int>(E * 4), kBfWord3);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(Sp), 0, kRecB, kBfWord3);
   const __amdgpu_buffer_rsrc_t rB =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(Bs), 0, static_cast<int>(E * 4), kBfWord3);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(Bs), 0, kRecB, kBfWord3);
   auto fetch = [&](BfSlabRegs& p, int y) {
     const int f0 = y * 64 - (y * (y - 1)) / 2;  // packed(y, y)
-    const int so = f0 * 256;
+    const int so = f0 * 128;
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const int vo = max(8 * rg + r - y, 0) * 256 + 8 * cp;  // rows below y: row f0, staged 0
-      p.a[r] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rS, vo, so, 0));
-      p.b[r] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rB, vo, so, 0));
+      const int vo = max(8 * rg + r - y, 0) * 128 + 4 * cp;  // rows below y: row f0, staged 0
+      p.a[r] = __builtin_amdgcn_raw_buffer_load_b32(rS, vo, so, 0);
+      p.b[r] = __builtin_amdgcn_raw_buffer_load_b32(rB, vo, so, 0);
     }
     const int zo = max((tid & 63) - y, 0) * 4;
-    p.za = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rS, zo, kBfN * 256 + f0 * 4, 0));
-    p.zb = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rB, zo, kBfN * 256 + f0 * 4, 0));
+    p.za = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rS, zo, kRecSB + f0 * 4, 0));
+    p.zb = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rB, zo, kRecSB + f0 * 4, 0));
   };
   auto stage = [&](const BfSlabRegs& p, int y, uint16_t* buf) {
     uint16_t* Ss = buf;
     uint16_t* Ds = buf + kBTW;
     uint16_t* DT = Ds + kBTW;
-    float m[8];
+    // rows below y are zero; the diagonal row arrives halved from the scan
+    uint32_t sa[8], sb[8];
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       const int x = 8 * rg + r;
-      m[r] = x < y ? 0.f : (x == y ? 0.5f : 1.f);
+      sa[r] = x < y ? 0u : p.a[r];
+      sb[r] = x < y ? 0u : p.b[r];
+      *reinterpret_cast<uint32_t*>(Ss + x * kBW + 2 * cp) = sa[r];
+      *reinterpret_cast<uint32_t*>(Ds + x * kBW + 2 * cp) = sb[r];
     }
-    uint32_t ta[4], tb[4];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int x = 8 * rg + r;
-      *reinterpret_cast<uint32_t*>(Ss + x * kBW + 2 * cp) =
-          pack_bf16x2(p.a[r].x * m[r], p.a[r].y * m[r]);
-      *reinterpret_cast<uint32_t*>(Ds + x * kBW + 2 * cp) =
-          pack_bf16x2(p.b[r].x * m[r], p.b[r].y * m[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float m0 = 2.f * m[2 * r], m1 = 2.f * m[2 * r + 1];
-      ta[r] = pack_bf16x2(p.b[2 * r].x * m0, p.b[2 * r + 1].x * m1);
-      tb[r] = pack_bf16x2(p.b[2 * r].y * m0, p.b[2 * r + 1].y * m1);
-    }
-    *reinterpret_cast<uint4*>(DT + (2 * cp) * kBP + 8 * rg) = make_uint4(ta[0], ta[1], ta[2], ta[3]);
+    *reinterpret_cast<uint4*>(DT + (2 * cp) * kBP + 8 * rg) =
+        make_uint4(lo_pair(sb[0], sb[1]), lo_pair(sb[2], sb[3]), lo_pair(sb[4], sb[5]),
+                   lo_pair(sb[6], sb[7]));
     *reinterpret_cast<uint4*>(DT + (2 * cp + 1) * kBP + 8 * rg) =
-        make_uint4(tb[0], tb[1], tb[2], tb[3]);
+        make_uint4(hi_pair(sb[0], sb[1]), hi_pair(sb[2], sb[3]), hi_pair(sb[4], sb[5]),
+                   hi_pair(sb[6], sb[7]));
     if (w == 0) {  // z column and the zero columns 65..79 of row tid
       const int x = tid;
-      const float mz = x < y ? 0.f : (x == y ? 0.5f : 1.f);
+      const float mz = x < y ? 0.f : 1.f;
       const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
       *reinterpret_cast<uint4*>(Ss + x * kBW + 64) = make_uint4(pack_bf16x2(p.za * mz, 0.f), 0u, 0u, 0u);
       *reinterpret_cast<uint4*>(Ss + x * kBW + 72) = zero;
@@ -369,7 +369,7 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
     }
     R += __shfl_xor(R, 32);
     if (h == 0) Rout[y] = 2.f * R;
-    const float ky = bf_f32(krow[y]);
+    const float ky = 2.f * bf_f32(krow[y]);  // DT holds dS with the diagonal halved
 #pragma unroll
     for (int i = 0; i < 16; ++i) dvacc[i] += ky * Qy[i];
   };
@@ -420,21 +420,308 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
   }
 }
 
+// ---------------------------------------------------------------------------
+// Chunk states on the bf16 matrix cores, d = dv = C = 64: for the packed
+// pairs f = (a, b), a <= b (row-major upper triangle),
+//   S[f][j] = sum_t x_ta x_tb y_tj,   z[f] = sum_t wt_t x_ta x_tb,
+// written as one record per chunk: S rounded to bf16 (rows of 64, through a
+// per-wave LDS tile so that a wave stores 32 whole rows), then z in fp32.  Forward states (kBwd =
+// false): x = k, y = v, wt = 1.  Backward states (kBwd): x = q, y = a_t and
+// wt = b_t from the coefficient rows; a_t enters as a bf16 pair hi + lo like
+// in the gradients.  The feature products are exact in fp32 and rounded to
+// bf16 once as the MFMA operand; z sums the fp32 products.  x and y are
+// staged transposed ([dim][token], bf16), so a lane reads the eight tokens of
+// its K slice with one 16-byte load.  Wave w takes the 32-feature tiles
+// w, w + 4, ...  grid (NC, BH), block 256.
+// ---------------------------------------------------------------------------
+template <bool kBwd>
+__global__ __launch_bounds__(256) void bwd_state_bf(const uint16_t* __restrict__ x,
+                                                    const void* __restrict__ yv,
+                                                    unsigned char* __restrict__ rec, int T,
+                                                    long long rec_bh) {
+  __shared__ __align__(16) uint16_t ot[4 * 32 * kBP];  // per-wave output rows
+  __shared__ __align__(16) uint16_t xT[64 * kBP];
+  __shared__ __align__(16) uint16_t yT[64 * kBP];
+  __shared__ __align__(16) uint16_t yL[kBwd ? 64 * kBP : 8];
+  __shared__ __align__(16) float wt[64];
+  __shared__ uint16_t pairs[kBfN];
+  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  const long long t0 = static_cast<long long>(c) * 64;
+  const int nt = static_cast<int>(min(64LL, static_cast<long long>(T) - t0));
+  const long long hb = static_cast<long long>(bh) * T;
+  for (int a = tid; a < 64; a += 256)
+    for (int b = a; b < 64; ++b)
+      pairs[a * 64 - a * (a - 1) / 2 + (b - a)] = static_cast<uint16_t>(a | (b << 8));
+  {
+    const int rg = tid >> 5, cp = tid & 31;  // rows 8 rg + r, columns 2 cp, 2 cp + 1
+    const uint16_t* xh = x + (hb + t0) * 64;
+    uint32_t xv[8], yh[8], yl[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int t = 8 * rg + r, tc = min(t, nt - 1);
+      const bool in = t < nt;
+      const uint32_t x2 = *reinterpret_cast<const uint32_t*>(xh + tc * 64 + 2 * cp);
+      xv[r] = in ? x2 : 0u;
+      if constexpr (kBwd) {
+        const float* ar = static_cast<const float*>(yv) + (hb + t0 + tc) * 65;
+        const float a0 = ar[2 * cp], a1 = ar[2 * cp + 1];
+        const uint32_t hi = pack_bf16x2(a0, a1);
+        yh[r] = in ? hi : 0u;
+        yl[r] = in ? pack_bf16x2(a0 - bf16lo_f32(hi), a1 - bf16hi_f32(hi)) : 0u;
+      } else {
+        const uint16_t* vh = static_cast<const uint16_t*>(yv) + (hb + t0) * 64;
+        const uint32_t v2 = *reinterpret_cast<const uint32_t*>(vh + tc * 64 + 2 * cp);
+        yh[r] = in ? v2 : 0u;
+        yl[r] = 0u;
+      }
+    }
+    auto put_t = [&](uint16_t* dst, const uint32_t* s2) {
+      *reinterpret_cast<uint4*>(dst + (2 * cp) * kBP + 8 * rg) =
+          make_uint4(lo_pair(s2[0], s2[1]), lo_pair(s2[2], s2[3]), lo_pair(s2[4], s2[5]),
+                     lo_pair(s2[6], s2[7]));
+      *reinterpret_cast<uint4*>(dst + (2 * cp + 1) * kBP + 8 * rg) =
+          make_uint4(hi_pair(s2[0], s2[1]), hi_pair(s2[2], s2[3]), hi_pair(s2[4], s2[5]),
+                     hi_pair(s2[6], s2[7]));
+    };
+    put_t(xT, xv);
+    put_t(yT, yh);
+    if constexpr (kBwd) put_t(yL, yl);
+    if (tid < 64) {
+      float b = 1.f;
+      if constexpr (kBwd)
+        b = tid < nt ? static_cast<const float*>(yv)[(hb + t0 + tid) * 65 + 64] : 0.f;
+      wt[tid] = b;
+    }
+  }
+  __syncthreads();
+  unsigned char* r0 = rec + bh * rec_bh + static_cast<long long>(c) * kRecB;
+  uint16_t* ow = ot + w * 32 * kBP;
+  for (int ft = w; ft < kBfN / 32; ft += 4) {
+    const int f = 32 * ft + l32;
+    const int pa = pairs[f] & 0xFF, pb = pairs[f] >> 8;
+    f32x16 acc0 = {}, acc1 = {};
+    float zp = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int tk = 16 * ks + 8 * h;
+      const uint4 xa = *reinterpret_cast<const uint4*>(xT + pa * kBP + tk);
+      const uint4 xb = *reinterpret_cast<const uint4*>(xT + pb * kBP + tk);
+      const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w}, wb[4] = {xb.x, xb.y, xb.z, xb.w};
+      uint32_t pk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = bf16lo_f32(wa[e]) * bf16lo_f32(wb[e]);
+        const float p1 = bf16hi_f32(wa[e]) * bf16hi_f32(wb[e]);
+        pk[e] = pack_bf16x2(p0, p1);
+        if constexpr (kBwd)  // padded tokens have x = 0 and wt = 0
+          zp += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;
+        else
+          zp += p0 + p1;
+      }
+      const bf16x8 A = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      acc0 = mfma_bf(A, ld8(yT + l32 * kBP + tk), acc0);
+      acc1 = mfma_bf(A, ld8(yT + (32 + l32) * kBP + tk), acc1);
+      if constexpr (kBwd) {
+        acc0 = mfma_bf(A, ld8(yL + l32 * kBP + tk), acc0);
+        acc1 = mfma_bf(A, ld8(yL + (32 + l32) * kBP + tk), acc1);
+      }
+    }
+    zp += __shfl_xor(zp, 32);
+    // the tile's 32 rows as bf16 into this wave's LDS rows, then 16-byte
+    // pieces of whole rows to HBM (a wave's LDS accesses complete in order)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 8 * (i >> 2) + 4 * h + (i & 3);
+      ow[r * kBP + l32] = bf_bits(acc0[i]);
+      ow[r * kBP + 32 + l32] = bf_bits(acc1[i]);
+    }
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int ch = lane + 64 * q4, r = ch >> 3, part = ch & 7;
+      *reinterpret_cast<uint4*>(r0 + static_cast<long long>(32 * ft + r) * 128 + 16 * part) =
+          *reinterpret_cast<const uint4*>(ow + r * kBP + 8 * part);
+    }
+    if (h == 0) reinterpret_cast<float*>(r0 + kRecSB)[f] = zp;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive prefix (or, kReverse, suffix) over the chunk records of this path,
+// in place: record c receives w(e) x the sum over the records before (after)
+// it, summed in fp32; S elements are read and written as bf16, z as fp32, and
+// w = 1/2 on the diagonal features (a, a), 1 elsewhere.  A thread takes one
+// 16-byte piece of the record (8 bf16 of S or 4 fp32 of z) in kSR consecutive
+// records of a 64-record block: an up- and down-sweep in registers, then the
+// kSG row groups of the workgroup join their block sums through LDS.  The S / z
+// boundary falls on a workgroup boundary (kRecS16 is a multiple of kSC).
+// grid (ceil(kRec16 / kSC), BH), block 256.
+// ---------------------------------------------------------------------------
+constexpr int kSC = 32;  // 16-byte pieces per workgroup
+constexpr int kSG = 8;   // row groups
+constexpr int kSR = 8;   // records per thread and block
+static_assert(kRecS16 % kSC == 0, "a workgroup reads one element type");
+
+// Whether packed index f (0 <= f < 2080) is a diagonal pair: f = D(a) =
+// 64 a - a (a - 1) / 2 for the row a with D(a) <= f < D(a + 1), which solves
+// a^2 - 129 a + 2 f = 0 (the square root estimate is corrected by one either
+// way, then checked exactly).
+__device__ __forceinline__ bool diag_feature(int f) {
+  auto D = [](int a) { return 64 * a - a * (a - 1) / 2; };
+  int a = static_cast<int>((129.f - sqrtf(16641.f - 8.f * static_cast<float>(f))) * 0.5f);
+  a = max(0, min(63, a));
+  if (a < 63 && D(a + 1) <= f) ++a;
+  if (a > 0 && D(a) > f) --a;
+  return D(a) == f;
+}
+
+template <bool kReverse>
+__global__ __launch_bounds__(256) void scan_bf(unsigned char* __restrict__ rec, int N,
+                                               long long rec_bh) {
+  __shared__ float4 tot[kSG][kSC][2];
+  const int tid = threadIdx.x, cg = tid % kSC, rg = tid / kSC;
+  const int pc = blockIdx.x * kSC + cg;
+  const bool active = pc < kRec16;
+  const bool isS = blockIdx.x * kSC < kRecS16;  // uniform over the workgroup
+  unsigned char* rb = rec + blockIdx.y * rec_bh + 16LL * pc;
+  float w[8], carry[8];
+  if (isS) {
+    const float wv = diag_feature(pc >> 3) ? 0.5f : 1.f;  // 8 pieces per 64-wide row
+#pragma unroll
+    for (int x = 0; x < 8; ++x) w[x] = wv;
+  } else {
+    const int zf = 4 * (pc - kRecS16);
+#pragma unroll
+    for (int x = 0; x < 8; ++x) w[x] = (x < 4 && diag_feature(zf + x)) ? 0.5f : 1.f;
+  }
+#pragma unroll
+  for (int x = 0; x < 8; ++x) carry[x] = 0.f;
+  for (int r0 = 0; r0 < N; r0 += kSG * kSR) {
+    const int rbase = r0 + rg * kSR;
+    float v[kSR][8];
+#pragma unroll
+    for (int j = 0; j < kSR; ++j) {
+      const int rr = rbase + j;
+      uint4 u = make_uint4(0u, 0u, 0u, 0u);
+      if (active && rr < N)
+        u = *reinterpret_cast<const uint4*>(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) *
+                                                     kRecB);
+      const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (isS) {
+          v[j][2 * e] = bf16lo_f32(uw[e]);
+          v[j][2 * e + 1] = bf16hi_f32(uw[e]);
+        } else {
+          v[j][e] = __uint_as_float(uw[e]);
+          v[j][4 + e] = 0.f;
+        }
+      }
+    }
+#pragma unroll
+    for (int d = 1; d < kSR; d <<= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kSR; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v[j][x] += v[j - d][x];
+    float gsum[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      gsum[x] = v[kSR - 1][x];
+      v[kSR - 1][x] = 0.f;
+    }
+#pragma unroll
+    for (int d = kSR / 2; d >= 1; d >>= 1)
+#pragma unroll
+      for (int j = 2 * d - 1; j < kSR; j += 2 * d)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          const float left = v[j - d][x];
+          v[j - d][x] = v[j][x];
+          v[j][x] += left;
+        }
+    tot[rg][cg][0] = make_float4(gsum[0], gsum[1], gsum[2], gsum[3]);
+    tot[rg][cg][1] = make_float4(gsum[4], gsum[5], gsum[6], gsum[7]);
+    __syncthreads();
+    float pre[8], blk[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      pre[x] = carry[x];
+      blk[x] = 0.f;
+    }
+#pragma unroll
+    for (int g2 = 0; g2 < kSG; ++g2) {
+      const float4 t0 = tot[g2][cg][0], t1 = tot[g2][cg][1];
+      const float tv[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        if (g2 < rg) pre[x] += tv[x];
+        blk[x] += tv[x];
+      }
+    }
+    __syncthreads();  // tot is rewritten by the next block
+#pragma unroll
+    for (int j = 0; j < kSR; ++j) {
+      const int rr = rbase + j;
+      if (!(active && rr < N)) continue;
+      float o[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) o[x] = w[x] * (pre[x] + v[j][x]);
+      const uint4 u = isS ? make_uint4(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                       pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7]))
+                          : make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]),
+                                       __float_as_uint(o[2]), __float_as_uint(o[3]));
+      *reinterpret_cast<uint4*>(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) * kRecB) = u;
+    }
+#pragma unroll
+    for (int x = 0; x < 8; ++x) carry[x] += blk[x];
+  }
+}
+
 }  // namespace
 
 bool bwd_bf_ok(int d, int dv, int C, int g) { return d == 64 && dv == 64 && C == 64 && g == 1; }
 
-hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const float* ab,
-                              const float* frec, const float* brec, float* dq, float* dk,
-                              float* dv_out, int BH, int T, long long bh_stride, long long E,
-                              hipStream_t st) {
+size_t bwd_bf_record_bytes() { return kRecB; }
+
+hipError_t launch_bwd_state_bf(bool backward, const void* x, const void* y, void* rec, int BH,
+                               int T, hipStream_t st) {
   const int NC = (T + 63) / 64;
+  const long long rec_bh = static_cast<long long>(NC) * kRecB;
+  unsigned char* r = static_cast<unsigned char*>(rec);
+  if (backward)
+    bwd_state_bf<true><<<dim3(NC, BH), 256, 0, st>>>(static_cast<const uint16_t*>(x), y, r, T,
+                                                     rec_bh);
+  else
+    bwd_state_bf<false><<<dim3(NC, BH), 256, 0, st>>>(static_cast<const uint16_t*>(x), y, r, T,
+                                                      rec_bh);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_t st) {
+  const int NC = (T + 63) / 64;
+  const long long rec_bh = static_cast<long long>(NC) * kRecB;
+  const dim3 grid((kRec16 + kSC - 1) / kSC, BH);
+  unsigned char* r = static_cast<unsigned char*>(rec);
+  if (reverse)
+    scan_bf<true><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+  else
+    scan_bf<false><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const float* ab,
+                              const void* frec, const void* brec, float* dq, float* dk,
+                              float* dv_out, int BH, int T, hipStream_t st) {
+  const int NC = (T + 63) / 64;
+  const long long rec_bh = static_cast<long long>(NC) * kRecB;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad_bf),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, kBfLds);
   if (e != hipSuccess) return e;
   bwd_grad_bf<<<dim3(NC, BH), 256, kBfLds, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-      static_cast<const uint16_t*>(v), ab, frec, brec, dq, dk, dv_out, T, bh_stride, E);
+      static_cast<const uint16_t*>(v), ab, static_cast<const unsigned char*>(frec),
+      static_cast<const unsigned char*>(brec), dq, dk, dv_out, T, rec_bh);
   return hipGetLastError();
 }
 

@@ -69,12 +69,22 @@ hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* o
 bool bwd_supported(int d, int dv, int C, int g);
 // Shapes of the bf16 matrix-core gradients kernel: d = dv = C = 64, g = 1.
 bool bwd_bf_ok(int d, int dv, int C, int g);
-// Gradients of every chunk from the records, a_t | b_t rows (ab, row stride
-// 65) and bf16 q, k, v; q, k, v 4-byte and dq, dk, dv 16-byte aligned.
+// Records of that path, per chunk and head: S as bf16 rows of 64, then z as
+// fp32 (bwd_bf_record_bytes() bytes, chunk-major within a head).
+size_t bwd_bf_record_bytes();
+// Chunk records of every chunk on the bf16 matrix cores for bf16 x: forward
+// states (x = k, y = v bf16) or backward states (x = q, y = the a_t | b_t
+// rows, fp32, row stride 65).
+hipError_t launch_bwd_state_bf(bool backward, const void* x, const void* y, void* rec, int BH,
+                               int T, hipStream_t st);
+// Exclusive prefix (reverse: suffix) of those records in place, diagonal
+// features weighted 1/2.
+hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_t st);
+// Gradients of every chunk from the scanned records, a_t | b_t rows (ab, row
+// stride 65) and bf16 q, k, v; q, k, v 4-byte and dq, dk, dv 16-byte aligned.
 hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const float* ab,
-                              const float* frec, const float* brec, float* dq, float* dk,
-                              float* dv_out, int BH, int T, long long bh_stride, long long E,
-                              hipStream_t st);
+                              const void* frec, const void* brec, float* dq, float* dk,
+                              float* dv_out, int BH, int T, hipStream_t st);
 size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g);
 // ev: null, or 7 events recorded before the first kernel and after each of the
 // six launches (forward states, prefix scan, coefficients, backward states,
