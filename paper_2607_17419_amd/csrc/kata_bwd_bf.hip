@@ -42,12 +42,14 @@ namespace {
 // slab transposed, DT[j][x] = dS_slab[x][j] (1/2 on the diagonal, 1 off it, 0
 // below), so that with the pair weights (1 on the diagonal, 2 off it)
 //   dv^T[j][i] += 2 k_i[y] sum_x DT[j][x] k_i[x].
-// Waves: 0-1 own dq of token tile w, 2-3 dk of key tile w - 2, and every wave
-// one 32 x 32 tile (value tile w >> 1, key tile w & 1) of dv.  The record rows
-// of the next slab are fetched into registers (buffer loads) while the current
-// one is used, and the slabs are double-buffered in LDS, so one barrier per
-// slab orders staging and use.  grid (NC, BH), block 256, dynamic LDS kBfLds
-// bytes (one workgroup per CU).
+// Two groups of four waves; group g takes the slabs y = g, g + 2, ... in its own
+// LDS slab buffer, so each SIMD runs two waves (one per group).  In a group,
+// waves 0-1 own dq of token tile w, 2-3 dk of key tile w - 2, and every wave
+// one 32 x 32 tile (value tile w >> 1, key tile w & 1) of dv.  Group 0 also
+// stages the chunk rows and takes the in-chunk terms; at the end group 1 adds
+// its accumulators through LDS.  The record rows of a group's next slab are
+// fetched into registers (buffer loads) while the current one is used.
+// grid (NC, BH), block 512, dynamic LDS kBfLds bytes (one workgroup per CU).
 // ---------------------------------------------------------------------------
 constexpr int kBP = 72;         // bf16 row stride of a 64 x 64 operand tile
 constexpr int kBW = 88;         // bf16 row stride of a tile with a 65th column (K = 80)
@@ -101,7 +103,7 @@ struct BfSlabRegs {
   float za, zb;
 };
 
-__global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict__ q,
                                                       const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v,
                                                       const float* __restrict__ ab,
@@ -128,7 +130,9 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
   uint16_t* PmT = Pm + kBT;
   uint16_t* WT = PmT + kBT;
 
-  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  // two groups of four waves: group g takes the slabs y = g, g + 2, ...
+  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x & 255;
+  const int grp = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 8);
   const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, l32 = lane & 31;
   const long long t0 = static_cast<long long>(c) * 64;
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
   };
 
   // ---- chunk rows: q, k, v, a (bf16) row-major and q, k, a transposed ----------
-  {
+  if (grp == 0) {
     const uint16_t* qh = q + (hb + t0) * 64;
     const uint16_t* kh = k + (hb + t0) * 64;
     const uint16_t* vh = v + (hb + t0) * 64;
@@ -245,14 +249,14 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
       *reinterpret_cast<uint4*>(Al + tid * kBW + 72) = zero;
     }
   }
-  // the first two slabs' record rows are on their way during the in-chunk terms
+  // each group's first slab is on its way during the in-chunk terms
   BfSlabRegs pf0;
-  fetch(pf0, 0);
+  fetch(pf0, grp);
   __syncthreads();
 
   // ---- in-chunk scores: wave w takes the (key tile w >> 1, token tile w & 1)
-  // tile of Sc^T and Cw^T, then writes Pm, Pm^T and W^T ----------------------------
-  {
+  // tile of Sc^T and Cw^T, then writes Pm, Pm^T and W^T (group 0) ---------------
+  if (grp == 0) {
     const int S = w >> 1, Tt = w & 1;
     f32x16 sc = {}, cw = {};
 #pragma unroll
@@ -290,7 +294,7 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
   const int Tw = w & 1;  // token tile (dq waves) / key tile (dk waves) / key tile of dv
   const int J = w >> 1;  // value tile of dv
   f32x16 acc0 = {}, acc1 = {}, dvacc = {};
-  {
+  if (grp == 0) {
     const uint16_t* Xa = dqw ? KT : QT;
     const uint16_t* Xb = (dqw ? Pm : PmT) + (32 * Tw + l32) * kBP + 8 * h;
 #pragma unroll
@@ -374,20 +378,35 @@ __global__ __launch_bounds__(256, 1) void bwd_grad_bf(const uint16_t* __restrict
     for (int i = 0; i < 16; ++i) dvacc[i] += ky * Qy[i];
   };
 
-  uint16_t* buf0 = slab;
-  uint16_t* buf1 = slab + kBfSlab / 2;
-  stage(pf0, 0, buf0);
-  fetch(pf0, 1);
-  __syncthreads();
-  for (int y = 0; y < 64; y += 2) {
-    stage(pf0, y + 1, buf1);
+  uint16_t* mybuf = slab + grp * (kBfSlab / 2);
+  for (int i = 0; i < 32; ++i) {
+    const int y = 2 * i + grp;
+    stage(pf0, y, mybuf);
     fetch(pf0, min(y + 2, 63));
-    compute(y, buf0);
     __syncthreads();
-    stage(pf0, y + 2, buf0);
-    fetch(pf0, min(y + 3, 63));
-    compute(y + 1, buf1);
+    compute(y, mybuf);
     __syncthreads();
+  }
+  // group 1 hands its accumulators to group 0 through the (free) slab buffers
+  float* red = reinterpret_cast<float*>(slab) + (w * 64 + lane) * 48;
+  if (grp == 1) {
+#pragma unroll
+    for (int mq = 0; mq < 4; ++mq) {
+      *reinterpret_cast<float4*>(red + 4 * mq) =
+          make_float4(acc0[4 * mq], acc0[4 * mq + 1], acc0[4 * mq + 2], acc0[4 * mq + 3]);
+      *reinterpret_cast<float4*>(red + 16 + 4 * mq) =
+          make_float4(acc1[4 * mq], acc1[4 * mq + 1], acc1[4 * mq + 2], acc1[4 * mq + 3]);
+      *reinterpret_cast<float4*>(red + 32 + 4 * mq) =
+          make_float4(dvacc[4 * mq], dvacc[4 * mq + 1], dvacc[4 * mq + 2], dvacc[4 * mq + 3]);
+    }
+  }
+  __syncthreads();
+  if (grp == 1) return;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    acc0[i] += red[i];
+    acc1[i] += red[16 + i];
+    dvacc[i] += red[32 + i];
   }
 
   // ---- outputs: accumulators plus the slab row sums ----------------------------
@@ -718,7 +737,7 @@ hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd_grad_bf),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, kBfLds);
   if (e != hipSuccess) return e;
-  bwd_grad_bf<<<dim3(NC, BH), 256, kBfLds, st>>>(
+  bwd_grad_bf<<<dim3(NC, BH), 512, kBfLds, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
       static_cast<const uint16_t*>(v), ab, static_cast<const unsigned char*>(frec),
       static_cast<const unsigned char*>(brec), dq, dk, dv_out, T, rec_bh);
