@@ -571,14 +571,14 @@ __global__ __launch_bounds__(256) void bwd_state_bf(const uint16_t* __restrict__
 // it, summed in fp32; S elements are read and written as bf16, z as fp32, and
 // w = 1/2 on the diagonal features (a, a), 1 elsewhere.  A thread takes one
 // 16-byte piece of the record (8 bf16 of S or 4 fp32 of z) in kSR consecutive
-// records of a 64-record block: an up- and down-sweep in registers, then the
-// kSG row groups of the workgroup join their block sums through LDS.  The S / z
+// records of a kSG x kSR-record block: an up- and down-sweep in registers, then
+// the kSG row groups of the workgroup join their block sums through LDS (kSR
+// shrinks for short sequences so that every row group has records).  The S / z
 // boundary falls on a workgroup boundary (kRecS16 is a multiple of kSC).
 // grid (ceil(kRec16 / kSC), BH), block 256.
 // ---------------------------------------------------------------------------
 constexpr int kSC = 32;  // 16-byte pieces per workgroup
 constexpr int kSG = 8;   // row groups
-constexpr int kSR = 8;   // records per thread and block
 static_assert(kRecS16 % kSC == 0, "a workgroup reads one element type");
 
 // Whether packed index f (0 <= f < 2080) is a diagonal pair: f = D(a) =
@@ -594,7 +594,7 @@ __device__ __forceinline__ bool diag_feature(int f) {
   return D(a) == f;
 }
 
-template <bool kReverse>
+template <bool kReverse, int kSR>
 __global__ __launch_bounds__(256) void scan_bf(unsigned char* __restrict__ rec, int N,
                                                long long rec_bh) {
   __shared__ float4 tot[kSG][kSC][2];
@@ -722,10 +722,21 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
   const long long rec_bh = static_cast<long long>(NC) * kRecB;
   const dim3 grid((kRec16 + kSC - 1) / kSC, BH);
   unsigned char* r = static_cast<unsigned char*>(rec);
-  if (reverse)
-    scan_bf<true><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+  auto go = [&](auto rows) {
+    constexpr int R = decltype(rows)::value;
+    if (reverse)
+      scan_bf<true, R><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+    else
+      scan_bf<false, R><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+  };
+  if (NC >= 8 * kSG)
+    go(std::integral_constant<int, 8>{});
+  else if (NC >= 4 * kSG)
+    go(std::integral_constant<int, 4>{});
+  else if (NC >= 2 * kSG)
+    go(std::integral_constant<int, 2>{});
   else
-    scan_bf<false><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+    go(std::integral_constant<int, 1>{});
   return hipGetLastError();
 }
 
