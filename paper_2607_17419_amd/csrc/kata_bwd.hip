@@ -51,6 +51,12 @@ __host__ __device__ __forceinline__ int bwd_n(int d, int g) {
   return g * ((d / g) * (d / g + 1) / 2);
 }
 
+typedef float mf32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ mf32x16 mfma_f32(float a, float b, mf32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
 constexpr int kBFB = 16;  // features per workgroup of the state kernels
 constexpr int kBTB = 32;  // tokens staged per pass
 
@@ -136,10 +142,12 @@ __global__ __launch_bounds__(256) void bwd_chunk_state(const Tx* __restrict__ x,
 // with Z_pre the prefix z (fp32, chunk c at zsrc + bh z_bh + c z_c, diagonal
 // features scaled by zdiag) unpacked into a symmetric d x d matrix (zero across
 // feature blocks), then ab[t] = (dout_t / D_t, -<dout_t, o_t> / D_t), zeros
-// when D_t = 0.  Four lanes per token: lane part p takes the coordinates
-// 16 p .. 16 p + 15 of Z_pre q_t, the keys s = p, p + 4, ... and the values
-// j = p, p + 4, ...; shuffles join the parts.  The token's q row is held in
-// registers.  grid (NC, BH), block 256 (C <= 64), dynamic LDS bwd_coef_smem.
+// when D_t = 0.  Both sums are contractions on the fp32 matrix cores
+// (v_mfma_f32_32x32x2_f32): wave w takes the coordinate / key tile w >> 1 and
+// the token tile w & 1 of  Y = Z_pre Q^T  (then q_t . Y[:, t] over its rows)
+// and of the block scores  Sc_b = K_b Q_b^T  (squared, s <= t); the two tiles'
+// partial sums meet in LDS.  Four lanes per token then form a_t | b_t.
+// grid (NC, BH), block 256 (C <= 64), dynamic LDS bwd_coef_smem.
 // ---------------------------------------------------------------------------
 constexpr int kCS = 65;  // fp32 row stride of the coefficient kernel's tiles
 
@@ -157,6 +165,7 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   float* Z = bsm;             // [64][kCS] unpacked z_pre
   float* qs = Z + 64 * kCS;   // [64][kCS]
   float* ks = qs + 64 * kCS;  // [64][kCS]
+  float* red = ks + 64 * kCS;  // [2][64] partial D of the two coordinate tiles
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const long long t0 = static_cast<long long>(c) * C;
   const int nt = static_cast<int>(min(static_cast<long long>(C), T - t0));
@@ -174,40 +183,40 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
     ks[x * kCS + y] = in ? load_f32(kh, static_cast<long long>(x) * d + y) : 0.f;
   }
   __syncthreads();
-  const int r = tid >> 2, p = tid & 3;
-  float qr[64];
+  {
+    const int lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int X = w >> 1, t = 32 * (w & 1) + l32;
+    const float* qt = qs + t * kCS;
+    // prefix: Y[x][t] = sum_y Z[x][y] q_t[y] for the 32 rows x of tile X
+    mf32x16 yz = {};
+    const float* zr = Z + (32 * X + l32) * kCS;
+    for (int s2 = 0; s2 < 32; ++s2) yz = mfma_f32(zr[2 * s2 + h], qt[2 * s2 + h], yz);
+    float part = 0.f;
 #pragma unroll
-  for (int y = 0; y < 64; ++y) qr[y] = qs[r * kCS + y];
-  float D = 0.f;
-  // prefix: sum over this part's coordinates x of q_x (Z q)_x
-  for (int xi = 0; xi < 16; ++xi) {
-    const int x = 16 * p + xi;
-    const float* zr = Z + x * kCS;
-    float zq = 0.f;
-#pragma unroll
-    for (int y = 0; y < 64; ++y) zq += zr[y] * qr[y];
-    D += qs[r * kCS + x] * zq;
-  }
-  // in-chunk squared scores of the keys s <= r of this part
-  if (g == 1) {
-    for (int s = p; s <= r; s += 4) {
-      const float* kr = ks + s * kCS;
-      float sc = 0.f;
-#pragma unroll
-      for (int x = 0; x < 64; ++x) sc += qr[x] * kr[x];
-      D += sc * sc;
-    }
-  } else {
-    for (int s = p; s <= r; s += 4)
-      for (int blk = 0; blk < g; ++blk) {
-        float sc = 0.f;
-        for (int x = blk * m; x < blk * m + m; ++x) sc += qs[r * kCS + x] * ks[s * kCS + x];
-        D += sc * sc;
+    for (int i = 0; i < 16; ++i) part += qt[32 * X + 8 * (i >> 2) + 4 * h + (i & 3)] * yz[i];
+    // in-chunk: Sc_b[s][t] = sum_{x in block b} k_s[x] q_t[x] for the keys s of tile X
+    const float* kr = ks + (32 * X + l32) * kCS;
+    for (int blk = 0; blk < g; ++blk) {
+      const int x0 = blk * m, x1 = x0 + m;
+      mf32x16 sc = {};
+      for (int xs = x0 & ~1; xs < x1; xs += 2) {
+        const int x = xs + h;
+        const bool inb = x >= x0 && x < x1;
+        sc = mfma_f32(inb ? kr[x] : 0.f, inb ? qt[x] : 0.f, sc);
       }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int s_ = 32 * X + 8 * (i >> 2) + 4 * h + (i & 3);
+        if (s_ <= t) part += sc[i] * sc[i];
+      }
+    }
+    part += __shfl_xor(part, 32);
+    if (h == 0) red[X * 64 + t] = part;
   }
-  D += __shfl_xor(D, 1);
-  D += __shfl_xor(D, 2);
+  __syncthreads();
+  const int r = tid >> 2, p = tid & 3;
   if (r < nt) {
+    const float D = red[r] + red[64 + r];
     const long long row = static_cast<long long>(bh) * T + t0 + r;
     const float* dr = dout + row * dv;
     const float* orow = o + row * dv;
@@ -361,14 +370,9 @@ __global__ __launch_bounds__(256) void bwd_grad(const Tin* __restrict__ q,
 // fp32 matrix-core variants (v_mfma_f32_32x32x2_f32: lane l holds A[l % 32][l / 32]
 // and B[l / 32][l % 32]; result column l % 32, rows 8 (i / 4) + 4 (l / 32) + i % 4),
 // for C <= 64, d <= 64, dv <= 64.  Same arithmetic (fp32 products, fp32
-// accumulation) as the VALU kernels above, in another summation order.
+// accumulation) as the VALU kernels above, in another summation order.  The
+// coefficient kernel above uses the same instruction (mfma_f32).
 // ===========================================================================
-
-typedef float mf32x16 __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ mf32x16 mfma_f32(float a, float b, mf32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-}
 
 constexpr int kMS = 65;  // LDS row stride (floats) of the 64-row staging tiles
 
@@ -705,7 +709,7 @@ size_t bwd_grad_smem(int d, int C, int g) {
           2 * static_cast<size_t>(C) * kYB) * sizeof(float) + n * sizeof(uint16_t);
 }
 
-size_t bwd_coef_smem(int, int, int) { return 3 * 64 * kCS * sizeof(float); }
+size_t bwd_coef_smem(int, int, int) { return (3 * 64 * kCS + 2 * 64) * sizeof(float); }
 
 }  // namespace
 
