@@ -43,7 +43,9 @@ namespace {
 // below), so that with the pair weights (1 on the diagonal, 2 off it)
 //   dv^T[j][i] += 2 k_i[y] sum_x DT[j][x] k_i[x].
 // Two groups of four waves; group g takes the slabs y = g, g + 2, ... in its own
-// LDS slab buffer, so each SIMD runs two waves (one per group).  In a group,
+// LDS slab buffer, so each SIMD runs two waves (one per group).  The groups
+// stage and compute in step: two computing waves on a SIMD hide each other's
+// MFMA and epilogue latency (running them a phase apart was slower).  In a group,
 // waves 0-1 own dq of token tile w, 2-3 dk of key tile w - 2, and every wave
 // one 32 x 32 tile (value tile w >> 1, key tile w & 1) of dv.  Group 0 also
 // stages the chunk rows and takes the in-chunk terms; at the end group 1 adds

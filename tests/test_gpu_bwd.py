@@ -114,7 +114,7 @@ def test_bwd_one_token(kata, orc):
         assert np.all(np.linalg.norm(g_, axis=-1) <= scale * 2 * np.sqrt(D) + 1e-6)
 
 
-@pytest.mark.parametrize("T", [2, 63, 64, 65, 300, 1025])
+@pytest.mark.parametrize("T", [2, 63, 64, 65, 300, 1025, 2100])
 def test_bwd_ragged_m1(kata, orc, T):
     log(f"case bwd M1 bf16 inputs B1 H2 T{T} d64 dv64 C64")
     inp = workloads.make_inputs("mid_bf16", B=1, H=2, T=T)
