@@ -284,15 +284,21 @@ kata_status_t bwd_check(int B, int H, int T, int d, int dv, int C, int g, int dt
   return KATA_OK;
 }
 
+// Non-null, 16-byte aligned tensors of the backward (checked before any HIP call).
+bool bwd_ptrs_ok(const void* q, const void* k, const void* v, const float* out,
+                 const float* dout, const float* dq, const float* dk, const float* dvv) {
+  for (const void* p : {q, k, v, static_cast<const void*>(out), static_cast<const void*>(dout),
+                        static_cast<const void*>(dq), static_cast<const void*>(dk),
+                        static_cast<const void*>(dvv)})
+    if (!p || !aligned16(p)) return false;
+  return true;
+}
+
 kata_status_t bwd_ws(const void* q, const void* k, const void* v, const float* out,
                      const float* dout, float* dq, float* dk, float* dvv, int B, int H, int T,
                      int d, int dv, int C, int g, kata_dtype_t dtype, void* workspace,
                      size_t workspace_bytes, hipEvent_t* ev, hipStream_t stream) {
-  if (!q || !k || !v || !out || !dout || !dq || !dk || !dvv) return KATA_ERR_INVALID_ARG;
-  for (const void* p : {q, k, v, static_cast<const void*>(out), static_cast<const void*>(dout),
-                        static_cast<const void*>(dq), static_cast<const void*>(dk),
-                        static_cast<const void*>(dvv)})
-    if (!aligned16(p)) return KATA_ERR_INVALID_ARG;
+  if (!bwd_ptrs_ok(q, k, v, out, dout, dq, dk, dvv)) return KATA_ERR_INVALID_ARG;
   const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
   if (c != KATA_OK) return c;
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
@@ -545,7 +551,7 @@ kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v, cons
                                const float* dout, float* dq, float* dk, float* dv_out, int B,
                                int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
                                hipStream_t stream) {
-  if (!q || !k || !v || !out || !dout || !dq || !dk || !dv_out) return KATA_ERR_INVALID_ARG;
+  if (!bwd_ptrs_ok(q, k, v, out, dout, dq, dk, dv_out)) return KATA_ERR_INVALID_ARG;
   const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
   if (c != KATA_OK) return c;
   const size_t bytes = kata::bwd_workspace(B * H, T, d, dv, C, g);

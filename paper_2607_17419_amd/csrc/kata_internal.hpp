@@ -81,7 +81,8 @@ hipError_t launch_bwd_state_bf(bool backward, const void* x, const void* y, void
 // features weighted 1/2.
 hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_t st);
 // Gradients of every chunk from the scanned records, a_t | b_t rows (ab, row
-// stride 65) and bf16 q, k, v; q, k, v 4-byte and dq, dk, dv 16-byte aligned.
+// stride 65) and bf16 q, k, v; every tensor 16-byte aligned (as the C ABI
+// requires).
 hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const float* ab,
                               const void* frec, const void* brec, float* dq, float* dk,
                               float* dv_out, int BH, int T, hipStream_t st);

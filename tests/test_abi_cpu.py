@@ -242,6 +242,10 @@ def test_lin_workspace_and_span_host_logic():
     ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 65, 1, 0), 2),  # C > 64
     ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 80, 16, 32, 1, 0), 2),  # d > 64
     ((FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 16, 300, 32, 1, 0), 2),  # dv > 256
+    ((ctypes.c_void_p(0x100002), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 64, 64, 64,
+      1, 1), 1),  # bf16 q not 16-byte aligned
+    ((FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x100008), FAKE, FAKE, 1, 1, 8, 64, 64, 64,
+      1, 1), 1),  # dq not 16-byte aligned
 ])
 def test_bwd_rejects_before_gpu(args, expect):
     assert kata.lib().kata_bwd_chunked(*args, NUL) == expect

@@ -249,3 +249,4 @@ def test_bwd_full_length_two_heads(kata, orc):
             assert np.allclose(ex[2].sum(axis=2), dout.sum(axis=2), rtol=1e-4, atol=1e-3)
             scale = np.linalg.norm(ex[0], axis=-1) * np.linalg.norm(inp["q"], axis=-1)
             assert np.all(np.abs(qd) <= 1e-4 * scale + 1e-5)
+
