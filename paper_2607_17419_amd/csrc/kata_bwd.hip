@@ -175,9 +175,12 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   for (int i = tid; i < 64 * 64; i += 256) {
     const int x = i >> 6, y = i & 63;
     float zv = 0.f;
-    if (x < d && y < d && x / m == y / m)
-      zv = (x == y ? zdiag : 1.f) * zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
-    Z[x * kCS + y] = zv;
+    if (g == 1) {  // one block: no block index to divide out
+      if (x < d && y < d) zv = zp[packed_index(min(x, y), max(x, y), d)];
+    } else if (x < d && y < d && x / m == y / m) {
+      zv = zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
+    }
+    Z[x * kCS + y] = (x == y ? zdiag : 1.f) * zv;
     const bool in = x < nt && y < d;
     qs[x * kCS + y] = in ? load_f32(qh, static_cast<long long>(x) * d + y) : 0.f;
     ks[x * kCS + y] = in ? load_f32(kh, static_cast<long long>(x) * d + y) : 0.f;
