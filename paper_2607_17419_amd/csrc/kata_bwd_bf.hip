@@ -577,9 +577,9 @@ __global__ __launch_bounds__(256) void bwd_state_bf(const uint16_t* __restrict__
 // the kSG row groups of the workgroup join their block sums through LDS (kSR
 // shrinks for short sequences so that every row group has records).  The S / z
 // boundary falls on a workgroup boundary (kRecS16 is a multiple of kSC).
-// grid (ceil(kRec16 / kSC), BH), block 256.
+// grid (ceil(kRec16 / kSC), BH), block kSC x kSG.
 // ---------------------------------------------------------------------------
-constexpr int kSC = 32;  // 16-byte pieces per workgroup
+constexpr int kSC = 16;  // 16-byte pieces per workgroup
 constexpr int kSG = 8;   // row groups
 static_assert(kRecS16 % kSC == 0, "a workgroup reads one element type");
 
@@ -597,7 +597,7 @@ __device__ __forceinline__ bool diag_feature(int f) {
 }
 
 template <bool kReverse, int kSR>
-__global__ __launch_bounds__(256) void scan_bf(unsigned char* __restrict__ rec, int N,
+__global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__ rec, int N,
                                                long long rec_bh) {
   __shared__ float4 tot[kSG][kSC][2];
   const int tid = threadIdx.x, cg = tid % kSC, rg = tid / kSC;
@@ -727,9 +727,9 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
   auto go = [&](auto rows) {
     constexpr int R = decltype(rows)::value;
     if (reverse)
-      scan_bf<true, R><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+      scan_bf<true, R><<<grid, kSC * kSG, 0, st>>>(r, NC, rec_bh);
     else
-      scan_bf<false, R><<<grid, 256, 0, st>>>(r, NC, rec_bh);
+      scan_bf<false, R><<<grid, kSC * kSG, 0, st>>>(r, NC, rec_bh);
   };
   if (NC >= 8 * kSG)
     go(std::integral_constant<int, 8>{});
