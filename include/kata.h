@@ -286,8 +286,14 @@ KATA_API int kata_lin_default_span(int B, int H, int T, int d, int dv, int C,
  *             [B][H][T][dv] (kata_fwd_chunked or kata_mg_fwd_chunked), dout :
  *             fp32 [B][H][T][dv]; dq, dk : fp32 [B][H][T][d], dv_out : fp32
  *             [B][H][T][dv], overwritten, none aliasing an input.
- *   Supported: d <= 64, dv <= 256, C <= 64, g | d, fp32 or bf16 inputs; fp32
- *   arithmetic.  Else KATA_ERR_UNSUPPORTED (shape) or KATA_ERR_INVALID_ARG.
+ *   Supported: d <= 64, dv <= 256, C <= 64, g | d, fp32 or bf16 inputs.  Else
+ *   KATA_ERR_UNSUPPORTED (shape) or KATA_ERR_INVALID_ARG.
+ *   Arithmetic: fp32 throughout, except for bf16 inputs with d = dv = C = 64
+ *   and g = 1, where the chunk states, the scanned state records (S rounded to
+ *   bf16, z fp32, fp32 sums) and the gradient products run on the bf16 matrix
+ *   cores with fp32 accumulation, a_t and b_t entering as bf16 hi + lo pairs;
+ *   that path's gradients are within 2e-2 (per-head relative l2) of the exact
+ *   ones, about 2e-3 on the test workloads.
  *   workspace : >= kata_bwd_workspace_bytes(...) bytes, 256-byte aligned,
  *   caller-owned, contents undefined on exit; kata_bwd_chunked allocates it
  *   stream-ordered.  stage_events : 7 caller-created events, recorded before
