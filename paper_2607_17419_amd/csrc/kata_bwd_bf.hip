@@ -46,8 +46,10 @@ namespace {
 // LDS slab buffer, so each SIMD runs two waves (one per group).  The groups
 // stage and compute in step: two computing waves on a SIMD hide each other's
 // MFMA and epilogue latency (running them a phase apart was slower).  In a group,
-// waves 0-1 own dq of token tile w, 2-3 dk of key tile w - 2, and every wave
-// one 32 x 32 tile (value tile w >> 1, key tile w & 1) of dv.  Group 0 also
+// the waves of role 0-1 own dq of token tile role, 2-3 dk of key tile role - 2,
+// and every wave one 32 x 32 tile (value tile role >> 1, key tile role & 1) of
+// dv; role = w in group 0 and w + 2 (mod 4) in group 1, so that every SIMD
+// pairs a dq and a dk wave (dq has twice the slab MFMAs).  Group 0 also
 // stages the chunk rows and takes the in-chunk terms; at the end group 1 adds
 // its accumulators through LDS.  The record rows of a group's next slab are
 // fetched into registers (buffer loads) while the current one is used.
@@ -292,9 +294,13 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
   __syncthreads();
 
   // ---- in-chunk products and the per-wave operands of the slab loop ------------
-  const bool dqw = w < 2;
-  const int Tw = w & 1;  // token tile (dq waves) / key tile (dk waves) / key tile of dv
-  const int J = w >> 1;  // value tile of dv
+  // compute role: group 1 is rotated by two, so that each SIMD (wave w of
+  // both groups) runs one dq wave and one dk wave (the dq side has twice the
+  // slab MFMAs: a_t enters as hi + lo)
+  const int role = (w + 2 * grp) & 3;
+  const bool dqw = role < 2;
+  const int Tw = role & 1;  // token tile (dq) / key tile (dk) / key tile of dv
+  const int J = role >> 1;  // value tile of dv
   f32x16 acc0 = {}, acc1 = {}, dvacc = {};
   if (grp == 0) {
     const uint16_t* Xa = dqw ? KT : QT;
@@ -390,7 +396,7 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
     __syncthreads();
   }
   // group 1 hands its accumulators to group 0 through the (free) slab buffers
-  float* red = reinterpret_cast<float*>(slab) + (w * 64 + lane) * 48;
+  float* red = reinterpret_cast<float*>(slab) + (role * 64 + lane) * 48;
   if (grp == 1) {
 #pragma unroll
     for (int mq = 0; mq < 4; ++mq) {
