@@ -329,6 +329,11 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
   const uint16_t* xrow = (dqw ? Qs : Ks) + (32 * Tw + l32) * kBP;  // q_t or k_i of this lane
   const uint16_t* krow = Ks + (32 * Tw + l32) * kBP;               // k_i of the dv column
   float* Rout = (dqw ? dqR : dkR) + (32 * Tw + l32) * kBR;
+  float xr[2][16];  // x_t[x] (q or k of this lane's token) for its accumulator rows x
+#pragma unroll
+  for (int X = 0; X < 2; ++X)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xr[X][i] = bf_f32(xrow[32 * X + 8 * (i >> 2) + 4 * h + (i & 3)]);
   __syncthreads();  // the in-chunk tiles are dead: the slab buffers take over
 
   auto compute = [&](int y, const uint16_t* buf) {
@@ -355,29 +360,17 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
       Qy = mfma_bf(ld8(DT + (32 * J + l32) * kBP + 16 * ks + 8 * h), ld8(krow + 16 * ks + 8 * h), Qy);
     const float s2 = 2.f * bf_f32(xrow[y]);
     float R = 0.f;
-    // x_t[x] of this lane's accumulator rows x = 32 X + 8 m + 4 h + e, four per read
-    auto xq = [&](int X, int mq) { return *reinterpret_cast<const uint2*>(xrow + 32 * X + 8 * mq + 4 * h); };
     if (x0) {
 #pragma unroll
-      for (int mq = 0; mq < 4; ++mq) {
-        const uint2 xw = xq(0, mq);
-        const float xv[4] = {bf16lo_f32(xw.x), bf16hi_f32(xw.x), bf16lo_f32(xw.y), bf16hi_f32(xw.y)};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc0[4 * mq + e] += s2 * P0[4 * mq + e];
-          R += xv[e] * P0[4 * mq + e];
-        }
+      for (int i = 0; i < 16; ++i) {
+        acc0[i] += s2 * P0[i];
+        R += xr[0][i] * P0[i];
       }
     }
 #pragma unroll
-    for (int mq = 0; mq < 4; ++mq) {
-      const uint2 xw = xq(1, mq);
-      const float xv[4] = {bf16lo_f32(xw.x), bf16hi_f32(xw.x), bf16lo_f32(xw.y), bf16hi_f32(xw.y)};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc1[4 * mq + e] += s2 * P1[4 * mq + e];
-        R += xv[e] * P1[4 * mq + e];
-      }
+    for (int i = 0; i < 16; ++i) {
+      acc1[i] += s2 * P1[i];
+      R += xr[1][i] * P1[i];
     }
     R += __shfl_xor(R, 32);
     if (h == 0) Rout[y] = 2.f * R;
