@@ -336,12 +336,13 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
     for (int i = 0; i < 16; ++i) xr[X][i] = bf_f32(xrow[32 * X + 8 * (i >> 2) + 4 * h + (i & 3)]);
   __syncthreads();  // the in-chunk tiles are dead: the slab buffers take over
 
-  auto compute = [&](int y, const uint16_t* buf) {
+  // x0: x tile 0 still holds rows x >= y (y < 32), a compile-time switch
+  auto compute = [&](auto x0c, int y, const uint16_t* buf) {
+    constexpr bool x0 = decltype(x0c)::value;
     const uint16_t* Sl = buf + (dqw ? 0 : kBTW);
     const uint16_t* DT = buf + 2 * kBTW;
     f32x16 P0 = {}, P1 = {}, Qy = {};
-    const bool x0 = y < 32;  // x tile 0 holds rows x >= y
-    if (x0) {
+    if constexpr (x0) {
 #pragma unroll
       for (int ks = 0; ks < 5; ++ks) {
         const bf16x8 sf = ld8(Sl + l32 * kBW + 16 * ks + 8 * h);
@@ -360,7 +361,7 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
       Qy = mfma_bf(ld8(DT + (32 * J + l32) * kBP + 16 * ks + 8 * h), ld8(krow + 16 * ks + 8 * h), Qy);
     const float s2 = 2.f * bf_f32(xrow[y]);
     float R = 0.f;
-    if (x0) {
+    if constexpr (x0) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         acc0[i] += s2 * P0[i];
@@ -380,12 +381,20 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
   };
 
   uint16_t* mybuf = slab + grp * (kBfSlab / 2);
-  for (int i = 0; i < 32; ++i) {
+  for (int i = 0; i < 16; ++i) {
+    const int y = 2 * i + grp;
+    stage(pf0, y, mybuf);
+    fetch(pf0, y + 2);
+    __syncthreads();
+    compute(std::true_type{}, y, mybuf);
+    __syncthreads();
+  }
+  for (int i = 16; i < 32; ++i) {
     const int y = 2 * i + grp;
     stage(pf0, y, mybuf);
     fetch(pf0, min(y + 2, 63));
     __syncthreads();
-    compute(y, mybuf);
+    compute(std::false_type{}, y, mybuf);
     __syncthreads();
   }
   // group 1 hands its accumulators to group 0 through the (free) slab buffers
