@@ -101,7 +101,7 @@ __device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {
 
 // One slab's record values in registers: rows 8 rg .. 8 rg + 7 of the slab
 // tile, columns 2 cp, 2 cp + 1 of S and dS (bf16 pairs), and the z / dz of
-// row tid % 64.
+// row lane.
 struct BfSlabRegs {
   uint32_t a[8], b[8];
   float za, zb;
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
       p.a[r] = __builtin_amdgcn_raw_buffer_load_b32(rS, vo, so, 0);
       p.b[r] = __builtin_amdgcn_raw_buffer_load_b32(rB, vo, so, 0);
     }
-    const int zo = max((tid & 63) - y, 0) * 4;
+    const int zo = max(lane - y, 0) * 4;
     p.za = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rS, zo, kRecSB + f0 * 4, 0));
     p.zb = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rB, zo, kRecSB + f0 * 4, 0));
   };
@@ -185,8 +185,9 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
     *reinterpret_cast<uint4*>(DT + (2 * cp + 1) * kBP + 8 * rg) =
         make_uint4(hi_pair(sb[0], sb[1]), hi_pair(sb[2], sb[3]), hi_pair(sb[4], sb[5]),
                    hi_pair(sb[6], sb[7]));
-    if (w == 0) {  // z column and the zero columns 65..79 of row tid
-      const int x = tid;
+    if (w == 3) {  // z column and the zero columns 65..79 of row lane (wave 3
+                   // stages every slab)
+      const int x = lane;
       const float mz = x < y ? 0.f : 1.f;
       const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
       *reinterpret_cast<uint4*>(Ss + x * kBW + 64) = make_uint4(pack_bf16x2(p.za * mz, 0.f), 0u, 0u, 0u);
@@ -391,8 +392,12 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
   }
   for (int i = 16; i < 32; ++i) {
     const int y = 2 * i + grp;
-    stage(pf0, y, mybuf);
-    fetch(pf0, min(y + 2, 63));
+    // rows 0..31 (staged by waves 0 and 1) are zero once slab 32 + grp has
+    // been staged, so those waves stage and fetch nothing after it
+    if (w >= 2 || i == 16) {
+      stage(pf0, y, mybuf);
+      fetch(pf0, min(y + 2, 63));
+    }
     __syncthreads();
     compute(std::false_type{}, y, mybuf);
     __syncthreads();
