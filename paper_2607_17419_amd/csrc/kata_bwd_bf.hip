@@ -382,19 +382,23 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
   };
 
   uint16_t* mybuf = slab + grp * (kBfSlab / 2);
+  // wave w stages rows 16 w .. 16 w + 15; once the group's previous slab
+  // (y - 2) has zeroed them all (16 w + 16 <= y - 2) they stay zero, and the
+  // wave stages and fetches nothing more (wave 3 also stages z every slab)
+  auto live = [&](int y) { return 16 * w + 18 > y; };
   for (int i = 0; i < 16; ++i) {
     const int y = 2 * i + grp;
-    stage(pf0, y, mybuf);
-    fetch(pf0, y + 2);
+    if (live(y)) {
+      stage(pf0, y, mybuf);
+      fetch(pf0, y + 2);
+    }
     __syncthreads();
     compute(std::true_type{}, y, mybuf);
     __syncthreads();
   }
   for (int i = 16; i < 32; ++i) {
     const int y = 2 * i + grp;
-    // rows 0..31 (staged by waves 0 and 1) are zero once slab 32 + grp has
-    // been staged, so those waves stage and fetch nothing after it
-    if (w >= 2 || i == 16) {
+    if (live(y)) {
       stage(pf0, y, mybuf);
       fetch(pf0, min(y + 2, 63));
     }
