@@ -358,7 +358,7 @@ __global__ __launch_bounds__(512, 1) void bwd_grad_bf(const uint16_t* __restrict
       if (dqw) P1 = mfma_bf(sf, bfl[ks], P1);
     }
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)  // rows below y are staged as zeros
+    for (int ks = x0 ? 0 : 2; ks < 4; ++ks)  // rows below y are zero (all of x < 32 once y >= 32)
       Qy = mfma_bf(ld8(DT + (32 * J + l32) * kBP + 16 * ks + 8 * h), ld8(krow + 16 * ks + 8 * h), Qy);
     const float s2 = 2.f * bf_f32(xrow[y]);
     float R = 0.f;
