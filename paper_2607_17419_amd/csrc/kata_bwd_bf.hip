@@ -596,8 +596,8 @@ __global__ __launch_bounds__(256) void bwd_state_bf(const uint16_t* __restrict__
 // boundary falls on a workgroup boundary (kRecS16 is a multiple of kSC).
 // grid (ceil(kRec16 / kSC), BH), block kSC x kSG.
 // ---------------------------------------------------------------------------
-constexpr int kSC = 16;  // 16-byte pieces per workgroup
-constexpr int kSG = 8;   // row groups
+constexpr int kSC = 32;  // 16-byte pieces per workgroup (512 contiguous bytes of a record)
+constexpr int kSG = 2;   // row groups (one wave per workgroup: measured fastest)
 static_assert(kRecS16 % kSC == 0, "a workgroup reads one element type");
 
 // Whether packed index f (0 <= f < 2080) is a diagonal pair: f = D(a) =
@@ -611,6 +611,20 @@ __device__ __forceinline__ bool diag_feature(int f) {
   if (a < 63 && D(a + 1) <= f) ++a;
   if (a > 0 && D(a) > f) --a;
   return D(a) == f;
+}
+
+// Every record piece is read once and written once per scan, so both go past
+// the caches (non-temporal).  With the one-wave, 512-byte workgroup shape above
+// a scan at B8 H16 T4096 measured 0.79 ms, against 0.94 ms with cached access
+// and 16 x 8 workgroups.
+typedef unsigned scan_u4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream_load_u4(const unsigned char* p) {
+  const scan_u4 t = __builtin_nontemporal_load(reinterpret_cast<const scan_u4*>(p));
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void stream_store_u4(unsigned char* p, uint4 u) {
+  const scan_u4 t = {u.x, u.y, u.z, u.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<scan_u4*>(p));
 }
 
 template <bool kReverse, int kSR>
@@ -642,8 +656,7 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
       const int rr = rbase + j;
       uint4 u = make_uint4(0u, 0u, 0u, 0u);
       if (active && rr < N)
-        u = *reinterpret_cast<const uint4*>(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) *
-                                                     kRecB);
+        u = stream_load_u4(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) * kRecB);
       const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -709,7 +722,7 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
                                        pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7]))
                           : make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]),
                                        __float_as_uint(o[2]), __float_as_uint(o[3]));
-      *reinterpret_cast<uint4*>(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) * kRecB) = u;
+      stream_store_u4(rb + static_cast<long long>(kReverse ? N - 1 - rr : rr) * kRecB, u);
     }
 #pragma unroll
     for (int x = 0; x < 8; ++x) carry[x] += blk[x];

@@ -189,7 +189,22 @@ __global__ __launch_bounds__(256) void chunk_out_f32(
 // state).  One workgroup per head; S is streamed once (read-modify-write).
 // grid BH, block 256; d <= 64, dv <= 256.
 // ---------------------------------------------------------------------------
-constexpr int kDecodeUnroll = 8;  // S rows per thread whose loads are in flight together
+// S rows per thread whose loads are in flight together.  26 divides the 130
+// rows each thread walks at n = 2080, dv = 64 and still fits 256 VGPRs
+// (measured against 8, 16, 32, 40 and 48).
+constexpr int kDecodeUnroll = 26;
+
+// The state is touched once per step: stream it past the caches (non-temporal
+// loads and stores; together they raise the step from 5.1 to 5.85 TB/s).
+typedef float decode_f4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 stream_load4(const float* p) {
+  const decode_f4 t = __builtin_nontemporal_load(reinterpret_cast<const decode_f4*>(p));
+  return make_float4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void stream_store4(float* p, float4 s) {
+  const decode_f4 t = {s.x, s.y, s.z, s.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<decode_f4*>(p));
+}
 
 template <typename Tin>
 __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
@@ -233,7 +248,7 @@ __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
       s.y += pk * v1;
       s.z += pk * v2;
       s.w += pk * v3;
-      *reinterpret_cast<float4*>(Sh + static_cast<long long>(f) * dv + jbase) = s;
+      stream_store4(Sh + static_cast<long long>(f) * dv + jbase, s);
       num[0] += pq * s.x;
       num[1] += pq * s.y;
       num[2] += pq * s.z;
@@ -245,13 +260,12 @@ __global__ __launch_bounds__(256) void decode_step_f32(float* __restrict__ S,
       float4 s[kDecodeUnroll];
 #pragma unroll
       for (int u = 0; u < kDecodeUnroll; ++u)
-        s[u] = *reinterpret_cast<const float4*>(
-            Sh + static_cast<long long>(f + u * rows_per_pass) * dv + jbase);
+        s[u] = stream_load4(Sh + static_cast<long long>(f + u * rows_per_pass) * dv + jbase);
 #pragma unroll
       for (int u = 0; u < kDecodeUnroll; ++u) row(f + u * rows_per_pass, s[u]);
     }
     for (; f < n; f += rows_per_pass)
-      row(f, *reinterpret_cast<const float4*>(Sh + static_cast<long long>(f) * dv + jbase));
+      row(f, stream_load4(Sh + static_cast<long long>(f) * dv + jbase));
   } else {
     const int rows_per_pass = 256 / dv;  // dv <= 256
     jbase = tid % dv;
