@@ -6,6 +6,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <cstring>
 
 #include "kata.h"
 #include "kata_internal.hpp"
@@ -69,6 +70,19 @@ size_t workspace_for(Path path, int B, int H, int T, int d, int dv, int C, int g
 }
 
 kata_status_t from_hip(hipError_t e) { return e == hipSuccess ? KATA_OK : KATA_ERR_HIP; }
+
+// Stream-ordered workspace of the allocating entry points.  A failed
+// allocation returns KATA_ERR_HIP and clears the thread's last-error state, so
+// that the failure is not reported again by a later call's hipGetLastError.
+kata_status_t alloc_ws(void** ws, size_t bytes, hipStream_t stream) {
+  *ws = nullptr;
+  if (hipMallocAsync(ws, bytes, stream) != hipSuccess || *ws == nullptr) {
+    (void)hipGetLastError();
+    *ws = nullptr;
+    return KATA_ERR_HIP;
+  }
+  return KATA_OK;
+}
 
 int default_span_of(int B, int H, int T, int d, int dv, int C, int dtype, int g) {
   const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
@@ -136,7 +150,7 @@ kata_status_t fwd_alloc(const void* q, const void* k, const void* v, float* out,
   const int span = (p == Path::kFp32) ? 1 : default_span(C, p);
   const size_t bytes = workspace_for(p, B, H, T, d, dv, C, g, span);
   void* ws = nullptr;
-  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  if (alloc_ws(&ws, bytes, stream) != KATA_OK) return KATA_ERR_HIP;
   const kata_status_t st =
       fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span, ws, bytes, nullptr, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);
@@ -311,6 +325,25 @@ kata_status_t bwd_ws(const void* q, const void* k, const void* v, const float* o
                                                  g, workspace, stream, ev));
 }
 
+// Enum arguments arrive from C callers as plain ints and may hold any value;
+// in C++ an enum object outside its enumerators' range must not be read as
+// that enum type, so the entry points look at their bits first.
+template <typename E>
+int enum_bits(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "enums of the C ABI are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+bool dtype_ok(const kata_dtype_t& t) {
+  const int v = enum_bits(t);
+  return v == KATA_F32 || v == KATA_BF16;
+}
+bool feature_ok(const kata_lin_feature_t& f) {
+  const int v = enum_bits(f);
+  return v >= KATA_LIN_IDENTITY && v <= KATA_LIN_LORENTZ_S;
+}
+
 }  // namespace
 
 extern "C" {
@@ -318,7 +351,7 @@ extern "C" {
 int kata_abi_version(void) { return 103; }
 
 const char* kata_status_string(kata_status_t s) {
-  switch (s) {
+  switch (enum_bits(s)) {
     case KATA_OK: return "KATA_OK";
     case KATA_ERR_INVALID_ARG: return "KATA_ERR_INVALID_ARG";
     case KATA_ERR_UNSUPPORTED: return "KATA_ERR_UNSUPPORTED";
@@ -330,11 +363,13 @@ const char* kata_status_string(kata_status_t s) {
 // ---- KATA-M1 ----------------------------------------------------------------
 
 int kata_fwd_default_span(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return 0;
   return default_span_of(B, H, T, d, dv, C, dtype, 1);
 }
 
 size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                 int span_chunks) {
+  if (!dtype_ok(dtype)) return 0;
   return fwd_workspace_bytes(B, H, T, d, dv, C, dtype, 1, span_chunks);
 }
 
@@ -342,6 +377,7 @@ kata_status_t kata_fwd_chunked_ws(const void* q, const void* k, const void* v, f
                                   int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                   int span_chunks, void* workspace, size_t workspace_bytes,
                                   hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_ws(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
                 workspace_bytes, nullptr, stream);
 }
@@ -351,6 +387,7 @@ kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v
                                      kata_dtype_t dtype, int span_chunks, void* workspace,
                                      size_t workspace_bytes, hipEvent_t* stage_events,
                                      hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_timed(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
                    workspace_bytes, stage_events, stream);
 }
@@ -358,29 +395,33 @@ kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v
 kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
                                int H, int T, int d, int dv, int C, kata_dtype_t dtype,
                                hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_alloc(q, k, v, out, B, H, T, d, dv, C, 1, dtype, stream);
 }
 
 size_t kata_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return 0;
   return quad_workspace_bytes(B, H, T, d, dv, dtype, 1);
 }
 
 kata_status_t kata_fwd_quadratic_ws(const void* q, const void* k, const void* v, float* out, int B,
                                     int H, int T, int d, int dv, kata_dtype_t dtype,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return quad_ws(q, k, v, out, B, H, T, d, dv, 1, dtype, workspace, workspace_bytes, stream);
 }
 
 kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, float* out, int B,
                                  int H, int T, int d, int dv, kata_dtype_t dtype,
                                  hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
   const kata_status_t c = quad_check(B, H, T, d, dv, dtype, 1);
   if (c != KATA_OK) return c;
   const size_t bytes = kata::mfma_quadratic_workspace(B * H, T, dv);
   void* ws = nullptr;
-  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  if (alloc_ws(&ws, bytes, stream) != KATA_OK) return KATA_ERR_HIP;
   const kata_status_t st = quad_ws(q, k, v, out, B, H, T, d, dv, 1, dtype, ws, bytes, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);
   if (st != KATA_OK) return st;
@@ -389,12 +430,14 @@ kata_status_t kata_fwd_quadratic(const void* q, const void* k, const void* v, fl
 
 kata_status_t kata_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
                                  int T, int d, int dv, kata_dtype_t dtype, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return prefill(k, v, S, z, B, H, T, d, dv, 1, dtype, stream);
 }
 
 kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k, const void* v,
                                float* out, int B, int H, int d, int dv, kata_dtype_t dtype,
                                hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return decode(S, z, q, k, v, out, B, H, d, dv, 1, dtype, stream);
 }
 
@@ -402,6 +445,7 @@ kata_status_t kata_decode_step(float* S, float* z, const void* q, const void* k,
 
 size_t kata_mg_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
                                    kata_dtype_t dtype, int span_chunks) {
+  if (!dtype_ok(dtype)) return 0;
   return fwd_workspace_bytes(B, H, T, d, dv, C, dtype, g, span_chunks);
 }
 
@@ -409,6 +453,7 @@ kata_status_t kata_mg_fwd_chunked_ws(const void* q, const void* k, const void* v
                                      int B, int H, int T, int d, int dv, int C, int g,
                                      kata_dtype_t dtype, int span_chunks, void* workspace,
                                      size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span_chunks, workspace,
                 workspace_bytes, nullptr, stream);
 }
@@ -418,6 +463,7 @@ kata_status_t kata_mg_fwd_chunked_timed(const void* q, const void* k, const void
                                         kata_dtype_t dtype, int span_chunks, void* workspace,
                                         size_t workspace_bytes, hipEvent_t* stage_events,
                                         hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_timed(q, k, v, out, B, H, T, d, dv, C, g, dtype, span_chunks, workspace,
                    workspace_bytes, stage_events, stream);
 }
@@ -425,11 +471,13 @@ kata_status_t kata_mg_fwd_chunked_timed(const void* q, const void* k, const void
 kata_status_t kata_mg_fwd_chunked(const void* q, const void* k, const void* v, float* out, int B,
                                   int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
                                   hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_alloc(q, k, v, out, B, H, T, d, dv, C, g, dtype, stream);
 }
 
 size_t kata_mg_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, int g,
                                              kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return 0;
   return quad_workspace_bytes(B, H, T, d, dv, dtype, g);
 }
 
@@ -437,30 +485,36 @@ kata_status_t kata_mg_fwd_quadratic_ws(const void* q, const void* k, const void*
                                        int B, int H, int T, int d, int dv, int g,
                                        kata_dtype_t dtype, void* workspace,
                                        size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return quad_ws(q, k, v, out, B, H, T, d, dv, g, dtype, workspace, workspace_bytes, stream);
 }
 
 kata_status_t kata_mg_prefill_state(const void* k, const void* v, float* S, float* z, int B, int H,
                                     int T, int d, int dv, int g, kata_dtype_t dtype,
                                     hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return prefill(k, v, S, z, B, H, T, d, dv, g, dtype, stream);
 }
 
 kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, const void* k, const void* v,
                                   float* out, int B, int H, int d, int dv, int g,
                                   kata_dtype_t dtype, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return decode(S, z, q, k, v, out, B, H, d, dv, g, dtype, stream);
 }
 
 // ---- linear features -----------------------------------------------------------
 
 int kata_lin_dim(int d, kata_lin_feature_t feature) {
+  if (!feature_ok(feature)) return 0;
   if (d < 1 || feature < KATA_LIN_IDENTITY || feature > KATA_LIN_LORENTZ_S) return 0;
   return kata::lin_dim(d, feature);
 }
 
 int kata_lin_default_span(int B, int H, int T, int d, int dv, int C, kata_lin_feature_t feature,
                           kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return 0;
+  if (!feature_ok(feature)) return 0;
   const Path p = lin_path(B, H, T, d, dv, C, feature, 0.f, 1, dtype);
   if (p == Path::kInvalid || p == Path::kUnsupported) return 0;
   return lin_default_span(B, H, T, C, p);
@@ -469,6 +523,8 @@ int kata_lin_default_span(int B, int H, int T, int d, int dv, int C, kata_lin_fe
 size_t kata_lin_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C,
                                     kata_lin_feature_t feature, kata_dtype_t dtype,
                                     int span_chunks) {
+  if (!dtype_ok(dtype)) return 0;
+  if (!feature_ok(feature)) return 0;
   const Path p = lin_path(B, H, T, d, dv, C, feature, 0.f, 1, dtype);
   if (p == Path::kInvalid || p == Path::kUnsupported || span_chunks < 0) return 0;
   if (span_chunks == 0) span_chunks = lin_default_span(B, H, T, C, p);
@@ -481,6 +537,8 @@ kata_status_t kata_lin_fwd_chunked_ws(const void* q, const void* k, const void* 
                                       kata_lin_feature_t feature, float eps, int normalize,
                                       kata_dtype_t dtype, int span_chunks, void* workspace,
                                       size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  if (!feature_ok(feature)) return KATA_ERR_INVALID_ARG;
   return lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype, span_chunks,
                 workspace, workspace_bytes, nullptr, stream);
 }
@@ -491,6 +549,8 @@ kata_status_t kata_lin_fwd_chunked_timed(const void* q, const void* k, const voi
                                          kata_dtype_t dtype, int span_chunks, void* workspace,
                                          size_t workspace_bytes, hipEvent_t* stage_events,
                                          hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  if (!feature_ok(feature)) return KATA_ERR_INVALID_ARG;
   if (!stage_events) return KATA_ERR_INVALID_ARG;
   for (int i = 0; i < 4; ++i)
     if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
@@ -502,6 +562,8 @@ kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v, 
                                    int H, int T, int d, int dv, int C, kata_lin_feature_t feature,
                                    float eps, int normalize, kata_dtype_t dtype,
                                    hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  if (!feature_ok(feature)) return KATA_ERR_INVALID_ARG;
   if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
   const Path p = lin_path(B, H, T, d, dv, C, feature, eps, normalize, dtype);
@@ -510,7 +572,7 @@ kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v, 
   const int span = lin_default_span(B, H, T, C, p);
   const size_t bytes = lin_workspace_for(p, B, H, T, d, dv, C, feature, span);
   void* ws = nullptr;
-  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  if (alloc_ws(&ws, bytes, stream) != KATA_OK) return KATA_ERR_HIP;
   const kata_status_t st = lin_ws(q, k, v, out, B, H, T, d, dv, C, feature, eps, normalize, dtype,
                                   span, ws, bytes, nullptr, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);
@@ -522,6 +584,7 @@ kata_status_t kata_lin_fwd_chunked(const void* q, const void* k, const void* v, 
 
 size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
                                 kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return 0;
   if (bwd_check(B, H, T, d, dv, C, g, dtype) != KATA_OK) return 0;
   return kata::bwd_workspace(B * H, T, d, dv, C, g);
 }
@@ -530,6 +593,7 @@ kata_status_t kata_bwd_chunked_ws(const void* q, const void* k, const void* v, c
                                   const float* dout, float* dq, float* dk, float* dv_out, int B,
                                   int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype, workspace,
                 workspace_bytes, nullptr, stream);
 }
@@ -540,6 +604,7 @@ kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, const void* v
                                      int g, kata_dtype_t dtype, void* workspace,
                                      size_t workspace_bytes, hipEvent_t* stage_events,
                                      hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   if (!stage_events) return KATA_ERR_INVALID_ARG;
   for (int i = 0; i < 7; ++i)
     if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
@@ -551,12 +616,13 @@ kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v, cons
                                const float* dout, float* dq, float* dk, float* dv_out, int B,
                                int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype,
                                hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   if (!bwd_ptrs_ok(q, k, v, out, dout, dq, dk, dv_out)) return KATA_ERR_INVALID_ARG;
   const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
   if (c != KATA_OK) return c;
   const size_t bytes = kata::bwd_workspace(B * H, T, d, dv, C, g);
   void* ws = nullptr;
-  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) return KATA_ERR_HIP;
+  if (alloc_ws(&ws, bytes, stream) != KATA_OK) return KATA_ERR_HIP;
   const kata_status_t st = bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype,
                                   ws, bytes, nullptr, stream);
   const hipError_t fe = hipFreeAsync(ws, stream);

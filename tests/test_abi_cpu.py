@@ -267,3 +267,32 @@ def test_bwd_workspace_host_logic():
     assert L.kata_bwd_chunked_ws(*base, ctypes.c_void_p(0x100000), need - 1, NUL) == 1
     assert L.kata_bwd_chunked_ws(*base, ctypes.c_void_p(0x100010), need, NUL) == 1
     assert L.kata_bwd_chunked_timed(*base, ctypes.c_void_p(0x100000), need, NUL, NUL) == 1
+
+
+# Shapes whose workspace (terabytes) no device holds: the allocating entry
+# points validate them, fail the stream-ordered allocation and return
+# KATA_ERR_HIP before any launch, on a machine with or without a GPU.
+HUGE_BH, HUGE_T = 16384, 983040
+
+
+def huge_alloc_calls(L, ptr):
+    F = ptr
+    B, H, T = 1, HUGE_BH, HUGE_T
+    return [
+        ("kata_fwd_chunked", lambda: L.kata_fwd_chunked(F, F, F, F, B, H, T, 64, 64, 64, 1, NUL)),
+        ("kata_mg_fwd_chunked",
+         lambda: L.kata_mg_fwd_chunked(F, F, F, F, B, H, T, 64, 64, 64, 2, 1, NUL)),
+        ("kata_fwd_quadratic",
+         lambda: L.kata_fwd_quadratic(F, F, F, F, B, H, T, 64, 64, 1, NUL)),
+        ("kata_bwd_chunked",
+         lambda: L.kata_bwd_chunked(F, F, F, F, F, F, F, F, B, H, T, 64, 64, 64, 1, 1, NUL)),
+    ]
+
+
+def test_allocation_failure_is_hip_error():
+    L = kata.lib()
+    assert L.kata_fwd_workspace_bytes(1, HUGE_BH, HUGE_T, 64, 64, 64, 1, 0) > (1 << 40)
+    for name, call in huge_alloc_calls(L, FAKE):
+        assert call() == 3, name
+        # nothing is left behind: a plain validation error reports as such
+        assert L.kata_fwd_chunked(NUL, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 0, NUL) == 1

@@ -75,13 +75,34 @@ def _check_f32(got, ref, what):
         assert np.all(np.isfinite(a)) and err <= tol, (what, name)
 
 
-def _check_rel(got, ref, what, tol=BF16_REL):
+def _check_rel(got, ref, what, tol=BF16_REL, per_row=True):
+    """Per-head relative l2 error of each gradient tensor, and per row: the
+    error of row t against max(|ref_t|, the rms row norm of its head), so an
+    error confined to one chunk or slab of a long head cannot hide under the
+    head's norm, while rows with tiny gradients are held to the head's scale.
+
+    The per-row bound applies to the backward fed the exact forward output.
+    Given the library's own forward output instead, dq_t carries b_t =
+    -<dout_t, o_t> / D_t times dD_t/dq_t, a term that cancels exactly against
+    the rest of dq_t only for the exact o_t: the forward's bf16 rounding of
+    o_t (a few 1e-3) then shows up in rows where that cancellation is deep,
+    which is conditioning of the composition, not an error of the backward;
+    those runs keep the per-head bound only."""
     for name, a, b in zip(("dq", "dk", "dv"), got, ref):
-        a = a.astype(np.float64).reshape(-1, b.shape[2] * b.shape[3])
-        b = b.reshape(-1, b.shape[2] * b.shape[3])
-        rel = np.linalg.norm(a - b, axis=1) / np.maximum(np.linalg.norm(b, axis=1), 1e-30)
-        log(f"  {what} {name}: max per-head rel l2 err {float(rel.max()):.3e} (tol {tol:.0e})")
+        T, w = b.shape[2], b.shape[3]
+        a = a.astype(np.float64).reshape(-1, T, w)
+        b = b.reshape(-1, T, w)
+        rel = (np.linalg.norm((a - b).reshape(-1, T * w), axis=1) /
+               np.maximum(np.linalg.norm(b.reshape(-1, T * w), axis=1), 1e-30))
+        row_err = np.linalg.norm(a - b, axis=2)
+        row_ref = np.linalg.norm(b, axis=2)
+        rms = np.sqrt(np.mean(row_ref ** 2, axis=1, keepdims=True))
+        row_rel = row_err / np.maximum(np.maximum(row_ref, rms), 1e-30)
+        log(f"  {what} {name}: max per-head rel l2 err {float(rel.max()):.3e}, "
+            f"max per-row {float(row_rel.max()):.3e} (tol {tol:.0e})")
         assert np.all(np.isfinite(a)) and float(rel.max()) <= tol, (what, name)
+        if per_row:
+            assert float(row_rel.max()) <= tol, (what, name, "per row")
 
 
 @pytest.mark.parametrize("g", [1, 2, 4])
@@ -123,7 +144,7 @@ def test_bwd_ragged_m1(kata, orc, T):
     o_ref = orc.fwd(inp["q"], inp["k"], inp["v"])
     _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=o_ref), ref, f"T{T} bwd",
                tol=BF16_GRAD_REL)
-    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1), ref, f"T{T} fwd+bwd")
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1), ref, f"T{T} fwd+bwd", per_row=False)
 
 
 @pytest.mark.parametrize("C,g", [(16, 1), (32, 1), (48, 2), (64, 2), (64, 4)])
@@ -136,7 +157,8 @@ def test_bwd_chunks_and_blocks(kata, orc, C, g):
     o_ref = orc.fwd_mg(inp["q"], inp["k"], inp["v"], g)
     _check_rel(_gpu_bwd(kata, inp, "bf16", dout, C, g, out=o_ref), ref, f"C{C} g{g} bwd",
                tol=BF16_GRAD_REL if _bf_path(64, 64, C, g) else F32_GRAD_REL)
-    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, C, g, fwd_C=64), ref, f"C{C} g{g} fwd+bwd")
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, C, g, fwd_C=64), ref, f"C{C} g{g} fwd+bwd",
+               per_row=False)
 
 
 def test_bwd_value_width_and_recall(kata, orc):
@@ -165,7 +187,10 @@ def test_bwd_value_width_and_recall(kata, orc):
     inp = workloads.make_inputs("recall_bf16", B=1, H=2, T=1500)
     dout = _dout(inp["v"].shape, 23)
     ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
-    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, fwd_C=128), ref, "recall fwd+bwd")
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=orc.fwd(inp["q"], inp["k"], inp["v"])),
+               ref, "recall bwd", tol=F32_GRAD_REL)
+    _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1, fwd_C=128), ref, "recall fwd+bwd",
+               per_row=False)
 
 
 def test_bwd_zero_denominator(kata, orc):
@@ -223,7 +248,7 @@ def test_bwd_full_length_two_heads(kata, orc):
     dout = _dout(inp["v"].shape, 37)
     ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
     got = _gpu_bwd(kata, inp, "bf16", dout, 64, 1)
-    _check_rel(got, ref, "T4096 fwd+bwd")
+    _check_rel(got, ref, "T4096 fwd+bwd", per_row=False)
     # invariants, on the backward fed the exact forward output (q_t . dq_t equals
     # 2 <dout_t, o_t - o_given>, so it vanishes only for the exact o): the value
     # gradients sum to the output cotangents; q_t . dq_t = 0.  C = 32 runs the
