@@ -23,8 +23,9 @@
  *    on an error nothing is launched and nothing is written.
  *  - Calls only enqueue work on `stream` and return; they never synchronise.
  *    A device fault surfaces at the caller's next synchronisation.
- *  - The library keeps no global mutable state; calls from several threads
- *    are safe.  NaN and Inf in inputs propagate; inputs are not normalised.
+ *  - The library keeps no global mutable state (except the scratch array of
+ *    kata_fwd_chunked_noalloc, see there); calls from several threads are
+ *    safe.  NaN and Inf in inputs propagate; inputs are not normalised.
  *  - Packed state layout (decode and prefill): the n = d(d+1)/2 features of
  *    the pair (a, b), a <= b, in row-major upper-triangle order,
  *        f(a, b) = a*d - a*(a-1)/2 + (b - a),
@@ -70,6 +71,30 @@ typedef enum { KATA_F32 = 0, KATA_BF16 = 1 } kata_dtype_t;
 KATA_API kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, float* out,
                                int B, int H, int T, int d, int dv, int C,
                                kata_dtype_t dtype, hipStream_t stream);
+
+/*
+ * kata_fwd_chunked for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, default span and results as kata_fwd_chunked; it calls no
+ * hipMalloc / hipFree or allocating library routine.  Its workspace is a
+ * library-owned device array of kata_noalloc_scratch_bytes() bytes (256 MiB),
+ * one per GPU, held by every GPU the library runs on until the process ends;
+ * the first call on a device looks up that device's copy (the stream's device;
+ * the current device for the null stream).
+ *   Returns KATA_ERR_UNSUPPORTED when the workspace kata_fwd_chunked would
+ *   allocate (kata_fwd_workspace_bytes at the default span) exceeds the array,
+ *   e.g. B*H*T above about 650k head-tokens at d = dv = 64 on the bf16 path.
+ *   Every call on one GPU shares that GPU's array and leaves its contents
+ *   behind: calls that overlap on one GPU (different streams, or host
+ *   threads) race and give undefined results.  No kernel reads scratch that
+ *   the same call has not written, so nothing is cleared between calls.
+ */
+KATA_API kata_status_t kata_fwd_chunked_noalloc(const void* q, const void* k, const void* v,
+                                                float* out, int B, int H, int T, int d, int dv,
+                                                int C, kata_dtype_t dtype, hipStream_t stream);
+
+/* Size in bytes of the per-device scratch array of kata_fwd_chunked_noalloc. */
+KATA_API size_t kata_noalloc_scratch_bytes(void);
 
 /*
  * The same forward with caller-provided workspace and an explicit span.

@@ -37,6 +37,7 @@ EXPORTED = (
     "kata_lin_fwd_chunked_timed", "kata_lin_fwd_workspace_bytes", "kata_lin_default_span",
     "kata_bwd_chunked", "kata_bwd_chunked_ws", "kata_bwd_chunked_timed",
     "kata_bwd_workspace_bytes",
+    "kata_fwd_chunked_noalloc", "kata_noalloc_scratch_bytes",
     "kata_status_string", "kata_abi_version",
 )
 
@@ -65,6 +66,10 @@ def lib():
     vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     L.kata_fwd_chunked.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
     L.kata_fwd_chunked.restype = i
+    L.kata_fwd_chunked_noalloc.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+    L.kata_fwd_chunked_noalloc.restype = i
+    L.kata_noalloc_scratch_bytes.argtypes = []
+    L.kata_noalloc_scratch_bytes.restype = sz
     L.kata_fwd_chunked_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp]
     L.kata_fwd_chunked_ws.restype = i
     L.kata_fwd_chunked_timed.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp, vp]
@@ -247,6 +252,26 @@ def fwd_chunked_alloc(q, k, v, C: int, out=None, stream=None):
     _check(lib().kata_fwd_chunked(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
                                   B, H, T, d, dv, C, code, _stream(stream, q.device)),
            "kata_fwd_chunked")
+    return out
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(lib().kata_noalloc_scratch_bytes())
+
+
+def fwd_chunked_noalloc(q, k, v, C: int, out=None, stream=None):
+    """Causal forward via kata_fwd_chunked_noalloc (workspace in the library's
+    per-device scratch array, nothing allocated by the library); returns out
+    [B,H,T,dv] fp32 (allocated here by torch if not given)."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    _check(lib().kata_fwd_chunked_noalloc(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                          _dev(out, "out"), B, H, T, d, dv, C, code,
+                                          _stream(stream, q.device)),
+           "kata_fwd_chunked_noalloc")
     return out
 
 

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "kata.h"
 #include "kata_internal.hpp"
@@ -156,6 +157,72 @@ kata_status_t fwd_alloc(const void* q, const void* k, const void* v, float* out,
   const hipError_t fe = hipFreeAsync(ws, stream);
   if (st != KATA_OK) return st;
   return from_hip(fe);
+}
+
+// ---- allocation-free forward ------------------------------------------------
+// The workspace of kata_fwd_chunked_noalloc is this file-scope device array:
+// every GPU the library runs on holds its own copy until the process ends.
+// Host code never passes the array's name to a kernel (on the host it is only
+// a stand-in symbol); it uses the device address that hipGetSymbolAddress
+// returns for the device the call runs on, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = static_cast<size_t>(256) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};  // device address of `scratch`, per device
+
+// Device address of the scratch array on the device that `stream` belongs to
+// (the current device for the null stream).  The first call on a device makes
+// that device current for the lookup and restores the caller's device.
+kata_status_t scratch_ptr(hipStream_t stream, void** out) {
+  *out = nullptr;
+  int cur = -1, dev = -1;
+  if (hipGetDevice(&cur) != hipSuccess) {
+    (void)hipGetLastError();
+    return KATA_ERR_HIP;
+  }
+  dev = cur;
+  if (stream != nullptr && hipStreamGetDevice(stream, &dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return KATA_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return KATA_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return KATA_ERR_HIP;
+    }
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return KATA_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return KATA_OK;
+}
+
+kata_status_t fwd_noalloc(const void* q, const void* k, const void* v, float* out, int B, int H,
+                          int T, int d, int dv, int C, int g, kata_dtype_t dtype,
+                          hipStream_t stream) {
+  if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
+  if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
+  if (p == Path::kUnsupported) return KATA_ERR_UNSUPPORTED;
+  const int span = (p == Path::kFp32) ? 1 : default_span(C, p);
+  const size_t bytes = workspace_for(p, B, H, T, d, dv, C, g, span);
+  if (bytes > kNoAllocScratchBytes) return KATA_ERR_UNSUPPORTED;  // beyond the scratch array
+  void* ws = nullptr;
+  const kata_status_t st = scratch_ptr(stream, &ws);
+  if (st != KATA_OK) return st;
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, g, dtype, span, ws, kNoAllocScratchBytes,
+                nullptr, stream);
 }
 
 // Quadratic form: bf16 MFMA path only.
@@ -348,7 +415,7 @@ bool feature_ok(const kata_lin_feature_t& f) {
 
 extern "C" {
 
-int kata_abi_version(void) { return 103; }
+int kata_abi_version(void) { return 104; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (enum_bits(s)) {
@@ -398,6 +465,15 @@ kata_status_t kata_fwd_chunked(const void* q, const void* k, const void* v, floa
   if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_alloc(q, k, v, out, B, H, T, d, dv, C, 1, dtype, stream);
 }
+
+kata_status_t kata_fwd_chunked_noalloc(const void* q, const void* k, const void* v, float* out,
+                                       int B, int H, int T, int d, int dv, int C,
+                                       kata_dtype_t dtype, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  return fwd_noalloc(q, k, v, out, B, H, T, d, dv, C, 1, dtype, stream);
+}
+
+size_t kata_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
 
 size_t kata_fwd_quadratic_workspace_bytes(int B, int H, int T, int d, int dv, kata_dtype_t dtype) {
   if (!dtype_ok(dtype)) return 0;

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 103
+    assert L.kata_abi_version() == 104
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
