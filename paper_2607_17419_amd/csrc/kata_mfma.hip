@@ -287,26 +287,53 @@ __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 
 
 // ---------------------------------------------------------------------------
 // K2: span state.  1-D grid of workgroups of 256 threads (4 waves).  A span
-// gets NB blocks: NUW = ceil(NST / kUW) slot waves, then one wave for Z and
-// V^T (any further wave only helps stage).  Block id -> (span, part) keeps
-// the blocks of one span on one XCD (equal id % 8), dispatched back to back,
-// so the later blocks' reads of the span's K and V hit that XCD's L2.
+// gets NB blocks: NUW = ceil(NST / kUW) slot waves, then one wave for Z (any
+// further wave only helps stage).  Block id -> (span, part) keeps the blocks
+// of one span on one XCD (equal id % 8), dispatched back to back, so the later
+// blocks' reads of the span's K and V hit that XCD's L2.
 // Slot wave gw owns slot tiles [gw*kUW, +kUW); tiles past the last one
 // compute on a valid row and skip their store, so every wave runs the same
-// branch-free MFMA loop.  The Z wave computes Z = K^T K and writes the span's
-// V^T (bf16, [dv][LV], keys of every 16-key group in the order 0-3, 8-11,
-// 4-7, 12-15: the K order of the output kernel's P V product).
-// K and V are staged transposed ([dim][token]) through a three-buffer LDS
-// ring in blocks of kTB2 tokens; a slot wave loads the LDS fragments of
-// K-step ks+1 before it computes K-step ks.
+// branch-free MFMA loop.  The Z wave computes Z = K^T K.
+//
+// Arithmetic.  K and V are staged transposed ([dim][token]) in fp16 through a
+// three-buffer LDS ring in blocks of kTB2 tokens, and the state is an fp16
+// MFMA product with fp32 accumulation: a feature k_x k_y of two tokens is one
+// packed fp16 multiply (v_pk_mul_f16) of two staged fp16 pairs, the B operand
+// as it stands, with no conversion step.  bf16 inputs convert to fp16 exactly
+// within fp16's exponent range, so each span gets power-of-two scales:
+//   * if the first staged block's largest |k| lies in [2^-4, 2^4) and its
+//     largest |v| in [2^-8, 2^8), the span runs unscaled (no extra work);
+//   * otherwise, or if the unscaled pass produced a non-finite state (a later
+//     block outgrew fp16: an fp16 overflow becomes inf, caught when the state
+//     is written), the workgroup reads the span once for its exact maxima and
+//     runs again with k -> k 2^-ek, v -> v 2^-ev (largest |k|, |v| in [1, 2)),
+//     undoing the scales exactly when it writes the record.
+// Features are rounded once, to fp16 (unit roundoff 2^-11, finer than a bf16
+// rounding); the records are written in bf16 as before.
+//
+// The workgroup with part 0 also writes the span's V^T (bf16, [dv][LV], keys
+// of every 16-key group in the order 0-3, 8-11, 4-7, 12-15: the K order of
+// the output kernel's P V product) straight from its staging registers.
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
 // ---------------------------------------------------------------------------
 constexpr int kTB2 = 128;           // tokens per staged block
-constexpr int kRow2 = kTB2 + 8;     // V^T row length in LDS (bf16): rows 272 B apart
-constexpr int kRowK2 = kTB2 + 4;    // K row length in LDS (fp32): rows 528 B apart
-constexpr int kGapK2 = 32;          // fp32 gap before key row d/2 (see krow)
+constexpr int kRow2 = kTB2 + 8;     // K^T / V^T row length in LDS (fp16): rows 272 B apart
+constexpr int kGapK2 = 64;          // fp16 gap (32 banks) before key rows DM/2, DM, ... (krow)
 constexpr int kUW = 6;              // slot tiles per slot wave
 constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
+
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+
+// fp16 MFMAs of the state kernel from inline assembly (AGPR accumulators).
+// The first one of a slot tile starts with s_nop 1: its B fragment comes from
+// the VALU (the feature products), at most one instruction earlier.
+__device__ __forceinline__ void mfma16_first(f32x16& acc, const f16x8& a, const f16x8& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma16(f32x16& acc, const f16x8& a, const f16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
 
 template <int D, int DV, int NG>
 struct StateGrid {
@@ -315,6 +342,24 @@ struct StateGrid {
   static constexpr int NUW = NG * NUWB;        // slot waves per span
   static constexpr int NB = (NUW + 1 + 3) / 4;  // workgroups per span
 };
+
+// Largest |x| of the bf16 values in the 32-bit words of v, as a bf16 bit
+// pattern (the magnitude bits order like the magnitudes).
+__device__ __forceinline__ uint32_t absmax_bits(uint32_t m, uint4 v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
+    m = max(m, max(lo, hi));
+  }
+  return m;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = max(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), o)));
+  return x;
+}
 
 template <int D, int DV, int NG>
 __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restrict__ k,
@@ -331,18 +376,20 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   static_assert(UW % NXR == 0, "unit parity must be static");
   static_assert(G::MT == 2, "the slot loop issues the two dv tiles of a slot tile together");
   constexpr int KS = kTB2 / 16;                      // K-steps per staged block
-  // K is kept in LDS widened to fp32 (exact), so that the feature products
-  // are plain multiplies of LDS values.  Key row r of a K buffer starts at
-  // krow(r).  The slot tiles read rows r and r + DM/2 of a feature block in
-  // the same 16-lane phase of a ds_read_b128; with a uniform stride they
-  // would share banks, a gap of kGapK2 floats (32 banks) after every DM/2 rows
-  // moves alternate half-blocks to the other half of the banks.
-  constexpr int KBUFE = D * kRowK2 + (2 * NG - 1) * kGapK2;  // floats of one K buffer
-  constexpr unsigned KBUF = KBUFE * 4;               // bytes of one K buffer
+  // Key row r of a K buffer starts at krow(r) (fp16 elements).  The slot tiles
+  // read rows r and r + DM/2 of a feature block in the same 16-lane phase of a
+  // ds_read_b128; a gap of kGapK2 halves (32 banks) after every DM/2 rows moves
+  // alternate half-blocks to the other half of the banks.
+  constexpr int KBUFE = D * kRow2 + (2 * NG - 1) * kGapK2;  // halves of one K buffer
+  constexpr unsigned KBUF = KBUFE * 2;               // bytes of one K buffer
   constexpr unsigned VBUF = DV * kRow2 * 2;          // bytes of one V buffer
-  auto krow = [](int r) { return r * kRowK2 + (r / (DM / 2)) * kGapK2; };
-  __shared__ __attribute__((aligned(16))) float kT[kNBuf2][KBUFE];
-  __shared__ __attribute__((aligned(16))) uint16_t vT[kNBuf2][DV][kRow2];
+  auto krow = [](int r) { return r * kRow2 + (r / (DM / 2)) * kGapK2; };
+  // K and V buffers in one array: the record epilogue reuses it as a whole
+  constexpr int POOL = kNBuf2 * KBUFE + kNBuf2 * DV * kRow2;
+  __shared__ __attribute__((aligned(16))) uint16_t pool[POOL];
+  auto& kT = *reinterpret_cast<uint16_t(*)[kNBuf2][KBUFE]>(&pool[0]);
+  auto& vT = *reinterpret_cast<uint16_t(*)[kNBuf2][DV][kRow2]>(&pool[kNBuf2 * KBUFE]);
+  __shared__ uint32_t red[4];  // K and V magnitude maxima, non-finite flag
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -359,6 +406,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
   const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
   uint16_t* rec = spanst + static_cast<long long>(sp) * G::E;
+  uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
   const int nblk = static_cast<int>((span_end - span0 + kTB2 - 1) / kTB2);
 
   // staging: task -> (pair p of tokens, 8-wide column group cg); K then V
@@ -389,7 +437,13 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       }
     }
   };
-  auto commit = [&](int buf, long long t0, auto i0_c, auto i1_c) __attribute__((always_inline)) {
+  // Commit: write the fetched pairs into LDS as fp16 (times the span's scale
+  // when SC), and (vt) the bf16 V^T pairs of block bi into the span's V^T.
+  // Token pair (2p, 2p+1) of a 16-key group sits at position
+  // 16 (p / 8) + 8 ((p / 2) % 2) + 4 (p / 4 % 2) + 2 (p % 2) of the V^T row.
+  auto commit = [&](auto sc_c, int buf, long long t0, float sk, float sv, bool vt, int bi,
+                    auto i0_c, auto i1_c) __attribute__((always_inline)) {
+    constexpr bool SC = decltype(sc_c)::value;
 #pragma unroll
     for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
       const int cg = wave + 4 * i, p = lane;
@@ -398,31 +452,44 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       const uint32_t b[4] = {st_hi[i].x, st_hi[i].y, st_hi[i].z, st_hi[i].w};
       // v_perm byte selectors: 0-3 pick bytes of the second operand, 4-7 of
       // the first, 0x0c gives a zero byte; tokens at or past the span end
-      // become zeros
-      if (cg < KG) {
-        // K: dim 8cg+2e of tokens (2p, 2p+1) is (a.lo, b.lo) widened to fp32,
-        // dim 8cg+2e+1 is (a.hi, b.hi); rows 8cg .. 8cg+7 lie between two
-        // gaps (DM/2 is a multiple of 8)
-        const uint32_t lo_a = va ? 0x01000c0cu : 0x0c0c0c0cu, hi_a = va ? 0x03020c0cu : 0x0c0c0c0cu;
-        const uint32_t lo_b = vb ? 0x01000c0cu : 0x0c0c0c0cu, hi_b = vb ? 0x03020c0cu : 0x0c0c0c0cu;
-        float* base = &kT[buf][krow(8 * cg) + 2 * p];
+      // become zeros.  lo / hi: the low / high bf16 of a word as an fp32
+      // bit pattern.
+      const uint32_t lo_a = va ? 0x01000c0cu : 0x0c0c0c0cu, hi_a = va ? 0x03020c0cu : 0x0c0c0c0cu;
+      const uint32_t lo_b = vb ? 0x01000c0cu : 0x0c0c0c0cu, hi_b = vb ? 0x03020c0cu : 0x0c0c0c0cu;
+      const float scale = (cg < KG) ? sk : sv;
+      uint16_t* base = (cg < KG) ? &kT[buf][krow(8 * cg) + 2 * p]
+                                 : &vT[buf][8 * (cg - KG)][2 * p];
+      // rows 8cg .. 8cg+7 of a K buffer lie between two gaps (DM/2 is a
+      // multiple of 8), as do all rows of a V buffer
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          *reinterpret_cast<uint2*>(base + (2 * e) * kRowK2) =
-              make_uint2(__builtin_amdgcn_perm(0u, a[e], lo_a), __builtin_amdgcn_perm(0u, b[e], lo_b));
-          *reinterpret_cast<uint2*>(base + (2 * e + 1) * kRowK2) =
-              make_uint2(__builtin_amdgcn_perm(0u, a[e], hi_a), __builtin_amdgcn_perm(0u, b[e], hi_b));
+      for (int e = 0; e < 4; ++e) {
+        float xl = __uint_as_float(__builtin_amdgcn_perm(0u, a[e], lo_a));
+        float yl = __uint_as_float(__builtin_amdgcn_perm(0u, b[e], lo_b));
+        float xh = __uint_as_float(__builtin_amdgcn_perm(0u, a[e], hi_a));
+        float yh = __uint_as_float(__builtin_amdgcn_perm(0u, b[e], hi_b));
+        if constexpr (SC) {
+          xl *= scale;
+          yl *= scale;
+          xh *= scale;
+          yh *= scale;
         }
-      } else {
-        // V^T (bf16): element 2e is (a.lo, b.lo), 2e+1 (a.hi, b.hi)
+        // the conversions are exact in fp16's range (round-toward-zero only
+        // below it)
+        *reinterpret_cast<uint32_t*>(base + (2 * e) * kRow2) =
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(xl, yl));
+        *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2) =
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(xh, yh));
+      }
+      if (vt && cg >= KG) {
         const uint32_t sel_e = (va ? 0x0100u : 0x0c0cu) | (vb ? 0x05040000u : 0x0c0c0000u);
         const uint32_t sel_o = (va ? 0x0302u : 0x0c0cu) | (vb ? 0x07060000u : 0x0c0c0000u);
-        uint16_t* base = &vT[buf][8 * (cg - KG)][0];
+        const int pos = 16 * (p >> 3) + 8 * ((p >> 1) & 1) + 4 * ((p >> 2) & 1) + 2 * (p & 1);
+        uint16_t* dst = vt_rec + static_cast<long long>(8 * (cg - KG)) * LV + kTB2 * bi + pos;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          *reinterpret_cast<uint32_t*>(base + (2 * e) * kRow2 + 2 * p) =
+          *reinterpret_cast<uint32_t*>(dst + static_cast<long long>(2 * e) * LV) =
               __builtin_amdgcn_perm(b[e], a[e], sel_e);
-          *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2 + 2 * p) =
+          *reinterpret_cast<uint32_t*>(dst + static_cast<long long>(2 * e + 1) * LV) =
               __builtin_amdgcn_perm(b[e], a[e], sel_o);
         }
       }
@@ -430,10 +497,64 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   };
   using I0 = std::integral_constant<int, 0>;
   using IT = std::integral_constant<int, TPT>;
+  using Yes = std::true_type;
+  using No = std::false_type;
   static_assert(TPT <= KS, "one staging piece per K-step at most");
-  const char* kbase = reinterpret_cast<const char*>(&kT[0][0]);  // fp32 K buffers
+  const char* kbase = reinterpret_cast<const char*>(&kT[0][0]);  // fp16 K buffers
   const char* vbase = reinterpret_cast<const char*>(&vT[0][0][0]);
 
+  // ---- scales of the span --------------------------------------------------
+  if (tid < 4) red[tid] = 0u;
+  fetch(span0, I0{}, IT{});  // block 0, kept in the staging registers
+  uint32_t mk = 0u, mv = 0u;
+#pragma unroll
+  for (int i = 0; i < TPT; ++i) {
+    if (wave + 4 * i < KG) {
+      mk = absmax_bits(absmax_bits(mk, st_lo[i]), st_hi[i]);
+    } else {
+      mv = absmax_bits(absmax_bits(mv, st_lo[i]), st_hi[i]);
+    }
+  }
+  mk = wave_max_u32(mk);
+  mv = wave_max_u32(mv);
+  __syncthreads();
+  if (lane == 0) {
+    atomicMax(&red[0], mk);
+    atomicMax(&red[1], mv);
+  }
+  __syncthreads();
+  // bf16 exponent fields of the largest |k|, |v| of block 0 (255: inf / NaN)
+  int ek = static_cast<int>(red[0] >> 7), ev = static_cast<int>(red[1] >> 7);
+  const bool nonfinite_in = ek >= 255 || ev >= 255;
+  bool scaled = !nonfinite_in && !(ek >= 127 - 4 && ek < 127 + 4 && ev >= 127 - 8 && ev < 127 + 8);
+  // Exact maxima of the whole span (read once more; only for spans outside
+  // the unscaled range) -> exponents of the scales.
+  auto span_scales = [&]() __attribute__((always_inline)) {
+    uint32_t m2k = 0u, m2v = 0u;
+    const long long n16 = (span_end - span0) * ((D + DV) / 8);  // 16-byte pieces
+    for (long long j = tid; j < n16; j += 256) {
+      const long long t = span0 + j / ((D + DV) / 8);
+      const int pc = static_cast<int>(j % ((D + DV) / 8));
+      if (pc < KG) m2k = absmax_bits(m2k, *reinterpret_cast<const uint4*>(kh + t * D + 8 * pc));
+      else m2v = absmax_bits(m2v, *reinterpret_cast<const uint4*>(vh + t * DV + 8 * (pc - KG)));
+    }
+    m2k = wave_max_u32(m2k);
+    m2v = wave_max_u32(m2v);
+    __syncthreads();
+    if (tid < 2) red[tid] = 0u;
+    __syncthreads();
+    if (lane == 0) {
+      atomicMax(&red[0], m2k);
+      atomicMax(&red[1], m2v);
+    }
+    __syncthreads();
+    ek = static_cast<int>(red[0] >> 7);
+    ev = static_cast<int>(red[1] >> 7);
+    fetch(span0, I0{}, IT{});  // block 0 again, for the scaled pass
+  };
+  if (scaled) span_scales();
+
+  // ---- the span's passes ------------------------------------------------------
   // Three-deep ring: block bi is read from buffer bi % 3 while block bi+1 is
   // published into the next buffer piece by piece (staging task j of each
   // thread), and each piece's registers are refilled with block bi+2 right
@@ -441,257 +562,281 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   // Every block issues the same loads whether or not their data is used
   // (past the span's last block they re-read clamped, valid addresses), so the
   // count of loads in flight is the same on every path.
-  fetch(span0, I0{}, IT{});
-  commit(0, span0, I0{}, IT{});
-  fetch(span0 + kTB2, I0{}, IT{});
-  lds_barrier();
+  // (straight-line code, at most one unscaled and one scaled pass: a loop
+  // around the passes would keep every register of a pass live across it)
+  float fin = 0.f;  // sum of the written state: non-finite iff some value is
+  auto run = [&](auto sc_c, bool vt) __attribute__((always_inline)) {
+      constexpr bool SC = decltype(sc_c)::value;
+      // scales: 2^-e maps the largest |k| (|v|) of the span into [1, 2)
+      const int xk = SC ? max(ek, 1) - 127 : 0, xv = SC ? max(ev, 1) - 127 : 0;
+      const float sk = ldexpf(1.f, -xk), sv = ldexpf(1.f, -xv);
+      commit(sc_c, 0, span0, sk, sv, vt, 0, I0{}, IT{});
+      fetch(span0 + kTB2, I0{}, IT{});
+      lds_barrier();
 
-  if (gw >= SG::NUW) {
-    // ---- Z = K^T K over the span and the span's V^T (wave NUW) --------------
-    const bool zwave = gw == SG::NUW;
-    uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
-    // Z_blk = K_blk^T K_blk for each feature block: the diagonal ZMB x ZMB
-    // tile blocks of K^T K
-    constexpr int ZT = D / 32;  // 32-row tiles of K
-    f32x16 zacc[NG][G::ZMB][G::ZMB];
+      if (gw >= SG::NUW) {
+        // ---- Z = K^T K over the span (wave NUW) ---------------------------------
+        const bool zwave = gw == SG::NUW;
+        // Z_blk = K_blk^T K_blk for each feature block: the diagonal ZMB x ZMB
+        // tile blocks of K^T K
+        constexpr int ZT = D / 32;  // 32-row tiles of K
+        f32x16 zacc[NG][G::ZMB][G::ZMB];
 #pragma unroll
-    for (int bb = 0; bb < NG; ++bb)
+        for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-      for (int a = 0; a < G::ZMB; ++a)
+          for (int a = 0; a < G::ZMB; ++a)
 #pragma unroll
-        for (int b = 0; b < G::ZMB; ++b)
+            for (int b = 0; b < G::ZMB; ++b)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) zacc[bb][a][b][r] = 0.f;
-    for (int bi = 0; bi < nblk; ++bi) {
-      const int buf = bi % kNBuf2;
-      if (bi + 1 < nblk)
-        commit((bi + 1) % kNBuf2, span0 + static_cast<long long>(bi + 1) * kTB2, I0{}, IT{});
-      fetch(span0 + static_cast<long long>(bi + 2) * kTB2, I0{}, IT{});
-      if (zwave) {
+              for (int r = 0; r < 16; ++r) zacc[bb][a][b][r] = 0.f;
+        for (int bi = 0; bi < nblk; ++bi) {
+          const int buf = bi % kNBuf2;
+          if (bi + 1 < nblk)
+            commit(sc_c, (bi + 1) % kNBuf2, span0 + static_cast<long long>(bi + 1) * kTB2, sk,
+                   sv, vt, bi + 1, I0{}, IT{});
+          fetch(span0 + static_cast<long long>(bi + 2) * kTB2, I0{}, IT{});
+          if (zwave) {
 #pragma unroll
-        for (int i = 0; i < (DV * kTB2 / 8) / 64; ++i) {
-          const int task = lane + 64 * i;
-          const int m = task / (kTB2 / 8), h = task % (kTB2 / 8);  // row, chunk of 8 keys
-          const int grp = h >> 1, hg = h & 1;
-          const uint16_t* row = &vT[buf][m][16 * grp + 4 * hg];
-          const uint2 lo = *reinterpret_cast<const uint2*>(row);
-          const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
-          *reinterpret_cast<uint4*>(vt_rec + static_cast<long long>(m) * LV + kTB2 * bi + 8 * h) =
-              make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
+            for (int ks = 0; ks < KS; ++ks) {
+              f16x8 A[ZT];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          bf16x8 A[ZT];
+              for (int a = 0; a < ZT; ++a)
+                A[a] = *reinterpret_cast<const f16x8*>(&kT[buf][krow(32 * a + c) + 16 * ks + 8 * g]);
 #pragma unroll
-          for (int a = 0; a < ZT; ++a) {
-            // the fp32 values are bf16 values: keep their upper halves
-            const float* kr = &kT[buf][krow(32 * a + c) + 16 * ks + 8 * g];
-            const uint4 f0 = *reinterpret_cast<const uint4*>(kr);
-            const uint4 f1 = *reinterpret_cast<const uint4*>(kr + 4);
-            A[a] = __builtin_bit_cast(
-                bf16x8, make_uint4(__builtin_amdgcn_perm(f0.y, f0.x, 0x07060302u),
-                                   __builtin_amdgcn_perm(f0.w, f0.z, 0x07060302u),
-                                   __builtin_amdgcn_perm(f1.y, f1.x, 0x07060302u),
-                                   __builtin_amdgcn_perm(f1.w, f1.z, 0x07060302u)));
+              for (int bb = 0; bb < NG; ++bb)
+#pragma unroll
+                for (int a = 0; a < G::ZMB; ++a)
+#pragma unroll
+                  for (int b = 0; b < G::ZMB; ++b)
+                    zacc[bb][a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+                        A[bb * G::ZMB + a], A[bb * G::ZMB + b], zacc[bb][a][b], 0, 0, 0);
+            }
           }
+          lds_barrier();
+        }
+        if (zwave) {
 #pragma unroll
           for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-            for (int a = 0; a < G::ZMB; ++a)
+            for (int za = 0; za < G::ZMB; ++za)
 #pragma unroll
-              for (int b = 0; b < G::ZMB; ++b)
-                zacc[bb][a][b] = mfma32(A[bb * G::ZMB + a], A[bb * G::ZMB + b], zacc[bb][a][b]);
+              for (int zb = 0; zb < G::ZMB; ++zb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                  const int a = 32 * za + 8 * (r >> 2) + 4 * g + (r & 3);  // inside the block
+                  const int b = 32 * zb + c;
+                  float x = zacc[bb][za][zb][r];
+                  if constexpr (decltype(sc_c)::value) x = ldexpf(x, 2 * xk);
+                  fin += x;
+                  __bf16 h = static_cast<__bf16>(x);
+                  rec[G::ES + static_cast<long long>(bb) * DM * DM + zop_index<DM>(a, b)] =
+                      __builtin_bit_cast(uint16_t, h);
+                }
         }
+        return;
       }
-      lds_barrier();
-    }
-    if (zwave) {
-#pragma unroll
-      for (int bb = 0; bb < NG; ++bb)
-#pragma unroll
-        for (int za = 0; za < G::ZMB; ++za)
-#pragma unroll
-          for (int zb = 0; zb < G::ZMB; ++zb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int a = 32 * za + 8 * (r >> 2) + 4 * g + (r & 3);  // inside the block
-              const int b = 32 * zb + c;
-              __bf16 h = static_cast<__bf16>(zacc[bb][za][zb][r]);
-              rec[G::ES + static_cast<long long>(bb) * DM * DM + zop_index<DM>(a, b)] =
-                  __builtin_bit_cast(uint16_t, h);
-            }
-    }
-    return;
-  }
 
-  // ---- S_span^T = V^T Phi(K) for this wave's slot tiles ----------------------
-  // slot wave gw covers tiles [unit0, unit0 + UW) of feature block blk (tiles
-  // past the block's last one are computed on a valid row and not stored)
-  const int blk = gw / SG::NUWB;
-  const int unit0 = (gw % SG::NUWB) * UW;
-  // per-lane byte offsets of the fragments inside buffer 0, column 8*g
-  unsigned xo[NXR], yo[UW], vo[G::MT];
+      // ---- S_span^T = V^T Phi(K) for this wave's slot tiles --------------------
+      // slot wave gw covers tiles [unit0, unit0 + UW) of feature block blk
+      // (tiles past the block's last one are computed on a valid row and not
+      // stored)
+      const int blk = gw / SG::NUWB;
+      const int unit0 = (gw % SG::NUWB) * UW;
+      // per-lane byte offsets of the fragments inside buffer 0, column 8*g
+      unsigned xo[NXR], yo[UW], vo[G::MT];
 #pragma unroll
-  for (int p = 0; p < NXR; ++p) {
-    int xr, yy;
-    slot_pair<DM>(32 * p + c, xr, yy);
-    xo[p] = static_cast<unsigned>((krow(DM * blk + xr) + 8 * g) * 4);
-  }
+      for (int p = 0; p < NXR; ++p) {
+        int xr, yy;
+        slot_pair<DM>(32 * p + c, xr, yy);
+        xo[p] = static_cast<unsigned>((krow(DM * blk + xr) + 8 * g) * 2);
+      }
 #pragma unroll
-  for (int u = 0; u < UW; ++u) {
-    int xx, yr;
-    const int unit = unit0 + u < G::NSTM ? unit0 + u : G::NSTM - 1;  // valid row; store skipped
-    slot_pair<DM>(32 * unit + c, xx, yr);
-    yo[u] = static_cast<unsigned>((krow(DM * blk + yr) + 8 * g) * 4);
-  }
-#pragma unroll
-  for (int m = 0; m < G::MT; ++m) vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
-
-  f32x16 acc[UW][G::MT];
-#pragma unroll
-  for (int u = 0; u < UW; ++u)
-#pragma unroll
-    for (int m = 0; m < G::MT; ++m)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
-
-  // LDS fragments: the y rows of the slot tiles (8 fp32 tokens each, reloaded
-  // for the next K-step as soon as the features they feed are computed), the
-  // x rows (reloaded for the next K-step after their last use in this one)
-  // and V^T double buffered by K-step parity.
-  struct F8 {
-    float v[8];
-  };
-  F8 fy[UW], fx[NXR];
-  uint4 fv[2][G::MT];
-  auto ld8 = [](const char* p) __attribute__((always_inline)) {
-    const uint4 a = *reinterpret_cast<const uint4*>(p);
-    const uint4 b = *reinterpret_cast<const uint4*>(p + 16);
-    F8 r;
-    r.v[0] = __uint_as_float(a.x);
-    r.v[1] = __uint_as_float(a.y);
-    r.v[2] = __uint_as_float(a.z);
-    r.v[3] = __uint_as_float(a.w);
-    r.v[4] = __uint_as_float(b.x);
-    r.v[5] = __uint_as_float(b.y);
-    r.v[6] = __uint_as_float(b.z);
-    r.v[7] = __uint_as_float(b.w);
-    return r;
-  };
-  auto ldv = [&](int set, const char* vb, unsigned ko) __attribute__((always_inline)) {
-#pragma unroll
-    for (int m = 0; m < G::MT; ++m) fv[set][m] = *reinterpret_cast<const uint4*>(vb + vo[m] + ko);
-  };
-  auto pack8 = [](const float pr[8]) __attribute__((always_inline)) {
-    return __builtin_bit_cast(
-        bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                           pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
-  };
-  // tile u of a K-step computes the features of tile u+1, whose x row has
-  // parity (u+1) % NXR; the x row of parity p is reloaded for the next K-step
-  // after xlast(p), the last tile of this K-step that uses it
-  auto xlast = [](int p) {
-    int last = -1;
-    for (int u = 0; u + 1 < UW; ++u)
-      if ((u + 1) % NXR == p) last = u;
-    return last;
-  };
-  // Per staged block: publish block bi+1 and fetch block bi+2 piece by piece;
-  // the features of tile u+1 are computed under the MFMAs of tile u (the
-  // block's first tile beforehand).
-  for (int bi = 0; bi < nblk; ++bi) {
-    const int buf = bi % kNBuf2;
-    const int nbuf = (bi + 1) % kNBuf2;
-    const char* kb = kbase + buf * KBUF;
-    const char* vb = vbase + buf * VBUF;
-    const bool more1 = bi + 1 < nblk;
-    const long long t1 = span0 + static_cast<long long>(bi + 1) * kTB2;
-    const long long t2 = t1 + kTB2;
-    ldv(0, vb, 0u);
-#pragma unroll
-    for (int p = 0; p < NXR; ++p) fx[p] = ld8(kb + xo[p]);
-#pragma unroll
-    for (int u = 0; u < UW; ++u) fy[u] = ld8(kb + yo[u]);
-    // B fragments: bq[0] the next tile's, bq[1], bq[2] the two before (kept
-    // live so that a new fragment never reuses the registers of an MFMA that
-    // may still be running, see hold)
-    bf16x8 bq[3];
-    {
-      float pr[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) pr[j] = fx[0].v[j] * fy[0].v[j];
-      bq[0] = pack8(pr);
-    }
-    bq[1] = bq[0];
-    bq[2] = bq[0];
-    auto push = [&](const float pr[8]) __attribute__((always_inline)) {
-      bq[2] = bq[1];
-      bq[1] = bq[0];
-      bq[0] = pack8(pr);
-      hold(bq[1], bq[2]);
-    };
-    static_for<0, KS>([&](auto ks_c) {
-      constexpr int ks = decltype(ks_c)::value;
-      constexpr int cur = ks & 1;
-      constexpr unsigned kn = 64u * (ks + 1);  // byte column of K-step ks+1 (16 fp32)
-      constexpr unsigned vn = 32u * (ks + 1);  // ... in the bf16 V^T rows
-      static_for<0, TPT>([&](auto j_c) {  // staging piece j at K-step j*KS/TPT
-        constexpr int j = decltype(j_c)::value;
-        if constexpr (j * KS / TPT == ks) {
-          using J = std::integral_constant<int, j>;
-          using J1 = std::integral_constant<int, j + 1>;
-          if (more1) commit(nbuf, t1, J{}, J1{});
-          fetch(t2, J{}, J1{});
-        }
-      });
-      const bf16x8 va0 = __builtin_bit_cast(bf16x8, fv[cur][0]);
-      const bf16x8 va1 = __builtin_bit_cast(bf16x8, fv[cur][1]);
-      static_for<0, UW>([&](auto u_c) {
-        constexpr int u = decltype(u_c)::value;
-        // fy[u] fed the features of (ks, u): reload it for (ks+1, u)
-        if constexpr (ks + 1 < KS && u > 0) fy[u] = ld8(kb + yo[u] + kn);
-        if constexpr (u + 1 < UW) {
-          float pr[8];
-          mfma2_prod8(acc[u][0], acc[u][1], va0, va1, bq[0], fx[(u + 1) % NXR].v,
-                      fy[u + 1].v, pr);
-          push(pr);
-          if constexpr (ks + 1 < KS && u == 0) fy[0] = ld8(kb + yo[0] + kn);
-          // V^T of K-step ks+1 into the other buffer, whose last readers (the
-          // previous K-step's final tile) are two tiles old now
-          if constexpr (ks + 1 < KS && u == 1) ldv(cur ^ 1, vb, vn);
-          if constexpr (ks + 1 < KS) {
-#pragma unroll
-            for (int p = 0; p < NXR; ++p)
-              if (u == xlast(p)) fx[p] = ld8(kb + xo[p] + kn);
-          }
-        } else if constexpr (ks + 1 < KS) {
-          float pr[8];
-          mfma2_prod8(acc[u][0], acc[u][1], va0, va1, bq[0], fx[0].v, fy[0].v, pr);
-          push(pr);
-        } else {
-          mfma2(acc[u][0], acc[u][1], va0, va1, bq[0]);
-        }
-      });
-    });
-    lds_barrier();
-  }
-  mfma_drain();
-
-  // write this wave's tiles of the span record (bf16)
-#pragma unroll
-  for (int u = 0; u < UW; ++u) {
-    const int unit = blk * G::NSTM + unit0 + u;  // tile of the whole record
-    if (unit0 + u < G::NSTM) {
+      for (int u = 0; u < UW; ++u) {
+        int xx, yr;
+        const int unit = unit0 + u < G::NSTM ? unit0 + u : G::NSTM - 1;  // valid row; no store
+        slot_pair<DM>(32 * unit + c, xx, yr);
+        yo[u] = static_cast<unsigned>((krow(DM * blk + yr) + 8 * g) * 2);
+      }
 #pragma unroll
       for (int m = 0; m < G::MT; ++m)
+        vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
+
+      f32x16 acc[UW][G::MT];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int dvrow = 32 * m + 8 * (r >> 2) + 4 * g + (r & 3);
-          __bf16 h = static_cast<__bf16>(acc[u][m][r]);
-          rec[static_cast<long long>(dvrow) * G::NSLOT + 32 * unit + c] =
-              __builtin_bit_cast(uint16_t, h);
+      for (int u = 0; u < UW; ++u)
+#pragma unroll
+        for (int m = 0; m < G::MT; ++m) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
+          asm volatile("" : "+a"(acc[u][m]));
         }
+
+      // LDS fragments: the y rows of the slot tiles (8 fp16 tokens each,
+      // reloaded for the next K-step as soon as the features they feed are
+      // computed), the x rows (reloaded for the next K-step after their last
+      // use in this one) and V^T double buffered by K-step parity.
+      f16x8 fy[UW], fx[NXR], fv[2][G::MT];
+      auto ld16 = [](const char* p) __attribute__((always_inline)) {
+        return *reinterpret_cast<const f16x8*>(p);
+      };
+      auto ldv = [&](int set, const char* vb, unsigned ko) __attribute__((always_inline)) {
+#pragma unroll
+        for (int m = 0; m < G::MT; ++m) fv[set][m] = ld16(vb + vo[m] + ko);
+      };
+      // tile u of a K-step computes the features of tile u+1, whose x row has
+      // parity (u+1) % NXR; the x row of parity p is reloaded for the next
+      // K-step after xlast(p), the last tile of this K-step that uses it
+      auto xlast = [](int p) {
+        int last = -1;
+        for (int u = 0; u + 1 < UW; ++u)
+          if ((u + 1) % NXR == p) last = u;
+        return last;
+      };
+      // Per staged block: publish block bi+1 and fetch block bi+2 piece by
+      // piece; the features of tile u+1 are computed between the two MFMAs of
+      // tile u (the block's first tile beforehand).
+      for (int bi = 0; bi < nblk; ++bi) {
+        const int buf = bi % kNBuf2;
+        const int nbuf = (bi + 1) % kNBuf2;
+        const char* kb = kbase + buf * KBUF;
+        const char* vb = vbase + buf * VBUF;
+        const bool more1 = bi + 1 < nblk;
+        const long long t1 = span0 + static_cast<long long>(bi + 1) * kTB2;
+        const long long t2 = t1 + kTB2;
+        ldv(0, vb, 0u);
+#pragma unroll
+        for (int p = 0; p < NXR; ++p) fx[p] = ld16(kb + xo[p]);
+#pragma unroll
+        for (int u = 0; u < UW; ++u) fy[u] = ld16(kb + yo[u]);
+        // B fragments: bq[0] the next tile's, bq[1], bq[2] the two before
+        // (kept live so that a new fragment never reuses the registers of an
+        // MFMA that may still be running, see hold)
+        f16x8 bq[3];
+        bq[0] = fx[0] * fy[0];
+        bq[1] = bq[0];
+        bq[2] = bq[0];
+        auto push = [&](const f16x8& nb) __attribute__((always_inline)) {
+          bq[2] = bq[1];
+          bq[1] = bq[0];
+          bq[0] = nb;
+          hold(bq[1], bq[2]);
+        };
+        static_for<0, KS>([&](auto ks_c) {
+          constexpr int ks = decltype(ks_c)::value;
+          constexpr int cur = ks & 1;
+          constexpr unsigned kn = 32u * (ks + 1);  // byte column of K-step ks+1 (16 fp16)
+          static_for<0, TPT>([&](auto j_c) {  // staging piece j at K-step j*KS/TPT
+            constexpr int j = decltype(j_c)::value;
+            if constexpr (j * KS / TPT == ks) {
+              using J = std::integral_constant<int, j>;
+              using J1 = std::integral_constant<int, j + 1>;
+              if (more1) commit(sc_c, nbuf, t1, sk, sv, vt, bi + 1, J{}, J1{});
+              fetch(t2, J{}, J1{});
+            }
+          });
+          const f16x8 va0 = fv[cur][0];
+          const f16x8 va1 = fv[cur][1];
+          static_for<0, UW>([&](auto u_c) {
+            constexpr int u = decltype(u_c)::value;
+            // fy[u] fed the features of (ks, u): reload it for (ks+1, u)
+            if constexpr (ks + 1 < KS && u > 0) fy[u] = ld16(kb + yo[u] + kn);
+            if constexpr (u + 1 < UW || ks + 1 < KS) {
+              // the next tile's features (tile u+1 of this K-step, or tile 0
+              // of the next one), half before and half after the first MFMA:
+              // the next tile's first MFMA then comes three instructions
+              // after the last product it reads (two wait states needed),
+              // so no s_nop is needed there
+              constexpr int un = (u + 1 < UW) ? u + 1 : 0;
+              mfma16_first(acc[u][0], va0, bq[0]);
+              __builtin_amdgcn_sched_barrier(0);
+              const f16x8 nb = fx[un % NXR] * fy[un];
+              __builtin_amdgcn_sched_barrier(0);
+              mfma16(acc[u][1], va1, bq[0]);
+              __builtin_amdgcn_sched_barrier(0);
+              push(nb);
+            } else {
+              // the block's last tile: its features are one instruction old
+              mfma16_first(acc[u][0], va0, bq[0]);
+              mfma16(acc[u][1], va1, bq[0]);
+            }
+            if constexpr (u + 1 < UW && ks + 1 < KS) {
+              if constexpr (u == 0) fy[0] = ld16(kb + yo[0] + kn);
+              // V^T of K-step ks+1 into the other buffer, whose last readers
+              // (the previous K-step's final tile) are two tiles old now
+              if constexpr (u == 1) ldv(cur ^ 1, vb, kn);
+#pragma unroll
+              for (int p = 0; p < NXR; ++p)
+                if (u == xlast(p)) fx[p] = ld16(kb + xo[p] + kn);
+            }
+          });
+        });
+        lds_barrier();
+      }
+      mfma_drain();
+
+      // Write this wave's tiles of the span record (bf16), undoing the scales.
+      // The accumulators hold 4 consecutive dv rows of one slot per lane; they
+      // go through LDS (this wave's own region of the free staging buffers,
+      // [dv][HU*32 + 8] bf16, HU tiles at a time) so that the record is
+      // written in 16-byte pieces of 8 consecutive slots.
+      constexpr int HU = UW / 2;       // tiles per round
+      constexpr int RS = HU * 32 + 8;  // bf16 per LDS row (16-byte aligned rows)
+      static_assert(UW % 2 == 0 && 4 * DV * RS <= POOL, "record rounds fit the staging LDS");
+      uint16_t* ep = &pool[wave * DV * RS];
+      constexpr int CPR = HU * 4;  // 16-byte pieces per row and round
+      static_for<0, 2>([&](auto h_c) {
+        constexpr int h = decltype(h_c)::value;
+#pragma unroll
+        for (int uu = 0; uu < HU; ++uu) {
+          const int u = h * HU + uu;
+#pragma unroll
+          for (int m = 0; m < G::MT; ++m)
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+              const int dvrow = 32 * m + 8 * (r >> 2) + 4 * g + (r & 3);
+              float x0 = acc[u][m][r], x1 = acc[u][m][r + 1];
+              if constexpr (decltype(sc_c)::value) {
+                x0 = ldexpf(x0, 2 * xk + xv);
+                x1 = ldexpf(x1, 2 * xk + xv);
+              }
+              if (unit0 + u < G::NSTM) fin += x0 + x1;
+              const uint32_t w = pack_bf16x2(x0, x1);  // rows dvrow, dvrow + 1
+              ep[dvrow * RS + 32 * uu + c] = static_cast<uint16_t>(w);
+              ep[(dvrow + 1) * RS + 32 * uu + c] = static_cast<uint16_t>(w >> 16);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int i = 0; i < DV * CPR / 64; ++i) {
+          const int kc = lane + 64 * i;
+          const int row = kc / CPR, pc = kc % CPR;
+          const uint4 w = *reinterpret_cast<const uint4*>(ep + row * RS + 8 * pc);
+          if (unit0 + h * HU + pc / 4 < G::NSTM)
+            *reinterpret_cast<uint4*>(rec + static_cast<long long>(row) * G::NSLOT +
+                                      32 * (blk * G::NSTM + unit0 + h * HU) + 8 * pc) = w;
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // reads done before the next round's writes
+        __builtin_amdgcn_wave_barrier();
+      });
+  };
+  if (!scaled) {
+    run(No{}, part == 0);
+    // A non-finite state from finite inputs means an fp16 overflow in the
+    // unscaled pass: run the span again with its scales.
+    if (!nonfinite_in) {
+      const bool bad = !(fabsf(fin) <= 3.0e38f);
+      __syncthreads();
+      if (bad) red[2] = 1u;
+      __syncthreads();
+      if (red[2] != 0u) {
+        scaled = true;
+        span_scales();
+        run(Yes{}, false);
+      }
     }
+  } else {
+    run(Yes{}, part == 0);
   }
 }
 

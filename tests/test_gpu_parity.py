@@ -305,3 +305,34 @@ def test_decode_full_size_sampled(kata, orc):
         ref = orc.fwd_rows(qc, kc, vc, np.zeros_like(rows), rows)
         assert_bf16_close(got[b, h], ref, f"decode head {bh}")
         assert float(np.max(row_rel_err(got[b, h], ref))) < 1e-4
+
+
+# ---------------------------------------------------------------------------
+# input magnitudes: the MFMA path's state products are fp16 with per-span
+# power-of-two scales; every case must match the oracle at the same bar
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("ks,vs", [(300.0, 1.0), (2.0 ** -10, 1.0), (1.0, 3.0e4), (1.0, 1e-6),
+                                   (2.0 ** -40, 2.0 ** 20), (50.0, 200.0), (4.0, 50.0)])
+def test_input_magnitudes(kata, orc, ks, vs):
+    log(f"case magnitudes k x {ks:g}, v x {vs:g}: B1 H2 T2500 d64 C64")
+    rng = np.random.default_rng(71)
+    q, k, v = workloads.gaussian_qkv(rng, 1, 2, 2500, 64, 64)
+    (qv, kv, vv), (qd, kd, vd) = workloads._finish([q, k * np.float32(ks), v * np.float32(vs)],
+                                                   "bf16")
+    got = _run_fwd(kata, dict(q_dev=qd, k_dev=kd, v_dev=vd), "bf16", 64)
+    assert_bf16_close(got, orc.fwd(qv, kv, vv), f"k x {ks:g}, v x {vs:g}")
+
+
+def test_later_block_outgrows_first(kata, orc):
+    # the first 128 keys of every span are unit vectors, later keys are 2000x
+    # larger (their fp16 feature products overflow without a scale): the
+    # span is redone with its exact scales
+    log("case later keys 2000x the first block's: B1 H2 T3000 d64 C64")
+    rng = np.random.default_rng(72)
+    q, k, v = workloads.gaussian_qkv(rng, 1, 2, 3000, 64, 64)
+    big = (np.arange(3000) % 1024) >= 128
+    k = k * np.where(big, np.float32(2000.0), np.float32(1.0))[None, None, :, None]
+    (qv, kv, vv), (qd, kd, vd) = workloads._finish([q, k, v], "bf16")
+    got = _run_fwd(kata, dict(q_dev=qd, k_dev=kd, v_dev=vd), "bf16", 64)
+    assert_bf16_close(got, orc.fwd(qv, kv, vv), "later keys 2000x")
