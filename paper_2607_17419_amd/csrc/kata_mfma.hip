@@ -996,33 +996,6 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     tlive[i] = tq0[i] < span_end;
   }
 
-  // bf16 query fragments for the d-contractions, per feature block:
-  // qf[i][KZM*bb + kz] holds q[t][DM*bb + 8*kz + RM*g .. +7] of this lane's
-  // query t = tq0 + c (with one block: q[t][8*kz + R*g ..]).
-  bf16x8 qf[NQ][G::KZ];
-#pragma unroll
-  for (int i = 0; i < NQ; ++i) {
-    const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
-#pragma unroll
-    for (int kz = 0; kz < G::KZ; ++kz)
-      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + DM * (kz / KZM) +
-                                                   8 * (kz % KZM) + RM * g);
-  }
-
-  // Z_pre operand fragments of each feature block (see below)
-  bf16x8 zA[NG][G::ZMB][KZM];
-  if constexpr (!QUAD) {
-#pragma unroll
-    for (int bb = 0; bb < NG; ++bb) {
-      const uint16_t* zop = rec + G::ES + static_cast<long long>(bb) * DM * DM;
-#pragma unroll
-      for (int m = 0; m < G::ZMB; ++m)
-#pragma unroll
-        for (int kz = 0; kz < KZM; ++kz)
-          zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * KZM + kz) * 64 + lane) * 8);
-    }
-  }
-
   // ---- staging copies of both phases ------------------------------------------
   // Stages cover the key blocks of the workgroup's last live tile; every
   // wave runs all of them (the stage barriers are workgroup-wide).
@@ -1084,17 +1057,50 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       g2lds16(rec + 16 * kKC * stg + off, buf + (i * W + wave) * 512);
     }
   };
-  // The query and Z fragments are in registers before any copy is issued:
-  // copies are not counted by the compiler's waits, and a wait for a load
-  // issued before them must not wait for them.  From here on the only vector
-  // memory operations are copies (and the final stores).
-  wait_vmcnt<0>();
+  // Stage 0 of the in-span phase is issued first and the query and Z
+  // fragments are loaded behind it; the workgroup waits for that one memory
+  // round trip (the compiler's wait before the empty asm below: loads
+  // complete in order, so it also covers the copies issued before them), and
+  // only then issues the in-span stage 1 and the readout's stages 0 and 1,
+  // which arrive under the first stage's work.  From here on the only vector
+  // memory operations in flight are copies (and the final stores), which the
+  // pipeline's own waits count.
+  issue_i(0, g_stage0);
+
+  // bf16 query fragments for the d-contractions, per feature block:
+  // qf[i][KZM*bb + kz] holds q[t][DM*bb + 8*kz + RM*g .. +7] of this lane's
+  // query t = tq0 + c (with one block: q[t][8*kz + R*g ..]).
+  bf16x8 qf[NQ][G::KZ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
+#pragma unroll
+    for (int kz = 0; kz < G::KZ; ++kz)
+      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + DM * (kz / KZM) +
+                                                   8 * (kz % KZM) + RM * g);
+  }
+
+  // Z_pre operand fragments of each feature block (see below)
+  bf16x8 zA[NG][G::ZMB][KZM];
+  if constexpr (!QUAD) {
+#pragma unroll
+    for (int bb = 0; bb < NG; ++bb) {
+      const uint16_t* zop = rec + G::ES + static_cast<long long>(bb) * DM * DM;
+#pragma unroll
+      for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+        for (int kz = 0; kz < KZM; ++kz)
+          zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * KZM + kz) * 64 + lane) * 8);
+    }
+  }
+
+  asm volatile("" ::"v"(qf[0][0]), "v"(qf[NQ - 1][G::KZ - 1]));
+  if constexpr (!QUAD) asm volatile("" ::"v"(zA[0][0][0]), "v"(zA[NG - 1][G::ZMB - 1][KZM - 1]));
+  if (nstage > 1) issue_i(1, g_stage1);
   if constexpr (!QUAD) {
     issue_r(std::integral_constant<int, 0>{});
     if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
   }
-  issue_i(0, g_stage0);
-  if (nstage > 1) issue_i(1, g_stage1);
 
   // The P V / readout accumulators live in AGPRs from here to the stores.
   // The empty asm makes the zeros exist here: otherwise the compiler writes
@@ -1322,8 +1328,7 @@ __global__ __launch_bounds__(256) void span_output_kernel(
     const char* b0 = reinterpret_cast<const char*>(g_stage0);
     const char* b1 = reinterpret_cast<const char*>(g_stage1);
     const char* b2 = reinterpret_cast<const char*>(g_stage2);
-    // stage 0 (copies issued at the start, after the readout's first two)
-    if (nstage > 1) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
+    // stage 0 (its copies were waited for with the query fragments)
     lds_barrier();
     if (nstage > 2) issue_i(2, g_stage2);
     ldA(b0, integral_constant<int, 0>{}, A[0]);
@@ -1415,8 +1420,9 @@ __global__ __launch_bounds__(256) void span_output_kernel(
             none);
       hold(bx[0]);
     }
-    mfma_drain();   // the P V accumulators are moved by compiler code next
-    lds_barrier();  // every wave is done with the intra buffers
+    mfma_drain();    // the P V accumulators are moved by compiler code next
+    wait_vmcnt<0>();  // the readout's first stages (a single in-span stage waits for nothing)
+    lds_barrier();   // every wave is done with the intra buffers
   }
 
   // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
