@@ -111,6 +111,132 @@ def algorithmic(w, L, g=1):
                 total_flop=state + output)
 
 
+def bench_fwd(kata, dev, hip, w, steps, warmup, span=0, inp=None):
+    """Chunked forward of workload `w` (inputs resident on the device): wall
+    time per step over `steps` calls after `warmup`, and per-stage times from
+    the HIP events the library records on the launch stream between its three
+    kernels (span / chunk state, associative scan, output)."""
+    import torch
+    if inp is None:
+        import workloads
+        inp = workloads.make_inputs(w)
+    q = upload(inp["q_dev"], w.dtype, dev)
+    k = upload(inp["k_dev"], w.dtype, dev)
+    v = upload(inp["v_dev"], w.dtype, dev)
+    code = kata.KATA_BF16 if w.dtype == "bf16" else kata.KATA_F32
+    span = span or kata.default_span(w.B, w.H, w.T, w.d, w.dv, w.C, code)
+    L = min(span * w.C, -(-w.T // w.C) * w.C)
+    out = torch.empty((w.B, w.H, w.T, w.dv), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(256, kata.workspace_bytes(w.B, w.H, w.T, w.d, w.dv, w.C, code, span)),
+                     dtype=torch.uint8, device=dev)
+    ev = Events(hip, 4 * max(steps, warmup))
+    for i in range(warmup):
+        kata.fwd_chunked_timed(q, k, v, w.C, ev.block(4 * i), span_chunks=span, out=out,
+                               workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        kata.fwd_chunked_timed(q, k, v, w.C, ev.block(4 * i), span_chunks=span, out=out,
+                               workspace=ws)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    names = ("span_state", "scan", "span_output")
+    stage = {nm: sum(ev.elapsed(4 * i + j, 4 * i + j + 1) for i in range(steps)) / steps
+             for j, nm in enumerate(names)}
+    ev.close()
+    ms = 1e3 * elapsed / steps
+    res = {"ms": ms, "stage": stage, "span": span, "L": L, "code": code}
+    return res, (q, k, v)
+
+
+def fwd_row(w, r):
+    """Summary of one forward workload: tokens/s, stage times, and on the bf16
+    MFMA path the MFMA fractions of the state and output kernels (algorithmic
+    flops) and the scan's HBM rate (algorithmic bytes)."""
+    alg = algorithmic(w, r["L"])
+    st = r["stage"]
+    row = {"workload": f"{w.name}: {w.note}", "tokens_per_s": w.B * w.T / (r["ms"] * 1e-3),
+           "ms_per_step": round(r["ms"], 4), "kernel_ms": round(sum(st.values()), 4),
+           "span_chunks": r["span"], "stages_ms": {nm: round(t, 4) for nm, t in st.items()}}
+    if w.dtype == "bf16":
+        def mf(flop, t_ms):
+            tf = flop / (t_ms * 1e-3) / 1e12
+            return {"bound": "mfma", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+        gbs = alg["scan_bytes"] / (st["scan"] * 1e-3) / 1e9
+        row["stage_roofline"] = {
+            "span_state": mf(alg["state_flop"], st["span_state"]),
+            "span_output": mf(alg["output_flop"], st["span_output"]),
+            "scan": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}}
+        row["mfma_frac_end_to_end"] = round(
+            alg["total_flop"] / (r["ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        row["algorithmic_gflop_per_step"] = round(alg["total_flop"] / 1e9, 2)
+    else:
+        row["note"] = ("fp32 inputs run on the fp32 VALU path (per-chunk states); "
+                       "latency-bound at this size, reported as time per call")
+    return row
+
+
+def bench_configs(kata, dev, hip, names=("tiny_f32", "mid_bf16", "recall_bf16"), steps=20,
+                  warmup=5):
+    """The other forward workloads, each in the library's default launch
+    configuration (default span), on their seeded inputs."""
+    import torch
+    import workloads
+    out = {}
+    for nm in names:
+        w = workloads.WORKLOADS[nm]
+        r, tensors = bench_fwd(kata, dev, hip, w, steps, warmup)
+        out[nm] = fwd_row(w, r)
+        del tensors
+        torch.cuda.empty_cache()
+    return out
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _single_thread_rate(workload, seconds):
+    """The oracle on one thread (a child process with OMP_NUM_THREADS=1, so the
+    OpenMP runtime of this process keeps its setting): evenly spaced rows of
+    the workload's heads for about `seconds`, extrapolated like the main
+    sample.  Returns (tokens/s, rows, elapsed s)."""
+    import subprocess
+    code = f"""
+import sys, time, json
+sys.path.insert(0, {ROOT!r})
+import numpy as np, oracle, workloads
+w = workloads.WORKLOADS[{workload!r}]
+inp = workloads.make_inputs(w, B=1, H=1)  # one head of the same recipe: the rows' cost
+orc = oracle.Oracle()
+q, k, v = (np.ascontiguousarray(inp[n], dtype=np.float64) for n in ("q", "k", "v"))
+BH = w.B * w.H
+t0 = time.perf_counter(); orc.fwd_rows(q, k, v, np.zeros(1, np.int64), np.full(1, w.T - 1)); cal = time.perf_counter() - t0
+R = max(1, min(int({seconds} / max(cal / w.T * (w.T / 2.0), 1e-12)), w.T))
+rows = ((np.arange(R) + 0.5) * w.T / R).astype(np.int64)
+bh = np.zeros(R, np.int64)
+t0 = time.perf_counter(); orc.fwd_rows(q, k, v, bh, rows); el = time.perf_counter() - t0
+units = float(np.sum(rows + 1)); full = BH * w.T * (w.T + 1) / 2.0
+print(json.dumps({{"rate": (w.B * w.T) / (el * full / units), "rows": int(R), "elapsed": el,
+                  "threads": orc.num_threads()}}))
+"""
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                       timeout=max(120, 8 * seconds))
+    if r.returncode != 0:
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def cpu_baseline(w, inp, seconds):
     import numpy as np
     import oracle
@@ -148,14 +274,21 @@ def cpu_baseline(w, inp, seconds):
             break
     full_units = BH * w.T * (w.T + 1) / 2.0
     full_time = el * full_units / sample_units
+    single = _single_thread_rate(w.name, max(2.0, seconds / 3.0))
     return {
         "value": (w.B * w.T) / full_time,
         "unit": "tokens/s",
         "cores": orc.num_threads(),
         "kind": "oracle",
+        "cpu_model": _cpu_model(),
         "sample": (f"{nrows} rows ({rdone} spread over the sequence per head x {BH} heads) of "
-                   f"the fp64 O(T^2) definition on the same inputs, {el:.1f} s; full-workload "
-                   f"time extrapolated by the summed row lengths ({full_time:.3g} s)"),
+                   f"the fp64 O(T^2) definition on the same inputs, {el:.1f} s on "
+                   f"{orc.num_threads()} OpenMP threads; full-workload time extrapolated by the "
+                   f"summed row lengths ({full_time:.3g} s)"),
+        "single_thread": None if single is None else {
+            "value": single["rate"], "unit": "tokens/s", "threads": single["threads"],
+            "sample": (f"{single['rows']} evenly spaced rows of head 0 on one thread, "
+                       f"{single['elapsed']:.1f} s, extrapolated the same way")},
     }
 
 
@@ -188,6 +321,12 @@ def bench_decode(kata, dev, hip):
     bytes_step = w.B * w.H * (2 * (n * w.dv + n) * 4 + (2 * w.d + w.dv) * 2 + w.dv * 4)
     avg = sum(per_step) / len(per_step)
     gbs = bytes_step / (avg * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            ent = json.load(f).get("decode_step", {})
+        if ent.get("source_sha") == source_sha(("kata_fp32.hip", "kata_common.hpp")):
+            traffic = ent.get("hbm_bytes_per_launch")
     return {
         "workload": f"decode_bf16: {w.note}",
         "tokens_per_s": w.B * w.steps / el,
@@ -195,7 +334,7 @@ def bench_decode(kata, dev, hip):
         "kernel_ms_per_step": avg,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "algorithmic_bytes_per_launch": bytes_step},
+                     "algorithmic_bytes_per_launch": bytes_step, "traffic": traffic},
     }
 
 
@@ -610,11 +749,20 @@ def ingest_traffic(root, workload, span):
         kib, nd = _per_dispatch(rows, cnt, name)
         cal[cnt] = {"copy_kernel": name[:80], "kib_per_dispatch": kib, "dispatches": nd,
                     "factor": COPY_BYTES / (kib * 1024.0)}
-    res = {"source_sha": source_sha(), "workload": workload, "span_chunks": span,
-           "calibration": {"copy_bytes": COPY_BYTES, **cal}}
-    fetch_rows = _counter_rows(os.path.join(root, "fetch"))
-    write_rows = _counter_rows(os.path.join(root, "write"))
-    for key, match in KERNELS.items():
+    # sections whose counter runs are not under `root` keep their earlier entries
+    res = {}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            res = json.load(fh)
+    res["calibration"] = {"copy_bytes": COPY_BYTES, **cal}
+    m1 = os.path.isdir(os.path.join(root, "fetch")) and os.path.isdir(os.path.join(root, "write"))
+    if m1:
+        for key in KERNELS:
+            res.pop(key, None)
+        res.update({"source_sha": source_sha(), "workload": workload, "span_chunks": span})
+    fetch_rows = _counter_rows(os.path.join(root, "fetch")) if m1 else []
+    write_rows = _counter_rows(os.path.join(root, "write")) if m1 else []
+    for key, match in (KERNELS.items() if m1 else ()):
         fk, nf = _per_dispatch(fetch_rows, "FETCH_SIZE", match)
         wk, nw = _per_dispatch(write_rows, "WRITE_SIZE", match)
         if fk is None or wk is None:
@@ -624,6 +772,19 @@ def ingest_traffic(root, workload, span):
         res[key] = {"fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
                     "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
                     "hbm_bytes_per_launch": fb + wb}
+    if os.path.isdir(os.path.join(root, "dfetch")) and os.path.isdir(os.path.join(root, "dwrite")):
+        # the decode step (bench.py --decode-probe): 132 launches of decode_step_f32
+        fk, nf = _per_dispatch(_counter_rows(os.path.join(root, "dfetch")), "FETCH_SIZE",
+                               "decode_step_f32")
+        wk, nw = _per_dispatch(_counter_rows(os.path.join(root, "dwrite")), "WRITE_SIZE",
+                               "decode_step_f32")
+        if fk is not None and wk is not None:
+            fb = fk * 1024.0 * cal["FETCH_SIZE"]["factor"]
+            wb = wk * 1024.0 * cal["WRITE_SIZE"]["factor"]
+            res["decode_step"] = {"fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
+                                  "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                                  "hbm_bytes_per_launch": fb + wb,
+                                  "source_sha": source_sha(("kata_fp32.hip", "kata_common.hpp"))}
     if os.path.isdir(os.path.join(root, "lfetch")) and os.path.isdir(os.path.join(root, "lwrite")):
         lres = {"source_sha": source_sha(LIN_SOURCES), "workload": "scan_long_bf16",
                 "feature": "identity"}
@@ -663,6 +824,10 @@ def main():
                     help="only run the psi(x) = x linear-feature forward (for rocprofv3 --pmc)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
+    ap.add_argument("--decode-probe", action="store_true",
+                    help="only run the decode workload (for rocprofv3 --pmc)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload forward rows (tiny, mid, recall)")
     ap.add_argument("--ingest-traffic", metavar="DIR",
                     help="write profiles/traffic_counters.json from the --pmc runs under DIR")
     args = ap.parse_args()
@@ -681,6 +846,11 @@ def main():
     if args.linear_probe:
         import paper_2607_17419_amd as kata
         res = bench_linear(kata, "cuda:0", _hip(), steps=3, warmup=1, probe=True)
+        print(json.dumps(res), flush=True)
+        return
+    if args.decode_probe:
+        import paper_2607_17419_amd as kata
+        res = bench_decode(kata, "cuda:0", _hip())
         print(json.dumps(res), flush=True)
         return
 
@@ -773,6 +943,8 @@ def main():
         "algorithmic_gflop_per_step": round(alg["total_flop"] / 1e9, 2),
         "kernel_source_sha": sha,
     }
+    if not args.no_configs:
+        res["configs"] = bench_configs(kata, dev, hip)
     if not args.no_decode:
         res["decode"] = bench_decode(kata, dev, hip)
         res["practical_hbm"] = hbm_ceiling(dev)
@@ -789,5 +961,25 @@ def main():
     print(json.dumps(res), flush=True)
 
 
+def _no_children_left():
+    """bench.py starts one child (the single-thread oracle timing, waited for);
+    report on stderr and end anything else still attached to this process."""
+    try:
+        import psutil
+    except ImportError:
+        return
+    kids = psutil.Process().children(recursive=True)
+    for p in kids:
+        try:
+            print(f"bench.py: ending leftover child {p.pid} {p.name()}", file=sys.stderr)
+            p.terminate()
+        except psutil.Error:
+            pass
+    psutil.wait_procs(kids, timeout=5)
+
+
 if __name__ == "__main__":
-    main()
+    try:
+        main()
+    finally:
+        _no_children_left()
