@@ -97,8 +97,9 @@ def algorithmic(w, L, g=1):
                      output  2*n*dv + 2*n + (C+1)*(d+dv)
                              (phi(q)^T S and phi(q)^T z readouts, causal
                               intra-chunk QK^T and PV at chunk size C)
-    scan: one bf16 read of every span state (n*(dv+1) values) and one bf16
-          write of its exclusive prefix, per span and head.
+    scan: one bf16 read of every span state but the last (n*(dv+1) values;
+          the last span's state enters no exclusive prefix) and one bf16
+          write of every span's exclusive prefix, per head.
     """
     m = w.d // g
     n = g * (m * (m + 1) // 2)
@@ -106,7 +107,7 @@ def algorithmic(w, L, g=1):
     NS = (w.T + L - 1) // L
     state = (2 * n * w.dv + n) * ht
     output = (2 * n * w.dv + 2 * n + (w.C + 1) * (w.d + w.dv)) * ht
-    scan_bytes = NS * w.B * w.H * n * (w.dv + 1) * (2 + 2)
+    scan_bytes = (2 * NS - 1) * w.B * w.H * n * (w.dv + 1) * 2
     return dict(n=n, state_flop=state, output_flop=output, scan_bytes=scan_bytes,
                 total_flop=state + output)
 
@@ -661,7 +662,7 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
 # the KATA-M1 kernels of the d = 64 long-context workload (the M2 and
 # quadratic-form instantiations share the names, not the template arguments)
 KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
-           "scan": "scan_exclusive_bf16<kata::SlotWeight<64, 64, 1> >",
+           "scan": "scan_exclusive_bf16<8, kata::SlotWeight<64, 64, 1> >",
            "span_output": "span_output_kernel<64, 64, 1, false>"}
 COPY_BYTES = 1 << 30
 # the linear-feature kernels of psi(x) = x (plain readout) at d = dv = 64

@@ -1666,9 +1666,8 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
                                                       sp0 + cnt);
   }
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
-  dim3 g3(static_cast<unsigned>((G::E + kEB16 - 1) / kEB16), BH);
-  scan_exclusive_bf16<SlotWeight<D, DV, NG>><<<g3, 256, 0, st>>>(
-      spanst, NS, G::E, static_cast<long long>(NS) * G::E, SlotWeight<D, DV, NG>{});
+  launch_scan_exclusive_bf16(spanst, NS, G::E, static_cast<long long>(NS) * G::E, BH,
+                             SlotWeight<D, DV, NG>{}, st);
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   const int qblocks = (L + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {

@@ -96,19 +96,26 @@ namespace kata {
 // In-place exclusive prefix over bf16 records (the MFMA path's span states):
 //   rec[bh][c][e] <- bf16( w(e) * sum_{c' < c} rec[bh][c'][e] ),  rec[.][0][.] = 0,
 // with the sums carried in fp32.  Blocked Blelloch scan along the record
-// axis: a workgroup owns kEB16 consecutive elements of every record; thread
-// (column group cg, row group rg) holds 8 elements x kRPT16 records in
-// registers and runs the up-sweep / down-sweep over its records there; the
-// row-group totals are scanned across the kRG16 groups through LDS; blocks of
-// kRG16 * kRPT16 records are chained by an fp32 carry.  All of a thread's
-// loads of a block are in flight together (16-byte accesses, 512-byte rows).
-// E must be a multiple of 8.  grid (ceil(E / kEB16), BH), block 256.
+// axis: thread (column group cg, row group rg) holds 8 elements x kRPT16
+// records in registers and runs the up-sweep / down-sweep over its records
+// there; with RG > 1 row groups the row-group totals are scanned across the
+// groups through LDS; blocks of RG * kRPT16 records are chained by an fp32
+// carry.  A workgroup owns 8 * (256 / RG) consecutive elements of every
+// record, so short record axes take few row groups and wide element slices
+// (RG = 1 for up to 16 records: no idle row groups, no LDS exchange) and long
+// ones take eight.  The last record's input never enters an exclusive prefix
+// and is not read.  All of a thread's loads of a block are in flight together
+// (16-byte accesses).  E must be a multiple of 8.
+// grid (ceil(E / scan_bf16_elems(RG)), BH), block 256.
 // ---------------------------------------------------------------------------
-constexpr int kCG16 = 32;                // column groups of 8 elements
-constexpr int kEB16 = 8 * kCG16;         // elements per workgroup (256)
-constexpr int kRG16 = 256 / kCG16;       // row groups (8)
-constexpr int kRPT16 = 16;               // records per thread and block
-constexpr int kNB16 = kRG16 * kRPT16;    // records per block (128)
+constexpr int kRPT16 = 16;  // records per thread and block
+
+__host__ __device__ constexpr int scan_bf16_elems(int rg) { return 8 * (256 / rg); }
+
+// Row groups for N records: the fewest that cover N in one block, at most 8.
+inline int scan_bf16_row_groups(int N) {
+  return N <= kRPT16 ? 1 : N <= 2 * kRPT16 ? 2 : N <= 4 * kRPT16 ? 4 : 8;
+}
 
 // Records are read once and written once: non-temporal 16-byte accesses keep
 // them from lingering dirty in the caches, where their write-back would
@@ -124,13 +131,17 @@ __device__ __forceinline__ void stream_store_b128(uint16_t* p, uint4 u) {
   __builtin_nontemporal_store(t, reinterpret_cast<scan_b128*>(p));
 }
 
-template <typename Weight>
+template <int RG, typename Weight>
 __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N, long long E,
                                                            long long bh_stride, Weight weight) {
-  __shared__ float tot[kRG16][kEB16];
+  static_assert(RG == 1 || RG == 2 || RG == 4 || RG == 8, "row groups");
+  constexpr int CG = 256 / RG;              // column groups of 8 elements
+  constexpr int EB = scan_bf16_elems(RG);   // elements per workgroup
+  constexpr int NB = RG * kRPT16;           // records per block
+  __shared__ float tot[RG][EB];
   const int tid = threadIdx.x;
-  const int cg = tid % kCG16, rg = tid / kCG16;
-  const long long ec = static_cast<long long>(blockIdx.x) * kEB16 + 8 * cg;
+  const int cg = tid % CG, rg = tid / CG;
+  const long long ec = static_cast<long long>(blockIdx.x) * EB + 8 * cg;
   uint16_t* rb = rec + blockIdx.y * bh_stride;
   const bool active = ec < E;
   float w[8], carry[8];
@@ -139,13 +150,13 @@ __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N,
     w[x] = active ? weight(ec + x) : 0.f;
     carry[x] = 0.f;
   }
-  for (int r0 = 0; r0 < N; r0 += kNB16) {
+  for (int r0 = 0; r0 < N; r0 += NB) {
     const int rbase = r0 + rg * kRPT16;  // this thread's first record
     float v[kRPT16][8];
 #pragma unroll
     for (int j = 0; j < kRPT16; ++j) {
       uint4 q4 = make_uint4(0u, 0u, 0u, 0u);
-      if (active && rbase + j < N)
+      if (active && rbase + j < N - 1)
         q4 = stream_load_b128(rb + static_cast<long long>(rbase + j) * E + ec);
       const uint32_t q[4] = {q4.x, q4.y, q4.z, q4.w};
 #pragma unroll
@@ -178,25 +189,29 @@ __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N,
           v[j - d][x] = v[j][x];
           v[j][x] += left;
         }
-    // exclusive scan of the row-group totals, plus the block total for the carry
-#pragma unroll
-    for (int x = 0; x < 8; ++x) tot[rg][8 * cg + x] = gsum[x];
-    __syncthreads();
     float pre[8], blk[8];
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
       pre[x] = carry[x];
-      blk[x] = 0.f;
+      blk[x] = gsum[x];
     }
+    if constexpr (RG > 1) {
+      // exclusive scan of the row-group totals, plus the block total for the carry
 #pragma unroll
-    for (int g2 = 0; g2 < kRG16; ++g2)
+      for (int x = 0; x < 8; ++x) tot[rg][8 * cg + x] = gsum[x];
+      __syncthreads();
 #pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const float t = tot[g2][8 * cg + x];
-        if (g2 < rg) pre[x] += t;
-        blk[x] += t;
-      }
-    __syncthreads();  // tot is rewritten by the next block
+      for (int x = 0; x < 8; ++x) blk[x] = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < RG; ++g2)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          const float t = tot[g2][8 * cg + x];
+          if (g2 < rg) pre[x] += t;
+          blk[x] += t;
+        }
+      __syncthreads();  // tot is rewritten by the next block
+    }
 #pragma unroll
     for (int j = 0; j < kRPT16; ++j) {
       if (active && rbase + j < N) {
@@ -211,6 +226,21 @@ __global__ __launch_bounds__(256) void scan_exclusive_bf16(uint16_t* rec, int N,
     }
 #pragma unroll
     for (int x = 0; x < 8; ++x) carry[x] += blk[x];
+  }
+}
+
+// Launch the bf16 record scan with the row-group count scan_bf16_row_groups(N).
+template <typename Weight>
+void launch_scan_exclusive_bf16(uint16_t* rec, int N, long long E, long long bh_stride, int BH,
+                                Weight weight, hipStream_t st) {
+  const int rg = scan_bf16_row_groups(N);
+  const dim3 grid(static_cast<unsigned>((E + scan_bf16_elems(rg) - 1) / scan_bf16_elems(rg)),
+                  static_cast<unsigned>(BH));
+  switch (rg) {
+    case 1: scan_exclusive_bf16<1><<<grid, 256, 0, st>>>(rec, N, E, bh_stride, weight); break;
+    case 2: scan_exclusive_bf16<2><<<grid, 256, 0, st>>>(rec, N, E, bh_stride, weight); break;
+    case 4: scan_exclusive_bf16<4><<<grid, 256, 0, st>>>(rec, N, E, bh_stride, weight); break;
+    default: scan_exclusive_bf16<8><<<grid, 256, 0, st>>>(rec, N, E, bh_stride, weight); break;
   }
 }
 

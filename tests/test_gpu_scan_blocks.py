@@ -1,12 +1,14 @@
-"""GPU parity of the record scans past one block of records per head.
+"""GPU parity of the record scans at every record-block shape.
 
-The bf16 span-record scan keeps up to 128 records of a head in registers and
-carries an fp32 running sum from one 128-record block to the next; the fp32
-path's chunk-record scan does the same with 128-record blocks.  Every case
-here gives a head more than 128 records, so the carry runs (section
-"Tree-scan inter-chunk reduction": the associative scan over chunk states),
-and compares the output with the CPU oracle's definition.  Every case prints
-its name and shape before it launches anything.
+The bf16 span-record scan splits a head's records into blocks of 1, 2, 4 or 8
+row groups of 16 records (chosen by the record count), keeps a block in
+registers and carries an fp32 running sum from one block to the next; the
+fp32 path's chunk-record scan does the same with 128-record blocks.  The
+row-group cases sit on both sides of each row-group boundary; every other
+case gives a head more than 128 records, so the carry runs (section
+"Tree-scan inter-chunk reduction": the associative scan over chunk states).
+Each compares the output with the CPU oracle's definition and prints its
+name and shape before it launches anything.
 """
 from __future__ import annotations
 
@@ -43,6 +45,18 @@ def _run(kata, inp, dtype, C, span=0, g=1):
     del q, k, v, out
     torch.cuda.empty_cache()
     return res
+
+
+@pytest.mark.parametrize("n_rec", [1, 2, 5, 16, 17, 32, 33, 64, 65])
+def test_span1_row_group_boundaries(kata, orc, n_rec):
+    # the scan takes 1, 2, 4 or 8 row groups of 16 records by the record
+    # count; these counts sit on both sides of each boundary
+    T = 64 * n_rec - 13
+    log(f"case span_chunks=1 B1 H2 T{T} d64 C64 ({n_rec} records per head), all rows")
+    inp = workloads.make_inputs("mid_bf16", B=1, H=2, T=T)
+    got = _run(kata, inp, "bf16", 64, span=1)
+    ref = orc.fwd(inp["q"], inp["k"], inp["v"])
+    assert_bf16_close(got, ref, f"span 1, {n_rec} records")
 
 
 def test_span1_129_records_all_rows(kata, orc):
