@@ -431,14 +431,16 @@ def bench_m2(kata, dev, hip, w, q, k, v, steps=10, warmup=3):
 PAPER_TREE_SCAN_H100 = {2048: 19.4, 4096: 39.9, 8192: 44.5, 16384: 47.6, 32768: 49.4,
                         65536: 67.5, 131072: 69.4}
 LIN_FEATURES = {0: "identity (plain readout)", 1: "relu+eps", 2: "elu+1",
-                4: "lorentz (n_psi = d variant)"}
+                3: "lorentz lift (n_psi = d + 1)", 4: "lorentz (n_psi = d variant)"}
 
 
-def lin_bytes(B, H, T, d, dv, L):
+def lin_bytes(B, H, T, d, dv, L, n=None):
     """Algorithmic HBM bytes of the three linear-feature kernels (bf16 q, k, v;
-    fp32 records of S (d x dv) and z (d) per span of L tokens; fp32 output)."""
+    fp32 records of S (n x dv) and z (n) per span of L tokens, n = n_psi,
+    d by default; fp32 output)."""
     NS = -(-T // L)
-    rec = B * H * NS * (d * dv + d) * 4
+    n = d if n is None else n
+    rec = B * H * NS * (n * dv + n) * 4
     qk = B * H * T * d * 2
     vv = B * H * T * dv * 2
     return {"span_state": qk + vv + rec, "scan": 2 * rec,
@@ -503,7 +505,7 @@ def bench_linear(kata, dev, hip, steps=10, warmup=3, probe=False):
     per_feature = {}
     for f, name in LIN_FEATURES.items():
         ms, stage, L = run(w.B, w.H, w.T, w.C, f, q, k, v)
-        by = lin_bytes(w.B, w.H, w.T, w.d, w.dv, L)
+        by = lin_bytes(w.B, w.H, w.T, w.d, w.dv, L, w.d + 1 if f == 3 else w.d)
         roofs = {}
         for nm, t in stage.items():
             gbs = by[nm] / (t * 1e-3) / 1e9

@@ -250,8 +250,9 @@ KATA_API kata_status_t kata_mg_decode_step(float* S, float* z, const void* q, co
  * form (paragraph "Three-kernel pipeline" of that appendix).
  *   feature : a kata_lin_feature_t; eps (>= 0, finite) is used by
  *             KATA_LIN_RELU only.  n_psi = kata_lin_dim(d, feature).
- *   Fast path (bf16 MFMA): dtype = KATA_BF16, d = dv = 64, n_psi = d (every
- *   feature but KATA_LIN_LORENTZ), C a multiple of 64 up to 1024.  Every
+ *   Fast path (bf16 MFMA): dtype = KATA_BF16, d = dv = 64, every feature, C a
+ *   multiple of 64 up to 1024 (KATA_LIN_LORENTZ's extra coordinate ||x|| is
+ *   carried as a rank-one fp32 term beside the d x d MFMA state).  Every
  *   other shape with d <= 64, dv <= 256 and C <= 128 runs on the fp32 path;
  *   anything else is KATA_ERR_UNSUPPORTED.
  *   span_chunks, workspace, stage_events: as for kata_fwd_chunked_ws and

@@ -318,7 +318,8 @@ int lin_default_span(int B, int H, int T, int C, Path path) {
 size_t lin_workspace_for(Path p, int B, int H, int T, int d, int dv, int C, int feature,
                          int span_chunks) {
   if (p == Path::kFp32) return kata::lin_fp32_workspace(B * H, T, d, dv, C, feature);
-  if (p == Path::kMfma) return kata::lin_mfma_workspace(B * H, T, span_tokens(T, C, span_chunks));
+  if (p == Path::kMfma)
+    return kata::lin_mfma_workspace(B * H, T, span_tokens(T, C, span_chunks), feature);
   return 0;
 }
 

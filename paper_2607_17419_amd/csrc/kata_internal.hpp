@@ -60,7 +60,7 @@ hipError_t launch_lin_fp32(const void* q, const void* k, const void* v, float* o
                            int d, int dv, int C, int feature, float eps, int normalize, void* ws,
                            hipStream_t st, hipEvent_t* ev);
 bool lin_mfma_supported(int T, int d, int dv, int C, int feature);
-size_t lin_mfma_workspace(int BH, int T, int L);
+size_t lin_mfma_workspace(int BH, int T, int L, int feature);
 hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* out, int BH, int T,
                            int feature, float eps, int normalize, int L, void* ws, hipStream_t st,
                            hipEvent_t* ev);

@@ -15,10 +15,14 @@
 // record's prefix with the causal pattern inside the record.
 //  - fp32 path: one record per chunk of C tokens, fp32 arithmetic, any
 //    feature, d <= 64, dv <= 256, C <= 128, fp32 or bf16 inputs.
-//  - bf16 MFMA path (d = dv = 64, n_psi = d): one record per span of L tokens
-//    (a multiple of 64); inside a span the output kernel walks 64-token chunks
-//    in order and carries the running state on chip.  Every contraction is a
-//    v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+//  - bf16 MFMA path (d = dv = 64; every feature): one record per span of L
+//    tokens (a multiple of 64); inside a span the output kernel walks 64-token
+//    chunks in order and carries the running state on chip.  Every d x d
+//    contraction is a v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The
+//    Lorentz lift's extra coordinate ||x|| is a rank-one addition to the
+//    weights, <psi(q), psi(k)> = q . k + ||q|| ||k||: it adds one state row
+//    sum ||k|| v^T and one normaliser term sum ||k||, kept in fp32 beside
+//    the d x d part, and the term ||q|| ||k|| to each in-chunk score.
 #include <cmath>
 
 #include "kata_internal.hpp"
@@ -225,6 +229,12 @@ constexpr int kLD = 64;   // feature / value width of the MFMA path
 constexpr int kLCH = 64;  // tokens per chunk inside a span
 constexpr int kLS = 72;   // LDS row stride (bf16 elements)
 constexpr long long kLE = static_cast<long long>(kLD) * kLD + kLD;  // record: S then z
+// Lorentz-lift record: the d x d record, then the extra state row
+// sum ||k|| v^T (kLD values), then sum ||k|| and three zeros (a multiple of
+// four elements for the scan's 16-byte accesses).
+constexpr long long kLEL = kLE + kLD + 4;
+template <int F>
+constexpr long long lin_record() { return F == kLinLorentz ? kLEL : kLE; }
 // Raw-buffer descriptor word 3 (32-bit data format, no swizzle) of gfx9-class
 // buffer resources; out-of-range accesses are dropped.
 constexpr int kBufWord3 = 0x00020000;
@@ -330,6 +340,37 @@ __device__ __forceinline__ void lin_stage_features(const LinStage& s, float (*x)
   }
 }
 
+// ||x|| of the thread's two staged key rows (raw coordinates, zero rows for
+// padded tokens): the eight lanes that share a token combine their parts.
+__device__ __forceinline__ void lin_row_norms(const float (*x)[8], float* nk) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += x[i][e] * x[i][e];
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    nk[i] = sqrtf(s);
+  }
+}
+
+// Wave w's share of a chunk's Lorentz-lift state row: lane j sums
+// nk[t] * V^T[j][t] over the chunk's tokens 16 w .. 16 w + 15 (V^T rows of
+// stride kLS in LDS, bf16).
+__device__ __forceinline__ float lin_lift_part(const uint16_t* vt, const float* nk, int w,
+                                               int lane) {
+  const uint4 u0 = *reinterpret_cast<const uint4*>(&vt[lane * kLS + 16 * w]);
+  const uint4 u1 = *reinterpret_cast<const uint4*>(&vt[lane * kLS + 16 * w + 8]);
+  float y[16];
+  unpack8(u0, y);
+  unpack8(u1, y + 8);
+  float acc = 0.f;
+#pragma unroll
+  for (int t = 0; t < 16; ++t) acc += nk[16 * w + t] * y[t];
+  return acc;
+}
+
 // Transposed LDS writes: element e of the thread's two tokens goes to row
 // 8 fg + e, columns 2 tp and 2 tp + 1 (one 4-byte write).
 __device__ __forceinline__ void lin_write_t(uint16_t* dst, const float (*x)[8], int fg, int tp) {
@@ -349,6 +390,9 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
                                                       float* rec, int T, int L, int NS, float eps) {
   __shared__ __align__(16) uint16_t kt[2][kLD * kLS];
   __shared__ __align__(16) uint16_t vt[2][kLD * kLS];
+  constexpr bool LIFT = F == kLinLorentz;
+  __shared__ __align__(16) float nks[LIFT ? 2 : 1][LIFT ? kLCH : 1];  // ||k|| per chunk token
+  __shared__ float red[LIFT ? 4 : 1][LIFT ? kLD + 1 : 1];
   const int bh = blockIdx.x / NS, sp = blockIdx.x % NS;
   const long long tbeg = static_cast<long long>(sp) * L;
   const long long tend = tbeg + L < T ? tbeg + L : T;
@@ -363,6 +407,7 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   float zp = 0.f;
+  float lift = 0.f, liftz = 0.f;  // lane j: sum ||k|| v_j and sum ||k|| over the wave's tokens
   // two chunks in flight: chunk ch + 2 is loaded into the registers chunk ch
   // has just left, right after the barrier that publishes chunk ch
   LinStage s0, s1;
@@ -375,6 +420,14 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
     lin_stage_values(sg, y);
     lin_write_t(kt[buf], x, fg, tp);
     lin_write_t(vt[buf], y, fg, tp);
+    if constexpr (LIFT) {
+      float nk[2];
+      lin_row_norms(x, nk);
+      if (fg == 0) {
+        nks[buf][2 * tp] = nk[0];
+        nks[buf][2 * tp + 1] = nk[1];
+      }
+    }
     __syncthreads();
     // unconditional (the last chunk is re-read near the end), so that no
     // branch joins the pending loads
@@ -387,12 +440,17 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
       acc = lin_mfma(a, b, acc);
       if (vb2 == 0) zp += sum8(a);
     }
+    if constexpr (LIFT) {
+      lift += lin_lift_part(vt[buf], nks[buf], w, lane);
+#pragma unroll
+      for (int t = 0; t < 16; ++t) liftz += nks[buf][16 * w + t];
+    }
   };
   for (int ch = 0; ch < nch; ch += 2) {
     step(s0, ch);
     if (ch + 1 < nch) step(s1, ch + 1);
   }
-  float* r = rec + (static_cast<long long>(bh) * NS + sp) * kLE;
+  float* r = rec + (static_cast<long long>(bh) * NS + sp) * lin_record<F>();
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int f = 32 * fb + 8 * (i >> 2) + 4 * h + (i & 3);
@@ -400,17 +458,36 @@ __global__ __launch_bounds__(256) void lin_span_state(const uint16_t* k, const u
   }
   zp += __shfl_xor(zp, 32);
   if (vb2 == 0 && h == 0) r[kLD * kLD + 32 * fb + l32] = zp;
+  if constexpr (LIFT) {
+    red[w][lane] = lift;
+    if (lane == 0) red[w][kLD] = liftz;
+    __syncthreads();
+    if (tid < kLD + 4) {
+      float t = 0.f;
+      if (tid <= kLD) t = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+      r[kLE + tid] = t;  // the row, the normaliser term, three zeros
+    }
+  }
 }
 
 // psi of the wave's query rows in B-operand order (kk-th 16-feature step,
 // half h: features 16 kk + 8 h .. +7); the Lorentz variant's norm combines the
 // two halves of a row (lanes l and l ^ 32).
 template <int F>
-__device__ __forceinline__ void lin_query_features(const uint4* raw, bf16x8* qa, float eps, int h) {
+__device__ __forceinline__ void lin_query_features(const uint4* raw, bf16x8* qa, float eps, int h,
+                                                   float& nq) {
   float x[4][8];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) unpack8(raw[kk], x[kk]);
-  if constexpr (F == kLinLorentzS) {
+  if constexpr (F == kLinLorentz) {  // raw coordinates, plus ||q|| of the whole row
+    float nrm = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) nrm += x[kk][e] * x[kk][e];
+    nrm += __shfl_xor(nrm, 32);
+    nq = sqrtf(nrm);
+  } else if constexpr (F == kLinLorentzS) {
     float nrm = 0.f;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
@@ -448,6 +525,8 @@ __device__ __forceinline__ void lin_query_load(uint4* raw, const uint16_t* qb, l
 //   O^T = sum_kb V_kb^T P^T(kb) + S_run^T psi(Q)^T;
 //   D = sum of the P^T column + psi(q) . z_run (normalised readout);
 //   then S_run += psi(K_c)^T V_c and z_run += psi(K_c)^T 1 for the next chunk.
+// The Lorentz lift adds ||k|| ||q|| to each score, ||q|| l_run to O (l_run =
+// sum ||k|| v, fp32 in LDS) and ||q|| m_run to D (m_run = sum ||k||).
 // grid BH * NS (1-D), block 256.
 // ---------------------------------------------------------------------------
 template <int F, bool NORM>
@@ -460,6 +539,12 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
   __shared__ __align__(16) uint16_t kr[kLCH * kLS];
   __shared__ __align__(16) uint16_t st[kLD * kLS];
   __shared__ __align__(16) float zs[kLD];
+  constexpr bool LIFT = F == kLinLorentz;
+  constexpr int LX = LIFT ? kLD : 1;
+  __shared__ __align__(16) float nks[LIFT ? kLCH : 1];  // ||k|| of the staged chunk's tokens
+  __shared__ __align__(16) float lrun[LX];              // l_run
+  __shared__ float lpart[LIFT ? 4 : 1][LX + 1];         // per-wave chunk sums of l and m
+  __shared__ float mrun;                                // m_run
   const int bh = blockIdx.x / NS, sp = blockIdx.x % NS;
   const long long tbeg = static_cast<long long>(sp) * L;
   const long long tend = tbeg + L < T ? tbeg + L : T;
@@ -479,13 +564,17 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
   const int krow = 16 * (l32 >> 4) + 8 * ((l32 >> 2) & 1) + 4 * ((l32 >> 3) & 1) + (l32 & 3);
 
   // running state tile from the exclusive prefix
-  const float* r = rec + (static_cast<long long>(bh) * NS + sp) * kLE;
+  const float* r = rec + (static_cast<long long>(bh) * NS + sp) * lin_record<F>();
   f32x16 sacc;
 #pragma unroll
   for (int i = 0; i < 16; ++i)
     sacc[i] = r[(32 * fb + 8 * (i >> 2) + 4 * h + (i & 3)) * kLD + 32 * vb2 + l32];
   float zp = 0.f;
   if (NORM && tid < kLD) zs[tid] = r[kLD * kLD + tid];
+  if constexpr (LIFT) {
+    if (tid < kLD) lrun[tid] = r[kLE + tid];
+    if (tid == kLD) mrun = r[kLE + kLD];
+  }
   auto write_state = [&]() {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -506,6 +595,7 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
   LinStage sg;
   uint4 qraw[4];
   bf16x8 qa[4];
+  float nq = 0.f;  // ||q|| of this lane's query (Lorentz lift)
   auto stage_in = [&]() {
     float x[2][8], y[2][8];
     lin_stage_features<F>(sg, x, eps, fg);
@@ -515,7 +605,15 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       *reinterpret_cast<bf16x8*>(&kr[(2 * tp + i) * kLS + 8 * fg]) = pack8(x[i]);
-    lin_query_features<F>(qraw, qa, eps, h);
+    if constexpr (LIFT) {
+      float nk[2];
+      lin_row_norms(x, nk);
+      if (fg == 0) {
+        nks[2 * tp] = nk[0];
+        nks[2 * tp + 1] = nk[1];
+      }
+    }
+    lin_query_features<F>(qraw, qa, eps, h, nq);
   };
   auto load_chunk = [&](int c) {
     const long long tn = tbeg + static_cast<long long>(c < nch ? c : nch - 1) * kLCH;
@@ -543,6 +641,11 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
         p = lin_mfma(lds8(&kr[(32 * kb + krow) * kLS + 16 * kk + 8 * h]), qa[kk], p);
+      if constexpr (LIFT) {
+        // + ||k|| ||q||: p[i] holds key 32 kb + 16 (i / 8) + 8 h + i % 8
+#pragma unroll
+        for (int i = 0; i < 16; ++i) p[i] += nks[32 * kb + 16 * (i >> 3) + 8 * h + (i & 7)] * nq;
+      }
       if (kb == qb) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -566,6 +669,11 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
       oacc = lin_mfma(lds8(&st[(32 * vb2 + l32) * kLS + 16 * kk + 8 * h]), qa[kk], oacc);
+    if constexpr (LIFT) {
+      // + ||q|| l_run: oacc[i] holds value column 32 vb2 + 8 (i / 4) + 4 h + i % 4
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[i] += lrun[32 * vb2 + 8 * (i >> 2) + 4 * h + (i & 3)] * nq;
+    }
     if constexpr (NORM) {
       float dz = 0.f;
 #pragma unroll
@@ -577,6 +685,7 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
               bf16hi_f32(u.y) * z0.w + bf16lo_f32(u.z) * z1.x + bf16hi_f32(u.z) * z1.y +
               bf16lo_f32(u.w) * z1.z + bf16hi_f32(u.w) * z1.w;
       }
+      if constexpr (LIFT) dz += h == 0 ? nq * mrun : 0.f;
       float den = dsum + dz;
       den += __shfl_xor(den, 32);
       const float inv = den > 0.f ? 1.f / den : 0.f;
@@ -605,8 +714,21 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
       sacc = lin_mfma(a, lds8(&vt[(32 * vb2 + l32) * kLS + 16 * ks + 8 * h]), sacc);
       if (NORM && vb2 == 0) zp += sum8(a);
     }
+    if constexpr (LIFT) {
+      lpart[w][lane] = lin_lift_part(vt, nks, w, lane);
+      if (lane == 0) {
+        float m = 0.f;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) m += nks[16 * w + t];
+        lpart[w][kLD] = m;
+      }
+    }
     __syncthreads();
     if (ch + 1 < nch) {
+      if constexpr (LIFT) {
+        if (tid < kLD) lrun[tid] += lpart[0][tid] + lpart[1][tid] + lpart[2][tid] + lpart[3][tid];
+        if (tid == kLD) mrun += lpart[0][kLD] + lpart[1][kLD] + lpart[2][kLD] + lpart[3][kLD];
+      }
       write_state();
       if constexpr (NORM) {
         zp += __shfl_xor(zp, 32);
@@ -620,13 +742,13 @@ __global__ __launch_bounds__(256) void lin_span_output(const uint16_t* q, const 
 }
 
 bool lin_mfma_supported(int T, int d, int dv, int C, int feature) {
-  return d == kLD && dv == kLD && feature != kLinLorentz && C % kLCH == 0 && C <= 1024 &&
-         T < kLinMaxT;
+  return d == kLD && dv == kLD && C % kLCH == 0 && C <= 1024 && T < kLinMaxT;
 }
 
-size_t lin_mfma_workspace(int BH, int T, int L) {
+size_t lin_mfma_workspace(int BH, int T, int L, int feature) {
   const long long NS = (static_cast<long long>(T) + L - 1) / L;
-  return static_cast<size_t>(BH) * NS * kLE * sizeof(float);
+  const long long E = feature == kLinLorentz ? kLEL : kLE;
+  return static_cast<size_t>(BH) * NS * E * sizeof(float);
 }
 
 template <int F, bool NORM>
@@ -641,9 +763,11 @@ static hipError_t run_lin_mfma(const void* q, const void* k, const void* v, floa
   lin_span_state<F><<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(k),
                                          static_cast<const uint16_t*>(v), rec, T, L, NS, eps);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
+  constexpr long long E = lin_record<F>();
+  static_assert(E % 4 == 0, "the fp32 scan moves 16-byte pieces");
   scan_exclusive_f32x4<LinUnitWeight>
-      <<<dim3(static_cast<unsigned>((kLE + kEB4 - 1) / kEB4), BH), 256, 0, st>>>(
-          rec, NS, kLE, kLE * NS, LinUnitWeight{});
+      <<<dim3(static_cast<unsigned>((E + kEB4 - 1) / kEB4), BH), 256, 0, st>>>(
+          rec, NS, E, E * NS, LinUnitWeight{});
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   lin_span_output<F, NORM><<<grid, 256, 0, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
@@ -664,6 +788,7 @@ hipError_t launch_lin_mfma(const void* q, const void* k, const void* v, float* o
     KATA_LIN_CASE(kLinIdentity)
     KATA_LIN_CASE(kLinRelu)
     KATA_LIN_CASE(kLinElu)
+    KATA_LIN_CASE(kLinLorentz)
     KATA_LIN_CASE(kLinLorentzS)
     default:
       return hipErrorInvalidValue;

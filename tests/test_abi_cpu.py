@@ -212,9 +212,14 @@ def test_lin_workspace_and_span_host_logic():
         16 * 128 * (64 * 64 + 64) * 4
     assert L.kata_lin_default_span(1, 16, 2048, 64, 64, 128, 0, 1) == 1
     assert L.kata_lin_default_span(1, 16, 16384, 64, 64, 64, 2, 1) == 4
-    # the Lorentz lift (n_psi = d + 1) runs on the fp32 path: one record per chunk
-    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 128, 3, 1) == 1
-    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 256, 3, 1) == 0  # C > 128 there
+    # the Lorentz lift (n_psi = d + 1) on the MFMA path: the d x d record, the
+    # extra row sum ||k|| v (64), sum ||k|| and three zeros per span
+    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 128, 3, 1) == 8
+    assert L.kata_lin_fwd_workspace_bytes(1, 16, 131072, 64, 64, 128, 3, 1, 0) == \
+        16 * 128 * (64 * 64 + 64 + 64 + 4) * 4
+    # ... and on the fp32 path (C not a multiple of 64): one record per chunk
+    assert L.kata_lin_default_span(1, 16, 131072, 64, 64, 96, 3, 1) == 1
+    assert L.kata_lin_default_span(1, 16, 131072, 32, 32, 256, 3, 1) == 0  # C > 128 there
     assert L.kata_lin_fwd_workspace_bytes(1, 2, 1000, 64, 64, 100, 3, 1, 0) == \
         2 * 10 * (65 * 64 + 65) * 4
     # fp32 inputs take the fp32 path, whatever the shape

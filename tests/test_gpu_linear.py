@@ -49,7 +49,7 @@ def _run(kata, inp, dtype, C, feature, normalize, span=0, eps=EPS):
     return out.cpu().numpy()
 
 
-@pytest.mark.parametrize("feature", [IDENT, RELU, ELU, LOR_S])
+@pytest.mark.parametrize("feature", [IDENT, RELU, ELU, LOR, LOR_S])
 @pytest.mark.parametrize("T", [1, 63, 64, 65, 300, 1025, 2100])
 def test_fast_path_ragged(kata, orc, feature, T):
     norm = _norm_of(feature)
@@ -60,10 +60,26 @@ def test_fast_path_ragged(kata, orc, feature, T):
     assert_bf16_close(got, ref, f"{NAMES[feature]} T {T}")
 
 
+def test_fast_path_lorentz_unnormalised_and_scaled(kata, orc):
+    # the lift's extra term in the plain readout (no denominator to hide an
+    # error in it), and keys whose norms vary over the span, so that the
+    # rank-one term's share of every weight differs from token to token
+    T = 1500
+    log(f"case linear lorentz plain readout, key scales 0.25..4, B1 H2 T{T} C64 span 2")
+    inp = dict(workloads.make_inputs("scan_long_bf16", B=1, H=2, T=T))
+    rng = np.random.default_rng(77)
+    scale = (2.0 ** rng.integers(-2, 3, size=(1, 2, T, 1))).astype(np.float32)
+    inp["k"] = inp["k"] * scale  # powers of two: the bf16 copy stays exact
+    inp["k_dev"] = workloads.round_bf16(inp["k"])
+    got = _run(kata, inp, "bf16", 64, LOR, False, span=2)
+    ref = orc.lin_fwd(inp["q"], inp["k"], inp["v"], LOR, EPS, False)
+    assert_bf16_close(got, ref, "lorentz plain readout")
+
+
 @pytest.mark.parametrize("C,span", [(64, 1), (64, 3), (128, 2), (256, 1), (1024, 1), (64, 0)])
 def test_fast_path_spans(kata, orc, C, span):
     T = 2500
-    for feature in (IDENT, ELU):
+    for feature in (IDENT, ELU, LOR):
         norm = _norm_of(feature)
         log(f"case linear {NAMES[feature]} C={C} span={span} B2 H2 T{T}")
         inp = workloads.make_inputs("scan_long_bf16", B=2, H=2, T=T)
@@ -123,8 +139,8 @@ def test_fp32_path(kata, orc, feature, d, dv, C):
 
 @pytest.mark.parametrize("feature", [LOR, RELU])
 def test_bf16_inputs_fp32_path(kata, orc, feature):
-    # the Lorentz lift (n_psi = d + 1) and chunk sizes that are not multiples
-    # of 64 run on the fp32 path with bf16 inputs
+    # chunk sizes that are not multiples of 64 run on the fp32 path with
+    # bf16 inputs (the Lorentz lift, n_psi = d + 1, with its d + 1 features)
     T = 777
     log(f"case linear {NAMES[feature]} bf16 inputs on the fp32 path C=96 B1 H2 T{T}")
     inp = workloads.make_inputs("scan_long_bf16", B=1, H=2, T=T)
@@ -162,7 +178,7 @@ def test_timed_and_alloc_entry_points_match(kata):
         hip.hipEventDestroy(evs[i])
 
 
-@pytest.mark.parametrize("feature", [IDENT, ELU, LOR_S])
+@pytest.mark.parametrize("feature", [IDENT, ELU, LOR, LOR_S])
 def test_full_size_sampled_rows(kata, orc, feature):
     # the bench workload (B1 H16 T131072 d64 C128) in the bench's launch
     # configuration (default span), checked on sampled rows
