@@ -1571,6 +1571,383 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// K4, eight-wave form (d = dv = 64, one feature block).  Same records, V^T
+// layout and stage buffers as span_output_kernel, but 512 threads owning 512
+// queries (16 tiles of 32): wave w holds tiles w and 15 - w, so two waves
+// share each SIMD with balanced causal work (waves w and w + 4 hold tiles
+// adding up to 30), and one wave's VALU work (squared scores, query feature
+// products) issues while the other's MFMAs run.  With a single wave per SIMD
+// VALU issues at about half the rate and largely adds to the MFMA time.
+// Twice the queries per workgroup halve the prefix-record bytes streamed
+// into LDS per query (the readout's dominant copy traffic) and the in-span
+// K / V^T copies; every LDS fragment feeds two tiles.  A wave skips the MFMAs
+// of key blocks past a tile's diagonal (it still takes part in every stage
+// barrier and copy).  MFMAs are compiler builtins (the compiler inserts the
+// wait states).  Grid: 8 * ceil(L / 512) * ceil(spans / 8) workgroups, one
+// per CU (160 KB of LDS), a span's workgroups on one XCD.
+// ---------------------------------------------------------------------------
+constexpr int kQB8 = 512;  // queries per workgroup of the eight-wave form
+
+template <int D, int DV, int NG>
+__global__ __launch_bounds__(512) void span_output8_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
+    int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
+  using G = GeoG<D, DV, NG>;
+  static_assert(D == 64 && DV == 64 && NG == 1, "the eight-wave form covers d = dv = 64, g = 1");
+  constexpr int R = G::RM, KZ = G::KZ;
+  constexpr int W = 8, NQ = 2, NT = kQB8 / 32;
+  constexpr int KCH = D / 8;                    // 16-byte chunks per key row
+  constexpr int KCHUNKS = kKB * KCH;            // K rows of one intra stage
+  constexpr int VCH = kKB / 8;                  // chunks per V^T row of one stage (16)
+  constexpr int VCHUNKS = DV * VCH;
+  constexpr int ICH = KCHUNKS + VCHUNKS;        // chunks per intra stage
+  static_assert(ICH * 16 <= kStageBytes && KCHUNKS % (64 * W) == 0 && VCHUNKS % (64 * W) == 0,
+                "intra stage size");
+  constexpr int IPW_K = KCHUNKS / (64 * W);     // copy instructions per wave: K rows
+  constexpr int IPW_I = ICH / (64 * W);         // ... K rows then V^T rows
+  constexpr int SCH = 2 * kKC;                  // chunks per S_pre row of one stage (32)
+  constexpr int SCHUNKS = DV * SCH;
+  static_assert(SCHUNKS * 16 <= kStageBytes && SCHUNKS % (64 * W) == 0, "readout stage size");
+  constexpr int IPW_R = SCHUNKS / (64 * W);
+  constexpr int NSTAGE_R = (G::NKS + kKC - 1) / kKC;
+  static_assert(G::MT == 2 && G::ZMB == 2, "two dv tiles, two Z tiles");
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane & 31, g = lane >> 5;
+  const int id = blockIdx.x;
+  const int jx = id >> 3;
+  const int qb = jx % QB;
+  const int sp = sp0 + 8 * (jx / QB) + (id & 7);
+  if (sp >= nsp) return;  // whole workgroup: padding of the grid
+  const int s = sp % NS, bh = sp / NS;
+  const long long span0 = static_cast<long long>(s) * L;
+  const long long span_end = min(static_cast<long long>(T), span0 + L);
+  const long long wg_q0 = span0 + static_cast<long long>(qb) * kQB8;
+  if (wg_q0 >= span_end) return;  // whole workgroup beyond the sequence
+  const uint16_t* qh = q + static_cast<long long>(bh) * T * D;
+  const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
+  const uint16_t* rec = pre + static_cast<long long>(sp) * G::E;
+  const uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
+
+  int tile[NQ];
+  long long tq0[NQ];
+  bool tlive[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    tile[i] = qb * NT + (i == 0 ? wave : NT - 1 - wave);
+    tq0[i] = span0 + 32LL * tile[i];
+    tlive[i] = tq0[i] < span_end;
+  }
+
+  // ---- staging copies of both phases ------------------------------------------
+  int last_tile = qb * NT + NT - 1;
+  const int last_key_tile = static_cast<int>((span_end - 1 - span0) / 32);
+  if (last_tile > last_key_tile) last_tile = last_key_tile;
+  const int nstage = (last_tile + 1 + 3) / 4;  // 128-key intra stages
+  // Copy i of a lane writes LDS chunk P = 512 i + 64 wave + lane.  Its source
+  // row grows by a constant with i and the XOR swizzle of its chunk does not
+  // depend on i (kswz uses the row's low three bits and bits 3-5 of the row
+  // minus 64 i; rswz the row's low four bits), so one offset per operand
+  // serves all of a lane's copies:
+  //   K    row 64 i + 8 wave + lane / 8,   chunk lane % 8
+  //   V^T  row 32 i' + 4 wave + lane / 16, chunk lane % 16 (i' = i - IPW_K)
+  //   S^T  row 16 i + 2 wave + lane / 32,  chunk lane % 32
+  static_assert(KCH == 8 && VCH == 16 && SCH == 32 && W == 8, "copy geometry");
+  const int krow0 = 8 * wave + (lane >> 3);
+  const int ksrc0 = krow0 * D + 8 * ((lane & 7) ^ kswz<D>(krow0));
+  const int vrow0 = 4 * wave + (lane >> 4);
+  const int vsrc0 = vrow0 * LV + 8 * ((lane & 15) ^ rswz(vrow0));
+  const int rrow0 = 2 * wave + g;
+  const int rcl = c ^ rswz(rrow0);  // the chunk a lane copies of its S^T row
+  const int rsrc0 = rrow0 * G::NSLOT + 8 * rcl;
+  auto issue_i = [&](int st, uint16_t* buf) __attribute__((always_inline)) {
+    const long long key0 = span0 + static_cast<long long>(st) * kKB;
+#pragma unroll
+    for (int i = 0; i < IPW_I; ++i) {
+      const void* src;
+      if (i < IPW_K) {
+        // keys past the sequence: re-read the last row (never used)
+        const long long over = key0 + krow0 + 64 * i - (T - 1);
+        src = kh + key0 * D + ksrc0 + 64 * i * D - (over > 0 ? over * D : 0);
+      } else {
+        src = vt_rec + st * kKB + vsrc0 + 32 * (i - IPW_K) * LV;
+      }
+      g2lds16(src, buf + (i * W + wave) * 512);
+    }
+  };
+  auto issue_r = [&](auto stg_c) __attribute__((always_inline)) {
+    constexpr int stg = decltype(stg_c)::value;
+    constexpr int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
+    uint16_t* buf = stage_buf((3 + stg) % 5);
+    // chunks past the last K-step: re-read the row's first chunk (never used)
+    int off = rsrc0;
+    if constexpr (kc < kKC) {
+      if (rcl >= 2 * kc) off -= 8 * rcl;
+    }
+#pragma unroll
+    for (int i = 0; i < IPW_R; ++i)
+      g2lds16(rec + 16 * kKC * stg + off + 16 * i * G::NSLOT, buf + (i * W + wave) * 512);
+  };
+  // Stage 0 of the in-span phase first, the query and Z fragments behind it;
+  // the wave waits for that one round trip (loads complete in order, so the
+  // compiler's wait for the fragments covers the copies issued before them;
+  // every fragment is consumed, so no load is left to be waited for behind
+  // later copies), then issues in-span stage 1 and readout stages 0 and 1.
+  issue_i(0, g_stage0);
+  bf16x8 qf[NQ][KZ];  // q[t][8 kz + R g .. +7] of this lane's query t = tq0 + c
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
+#pragma unroll
+    for (int kz = 0; kz < KZ; ++kz)
+      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + 8 * kz + R * g);
+  }
+  bf16x8 zA[G::ZMB][KZ];
+#pragma unroll
+  for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+    for (int kz = 0; kz < KZ; ++kz)
+      zA[m][kz] = *reinterpret_cast<const bf16x8*>(rec + G::ES + ((m * KZ + kz) * 64 + lane) * 8);
+#pragma unroll
+  for (int i = 0; i < NQ; ++i)
+#pragma unroll
+    for (int kz = 0; kz < KZ; ++kz) asm volatile("" ::"v"(qf[i][kz]));
+#pragma unroll
+  for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+    for (int kz = 0; kz < KZ; ++kz) asm volatile("" ::"v"(zA[m][kz]));
+  if (nstage > 1) issue_i(1, g_stage1);
+  issue_r(std::integral_constant<int, 0>{});
+  if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+
+  // ---- denominator from the prefix: q^T Z_pre q ------------------------------
+  float dpart[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    f32x16 az[G::ZMB];
+#pragma unroll
+    for (int m = 0; m < G::ZMB; ++m) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) az[m][r] = 0.f;
+#pragma unroll
+      for (int kz = 0; kz < KZ; ++kz) az[m] = mfma32(zA[m][kz], qf[i][kz], az[m]);
+    }
+    float dsum = 0.f;
+#pragma unroll
+    for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        // row sigma = 16m + r + R g: element (16m + r) % 8 of fragment (16m + r) / 8
+        const int x = 16 * m + r;
+        const uint32_t w = word_of(qf[i][x >> 3], (x & 7) >> 1);
+        dsum += ((x & 1) ? bf16hi_f32(w) : bf16lo_f32(w)) * az[m][r];
+      }
+    dpart[i] = dsum;
+  }
+
+  f32x16 acc[2][NQ];  // O^T of tile i, dv columns 32 m .. 32 m + 31
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int i = 0; i < NQ; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][i][r] = 0.f;
+
+  // ---- causal squared-score attention inside the span -----------------------
+  // Per 32-key block kb and live tile i with kb up to its diagonal:
+  // S = K_kb Q_i^T (KZ MFMAs), P = S^2 (masked above the diagonal on the
+  // diagonal block; the row sums go to the denominator), O_i^T += V_kb^T P
+  // (four MFMAs: two dv halves x two 16-key halves; the lane's score
+  // registers are directly the P fragment in the permuted key order of V^T).
+  // The block's K and V^T fragments are read from LDS once for both tiles.
+  {
+    unsigned kfo[2][KZ];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int kz = 0; kz < KZ; ++kz) {
+        const int krow = 32 * h + c;
+        const int chunk = kz + (R / 8) * g;
+        kfo[h][kz] = static_cast<unsigned>((krow * KCH + (chunk ^ kswz<D>(krow))) * 16);
+      }
+    unsigned vfo[4][2];
+#pragma unroll
+    for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+      for (int kv = 0; kv < 2; ++kv)
+        vfo[sb][kv] = static_cast<unsigned>(
+            (KCHUNKS + c * VCH + ((4 * sb + 2 * kv + g) ^ rswz(c))) * 16);
+    int tdiag[NQ];  // a tile's diagonal block, -1 for a tile beyond the sequence
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) tdiag[i] = __builtin_amdgcn_readfirstlane(tlive[i] ? tile[i] : -1);
+    const int tmax = tdiag[0] > tdiag[1] ? tdiag[0] : tdiag[1];
+
+    auto block = [&](const char* buf, auto sb_c, int kb) __attribute__((always_inline)) {
+      constexpr int sb = decltype(sb_c)::value;
+      if (kb > tmax) return;  // wave-uniform: past both diagonals
+      bf16x8 A[KZ];
+#pragma unroll
+      for (int kz = 0; kz < KZ; ++kz)
+        A[kz] = *reinterpret_cast<const bf16x8*>(buf + (sb >> 1) * (64 * KCH * 16) +
+                                                 kfo[sb & 1][kz]);
+      bf16x8 V[2][2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int kv = 0; kv < 2; ++kv)
+          V[m][kv] = *reinterpret_cast<const bf16x8*>(buf + vfo[sb][kv] + m * (32 * VCH * 16));
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        if (kb > tdiag[i]) continue;  // wave-uniform
+        f32x16 sc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+#pragma unroll
+        for (int kz = 0; kz < KZ; ++kz) sc = mfma32(A[kz], qf[i][kz], sc);
+        uint32_t bw[8];
+        if (kb < tdiag[i]) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float p0 = sc[2 * j] * sc[2 * j];
+            const float p1 = sc[2 * j + 1] * sc[2 * j + 1];
+            dpart[i] += p0 + p1;
+            bw[j] = pack_bf16x2(p0, p1);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int r0 = 2 * j, r1 = 2 * j + 1;
+            const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : sc[r0] * sc[r0];
+            const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : sc[r1] * sc[r1];
+            dpart[i] += p0 + p1;
+            bw[j] = pack_bf16x2(p0, p1);
+          }
+        }
+#pragma unroll
+        for (int kv = 0; kv < 2; ++kv) {
+          const bf16x8 Bp = __builtin_bit_cast(
+              bf16x8, make_uint4(bw[4 * kv], bw[4 * kv + 1], bw[4 * kv + 2], bw[4 * kv + 3]));
+          acc[0][i] = mfma32(V[0][kv], Bp, acc[0][i]);
+          acc[1][i] = mfma32(V[1][kv], Bp, acc[1][i]);
+        }
+      }
+    };
+
+    const char* b0 = reinterpret_cast<const char*>(g_stage0);
+    const char* b1 = reinterpret_cast<const char*>(g_stage1);
+    const char* b2 = reinterpret_cast<const char*>(g_stage2);
+    lds_barrier();  // stage 0 (its copies were waited for with the fragments)
+    if (nstage > 2) issue_i(2, g_stage2);
+    for (int st = 0; st < nstage; ++st) {
+      if (st > 0) {
+        if (st + 1 < nstage) wait_vmcnt<IPW_I>(); else wait_vmcnt<0>();
+        lds_barrier();  // stage st has landed; every wave is done with stage st - 1
+        if (st + 2 < nstage)
+          issue_i(st + 2, const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(b2)));
+      }
+      block(b0, std::integral_constant<int, 0>{}, 4 * st);
+      block(b0, std::integral_constant<int, 1>{}, 4 * st + 1);
+      block(b0, std::integral_constant<int, 2>{}, 4 * st + 2);
+      block(b0, std::integral_constant<int, 3>{}, 4 * st + 3);
+      const char* t = b0;
+      b0 = b1;
+      b1 = b2;
+      b2 = t;
+    }
+    wait_vmcnt<0>();  // the readout's first stages
+    lds_barrier();    // every wave is done with the intra buffers
+  }
+  // Readout stage s sits in buffer (3 + s) % 5 and is copied in four stages
+  // ahead: stages 0 and 1 came with the prologue, 2 to 4 go now (into the
+  // in-span buffers), and stage s + 4 is issued once every wave is done with
+  // stage s - 1, whose buffer it takes.
+  static_for<2, (NSTAGE_R < 5 ? NSTAGE_R : 5)>([&](auto stg_c) { issue_r(stg_c); });
+
+  // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
+  // rotated fp32 query rows: qr[i][x] = q[t][(x + R g) % D]; the lane's own
+  // fragments hold x < R, the lane 32 away holds the rest
+  float qr[NQ][D];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i)
+#pragma unroll
+    for (int kz = 0; kz < KZ; ++kz) {
+      const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
+      const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
+        qr[i][8 * kz + 2 * e] = bf16lo_f32(w[e]);
+        qr[i][8 * kz + 2 * e + 1] = bf16hi_f32(w[e]);
+        qr[i][8 * kz + R + 2 * e] = bf16lo_f32(pw);
+        qr[i][8 * kz + R + 2 * e + 1] = bf16hi_f32(pw);
+      }
+    }
+  // A fragment of K-step kk: row c (and c + 32), chunk (2 (kk % 8) + g) ^ (c % 16)
+  // of the 32 in the row, plus 256 bytes for kk >= 8; formed per K-step (a
+  // XOR and an add) rather than held in eight registers
+  const unsigned arow = static_cast<unsigned>(c * SCH * 16);
+  const unsigned asw = static_cast<unsigned>(g ^ rswz(c));
+  const bool any_live = tlive[0] || tlive[1];
+  static_for<0, NSTAGE_R>([&](auto stg_c) {
+    constexpr int stg = decltype(stg_c)::value;
+    constexpr int k0 = stg * kKC;
+    constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
+    if constexpr (stg >= 2) {
+      // stages stg + 1 .. min(stg + 3, last) may stay in flight
+      constexpr int later = (NSTAGE_R - 1 - stg < 3) ? NSTAGE_R - 1 - stg : 3;
+      wait_vmcnt<IPW_R * later>();
+    }
+    if constexpr (stg >= 1) lds_barrier();  // stage stg landed; stage stg - 1 consumed
+    if constexpr (stg >= 1 && stg + 4 < NSTAGE_R) issue_r(std::integral_constant<int, stg + 4>{});
+    if (!any_live) return;  // wave-uniform: dead tiles only take part in the staging
+    const char* Sb = reinterpret_cast<const char*>(stage_buf((3 + stg) % 5));
+    static_for<0, kc>([&](auto kk_c) {
+      constexpr int kk = decltype(kk_c)::value;
+      constexpr int kap = k0 + kk;
+      constexpr int r1 = (8 * kap) % R, dl = (8 * kap) / R;
+      const char* ap = Sb + arow + ((static_cast<unsigned>(2 * (kk & 7)) ^ asw) << 4) + (kk >> 3) * 256;
+      const bf16x8 A0 = *reinterpret_cast<const bf16x8*>(ap);
+      const bf16x8 A1 = *reinterpret_cast<const bf16x8*>(ap + 32 * SCH * 16);
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        float pr[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pr[j] = qr[i][r1 + j] * qr[i][(r1 + j + dl) % D];
+        const bf16x8 bq = __builtin_bit_cast(
+            bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                               pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+        acc[0][i] = mfma32(A0, bq, acc[0][i]);
+        acc[1][i] = mfma32(A1, bq, acc[1][i]);
+      }
+    });
+  });
+
+  // ---- normalise and store ---------------------------------------------------
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const float Dt = dpart[i] + __shfl_xor(dpart[i], 32);
+    const long long t = tq0[i] + c;
+    if (!tlive[i] || t >= span_end) continue;
+    const float inv = (Dt > 0.f) ? 1.f / Dt : 0.f;
+    float* orow = out + (static_cast<long long>(bh) * T + t) * DV;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        float4 o;
+        o.x = acc[m][i][4 * r4 + 0] * inv;
+        o.y = acc[m][i][4 * r4 + 1] * inv;
+        o.z = acc[m][i][4 * r4 + 2] * inv;
+        o.w = acc[m][i][4 * r4 + 3] * inv;
+        *reinterpret_cast<float4*>(orow + 32 * m + 8 * r4 + 4 * g) = o;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // V^T of a whole head for the quadratic form: vtp[bh][dv][LV] bf16, keys of
 // every 16-key group in the order 0-3, 8-11, 4-7, 12-15 (the key order of the
 // output kernel's P V product, as the state kernel writes it per span), keys
@@ -1673,8 +2050,14 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output_kernel<D, DV, NG, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA,
-                                                              NS, qblocks, sp0, sp0 + cnt);
+    if constexpr (D == 64 && DV == 64 && NG == 1) {
+      const int qb8 = (L + kQB8 - 1) / kQB8;
+      const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
+      span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
+                                                          qb8, sp0, sp0 + cnt);
+    } else
+      span_output_kernel<D, DV, NG, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L,
+                                                                LA, NS, qblocks, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
