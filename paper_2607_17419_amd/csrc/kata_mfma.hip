@@ -319,7 +319,7 @@ __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 
 constexpr int kTB2 = 128;           // tokens per staged block
 constexpr int kRow2 = kTB2 + 8;     // K^T / V^T row length in LDS (fp16): rows 272 B apart
 constexpr int kGapK2 = 64;          // fp16 gap (32 banks) before key rows DM/2, DM, ... (krow)
-constexpr int kUW = 6;              // slot tiles per slot wave
+constexpr int kUW = 6;              // slot tiles per slot wave (four-wave form)
 constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
 
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
@@ -335,12 +335,18 @@ __device__ __forceinline__ void mfma16(f32x16& acc, const f16x8& a, const f16x8&
   asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 
+// Workgroup shape of K2.  d = 64 with one feature block runs eight waves of
+// three slot tiles (two waves per SIMD: one wave's feature products and
+// staging issue while the other's MFMAs run); the other shapes run four
+// waves of six tiles, one per SIMD.
 template <int D, int DV, int NG>
 struct StateGrid {
+  static constexpr int NW = (D == 64 && NG == 1) ? 8 : 4;  // waves per workgroup
+  static constexpr int UW = NW == 8 ? 3 : kUW;             // slot tiles per slot wave
   // slot waves per feature block (a wave's tiles never straddle two blocks)
-  static constexpr int NUWB = (GeoG<D, DV, NG>::NSTM + kUW - 1) / kUW;
-  static constexpr int NUW = NG * NUWB;        // slot waves per span
-  static constexpr int NB = (NUW + 1 + 3) / 4;  // workgroups per span
+  static constexpr int NUWB = (GeoG<D, DV, NG>::NSTM + UW - 1) / UW;
+  static constexpr int NUW = NG * NUWB;                   // slot waves per span
+  static constexpr int NB = (NUW + 1 + NW - 1) / NW;      // workgroups per span
 };
 
 // Largest |x| of the bf16 values in the 32-bit words of v, as a bf16 bit
@@ -362,7 +368,7 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
 }
 
 template <int D, int DV, int NG>
-__global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restrict__ k,
+__global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_kernel(const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ spanst,
                                                          uint16_t* __restrict__ vtp, int T,
@@ -370,10 +376,11 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
                                                          int nsp) {
   using G = GeoG<D, DV, NG>;
   using SG = StateGrid<D, DV, NG>;
-  constexpr int UW = kUW;
+  constexpr int UW = SG::UW;
+  constexpr int NW = SG::NW;
+  constexpr int NTH = 64 * NW;  // threads per workgroup
   constexpr int DM = G::DM;
   constexpr int NXR = DM / 32;  // distinct x rows per lane (x depends on tile % NXR)
-  static_assert(UW % NXR == 0, "unit parity must be static");
   static_assert(G::MT == 2, "the slot loop issues the two dv tiles of a slot tile together");
   constexpr int KS = kTB2 / 16;                      // K-steps per staged block
   // Key row r of a K buffer starts at krow(r) (fp16 elements).  The slot tiles
@@ -400,7 +407,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   const int sp = sp0 + 8 * (jx / SG::NB) + (id & 7);
   if (sp >= nsp) return;  // whole workgroup: padding of the grid
   const int s = sp % NS, bh = sp / NS;
-  const int gw = part * 4 + wave;  // wave index inside the span
+  const int gw = part * NW + wave;  // wave index inside the span
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
@@ -413,8 +420,8 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   constexpr int KG = D / 8, VG = DV / 8;
   constexpr int NPAIR = kTB2 / 2;
   constexpr int NTASK = NPAIR * (KG + VG);
-  static_assert(NTASK % 256 == 0 && NPAIR == 64, "staging: one token pair per lane");
-  constexpr int TPT = NTASK / 256;
+  static_assert(NTASK % NTH == 0 && NPAIR == 64, "staging: one token pair per lane");
+  constexpr int TPT = NTASK / NTH;
   uint4 st_lo[TPT], st_hi[TPT];
   // Fetch / commit the staging tasks [i0, i1) of this thread for the block
   // starting at token t0.  The loads are unconditional (token index clamped
@@ -424,7 +431,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   auto fetch = [&](long long t0, auto i0_c, auto i1_c) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
-      const int cg = wave + 4 * i, p = lane;  // wave-uniform column group
+      const int cg = wave + NW * i, p = lane;  // wave-uniform column group
       const long long ta = min(t0 + 2 * p, static_cast<long long>(T) - 1);
       const long long tb = min(t0 + 2 * p + 1, static_cast<long long>(T) - 1);
       if (cg < KG) {
@@ -446,7 +453,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
     constexpr bool SC = decltype(sc_c)::value;
 #pragma unroll
     for (int i = decltype(i0_c)::value; i < decltype(i1_c)::value; ++i) {
-      const int cg = wave + 4 * i, p = lane;
+      const int cg = wave + NW * i, p = lane;
       const bool va = t0 + 2 * p < span_end, vb = t0 + 2 * p + 1 < span_end;
       const uint32_t a[4] = {st_lo[i].x, st_lo[i].y, st_lo[i].z, st_lo[i].w};
       const uint32_t b[4] = {st_hi[i].x, st_hi[i].y, st_hi[i].z, st_hi[i].w};
@@ -509,7 +516,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   uint32_t mk = 0u, mv = 0u;
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
-    if (wave + 4 * i < KG) {
+    if (wave + NW * i < KG) {
       mk = absmax_bits(absmax_bits(mk, st_lo[i]), st_hi[i]);
     } else {
       mv = absmax_bits(absmax_bits(mv, st_lo[i]), st_hi[i]);
@@ -532,7 +539,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
   auto span_scales = [&]() __attribute__((always_inline)) {
     uint32_t m2k = 0u, m2v = 0u;
     const long long n16 = (span_end - span0) * ((D + DV) / 8);  // 16-byte pieces
-    for (long long j = tid; j < n16; j += 256) {
+    for (long long j = tid; j < n16; j += NTH) {
       const long long t = span0 + j / ((D + DV) / 8);
       const int pc = static_cast<int>(j % ((D + DV) / 8));
       if (pc < KG) m2k = absmax_bits(m2k, *reinterpret_cast<const uint4*>(kh + t * D + 8 * pc));
@@ -644,10 +651,12 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       const int unit0 = (gw % SG::NUWB) * UW;
       // per-lane byte offsets of the fragments inside buffer 0, column 8*g
       unsigned xo[NXR], yo[UW], vo[G::MT];
+      // fx[p] serves the local tiles u with u % NXR == p, whose x row is that
+      // of global tile parity (unit0 + p) % NXR
 #pragma unroll
       for (int p = 0; p < NXR; ++p) {
         int xr, yy;
-        slot_pair<DM>(32 * p + c, xr, yy);
+        slot_pair<DM>(32 * ((unit0 + p) % NXR) + c, xr, yy);
         xo[p] = static_cast<unsigned>((krow(DM * blk + xr) + 8 * g) * 2);
       }
 #pragma unroll
@@ -661,6 +670,10 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       for (int m = 0; m < G::MT; ++m)
         vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
 
+      // Accumulators: with one wave per SIMD in AGPRs, fed by MFMAs from
+      // inline assembly with hand-counted wait states; with two waves per
+      // SIMD (256 registers each) by compiler builtins, which place them and
+      // insert the wait states.
       f32x16 acc[UW][G::MT];
 #pragma unroll
       for (int u = 0; u < UW; ++u)
@@ -668,8 +681,16 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
         for (int m = 0; m < G::MT; ++m) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
-          asm volatile("" : "+a"(acc[u][m]));
+          if constexpr (NW != 8) asm volatile("" : "+a"(acc[u][m]));
         }
+      auto mf_first = [](f32x16& a, const f16x8& x, const f16x8& y) __attribute__((always_inline)) {
+        if constexpr (NW == 8) a = __builtin_amdgcn_mfma_f32_32x32x16_f16(x, y, a, 0, 0, 0);
+        else mfma16_first(a, x, y);
+      };
+      auto mf = [](f32x16& a, const f16x8& x, const f16x8& y) __attribute__((always_inline)) {
+        if constexpr (NW == 8) a = __builtin_amdgcn_mfma_f32_32x32x16_f16(x, y, a, 0, 0, 0);
+        else mfma16(a, x, y);
+      };
 
       // LDS fragments: the y rows of the slot tiles (8 fp16 tokens each,
       // reloaded for the next K-step as soon as the features they feed are
@@ -747,17 +768,17 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
               // after the last product it reads (two wait states needed),
               // so no s_nop is needed there
               constexpr int un = (u + 1 < UW) ? u + 1 : 0;
-              mfma16_first(acc[u][0], va0, bq[0]);
+              mf_first(acc[u][0], va0, bq[0]);
               __builtin_amdgcn_sched_barrier(0);
               const f16x8 nb = fx[un % NXR] * fy[un];
               __builtin_amdgcn_sched_barrier(0);
-              mfma16(acc[u][1], va1, bq[0]);
+              mf(acc[u][1], va1, bq[0]);
               __builtin_amdgcn_sched_barrier(0);
               push(nb);
             } else {
               // the block's last tile: its features are one instruction old
-              mfma16_first(acc[u][0], va0, bq[0]);
-              mfma16(acc[u][1], va1, bq[0]);
+              mf_first(acc[u][0], va0, bq[0]);
+              mf(acc[u][1], va1, bq[0]);
             }
             if constexpr (u + 1 < UW && ks + 1 < KS) {
               if constexpr (u == 0) fy[0] = ld16(kb + yo[0] + kn);
@@ -779,15 +800,16 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
       // go through LDS (this wave's own region of the free staging buffers,
       // [dv][HU*32 + 8] bf16, HU tiles at a time) so that the record is
       // written in 16-byte pieces of 8 consecutive slots.
-      constexpr int HU = UW / 2;       // tiles per round
-      constexpr int RS = HU * 32 + 8;  // bf16 per LDS row (16-byte aligned rows)
-      static_assert(UW % 2 == 0 && 4 * DV * RS <= POOL, "record rounds fit the staging LDS");
+      constexpr int HU = (UW + 1) / 2;  // tiles per round (the second may have fewer)
+      constexpr int RS = HU * 32 + 8;   // bf16 per LDS row (16-byte aligned rows)
+      static_assert(NW * DV * RS <= POOL, "record rounds fit the staging LDS");
       uint16_t* ep = &pool[wave * DV * RS];
       constexpr int CPR = HU * 4;  // 16-byte pieces per row and round
       static_for<0, 2>([&](auto h_c) {
         constexpr int h = decltype(h_c)::value;
+        constexpr int NU = (h == 0) ? HU : UW - HU;  // tiles of this round
 #pragma unroll
-        for (int uu = 0; uu < HU; ++uu) {
+        for (int uu = 0; uu < NU; ++uu) {
           const int u = h * HU + uu;
 #pragma unroll
           for (int m = 0; m < G::MT; ++m)
@@ -812,7 +834,7 @@ __global__ __launch_bounds__(256) void span_state_kernel(const uint16_t* __restr
           const int kc = lane + 64 * i;
           const int row = kc / CPR, pc = kc % CPR;
           const uint4 w = *reinterpret_cast<const uint4*>(ep + row * RS + 8 * pc);
-          if (unit0 + h * HU + pc / 4 < G::NSTM)
+          if (pc / 4 < NU && unit0 + h * HU + pc / 4 < G::NSTM)
             *reinterpret_cast<uint4*>(rec + static_cast<long long>(row) * G::NSLOT +
                                       32 * (blk * G::NSTM + unit0 + h * HU) + 8 * pc) = w;
         }
@@ -2039,7 +2061,7 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb2 = 8u * StateGrid<D, DV, NG>::NB * static_cast<unsigned>((cnt + 7) / 8);
-    span_state_kernel<D, DV, NG><<<nb2, 256, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
+    span_state_kernel<D, DV, NG><<<nb2, 64 * StateGrid<D, DV, NG>::NW, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
                                                       sp0 + cnt);
   }
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
