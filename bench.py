@@ -665,7 +665,7 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
 # quadratic-form instantiations share the names, not the template arguments)
 KERNELS = {"span_state": "span_state_kernel<64, 64, 1>",
            "scan": "scan_exclusive_bf16<8, kata::SlotWeight<64, 64, 1> >",
-           "span_output": "span_output_kernel<64, 64, 1, false>"}
+           "span_output": "span_output8_kernel<64, 64, 1>"}
 COPY_BYTES = 1 << 30
 # the linear-feature kernels of psi(x) = x (plain readout) at d = dv = 64
 LIN_KERNELS = {"span_state": "lin_span_state<0>",

@@ -1593,8 +1593,9 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// K4, eight-wave form (d = dv = 64, one feature block).  Same records, V^T
-// layout and stage buffers as span_output_kernel, but 512 threads owning 512
+// K4, eight-wave form (dv = 64; d = 64 with one or two feature blocks, d =
+// 32).  Same records, V^T layout and stage buffers as span_output_kernel
+// (which keeps the quadratic form), but 512 threads owning 512
 // queries (16 tiles of 32): wave w holds tiles w and 15 - w, so two waves
 // share each SIMD with balanced causal work (waves w and w + 4 hold tiles
 // adding up to 30), and one wave's VALU work (squared scores, query feature
@@ -1616,8 +1617,8 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
     const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
     int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
-  static_assert(D == 64 && DV == 64 && NG == 1, "the eight-wave form covers d = dv = 64, g = 1");
-  constexpr int R = G::RM, KZ = G::KZ;
+  static_assert(DV == 64, "the eight-wave form covers dv = 64");
+  constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM, KZ = G::KZ;
   constexpr int W = 8, NQ = 2, NT = kQB8 / 32;
   constexpr int KCH = D / 8;                    // 16-byte chunks per key row
   constexpr int KCHUNKS = kKB * KCH;            // K rows of one intra stage
@@ -1633,7 +1634,7 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   static_assert(SCHUNKS * 16 <= kStageBytes && SCHUNKS % (64 * W) == 0, "readout stage size");
   constexpr int IPW_R = SCHUNKS / (64 * W);
   constexpr int NSTAGE_R = (G::NKS + kKC - 1) / kKC;
-  static_assert(G::MT == 2 && G::ZMB == 2, "two dv tiles, two Z tiles");
+  static_assert(G::MT == 2, "two dv tiles");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -1669,17 +1670,14 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   const int last_key_tile = static_cast<int>((span_end - 1 - span0) / 32);
   if (last_tile > last_key_tile) last_tile = last_key_tile;
   const int nstage = (last_tile + 1 + 3) / 4;  // 128-key intra stages
-  // Copy i of a lane writes LDS chunk P = 512 i + 64 wave + lane.  Its source
-  // row grows by a constant with i and the XOR swizzle of its chunk does not
-  // depend on i (kswz uses the row's low three bits and bits 3-5 of the row
-  // minus 64 i; rswz the row's low four bits), so one offset per operand
-  // serves all of a lane's copies:
-  //   K    row 64 i + 8 wave + lane / 8,   chunk lane % 8
+  // Copy i of a lane writes LDS chunk P = 512 i + 64 wave + lane.  K rows are
+  // KCH chunks long and their copies are formed per copy (one or two per
+  // stage).  For V^T and S^T the source row grows by a constant with i and the
+  // XOR swizzle of the lane's chunk does not depend on i (rswz uses the row's
+  // low four bits), so one offset per operand serves all of a lane's copies:
   //   V^T  row 32 i' + 4 wave + lane / 16, chunk lane % 16 (i' = i - IPW_K)
   //   S^T  row 16 i + 2 wave + lane / 32,  chunk lane % 32
-  static_assert(KCH == 8 && VCH == 16 && SCH == 32 && W == 8, "copy geometry");
-  const int krow0 = 8 * wave + (lane >> 3);
-  const int ksrc0 = krow0 * D + 8 * ((lane & 7) ^ kswz<D>(krow0));
+  static_assert(VCH == 16 && SCH == 32 && W == 8 && KCHUNKS % 512 == 0, "copy geometry");
   const int vrow0 = 4 * wave + (lane >> 4);
   const int vsrc0 = vrow0 * LV + 8 * ((lane & 15) ^ rswz(vrow0));
   const int rrow0 = 2 * wave + g;
@@ -1691,9 +1689,11 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
     for (int i = 0; i < IPW_I; ++i) {
       const void* src;
       if (i < IPW_K) {
+        const int P = (i * W + wave) * 64 + lane;
+        const int r = P / KCH, pos = P % KCH;
         // keys past the sequence: re-read the last row (never used)
-        const long long over = key0 + krow0 + 64 * i - (T - 1);
-        src = kh + key0 * D + ksrc0 + 64 * i * D - (over > 0 ? over * D : 0);
+        const long long over = key0 + r - (T - 1);
+        src = kh + (key0 + r) * D + 8 * (pos ^ kswz<D>(r)) - (over > 0 ? over * D : 0);
       } else {
         src = vt_rec + st * kKB + vsrc0 + 32 * (i - IPW_K) * LV;
       }
@@ -1719,53 +1719,63 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   // every fragment is consumed, so no load is left to be waited for behind
   // later copies), then issues in-span stage 1 and readout stages 0 and 1.
   issue_i(0, g_stage0);
-  bf16x8 qf[NQ][KZ];  // q[t][8 kz + R g .. +7] of this lane's query t = tq0 + c
+  // qf[i][KZM bb + kz] holds q[t][DM bb + 8 kz + RM g .. +7] of this lane's
+  // query t = tq0 + c, per feature block bb
+  bf16x8 qf[NQ][KZ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     const long long t = min(tq0[i] + c, static_cast<long long>(T) - 1);
 #pragma unroll
     for (int kz = 0; kz < KZ; ++kz)
-      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + 8 * kz + R * g);
+      qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + DM * (kz / KZM) +
+                                                   8 * (kz % KZM) + RM * g);
   }
-  bf16x8 zA[G::ZMB][KZ];
+  // Z_pre operand fragments of each feature block
+  bf16x8 zA[NG][G::ZMB][KZM];
 #pragma unroll
-  for (int m = 0; m < G::ZMB; ++m)
+  for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-    for (int kz = 0; kz < KZ; ++kz)
-      zA[m][kz] = *reinterpret_cast<const bf16x8*>(rec + G::ES + ((m * KZ + kz) * 64 + lane) * 8);
+    for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+      for (int kz = 0; kz < KZM; ++kz)
+        zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(
+            rec + G::ES + static_cast<long long>(bb) * DM * DM + ((m * KZM + kz) * 64 + lane) * 8);
 #pragma unroll
   for (int i = 0; i < NQ; ++i)
 #pragma unroll
     for (int kz = 0; kz < KZ; ++kz) asm volatile("" ::"v"(qf[i][kz]));
 #pragma unroll
-  for (int m = 0; m < G::ZMB; ++m)
+  for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-    for (int kz = 0; kz < KZ; ++kz) asm volatile("" ::"v"(zA[m][kz]));
+    for (int m = 0; m < G::ZMB; ++m)
+#pragma unroll
+      for (int kz = 0; kz < KZM; ++kz) asm volatile("" ::"v"(zA[bb][m][kz]));
   if (nstage > 1) issue_i(1, g_stage1);
   issue_r(std::integral_constant<int, 0>{});
   if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
 
-  // ---- denominator from the prefix: q^T Z_pre q ------------------------------
+  // ---- denominator from the prefix: sum over blocks of q_bb^T Z_bb q_bb ------
   float dpart[NQ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
-    f32x16 az[G::ZMB];
-#pragma unroll
-    for (int m = 0; m < G::ZMB; ++m) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) az[m][r] = 0.f;
-#pragma unroll
-      for (int kz = 0; kz < KZ; ++kz) az[m] = mfma32(zA[m][kz], qf[i][kz], az[m]);
-    }
     float dsum = 0.f;
 #pragma unroll
-    for (int m = 0; m < G::ZMB; ++m)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        // row sigma = 16m + r + R g: element (16m + r) % 8 of fragment (16m + r) / 8
-        const int x = 16 * m + r;
-        const uint32_t w = word_of(qf[i][x >> 3], (x & 7) >> 1);
-        dsum += ((x & 1) ? bf16hi_f32(w) : bf16lo_f32(w)) * az[m][r];
+      for (int m = 0; m < G::ZMB; ++m) {
+        f32x16 az;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) az[r] = 0.f;
+#pragma unroll
+        for (int kz = 0; kz < KZM; ++kz) az = mfma32(zA[bb][m][kz], qf[i][KZM * bb + kz], az);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          // row sigma = 16m + r + RM g of block bb: element (16m + r) % 8 of the
+          // block's fragment (16m + r) / 8
+          const int x = 16 * m + r;
+          const uint32_t w = word_of(qf[i][KZM * bb + (x >> 3)], (x & 7) >> 1);
+          dsum += ((x & 1) ? bf16hi_f32(w) : bf16lo_f32(w)) * az[r];
+        }
       }
     dpart[i] = dsum;
   }
@@ -1792,7 +1802,7 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 #pragma unroll
       for (int kz = 0; kz < KZ; ++kz) {
         const int krow = 32 * h + c;
-        const int chunk = kz + (R / 8) * g;
+        const int chunk = (DM / 8) * (kz / KZM) + (kz % KZM) + (RM / 8) * g;
         kfo[h][kz] = static_cast<unsigned>((krow * KCH + (chunk ^ kswz<D>(krow))) * 16);
       }
     unsigned vfo[4][2];
@@ -1824,17 +1834,28 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 #pragma unroll
       for (int i = 0; i < NQ; ++i) {
         if (kb > tdiag[i]) continue;  // wave-uniform
-        f32x16 sc;
+        // scores per feature block; the weight is the sum of their squares
+        f32x16 sc[NG];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+        for (int bb = 0; bb < NG; ++bb) {
 #pragma unroll
-        for (int kz = 0; kz < KZ; ++kz) sc = mfma32(A[kz], qf[i][kz], sc);
+          for (int r = 0; r < 16; ++r) sc[bb][r] = 0.f;
+#pragma unroll
+          for (int kz = 0; kz < KZM; ++kz)
+            sc[bb] = mfma32(A[KZM * bb + kz], qf[i][KZM * bb + kz], sc[bb]);
+        }
+        auto p_of = [&](int r) __attribute__((always_inline)) {
+          float p = sc[0][r] * sc[0][r];
+#pragma unroll
+          for (int bb = 1; bb < NG; ++bb) p += sc[bb][r] * sc[bb][r];
+          return p;
+        };
         uint32_t bw[8];
         if (kb < tdiag[i]) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const float p0 = sc[2 * j] * sc[2 * j];
-            const float p1 = sc[2 * j + 1] * sc[2 * j + 1];
+            const float p0 = p_of(2 * j);
+            const float p1 = p_of(2 * j + 1);
             dpart[i] += p0 + p1;
             bw[j] = pack_bf16x2(p0, p1);
           }
@@ -1842,8 +1863,8 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int r0 = 2 * j, r1 = 2 * j + 1;
-            const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : sc[r0] * sc[r0];
-            const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : sc[r1] * sc[r1];
+            const float p0 = (8 * (r0 >> 2) + 4 * g + (r0 & 3) > c) ? 0.f : p_of(r0);
+            const float p1 = (8 * (r1 >> 2) + 4 * g + (r1 & 3) > c) ? 0.f : p_of(r1);
             dpart[i] += p0 + p1;
             bw[j] = pack_bf16x2(p0, p1);
           }
@@ -1889,22 +1910,24 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   static_for<2, (NSTAGE_R < 5 ? NSTAGE_R : 5)>([&](auto stg_c) { issue_r(stg_c); });
 
   // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
-  // rotated fp32 query rows: qr[i][x] = q[t][(x + R g) % D]; the lane's own
-  // fragments hold x < R, the lane 32 away holds the rest
+  // rotated fp32 query rows per feature block:
+  // qr[i][DM bb + x] = q[t][DM bb + (x + RM g) % DM]; the lane's own
+  // fragments of block bb hold x < RM, the lane 32 away holds the rest
   float qr[NQ][D];
 #pragma unroll
   for (int i = 0; i < NQ; ++i)
 #pragma unroll
     for (int kz = 0; kz < KZ; ++kz) {
+      const int base = DM * (kz / KZM) + 8 * (kz % KZM);
       const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
       const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
-        qr[i][8 * kz + 2 * e] = bf16lo_f32(w[e]);
-        qr[i][8 * kz + 2 * e + 1] = bf16hi_f32(w[e]);
-        qr[i][8 * kz + R + 2 * e] = bf16lo_f32(pw);
-        qr[i][8 * kz + R + 2 * e + 1] = bf16hi_f32(pw);
+        qr[i][base + 2 * e] = bf16lo_f32(w[e]);
+        qr[i][base + 2 * e + 1] = bf16hi_f32(w[e]);
+        qr[i][base + RM + 2 * e] = bf16lo_f32(pw);
+        qr[i][base + RM + 2 * e + 1] = bf16hi_f32(pw);
       }
     }
   // A fragment of K-step kk: row c (and c + 32), chunk (2 (kk % 8) + g) ^ (c % 16)
@@ -1929,7 +1952,10 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
     static_for<0, kc>([&](auto kk_c) {
       constexpr int kk = decltype(kk_c)::value;
       constexpr int kap = k0 + kk;
-      constexpr int r1 = (8 * kap) % R, dl = (8 * kap) / R;
+      // K-step kl of feature block bb: slots 16 kl + 8 g + j pair registers
+      // r1 + j and r1 + j + dl of the block's rotated row
+      constexpr int bb = kap / G::NKSM, kl = kap % G::NKSM;
+      constexpr int r1 = (8 * kl) % RM, dl = (8 * kl) / RM;
       const char* ap = Sb + arow + ((static_cast<unsigned>(2 * (kk & 7)) ^ asw) << 4) + (kk >> 3) * 256;
       const bf16x8 A0 = *reinterpret_cast<const bf16x8*>(ap);
       const bf16x8 A1 = *reinterpret_cast<const bf16x8*>(ap + 32 * SCH * 16);
@@ -1937,7 +1963,8 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
       for (int i = 0; i < NQ; ++i) {
         float pr[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) pr[j] = qr[i][r1 + j] * qr[i][(r1 + j + dl) % D];
+        for (int j = 0; j < 8; ++j)
+          pr[j] = qr[i][DM * bb + r1 + j] * qr[i][DM * bb + (r1 + j + dl) % DM];
         const bf16x8 bq = __builtin_bit_cast(
             bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
                                pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
@@ -2068,18 +2095,12 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   launch_scan_exclusive_bf16(spanst, NS, G::E, static_cast<long long>(NS) * G::E, BH,
                              SlotWeight<D, DV, NG>{}, st);
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
-  const int qblocks = (L + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
+  const int qb8 = (L + kQB8 - 1) / kQB8;
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
-    const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    if constexpr (D == 64 && DV == 64 && NG == 1) {
-      const int qb8 = (L + kQB8 - 1) / kQB8;
-      const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
-      span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
-                                                          qb8, sp0, sp0 + cnt);
-    } else
-      span_output_kernel<D, DV, NG, false><<<nb4, 256, 0, st>>>(qq, kk, spanst, vtp, out, T, L,
-                                                                LA, NS, qblocks, sp0, sp0 + cnt);
+    const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
+    span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
+                                                        qb8, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
