@@ -341,7 +341,7 @@ __device__ __forceinline__ void mfma16(f32x16& acc, const f16x8& a, const f16x8&
 // waves of six tiles, one per SIMD.
 template <int D, int DV, int NG>
 struct StateGrid {
-  static constexpr int NW = (D == 64 && NG == 1) ? 8 : 4;  // waves per workgroup
+  static constexpr int NW = D == 64 ? 8 : 4;  // waves per workgroup
   static constexpr int UW = NW == 8 ? 3 : kUW;             // slot tiles per slot wave
   // slot waves per feature block (a wave's tiles never straddle two blocks)
   static constexpr int NUWB = (GeoG<D, DV, NG>::NSTM + UW - 1) / UW;
