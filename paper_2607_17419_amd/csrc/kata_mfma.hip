@@ -200,60 +200,19 @@ __device__ __forceinline__ uint32_t word_of(const bf16x8& f, int j) {
   return j == 0 ? w.x : (j == 1 ? w.y : (j == 2 ? w.z : w.w));
 }
 
-// The two MFMAs of one tile (a0 += A0 * bf, a1 += A1 * bf: the two 32-wide
-// halves of dv) with the eight feature products of the next tile
-// (p_j = x_j * y_j, fp32) issued between them.  A wave issues in order and an
-// MFMA holds the matrix pipe for 32 cycles: the products take about as long
-// as the first MFMA, so the second issues without waiting, and the
-// conversions that follow run under it.  s_nop 1 first: a VALU write of bf
-// (its conversion) must be 2 wait states old when the MFMA reads it.  The
-// accumulators stay in AGPRs, which no VALU instruction writes; any later
-// read of them waits for the MFMA first (mfma_drain).
-__device__ __forceinline__ void mfma2_prod8(f32x16& a0, f32x16& a1, const bf16x8& A0,
-                                            const bf16x8& A1, const bf16x8& bf,
-                                            const float x[8], const float y[8], float p[8]) {
-  asm volatile(
-      "s_nop 1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %10, %12, %0\n\t"
-      "v_mul_f32 %2, %13, %21\n\t"
-      "v_mul_f32 %3, %14, %22\n\t"
-      "v_mul_f32 %4, %15, %23\n\t"
-      "v_mul_f32 %5, %16, %24\n\t"
-      "v_mul_f32 %6, %17, %25\n\t"
-      "v_mul_f32 %7, %18, %26\n\t"
-      "v_mul_f32 %8, %19, %27\n\t"
-      "v_mul_f32 %9, %20, %28\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %11, %12, %1"
-      : "+a"(a0), "+a"(a1), "=&v"(p[0]), "=&v"(p[1]), "=&v"(p[2]), "=&v"(p[3]), "=&v"(p[4]),
-        "=&v"(p[5]), "=&v"(p[6]), "=&v"(p[7])
-      : "v"(A0), "v"(A1), "v"(bf), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]),
-        "v"(x[5]), "v"(x[6]), "v"(x[7]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "v"(y[4]),
-        "v"(y[5]), "v"(y[6]), "v"(y[7]));
-}
-
-// The two MFMAs of the last slot tile of a staged block (nothing to overlap).
-__device__ __forceinline__ void mfma2(f32x16& a0, f32x16& a1, const bf16x8& va0,
-                                      const bf16x8& va1, const bf16x8& bf) {
-  asm volatile(
-      "s_nop 1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %3, %4, %1"
-      : "+a"(a0), "+a"(a1)
-      : "v"(va0), "v"(va1), "v"(bf));
-}
-
-// Single MFMAs from inline assembly, for sequences whose order the caller
-// fixes with scheduling barriers: mfma_a accumulates into AGPRs, mfma_vz and
-// mfma_v start and continue a chain in VGPRs (read by VALU afterwards, which
-// the caller keeps at least two MFMA issues away from the chain's last MFMA).
+// Single MFMAs for sequences whose order the caller fixes with scheduling
+// barriers (compiler builtins: the compiler inserts the wait states between
+// an MFMA and the VALU instructions around it): mfma_a and mfma_v accumulate,
+// mfma_vz starts a chain from zero.
 __device__ __forceinline__ void mfma_a(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
 }
 __device__ __forceinline__ void mfma_vz(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
+  const f32x16 z = {};
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, z, 0, 0, 0);
 }
 __device__ __forceinline__ void mfma_v(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
 }
 
 // Keeps the operand registers of recently issued MFMAs live up to this point,
@@ -267,12 +226,6 @@ __device__ __forceinline__ void hold1(const T& x) {
 template <typename... Ts>
 __device__ __forceinline__ void hold(const Ts&... xs) {
   (hold1(xs), ...);
-}
-
-// Wait states after MFMAs issued from inline assembly, before any other
-// instruction reads their accumulators (covers the 16-pass case).
-__device__ __forceinline__ void mfma_drain() {
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
 // XOR swizzles of 16-byte chunks inside LDS rows; a row's logical chunk c is
@@ -325,24 +278,14 @@ constexpr int kNBuf2 = 3;           // LDS ring of staged blocks
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
 
-// fp16 MFMAs of the state kernel from inline assembly (AGPR accumulators).
-// The first one of a slot tile starts with s_nop 1: its B fragment comes from
-// the VALU (the feature products), at most one instruction earlier.
-__device__ __forceinline__ void mfma16_first(f32x16& acc, const f16x8& a, const f16x8& b) {
-  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-__device__ __forceinline__ void mfma16(f32x16& acc, const f16x8& a, const f16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-
-// Workgroup shape of K2.  d = 64 with one feature block runs eight waves of
-// three slot tiles (two waves per SIMD: one wave's feature products and
-// staging issue while the other's MFMAs run); the other shapes run four
-// waves of six tiles, one per SIMD.
+// Workgroup shape of K2.  d = 64 runs eight waves of three slot tiles (two
+// waves per SIMD: one wave's feature products and staging issue while the
+// other's MFMAs run); d = 32 runs four waves of six tiles, one per SIMD (its
+// staging tasks do not divide over 512 threads).
 template <int D, int DV, int NG>
 struct StateGrid {
   static constexpr int NW = D == 64 ? 8 : 4;  // waves per workgroup
-  static constexpr int UW = NW == 8 ? 3 : kUW;             // slot tiles per slot wave
+  static constexpr int UW = NW == 8 ? 3 : kUW;  // slot tiles per slot wave
   // slot waves per feature block (a wave's tiles never straddle two blocks)
   static constexpr int NUWB = (GeoG<D, DV, NG>::NSTM + UW - 1) / UW;
   static constexpr int NUW = NG * NUWB;                   // slot waves per span
@@ -670,26 +613,17 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
       for (int m = 0; m < G::MT; ++m)
         vo[m] = static_cast<unsigned>(((32 * m + c) * kRow2 + 8 * g) * 2);
 
-      // Accumulators: with one wave per SIMD in AGPRs, fed by MFMAs from
-      // inline assembly with hand-counted wait states; with two waves per
-      // SIMD (256 registers each) by compiler builtins, which place them and
-      // insert the wait states.
+      // Accumulators fed by compiler-builtin MFMAs: the compiler places them
+      // and inserts the wait states.
       f32x16 acc[UW][G::MT];
 #pragma unroll
       for (int u = 0; u < UW; ++u)
 #pragma unroll
-        for (int m = 0; m < G::MT; ++m) {
+        for (int m = 0; m < G::MT; ++m)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[u][m][r] = 0.f;
-          if constexpr (NW != 8) asm volatile("" : "+a"(acc[u][m]));
-        }
-      auto mf_first = [](f32x16& a, const f16x8& x, const f16x8& y) __attribute__((always_inline)) {
-        if constexpr (NW == 8) a = __builtin_amdgcn_mfma_f32_32x32x16_f16(x, y, a, 0, 0, 0);
-        else mfma16_first(a, x, y);
-      };
       auto mf = [](f32x16& a, const f16x8& x, const f16x8& y) __attribute__((always_inline)) {
-        if constexpr (NW == 8) a = __builtin_amdgcn_mfma_f32_32x32x16_f16(x, y, a, 0, 0, 0);
-        else mfma16(a, x, y);
+        a = __builtin_amdgcn_mfma_f32_32x32x16_f16(x, y, a, 0, 0, 0);
       };
 
       // LDS fragments: the y rows of the slot tiles (8 fp16 tokens each,
@@ -763,12 +697,9 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
             if constexpr (ks + 1 < KS && u > 0) fy[u] = ld16(kb + yo[u] + kn);
             if constexpr (u + 1 < UW || ks + 1 < KS) {
               // the next tile's features (tile u+1 of this K-step, or tile 0
-              // of the next one), half before and half after the first MFMA:
-              // the next tile's first MFMA then comes three instructions
-              // after the last product it reads (two wait states needed),
-              // so no s_nop is needed there
+              // of the next one) between the tile's two MFMAs
               constexpr int un = (u + 1 < UW) ? u + 1 : 0;
-              mf_first(acc[u][0], va0, bq[0]);
+              mf(acc[u][0], va0, bq[0]);
               __builtin_amdgcn_sched_barrier(0);
               const f16x8 nb = fx[un % NXR] * fy[un];
               __builtin_amdgcn_sched_barrier(0);
@@ -777,7 +708,7 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
               push(nb);
             } else {
               // the block's last tile: its features are one instruction old
-              mf_first(acc[u][0], va0, bq[0]);
+              mf(acc[u][0], va0, bq[0]);
               mf(acc[u][1], va1, bq[0]);
             }
             if constexpr (u + 1 < UW && ks + 1 < KS) {
@@ -793,7 +724,6 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
         });
         lds_barrier();
       }
-      mfma_drain();
 
       // Write this wave's tiles of the span record (bf16), undoing the scales.
       // The accumulators hold 4 consecutive dv rows of one slot per lane; they
@@ -863,19 +793,20 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
 }
 
 // ---------------------------------------------------------------------------
-// K4: span output.  1-D grid of workgroups of 256 threads (4 waves), one per
-// CU (160 KB of LDS in five 32 KB stage buffers).  A span has QB = L/256
-// query blocks; block id -> (span, query block) keeps the query blocks of a
-// span on one XCD (equal id % 8), dispatched back to back, so they share the
-// span's prefix record and keys in that XCD's L2.
-// The workgroup owns 8 query tiles of 32 (span-relative tile index 8*qb + i);
-// wave w takes tiles {w, 7-w}, which balances the causal work.
-// Operands are staged by direct global -> LDS copies, three stages deep, so no
-// registers hold staged data and the copies of stage s+2 overlap the
-// arithmetic of stage s.  LDS fragment reads use per-lane offsets computed
-// once, so every read is a base register plus an immediate.
-// pre[bh][s][E] bf16: weighted S_pre^T as [dv][NSLOT], then Z_pre (operand order).
-// vtp[bh][s][dv][L] bf16: the span's V^T (permuted keys, see K2).
+// Quadratic form (and the stage buffers of K4).  quadratic_kernel: 1-D grid
+// of workgroups of 256 threads (4 waves), one per CU (LDS: the five 32 KB
+// stage buffers, of which it uses three).  A head (one span covering the
+// sequence) has QB = T/256 query blocks; block id -> (head, query block)
+// keeps the query blocks of a head on one XCD (equal id % 8) so they share
+// its keys in that XCD's L2.  The workgroup owns 8 query tiles of 32; wave w
+// takes tiles {w, 7-w}, which balances the causal work.  Operands are staged
+// by direct global -> LDS copies, three stages deep, so no registers hold
+// staged data and the copies of stage s+2 overlap the arithmetic of stage s.
+// LDS fragment reads use per-lane offsets computed once, so every read is a
+// base register plus an immediate.
+// pre[bh][s][E] bf16 (K4): weighted S_pre^T as [dv][NSLOT], then Z_pre
+// (operand order).  vtp[bh][s][dv][L] bf16: the span's V^T (permuted keys,
+// see K2).
 // ---------------------------------------------------------------------------
 constexpr int kKB = 128;        // keys per intra stage (four 32-key blocks)
 constexpr int kKC = 16;         // readout K-steps per stage
@@ -897,64 +828,34 @@ __device__ __forceinline__ uint16_t* stage_buf(int j) {
 
 
 // Scores of two query tiles against one 32-key block: sc_i = K_blk Q_i^T
-// over the d-contraction, the two accumulation chains interleaved, results in
-// VGPRs for the VALU that squares them.  The first MFMA of a chain takes a
-// zero accumulator.  s_nop 4 at the end: with the chains interleaved the last
-// write of sc0 is an MFMA and a full MFMA old when the block ends, sc1's last
-// write is covered by the first VALU instructions, which read sc0.
+// over the d-contraction, the two accumulation chains interleaved (compiler
+// builtins; the compiler inserts the wait states before the VALU reads them).
 template <int KZ>
 __device__ __forceinline__ void score2(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[KZ],
-                                       const bf16x8 (&q0)[KZ], const bf16x8 (&q1)[KZ]);
-template <>
-__device__ __forceinline__ void score2<4>(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[4],
-                                          const bf16x8 (&q0)[4], const bf16x8 (&q1)[4]) {
-  asm volatile(
-      "v_mfma_f32_32x32x16_bf16 %0, %2, %6, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %2, %10, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %3, %7, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %3, %11, %1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %4, %8, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %4, %12, %1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %5, %9, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %5, %13, %1\n\t"
-      "s_nop 4"
-      : "=&v"(sc0), "=&v"(sc1)
-      : "v"(A[0]), "v"(A[1]), "v"(A[2]), "v"(A[3]), "v"(q0[0]), "v"(q0[1]), "v"(q0[2]),
-        "v"(q0[3]), "v"(q1[0]), "v"(q1[1]), "v"(q1[2]), "v"(q1[3]));
-}
-template <>
-__device__ __forceinline__ void score2<2>(f32x16& sc0, f32x16& sc1, const bf16x8 (&A)[2],
-                                          const bf16x8 (&q0)[2], const bf16x8 (&q1)[2]) {
-  asm volatile(
-      "v_mfma_f32_32x32x16_bf16 %0, %2, %4, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %2, %6, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %3, %5, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %3, %7, %1\n\t"
-      "s_nop 4"
-      : "=&v"(sc0), "=&v"(sc1)
-      : "v"(A[0]), "v"(A[1]), "v"(q0[0]), "v"(q0[1]), "v"(q1[0]), "v"(q1[1]));
+                                       const bf16x8 (&q0)[KZ], const bf16x8 (&q1)[KZ]) {
+  mfma_vz(sc0, A[0], q0[0]);
+  mfma_vz(sc1, A[0], q1[0]);
+#pragma unroll
+  for (int kz = 1; kz < KZ; ++kz) {
+    mfma_v(sc0, A[kz], q0[kz]);
+    mfma_v(sc1, A[kz], q1[kz]);
+  }
 }
 
 // Scores of two query tiles against one 32-key block with two feature blocks
 // of 32 coordinates (K-steps 0, 1 of block 0 and 2, 3 of block 1): four
-// chains, tile 0's chains written by the 5th and 7th MFMA, so as for score2
-// tile 0's scores are a full MFMA old when the block ends.
+// chains, interleaved.
 __device__ __forceinline__ void score2b2(f32x16& s00, f32x16& s01, f32x16& s10, f32x16& s11,
                                          const bf16x8 (&A)[4], const bf16x8 (&q0)[4],
                                          const bf16x8 (&q1)[4]) {
-  asm volatile(
-      "v_mfma_f32_32x32x16_bf16 %0, %4, %8, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %2, %4, %12, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %6, %10, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %3, %6, %14, 0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %0, %5, %9, %0\n\t"
-      "v_mfma_f32_32x32x16_bf16 %2, %5, %13, %2\n\t"
-      "v_mfma_f32_32x32x16_bf16 %1, %7, %11, %1\n\t"
-      "v_mfma_f32_32x32x16_bf16 %3, %7, %15, %3\n\t"
-      "s_nop 4"
-      : "=&v"(s00), "=&v"(s01), "=&v"(s10), "=&v"(s11)
-      : "v"(A[0]), "v"(A[1]), "v"(A[2]), "v"(A[3]), "v"(q0[0]), "v"(q0[1]), "v"(q0[2]),
-        "v"(q0[3]), "v"(q1[0]), "v"(q1[1]), "v"(q1[2]), "v"(q1[3]));
+  mfma_vz(s00, A[0], q0[0]);
+  mfma_vz(s10, A[0], q1[0]);
+  mfma_vz(s01, A[2], q0[2]);
+  mfma_vz(s11, A[2], q1[2]);
+  mfma_v(s00, A[1], q0[1]);
+  mfma_v(s10, A[1], q1[1]);
+  mfma_v(s01, A[3], q0[3]);
+  mfma_v(s11, A[3], q1[3]);
 }
 
 template <int D, int DV>
@@ -962,11 +863,11 @@ struct OutGrid {
   static constexpr int QB_TOKENS = 256;  // queries per workgroup
 };
 
-template <int D, int DV, int NG, bool QUAD>
-__global__ __launch_bounds__(256) void span_output_kernel(
+template <int D, int DV, int NG>
+__global__ __launch_bounds__(256) void quadratic_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
-    int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
+    const uint16_t* __restrict__ vtp, float* __restrict__ out, int T, int L, int LV, int NS,
+    int QB, int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM;
   constexpr int NQ = 2, W = 4, NT = 8;
@@ -979,11 +880,6 @@ __global__ __launch_bounds__(256) void span_output_kernel(
                 "intra stage size");
   constexpr int IPW_K = KCHUNKS / 256;          // copy instructions per wave: K rows
   constexpr int IPW_I = ICH / 256;              // ... K rows then V^T rows
-  constexpr int SCH = 2 * kKC;                  // chunks per S_pre row of one stage (32)
-  constexpr int SCHUNKS = DV * SCH;
-  static_assert(SCHUNKS * 16 <= kStageBytes && SCHUNKS % 256 == 0, "readout stage size");
-  constexpr int IPW_R = SCHUNKS / 256;
-  constexpr int NSTAGE_R = (G::NKS + kKC - 1) / kKC;
   static_assert(G::MT == 2, "two dv tiles");
 
   const int tid = threadIdx.x;
@@ -992,9 +888,8 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   const int c = lane & 31, g = lane >> 5;
   const int id = blockIdx.x;
   const int jx = id >> 3;
-  // the quadratic form's query blocks differ in work by up to a factor QB:
-  // the longest go first
-  const int qb = QUAD ? QB - 1 - jx % QB : jx % QB;
+  // query blocks differ in work by up to a factor QB: the longest go first
+  const int qb = QB - 1 - jx % QB;
   const int sp = sp0 + 8 * (jx / QB) + (id & 7);
   if (sp >= nsp) return;  // whole workgroup: padding of the grid
   const int s = sp % NS, bh = sp / NS;
@@ -1004,7 +899,6 @@ __global__ __launch_bounds__(256) void span_output_kernel(
   if (wg_q0 >= span_end) return;  // whole workgroup beyond the sequence
   const uint16_t* qh = q + static_cast<long long>(bh) * T * D;
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
-  const uint16_t* rec = QUAD ? nullptr : pre + static_cast<long long>(sp) * G::E;
   const uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
 
   int tile[NQ];
@@ -1055,36 +949,11 @@ __global__ __launch_bounds__(256) void span_output_kernel(
       g2lds16(src, buf + (i * W + wave) * 512);
     }
   };
-  // readout copy i of this lane: S_pre row m, chunk cl of the stage's 32
-  int rsrc[IPW_R];
-#pragma unroll
-  for (int i = 0; i < IPW_R; ++i) {
-    const int P = (i * W + wave) * 64 + lane;
-    const int m = P / SCH, pos = P % SCH;
-    rsrc[i] = m * G::NSLOT + 8 * (pos ^ rswz(m));
-  }
-  auto issue_r = [&](auto stg_c) __attribute__((always_inline)) {
-    constexpr int stg = decltype(stg_c)::value;
-    constexpr int kc = (G::NKS - stg * kKC < kKC) ? (G::NKS - stg * kKC) : kKC;
-    uint16_t* buf = stage_buf((3 + stg) % 5);
-#pragma unroll
-    for (int i = 0; i < IPW_R; ++i) {
-      // chunks past the last K-step: re-read the row's first chunk (never used)
-      int off = rsrc[i];
-      if constexpr (kc < kKC) {
-        const int P = (i * W + wave) * 64 + lane;
-        const int cl = (P % SCH) ^ rswz(P / SCH);
-        if (cl >= 2 * kc) off -= 8 * cl;
-      }
-      g2lds16(rec + 16 * kKC * stg + off, buf + (i * W + wave) * 512);
-    }
-  };
-  // Stage 0 of the in-span phase is issued first and the query and Z
-  // fragments are loaded behind it; the workgroup waits for that one memory
-  // round trip (the compiler's wait before the empty asm below: loads
-  // complete in order, so it also covers the copies issued before them), and
-  // only then issues the in-span stage 1 and the readout's stages 0 and 1,
-  // which arrive under the first stage's work.  From here on the only vector
+  // Stage 0 is issued first and the query fragments are loaded behind it;
+  // the workgroup waits for that one memory round trip (the compiler's wait
+  // before the empty asm below: loads complete in order, so it also covers
+  // the copies issued before them), and only then issues stage 1, which
+  // arrives under the first stage's work.  From here on the only vector
   // memory operations in flight are copies (and the final stores), which the
   // pipeline's own waits count.
   issue_i(0, g_stage0);
@@ -1102,87 +971,23 @@ __global__ __launch_bounds__(256) void span_output_kernel(
                                                    8 * (kz % KZM) + RM * g);
   }
 
-  // Z_pre operand fragments of each feature block (see below)
-  bf16x8 zA[NG][G::ZMB][KZM];
-  if constexpr (!QUAD) {
 #pragma unroll
-    for (int bb = 0; bb < NG; ++bb) {
-      const uint16_t* zop = rec + G::ES + static_cast<long long>(bb) * DM * DM;
+  for (int i = 0; i < NQ; ++i)
 #pragma unroll
-      for (int m = 0; m < G::ZMB; ++m)
-#pragma unroll
-        for (int kz = 0; kz < KZM; ++kz)
-          zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(zop + ((m * KZM + kz) * 64 + lane) * 8);
-    }
-  }
-
-  asm volatile("" ::"v"(qf[0][0]), "v"(qf[NQ - 1][G::KZ - 1]));
-  if constexpr (!QUAD) asm volatile("" ::"v"(zA[0][0][0]), "v"(zA[NG - 1][G::ZMB - 1][KZM - 1]));
+    for (int kz = 0; kz < G::KZ; ++kz) asm volatile("" ::"v"(qf[i][kz]));
   if (nstage > 1) issue_i(1, g_stage1);
-  if constexpr (!QUAD) {
-    issue_r(std::integral_constant<int, 0>{});
-    if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
-  }
 
-  // The P V / readout accumulators live in AGPRs from here to the stores.
-  // The empty asm makes the zeros exist here: otherwise the compiler writes
-  // them just before the first MFMA that reads them, and as that MFMA is
-  // inline assembly it would not insert the wait states an MFMA needs after a
-  // VALU write of its accumulator.
+  // the P V accumulators
   f32x16 acc[G::MT][NQ];
 #pragma unroll
   for (int m = 0; m < G::MT; ++m)
 #pragma unroll
-    for (int i = 0; i < NQ; ++i) {
+    for (int i = 0; i < NQ; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][i][r] = 0.f;
-      asm volatile("" : "+a"(acc[m][i]));
-    }
-  float dpart[NQ];
-
-  // ---- denominator from the prefix: q^T Z_pre q ------------------------------
-  if constexpr (QUAD) {
+  float dpart[NQ];  // the denominators' row sums
 #pragma unroll
-    for (int i = 0; i < NQ; ++i) dpart[i] = 0.f;
-  } else {
-    // sum over the feature blocks of q_bb^T Z_bb q_bb
-    f32x16 az[NG][G::ZMB][NQ];
-#pragma unroll
-    for (int bb = 0; bb < NG; ++bb)
-#pragma unroll
-      for (int m = 0; m < G::ZMB; ++m)
-#pragma unroll
-        for (int i = 0; i < NQ; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) az[bb][m][i][r] = 0.f;
-#pragma unroll
-    for (int bb = 0; bb < NG; ++bb)
-#pragma unroll
-      for (int m = 0; m < G::ZMB; ++m)
-#pragma unroll
-        for (int kz = 0; kz < KZM; ++kz)
-#pragma unroll
-          for (int i = 0; i < NQ; ++i)
-            az[bb][m][i] = mfma32(zA[bb][m][kz], qf[i][KZM * bb + kz], az[bb][m][i]);
-#pragma unroll
-    for (int i = 0; i < NQ; ++i) {
-      float dsum = 0.f;
-#pragma unroll
-      for (int bb = 0; bb < NG; ++bb)
-#pragma unroll
-        for (int m = 0; m < G::ZMB; ++m)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            // row sigma = 16m + r + RM*g of block bb: element (16m + r) % 8 of
-            // the block's fragment (16m + r) / 8
-            const int x = 16 * m + r;
-            const uint32_t w = word_of(qf[i][KZM * bb + (x >> 3)], (x & 7) >> 1);
-            const float qa = (x & 1) ? bf16hi_f32(w) : bf16lo_f32(w);
-            dsum += qa * az[bb][m][i][r];
-          }
-      dpart[i] = dsum;
-    }
-  }
+  for (int i = 0; i < NQ; ++i) dpart[i] = 0.f;
 
   // ---- causal squared-score attention inside the span -----------------------
   // Per 32-key block kb and query tile i: S_i = K_kb Q_i^T (a chain of KZ
@@ -1442,133 +1247,7 @@ __global__ __launch_bounds__(256) void span_output_kernel(
             none);
       hold(bx[0]);
     }
-    mfma_drain();    // the P V accumulators are moved by compiler code next
-    wait_vmcnt<0>();  // the readout's first stages (a single in-span stage waits for nothing)
-    lds_barrier();   // every wave is done with the intra buffers
   }
-
-  // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
-  if constexpr (!QUAD) {
-    // rotated fp32 query rows, per feature block:
-    // qr[i][DM*bb + x] = q[t][DM*bb + (x + RM*g) % DM]; the lane's own bf16
-    // fragments of block bb hold x < RM, the lane 32 away holds the rest
-    float qr[NQ][D];
-#pragma unroll
-    for (int i = 0; i < NQ; ++i)
-#pragma unroll
-      for (int kz = 0; kz < G::KZ; ++kz) {
-        const int base = DM * (kz / KZM) + 8 * (kz % KZM);
-        const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
-        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
-          qr[i][base + 2 * e] = bf16lo_f32(w[e]);
-          qr[i][base + 2 * e + 1] = bf16hi_f32(w[e]);
-          qr[i][base + RM + 2 * e] = bf16lo_f32(pw);
-          qr[i][base + RM + 2 * e + 1] = bf16hi_f32(pw);
-        }
-      }
-    // A fragment offsets: rows 32*m + c, chunk (2*kk + g) ^ (c & 15); the kk & 8
-    // and m parts are immediates
-    unsigned afo[8];
-#pragma unroll
-    for (int k7 = 0; k7 < 8; ++k7)
-      afo[k7] = static_cast<unsigned>((c * SCH + ((2 * k7 + g) ^ rswz(c))) * 16);
-    auto pack8 = [](const float pr[8]) __attribute__((always_inline)) {
-      return __builtin_bit_cast(
-          bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                             pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
-    };
-    // query feature products of tile i at global K-step kap (K-step kl of
-    // feature block bb): slots 16*kl + 8*g + j of the block pair registers
-    // (r1 + j, r1 + j + delta) of the block's rotated row
-    auto fx = [&](int i, int kap, float x[8], float y[8]) __attribute__((always_inline)) {
-      const int bb = kap / G::NKSM, kl = kap % G::NKSM;
-      const int r1 = (8 * kl) % RM, dl = (8 * kl) / RM;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        x[j] = qr[i][DM * bb + r1 + j];
-        y[j] = qr[i][DM * bb + (r1 + j + dl) % DM];
-      }
-    };
-    // B fragments: bq[0] the next item's, bq[1], bq[2] the two before (kept
-    // live, see hold); the first item's features
-    bf16x8 bq[3];
-    {
-      float x[8], y[8];
-      fx(0, 0, x, y);
-      float pr[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) pr[j] = x[j] * y[j];
-      bq[0] = pack8(pr);
-      bq[1] = bq[0];
-      bq[2] = bq[0];
-    }
-    static_for<0, NSTAGE_R>([&](auto stg_c) {
-      constexpr int stg = decltype(stg_c)::value;
-      constexpr int k0 = stg * kKC;
-      constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
-      // stages 0 and 1 arrived during the earlier phases (the intra part
-      // ends with vmcnt 0 and a barrier)
-      if constexpr (stg >= 2) {
-        if constexpr (stg + 1 < NSTAGE_R) wait_vmcnt<IPW_R>(); else wait_vmcnt<0>();
-        lds_barrier();
-      }
-      if constexpr (stg + 2 < NSTAGE_R) issue_r(std::integral_constant<int, stg + 2>{});
-      const char* Sb = reinterpret_cast<const char*>(stage_buf((3 + stg) % 5));
-      // per-lane fragment bases of this stage buffer, formed once per stage
-      // (opaque to the compiler, which would otherwise fold the buffer's
-      // address back into every read; LDS immediates are only 16 bits)
-      const char* ap[8];
-#pragma unroll
-      for (int k7 = 0; k7 < 8; ++k7) {
-        uint32_t a32 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
-                           (const lds_void_t*)Sb)) + afo[k7];
-        asm volatile("" : "+v"(a32));
-        ap[k7] = (const char*)(const lds_void_t*)static_cast<uintptr_t>(a32);
-      }
-      auto lda = [&](int kk, bf16x8 A[2]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-          A[m] = *reinterpret_cast<const bf16x8*>(ap[kk & 7] + (kk >> 3) * 256 +
-                                                  m * (32 * SCH * 16));
-      };
-      // A fragments in a ring of three K-steps; the load for K-step kk+2 is
-      // issued after the first tile of K-step kk, when the registers it
-      // reuses (K-step kk-1) have not been read for two tiles
-      bf16x8 Ar[3][2];
-      lda(0, Ar[0]);
-      if constexpr (kc > 1) lda(1, Ar[1]);
-      static_for<0, kc>([&](auto kk_c) {
-        constexpr int kk = decltype(kk_c)::value;
-        constexpr int kap = k0 + kk;
-        constexpr int cur = kk % 3;
-        // item (kap, 0): MFMAs of tile 0, features of tile 1 at kap
-        {
-          float x[8], y[8], pr[8];
-          fx(1, kap, x, y);
-          mfma2_prod8(acc[0][0], acc[1][0], Ar[cur][0], Ar[cur][1], bq[0], x, y, pr);
-          bq[2] = bq[1];
-          bq[1] = bq[0];
-          bq[0] = pack8(pr);
-          hold(bq[1], bq[2]);
-        }
-        if constexpr (kk + 2 < kc) lda(kk + 2, Ar[(kk + 2) % 3]);
-        // item (kap, 1): MFMAs of tile 1, features of tile 0 at kap + 1
-        {
-          float x[8], y[8], pr[8];
-          fx(0, (kap + 1 < G::NKS) ? kap + 1 : kap, x, y);
-          mfma2_prod8(acc[0][1], acc[1][1], Ar[cur][0], Ar[cur][1], bq[0], x, y, pr);
-          bq[2] = bq[1];
-          bq[1] = bq[0];
-          bq[0] = pack8(pr);
-          hold(bq[1], bq[2]);
-        }
-      });
-    });
-  }
-  mfma_drain();
 
   // ---- normalise and store ---------------------------------------------------
 #pragma unroll
@@ -1593,9 +1272,9 @@ __global__ __launch_bounds__(256) void span_output_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// K4, eight-wave form (dv = 64; d = 64 with one or two feature blocks, d =
-// 32).  Same records, V^T layout and stage buffers as span_output_kernel
-// (which keeps the quadratic form), but 512 threads owning 512
+// K4: span output, eight-wave form (dv = 64; d = 64 with one or two feature
+// blocks, d = 32).  The in-span loop and stage buffers of quadratic_kernel
+// with the prefix readout added, and 512 threads owning 512
 // queries (16 tiles of 32): wave w holds tiles w and 15 - w, so two waves
 // share each SIMD with balanced causal work (waves w and w + 4 hold tiles
 // adding up to 30), and one wave's VALU work (squared scores, query feature
@@ -2127,9 +1806,9 @@ static hipError_t run_quadratic(const void* q, const void* k, const void* v, flo
   for (int sp0 = 0; sp0 < BH; sp0 += per) {
     const int cnt = BH - sp0 < per ? BH - sp0 : per;
     const unsigned nb4 = 8u * static_cast<unsigned>(qblocks) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output_kernel<D, DV, NG, true><<<nb4, 256, 0, st>>>(
-        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), nullptr, vtp, out, T, T,
-        LA, 1, qblocks, sp0, sp0 + cnt);
+    quadratic_kernel<D, DV, NG><<<nb4, 256, 0, st>>>(static_cast<const uint16_t*>(q),
+                                                     static_cast<const uint16_t*>(k), vtp, out, T,
+                                                     T, LA, 1, qblocks, sp0, sp0 + cnt);
   }
   return hipGetLastError();
 }
