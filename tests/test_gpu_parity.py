@@ -92,9 +92,11 @@ def test_mid_bf16_two_heads_full(kata, orc):
     assert_bf16_close(got, ref, "mid_bf16 B1 H2")
 
 
-@pytest.mark.parametrize("span", [1, 2, 3, 4, 16, 64])
+@pytest.mark.parametrize("span", [1, 2, 3, 4, 8, 16, 32, 64])
 def test_span_modes_agree(kata, orc, span):
     # span_chunks = 1 is the per-chunk form; larger spans fold chunks on chip
+    # (8: one 512-query output workgroup per span; 32 and 64: several per
+    # span, some of them wholly past T)
     T = 2 * 1024 + 37
     log(f"case span={span} B1 H2 T{T} d64 C64")
     inp = _inputs("mid_bf16", B=1, H=2, T=T)
