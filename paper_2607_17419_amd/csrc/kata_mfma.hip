@@ -1654,13 +1654,19 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   });
 
   // ---- normalise and store ---------------------------------------------------
+  // A tile's accumulators hold 4 consecutive dv columns of one query per
+  // lane; they go through this wave's own 16 KB of the (now idle) stage
+  // buffers, [32 queries][68 floats] per tile, so that each store
+  // instruction writes four whole 256-byte output rows.
+  lds_barrier();  // every wave is done with the readout buffers
+  float* ost = reinterpret_cast<float*>(stage_buf(wave >> 1)) + (wave & 1) * 4096;
+  constexpr int OS = DV + 4;  // floats per LDS row (16-byte aligned rows)
+  static_assert(32 * OS <= 4096, "one tile per round fits the wave's 16 KB");
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     const float Dt = dpart[i] + __shfl_xor(dpart[i], 32);
-    const long long t = tq0[i] + c;
-    if (!tlive[i] || t >= span_end) continue;
+    if (!tlive[i]) continue;  // wave-uniform
     const float inv = (Dt > 0.f) ? 1.f / Dt : 0.f;
-    float* orow = out + (static_cast<long long>(bh) * T + t) * DV;
 #pragma unroll
     for (int m = 0; m < 2; ++m)
 #pragma unroll
@@ -1670,8 +1676,21 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
         o.y = acc[m][i][4 * r4 + 1] * inv;
         o.z = acc[m][i][4 * r4 + 2] * inv;
         o.w = acc[m][i][4 * r4 + 3] * inv;
-        *reinterpret_cast<float4*>(orow + 32 * m + 8 * r4 + 4 * g) = o;
+        *reinterpret_cast<float4*>(ost + c * OS + 32 * m + 8 * r4 + 4 * g) = o;
       }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    // lane l: rows 4 j + l / 16 of the tile, 16-byte piece l % 16 of the row
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = 4 * j + (lane >> 4), pc = lane & 15;
+      const float4 o = *reinterpret_cast<const float4*>(ost + row * OS + 4 * pc);
+      const long long t = tq0[i] + row;
+      if (t < span_end)
+        *reinterpret_cast<float4*>(out + (static_cast<long long>(bh) * T + t) * DV + 4 * pc) = o;
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // reads done before the next tile's writes
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
