@@ -151,6 +151,23 @@ __global__ __launch_bounds__(256) void bwd_chunk_state(const Tx* __restrict__ x,
 // ---------------------------------------------------------------------------
 constexpr int kCS = 65;  // fp32 row stride of the coefficient kernel's tiles
 
+// Eight consecutive elements as fp32 (p 16-byte aligned).
+__device__ __forceinline__ void load8_f32(const bf16_t* p, float* v) {
+  const uint4 w = *reinterpret_cast<const uint4*>(p);
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[2 * e] = bf16lo_f32(u[e]);
+    v[2 * e + 1] = bf16hi_f32(u[e]);
+  }
+}
+__device__ __forceinline__ void load8_f32(const float* p, float* v) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
 template <typename Tin>
 __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
                                                 const Tin* __restrict__ k,
@@ -172,18 +189,78 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   const Tin* qh = q + (static_cast<long long>(bh) * T + t0) * d;
   const Tin* kh = k + (static_cast<long long>(bh) * T + t0) * d;
   const float* zp = zsrc + bh * z_bh + c * z_c;
+  // z_pre (g nm <= 2080 floats) is read once, coalesced, into the k tile's
+  // LDS and unpacked from there; q and k rows are read in 8-element pieces
+  // (16 bytes of bf16) where d allows it, k held in registers until every
+  // read of the staged z_pre is done
+  float* zl = ks;
+  static_assert(64 * kCS >= 2080, "the packed z_pre fits the k tile");
+  for (int i = tid; i < g * nm; i += 256) zl[i] = zp[i];
+  __syncthreads();
   for (int i = tid; i < 64 * 64; i += 256) {
     const int x = i >> 6, y = i & 63;
     float zv = 0.f;
     if (g == 1) {  // one block: no block index to divide out
-      if (x < d && y < d) zv = zp[packed_index(min(x, y), max(x, y), d)];
+      if (x < d && y < d) zv = zl[packed_index(min(x, y), max(x, y), d)];
     } else if (x < d && y < d && x / m == y / m) {
-      zv = zp[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
+      zv = zl[(x / m) * nm + packed_index(min(x, y) % m, max(x, y) % m, m)];
     }
     Z[x * kCS + y] = (x == y ? zdiag : 1.f) * zv;
-    const bool in = x < nt && y < d;
-    qs[x * kCS + y] = in ? load_f32(qh, static_cast<long long>(x) * d + y) : 0.f;
-    ks[x * kCS + y] = in ? load_f32(kh, static_cast<long long>(x) * d + y) : 0.f;
+  }
+  // 8-element pieces need d % 8 == 0 and 16-byte aligned q, k (row starts are
+  // then aligned too: t0 and every row offset are multiples of d)
+  const bool vec = d % 8 == 0 && ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k)) & 15) == 0;
+  const int pieces = d / 8;  // 8-element pieces per row (vec)
+  float kv[2][8];            // this thread's k pieces (vec: at most 64 x 8 / 256 = 2)
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int i = tid + 256 * j;
+      if (i >= 64 * pieces) break;
+      const int x = i / pieces, y0 = 8 * (i % pieces);
+      float qv[8];
+      if (x < nt) {
+        load8_f32(qh + static_cast<long long>(x) * d + y0, qv);
+        load8_f32(kh + static_cast<long long>(x) * d + y0, kv[j]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qv[e] = kv[j][e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[x * kCS + y0 + e] = qv[e];
+    }
+  } else {
+    for (int i = tid; i < 64 * 64; i += 256) {
+      const int x = i >> 6, y = i & 63;
+      const bool in = x < nt && y < d;
+      qs[x * kCS + y] = in ? load_f32(qh, static_cast<long long>(x) * d + y) : 0.f;
+    }
+  }
+  __syncthreads();  // every read of the staged z_pre is done: the k tile may be written
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int i = tid + 256 * j;
+      if (i >= 64 * pieces) break;
+      const int x = i / pieces, y0 = 8 * (i % pieces);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ks[x * kCS + y0 + e] = kv[j][e];
+    }
+  } else {
+    for (int i = tid; i < 64 * 64; i += 256) {
+      const int x = i >> 6, y = i & 63;
+      const bool in = x < nt && y < d;
+      ks[x * kCS + y] = in ? load_f32(kh, static_cast<long long>(x) * d + y) : 0.f;
+    }
+  }
+  // columns d .. 63 of the q and k tiles are read by the contractions below
+  // (K = 64): zero them when d < 64
+  if (d < 64) {
+    for (int i = tid; i < 64 * (64 - d); i += 256) {
+      const int x = i / (64 - d), y = d + i % (64 - d);
+      qs[x * kCS + y] = 0.f;
+      ks[x * kCS + y] = 0.f;
+    }
   }
   __syncthreads();
   {
