@@ -829,9 +829,15 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   // (the C ABI has checked that every tensor is 16-byte aligned)
   bool bf = false;
   if constexpr (std::is_same<Tin, bf16_t>::value) bf = bwd_bf_ok(d, dv, C, g);
+  // bf16 path: with enough heads to fill the chip, each state launch also
+  // scans (one pass, sequential over a head's chunks); with few heads the
+  // chunk-parallel state launch and the record scan are faster
+  const bool fused = bf && BH >= bwd_bf_fused_min_heads();
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  if (bf) {
+  if (fused) {
+    if ((e = launch_bwd_prefix_bf(false, k, v, frec, BH, T, st)) != hipSuccess) return e;
+  } else if (bf) {
     if ((e = launch_bwd_state_bf(false, k, v, frec, BH, T, st)) != hipSuccess) return e;
   } else if (mf)
     bwd_state_mf<Tin, Tin, false><<<gsm, 256, 0, st>>>(ki, vi, dv, frec, T, d, dv, C, g,
@@ -842,7 +848,9 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   const bool v4 = E % 4 == 0;
   const dim3 gscan4(static_cast<unsigned>((E + kEB4 - 1) / kEB4), BH);
-  if (bf) {
+  if (fused) {
+    // scanned by the state launch
+  } else if (bf) {
     if ((e = launch_bwd_scan_bf(false, frec, BH, T, st)) != hipSuccess) return e;
   } else if (v4)
     scan_exclusive_f32x4<BwdUnitWeight, false><<<gscan4, 256, 0, st>>>(frec, NC, E, bh_stride,
@@ -862,7 +870,9 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
                                                  bf ? NC * rq : bh_stride, bf ? rq : E,
                                                  bf ? 2.f : 1.f);
   if ((e = record(ev, 3, st)) != hipSuccess) return e;
-  if (bf) {
+  if (fused) {
+    if ((e = launch_bwd_prefix_bf(true, q, ab, brec, BH, T, st)) != hipSuccess) return e;
+  } else if (bf) {
     if ((e = launch_bwd_state_bf(true, q, ab, brec, BH, T, st)) != hipSuccess) return e;
   } else if (mf)
     bwd_state_mf<Tin, float, true><<<gsm, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
@@ -871,7 +881,9 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
     bwd_chunk_state<Tin, float, true><<<gs, 256, 0, st>>>(qi, ab, dv + 1, brec, T, d, dv, C, g,
                                                          bh_stride, E);
   if ((e = record(ev, 4, st)) != hipSuccess) return e;
-  if (bf) {
+  if (fused) {
+    // scanned by the state launch
+  } else if (bf) {
     if ((e = launch_bwd_scan_bf(true, brec, BH, T, st)) != hipSuccess) return e;
   } else if (v4)
     scan_exclusive_f32x4<BwdUnitWeight, true><<<gscan4, 256, 0, st>>>(brec, NC, E, bh_stride,

@@ -729,6 +729,209 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
   }
 }
 
+// ---------------------------------------------------------------------------
+// Chunk-state prefixes in one pass (state and exclusive scan fused), on the
+// bf16 matrix cores, d = dv = C = 64: record c receives w(f) x the sum of the
+// chunk states S_c'[f][j] = sum_t x_ta x_tb y_tj, z_c'[f] = sum_t wt_t x_ta x_tb
+// over the chunks c' < c (or, kBwd, c' > c), w = 1/2 on the diagonal features
+// (a, a); S rounded to bf16 once from the fp32 running sum, z in fp32.  Forward
+// (kBwd = false): x = k, y = v, wt = 1.  Backward (kBwd): x = q, y = a_t as a
+// bf16 pair hi + lo, wt = b_t from the coefficient rows.
+// Wave w of workgroup tg owns the 32-feature tile kPW tg + w of one head and
+// walks the head's chunks in scan order with the running sum of its tile in
+// registers: per chunk it writes the running sum as the record (the exclusive
+// prefix), then adds the chunk's state.  Each chunk's x and y are staged in LDS
+// once per workgroup, transposed ([dim][token]), and the next chunk's rows are
+// loaded into registers while the current one is contracted.  The kPG
+// workgroups of a head read the same rows: they are given workgroup ids of one
+// residue mod 8, which the dispatcher sends to one XCD, so the rows come from
+// that XCD's L2.  grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
+// ---------------------------------------------------------------------------
+constexpr int kPW = 5;                  // waves per workgroup (one feature tile each)
+constexpr int kPG = kBfN / 32 / kPW;    // workgroups per head
+static_assert(kPW * kPG * 32 == kBfN, "the feature tiles split evenly");
+
+// Raw rows of one chunk held in registers between their loads and their
+// staging (masked and converted only when staged, so that the loads stay in
+// flight over the contractions in between).
+template <bool kBwd>
+struct PrefixRaw {
+  uint32_t x[8];
+  uint32_t y[kBwd ? 1 : 8];
+  float a[kBwd ? 16 : 1];
+  float b;
+  int nt;  // valid rows of the chunk
+};
+
+template <bool kBwd>
+__global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __restrict__ x,
+                                                          const void* __restrict__ yv,
+                                                          unsigned char* __restrict__ rec,
+                                                          int T, int BH, long long rec_bh) {
+  constexpr int kTile = 64 * kBP;                   // one staged 64 x 64 tile
+  constexpr int kBuf = (kBwd ? 3 : 2) * kTile;      // x, y (and the y residue) of a chunk
+  __shared__ __align__(16) uint16_t ot[kPW * 32 * kBP];  // per-wave output rows
+  __shared__ __align__(16) uint16_t tiles[2 * kBuf];     // two chunks in flight
+  __shared__ __align__(16) float wts[2][64];
+  const int id = blockIdx.x, jx = id >> 3;
+  const int bh = 8 * (jx / kPG) + (id & 7), tg = jx % kPG;
+  if (bh >= BH) return;  // the whole workgroup
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  const int NC = (T + 63) / 64;
+  const long long hb = static_cast<long long>(bh) * T;
+  const int ft = kPW * tg + w, f = 32 * ft + l32;
+  // the pair (pa, pb) of feature f: the row pa of the upper triangle with
+  // D(pa) <= f < D(pa + 1), D(a) = 64 a - a (a - 1) / 2
+  int pa = 0;
+  while (pa < 63 && 64 * (pa + 1) - (pa + 1) * pa / 2 <= f) ++pa;
+  const int pb = pa + f - (64 * pa - pa * (pa - 1) / 2);
+  // diagonal rows of this wave's tile, one bit per row
+  const uint32_t dmask = static_cast<uint32_t>(__ballot(pa == pb));
+  const float wz = pa == pb ? 0.5f : 1.f;
+  // staging: threads below 256 take rows 8 rg .. 8 rg + 7, columns 2 cp, 2 cp + 1
+  const int rg = (tid >> 5) & 7, cp = tid & 31;
+  const bool stager = tid < 256;
+  auto chunk = [&](int it) { return kBwd ? NC - 1 - it : it; };
+  auto fetch = [&](PrefixRaw<kBwd>& R, int c) {
+    const long long t0 = static_cast<long long>(c) * 64;
+    R.nt = static_cast<int>(min(64LL, static_cast<long long>(T) - t0));
+    const uint16_t* xh = x + (hb + t0) * 64;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int tc = min(8 * rg + r, R.nt - 1);
+      R.x[r] = *reinterpret_cast<const uint32_t*>(xh + tc * 64 + 2 * cp);
+      if constexpr (kBwd) {
+        const float* arow = static_cast<const float*>(yv) + (hb + t0 + tc) * 65;
+        R.a[2 * r] = arow[2 * cp];  // rows of 65 floats: 4-byte aligned
+        R.a[2 * r + 1] = arow[2 * cp + 1];
+      } else {
+        const uint16_t* vh = static_cast<const uint16_t*>(yv) + (hb + t0) * 64;
+        R.y[r] = *reinterpret_cast<const uint32_t*>(vh + tc * 64 + 2 * cp);
+      }
+    }
+    if constexpr (kBwd)
+      if (tid < 64) R.b = static_cast<const float*>(yv)[(hb + t0 + min(tid, R.nt - 1)) * 65 + 64];
+  };
+  auto put_t = [&](uint16_t* dst, const uint32_t* s2) {
+    *reinterpret_cast<uint4*>(dst + (2 * cp) * kBP + 8 * rg) =
+        make_uint4(lo_pair(s2[0], s2[1]), lo_pair(s2[2], s2[3]), lo_pair(s2[4], s2[5]),
+                   lo_pair(s2[6], s2[7]));
+    *reinterpret_cast<uint4*>(dst + (2 * cp + 1) * kBP + 8 * rg) =
+        make_uint4(hi_pair(s2[0], s2[1]), hi_pair(s2[2], s2[3]), hi_pair(s2[4], s2[5]),
+                   hi_pair(s2[6], s2[7]));
+  };
+  auto stage = [&](const PrefixRaw<kBwd>& R, int buf) {
+    uint32_t xv[8], yh[8], yl[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const bool in = 8 * rg + r < R.nt;
+      xv[r] = in ? R.x[r] : 0u;
+      if constexpr (kBwd) {
+        const uint32_t hi = pack_bf16x2(R.a[2 * r], R.a[2 * r + 1]);
+        yh[r] = in ? hi : 0u;
+        yl[r] = in ? pack_bf16x2(R.a[2 * r] - bf16lo_f32(hi), R.a[2 * r + 1] - bf16hi_f32(hi))
+                   : 0u;
+      } else {
+        yh[r] = in ? R.y[r] : 0u;
+      }
+    }
+    uint16_t* tb = tiles + buf * kBuf;
+    put_t(tb, xv);
+    put_t(tb + kTile, yh);
+    if constexpr (kBwd) put_t(tb + 2 * kTile, yl);
+    if (tid < 64) wts[buf][tid] = tid < R.nt ? (kBwd ? R.b : 1.f) : 0.f;
+  };
+  f32x16 run0 = {}, run1 = {};
+  float zrun = 0.f;
+  uint16_t* ow = ot + w * 32 * kBP;
+  unsigned char* rh = rec + bh * rec_bh;
+  // chunk it: write its record (the running sum), then add its state
+  auto step = [&](int it) {
+    const int c = chunk(it), buf = it & 1;
+    // record c = the running sum (w = 1/2 on diagonal rows), as whole bf16 rows
+    // through this wave's LDS rows (a wave's LDS accesses complete in order)
+    unsigned char* r0 = rh + static_cast<long long>(c) * kRecB;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 8 * (i >> 2) + 4 * h + (i & 3);
+      const float wr = (dmask >> r) & 1u ? 0.5f : 1.f;
+      ow[r * kBP + l32] = bf_bits(wr * run0[i]);
+      ow[r * kBP + 32 + l32] = bf_bits(wr * run1[i]);
+    }
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int ch = lane + 64 * q4, r = ch >> 3, part = ch & 7;
+      *reinterpret_cast<uint4*>(r0 + static_cast<long long>(32 * ft + r) * 128 + 16 * part) =
+          *reinterpret_cast<const uint4*>(ow + r * kBP + 8 * part);
+    }
+    if (h == 0) reinterpret_cast<float*>(r0 + kRecSB)[f] = wz * zrun;
+    const uint16_t* xT = tiles + buf * kBuf;
+    const uint16_t* yT = xT + kTile;
+    const uint16_t* yL = xT + 2 * kTile;
+    const float* wt = wts[buf];
+    float zp = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int tk = 16 * ks + 8 * h;
+      const uint4 xa = *reinterpret_cast<const uint4*>(xT + pa * kBP + tk);
+      const uint4 xb = *reinterpret_cast<const uint4*>(xT + pb * kBP + tk);
+      const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w}, wb[4] = {xb.x, xb.y, xb.z, xb.w};
+      uint32_t pk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = bf16lo_f32(wa[e]) * bf16lo_f32(wb[e]);
+        const float p1 = bf16hi_f32(wa[e]) * bf16hi_f32(wb[e]);
+        pk[e] = pack_bf16x2(p0, p1);
+        zp += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;  // padded tokens: wt = 0
+      }
+      const bf16x8 A = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      run0 = mfma_bf(A, ld8(yT + l32 * kBP + tk), run0);
+      run1 = mfma_bf(A, ld8(yT + (32 + l32) * kBP + tk), run1);
+      if constexpr (kBwd) {
+        run0 = mfma_bf(A, ld8(yL + l32 * kBP + tk), run0);
+        run1 = mfma_bf(A, ld8(yL + (32 + l32) * kBP + tk), run1);
+      }
+    }
+    zrun += zp + __shfl_xor(zp, 32);
+  };
+  // Chunk it + 1 is staged (LDS buffer (it + 1) & 1) while chunk it is
+  // contracted from the other buffer, and the loads of chunk it + 1 + kAhead
+  // are issued into the register set just staged: kAhead chunks' loads are in
+  // flight (two for the forward states; one for the backward states, whose
+  // fp32 a_t rows take twice the registers).  One LDS-only barrier per chunk;
+  // the record stores and the loads stay in flight across it.
+  constexpr int kAhead = kBwd ? 1 : 2;
+  PrefixRaw<kBwd> Ra, Rb_;
+  PrefixRaw<kBwd>& R0 = Ra;
+  PrefixRaw<kBwd>& R1 = kAhead == 2 ? Rb_ : Ra;
+  // Every fetch is issued, past the last chunk as a repeat of it (its values
+  // are never staged): with the same loads on every path the compiler's wait
+  // before each staging counts exactly the loads and stores issued after it.
+  auto ahead = [&](int it) { return chunk(min(it, NC - 1)); };
+  if (stager) {
+    fetch(R0, chunk(0));
+    stage(R0, 0);
+    fetch(R1, ahead(1));
+    if (kAhead == 2) fetch(R0, ahead(2));
+  }
+  lds_barrier();
+  for (int it = 0; it < NC; it += 2) {
+    if (stager) {
+      if (it + 1 < NC) stage(R1, 1);
+      fetch(R1, ahead(it + 1 + kAhead));
+    }
+    step(it);
+    lds_barrier();  // buffer 0 is read by every wave; buffer 1 is staged
+    if (it + 1 >= NC) break;
+    if (stager) {
+      if (it + 2 < NC) stage(R0, 0);
+      fetch(R0, ahead(it + 2 + kAhead));
+    }
+    step(it + 1);
+    lds_barrier();
+  }
+}
+
 }  // namespace
 
 bool bwd_bf_ok(int d, int dv, int C, int g) { return d == 64 && dv == 64 && C == 64 && g == 1; }
@@ -769,6 +972,26 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
     go(std::integral_constant<int, 2>{});
   else
     go(std::integral_constant<int, 1>{});
+  return hipGetLastError();
+}
+
+// The fused launch runs 13 workgroups per head, each sequential over the
+// head's chunks: below 32 heads (416 workgroups, under two per CU) the
+// chunk-parallel state launch plus the scan is faster (measured at T = 4096:
+// 8 heads 0.11 ms fused against 0.09 ms; 40 heads 0.35 against 0.41 ms).
+int bwd_bf_fused_min_heads() { return 32; }
+
+hipError_t launch_bwd_prefix_bf(bool backward, const void* x, const void* y, void* rec, int BH,
+                                int T, hipStream_t st) {
+  const int NC = (T + 63) / 64;
+  const long long rec_bh = static_cast<long long>(NC) * kRecB;
+  const unsigned grid = static_cast<unsigned>(kPG * 8 * ((BH + 7) / 8));
+  unsigned char* r = static_cast<unsigned char*>(rec);
+  const uint16_t* xs = static_cast<const uint16_t*>(x);
+  if (backward)
+    bwd_prefix_bf<true><<<grid, 64 * kPW, 0, st>>>(xs, y, r, T, BH, rec_bh);
+  else
+    bwd_prefix_bf<false><<<grid, 64 * kPW, 0, st>>>(xs, y, r, T, BH, rec_bh);
   return hipGetLastError();
 }
 

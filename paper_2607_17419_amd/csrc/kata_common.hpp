@@ -43,4 +43,25 @@ __host__ __device__ __forceinline__ int packed_index(int a, int b, int d) {
   return a * d - a * (a - 1) / 2 + (b - a);
 }
 
+// Wait until at most N vector-memory operations of this wave are in flight
+// (lgkm and exp counters left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier that orders LDS only: this wave's LDS operations are
+// complete (lgkmcnt 0), then s_barrier.  Unlike __syncthreads() it does not
+// wait for outstanding vector-memory operations, so loads of later stages
+// (global -> LDS copies among them) and global stores stay in flight; callers
+// wait for a copied stage they consume with wait_vmcnt first.  The signal
+// fences keep the compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt and expcnt unchanged
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 }  // namespace kata

@@ -80,6 +80,12 @@ hipError_t launch_bwd_state_bf(bool backward, const void* x, const void* y, void
 // Exclusive prefix (reverse: suffix) of those records in place, diagonal
 // features weighted 1/2.
 hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_t st);
+// The exclusive prefix (backward: suffix) records of the same chunk states in
+// one pass, state and scan fused, diagonal features weighted 1/2; used from
+// bwd_bf_fused_min_heads() heads (batch x heads) on.
+int bwd_bf_fused_min_heads();
+hipError_t launch_bwd_prefix_bf(bool backward, const void* x, const void* y, void* rec, int BH,
+                                int T, hipStream_t st);
 // Gradients of every chunk from the scanned records, a_t | b_t rows (ab, row
 // stride 65) and bf16 q, k, v; every tensor 16-byte aligned (as the C ABI
 // requires).

@@ -172,26 +172,6 @@ __device__ __forceinline__ void g2lds16(const void* gsrc, void* lds_wave_base) {
                : "memory", "m0");
 }
 
-// Wait until at most N vector-memory operations of this wave are in flight
-// (lgkm and exp counters left alone).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (((N >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Workgroup barrier that orders LDS only: this wave's LDS operations are
-// complete (lgkmcnt 0), then s_barrier.  Unlike __syncthreads() it does not
-// wait for outstanding vector-memory operations, so global -> LDS copies of
-// later stages stay in flight; callers wait for the stage they consume with
-// wait_vmcnt first.  The signal fences keep the compiler from moving memory
-// accesses across the barrier.
-__device__ __forceinline__ void lds_barrier() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt and expcnt unchanged
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
 // 32-bit word j (0..3) of a 16-byte fragment, j known at compile time after
 // unrolling.

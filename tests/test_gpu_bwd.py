@@ -147,6 +147,37 @@ def test_bwd_ragged_m1(kata, orc, T):
     _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1), ref, f"T{T} fwd+bwd", per_row=False)
 
 
+@pytest.mark.parametrize("B,H,T", [(2, 16, 333), (4, 9, 130), (1, 40, 64)])
+def test_bwd_fused_state_scan(kata, orc, B, H, T):
+    # From 32 heads on, the bf16 path computes each record stream (prefix of the
+    # forward states, suffix of the backward states) in one launch that walks a
+    # head's chunks in order; with fewer heads it runs the chunk-parallel state
+    # launch and a scan.  B x H = 32, 36 (not a multiple of the 8 heads a
+    # workgroup row spans) and 40 with a single chunk; against the oracle, and
+    # against the same heads run one at a time (the other path).
+    import torch
+    log(f"case bwd fused state+scan bf16 B{B} H{H} T{T} d64 dv64 C64")
+    inp = workloads.make_inputs("mid_bf16", B=B, H=H, T=T)
+    dout = _dout(inp["v"].shape, 41 + H)
+    ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
+    o_ref = orc.fwd(inp["q"], inp["k"], inp["v"])
+    got = _gpu_bwd(kata, inp, "bf16", dout, 64, 1, out=o_ref)
+    _check_rel(got, ref, f"B{B} H{H} T{T} bwd", tol=BF16_GRAD_REL)
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out = torch.from_numpy(np.ascontiguousarray(o_ref, dtype=np.float32)).to(q.device)
+    d_out = torch.from_numpy(dout).to(q.device)
+    for b, h in ((0, 0), (B - 1, H - 1)):
+        one = kata.bwd_chunked(*(x[b:b + 1, h:h + 1].contiguous() for x in (q, k, v, out, d_out)),
+                               64, 1)
+        torch.cuda.synchronize()
+        for name, a, g_ in zip(("dq", "dk", "dv"), one, got):
+            a = a.cpu().numpy()[0, 0].astype(np.float64)
+            g_ = g_[b, h].astype(np.float64)
+            rel = np.linalg.norm(a - g_) / max(np.linalg.norm(g_), 1e-30)
+            log(f"  head ({b}, {h}) {name}: fused vs per-head rel l2 {rel:.3e}")
+            assert rel <= BF16_GRAD_REL, (b, h, name)
+
+
 @pytest.mark.parametrize("C,g", [(16, 1), (32, 1), (48, 2), (64, 2), (64, 4)])
 def test_bwd_chunks_and_blocks(kata, orc, C, g):
     T = 700
