@@ -557,7 +557,9 @@ def bwd_record_bytes(d, dv):
 def bwd_bytes(BH, T, d, dv, C):
     """Algorithmic HBM bytes per launch of the bf16-path backward kernels:
     chunk states write one record per chunk and read the chunk's x (bf16) and
-    y rows (v bf16, or a | b fp32); each scan reads and writes every record;
+    y rows (v bf16, or a | b fp32) -- also where the launch writes the scanned
+    records directly (state and scan in one pass); each scan reads and writes
+    every record;
     the gradients read two records, the bf16 q, k, v rows and the fp32 a | b
     rows, and write the fp32 dq, dk, dv rows."""
     NC = -(-T // C)
@@ -626,6 +628,12 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
                  "gradients")
         st = {nm: sum(bev.elapsed(7 * i + j, 7 * i + j + 1) for i in range(steps)) / steps
               for j, nm in enumerate(names)}
+        # with the state and the scan in one launch per record stream, the scan
+        # intervals hold no kernel (their event gaps go to the state stages)
+        fused = kata.bwd_fused_scan(B, H, T, d, dv, C, 1, kata.KATA_BF16) == 1
+        if fused:
+            st["fwd_states"] += st.pop("prefix_scan")
+            st["bwd_states"] += st.pop("suffix_scan")
         fwd_ms = sum(fev.elapsed(4 * i, 4 * i + 3) for i in range(steps)) / steps
         fev.close()
         bev.close()
@@ -644,17 +652,18 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
                 r["mfma_bf16"] = {"achieved": round(tf, 1), "peak": PEAK_BF16_TFLOPS,
                                   "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
             return r
-        rows.append({"T": T, "inputs": src, "train_step_ms": round(ms, 3),
-                     "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
-                     "tokens_per_s": B * T / (ms * 1e-3),
-                     "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
-                     "gradients_roofline": hbm_rate(by["gradients"], st["gradients"], fl["grad"]),
-                     "bwd_states_roofline": hbm_rate(by["bwd_states"], st["bwd_states"],
-                                                     fl["state"]),
-                     "fwd_states_roofline": hbm_rate(by["fwd_states"], st["fwd_states"],
-                                                     fl["state"]),
-                     "suffix_scan_roofline": hbm_rate(by["scan"], st["suffix_scan"]),
-                     "paper_linear_state_m1_train_step_h100_ms": PAPER_TRAIN_STEP_H100.get(T)})
+        row = {"T": T, "inputs": src, "train_step_ms": round(ms, 3),
+               "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
+               "tokens_per_s": B * T / (ms * 1e-3),
+               "state_and_scan_fused": fused,
+               "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
+               "gradients_roofline": hbm_rate(by["gradients"], st["gradients"], fl["grad"]),
+               "bwd_states_roofline": hbm_rate(by["bwd_states"], st["bwd_states"], fl["state"]),
+               "fwd_states_roofline": hbm_rate(by["fwd_states"], st["fwd_states"], fl["state"])}
+        if not fused:
+            row["suffix_scan_roofline"] = hbm_rate(by["scan"], st["suffix_scan"])
+        row["paper_linear_state_m1_train_step_h100_ms"] = PAPER_TRAIN_STEP_H100.get(T)
+        rows.append(row)
         del fws, bws, out, grads, q, k, v, dout
         torch.cuda.empty_cache()
     return {"config": "KATA-M1 B8 H16 d64 dv64 C64, bf16 inputs, fp32 gradients of "

@@ -324,7 +324,9 @@ KATA_API int kata_lin_default_span(int B, int H, int T, int d, int dv, int C,
  *   caller-owned, contents undefined on exit; kata_bwd_chunked allocates it
  *   stream-ordered.  stage_events : 7 caller-created events, recorded before
  *   the first launch and after each of the six (forward states, prefix scan,
- *   per-token coefficients, backward states, suffix scan, gradients).
+ *   per-token coefficients, backward states, suffix scan, gradients); where
+ *   kata_bwd_fused_scan() is 1 each state launch also writes the scanned
+ *   records and the two scan intervals are empty.
  */
 KATA_API kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v,
                                         const float* out, const float* dout, float* dq,
@@ -345,6 +347,12 @@ KATA_API kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, cons
                                               hipEvent_t* stage_events, hipStream_t stream);
 KATA_API size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
                                          kata_dtype_t dtype);
+/* 1 when kata_bwd_chunked* computes the prefix and suffix records of this
+ * shape with the state and the scan in one launch each (bf16 inputs at
+ * d = dv = C = 64, g = 1, from 32 heads B x H on), 0 when it runs a state launch
+ * and a scan launch for each, -1 for an unsupported shape. */
+KATA_API int kata_bwd_fused_scan(int B, int H, int T, int d, int dv, int C, int g,
+                                 kata_dtype_t dtype);
 
 /* Static, human-readable name of a status code. */
 KATA_API const char* kata_status_string(kata_status_t s);

@@ -36,7 +36,7 @@ EXPORTED = (
     "kata_lin_dim", "kata_lin_fwd_chunked", "kata_lin_fwd_chunked_ws",
     "kata_lin_fwd_chunked_timed", "kata_lin_fwd_workspace_bytes", "kata_lin_default_span",
     "kata_bwd_chunked", "kata_bwd_chunked_ws", "kata_bwd_chunked_timed",
-    "kata_bwd_workspace_bytes",
+    "kata_bwd_workspace_bytes", "kata_bwd_fused_scan",
     "kata_fwd_chunked_noalloc", "kata_noalloc_scratch_bytes",
     "kata_status_string", "kata_abi_version",
 )
@@ -130,6 +130,8 @@ def lib():
     L.kata_bwd_chunked_timed.restype = i
     L.kata_bwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
     L.kata_bwd_workspace_bytes.restype = sz
+    L.kata_bwd_fused_scan.argtypes = [i, i, i, i, i, i, i, i]
+    L.kata_bwd_fused_scan.restype = i
     L.kata_status_string.argtypes = [i]
     L.kata_status_string.restype = ctypes.c_char_p
     L.kata_abi_version.argtypes = []
@@ -520,6 +522,11 @@ def lin_fwd_chunked_alloc(q, k, v, C: int, feature: int, eps: float = 0.0,
 
 def bwd_workspace_bytes(B, H, T, d, dv, C, g, dtype_code) -> int:
     return int(lib().kata_bwd_workspace_bytes(B, H, T, d, dv, C, g, dtype_code))
+
+
+def bwd_fused_scan(B, H, T, d, dv, C, g, dtype_code) -> int:
+    """1 when the backward's state launches also scan (kata_bwd_fused_scan)."""
+    return int(lib().kata_bwd_fused_scan(B, H, T, d, dv, C, g, dtype_code))
 
 
 def bwd_chunked(q, k, v, out, dout, C: int, g: int = 1, workspace=None, stream=None,

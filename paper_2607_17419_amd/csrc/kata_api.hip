@@ -416,7 +416,7 @@ bool feature_ok(const kata_lin_feature_t& f) {
 
 extern "C" {
 
-int kata_abi_version(void) { return 104; }
+int kata_abi_version(void) { return 105; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (enum_bits(s)) {
@@ -664,6 +664,12 @@ size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g
   if (!dtype_ok(dtype)) return 0;
   if (bwd_check(B, H, T, d, dv, C, g, dtype) != KATA_OK) return 0;
   return kata::bwd_workspace(B * H, T, d, dv, C, g);
+}
+
+int kata_bwd_fused_scan(int B, int H, int T, int d, int dv, int C, int g, kata_dtype_t dtype) {
+  if (!dtype_ok(dtype)) return -1;
+  if (bwd_check(B, H, T, d, dv, C, g, dtype) != KATA_OK) return -1;
+  return kata::bwd_fused_scan(B * H, d, dv, C, g, dtype == KATA_BF16) ? 1 : 0;
 }
 
 kata_status_t kata_bwd_chunked_ws(const void* q, const void* k, const void* v, const float* out,

@@ -832,7 +832,7 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   // bf16 path: with enough heads to fill the chip, each state launch also
   // scans (one pass, sequential over a head's chunks); with few heads the
   // chunk-parallel state launch and the record scan are faster
-  const bool fused = bf && BH >= bwd_bf_fused_min_heads();
+  const bool fused = bf && bwd_fused_scan(BH, d, dv, C, g, true);
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
   if (fused) {

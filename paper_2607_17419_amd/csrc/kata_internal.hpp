@@ -84,6 +84,10 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
 // one pass, state and scan fused, diagonal features weighted 1/2; used from
 // bwd_bf_fused_min_heads() heads (batch x heads) on.
 int bwd_bf_fused_min_heads();
+// Whether the backward of this shape fuses each state launch with its scan.
+inline bool bwd_fused_scan(int BH, int d, int dv, int C, int g, bool bf16_inputs) {
+  return bf16_inputs && bwd_bf_ok(d, dv, C, g) && BH >= bwd_bf_fused_min_heads();
+}
 hipError_t launch_bwd_prefix_bf(bool backward, const void* x, const void* y, void* rec, int BH,
                                 int T, hipStream_t st);
 // Gradients of every chunk from the scanned records, a_t | b_t rows (ab, row

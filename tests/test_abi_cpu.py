@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 104
+    assert L.kata_abi_version() == 105
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
@@ -254,6 +254,20 @@ def test_lin_workspace_and_span_host_logic():
 ])
 def test_bwd_rejects_before_gpu(args, expect):
     assert kata.lib().kata_bwd_chunked(*args, NUL) == expect
+
+
+def test_bwd_fused_scan_host_logic():
+    L = kata.lib()
+    # bf16 inputs at d = dv = C = 64, g = 1 fuse the state launches with the
+    # scans from 32 heads on; every other supported shape keeps both launches
+    assert L.kata_bwd_fused_scan(2, 16, 333, 64, 64, 64, 1, 1) == 1
+    assert L.kata_bwd_fused_scan(1, 31, 4096, 64, 64, 64, 1, 1) == 0
+    assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 64, 1, 0) == 0   # fp32 inputs
+    assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 32, 1, 1) == 0   # C = 32
+    assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 64, 2, 1) == 0   # g = 2
+    assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 65, 1, 1) == -1  # unsupported
+    assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 64, 1, 7) == -1  # bad dtype
+    assert kata.bwd_fused_scan(8, 16, 4096, 64, 64, 64, 1, kata.KATA_BF16) == 1
 
 
 def test_bwd_workspace_host_logic():
