@@ -737,30 +737,32 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
 // (a, a); S rounded to bf16 once from the fp32 running sum, z in fp32.  Forward
 // (kBwd = false): x = k, y = v, wt = 1.  Backward (kBwd): x = q, y = a_t as a
 // bf16 pair hi + lo, wt = b_t from the coefficient rows.
-// Wave w of workgroup tg owns the 32-feature tile kPW tg + w of one head and
-// walks the head's chunks in scan order with the running sum of its tile in
-// registers: per chunk it writes the running sum as the record (the exclusive
-// prefix), then adds the chunk's state.  Each chunk's x and y are staged in LDS
-// once per workgroup, transposed ([dim][token]), and the next chunk's rows are
-// loaded into registers while the current one is contracted.  The kPG
-// workgroups of a head read the same rows: they are given workgroup ids of one
-// residue mod 8, which the dispatcher sends to one XCD, so the rows come from
-// that XCD's L2.  grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
+// Wave w of workgroup tg owns the 32-feature tile kPW tg + w of one head (the
+// last workgroup's waves past the 65th tile only stage) and walks the head's
+// chunks in scan order with the running sum of its tile in registers: per
+// chunk it writes the running sum as the record (the exclusive prefix), then
+// adds the chunk's state.  Each chunk's x and y are staged in LDS once per
+// workgroup, transposed ([dim][token]), by all four waves (one per SIMD, so
+// that every SIMD carries the same work), and the next chunks' rows are loaded
+// into registers while the current one is contracted.  The kPG workgroups of a
+// head read the same rows: they are given workgroup ids of one residue mod 8,
+// which the dispatcher sends to one XCD, so the rows come from that XCD's L2.
+// grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
 // ---------------------------------------------------------------------------
-constexpr int kPW = 5;                  // waves per workgroup (one feature tile each)
-constexpr int kPG = kBfN / 32 / kPW;    // workgroups per head
-static_assert(kPW * kPG * 32 == kBfN, "the feature tiles split evenly");
+constexpr int kPW = 4;                        // waves per workgroup (one feature tile each)
+constexpr int kPT = kBfN / 32;                // feature tiles per record
+constexpr int kPG = (kPT + kPW - 1) / kPW;    // workgroups per head
+static_assert(kPT * 32 == kBfN && kPW * 64 == 256, "tiles of 32 features; 256 stagers");
 
 // Raw rows of one chunk held in registers between their loads and their
-// staging (masked and converted only when staged, so that the loads stay in
-// flight over the contractions in between).
+// staging (converted only when staged, so that the loads stay in flight over
+// the contractions in between).
 template <bool kBwd>
 struct PrefixRaw {
   uint32_t x[8];
   uint32_t y[kBwd ? 1 : 8];
   float a[kBwd ? 16 : 1];
   float b;
-  int nt;  // valid rows of the chunk
 };
 
 template <bool kBwd>
@@ -779,7 +781,9 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const int NC = (T + 63) / 64;
   const long long hb = static_cast<long long>(bh) * T;
-  const int ft = kPW * tg + w, f = 32 * ft + l32;
+  const int ft = kPW * tg + w;
+  const bool live = ft < kPT;              // wave-uniform
+  const int f = 32 * min(ft, kPT - 1) + l32;
   // the pair (pa, pb) of feature f: the row pa of the upper triangle with
   // D(pa) <= f < D(pa + 1), D(a) = 64 a - a (a - 1) / 2
   int pa = 0;
@@ -788,29 +792,44 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
   // diagonal rows of this wave's tile, one bit per row
   const uint32_t dmask = static_cast<uint32_t>(__ballot(pa == pb));
   const float wz = pa == pb ? 0.5f : 1.f;
-  // staging: threads below 256 take rows 8 rg .. 8 rg + 7, columns 2 cp, 2 cp + 1
-  const int rg = (tid >> 5) & 7, cp = tid & 31;
-  const bool stager = tid < 256;
+  // staging: thread tid takes rows 8 rg .. 8 rg + 7, columns 2 cp, 2 cp + 1
+  const int rg = tid >> 5, cp = tid & 31;
   auto chunk = [&](int it) { return kBwd ? NC - 1 - it : it; };
+  // rows through buffer loads: one resource per chunk whose range ends at the
+  // chunk's last valid row, so rows past the sequence's end read as zero, and
+  // one 32-bit lane offset plus the row number (an immediate) per row
+  const uint32_t xo = static_cast<uint32_t>(2 * (8 * rg * 64 + 2 * cp));
+  const uint32_t ao = static_cast<uint32_t>(4 * (8 * rg * 65 + 2 * cp));
   auto fetch = [&](PrefixRaw<kBwd>& R, int c) {
     const long long t0 = static_cast<long long>(c) * 64;
-    R.nt = static_cast<int>(min(64LL, static_cast<long long>(T) - t0));
-    const uint16_t* xh = x + (hb + t0) * 64;
+    const int nt = static_cast<int>(min(64LL, static_cast<long long>(T) - t0));
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(x + (hb + t0) * 64), 0, nt * 128, kBfWord3);
+    if constexpr (kBwd) {
+      const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(static_cast<const float*>(yv) + (hb + t0) * 65), 0, nt * 260,
+          kBfWord3);
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int tc = min(8 * rg + r, R.nt - 1);
-      R.x[r] = *reinterpret_cast<const uint32_t*>(xh + tc * 64 + 2 * cp);
-      if constexpr (kBwd) {
-        const float* arow = static_cast<const float*>(yv) + (hb + t0 + tc) * 65;
-        R.a[2 * r] = arow[2 * cp];  // rows of 65 floats: 4-byte aligned
-        R.a[2 * r + 1] = arow[2 * cp + 1];
-      } else {
-        const uint16_t* vh = static_cast<const uint16_t*>(yv) + (hb + t0) * 64;
-        R.y[r] = *reinterpret_cast<const uint32_t*>(vh + tc * 64 + 2 * cp);
+      for (int r = 0; r < 8; ++r) {
+        R.x[r] = __builtin_amdgcn_raw_buffer_load_b32(rx, xo + 128 * r, 0, 0);
+        R.a[2 * r] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(ra, ao + 260 * r, 0, 0));
+        R.a[2 * r + 1] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(ra, ao + 260 * r + 4, 0, 0));
+      }
+      if (tid < 64)
+        R.b = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, 260 * tid + 256,
+                                                                             0, 0));
+    } else {
+      const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(static_cast<const uint16_t*>(yv) + (hb + t0) * 64), 0, nt * 128,
+          kBfWord3);
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        R.x[r] = __builtin_amdgcn_raw_buffer_load_b32(rx, xo + 128 * r, 0, 0);
+        R.y[r] = __builtin_amdgcn_raw_buffer_load_b32(ry, xo + 128 * r, 0, 0);
       }
     }
-    if constexpr (kBwd)
-      if (tid < 64) R.b = static_cast<const float*>(yv)[(hb + t0 + min(tid, R.nt - 1)) * 65 + 64];
   };
   auto put_t = [&](uint16_t* dst, const uint32_t* s2) {
     *reinterpret_cast<uint4*>(dst + (2 * cp) * kBP + 8 * rg) =
@@ -824,22 +843,22 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
     uint32_t xv[8], yh[8], yl[8];
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const bool in = 8 * rg + r < R.nt;
-      xv[r] = in ? R.x[r] : 0u;
+      xv[r] = R.x[r];
       if constexpr (kBwd) {
-        const uint32_t hi = pack_bf16x2(R.a[2 * r], R.a[2 * r + 1]);
-        yh[r] = in ? hi : 0u;
-        yl[r] = in ? pack_bf16x2(R.a[2 * r] - bf16lo_f32(hi), R.a[2 * r + 1] - bf16hi_f32(hi))
-                   : 0u;
+        yh[r] = pack_bf16x2(R.a[2 * r], R.a[2 * r + 1]);
+        yl[r] = pack_bf16x2(R.a[2 * r] - bf16lo_f32(yh[r]), R.a[2 * r + 1] - bf16hi_f32(yh[r]));
       } else {
-        yh[r] = in ? R.y[r] : 0u;
+        yh[r] = R.y[r];
+        yl[r] = 0u;
       }
     }
+
     uint16_t* tb = tiles + buf * kBuf;
     put_t(tb, xv);
     put_t(tb + kTile, yh);
     if constexpr (kBwd) put_t(tb + 2 * kTile, yl);
-    if (tid < 64) wts[buf][tid] = tid < R.nt ? (kBwd ? R.b : 1.f) : 0.f;
+    if constexpr (kBwd)
+      if (tid < 64) wts[buf][tid] = R.b;  // zero past the sequence's end
   };
   f32x16 run0 = {}, run1 = {};
   float zrun = 0.f;
@@ -847,17 +866,29 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
   unsigned char* rh = rec + bh * rec_bh;
   // chunk it: write its record (the running sum), then add its state
   auto step = [&](int it) {
+    if (!live) return;
     const int c = chunk(it), buf = it & 1;
-    // record c = the running sum (w = 1/2 on diagonal rows), as whole bf16 rows
-    // through this wave's LDS rows (a wave's LDS accesses complete in order)
+    // record c = the running sum (w = 1/2 on diagonal features), as whole bf16
+    // rows through this wave's LDS rows (a wave's LDS accesses complete in
+    // order).  The running sums are the transposed tile: lane (l32, h) holds
+    // feature f's values j = 8 g + 4 h + 0..3 (run0) and 32 + those (run1),
+    // four consecutive bf16 of the record row per group g.
     unsigned char* r0 = rh + static_cast<long long>(c) * kRecB;
+    auto put_row = [&](float sc) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int r = 8 * (i >> 2) + 4 * h + (i & 3);
-      const float wr = (dmask >> r) & 1u ? 0.5f : 1.f;
-      ow[r * kBP + l32] = bf_bits(wr * run0[i]);
-      ow[r * kBP + 32 + l32] = bf_bits(wr * run1[i]);
-    }
+      for (int g = 0; g < 4; ++g) {
+        *reinterpret_cast<uint2*>(ow + l32 * kBP + 8 * g + 4 * h) =
+            make_uint2(pack_bf16x2(sc * run0[4 * g], sc * run0[4 * g + 1]),
+                       pack_bf16x2(sc * run0[4 * g + 2], sc * run0[4 * g + 3]));
+        *reinterpret_cast<uint2*>(ow + l32 * kBP + 32 + 8 * g + 4 * h) =
+            make_uint2(pack_bf16x2(sc * run1[4 * g], sc * run1[4 * g + 1]),
+                       pack_bf16x2(sc * run1[4 * g + 2], sc * run1[4 * g + 3]));
+      }
+    };
+    if (dmask != 0u)
+      put_row(wz);
+    else
+      put_row(1.f);  // no diagonal feature in this tile: no weight
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int ch = lane + 64 * q4, r = ch >> 3, part = ch & 7;
@@ -869,6 +900,7 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
     const uint16_t* yT = xT + kTile;
     const uint16_t* yL = xT + 2 * kTile;
     const float* wt = wts[buf];
+    (void)wt;
     float zp = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
@@ -882,14 +914,18 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
         const float p0 = bf16lo_f32(wa[e]) * bf16lo_f32(wb[e]);
         const float p1 = bf16hi_f32(wa[e]) * bf16hi_f32(wb[e]);
         pk[e] = pack_bf16x2(p0, p1);
-        zp += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;  // padded tokens: wt = 0
+        if constexpr (kBwd)  // padded tokens: wt = 0
+          zp += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;
+        else  // padded tokens: x = 0
+          zp += p0 + p1;
       }
-      const bf16x8 A = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-      run0 = mfma_bf(A, ld8(yT + l32 * kBP + tk), run0);
-      run1 = mfma_bf(A, ld8(yT + (32 + l32) * kBP + tk), run1);
+      // S^T tile: rows j of y (A operand), columns the 32 features (B operand)
+      const bf16x8 P = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      run0 = mfma_bf(ld8(yT + l32 * kBP + tk), P, run0);
+      run1 = mfma_bf(ld8(yT + (32 + l32) * kBP + tk), P, run1);
       if constexpr (kBwd) {
-        run0 = mfma_bf(A, ld8(yL + l32 * kBP + tk), run0);
-        run1 = mfma_bf(A, ld8(yL + (32 + l32) * kBP + tk), run1);
+        run0 = mfma_bf(ld8(yL + l32 * kBP + tk), P, run0);
+        run1 = mfma_bf(ld8(yL + (32 + l32) * kBP + tk), P, run1);
       }
     }
     zrun += zp + __shfl_xor(zp, 32);
@@ -908,25 +944,19 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
   // are never staged): with the same loads on every path the compiler's wait
   // before each staging counts exactly the loads and stores issued after it.
   auto ahead = [&](int it) { return chunk(min(it, NC - 1)); };
-  if (stager) {
-    fetch(R0, chunk(0));
-    stage(R0, 0);
-    fetch(R1, ahead(1));
-    if (kAhead == 2) fetch(R0, ahead(2));
-  }
+  fetch(R0, chunk(0));
+  stage(R0, 0);
+  fetch(R1, ahead(1));
+  if (kAhead == 2) fetch(R0, ahead(2));
   lds_barrier();
   for (int it = 0; it < NC; it += 2) {
-    if (stager) {
-      if (it + 1 < NC) stage(R1, 1);
-      fetch(R1, ahead(it + 1 + kAhead));
-    }
+    if (it + 1 < NC) stage(R1, 1);
+    fetch(R1, ahead(it + 1 + kAhead));
     step(it);
     lds_barrier();  // buffer 0 is read by every wave; buffer 1 is staged
     if (it + 1 >= NC) break;
-    if (stager) {
-      if (it + 2 < NC) stage(R0, 0);
-      fetch(R0, ahead(it + 2 + kAhead));
-    }
+    if (it + 2 < NC) stage(R0, 0);
+    fetch(R0, ahead(it + 2 + kAhead));
     step(it + 1);
     lds_barrier();
   }
@@ -975,8 +1005,8 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
   return hipGetLastError();
 }
 
-// The fused launch runs 13 workgroups per head, each sequential over the
-// head's chunks: below 32 heads (416 workgroups, under two per CU) the
+// The fused launch runs 17 workgroups per head, each sequential over the
+// head's chunks: below 32 heads (544 workgroups, about two per CU) the
 // chunk-parallel state launch plus the scan is faster (measured at T = 4096:
 // 8 heads 0.11 ms fused against 0.09 ms; 40 heads 0.35 against 0.41 ms).
 int bwd_bf_fused_min_heads() { return 32; }
