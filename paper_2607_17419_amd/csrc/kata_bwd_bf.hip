@@ -737,11 +737,12 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
 // (a, a); S rounded to bf16 once from the fp32 running sum, z in fp32.  Forward
 // (kBwd = false): x = k, y = v, wt = 1.  Backward (kBwd): x = q, y = a_t as a
 // bf16 pair hi + lo, wt = b_t from the coefficient rows.
-// Wave w of workgroup tg owns the 32-feature tile kPW tg + w of one head (the
-// last workgroup's waves past the 65th tile only stage) and walks the head's
-// chunks in scan order with the running sum of its tile in registers: per
-// chunk it writes the running sum as the record (the exclusive prefix), then
-// adds the chunk's state.  Each chunk's x and y are staged in LDS once per
+// Wave w of workgroup tg owns the kTW 32-feature tiles kTW (kPW tg + w) + u of
+// one head (tiles past the 65th are skipped; a wave with none only stages)
+// and walks the head's chunks in scan order with the running sums of its tiles
+// in registers: per chunk it writes each running sum as the record (the
+// exclusive prefix), then adds the chunk's state.  Two tiles per wave give two
+// independent MFMA chains and share the y operands.  Each chunk's x and y are staged in LDS once per
 // workgroup, transposed ([dim][token]), by all four waves (one per SIMD, so
 // that every SIMD carries the same work), and the next chunks' rows are loaded
 // into registers while the current one is contracted.  The kPG workgroups of a
@@ -749,9 +750,10 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
 // which the dispatcher sends to one XCD, so the rows come from that XCD's L2.
 // grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
 // ---------------------------------------------------------------------------
-constexpr int kPW = 4;                        // waves per workgroup (one feature tile each)
+constexpr int kPW = 4;                        // waves per workgroup
+constexpr int kTW = 2;                        // feature tiles per wave
 constexpr int kPT = kBfN / 32;                // feature tiles per record
-constexpr int kPG = (kPT + kPW - 1) / kPW;    // workgroups per head
+constexpr int kPG = (kPT + kPW * kTW - 1) / (kPW * kTW);  // workgroups per head
 static_assert(kPT * 32 == kBfN && kPW * 64 == 256, "tiles of 32 features; 256 stagers");
 
 // Raw rows of one chunk held in registers between their loads and their
@@ -781,17 +783,25 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const int NC = (T + 63) / 64;
   const long long hb = static_cast<long long>(bh) * T;
-  const int ft = kPW * tg + w;
-  const bool live = ft < kPT;              // wave-uniform
-  const int f = 32 * min(ft, kPT - 1) + l32;
-  // the pair (pa, pb) of feature f: the row pa of the upper triangle with
-  // D(pa) <= f < D(pa + 1), D(a) = 64 a - a (a - 1) / 2
-  int pa = 0;
-  while (pa < 63 && 64 * (pa + 1) - (pa + 1) * pa / 2 <= f) ++pa;
-  const int pb = pa + f - (64 * pa - pa * (pa - 1) / 2);
-  // diagonal rows of this wave's tile, one bit per row
-  const uint32_t dmask = static_cast<uint32_t>(__ballot(pa == pb));
-  const float wz = pa == pb ? 0.5f : 1.f;
+  const int ft0 = kTW * (kPW * tg + w);
+  const int nlive = max(0, min(kTW, kPT - ft0));  // tiles of this wave (wave-uniform)
+  int ft[kTW], f[kTW], pa[kTW], pb[kTW];
+  uint32_t dmask[kTW];
+  float wz[kTW];
+#pragma unroll
+  for (int u = 0; u < kTW; ++u) {
+    ft[u] = min(ft0 + u, kPT - 1);
+    f[u] = 32 * ft[u] + l32;
+    // the pair (pa, pb) of feature f: the row pa of the upper triangle with
+    // D(pa) <= f < D(pa + 1), D(a) = 64 a - a (a - 1) / 2
+    int a = 0;
+    while (a < 63 && 64 * (a + 1) - (a + 1) * a / 2 <= f[u]) ++a;
+    pa[u] = a;
+    pb[u] = a + f[u] - (64 * a - a * (a - 1) / 2);
+    // diagonal features of the tile, one bit per lane's feature
+    dmask[u] = static_cast<uint32_t>(__ballot(pa[u] == pb[u]));
+    wz[u] = pa[u] == pb[u] ? 0.5f : 1.f;
+  }
   // staging: thread tid takes rows 8 rg .. 8 rg + 7, columns 2 cp, 2 cp + 1
   const int rg = tid >> 5, cp = tid & 31;
   auto chunk = [&](int it) { return kBwd ? NC - 1 - it : it; };
@@ -860,75 +870,95 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
     if constexpr (kBwd)
       if (tid < 64) wts[buf][tid] = R.b;  // zero past the sequence's end
   };
-  f32x16 run0 = {}, run1 = {};
-  float zrun = 0.f;
+  f32x16 run0[kTW], run1[kTW];
+  float zrun[kTW];
+#pragma unroll
+  for (int u = 0; u < kTW; ++u) {
+    run0[u] = f32x16{};
+    run1[u] = f32x16{};
+    zrun[u] = 0.f;
+  }
   uint16_t* ow = ot + w * 32 * kBP;
   unsigned char* rh = rec + bh * rec_bh;
-  // chunk it: write its record (the running sum), then add its state
-  auto step = [&](int it) {
-    if (!live) return;
-    const int c = chunk(it), buf = it & 1;
-    // record c = the running sum (w = 1/2 on diagonal features), as whole bf16
-    // rows through this wave's LDS rows (a wave's LDS accesses complete in
-    // order).  The running sums are the transposed tile: lane (l32, h) holds
-    // feature f's values j = 8 g + 4 h + 0..3 (run0) and 32 + those (run1),
-    // four consecutive bf16 of the record row per group g.
-    unsigned char* r0 = rh + static_cast<long long>(c) * kRecB;
+  // record c = the running sum of tile u (w = 1/2 on diagonal features), as
+  // whole bf16 rows through this wave's LDS rows (a wave's LDS accesses
+  // complete in order).  The running sums are the transposed tile: lane
+  // (l32, h) holds feature f's values j = 8 g + 4 h + 0..3 (run0) and 32 +
+  // those (run1), four consecutive bf16 of the record row per group g.
+  auto put_record = [&](unsigned char* r0, int u) {
     auto put_row = [&](float sc) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         *reinterpret_cast<uint2*>(ow + l32 * kBP + 8 * g + 4 * h) =
-            make_uint2(pack_bf16x2(sc * run0[4 * g], sc * run0[4 * g + 1]),
-                       pack_bf16x2(sc * run0[4 * g + 2], sc * run0[4 * g + 3]));
+            make_uint2(pack_bf16x2(sc * run0[u][4 * g], sc * run0[u][4 * g + 1]),
+                       pack_bf16x2(sc * run0[u][4 * g + 2], sc * run0[u][4 * g + 3]));
         *reinterpret_cast<uint2*>(ow + l32 * kBP + 32 + 8 * g + 4 * h) =
-            make_uint2(pack_bf16x2(sc * run1[4 * g], sc * run1[4 * g + 1]),
-                       pack_bf16x2(sc * run1[4 * g + 2], sc * run1[4 * g + 3]));
+            make_uint2(pack_bf16x2(sc * run1[u][4 * g], sc * run1[u][4 * g + 1]),
+                       pack_bf16x2(sc * run1[u][4 * g + 2], sc * run1[u][4 * g + 3]));
       }
     };
-    if (dmask != 0u)
-      put_row(wz);
+    if (dmask[u] != 0u)
+      put_row(wz[u]);
     else
       put_row(1.f);  // no diagonal feature in this tile: no weight
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int ch = lane + 64 * q4, r = ch >> 3, part = ch & 7;
-      *reinterpret_cast<uint4*>(r0 + static_cast<long long>(32 * ft + r) * 128 + 16 * part) =
+      *reinterpret_cast<uint4*>(r0 + static_cast<long long>(32 * ft[u] + r) * 128 + 16 * part) =
           *reinterpret_cast<const uint4*>(ow + r * kBP + 8 * part);
     }
-    if (h == 0) reinterpret_cast<float*>(r0 + kRecSB)[f] = wz * zrun;
+    if (h == 0) reinterpret_cast<float*>(r0 + kRecSB)[f[u]] = wz[u] * zrun[u];
+  };
+  // chunk it: write its records (the running sums), then add its state
+  auto step = [&](int it) {
+    if (nlive == 0) return;
+    const int c = chunk(it), buf = it & 1;
+    unsigned char* r0 = rh + static_cast<long long>(c) * kRecB;
+    put_record(r0, 0);
+    if (nlive == kTW) put_record(r0, 1);
     const uint16_t* xT = tiles + buf * kBuf;
     const uint16_t* yT = xT + kTile;
     const uint16_t* yL = xT + 2 * kTile;
     const float* wt = wts[buf];
-    (void)wt;
-    float zp = 0.f;
+    float zp[kTW] = {};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int tk = 16 * ks + 8 * h;
-      const uint4 xa = *reinterpret_cast<const uint4*>(xT + pa * kBP + tk);
-      const uint4 xb = *reinterpret_cast<const uint4*>(xT + pb * kBP + tk);
-      const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w}, wb[4] = {xb.x, xb.y, xb.z, xb.w};
-      uint32_t pk[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = bf16lo_f32(wa[e]) * bf16lo_f32(wb[e]);
-        const float p1 = bf16hi_f32(wa[e]) * bf16hi_f32(wb[e]);
-        pk[e] = pack_bf16x2(p0, p1);
-        if constexpr (kBwd)  // padded tokens: wt = 0
-          zp += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;
-        else  // padded tokens: x = 0
-          zp += p0 + p1;
-      }
-      // S^T tile: rows j of y (A operand), columns the 32 features (B operand)
-      const bf16x8 P = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-      run0 = mfma_bf(ld8(yT + l32 * kBP + tk), P, run0);
-      run1 = mfma_bf(ld8(yT + (32 + l32) * kBP + tk), P, run1);
+      // the y rows j = l32 and 32 + l32 of this K step, shared by the tiles
+      const bf16x8 y0 = ld8(yT + l32 * kBP + tk), y1 = ld8(yT + (32 + l32) * kBP + tk);
+      bf16x8 l0, l1;
       if constexpr (kBwd) {
-        run0 = mfma_bf(ld8(yL + l32 * kBP + tk), P, run0);
-        run1 = mfma_bf(ld8(yL + (32 + l32) * kBP + tk), P, run1);
+        l0 = ld8(yL + l32 * kBP + tk);
+        l1 = ld8(yL + (32 + l32) * kBP + tk);
+      }
+#pragma unroll
+      for (int u = 0; u < kTW; ++u) {
+        const uint4 xa = *reinterpret_cast<const uint4*>(xT + pa[u] * kBP + tk);
+        const uint4 xb = *reinterpret_cast<const uint4*>(xT + pb[u] * kBP + tk);
+        const uint32_t wa[4] = {xa.x, xa.y, xa.z, xa.w}, wb[4] = {xb.x, xb.y, xb.z, xb.w};
+        uint32_t pk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = bf16lo_f32(wa[e]) * bf16lo_f32(wb[e]);
+          const float p1 = bf16hi_f32(wa[e]) * bf16hi_f32(wb[e]);
+          pk[e] = pack_bf16x2(p0, p1);
+          if constexpr (kBwd)  // padded tokens: wt = 0
+            zp[u] += wt[tk + 2 * e] * p0 + wt[tk + 2 * e + 1] * p1;
+          else  // padded tokens: x = 0
+            zp[u] += p0 + p1;
+        }
+        // S^T tile: rows j of y (A operand), columns the 32 features (B operand)
+        const bf16x8 P = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+        run0[u] = mfma_bf(y0, P, run0[u]);
+        run1[u] = mfma_bf(y1, P, run1[u]);
+        if constexpr (kBwd) {
+          run0[u] = mfma_bf(l0, P, run0[u]);
+          run1[u] = mfma_bf(l1, P, run1[u]);
+        }
       }
     }
-    zrun += zp + __shfl_xor(zp, 32);
+#pragma unroll
+    for (int u = 0; u < kTW; ++u) zrun[u] += zp[u] + __shfl_xor(zp[u], 32);
   };
   // Chunk it + 1 is staged (LDS buffer (it + 1) & 1) while chunk it is
   // contracted from the other buffer, and the loads of chunk it + 1 + kAhead
@@ -1005,8 +1035,8 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
   return hipGetLastError();
 }
 
-// The fused launch runs 17 workgroups per head, each sequential over the
-// head's chunks: below 32 heads (544 workgroups, about two per CU) the
+// The fused launch runs 9 workgroups per head, each sequential over the
+// head's chunks: below 32 heads (288 workgroups, about one per CU) the
 // chunk-parallel state launch plus the scan is faster (measured at T = 4096:
 // 8 heads 0.11 ms fused against 0.09 ms; 40 heads 0.35 against 0.41 ms).
 int bwd_bf_fused_min_heads() { return 32; }
