@@ -189,6 +189,21 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   const Tin* qh = q + (static_cast<long long>(bh) * T + t0) * d;
   const Tin* kh = k + (static_cast<long long>(bh) * T + t0) * d;
   const float* zp = zsrc + bh * z_bh + c * z_c;
+  // the output and cotangent rows of the epilogue (4 lanes per token, columns
+  // p, p + 4, ...), loaded first so that they arrive under the contractions
+  const int r = tid >> 2, p = tid & 3;
+  constexpr int kEJ = 16;  // columns per lane when dv <= 64
+  const long long row = static_cast<long long>(bh) * T + t0 + r;
+  float dre[kEJ], ore[kEJ];
+  const bool pre = dv <= 4 * kEJ && r < nt;
+  if (pre) {
+#pragma unroll
+    for (int i = 0; i < kEJ; ++i) {
+      const int j = p + 4 * i;
+      dre[i] = j < dv ? dout[row * dv + j] : 0.f;
+      ore[i] = j < dv ? o[row * dv + j] : 0.f;
+    }
+  }
   // z_pre (g nm <= 2080 floats) is read once, coalesced, into the k tile's
   // LDS and unpacked from there; q and k rows are read in 8-element pieces
   // (16 bytes of bf16) where d allows it, k held in registers until every
@@ -294,19 +309,25 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
     if (h == 0) red[X * 64 + t] = part;
   }
   __syncthreads();
-  const int r = tid >> 2, p = tid & 3;
   if (r < nt) {
     const float D = red[r] + red[64 + r];
-    const long long row = static_cast<long long>(bh) * T + t0 + r;
-    const float* dr = dout + row * dv;
-    const float* orow = o + row * dv;
-    float go = 0.f;
-    for (int j = p; j < dv; j += 4) go += dr[j] * orow[j];
-    go += __shfl_xor(go, 1);
-    go += __shfl_xor(go, 2);
     float* abr = ab + row * (dv + 1);
     const float inv = D > 0.f ? 1.f / D : 0.f;
-    for (int j = p; j < dv; j += 4) abr[j] = dr[j] * inv;
+    float go = 0.f;
+    if (pre) {
+#pragma unroll
+      for (int i = 0; i < kEJ; ++i) go += dre[i] * ore[i];
+#pragma unroll
+      for (int i = 0; i < kEJ; ++i)
+        if (p + 4 * i < dv) abr[p + 4 * i] = dre[i] * inv;
+    } else {
+      const float* dr = dout + row * dv;
+      const float* orow = o + row * dv;
+      for (int j = p; j < dv; j += 4) go += dr[j] * orow[j];
+      for (int j = p; j < dv; j += 4) abr[j] = dr[j] * inv;
+    }
+    go += __shfl_xor(go, 1);
+    go += __shfl_xor(go, 2);
     if (p == 0) abr[dv] = -go * inv;
   }
 }
