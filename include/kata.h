@@ -349,7 +349,7 @@ KATA_API size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int
                                          kata_dtype_t dtype);
 /* 1 when kata_bwd_chunked* computes the prefix and suffix records of this
  * shape with the state and the scan in one launch each (bf16 inputs at
- * d = dv = C = 64, g = 1, from 32 heads B x H on), 0 when it runs a state launch
+ * d = dv = C = 64, g = 1, from 16 heads B x H on), 0 when it runs a state launch
  * and a scan launch for each, -1 for an unsupported shape. */
 KATA_API int kata_bwd_fused_scan(int B, int H, int T, int d, int dv, int C, int g,
                                  kata_dtype_t dtype);

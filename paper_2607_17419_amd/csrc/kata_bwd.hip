@@ -850,8 +850,8 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   // (the C ABI has checked that every tensor is 16-byte aligned)
   bool bf = false;
   if constexpr (std::is_same<Tin, bf16_t>::value) bf = bwd_bf_ok(d, dv, C, g);
-  // bf16 path: with enough heads to fill the chip, each state launch also
-  // scans (one pass, sequential over a head's chunks); with few heads the
+  // bf16 path: from bwd_bf_fused_min_heads() heads on, each state launch also
+  // scans (one pass, sequential over a head's chunks); with fewer heads the
   // chunk-parallel state launch and the record scan are faster
   const bool fused = bf && bwd_fused_scan(BH, d, dv, C, g, true);
   hipError_t e = record(ev, 0, st);

@@ -1035,11 +1035,13 @@ hipError_t launch_bwd_scan_bf(bool reverse, void* rec, int BH, int T, hipStream_
   return hipGetLastError();
 }
 
-// The fused launch runs 9 workgroups per head, each sequential over the
-// head's chunks: below 32 heads (288 workgroups, about one per CU) the
-// chunk-parallel state launch plus the scan is faster (measured at T = 4096:
-// 8 heads 0.11 ms fused against 0.09 ms; 40 heads 0.35 against 0.41 ms).
-int bwd_bf_fused_min_heads() { return 32; }
+// The fused launches run 9 workgroups per head, each sequential over the
+// head's chunks, so their time hardly depends on the head count until the
+// chip is full: forward + backward record streams at T = 4096 take 0.29 ms
+// fused from 4 to 16 heads, while the chunk-parallel state launches and
+// scans take 0.18 ms at 8 heads and 0.36 ms at 16 (0.43 against 0.67 ms at 32
+// heads, 0.54 against 0.97 ms at 48).
+int bwd_bf_fused_min_heads() { return 16; }
 
 hipError_t launch_bwd_prefix_bf(bool backward, const void* x, const void* y, void* rec, int BH,
                                 int T, hipStream_t st) {

@@ -259,9 +259,9 @@ def test_bwd_rejects_before_gpu(args, expect):
 def test_bwd_fused_scan_host_logic():
     L = kata.lib()
     # bf16 inputs at d = dv = C = 64, g = 1 fuse the state launches with the
-    # scans from 32 heads on; every other supported shape keeps both launches
-    assert L.kata_bwd_fused_scan(2, 16, 333, 64, 64, 64, 1, 1) == 1
-    assert L.kata_bwd_fused_scan(1, 31, 4096, 64, 64, 64, 1, 1) == 0
+    # scans from 16 heads on; every other supported shape keeps both launches
+    assert L.kata_bwd_fused_scan(2, 8, 333, 64, 64, 64, 1, 1) == 1
+    assert L.kata_bwd_fused_scan(1, 15, 4096, 64, 64, 64, 1, 1) == 0
     assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 64, 1, 0) == 0   # fp32 inputs
     assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 32, 1, 1) == 0   # C = 32
     assert L.kata_bwd_fused_scan(8, 16, 4096, 64, 64, 64, 2, 1) == 0   # g = 2
