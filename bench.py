@@ -838,6 +838,8 @@ def main():
                     help="only run the plain-copy calibration kernel (for rocprofv3 --pmc)")
     ap.add_argument("--decode-probe", action="store_true",
                     help="only run the decode workload (for rocprofv3 --pmc)")
+    ap.add_argument("--backward-probe", action="store_true",
+                    help="only run the training step at T = 4096 (for rocprofv3 --pmc)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-workload forward rows (tiny, mid, recall)")
     ap.add_argument("--ingest-traffic", metavar="DIR",
@@ -863,6 +865,11 @@ def main():
     if args.decode_probe:
         import paper_2607_17419_amd as kata
         res = bench_decode(kata, "cuda:0", _hip())
+        print(json.dumps(res), flush=True)
+        return
+    if args.backward_probe:
+        import paper_2607_17419_amd as kata
+        res = bench_backward(kata, "cuda:0", _hip(), Ts=(4096,), steps=3, warmup=1)
         print(json.dumps(res), flush=True)
         return
 
