@@ -179,6 +179,34 @@ def test_bwd_fused_state_scan(kata, orc, B, H, T):
             assert rel <= BF16_GRAD_REL, (b, h, name)
 
 
+def test_bwd_fused_long_against_chunk_parallel(kata):
+    # 16 heads of 16421 tokens (257 chunks, the last one 37 tokens): the fused
+    # state+scan walk over many chunks against the chunk-parallel states and
+    # the blocked scan (the same heads run one at a time), on the same forward
+    # output; the two differ only in where the chunk states are rounded
+    import torch
+    B, H, T = 1, 16, 16384 + 37
+    log(f"case bwd fused vs chunk-parallel bf16 B{B} H{H} T{T} d64 C64")
+    assert kata.bwd_fused_scan(B, H, T, 64, 64, 64, 1, kata.KATA_BF16) == 1
+    assert kata.bwd_fused_scan(1, 1, T, 64, 64, 64, 1, kata.KATA_BF16) == 0
+    inp = workloads.make_inputs("mid_bf16", B=B, H=H, T=T)
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out = kata.fwd_chunked(q, k, v, 64)
+    d_out = torch.from_numpy(_dout(inp["v"].shape, 43)).to(q.device)
+    got = kata.bwd_chunked(q, k, v, out, d_out, 64, 1)
+    torch.cuda.synchronize()
+    for h in (0, 7, 15):
+        one = kata.bwd_chunked(*(x[:, h:h + 1].contiguous() for x in (q, k, v, out, d_out)), 64, 1)
+        torch.cuda.synchronize()
+        for name, a, g_ in zip(("dq", "dk", "dv"), one, got):
+            a = a[0, 0].double()
+            b = g_[0, h].double()
+            assert torch.isfinite(b).all(), (h, name)
+            rel = float((a - b).norm() / max(float(b.norm()), 1e-30))
+            log(f"  head {h} {name}: fused vs chunk-parallel rel l2 {rel:.3e}")
+            assert rel <= BF16_GRAD_REL, (h, name)
+
+
 @pytest.mark.parametrize("C,g", [(16, 1), (32, 1), (48, 2), (64, 2), (64, 4)])
 def test_bwd_chunks_and_blocks(kata, orc, C, g):
     T = 700
