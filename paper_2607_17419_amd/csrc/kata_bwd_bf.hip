@@ -904,8 +904,8 @@ __global__ __launch_bounds__(64 * kPW) void bwd_prefix_bf(const uint16_t* __rest
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int ch = lane + 64 * q4, r = ch >> 3, part = ch & 7;
-      *reinterpret_cast<uint4*>(r0 + static_cast<long long>(32 * ft[u] + r) * 128 + 16 * part) =
-          *reinterpret_cast<const uint4*>(ow + r * kBP + 8 * part);
+      stream_store_u4(r0 + static_cast<long long>(32 * ft[u] + r) * 128 + 16 * part,
+                      *reinterpret_cast<const uint4*>(ow + r * kBP + 8 * part));
     }
     if (h == 0) reinterpret_cast<float*>(r0 + kRecSB)[f[u]] = wz[u] * zrun[u];
   };
