@@ -748,7 +748,9 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
 // into registers while the current one is contracted.  The kPG workgroups of a
 // head read the same rows: they are given workgroup ids of one residue mod 8,
 // which the dispatcher sends to one XCD, so the rows come from that XCD's L2.
-// grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
+// The records are written past the caches (non-temporal): only later launches
+// read them, and cached they would evict from L2 the rows that the head's
+// other workgroups are about to read.  grid (kPG x 8 ceil(BH / 8)), block 64 kPW.
 // ---------------------------------------------------------------------------
 constexpr int kPW = 4;                        // waves per workgroup
 constexpr int kTW = 2;                        // feature tiles per wave
