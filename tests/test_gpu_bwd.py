@@ -147,14 +147,16 @@ def test_bwd_ragged_m1(kata, orc, T):
     _check_rel(_gpu_bwd(kata, inp, "bf16", dout, 64, 1), ref, f"T{T} fwd+bwd", per_row=False)
 
 
-@pytest.mark.parametrize("B,H,T", [(2, 16, 333), (3, 6, 130), (2, 8, 200), (1, 40, 64)])
+@pytest.mark.parametrize("B,H,T", [(2, 16, 333), (3, 6, 130), (2, 8, 200), (1, 40, 64),
+                                   (16, 1, 37)])
 def test_bwd_fused_state_scan(kata, orc, B, H, T):
     # From 16 heads on, the bf16 path computes each record stream (prefix of the
     # forward states, suffix of the backward states) in one launch that walks a
     # head's chunks in order; with fewer heads it runs the chunk-parallel state
     # launch and a scan.  B x H = 32, 18 (not a multiple of the 8 heads a
-    # workgroup row spans), 16 (the smallest fused count) and 40 with a single
-    # chunk; against the oracle, and
+    # workgroup row spans), 16 (the smallest fused count), 40 with a single
+    # chunk and 16 batches of one head with one partial chunk; against the
+    # oracle, and
     # against the same heads run one at a time (the other path).
     import torch
     log(f"case bwd fused state+scan bf16 B{B} H{H} T{T} d64 dv64 C64")
