@@ -181,6 +181,35 @@ def test_bwd_fused_state_scan(kata, orc, B, H, T):
             assert rel <= BF16_GRAD_REL, (b, h, name)
 
 
+def test_bwd_bench_configuration_sampled_heads(kata, orc):
+    # the training step's own shape (the mid workload, B8 H16 T4096, 128 heads:
+    # the fused state+scan path) against the oracle on three heads; those
+    # heads get the exact forward output, so the per-row bound applies
+    import torch
+    w = workloads.WORKLOADS["mid_bf16"]
+    log(f"case bwd bench configuration B{w.B} H{w.H} T{w.T} d64 C64, heads 0, 77, 127")
+    assert kata.bwd_fused_scan(w.B, w.H, w.T, 64, 64, 64, 1, kata.KATA_BF16) == 1
+    inp = workloads.make_inputs("mid_bf16")
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out = kata.fwd_chunked(q, k, v, 64)
+    dout = _dout(inp["v"].shape, 47)
+    heads = [0, 77, w.B * w.H - 1]
+    sel = lambda x, bh: x.reshape(w.B * w.H, w.T, x.shape[-1])[bh][None, None]
+    o_ex = {bh: orc.fwd(sel(inp["q"], bh), sel(inp["k"], bh), sel(inp["v"], bh)) for bh in heads}
+    out_flat = out.view(w.B * w.H, w.T, 64)
+    for bh in heads:
+        out_flat[bh] = torch.from_numpy(np.ascontiguousarray(o_ex[bh][0, 0], dtype=np.float32)).to(
+            out.device)
+    d_out = torch.from_numpy(dout).to(q.device)
+    got = kata.bwd_chunked(q, k, v, out, d_out, 64, 1)
+    torch.cuda.synchronize()
+    got = [g_.cpu().numpy() for g_ in got]
+    for bh in heads:
+        ref = orc.bwd_mg(sel(inp["q"], bh), sel(inp["k"], bh), sel(inp["v"], bh), sel(dout, bh), 1)
+        mine = tuple(sel(g_, bh) for g_ in got)
+        _check_rel(mine, ref, f"head {bh} bwd", tol=BF16_GRAD_REL)
+
+
 def test_bwd_fused_long_against_chunk_parallel(kata):
     # 16 heads of 16421 tokens (257 chunks, the last one 37 tokens): the fused
     # state+scan walk over many chunks against the chunk-parallel states and
