@@ -742,10 +742,11 @@ __global__ __launch_bounds__(kSC * kSG) void scan_bf(unsigned char* __restrict__
 // and walks the head's chunks in scan order with the running sums of its tiles
 // in registers: per chunk it writes each running sum as the record (the
 // exclusive prefix), then adds the chunk's state.  Two tiles per wave give two
-// independent MFMA chains and share the y operands.  Each chunk's x and y are staged in LDS once per
-// workgroup, transposed ([dim][token]), by all four waves (one per SIMD, so
-// that every SIMD carries the same work), and the next chunks' rows are loaded
-// into registers while the current one is contracted.  The kPG workgroups of a
+// independent MFMA chains and share the y operands.  Each chunk's x and y are
+// staged in LDS once per workgroup, transposed ([dim][token]), by all four
+// waves (one per SIMD, so that every SIMD carries the same work), and the next
+// chunks' rows are loaded into registers while the current one is
+// contracted.  The kPG workgroups of a
 // head read the same rows: they are given workgroup ids of one residue mod 8,
 // which the dispatcher sends to one XCD, so the rows come from that XCD's L2.
 // The records are written past the caches (non-temporal): only later launches
