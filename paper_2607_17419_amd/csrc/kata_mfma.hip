@@ -295,8 +295,8 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
                                                          const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ spanst,
                                                          uint16_t* __restrict__ vtp, int T,
-                                                         int L, int LV, int NS, int sp0,
-                                                         int nsp) {
+                                                         int L, int LV, int NS, int BH,
+                                                         int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   using SG = StateGrid<D, DV, NG>;
   constexpr int UW = SG::UW;
@@ -327,9 +327,14 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
   const int id = blockIdx.x;
   const int jx = id >> 3;
   const int part = jx % SG::NB;
-  const int sp = sp0 + 8 * (jx / SG::NB) + (id & 7);
-  if (sp >= nsp) return;  // whole workgroup: padding of the grid
-  const int s = sp % NS, bh = sp / NS;
+  // Work item li over the NS - 1 spans per head that enter a prefix (each
+  // head's last span is left out: vt_permute_kernel writes its V^T), head by
+  // head.  All of these spans carry the same work, so the XCD a work item
+  // lands on (work item mod 8) needs no balancing.
+  const int li = sp0 + 8 * (jx / SG::NB) + (id & 7);
+  if (li >= nsp) return;  // whole workgroup: padding of the grid
+  const int s = li % (NS - 1), bh = li / (NS - 1);
+  const int sp = bh * NS + s;  // span record index
   const int gw = part * NW + wave;  // wave index inside the span
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
@@ -1274,7 +1279,7 @@ template <int D, int DV, int NG>
 __global__ __launch_bounds__(512) void span_output8_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
-    int T, int L, int LV, int NS, int QB, int sp0, int nsp) {
+    int T, int L, int LV, int NS, int BH, int QB, int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   static_assert(DV == 64, "the eight-wave form covers dv = 64");
   constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM, KZ = G::KZ;
@@ -1302,9 +1307,13 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   const int id = blockIdx.x;
   const int jx = id >> 3;
   const int qb = jx % QB;
-  const int sp = sp0 + 8 * (jx / QB) + (id & 7);
-  if (sp >= nsp) return;  // whole workgroup: padding of the grid
-  const int s = sp % NS, bh = sp / NS;
+  // Work item li in span-major order, last spans first: the first spans (no
+  // readout) come last and fill the tail, and the eight XCDs (work item mod
+  // 8) get equal shares of every span position.
+  const int li = sp0 + 8 * (jx / QB) + (id & 7);
+  if (li >= nsp) return;  // whole workgroup: padding of the grid
+  const int s = NS - 1 - li / BH, bh = li % BH;
+  const int sp = bh * NS + s;  // span record index (head-major)
   const long long span0 = static_cast<long long>(s) * L;
   const long long span_end = min(static_cast<long long>(T), span0 + L);
   const long long wg_q0 = span0 + static_cast<long long>(qb) * kQB8;
@@ -1389,35 +1398,48 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
       qf[i][kz] = *reinterpret_cast<const bf16x8*>(qh + t * D + DM * (kz / KZM) +
                                                    8 * (kz % KZM) + RM * g);
   }
+  // The first span of a head has a zero prefix: its workgroups read no
+  // prefix record and skip the readout (wave-uniform).
+  const bool pfx = s > 0;
   // Z_pre operand fragments of each feature block
   bf16x8 zA[NG][G::ZMB][KZM];
+  if (pfx) {
 #pragma unroll
-  for (int bb = 0; bb < NG; ++bb)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-    for (int m = 0; m < G::ZMB; ++m)
+      for (int m = 0; m < G::ZMB; ++m)
 #pragma unroll
-      for (int kz = 0; kz < KZM; ++kz)
-        zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(
-            rec + G::ES + static_cast<long long>(bb) * DM * DM + ((m * KZM + kz) * 64 + lane) * 8);
+        for (int kz = 0; kz < KZM; ++kz)
+          zA[bb][m][kz] = *reinterpret_cast<const bf16x8*>(
+              rec + G::ES + static_cast<long long>(bb) * DM * DM + ((m * KZM + kz) * 64 + lane) * 8);
+  }
 #pragma unroll
   for (int i = 0; i < NQ; ++i)
 #pragma unroll
     for (int kz = 0; kz < KZ; ++kz) asm volatile("" ::"v"(qf[i][kz]));
+  if (pfx) {
 #pragma unroll
-  for (int bb = 0; bb < NG; ++bb)
+    for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
-    for (int m = 0; m < G::ZMB; ++m)
+      for (int m = 0; m < G::ZMB; ++m)
 #pragma unroll
-      for (int kz = 0; kz < KZM; ++kz) asm volatile("" ::"v"(zA[bb][m][kz]));
+        for (int kz = 0; kz < KZM; ++kz) asm volatile("" ::"v"(zA[bb][m][kz]));
+  }
   if (nstage > 1) issue_i(1, g_stage1);
-  issue_r(std::integral_constant<int, 0>{});
-  if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+  if (pfx) {
+    issue_r(std::integral_constant<int, 0>{});
+    if constexpr (NSTAGE_R > 1) issue_r(std::integral_constant<int, 1>{});
+  }
 
   // ---- denominator from the prefix: sum over blocks of q_bb^T Z_bb q_bb ------
   float dpart[NQ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     float dsum = 0.f;
+    if (!pfx) {
+      dpart[i] = 0.f;
+      continue;
+    }
 #pragma unroll
     for (int bb = 0; bb < NG; ++bb)
 #pragma unroll
@@ -1566,72 +1588,75 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   // ahead: stages 0 and 1 came with the prologue, 2 to 4 go now (into the
   // in-span buffers), and stage s + 4 is issued once every wave is done with
   // stage s - 1, whose buffer it takes.
-  static_for<2, (NSTAGE_R < 5 ? NSTAGE_R : 5)>([&](auto stg_c) { issue_r(stg_c); });
+  if (pfx) static_for<2, (NSTAGE_R < 5 ? NSTAGE_R : 5)>([&](auto stg_c) { issue_r(stg_c); });
 
-  // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
-  // rotated fp32 query rows per feature block:
-  // qr[i][DM bb + x] = q[t][DM bb + (x + RM g) % DM]; the lane's own
-  // fragments of block bb hold x < RM, the lane 32 away holds the rest
-  float qr[NQ][D];
+  if (pfx) {  // the first span's prefix is zero: no readout
+    // ---- readout of the span prefix: Phi_w(Q) S_pre ----------------------------
+    // rotated fp32 query rows per feature block:
+    // qr[i][DM bb + x] = q[t][DM bb + (x + RM g) % DM]; the lane's own
+    // fragments of block bb hold x < RM, the lane 32 away holds the rest
+    float qr[NQ][D];
 #pragma unroll
-  for (int i = 0; i < NQ; ++i)
+    for (int i = 0; i < NQ; ++i)
 #pragma unroll
-    for (int kz = 0; kz < KZ; ++kz) {
-      const int base = DM * (kz / KZM) + 8 * (kz % KZM);
-      const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
-      const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+      for (int kz = 0; kz < KZ; ++kz) {
+        const int base = DM * (kz / KZM) + 8 * (kz % KZM);
+        const uint4 w4 = __builtin_bit_cast(uint4, qf[i][kz]);
+        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
-        qr[i][base + 2 * e] = bf16lo_f32(w[e]);
-        qr[i][base + 2 * e + 1] = bf16hi_f32(w[e]);
-        qr[i][base + RM + 2 * e] = bf16lo_f32(pw);
-        qr[i][base + RM + 2 * e + 1] = bf16hi_f32(pw);
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t pw = static_cast<uint32_t>(__shfl_xor(static_cast<int>(w[e]), 32));
+          qr[i][base + 2 * e] = bf16lo_f32(w[e]);
+          qr[i][base + 2 * e + 1] = bf16hi_f32(w[e]);
+          qr[i][base + RM + 2 * e] = bf16lo_f32(pw);
+          qr[i][base + RM + 2 * e + 1] = bf16hi_f32(pw);
+        }
       }
-    }
-  // A fragment of K-step kk: row c (and c + 32), chunk (2 (kk % 8) + g) ^ (c % 16)
-  // of the 32 in the row, plus 256 bytes for kk >= 8; formed per K-step (a
-  // XOR and an add) rather than held in eight registers
-  const unsigned arow = static_cast<unsigned>(c * SCH * 16);
-  const unsigned asw = static_cast<unsigned>(g ^ rswz(c));
-  const bool any_live = tlive[0] || tlive[1];
-  static_for<0, NSTAGE_R>([&](auto stg_c) {
-    constexpr int stg = decltype(stg_c)::value;
-    constexpr int k0 = stg * kKC;
-    constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
-    if constexpr (stg >= 2) {
-      // stages stg + 1 .. min(stg + 3, last) may stay in flight
-      constexpr int later = (NSTAGE_R - 1 - stg < 3) ? NSTAGE_R - 1 - stg : 3;
-      wait_vmcnt<IPW_R * later>();
-    }
-    if constexpr (stg >= 1) lds_barrier();  // stage stg landed; stage stg - 1 consumed
-    if constexpr (stg >= 1 && stg + 4 < NSTAGE_R) issue_r(std::integral_constant<int, stg + 4>{});
-    if (!any_live) return;  // wave-uniform: dead tiles only take part in the staging
-    const char* Sb = reinterpret_cast<const char*>(stage_buf((3 + stg) % 5));
-    static_for<0, kc>([&](auto kk_c) {
-      constexpr int kk = decltype(kk_c)::value;
-      constexpr int kap = k0 + kk;
-      // K-step kl of feature block bb: slots 16 kl + 8 g + j pair registers
-      // r1 + j and r1 + j + dl of the block's rotated row
-      constexpr int bb = kap / G::NKSM, kl = kap % G::NKSM;
-      constexpr int r1 = (8 * kl) % RM, dl = (8 * kl) / RM;
-      const char* ap = Sb + arow + ((static_cast<unsigned>(2 * (kk & 7)) ^ asw) << 4) + (kk >> 3) * 256;
-      const bf16x8 A0 = *reinterpret_cast<const bf16x8*>(ap);
-      const bf16x8 A1 = *reinterpret_cast<const bf16x8*>(ap + 32 * SCH * 16);
-#pragma unroll
-      for (int i = 0; i < NQ; ++i) {
-        float pr[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          pr[j] = qr[i][DM * bb + r1 + j] * qr[i][DM * bb + (r1 + j + dl) % DM];
-        const bf16x8 bq = __builtin_bit_cast(
-            bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
-                               pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
-        acc[0][i] = mfma32(A0, bq, acc[0][i]);
-        acc[1][i] = mfma32(A1, bq, acc[1][i]);
+    // A fragment of K-step kk: row c (and c + 32), chunk (2 (kk % 8) + g) ^ (c % 16)
+    // of the 32 in the row, plus 256 bytes for kk >= 8; formed per K-step (a
+    // XOR and an add) rather than held in eight registers
+    const unsigned arow = static_cast<unsigned>(c * SCH * 16);
+    const unsigned asw = static_cast<unsigned>(g ^ rswz(c));
+    const bool any_live = tlive[0] || tlive[1];
+    static_for<0, NSTAGE_R>([&](auto stg_c) {
+      constexpr int stg = decltype(stg_c)::value;
+      constexpr int k0 = stg * kKC;
+      constexpr int kc = (G::NKS - k0 < kKC) ? (G::NKS - k0) : kKC;
+      if constexpr (stg >= 2) {
+        // stages stg + 1 .. min(stg + 3, last) may stay in flight
+        constexpr int later = (NSTAGE_R - 1 - stg < 3) ? NSTAGE_R - 1 - stg : 3;
+        wait_vmcnt<IPW_R * later>();
       }
+      if constexpr (stg >= 1) lds_barrier();  // stage stg landed; stage stg - 1 consumed
+      if constexpr (stg >= 1 && stg + 4 < NSTAGE_R) issue_r(std::integral_constant<int, stg + 4>{});
+      if (!any_live) return;  // wave-uniform: dead tiles only take part in the staging
+      const char* Sb = reinterpret_cast<const char*>(stage_buf((3 + stg) % 5));
+      static_for<0, kc>([&](auto kk_c) {
+        constexpr int kk = decltype(kk_c)::value;
+        constexpr int kap = k0 + kk;
+        // K-step kl of feature block bb: slots 16 kl + 8 g + j pair registers
+        // r1 + j and r1 + j + dl of the block's rotated row
+        constexpr int bb = kap / G::NKSM, kl = kap % G::NKSM;
+        constexpr int r1 = (8 * kl) % RM, dl = (8 * kl) / RM;
+        const char* ap = Sb + arow + ((static_cast<unsigned>(2 * (kk & 7)) ^ asw) << 4) + (kk >> 3) * 256;
+        const bf16x8 A0 = *reinterpret_cast<const bf16x8*>(ap);
+        const bf16x8 A1 = *reinterpret_cast<const bf16x8*>(ap + 32 * SCH * 16);
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) {
+          float pr[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            pr[j] = qr[i][DM * bb + r1 + j] * qr[i][DM * bb + (r1 + j + dl) % DM];
+          const bf16x8 bq = __builtin_bit_cast(
+              bf16x8, make_uint4(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]),
+                                 pack_bf16x2(pr[4], pr[5]), pack_bf16x2(pr[6], pr[7])));
+          acc[0][i] = mfma32(A0, bq, acc[0][i]);
+          acc[1][i] = mfma32(A1, bq, acc[1][i]);
+        }
+      });
     });
-  });
+
+  }
 
   // ---- normalise and store ---------------------------------------------------
   // A tile's accumulators hold 4 consecutive dv columns of one query per
@@ -1675,32 +1700,36 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// V^T of a whole head for the quadratic form: vtp[bh][dv][LV] bf16, keys of
-// every 16-key group in the order 0-3, 8-11, 4-7, 12-15 (the key order of the
-// output kernel's P V product, as the state kernel writes it per span), keys
-// at or past T zero.  A workgroup transposes 64 keys through LDS.
+// V^T of the keys key_base .. key_base + LV - 1 of every head, into
+// vtp + bh out_bh + out0 as [dv][LV] bf16, keys of every 16-key group in the
+// order 0-3, 8-11, 4-7, 12-15 (the key order of the output kernel's P V
+// product, as the state kernel writes it per span), keys at or past T zero:
+// a whole head for the quadratic form, or the last span of every head (whose
+// state the state kernel skips).  A workgroup transposes 64 keys through LDS.
 // grid (LV / 64, BH), block 256.
 // ---------------------------------------------------------------------------
 template <int DV>
 __global__ __launch_bounds__(256) void vt_permute_kernel(const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ vtp, int T,
-                                                         int LV) {
+                                                         int LV, int key_base,
+                                                         long long out_bh, long long out0) {
   constexpr int KEYS = 64, CH = DV / 8;  // keys per workgroup, 16-byte chunks per V row
   __shared__ uint32_t tile[KEYS][DV / 2 + 1];  // [key][dv pair], one word of padding
   const int bh = blockIdx.y;
   const long long key0 = static_cast<long long>(blockIdx.x) * KEYS;
-  const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
+  const uint16_t* vh = v + (static_cast<long long>(bh) * T + key_base) * DV;
+  const long long nkeys = static_cast<long long>(T) - key_base;
   for (int i = threadIdx.x; i < KEYS * CH; i += 256) {
     const int key = i / CH, ch = i % CH;
     uint4 x = make_uint4(0u, 0u, 0u, 0u);
-    if (key0 + key < T) x = *reinterpret_cast<const uint4*>(vh + (key0 + key) * DV + 8 * ch);
+    if (key0 + key < nkeys) x = *reinterpret_cast<const uint4*>(vh + (key0 + key) * DV + 8 * ch);
     tile[key][4 * ch + 0] = x.x;
     tile[key][4 * ch + 1] = x.y;
     tile[key][4 * ch + 2] = x.z;
     tile[key][4 * ch + 3] = x.w;
   }
   __syncthreads();
-  uint16_t* out = vtp + static_cast<long long>(bh) * DV * LV;
+  uint16_t* out = vtp + bh * out_bh + out0;
   for (int i = threadIdx.x; i < DV * (KEYS / 8); i += 256) {
     const int m = i / (KEYS / 8), h = i % (KEYS / 8);  // dv row, output chunk of 8 keys
     const int base = 16 * (h >> 1) + 4 * (h & 1);        // keys base+0..3, base+8..11
@@ -1762,23 +1791,33 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   const int nsp = BH * NS;
   hipError_t e = record(ev, 0, st);
   if (e != hipSuccess) return e;
-  // K2 in launches of at most kSpansPerLaunch spans (1-D grid size limit)
-  for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
-    const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
+  // K2 over the BH (NS - 1) spans that enter a prefix, in launches of at most
+  // kSpansPerLaunch spans (1-D grid size limit); none when every head is one
+  // span
+  const int nst = BH * (NS - 1);
+  for (int sp0 = 0; sp0 < nst; sp0 += kSpansPerLaunch) {
+    const int cnt = nst - sp0 < kSpansPerLaunch ? nst - sp0 : kSpansPerLaunch;
     const unsigned nb2 = 8u * StateGrid<D, DV, NG>::NB * static_cast<unsigned>((cnt + 7) / 8);
-    span_state_kernel<D, DV, NG><<<nb2, 64 * StateGrid<D, DV, NG>::NW, 0, st>>>(kk, vv, spanst, vtp, T, L, LA, NS, sp0,
-                                                      sp0 + cnt);
+    span_state_kernel<D, DV, NG><<<nb2, 64 * StateGrid<D, DV, NG>::NW, 0, st>>>(
+        kk, vv, spanst, vtp, T, L, LA, NS, BH, sp0, sp0 + cnt);
   }
+  // the last span of every head: V^T only (its state enters no prefix)
+  vt_permute_kernel<DV><<<dim3(static_cast<unsigned>(LA / 64), static_cast<unsigned>(BH)), 256, 0,
+                          st>>>(vv, vtp, T, LA, (NS - 1) * L,
+                                static_cast<long long>(NS) * DV * LA,
+                                static_cast<long long>(NS - 1) * DV * LA);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
-  launch_scan_exclusive_bf16(spanst, NS, G::E, static_cast<long long>(NS) * G::E, BH,
-                             SlotWeight<D, DV, NG>{}, st);
+  // one span per head: its prefix is zero and the output kernel reads none
+  if (NS > 1)
+    launch_scan_exclusive_bf16(spanst, NS, G::E, static_cast<long long>(NS) * G::E, BH,
+                               SlotWeight<D, DV, NG>{}, st);
   if ((e = record(ev, 2, st)) != hipSuccess) return e;
   const int qb8 = (L + kQB8 - 1) / kQB8;
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
     span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
-                                                        qb8, sp0, sp0 + cnt);
+                                                        BH, qb8, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
@@ -1797,7 +1836,8 @@ static hipError_t run_quadratic(const void* q, const void* k, const void* v, flo
   static_assert(kKB % 64 == 0, "the transpose writes whole 64-key groups");
   uint16_t* vtp = static_cast<uint16_t*>(ws);
   vt_permute_kernel<DV><<<dim3(static_cast<unsigned>(LA / 64), static_cast<unsigned>(BH)), 256, 0,
-                          st>>>(static_cast<const uint16_t*>(v), vtp, T, LA);
+                          st>>>(static_cast<const uint16_t*>(v), vtp, T, LA, 0,
+                                static_cast<long long>(DV) * LA, 0LL);
   const int qblocks = (T + OutGrid<D, DV>::QB_TOKENS - 1) / OutGrid<D, DV>::QB_TOKENS;
   // 8 * qblocks * ceil(cnt / 8) workgroups per launch, below 2^31
   int per = static_cast<int>((0x7fffffffLL / (8LL * qblocks)) * 8);
