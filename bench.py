@@ -97,16 +97,22 @@ def algorithmic(w, L, g=1):
                      output  2*n*dv + 2*n + (C+1)*(d+dv)
                              (phi(q)^T S and phi(q)^T z readouts, causal
                               intra-chunk QK^T and PV at chunk size C)
+    The state term counts every key but those of the last chunk (its state
+    enters no exclusive prefix) and the readout term every query but those of
+    the first chunk (its prefix is zero).
     scan: one bf16 read of every span state but the last (n*(dv+1) values;
           the last span's state enters no exclusive prefix) and one bf16
           write of every span's exclusive prefix, per head.
     """
     m = w.d // g
     n = g * (m * (m + 1) // 2)
-    ht = w.B * w.H * w.T
+    bh = w.B * w.H
+    ht = bh * w.T
     NS = (w.T + L - 1) // L
-    state = (2 * n * w.dv + n) * ht
-    output = (2 * n * w.dv + 2 * n + (w.C + 1) * (w.d + w.dv)) * ht
+    NC = (w.T + w.C - 1) // w.C
+    state = (2 * n * w.dv + n) * bh * (NC - 1) * w.C
+    output = ((2 * n * w.dv + 2 * n) * bh * (w.T - min(w.C, w.T))
+              + (w.C + 1) * (w.d + w.dv) * ht)
     scan_bytes = (2 * NS - 1) * w.B * w.H * n * (w.dv + 1) * 2
     return dict(n=n, state_flop=state, output_flop=output, scan_bytes=scan_bytes,
                 total_flop=state + output)
