@@ -244,9 +244,6 @@ __device__ __forceinline__ int rswz(int m) { return m & 15; }  // rows of >= 16 
 // Features are rounded once, to fp16 (unit roundoff 2^-11, finer than a bf16
 // rounding); the records are written in bf16 as before.
 //
-// The workgroup with part 0 also writes the span's V^T (bf16, [dv][LV], keys
-// of every 16-key group in the order 0-3, 8-11, 4-7, 12-15: the K order of
-// the output kernel's P V product) straight from its staging registers.
 // Writes the span record (bf16): S^T as [dv][NSLOT], then Z in operand order.
 // ---------------------------------------------------------------------------
 constexpr int kTB2 = 128;           // tokens per staged block
@@ -294,8 +291,7 @@ template <int D, int DV, int NG>
 __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_kernel(const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v,
                                                          uint16_t* __restrict__ spanst,
-                                                         uint16_t* __restrict__ vtp, int T,
-                                                         int L, int LV, int NS, int BH,
+                                                         int T, int L, int NS, int BH,
                                                          int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   using SG = StateGrid<D, DV, NG>;
@@ -341,7 +337,6 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
   const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
   uint16_t* rec = spanst + static_cast<long long>(sp) * G::E;
-  uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
   const int nblk = static_cast<int>((span_end - span0 + kTB2 - 1) / kTB2);
 
   // staging: task -> (pair p of tokens, 8-wide column group cg); K then V
@@ -373,10 +368,8 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
     }
   };
   // Commit: write the fetched pairs into LDS as fp16 (times the span's scale
-  // when SC), and (vt) the bf16 V^T pairs of block bi into the span's V^T.
-  // Token pair (2p, 2p+1) of a 16-key group sits at position
-  // 16 (p / 8) + 8 ((p / 2) % 2) + 4 (p / 4 % 2) + 2 (p % 2) of the V^T row.
-  auto commit = [&](auto sc_c, int buf, long long t0, float sk, float sv, bool vt, int bi,
+  // when SC).
+  auto commit = [&](auto sc_c, int buf, long long t0, float sk, float sv,
                     auto i0_c, auto i1_c) __attribute__((always_inline)) {
     constexpr bool SC = decltype(sc_c)::value;
 #pragma unroll
@@ -414,19 +407,6 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
             __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(xl, yl));
         *reinterpret_cast<uint32_t*>(base + (2 * e + 1) * kRow2) =
             __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(xh, yh));
-      }
-      if (vt && cg >= KG) {
-        const uint32_t sel_e = (va ? 0x0100u : 0x0c0cu) | (vb ? 0x05040000u : 0x0c0c0000u);
-        const uint32_t sel_o = (va ? 0x0302u : 0x0c0cu) | (vb ? 0x07060000u : 0x0c0c0000u);
-        const int pos = 16 * (p >> 3) + 8 * ((p >> 1) & 1) + 4 * ((p >> 2) & 1) + 2 * (p & 1);
-        uint16_t* dst = vt_rec + static_cast<long long>(8 * (cg - KG)) * LV + kTB2 * bi + pos;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          *reinterpret_cast<uint32_t*>(dst + static_cast<long long>(2 * e) * LV) =
-              __builtin_amdgcn_perm(b[e], a[e], sel_e);
-          *reinterpret_cast<uint32_t*>(dst + static_cast<long long>(2 * e + 1) * LV) =
-              __builtin_amdgcn_perm(b[e], a[e], sel_o);
-        }
       }
     }
   };
@@ -500,12 +480,12 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
   // (straight-line code, at most one unscaled and one scaled pass: a loop
   // around the passes would keep every register of a pass live across it)
   float fin = 0.f;  // sum of the written state: non-finite iff some value is
-  auto run = [&](auto sc_c, bool vt) __attribute__((always_inline)) {
+  auto run = [&](auto sc_c) __attribute__((always_inline)) {
       constexpr bool SC = decltype(sc_c)::value;
       // scales: 2^-e maps the largest |k| (|v|) of the span into [1, 2)
       const int xk = SC ? max(ek, 1) - 127 : 0, xv = SC ? max(ev, 1) - 127 : 0;
       const float sk = ldexpf(1.f, -xk), sv = ldexpf(1.f, -xv);
-      commit(sc_c, 0, span0, sk, sv, vt, 0, I0{}, IT{});
+      commit(sc_c, 0, span0, sk, sv, I0{}, IT{});
       fetch(span0 + kTB2, I0{}, IT{});
       lds_barrier();
 
@@ -528,7 +508,7 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
           const int buf = bi % kNBuf2;
           if (bi + 1 < nblk)
             commit(sc_c, (bi + 1) % kNBuf2, span0 + static_cast<long long>(bi + 1) * kTB2, sk,
-                   sv, vt, bi + 1, I0{}, IT{});
+                   sv, I0{}, IT{});
           fetch(span0 + static_cast<long long>(bi + 2) * kTB2, I0{}, IT{});
           if (zwave) {
 #pragma unroll
@@ -670,7 +650,7 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
             if constexpr (j * KS / TPT == ks) {
               using J = std::integral_constant<int, j>;
               using J1 = std::integral_constant<int, j + 1>;
-              if (more1) commit(sc_c, nbuf, t1, sk, sv, vt, bi + 1, J{}, J1{});
+              if (more1) commit(sc_c, nbuf, t1, sk, sv, J{}, J1{});
               fetch(t2, J{}, J1{});
             }
           });
@@ -758,7 +738,7 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
       });
   };
   if (!scaled) {
-    run(No{}, part == 0);
+    run(No{});
     // A non-finite state from finite inputs means an fp16 overflow in the
     // unscaled pass: run the span again with its scales.
     if (!nonfinite_in) {
@@ -769,11 +749,11 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
       if (red[2] != 0u) {
         scaled = true;
         span_scales();
-        run(Yes{}, false);
+        run(Yes{});
       }
     }
   } else {
-    run(Yes{}, part == 0);
+    run(Yes{});
   }
 }
 
@@ -790,8 +770,8 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
 // LDS fragment reads use per-lane offsets computed once, so every read is a
 // base register plus an immediate.
 // pre[bh][s][E] bf16 (K4): weighted S_pre^T as [dv][NSLOT], then Z_pre
-// (operand order).  vtp[bh][s][dv][L] bf16: the span's V^T (permuted keys,
-// see K2).
+// (operand order).  K4 stages K and V rows as they are in HBM; the quadratic
+// form reads vtp[bh][dv][LA] bf16, a permuted V^T (vt_permute_kernel).
 // ---------------------------------------------------------------------------
 constexpr int kKB = 128;        // keys per intra stage (four 32-key blocks)
 constexpr int kKC = 16;         // readout K-steps per stage
@@ -809,6 +789,16 @@ __shared__ __attribute__((aligned(16))) uint16_t g_stage4[kStageBytes / 2];
 __device__ __forceinline__ uint16_t* stage_buf(int j) {
   return j == 0 ? g_stage0
                 : (j == 1 ? g_stage1 : (j == 2 ? g_stage2 : (j == 3 ? g_stage3 : g_stage4)));
+}
+
+// Transposing LDS read of 16-bit elements (gfx950 ds_read_b64_tr_b16): in each
+// group of 16 lanes, lane j receives in slot s = 0..3 element j % 4 of the
+// 8-byte piece addressed by lane 4 s + j / 4 of its group.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_tr16(const void* p) {
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(const_cast<void*>(p)));
+  return __builtin_bit_cast(uint2, r);
 }
 
 
@@ -1267,7 +1257,9 @@ __global__ __launch_bounds__(256) void quadratic_kernel(
 // VALU issues at about half the rate and largely adds to the MFMA time.
 // Twice the queries per workgroup halve the prefix-record bytes streamed
 // into LDS per query (the readout's dominant copy traffic) and the in-span
-// K / V^T copies; every LDS fragment feeds two tiles.  A wave skips the MFMAs
+// K / V copies; every LDS fragment feeds two tiles.  V rows are staged as they
+// are in HBM and turned into V^T operands by transposing LDS reads, so no
+// transposed copy of V goes through HBM.  A wave skips the MFMAs
 // of key blocks past a tile's diagonal (it still takes part in every stage
 // barrier and copy).  MFMAs are compiler builtins (the compiler inserts the
 // wait states).  Grid: 8 * ceil(L / 512) * ceil(spans / 8) workgroups, one
@@ -1278,16 +1270,16 @@ constexpr int kQB8 = 512;  // queries per workgroup of the eight-wave form
 template <int D, int DV, int NG>
 __global__ __launch_bounds__(512) void span_output8_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    const uint16_t* __restrict__ pre, const uint16_t* __restrict__ vtp, float* __restrict__ out,
-    int T, int L, int LV, int NS, int BH, int QB, int sp0, int nsp) {
+    const uint16_t* __restrict__ v, const uint16_t* __restrict__ pre, float* __restrict__ out,
+    int T, int L, int NS, int BH, int QB, int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   static_assert(DV == 64, "the eight-wave form covers dv = 64");
   constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM, KZ = G::KZ;
   constexpr int W = 8, NQ = 2, NT = kQB8 / 32;
   constexpr int KCH = D / 8;                    // 16-byte chunks per key row
   constexpr int KCHUNKS = kKB * KCH;            // K rows of one intra stage
-  constexpr int VCH = kKB / 8;                  // chunks per V^T row of one stage (16)
-  constexpr int VCHUNKS = DV * VCH;
+  constexpr int VRCH = DV / 8;                  // 16-byte chunks per V row (8)
+  constexpr int VCHUNKS = kKB * VRCH;           // V rows of one intra stage
   constexpr int ICH = KCHUNKS + VCHUNKS;        // chunks per intra stage
   static_assert(ICH * 16 <= kStageBytes && KCHUNKS % (64 * W) == 0 && VCHUNKS % (64 * W) == 0,
                 "intra stage size");
@@ -1320,8 +1312,8 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   if (wg_q0 >= span_end) return;  // whole workgroup beyond the sequence
   const uint16_t* qh = q + static_cast<long long>(bh) * T * D;
   const uint16_t* kh = k + static_cast<long long>(bh) * T * D;
+  const uint16_t* vh = v + static_cast<long long>(bh) * T * DV;
   const uint16_t* rec = pre + static_cast<long long>(sp) * G::E;
-  const uint16_t* vt_rec = vtp + static_cast<long long>(sp) * DV * LV;
 
   int tile[NQ];
   long long tq0[NQ];
@@ -1340,14 +1332,16 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   const int nstage = (last_tile + 1 + 3) / 4;  // 128-key intra stages
   // Copy i of a lane writes LDS chunk P = 512 i + 64 wave + lane.  K rows are
   // KCH chunks long and their copies are formed per copy (one or two per
-  // stage).  For V^T and S^T the source row grows by a constant with i and the
-  // XOR swizzle of the lane's chunk does not depend on i (rswz uses the row's
-  // low four bits), so one offset per operand serves all of a lane's copies:
-  //   V^T  row 32 i' + 4 wave + lane / 16, chunk lane % 16 (i' = i - IPW_K)
+  // stage).  For V and S^T the source row grows by a constant with i and the
+  // XOR swizzle of the lane's chunk does not depend on i, so one offset per
+  // operand serves all of a lane's copies:
+  //   V    row 64 i' + 8 wave + lane / 8,  chunk (lane % 8) ^ vswz (i' = i - IPW_K)
   //   S^T  row 16 i + 2 wave + lane / 32,  chunk lane % 32
-  static_assert(VCH == 16 && SCH == 32 && W == 8 && KCHUNKS % 512 == 0, "copy geometry");
-  const int vrow0 = 4 * wave + (lane >> 4);
-  const int vsrc0 = vrow0 * LV + 8 * ((lane & 15) ^ rswz(vrow0));
+  // V rows are stored as they are in HBM, 128 bytes each, with chunk c of key
+  // row r at chunk c ^ 4 ((r >> 1) & 1); bit 1 of the row is bit 4 of the lane.
+  static_assert(VRCH == 8 && SCH == 32 && W == 8 && KCHUNKS % 512 == 0, "copy geometry");
+  const int vrow0 = 8 * wave + (lane >> 3);
+  const int vsrc0 = vrow0 * DV + 8 * ((lane & 7) ^ (4 * ((lane >> 4) & 1)));
   const int rrow0 = 2 * wave + g;
   const int rcl = c ^ rswz(rrow0);  // the chunk a lane copies of its S^T row
   const int rsrc0 = rrow0 * G::NSLOT + 8 * rcl;
@@ -1363,7 +1357,10 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
         const long long over = key0 + r - (T - 1);
         src = kh + (key0 + r) * D + 8 * (pos ^ kswz<D>(r)) - (over > 0 ? over * D : 0);
       } else {
-        src = vt_rec + st * kKB + vsrc0 + 32 * (i - IPW_K) * LV;
+        // keys past the sequence: re-read the last row (their weights are zero)
+        const int r = 64 * (i - IPW_K) + vrow0;
+        const long long over = key0 + r - (T - 1);
+        src = vh + key0 * DV + vsrc0 + 64 * (i - IPW_K) * DV - (over > 0 ? over * DV : 0);
       }
       g2lds16(src, buf + (i * W + wave) * 512);
     }
@@ -1486,13 +1483,23 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
         const int chunk = (DM / 8) * (kz / KZM) + (kz % KZM) + (RM / 8) * g;
         kfo[h][kz] = static_cast<unsigned>((krow * KCH + (chunk ^ kswz<D>(krow))) * 16);
       }
-    unsigned vfo[4][2];
+    // V^T fragments come from transposing reads of the V rows
+    // (ds_read_b64_tr_b16: lane j of a 16-lane group receives, in slot s,
+    // 16-bit element j % 4 of the 8-byte piece that lane 4 s + j / 4 of the
+    // group addresses).  Lane j of group G addresses key row 4 g + j / 4 of a
+    // 16-key half (plus 8 for the second read) and the piece holding dv
+    // 32 m + 16 (G % 2) + 4 (j % 4) .. + 3, so it receives dv 32 m + 16 (G % 2) + j
+    // of keys 4 g + 0..3 and 8 + 4 g + 0..3: the A operand in the key order of
+    // the score fragments (rows 8 (r / 4) + 4 g + r % 4).  The four rows a group
+    // reads fall in distinct banks under the chunk swizzle.
+    const int jl = lane & 15;
+    unsigned vfo[2];
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb)
-#pragma unroll
-      for (int kv = 0; kv < 2; ++kv)
-        vfo[sb][kv] = static_cast<unsigned>(
-            (KCHUNKS + c * VCH + ((4 * sb + 2 * kv + g) ^ rswz(c))) * 16);
+    for (int m = 0; m < 2; ++m) {
+      const int ch = 4 * m + 2 * ((lane >> 4) & 1) + ((jl & 3) >> 1);
+      vfo[m] = static_cast<unsigned>(KCHUNKS * 16 + (4 * g + (jl >> 2)) * (VRCH * 16) +
+                                     16 * (ch ^ (4 * ((jl >> 3) & 1))) + 8 * (jl & 1));
+    }
     int tdiag[NQ];  // a tile's diagonal block, -1 for a tile beyond the sequence
 #pragma unroll
     for (int i = 0; i < NQ; ++i) tdiag[i] = __builtin_amdgcn_readfirstlane(tlive[i] ? tile[i] : -1);
@@ -1510,8 +1517,11 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 #pragma unroll
       for (int m = 0; m < 2; ++m)
 #pragma unroll
-        for (int kv = 0; kv < 2; ++kv)
-          V[m][kv] = *reinterpret_cast<const bf16x8*>(buf + vfo[sb][kv] + m * (32 * VCH * 16));
+        for (int kv = 0; kv < 2; ++kv) {
+          const char* vp = buf + vfo[m] + (32 * sb + 16 * kv) * (VRCH * 16);
+          const uint2 lo = lds_tr16(vp), hi = lds_tr16(vp + 8 * (VRCH * 16));
+          V[m][kv] = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        }
 #pragma unroll
       for (int i = 0; i < NQ; ++i) {
         if (kb > tdiag[i]) continue;  // wave-uniform
@@ -1702,10 +1712,9 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
 // ---------------------------------------------------------------------------
 // V^T of the keys key_base .. key_base + LV - 1 of every head, into
 // vtp + bh out_bh + out0 as [dv][LV] bf16, keys of every 16-key group in the
-// order 0-3, 8-11, 4-7, 12-15 (the key order of the output kernel's P V
-// product, as the state kernel writes it per span), keys at or past T zero:
-// a whole head for the quadratic form, or the last span of every head (whose
-// state the state kernel skips).  A workgroup transposes 64 keys through LDS.
+// order 0-3, 8-11, 4-7, 12-15 (the key order of the quadratic kernel's P V
+// product), keys at or past T zero: the whole head for the quadratic form.
+// A workgroup transposes 64 keys through LDS.
 // grid (LV / 64, BH), block 256.
 // ---------------------------------------------------------------------------
 template <int DV>
@@ -1761,18 +1770,16 @@ static long long mfma_record(int d, int g) {
 
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-// Span length rounded up to whole intra stages so that every staged key
-// block lies inside the span's V^T record.
+// Sequence length rounded up to whole intra stages so that every staged key
+// block of the quadratic form lies inside its V^T copy.
 static int span_alloc(int L) { return (L + kKB - 1) / kKB * kKB; }
-static_assert(kKB % kTB2 == 0, "the state kernel writes V^T in whole staged blocks");
 
 constexpr int kSpansPerLaunch = 1 << 20;
 
-size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L, int g) {
+size_t mfma_forward_workspace(int BH, int T, int d, int /*dv*/, int L, int g) {
   const size_t NS = (static_cast<size_t>(T) + L - 1) / L;
   const size_t recs = static_cast<size_t>(BH) * NS * static_cast<size_t>(mfma_record(d, g));
-  const size_t vt = static_cast<size_t>(BH) * NS * dv * span_alloc(L);
-  return align256(recs * sizeof(uint16_t)) + align256(vt * sizeof(uint16_t));
+  return align256(recs * sizeof(uint16_t));
 }
 
 template <int D, int DV, int NG>
@@ -1780,11 +1787,7 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
                            int L, void* ws, hipStream_t st, hipEvent_t* ev) {
   using G = GeoG<D, DV, NG>;
   const int NS = (T + L - 1) / L;
-  const int LA = span_alloc(L);
-  const size_t recs = static_cast<size_t>(BH) * NS * G::E;
   uint16_t* spanst = static_cast<uint16_t*>(ws);
-  uint16_t* vtp =
-      reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + align256(recs * sizeof(uint16_t)));
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
@@ -1799,13 +1802,8 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
     const int cnt = nst - sp0 < kSpansPerLaunch ? nst - sp0 : kSpansPerLaunch;
     const unsigned nb2 = 8u * StateGrid<D, DV, NG>::NB * static_cast<unsigned>((cnt + 7) / 8);
     span_state_kernel<D, DV, NG><<<nb2, 64 * StateGrid<D, DV, NG>::NW, 0, st>>>(
-        kk, vv, spanst, vtp, T, L, LA, NS, BH, sp0, sp0 + cnt);
+        kk, vv, spanst, T, L, NS, BH, sp0, sp0 + cnt);
   }
-  // the last span of every head: V^T only (its state enters no prefix)
-  vt_permute_kernel<DV><<<dim3(static_cast<unsigned>(LA / 64), static_cast<unsigned>(BH)), 256, 0,
-                          st>>>(vv, vtp, T, LA, (NS - 1) * L,
-                                static_cast<long long>(NS) * DV * LA,
-                                static_cast<long long>(NS - 1) * DV * LA);
   if ((e = record(ev, 1, st)) != hipSuccess) return e;
   // one span per head: its prefix is zero and the output kernel reads none
   if (NS > 1)
@@ -1816,8 +1814,8 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, spanst, vtp, out, T, L, LA, NS,
-                                                        BH, qb8, sp0, sp0 + cnt);
+    span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, vv, spanst, out, T, L, NS, BH,
+                                                        qb8, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
