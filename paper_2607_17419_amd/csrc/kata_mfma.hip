@@ -10,12 +10,13 @@
 //
 //   K2  span_state : S_span = Phi(K)^T V and Z_span = K^T K, MFMA over the span,
 //                    Phi(K) generated on chip (never written to HBM); writes the
-//                    span record in bf16 and the span's V^T for K4.
+//                    span record in bf16.
 //   K3  scan       : in-place exclusive Blelloch prefix over the span records
 //                    (kata_scan.hpp), fp32 sums, written back as bf16 MFMA
 //                    operands with the feature weights.
 //   K4  span_output: squared-score attention inside the span (QK^T on MFMA,
-//                    squared and masked in registers, P V back through MFMA),
+//                    squared and masked in registers, P V back through MFMA,
+//                    V^T operands by transposing LDS reads of the V rows),
 //                    plus the readout Phi_w(Q) S_pre and q^T Z_pre q, then the
 //                    normalisation O = N / D.
 //
@@ -324,8 +325,7 @@ __global__ __launch_bounds__((64 * StateGrid<D, DV, NG>::NW)) void span_state_ke
   const int jx = id >> 3;
   const int part = jx % SG::NB;
   // Work item li over the NS - 1 spans per head that enter a prefix (each
-  // head's last span is left out: vt_permute_kernel writes its V^T), head by
-  // head.  All of these spans carry the same work, so the XCD a work item
+  // head's last span is left out), head by head.  All of these spans carry the same work, so the XCD a work item
   // lands on (work item mod 8) needs no balancing.
   const int li = sp0 + 8 * (jx / SG::NB) + (id & 7);
   if (li >= nsp) return;  // whole workgroup: padding of the grid
@@ -1471,8 +1471,9 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   // S = K_kb Q_i^T (KZ MFMAs), P = S^2 (masked above the diagonal on the
   // diagonal block; the row sums go to the denominator), O_i^T += V_kb^T P
   // (four MFMAs: two dv halves x two 16-key halves; the lane's score
-  // registers are directly the P fragment in the permuted key order of V^T).
-  // The block's K and V^T fragments are read from LDS once for both tiles.
+  // registers are directly the P fragment, and the V^T fragments are read in
+  // the same permuted key order).  The block's K and V fragments are read from
+  // LDS once for both tiles.
   {
     unsigned kfo[2][KZ];
 #pragma unroll
