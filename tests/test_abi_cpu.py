@@ -83,9 +83,9 @@ def test_workspace_and_span_host_logic():
     n = 16 * 17 // 2
     assert L.kata_fwd_workspace_bytes(1, 2, 256, 16, 16, 32, 0, 0) == 2 * 8 * (n * 16 + n) * 4
     assert L.kata_fwd_default_span(1, 2, 256, 16, 16, 32, 0) == 1
-    # MFMA path: default span folds about 1024 tokens
+    # MFMA path: default span folds about 1024 tokens (512 at d = 32)
     assert L.kata_fwd_default_span(1, 16, 131072, 64, 64, 64, 1) == 16
-    assert L.kata_fwd_default_span(4, 8, 16384, 32, 64, 128, 1) == 8
+    assert L.kata_fwd_default_span(4, 8, 16384, 32, 64, 128, 1) == 4
     # MFMA path: one bf16 record (2112 slots x 64 dv + 64 x 64 Z) per span and
     # head, scanned in place (the output kernel reads V itself)
     rec = 2112 * 64 + 64 * 64
