@@ -23,6 +23,12 @@
  *    on an error nothing is launched and nothing is written.
  *  - Calls only enqueue work on `stream` and return; they never synchronise.
  *    A device fault surfaces at the caller's next synchronisation.
+ *  - The calls that take a caller workspace (the _ws and _timed variants),
+ *    kata_fwd_chunked_noalloc, kata_prefill_state and kata_decode_step
+ *    enqueue kernel launches only (and the _timed variants event records), so
+ *    a caller may capture them into a HIP graph and replay it; the variants
+ *    without a workspace argument allocate theirs stream-ordered
+ *    (hipMallocAsync / hipFreeAsync) on `stream`.
  *  - The library keeps no global mutable state (except the scratch array of
  *    kata_fwd_chunked_noalloc, see there); calls from several threads are
  *    safe.  NaN and Inf in inputs propagate; inputs are not normalised.
