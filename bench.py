@@ -60,6 +60,11 @@ class Events:
         assert self.hip.hipEventElapsedTime(ctypes.byref(ms), self.ev[i], self.ev[j]) == 0
         return ms.value
 
+    def record(self, i, stream):
+        """Record event i on `stream` (a torch stream)."""
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        assert self.hip.hipEventRecord(self.ev[i], ctypes.c_void_p(stream.cuda_stream)) == 0
+
     def block(self, i):
         """Pointer to 4 consecutive events starting at index i."""
         return ctypes.c_void_p(ctypes.addressof(self.ev) + i * ctypes.sizeof(ctypes.c_void_p))
@@ -579,12 +584,13 @@ def bwd_bytes(BH, T, d, dv, C):
 
 
 def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=2):
-    """Training step of KATA-M1 (forward on the bf16 MFMA path, then the O(T)
-    chunked backward) at the paper's training-table shape B = 8, H = 16,
-    d = dv = 64, C = 64, bf16 inputs, fp32 gradients; per-stage HIP-event
-    times of the backward, and the HBM rates of its state, scan and gradients
-    kernels against their algorithmic bytes (with the bf16 matrix rates of
-    the state and gradients kernels beside them)."""
+    """Training step of KATA-M1 (forward on the bf16 MFMA path saving the row
+    denominators D_t, then the O(T) chunked backward taking them) at the
+    paper's training-table shape B = 8, H = 16, d = dv = 64, C = 64, bf16
+    inputs, fp32 gradients; per-stage HIP-event times of the backward, and the
+    HBM rates of its state, scan and gradients kernels against their
+    algorithmic bytes (with the bf16 matrix rates of the state and gradients
+    kernels beside them)."""
     import torch
     import workloads
     B, H, d, dv, C = 8, 16, 64, 64, 64
@@ -612,22 +618,26 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
         bws = torch.empty(kata.bwd_workspace_bytes(B, H, T, d, dv, C, 1, kata.KATA_BF16),
                           dtype=torch.uint8, device=dev)
         out = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+        den = torch.empty((B, H, T), dtype=torch.float32, device=dev)
         grads = tuple(torch.empty((B, H, T, x), dtype=torch.float32, device=dev)
                       for x in (d, d, dv))
-        fev = Events(hip, 4 * max(steps, warmup))
+        fev = Events(hip, 2 * max(steps, warmup))
         bev = Events(hip, 7 * max(steps, warmup))
-        for i in range(warmup):
-            kata.fwd_chunked_timed(q, k, v, C, fev.block(4 * i), span_chunks=span, out=out,
+        stream = torch.cuda.current_stream(dev)
+
+        def train_step(i):
+            fev.record(2 * i, stream)
+            kata.fwd_chunked_train(q, k, v, C, span_chunks=span, out=out, den=den,
                                    workspace=fws)
+            fev.record(2 * i + 1, stream)
             kata.bwd_chunked(q, k, v, out, dout, C, 1, workspace=bws, events=bev.block(7 * i),
-                             grads=grads)
+                             grads=grads, den=den)
+        for i in range(warmup):
+            train_step(i)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(steps):
-            kata.fwd_chunked_timed(q, k, v, C, fev.block(4 * i), span_chunks=span, out=out,
-                                   workspace=fws)
-            kata.bwd_chunked(q, k, v, out, dout, C, 1, workspace=bws, events=bev.block(7 * i),
-                             grads=grads)
+            train_step(i)
         torch.cuda.synchronize()
         ms = 1e3 * (time.perf_counter() - t0) / steps
         names = ("fwd_states", "prefix_scan", "coefficients", "bwd_states", "suffix_scan",
@@ -640,7 +650,7 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
         if fused:
             st["fwd_states"] += st.pop("prefix_scan")
             st["bwd_states"] += st.pop("suffix_scan")
-        fwd_ms = sum(fev.elapsed(4 * i, 4 * i + 3) for i in range(steps)) / steps
+        fwd_ms = sum(fev.elapsed(2 * i, 2 * i + 1) for i in range(steps)) / steps
         fev.close()
         bev.close()
         fl = bwd_flop(B * H, T, d, dv, C)
@@ -661,7 +671,7 @@ def bench_backward(kata, dev, hip, Ts=(1024, 2048, 4096, 8192), steps=5, warmup=
         row = {"T": T, "inputs": src, "train_step_ms": round(ms, 3),
                "forward_ms": round(fwd_ms, 3), "backward_ms": round(sum(st.values()), 3),
                "tokens_per_s": B * T / (ms * 1e-3),
-               "state_and_scan_fused": fused,
+               "state_and_scan_fused": fused, "forward_saves_denominators": True,
                "backward_stages_ms": {nm: round(t, 4) for nm, t in st.items()},
                "gradients_roofline": hbm_rate(by["gradients"], st["gradients"], fl["grad"]),
                "bwd_states_roofline": hbm_rate(by["bwd_states"], st["bwd_states"], fl["state"]),

@@ -132,6 +132,22 @@ KATA_API kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, cons
                                               void* workspace, size_t workspace_bytes,
                                               hipEvent_t* stage_events, hipStream_t stream);
 
+/*
+ * kata_fwd_chunked_ws for a training step: it also writes each row's
+ * denominator D_t = sum_{i<=t} (q_t . k_i)^2 (the normaliser of eq. linatt,
+ * fp32 as the forward computed it) to den, fp32 [B][H][T], caller-owned,
+ * 16-byte aligned, for kata_bwd_chunked_ex, which then need not form it again
+ * from the prefix states.  Supported on the bf16 MFMA path (the shapes of
+ * kata_fwd_chunked_ws with dtype KATA_BF16, d in {32, 64}, dv = 64, C a
+ * multiple of 32); other valid arguments give KATA_ERR_UNSUPPORTED.  den null:
+ * KATA_ERR_INVALID_ARG.
+ */
+KATA_API kata_status_t kata_fwd_chunked_train_ws(const void* q, const void* k, const void* v,
+                                                 float* out, float* den, int B, int H, int T,
+                                                 int d, int dv, int C, kata_dtype_t dtype,
+                                                 int span_chunks, void* workspace,
+                                                 size_t workspace_bytes, hipStream_t stream);
+
 /* Workspace bytes kata_fwd_chunked_ws needs for these arguments (0 when the
  * arguments are invalid or unsupported). */
 KATA_API size_t kata_fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C,
@@ -351,6 +367,21 @@ KATA_API kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, cons
                                               int d, int dv, int C, int g, kata_dtype_t dtype,
                                               void* workspace, size_t workspace_bytes,
                                               hipEvent_t* stage_events, hipStream_t stream);
+/*
+ * kata_bwd_chunked_ws with two optional arguments: den, null or the
+ * denominators D_t that kata_fwd_chunked_train_ws wrote for this forward
+ * (fp32 [B][H][T], 16-byte aligned), from which the per-token coefficients
+ * a_t, b_t are formed directly instead of from the prefix states (same values
+ * up to rounding); stage_events, null or 7 events as for
+ * kata_bwd_chunked_timed (all non-null).  Any supported backward shape.
+ */
+KATA_API kata_status_t kata_bwd_chunked_ex(const void* q, const void* k, const void* v,
+                                           const float* out, const float* dout, const float* den,
+                                           float* dq, float* dk, float* dv_out, int B, int H,
+                                           int T, int d, int dv, int C, int g,
+                                           kata_dtype_t dtype, void* workspace,
+                                           size_t workspace_bytes, hipEvent_t* stage_events,
+                                           hipStream_t stream);
 KATA_API size_t kata_bwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int g,
                                          kata_dtype_t dtype);
 /* 1 when kata_bwd_chunked* computes the prefix and suffix records of this

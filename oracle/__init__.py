@@ -55,6 +55,7 @@ def load(path: str | None = None):
     lib.kata_oracle_packed_index.argtypes = [_L, _L, _L]
     lib.kata_oracle_phi.argtypes = [_dp, _L, ctypes.c_int, _dp]
     lib.kata_oracle_fwd.argtypes = [_dp, _dp, _dp, _dp, _L, _L, _L, _L, _L]
+    lib.kata_oracle_den.argtypes = [_dp, _dp, _dp, _L, _L, _L, _L]
     lib.kata_oracle_fwd_rows.argtypes = [_dp, _dp, _dp, _L, _L, _L, _L, _L,
                                          _lp, _lp, _L, _dp]
     lib.kata_oracle_scan_exclusive.argtypes = [_dp, _L, _L, ctypes.c_int]
@@ -132,6 +133,15 @@ class Oracle:
         out = np.empty((B, H, T, dv))
         self.lib.kata_oracle_fwd(self._p(q), self._p(k), self._p(v), self._p(out),
                                  B, H, T, d, dv)
+        return out
+
+    def den(self, q, k):
+        """Row denominators of the definition, sum_{i<=t} (q_t . k_i)^2:
+        q, k [B,H,T,d] -> [B,H,T]."""
+        q, k = self._f64(q), self._f64(k)
+        B, H, T, d = q.shape
+        out = np.empty((B, H, T))
+        self.lib.kata_oracle_den(self._p(q), self._p(k), self._p(out), B, H, T, d)
         return out
 
     def fwd_rows(self, q, k, v, bh_idx, t_idx):

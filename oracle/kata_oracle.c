@@ -984,3 +984,26 @@ EXPORT void kata_oracle_bwd_chunked_mg(const double* q, const double* k, const d
     free(fst); free(bst); free(A); free(bv); free(ph); free(pw); free(Y); free(s);
   }
 }
+
+/*
+ * Denominators of the definition: den[bh][t] = sum_{i<=t} (q_t . k_i)^2, the
+ * normaliser phi(q_t)^T sum_{i<=t} phi(k_i) of eq. linatt with the rank-one
+ * PSD feature (<phi(q), phi(k)> = (q . k)^2); [B][H][T].
+ */
+EXPORT void kata_oracle_den(const double* q, const double* k, double* den, long B, long H,
+                            long T, long d) {
+  long BH = B * H;
+#pragma omp parallel for collapse(2) schedule(dynamic, 16)
+  for (long bh = 0; bh < BH; ++bh)
+    for (long t = 0; t < T; ++t) {
+      const double* qt = q + (bh * T + t) * d;
+      double D = 0.0;
+      for (long i = 0; i <= t; ++i) {
+        const double* ki = k + (bh * T + i) * d;
+        double s = 0.0;
+        for (long a = 0; a < d; ++a) s += qt[a] * ki[a];
+        D += s * s;
+      }
+      den[bh * T + t] = D;
+    }
+}

@@ -28,6 +28,7 @@ KATA_F32, KATA_BF16 = 0, 1
 # every symbol include/kata.h declares
 EXPORTED = (
     "kata_fwd_chunked", "kata_fwd_chunked_ws", "kata_fwd_chunked_timed", "kata_fwd_workspace_bytes",
+    "kata_fwd_chunked_train_ws", "kata_bwd_chunked_ex",
     "kata_fwd_default_span", "kata_fwd_quadratic", "kata_fwd_quadratic_ws",
     "kata_fwd_quadratic_workspace_bytes", "kata_prefill_state", "kata_decode_step",
     "kata_mg_fwd_chunked", "kata_mg_fwd_chunked_ws", "kata_mg_fwd_chunked_timed",
@@ -74,6 +75,8 @@ def lib():
     L.kata_fwd_chunked_ws.restype = i
     L.kata_fwd_chunked_timed.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp, vp]
     L.kata_fwd_chunked_timed.restype = i
+    L.kata_fwd_chunked_train_ws.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, vp, sz, vp]
+    L.kata_fwd_chunked_train_ws.restype = i
     L.kata_fwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
     L.kata_fwd_workspace_bytes.restype = sz
     L.kata_fwd_default_span.argtypes = [i, i, i, i, i, i, i]
@@ -128,6 +131,9 @@ def lib():
     L.kata_bwd_chunked_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i,
                                          vp, sz, vp, vp]
     L.kata_bwd_chunked_timed.restype = i
+    L.kata_bwd_chunked_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i,
+                                      vp, sz, vp, vp]
+    L.kata_bwd_chunked_ex.restype = i
     L.kata_bwd_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
     L.kata_bwd_workspace_bytes.restype = sz
     L.kata_bwd_fused_scan.argtypes = [i, i, i, i, i, i, i, i]
@@ -241,6 +247,29 @@ def fwd_chunked_timed(q, k, v, C: int, events, span_chunks: int = 0, out=None, w
                                         events, _stream(stream, q.device)),
            "kata_fwd_chunked_timed")
     return out
+
+
+def fwd_chunked_train(q, k, v, C: int, span_chunks: int = 0, out=None, den=None, workspace=None,
+                      stream=None):
+    """Forward via kata_fwd_chunked_train_ws, which also writes the row
+    denominators D_t for the backward; returns (out [B,H,T,dv], den [B,H,T])
+    fp32."""
+    import torch
+    B, H, T, d, dv = _qkv_shapes(q, k, v)
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, H, T, dv), dtype=torch.float32, device=q.device)
+    if den is None:
+        den = torch.empty((B, H, T), dtype=torch.float32, device=q.device)
+    nbytes = workspace_bytes(B, H, T, d, dv, C, code, span_chunks)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().kata_fwd_chunked_train_ws(_dev(q, "q"), _dev(k, "k"), _dev(v, "v"),
+                                           _dev(out, "out"), _dev(den, "den"), B, H, T, d, dv, C,
+                                           code, span_chunks, _dev(workspace, "workspace"),
+                                           workspace.numel(), _stream(stream, q.device)),
+           "kata_fwd_chunked_train_ws")
+    return out, den
 
 
 def fwd_chunked_alloc(q, k, v, C: int, out=None, stream=None):
@@ -530,10 +559,12 @@ def bwd_fused_scan(B, H, T, d, dv, C, g, dtype_code) -> int:
 
 
 def bwd_chunked(q, k, v, out, dout, C: int, g: int = 1, workspace=None, stream=None,
-                events=None, grads=None):
+                events=None, grads=None, den=None):
     """Gradients (dq, dk, dv) of the causal KATA-Mg forward (g = 1: M1) via
     kata_bwd_chunked_ws (or kata_bwd_chunked_timed when `events`, a ctypes
-    array of 7 HIP events, is given); fp32 tensors shaped like q, k, v."""
+    array of 7 HIP events, is given; or kata_bwd_chunked_ex when `den`, the
+    denominators from fwd_chunked_train, is given); fp32 tensors shaped like
+    q, k, v."""
     import torch
     B, H, T, d, dv = _qkv_shapes(q, k, v)
     code = _dtype_code(q)
@@ -551,7 +582,13 @@ def bwd_chunked(q, k, v, out, dout, C: int, g: int = 1, workspace=None, stream=N
     args = (_dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), _dev(dout, "dout"),
             _dev(dq, "dq"), _dev(dk, "dk"), _dev(dvv, "dv"), B, H, T, d, dv, C, g, code,
             _dev(workspace, "workspace"), workspace.numel())
-    if events is None:
+    if den is not None:
+        if den.dtype != torch.float32 or tuple(den.shape) != (B, H, T):
+            raise ValueError("den must be fp32 [B,H,T]")
+        args_ex = args[:5] + (_dev(den, "den"),) + args[5:]
+        _check(lib().kata_bwd_chunked_ex(*args_ex, events if events is not None else None,
+                                         _stream(stream, q.device)), "kata_bwd_chunked_ex")
+    elif events is None:
         _check(lib().kata_bwd_chunked_ws(*args, _stream(stream, q.device)), "kata_bwd_chunked_ws")
     else:
         _check(lib().kata_bwd_chunked_timed(*args, events, _stream(stream, q.device)),

@@ -105,12 +105,14 @@ size_t fwd_workspace_bytes(int B, int H, int T, int d, int dv, int C, int dtype,
   return workspace_for(p, B, H, T, d, dv, C, g, span_chunks);
 }
 
+// den: null, or where the MFMA path writes the denominators D_t (fp32 [B][H][T])
 kata_status_t fwd_ws(const void* q, const void* k, const void* v, float* out, int B, int H,
                      int T, int d, int dv, int C, int g, kata_dtype_t dtype, int span_chunks,
                      void* workspace, size_t workspace_bytes, hipEvent_t* ev,
-                     hipStream_t stream) {
+                     hipStream_t stream, float* den = nullptr) {
   if (!q || !k || !v || !out) return KATA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return KATA_ERR_INVALID_ARG;
+  if (den && !aligned16(den)) return KATA_ERR_INVALID_ARG;
   if (span_chunks < 0) return KATA_ERR_INVALID_ARG;
   const Path p = fwd_path(B, H, T, d, dv, C, dtype, g);
   if (p == Path::kInvalid) return KATA_ERR_INVALID_ARG;
@@ -124,9 +126,10 @@ kata_status_t fwd_ws(const void* q, const void* k, const void* v, float* out, in
   if (p == Path::kMfma) {
     const int L = span_tokens(T, C, span_chunks);
     if ((static_cast<long long>(T) + L - 1) / L > kGridYZ) return KATA_ERR_UNSUPPORTED;
-    return from_hip(
-        kata::launch_mfma_forward(q, k, v, out, BH, T, d, dv, g, L, workspace, stream, ev));
+    return from_hip(kata::launch_mfma_forward(q, k, v, out, den, BH, T, d, dv, g, L, workspace,
+                                              stream, ev));
   }
+  if (den) return KATA_ERR_UNSUPPORTED;  // denominators on the MFMA path only
   if (dtype == KATA_F32)
     return from_hip(kata::launch_fp32_forward<float>(q, k, v, out, BH, T, d, dv, C, g, workspace,
                                                      stream, ev));
@@ -381,21 +384,24 @@ bool bwd_ptrs_ok(const void* q, const void* k, const void* v, const float* out,
   return true;
 }
 
+// den: null, or the forward's denominators D_t (fp32 [B][H][T])
 kata_status_t bwd_ws(const void* q, const void* k, const void* v, const float* out,
                      const float* dout, float* dq, float* dk, float* dvv, int B, int H, int T,
                      int d, int dv, int C, int g, kata_dtype_t dtype, void* workspace,
-                     size_t workspace_bytes, hipEvent_t* ev, hipStream_t stream) {
+                     size_t workspace_bytes, hipEvent_t* ev, hipStream_t stream,
+                     const float* den = nullptr) {
   if (!bwd_ptrs_ok(q, k, v, out, dout, dq, dk, dvv)) return KATA_ERR_INVALID_ARG;
+  if (den && !aligned16(den)) return KATA_ERR_INVALID_ARG;
   const kata_status_t c = bwd_check(B, H, T, d, dv, C, g, dtype);
   if (c != KATA_OK) return c;
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return KATA_ERR_INVALID_ARG;
   if (workspace_bytes < kata::bwd_workspace(B * H, T, d, dv, C, g)) return KATA_ERR_INVALID_ARG;
   const int BH = B * H;
   if (dtype == KATA_F32)
-    return from_hip(kata::launch_bwd<float>(q, k, v, out, dout, dq, dk, dvv, BH, T, d, dv, C, g,
-                                            workspace, stream, ev));
-  return from_hip(kata::launch_bwd<kata::bf16_t>(q, k, v, out, dout, dq, dk, dvv, BH, T, d, dv, C,
-                                                 g, workspace, stream, ev));
+    return from_hip(kata::launch_bwd<float>(q, k, v, out, dout, den, dq, dk, dvv, BH, T, d, dv, C,
+                                            g, workspace, stream, ev));
+  return from_hip(kata::launch_bwd<kata::bf16_t>(q, k, v, out, dout, den, dq, dk, dvv, BH, T, d,
+                                                 dv, C, g, workspace, stream, ev));
 }
 
 // Enum arguments arrive from C callers as plain ints and may hold any value;
@@ -421,7 +427,7 @@ bool feature_ok(const kata_lin_feature_t& f) {
 
 extern "C" {
 
-int kata_abi_version(void) { return 105; }
+int kata_abi_version(void) { return 106; }
 
 const char* kata_status_string(kata_status_t s) {
   switch (enum_bits(s)) {
@@ -453,6 +459,16 @@ kata_status_t kata_fwd_chunked_ws(const void* q, const void* k, const void* v, f
   if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
   return fwd_ws(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
                 workspace_bytes, nullptr, stream);
+}
+
+kata_status_t kata_fwd_chunked_train_ws(const void* q, const void* k, const void* v, float* out,
+                                        float* den, int B, int H, int T, int d, int dv, int C,
+                                        kata_dtype_t dtype, int span_chunks, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  if (!den) return KATA_ERR_INVALID_ARG;
+  return fwd_ws(q, k, v, out, B, H, T, d, dv, C, 1, dtype, span_chunks, workspace,
+                workspace_bytes, nullptr, stream, den);
 }
 
 kata_status_t kata_fwd_chunked_timed(const void* q, const void* k, const void* v, float* out,
@@ -698,6 +714,19 @@ kata_status_t kata_bwd_chunked_timed(const void* q, const void* k, const void* v
     if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
   return bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype, workspace,
                 workspace_bytes, stage_events, stream);
+}
+
+kata_status_t kata_bwd_chunked_ex(const void* q, const void* k, const void* v, const float* out,
+                                  const float* dout, const float* den, float* dq, float* dk,
+                                  float* dv_out, int B, int H, int T, int d, int dv, int C, int g,
+                                  kata_dtype_t dtype, void* workspace, size_t workspace_bytes,
+                                  hipEvent_t* stage_events, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return KATA_ERR_INVALID_ARG;
+  if (stage_events)
+    for (int i = 0; i < 7; ++i)
+      if (!stage_events[i]) return KATA_ERR_INVALID_ARG;
+  return bwd_ws(q, k, v, out, dout, dq, dk, dv_out, B, H, T, d, dv, C, g, dtype, workspace,
+                workspace_bytes, stage_events, stream, den);
 }
 
 kata_status_t kata_bwd_chunked(const void* q, const void* k, const void* v, const float* out,

@@ -333,6 +333,58 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
 }
 
 // ---------------------------------------------------------------------------
+// Per-token coefficients from denominators the forward pass saved (den[t] =
+// D_t): ab[t] = (dout_t / D_t, -<dout_t, o_t> / D_t), zeros when D_t = 0, as
+// bwd_coef forms them, without recomputing D_t from the prefix records.
+// Sixteen lanes per token, so that each load instruction of a wave reads four
+// whole rows (16-byte pieces when dv % 4 == 0; rows are then 16-byte aligned);
+// the dot product meets over the 16 lanes.  A workgroup takes 64 tokens, each
+// wave 16 of them four at a time.  grid (ceil(T / 64), BH), block 256.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bwd_coef_den(const float* __restrict__ o,
+                                                    const float* __restrict__ dout,
+                                                    const float* __restrict__ den,
+                                                    float* __restrict__ ab, int T, int dv) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int sub = lane >> 4, pc = lane & 15;
+  const bool vec = (dv & 3) == 0;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const long long t = static_cast<long long>(blockIdx.x) * 64 + 16 * w + 4 * it + sub;
+    const bool ok = t < T;  // lanes past the sequence compute on its last row, store nothing
+    const long long row = static_cast<long long>(blockIdx.y) * T + (ok ? t : T - 1);
+    const float D = den[row];
+    const float inv = D > 0.f ? 1.f / D : 0.f;
+    const float* dr = dout + row * dv;
+    const float* orow = o + row * dv;
+    float* abr = ab + row * (dv + 1);
+    float go = 0.f;
+    if (vec) {
+      for (int j4 = pc; 4 * j4 < dv; j4 += 16) {
+        const float4 x = reinterpret_cast<const float4*>(dr)[j4];
+        const float4 y = reinterpret_cast<const float4*>(orow)[j4];
+        go += x.x * y.x + x.y * y.y + x.z * y.z + x.w * y.w;
+        if (ok) {  // ab rows are dv + 1 floats apart: four 4-byte stores
+          abr[4 * j4] = x.x * inv;
+          abr[4 * j4 + 1] = x.y * inv;
+          abr[4 * j4 + 2] = x.z * inv;
+          abr[4 * j4 + 3] = x.w * inv;
+        }
+      }
+    } else {
+      for (int j = pc; j < dv; j += 16) {
+        const float x = dr[j];
+        go += x * orow[j];
+        if (ok) abr[j] = x * inv;
+      }
+    }
+#pragma unroll
+    for (int m = 8; m > 0; m >>= 1) go += __shfl_xor(go, m);
+    if (ok && pc == 0) abr[dv] = -go * inv;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Gradients of chunk c.  grid (NC, BH), block 256, dynamic LDS
 // (4 C d + 3 C C + 2 C kYB) floats + n uint16 (C <= 64, d <= 64).
 // ---------------------------------------------------------------------------
@@ -829,8 +881,9 @@ bool bwd_supported(int d, int dv, int C, int g) {
 
 template <typename Tin>
 hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* out,
-                      const float* dout, float* dq, float* dk, float* dv_out, int BH, int T,
-                      int d, int dv, int C, int g, void* ws, hipStream_t st, hipEvent_t* ev) {
+                      const float* dout, const float* den, float* dq, float* dk, float* dv_out,
+                      int BH, int T, int d, int dv, int C, int g, void* ws, hipStream_t st,
+                      hipEvent_t* ev) {
   const int n = bwd_n(d, g);
   const int NC = (T + C - 1) / C;
   const long long E = static_cast<long long>(n) * dv + n;
@@ -887,9 +940,12 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
   const float* zsrc = bf ? reinterpret_cast<const float*>(reinterpret_cast<const char*>(frec) +
                                                           bwd_bf_record_bytes() - 4 * n)
                          : frec + static_cast<long long>(n) * dv;
-  bwd_coef<Tin><<<dim3(NC, BH), 256, cshm, st>>>(qi, ki, out, dout, zsrc, ab, T, d, dv, C, g,
-                                                 bf ? NC * rq : bh_stride, bf ? rq : E,
-                                                 bf ? 2.f : 1.f);
+  if (den != nullptr)
+    bwd_coef_den<<<dim3((T + 63) / 64, BH), 256, 0, st>>>(out, dout, den, ab, T, dv);
+  else
+    bwd_coef<Tin><<<dim3(NC, BH), 256, cshm, st>>>(qi, ki, out, dout, zsrc, ab, T, d, dv, C, g,
+                                                   bf ? NC * rq : bh_stride, bf ? rq : E,
+                                                   bf ? 2.f : 1.f);
   if ((e = record(ev, 3, st)) != hipSuccess) return e;
   if (fused) {
     if ((e = launch_bwd_prefix_bf(true, q, ab, brec, BH, T, st)) != hipSuccess) return e;
@@ -938,10 +994,10 @@ hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* 
 }
 
 template hipError_t launch_bwd<float>(const void*, const void*, const void*, const float*,
-                                      const float*, float*, float*, float*, int, int, int, int,
-                                      int, int, void*, hipStream_t, hipEvent_t*);
+                                      const float*, const float*, float*, float*, float*, int,
+                                      int, int, int, int, int, void*, hipStream_t, hipEvent_t*);
 template hipError_t launch_bwd<bf16_t>(const void*, const void*, const void*, const float*,
-                                       const float*, float*, float*, float*, int, int, int, int,
-                                       int, int, void*, hipStream_t, hipEvent_t*);
+                                       const float*, const float*, float*, float*, float*, int,
+                                       int, int, int, int, int, void*, hipStream_t, hipEvent_t*);
 
 }  // namespace kata

@@ -41,9 +41,10 @@ hipError_t launch_decode(float* S, float* z, const void* q, const void* k, const
 // g: feature blocks of KATA-Mg (1 or, at d = 64, 2)
 bool mfma_supported(int d, int dv, int C, int g);
 size_t mfma_forward_workspace(int BH, int T, int d, int dv, int L, int g);
-hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int g, int L, void* ws, hipStream_t st,
-                               hipEvent_t* ev);
+// den (nullable): the per-row denominators D_t, fp32 [BH][T]
+hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, float* den,
+                               int BH, int T, int d, int dv, int g, int L, void* ws,
+                               hipStream_t st, hipEvent_t* ev);
 size_t mfma_quadratic_workspace(int BH, int T, int dv);
 hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, float* out, int BH,
                                  int T, int d, int dv, int g, void* ws, hipStream_t st);
@@ -99,11 +100,13 @@ hipError_t launch_bwd_grad_bf(const void* q, const void* k, const void* v, const
 size_t bwd_workspace(int BH, int T, int d, int dv, int C, int g);
 // ev: null, or 7 events recorded before the first kernel and after each of the
 // six launches (forward states, prefix scan, coefficients, backward states,
-// suffix scan, gradients).
+// suffix scan, gradients).  den: null, or the forward's denominators D_t
+// (fp32 [BH][T]), which then replace the recomputed ones in the coefficients.
 template <typename Tin>
 hipError_t launch_bwd(const void* q, const void* k, const void* v, const float* out,
-                      const float* dout, float* dq, float* dk, float* dv_out, int BH, int T,
-                      int d, int dv, int C, int g, void* ws, hipStream_t st, hipEvent_t* ev);
+                      const float* dout, const float* den, float* dq, float* dk, float* dv_out,
+                      int BH, int T, int d, int dv, int C, int g, void* ws, hipStream_t st,
+                      hipEvent_t* ev);
 
 inline hipError_t record(hipEvent_t* ev, int i, hipStream_t st) {
   return ev ? hipEventRecord(ev[i], st) : hipSuccess;

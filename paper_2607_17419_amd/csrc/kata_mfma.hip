@@ -1271,7 +1271,7 @@ template <int D, int DV, int NG>
 __global__ __launch_bounds__(512) void span_output8_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const uint16_t* __restrict__ pre, float* __restrict__ out,
-    int T, int L, int NS, int BH, int QB, int sp0, int nsp) {
+    float* __restrict__ den, int T, int L, int NS, int BH, int QB, int sp0, int nsp) {
   using G = GeoG<D, DV, NG>;
   static_assert(DV == 64, "the eight-wave form covers dv = 64");
   constexpr int DM = G::DM, RM = G::RM, KZM = G::KZM, KZ = G::KZ;
@@ -1682,6 +1682,10 @@ __global__ __launch_bounds__(512) void span_output8_kernel(
   for (int i = 0; i < NQ; ++i) {
     const float Dt = dpart[i] + __shfl_xor(dpart[i], 32);
     if (!tlive[i]) continue;  // wave-uniform
+    if (den != nullptr && g == 0) {  // the denominators, for a backward pass
+      const long long t = tq0[i] + c;
+      if (t < span_end) den[static_cast<long long>(bh) * T + t] = Dt;
+    }
     const float inv = (Dt > 0.f) ? 1.f / Dt : 0.f;
 #pragma unroll
     for (int m = 0; m < 2; ++m)
@@ -1784,8 +1788,8 @@ size_t mfma_forward_workspace(int BH, int T, int d, int /*dv*/, int L, int g) {
 }
 
 template <int D, int DV, int NG>
-static hipError_t run_mfma(const void* q, const void* k, const void* v, float* out, int BH, int T,
-                           int L, void* ws, hipStream_t st, hipEvent_t* ev) {
+static hipError_t run_mfma(const void* q, const void* k, const void* v, float* out, float* den,
+                           int BH, int T, int L, void* ws, hipStream_t st, hipEvent_t* ev) {
   using G = GeoG<D, DV, NG>;
   const int NS = (T + L - 1) / L;
   uint16_t* spanst = static_cast<uint16_t*>(ws);
@@ -1815,8 +1819,8 @@ static hipError_t run_mfma(const void* q, const void* k, const void* v, float* o
   for (int sp0 = 0; sp0 < nsp; sp0 += kSpansPerLaunch) {
     const int cnt = nsp - sp0 < kSpansPerLaunch ? nsp - sp0 : kSpansPerLaunch;
     const unsigned nb8 = 8u * static_cast<unsigned>(qb8) * static_cast<unsigned>((cnt + 7) / 8);
-    span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, vv, spanst, out, T, L, NS, BH,
-                                                        qb8, sp0, sp0 + cnt);
+    span_output8_kernel<D, DV, NG><<<nb8, 512, 0, st>>>(qq, kk, vv, spanst, out, den, T, L, NS,
+                                                        BH, qb8, sp0, sp0 + cnt);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return record(ev, 3, st);
@@ -1859,12 +1863,15 @@ hipError_t launch_mfma_quadratic(const void* q, const void* k, const void* v, fl
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, int BH,
-                               int T, int d, int dv, int g, int L, void* ws, hipStream_t st,
-                               hipEvent_t* ev) {
-  if (d == 64 && dv == 64 && g == 1) return run_mfma<64, 64, 1>(q, k, v, out, BH, T, L, ws, st, ev);
-  if (d == 64 && dv == 64 && g == 2) return run_mfma<64, 64, 2>(q, k, v, out, BH, T, L, ws, st, ev);
-  if (d == 32 && dv == 64 && g == 1) return run_mfma<32, 64, 1>(q, k, v, out, BH, T, L, ws, st, ev);
+hipError_t launch_mfma_forward(const void* q, const void* k, const void* v, float* out, float* den,
+                               int BH, int T, int d, int dv, int g, int L, void* ws,
+                               hipStream_t st, hipEvent_t* ev) {
+  if (d == 64 && dv == 64 && g == 1)
+    return run_mfma<64, 64, 1>(q, k, v, out, den, BH, T, L, ws, st, ev);
+  if (d == 64 && dv == 64 && g == 2)
+    return run_mfma<64, 64, 2>(q, k, v, out, den, BH, T, L, ws, st, ev);
+  if (d == 32 && dv == 64 && g == 1)
+    return run_mfma<32, 64, 1>(q, k, v, out, den, BH, T, L, ws, st, ev);
   return hipErrorInvalidValue;
 }
 

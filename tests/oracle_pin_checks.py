@@ -757,13 +757,36 @@ def pin_bwd_chunked_equals_definition(orc):
                     assert np.allclose(a, b, rtol=1e-11, atol=1e-12), (g, C, mode)
 
 
+# ---------------------------------------------------------------------------
+# PIN: row denominators (the normaliser of eq. linatt), against the unpacked
+# feature space and closed forms
+# ---------------------------------------------------------------------------
+def pin_den(orc):
+    rng = _rng(77)
+    q, k, _ = _rand_qkv(rng, 1, 2, 9, 4, 3, unit=False)
+    got = orc.den(q, k)
+    for h in range(2):
+        PQ = np.einsum("ta,tb->tab", q[0, h], q[0, h]).reshape(9, 16)
+        PK = np.einsum("ta,tb->tab", k[0, h], k[0, h]).reshape(9, 16)
+        P = (PQ @ PK.T) * np.tril(np.ones((9, 9)))
+        assert np.allclose(got[0, h], P.sum(axis=1), rtol=1e-13, atol=1e-13)
+    # one unit direction for every query and key: D_t = t + 1
+    e = np.zeros((1, 1, 6, 5))
+    e[..., 2] = 1.0
+    assert np.array_equal(orc.den(e, e)[0, 0], np.arange(1.0, 7.0))
+    # queries orthogonal to every key: D = 0
+    qo = np.zeros((1, 1, 6, 5))
+    qo[..., 0] = 1.0
+    assert np.array_equal(orc.den(qo, e)[0, 0], np.zeros(6))
+
+
 ALL_PINS = [
     pin_packed_sizes, pin_packed_order, pin_phi_identity, pin_worked_example,
     pin_brute_force_unpacked, pin_convex_hull, pin_first_token, pin_gate_recursion,
     pin_zero_denominator, pin_identical_keys_running_mean,
     pin_orthonormal_keys_exact_recall, pin_weight_sample, pin_invariances,
     pin_chunked_equals_definition, pin_scan_equals_recurrence,
-    pin_decode_equals_forward, pin_rows_match_full,
+    pin_decode_equals_forward, pin_rows_match_full, pin_den,
     pin_mg_widths, pin_mg_phi, pin_mg_brute_force, pin_mg_special_cases,
     pin_mg_chunked_equals_definition, pin_mg_decode_equals_forward, pin_mg_rows_match_full,
     pin_lin_widths, pin_lin_features, pin_lin_brute_force, pin_lin_special_cases,

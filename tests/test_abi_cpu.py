@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     assert L.kata_status_string(2) == b"KATA_ERR_UNSUPPORTED"
     assert L.kata_status_string(3) == b"KATA_ERR_HIP"
     assert L.kata_status_string(42) == b"KATA_UNKNOWN_STATUS"
-    assert L.kata_abi_version() == 105
+    assert L.kata_abi_version() == 106
 
 
 FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced: validation fails first
@@ -315,3 +315,29 @@ def test_allocation_failure_is_hip_error():
         assert call() == 3, name
         # nothing is left behind: a plain validation error reports as such
         assert L.kata_fwd_chunked(NUL, FAKE, FAKE, FAKE, 1, 1, 8, 16, 16, 32, 0, NUL) == 1
+
+
+def test_train_forward_and_extended_backward_validate_before_gpu():
+    L = kata.lib()
+    # forward with denominators: den is required
+    st = L.kata_fwd_chunked_train_ws(FAKE, FAKE, FAKE, FAKE, NUL, 1, 1, 256, 64, 64, 64, 1, 0,
+                                     FAKE, 1 << 30, NUL)
+    assert st == 1
+    # misaligned den
+    st = L.kata_fwd_chunked_train_ws(FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x10004), 1, 1, 256,
+                                     64, 64, 64, 1, 0, FAKE, 1 << 30, NUL)
+    assert st == 1
+    # fp32 inputs take the fp32 path, which writes no denominators
+    need = L.kata_fwd_workspace_bytes(1, 2, 256, 16, 16, 32, 0, 0)
+    st = L.kata_fwd_chunked_train_ws(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 2, 256, 16, 16, 32, 0, 0,
+                                     FAKE, need, NUL)
+    assert st == 2
+    # backward: misaligned den, and an event array with a null entry
+    ws = L.kata_bwd_workspace_bytes(1, 1, 128, 64, 64, 64, 1, 1)
+    st = L.kata_bwd_chunked_ex(FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x10004), FAKE, FAKE,
+                               FAKE, 1, 1, 128, 64, 64, 64, 1, 1, FAKE, ws, NUL, NUL)
+    assert st == 1
+    events = (ctypes.c_void_p * 7)(*([0x10000] * 6 + [0]))
+    st = L.kata_bwd_chunked_ex(FAKE, FAKE, FAKE, FAKE, FAKE, NUL, FAKE, FAKE, FAKE, 1, 1, 128, 64,
+                               64, 64, 1, 1, FAKE, ws, events, NUL)
+    assert st == 1

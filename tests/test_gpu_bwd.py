@@ -366,3 +366,43 @@ def test_bwd_full_length_two_heads(kata, orc):
             scale = np.linalg.norm(ex[0], axis=-1) * np.linalg.norm(inp["q"], axis=-1)
             assert np.all(np.abs(qd) <= 1e-4 * scale + 1e-5)
 
+
+
+# ---------------------------------------------------------------------------
+# The training pair: a forward that saves the denominators D_t
+# (kata_fwd_chunked_train_ws) and the backward that takes them
+# (kata_bwd_chunked_ex) instead of forming D_t again from the prefix states.
+# The forward's D_t carries the bf16 rounding of the prefix records (Z_pre),
+# so it is held to the bf16 bound 2e-2 against the oracle's denominators (rows
+# with D_t at least 1e-6 of the head's largest); the gradients, of the
+# library's own forward output, to the per-head bound.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("B,H,T", [(1, 16, 1100), (1, 2, 700), (2, 3, 257), (1, 16, 4096)])
+def test_bwd_with_saved_denominators(kata, orc, B, H, T):
+    import torch
+    fused = kata.bwd_fused_scan(B, H, T, 64, 64, 64, 1, kata.KATA_BF16)
+    log(f"case train forward + backward with saved D_t: B{B} H{H} T{T} d64 C64 "
+        f"(state and scan fused: {fused})")
+    inp = workloads.make_inputs("mid_bf16", B=B, H=H, T=T)
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out, den = kata.fwd_chunked_train(q, k, v, 64)
+    plain = kata.fwd_chunked(q, k, v, 64)
+    torch.cuda.synchronize()
+    assert torch.equal(out, plain), "the training forward's output differs from the plain forward"
+    got_den = den.cpu().numpy().astype(np.float64)
+    ref_den = orc.den(inp["q"], inp["k"])
+    scale = np.max(ref_den, axis=2, keepdims=True)
+    live = ref_den >= 1e-6 * scale
+    rel = np.abs(got_den - ref_den)[live] / ref_den[live]
+    log(f"  D_t: max rel err {float(rel.max()):.3e} over {int(live.sum())} rows (tol {BF16_REL:.0e})")
+    assert np.all(np.isfinite(got_den)) and float(rel.max()) <= BF16_REL
+    dout = _dout(inp["v"].shape, 31 + T)
+    d_out = torch.from_numpy(dout).to(q.device)
+    got = [t.cpu().numpy() for t in kata.bwd_chunked(q, k, v, out, d_out, 64, den=den)]
+    if B * H * T <= 20000:
+        ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
+        _check_rel(got, ref, f"saved D_t B{B} H{H} T{T}", per_row=False)
+    # against the backward that forms D_t itself (same library forward output)
+    own = [t.cpu().numpy() for t in kata.bwd_chunked(q, k, v, out, d_out, 64)]
+    _check_rel(got, [o.astype(np.float64) for o in own], f"saved vs recomputed D_t T{T}",
+               per_row=False)

@@ -18,6 +18,9 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "kata_oracle.c")
 # 2 = the third, in the linear-feature code])
 MUTANTS = [
     ("drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {"),
+    ("den_drop_diagonal", "for (long i = 0; i <= t; ++i) {", "for (long i = 0; i < t; ++i) {", 5),
+    ("den_not_squared", "        D += s * s;\n      }\n      den[bh * T + t] = D;",
+     "        D += s;\n      }\n      den[bh * T + t] = D;"),
     ("abs_not_square", "double w = s * s;", "double w = fabs(s);"),
     ("weight_on_diagonal", "double w = (weighted && a != b) ? 2.0 : 1.0;",
      "double w = (weighted && a == b) ? 2.0 : 1.0;"),
