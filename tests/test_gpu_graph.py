@@ -142,3 +142,37 @@ def test_decode_step_graph(kata):
         assert np.array_equal(out.cpu().numpy(), ro), f"decode replay {r}: output differs"
         assert np.array_equal(S_g.cpu().numpy(), rS), f"decode replay {r}: S differs"
         assert np.array_equal(z_g.cpu().numpy(), rz), f"decode replay {r}: z differs"
+
+
+def test_training_pair_graph(kata):
+    # the forward that saves the denominators and the backward that takes
+    # them, captured together as one training step
+    import torch
+    B, H, T, C = 1, 16, 1100, 64
+    log(f"case graph: kata_fwd_chunked_train_ws + kata_bwd_chunked_ex B{B} H{H} T{T} d64 C{C}")
+    q, k, v = _dev3(workloads.make_inputs("mid_bf16", B=B, H=H, T=T))
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(5)
+    dout = torch.randn((B, H, T, 64), device="cuda:0", generator=gen)
+    fws = torch.empty(kata.workspace_bytes(B, H, T, 64, 64, C, kata.KATA_BF16), dtype=torch.uint8,
+                      device="cuda:0")
+    bws = torch.empty(kata.bwd_workspace_bytes(B, H, T, 64, 64, C, 1, kata.KATA_BF16),
+                      dtype=torch.uint8, device="cuda:0")
+    out, den = kata.fwd_chunked_train(q, k, v, C, workspace=fws)
+    grads = kata.bwd_chunked(q, k, v, out, dout, C, workspace=bws, den=den)
+    refs = [t.cpu().numpy() for t in (out, den) + tuple(grads)]
+    outs = [torch.empty_like(t) for t in (out, den) + tuple(grads)]
+
+    def step():
+        kata.fwd_chunked_train(q, k, v, C, out=outs[0], den=outs[1], workspace=fws)
+        kata.bwd_chunked(q, k, v, outs[0], dout, C, workspace=bws, den=outs[1],
+                         grads=tuple(outs[2:]))
+    g = _capture(step)
+    for r in range(REPLAYS):
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (o, ref) in enumerate(zip(outs, refs)):
+            assert np.array_equal(o.cpu().numpy(), ref), f"training pair: replay {r} output {i} differs"
