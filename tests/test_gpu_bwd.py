@@ -406,3 +406,24 @@ def test_bwd_with_saved_denominators(kata, orc, B, H, T):
     own = [t.cpu().numpy() for t in kata.bwd_chunked(q, k, v, out, d_out, 64)]
     _check_rel(got, [o.astype(np.float64) for o in own], f"saved vs recomputed D_t T{T}",
                per_row=False)
+
+
+@pytest.mark.parametrize("span", [0, 1])
+def test_train_forward_d32_denominators(kata, orc, span):
+    # d = 32 (recall inputs, C = 128): the training forward's output equals the
+    # plain forward's and its denominators match the oracle's
+    import torch
+    B, H, T = 1, 3, 3000
+    log(f"case train forward d32 B{B} H{H} T{T} C128 span_chunks={span}")
+    inp = workloads.make_inputs("recall_bf16", B=B, H=H, T=T)
+    q, k, v = (to_device(inp[n], "bf16") for n in ("q_dev", "k_dev", "v_dev"))
+    out, den = kata.fwd_chunked_train(q, k, v, 128, span_chunks=span)
+    plain = kata.fwd_chunked(q, k, v, 128, span_chunks=span)
+    torch.cuda.synchronize()
+    assert torch.equal(out, plain)
+    got = den.cpu().numpy().astype(np.float64)
+    ref = orc.den(inp["q"], inp["k"])
+    live = ref >= 1e-6 * np.max(ref, axis=2, keepdims=True)
+    rel = np.abs(got - ref)[live] / ref[live]
+    log(f"  D_t: max rel err {float(rel.max()):.3e} (tol {BF16_REL:.0e})")
+    assert np.all(np.isfinite(got)) and float(rel.max()) <= BF16_REL
