@@ -191,17 +191,22 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
   const float* zp = zsrc + bh * z_bh + c * z_c;
   // the output and cotangent rows of the epilogue (4 lanes per token, columns
   // p, p + 4, ...), loaded first so that they arrive under the contractions
-  const int r = tid >> 2, p = tid & 3;
-  constexpr int kEJ = 16;  // columns per lane when dv <= 64
-  const long long row = static_cast<long long>(bh) * T + t0 + r;
-  float dre[kEJ], ore[kEJ];
-  const bool pre = dv <= 4 * kEJ && r < nt;
+  // dv = 64: sixteen lanes per token, four tokens per wave at a time (token
+  // 16 w + 4 it + lane / 16, 16-byte piece lane % 16), so that each load reads
+  // four whole rows; other dv: four lanes per token, columns p, p + 4, ...
+  const int sub = (tid & 63) >> 4, pc = tid & 15, w6 = tid >> 6;
+  const bool pre = dv == 64;
+  float4 dre4[4], ore4[4];
   if (pre) {
 #pragma unroll
-    for (int i = 0; i < kEJ; ++i) {
-      const int j = p + 4 * i;
-      dre[i] = j < dv ? dout[row * dv + j] : 0.f;
-      ore[i] = j < dv ? o[row * dv + j] : 0.f;
+    for (int it = 0; it < 4; ++it) {
+      const int rt = 16 * w6 + 4 * it + sub;
+      dre4[it] = ore4[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (rt < nt) {
+        const long long rowt = static_cast<long long>(bh) * T + t0 + rt;
+        dre4[it] = reinterpret_cast<const float4*>(dout + rowt * 64)[pc];
+        ore4[it] = reinterpret_cast<const float4*>(o + rowt * 64)[pc];
+      }
     }
   }
   // z_pre (g nm <= 2080 floats) is read once, coalesced, into the k tile's
@@ -309,23 +314,38 @@ __global__ __launch_bounds__(256) void bwd_coef(const Tin* __restrict__ q,
     if (h == 0) red[X * 64 + t] = part;
   }
   __syncthreads();
+  if (pre) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int rt = 16 * w6 + 4 * it + sub;
+      const float D = red[rt] + red[64 + rt];
+      const float inv = D > 0.f ? 1.f / D : 0.f;
+      const float4 x = dre4[it], y = ore4[it];
+      float go = x.x * y.x + x.y * y.y + x.z * y.z + x.w * y.w;
+#pragma unroll
+      for (int m = 8; m > 0; m >>= 1) go += __shfl_xor(go, m);
+      if (rt < nt) {  // ab rows are 65 floats apart: four 4-byte stores
+        float* abr = ab + (static_cast<long long>(bh) * T + t0 + rt) * 65;
+        abr[4 * pc] = x.x * inv;
+        abr[4 * pc + 1] = x.y * inv;
+        abr[4 * pc + 2] = x.z * inv;
+        abr[4 * pc + 3] = x.w * inv;
+        if (pc == 0) abr[64] = -go * inv;
+      }
+    }
+    return;
+  }
+  const int r = tid >> 2, p = tid & 3;
   if (r < nt) {
+    const long long row = static_cast<long long>(bh) * T + t0 + r;
     const float D = red[r] + red[64 + r];
     float* abr = ab + row * (dv + 1);
     const float inv = D > 0.f ? 1.f / D : 0.f;
     float go = 0.f;
-    if (pre) {
-#pragma unroll
-      for (int i = 0; i < kEJ; ++i) go += dre[i] * ore[i];
-#pragma unroll
-      for (int i = 0; i < kEJ; ++i)
-        if (p + 4 * i < dv) abr[p + 4 * i] = dre[i] * inv;
-    } else {
-      const float* dr = dout + row * dv;
-      const float* orow = o + row * dv;
-      for (int j = p; j < dv; j += 4) go += dr[j] * orow[j];
-      for (int j = p; j < dv; j += 4) abr[j] = dr[j] * inv;
-    }
+    const float* dr = dout + row * dv;
+    const float* orow = o + row * dv;
+    for (int j = p; j < dv; j += 4) go += dr[j] * orow[j];
+    for (int j = p; j < dv; j += 4) abr[j] = dr[j] * inv;
     go += __shfl_xor(go, 1);
     go += __shfl_xor(go, 2);
     if (p == 0) abr[dv] = -go * inv;
