@@ -377,7 +377,8 @@ def test_bwd_full_length_two_heads(kata, orc):
 # with D_t at least 1e-6 of the head's largest); the gradients, of the
 # library's own forward output, to the per-head bound.
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("B,H,T", [(1, 16, 1100), (1, 2, 700), (2, 3, 257), (1, 16, 4096)])
+@pytest.mark.parametrize("B,H,T", [(1, 16, 1100), (1, 2, 700), (2, 3, 257), (1, 16, 4096),
+                                   (1, 2, 1), (1, 3, 63)])
 def test_bwd_with_saved_denominators(kata, orc, B, H, T):
     import torch
     fused = kata.bwd_fused_scan(B, H, T, 64, 64, 64, 1, kata.KATA_BF16)
@@ -399,6 +400,12 @@ def test_bwd_with_saved_denominators(kata, orc, B, H, T):
     dout = _dout(inp["v"].shape, 31 + T)
     d_out = torch.from_numpy(dout).to(q.device)
     got = [t.cpu().numpy() for t in kata.bwd_chunked(q, k, v, out, d_out, 64, den=den)]
+    if T == 1:
+        # o_0 = v_0, dv_0 = dout_0 (w_00 a_0, each rounded to bf16 once); the
+        # exact dq_0 = dk_0 = 0 leave only residues of the forward's rounding
+        # of o_0, which no relative bound holds (see _check_rel)
+        assert np.allclose(got[2], dout, rtol=1.25 * U2, atol=1e-6)
+        return
     if B * H * T <= 20000:
         ref = orc.bwd_mg(inp["q"], inp["k"], inp["v"], dout, 1)
         _check_rel(got, ref, f"saved D_t B{B} H{H} T{T}", per_row=False)
