@@ -176,3 +176,34 @@ def test_training_pair_graph(kata):
         torch.cuda.synchronize()
         for i, (o, ref) in enumerate(zip(outs, refs)):
             assert np.array_equal(o.cpu().numpy(), ref), f"training pair: replay {r} output {i} differs"
+
+
+@pytest.mark.parametrize("feature", [0, 3])
+def test_linear_features_graph(kata, feature):
+    # linear features (identity / Lorentz lift) and KATA-M2, caller workspaces
+    import torch
+    B, H, T, C = 1, 4, 2500, 128
+    log(f"case graph: kata_lin_fwd_chunked_ws feature {feature} B{B} H{H} T{T} d64 C{C}")
+    q, k, v = _dev3(workloads.make_inputs("mid_bf16", B=B, H=H, T=T))
+    ws = torch.empty(max(256, kata.lin_workspace_bytes(B, H, T, 64, 64, C, feature,
+                                                       kata.KATA_BF16)),
+                     dtype=torch.uint8, device="cuda:0")
+    ref = kata.lin_fwd_chunked(q, k, v, C, feature, eps=1e-3, workspace=ws).cpu().numpy()
+    out = torch.empty((B, H, T, 64), dtype=torch.float32, device="cuda:0")
+    g = _capture(lambda: kata.lin_fwd_chunked(q, k, v, C, feature, eps=1e-3, out=out,
+                                              workspace=ws))
+    _replay_and_check(g, [out], [ref], f"linear feature {feature}")
+
+
+def test_mg_graph(kata):
+    import torch
+    B, H, T, C = 1, 4, 2500, 64
+    log(f"case graph: kata_mg_fwd_chunked_ws g2 B{B} H{H} T{T} d64 C{C}")
+    q, k, v = _dev3(workloads.make_inputs("mid_bf16", B=B, H=H, T=T))
+    ws = torch.empty(max(256, int(kata.lib().kata_mg_fwd_workspace_bytes(B, H, T, 64, 64, C, 2,
+                                                                          kata.KATA_BF16, 0))),
+                     dtype=torch.uint8, device="cuda:0")
+    ref = kata.mg_fwd_chunked(q, k, v, C, 2, workspace=ws).cpu().numpy()
+    out = torch.empty((B, H, T, 64), dtype=torch.float32, device="cuda:0")
+    g = _capture(lambda: kata.mg_fwd_chunked(q, k, v, C, 2, out=out, workspace=ws))
+    _replay_and_check(g, [out], [ref], "KATA-M2")
