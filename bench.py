@@ -867,7 +867,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE "
-              f"{world}); the forward has no multi-GPU path in this build.", file=sys.stderr)
+              f"{world}); the library has no multi-GPU path (one process drives one GPU).", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_probe:
